@@ -1,0 +1,358 @@
+"""CPU oracle for forced-weight subset evaluation over attention rows.
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import, call or run
+this module: only the tests, the smoke check and the benchmark's CPU-baseline
+leg use it.  It shares no code with the HIP library and imports none of it.
+
+Every function is a plain, slow, float64 transcription of a definition in
+"Trust the Mass: Forced Weights in KV-Cache Eviction" (Shi, Gu; arXiv
+2608.25230).  Numbering follows the paper: Section 2.1 (Definition 2.1,
+Lemma 2.2, Example 2.3, the balancing selector), Section 2.2 (Definition 2.5),
+Section 4 ("ContourKV", "Setup and measured memory"), Appendix A.
+
+Notation map (paper -> here): budget s -> k; kept set A -> S; mass p_j -> p;
+mu -> dense output o; m_A -> forced output o_S; es(A) -> gap; 1 - p(A) ->
+dropped mass; top-mass set A*_s -> top-k set; balancing selector -> swap rule.
+
+Readings where the paper is silent (each also listed in the design notes):
+  * ties in the top-mass set go to the lower key index, and the set is chosen
+    on the logits (exp is monotone, so this is the set of largest masses);
+  * among best subsets of equal error the lexicographically smallest ascending
+    index tuple wins; among equally good swaps the smallest (out, in) pair;
+  * the closed fraction is 0 when the top-k error is 0 (nothing to close);
+  * the swap rule accepts a swap only on a strict decrease and stops after
+    ``max_iters`` swaps;
+  * the dropped-mass curve is indexed by the number of kept keys, 0..n, and is
+    a suffix sum of the sorted importances;
+  * the ContourKV budget counts the recency floor, is exact (ties at the
+    threshold broken by (cell, position) ascending) and has no per-cell cap.
+
+Parity status: every function here is pinned by the not-gpu tests (worked
+examples of the paper, closed forms, identities, brute force, permutation
+invariance, the hardness family in exact rationals); none is "parity unpinned".
+"""
+from __future__ import annotations
+
+import functools
+import itertools
+import math
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+# ----------------------------------------------------------------------------
+# Instance (Definition 2.1): weights of one query row and the dense output
+# ----------------------------------------------------------------------------
+
+
+def logits(q: np.ndarray, K: np.ndarray, scale: float, bias: Optional[np.ndarray] = None) -> np.ndarray:
+    """Attention logits of query rows ``q`` [..., d] against keys ``K`` [n, d]:
+    z_j = scale * <q, k_j> + bias_j.  At an attention head, p is one softmax
+    query row (Definition 2.1 and the text after it)."""
+    z = float(scale) * (np.asarray(q, np.float64) @ np.asarray(K, np.float64).T)
+    if bias is not None:
+        z = z + np.asarray(bias, np.float64)
+    return z
+
+
+def weights(z: np.ndarray) -> np.ndarray:
+    """Softmax along the last axis: the strictly positive probability vector p
+    of Definition 2.1."""
+    z = np.asarray(z, np.float64)
+    e = np.exp(z - z.max(axis=-1, keepdims=True))
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def dense_output(p: np.ndarray, V: np.ndarray) -> np.ndarray:
+    """mu = sum_j p_j v_j, the dense attention output (Definition 2.1)."""
+    return np.asarray(p, np.float64) @ np.asarray(V, np.float64)
+
+
+# ----------------------------------------------------------------------------
+# Top-mass set and the forced-weight operator (Definition 2.1)
+# ----------------------------------------------------------------------------
+
+
+def top_mass_set(z: np.ndarray, k: int) -> np.ndarray:
+    """A*_k: the k keys of largest mass, in rank order (largest first), ties to
+    the lower index.  Ranked on the logits z, which order the masses the same
+    way."""
+    z = np.asarray(z, np.float64)
+    order = np.lexsort((np.arange(z.size), -z))
+    return order[:k]
+
+
+def kept_mass(p: np.ndarray, S: Sequence[int]) -> float:
+    """p(S) = sum_{j in S} p_j."""
+    return float(np.sum(np.asarray(p, np.float64)[np.asarray(S, np.int64)]))
+
+
+def dropped_mass(p: np.ndarray, S: Sequence[int]) -> float:
+    """pbar(S) = 1 - p(S), summed over the dropped keys themselves."""
+    keep = np.zeros(len(p), bool)
+    keep[np.asarray(S, np.int64)] = True
+    return float(np.sum(np.asarray(p, np.float64)[~keep]))
+
+
+def forced_output(p: np.ndarray, V: np.ndarray, S: Sequence[int]) -> np.ndarray:
+    """m_S = sum_{j in S} (p_j / p(S)) v_j: what a deployed sparse operator
+    returns once the kept weights are renormalised (Definition 2.1)."""
+    S = np.asarray(S, np.int64)
+    pS = np.asarray(p, np.float64)[S]
+    return (pS @ np.asarray(V, np.float64)[S]) / pS.sum()
+
+
+def forced_error(p: np.ndarray, V: np.ndarray, S: Sequence[int]) -> float:
+    """es(S) = || mu - m_S ||_2, computed directly from its definition."""
+    mu = dense_output(p, V)
+    return float(np.linalg.norm(forced_output(p, V, S) - mu))
+
+
+def row_dense_topk(z: np.ndarray, V: np.ndarray, ks: Sequence[int]) -> Dict[str, np.ndarray]:
+    """For one row with logits z and values V: dense output o, and for every
+    budget k the top-k set (rank order), forced output o_S, gap ||o_S - o||
+    and dropped mass."""
+    p = weights(z)
+    o = dense_output(p, V)
+    kmax = max(ks)
+    top = top_mass_set(z, kmax)
+    o_s, gap, drop = [], [], []
+    for k in ks:
+        S = top[:k]
+        oS = forced_output(p, V, S)
+        o_s.append(oS)
+        gap.append(float(np.linalg.norm(oS - o)))
+        drop.append(dropped_mass(p, S))
+    return dict(p=p, o=o, o_s=np.array(o_s), gap=np.array(gap), dropped=np.array(drop),
+                topk_idx=top)
+
+
+def dense_topk(q: np.ndarray, K: np.ndarray, V: np.ndarray, scale: np.ndarray,
+               bias: Optional[np.ndarray], ks: Sequence[int]) -> Dict[str, np.ndarray]:
+    """Batched ``row_dense_topk`` over q [H][G][d], K, V [H][n][d]."""
+    H, G, d = q.shape
+    nk = len(ks)
+    out = dict(o=np.zeros((H, G, d)), o_s=np.zeros((nk, H, G, d)), gap=np.zeros((nk, H, G)),
+               dropped=np.zeros((nk, H, G)), topk_idx=np.zeros((H, G, max(ks)), np.int64))
+    for h in range(H):
+        Z = logits(q[h], K[h], scale[h], bias)
+        for g in range(G):
+            r = row_dense_topk(Z[g], V[h], ks)
+            out["o"][h, g] = r["o"]
+            out["o_s"][:, h, g] = r["o_s"]
+            out["gap"][:, h, g] = r["gap"]
+            out["dropped"][:, h, g] = r["dropped"]
+            out["topk_idx"][h, g] = r["topk_idx"]
+    return out
+
+
+# ----------------------------------------------------------------------------
+# Exhaustive best subset (Section 2.2, Definition 2.5, with the whole row as
+# the candidate set) and the closed fraction
+# ----------------------------------------------------------------------------
+
+
+@functools.lru_cache(maxsize=16)
+def combinations_table(n: int, k: int) -> np.ndarray:
+    """All size-k subsets of range(n), ascending tuples in lexicographic order."""
+    return np.array(list(itertools.combinations(range(n), k)), dtype=np.int64).reshape(-1, k)
+
+
+def subset_errors(p: np.ndarray, V: np.ndarray, combos: np.ndarray, chunk: int = 1 << 15) -> np.ndarray:
+    """es(A) for every row A of ``combos`` from the definition: the kept
+    numerator sum_{j in A} p_j v_j is an indicator-matrix product."""
+    p = np.asarray(p, np.float64)
+    V = np.asarray(V, np.float64)
+    mu = p @ V
+    pV = p[:, None] * V
+    n = p.size
+    out = np.empty(len(combos))
+    for lo in range(0, len(combos), chunk):
+        c = combos[lo:lo + chunk]
+        ind = np.zeros((len(c), n))
+        np.put_along_axis(ind, c, 1.0, axis=1)
+        num = ind @ pV
+        den = ind @ p
+        out[lo:lo + chunk] = np.linalg.norm(num / den[:, None] - mu, axis=1)
+    return out
+
+
+def best_subset(p: np.ndarray, V: np.ndarray, k: int) -> Tuple[np.ndarray, float]:
+    """ES(k) = min over |A| = k of es(A), by exhaustive enumeration in
+    lexicographic order; the first minimum (the lexicographically smallest
+    tuple) wins exact ties.  Returns (ascending indices, ES)."""
+    combos = combinations_table(len(p), k)
+    es = subset_errors(p, V, combos)
+    i = int(np.argmin(es))
+    best = combos[i].copy()
+    # report the winner's error through the same evaluator as any other set's
+    return best, forced_error(p, V, best)
+
+
+def closed_fraction(es_top: float, es_best: float) -> float:
+    """c = 1 - ES(k)/es(A*_k) (Definition 2.5); 0 when es(A*_k) = 0."""
+    if es_top == 0.0:
+        return 0.0
+    return 1.0 - es_best / es_top
+
+
+def row_best_subset(z: np.ndarray, V: np.ndarray, k: int) -> Dict[str, object]:
+    p = weights(z)
+    top = top_mass_set(z, k)
+    es_top = forced_error(p, V, top)
+    best, es_best = best_subset(p, V, k)
+    return dict(best_idx=best, best_gap=es_best, topk_gap=es_top,
+                closed=closed_fraction(es_top, es_best), dropped_topk=dropped_mass(p, top),
+                topk_idx=top)
+
+
+# ----------------------------------------------------------------------------
+# Swap rule: the balancing selector of Section 2.1
+# ----------------------------------------------------------------------------
+
+
+def _best_swap_direct(p: np.ndarray, V: np.ndarray, S: np.ndarray) -> Tuple[float, int, int]:
+    """Evaluate es(S - i + j) from the definition for every kept i and dropped
+    j; return (min es, i, j), ties to the smallest (i, j)."""
+    n = p.size
+    Sin = np.sort(S)
+    Sout = np.setdiff1d(np.arange(n), Sin)
+    cands = []
+    pairs = []
+    for i in Sin:
+        for j in Sout:
+            cands.append(np.sort(np.concatenate([Sin[Sin != i], [j]])))
+            pairs.append((int(i), int(j)))
+    es = subset_errors(p, V, np.array(cands, np.int64))
+    t = int(np.argmin(es))
+    return float(es[t]), pairs[t][0], pairs[t][1]
+
+
+def _best_swap_gform(p: np.ndarray, V: np.ndarray, S: np.ndarray) -> Tuple[float, int, int]:
+    """Same as ``_best_swap_direct`` through Lemma 2.2's second form
+    es(A) = ||g_A|| / p(A), g_A = sum_{j in A} p_j (v_j - mu):
+    ||g - u_i + u_j||^2 expands into norms, inner products with g and the
+    cross terms u_i . u_j (one float64 matrix product per call)."""
+    n = p.size
+    mu = p @ V
+    U = p[:, None] * (V - mu)
+    Sin = np.sort(S)
+    Sout = np.setdiff1d(np.arange(n), Sin)
+    g = U[Sin].sum(axis=0)
+    P = p[Sin].sum()
+    a_in, a_out = U[Sin] @ g, U[Sout] @ g
+    b_in, b_out = np.einsum("ij,ij->i", U[Sin], U[Sin]), np.einsum("ij,ij->i", U[Sout], U[Sout])
+    cross = U[Sin] @ U[Sout].T
+    num = (g @ g) + b_in[:, None] + b_out[None, :] - 2.0 * a_in[:, None] + 2.0 * a_out[None, :] - 2.0 * cross
+    den = (P - p[Sin][:, None] + p[Sout][None, :]) ** 2
+    val = np.maximum(num, 0.0) / den
+    t = int(np.argmin(val))
+    i, j = divmod(t, len(Sout))
+    return float(math.sqrt(val.flat[t])), int(Sin[i]), int(Sout[j])
+
+
+def swap_rule(p: np.ndarray, V: np.ndarray, k: int, max_iters: int,
+              start: Optional[Sequence[int]] = None, method: str = "auto"
+              ) -> Tuple[np.ndarray, np.ndarray, int]:
+    """Balancing selector: start at A*_k and repeatedly take the single
+    (kept, dropped) swap that most decreases es, stopping when no swap
+    decreases it or after ``max_iters`` swaps.  Returns (ascending final set,
+    gap trajectory of length max_iters+1 padded with NaN, number of swaps).
+    The trajectory holds es of each accepted set, from the definition."""
+    p = np.asarray(p, np.float64)
+    V = np.asarray(V, np.float64)
+    if start is None:
+        z = np.log(p)
+        start = top_mass_set(z, k)
+    S = np.sort(np.asarray(start, np.int64))
+    if method == "auto":
+        method = "direct" if p.size <= 32 else "gform"
+    search = _best_swap_direct if method == "direct" else _best_swap_gform
+    traj = np.full(max_iters + 1, np.nan)
+    cur = forced_error(p, V, S)
+    traj[0] = cur
+    it = 0
+    if k == 0 or k == p.size:
+        return S, traj, 0
+    while it < max_iters:
+        es_new, i, j = search(p, V, S)
+        if not es_new < cur:
+            break
+        S = np.sort(np.concatenate([S[S != i], [j]]))
+        it += 1
+        cur = forced_error(p, V, S)
+        traj[it] = cur
+    return S, traj, it
+
+
+# ----------------------------------------------------------------------------
+# Dropped-mass curve (Definition 2.1's least achievable dropped mass, as a
+# function of the budget) over a window-averaged importance score (Section 4)
+# ----------------------------------------------------------------------------
+
+
+def importance(Qw: np.ndarray, K: np.ndarray, scale: float, bias: Optional[np.ndarray] = None) -> np.ndarray:
+    """Observation-window score: r_j = mean over the window's query rows of the
+    softmax weight p_{g,j}."""
+    return weights(logits(Qw, K, scale, bias)).mean(axis=0)
+
+
+def dropped_mass_curve(r: np.ndarray) -> np.ndarray:
+    """curve[k] = sum of all but the k largest scores, k = 0..n: the least
+    dropped score when keeping k keys.  Summed from the smallest upward."""
+    srt = np.sort(np.asarray(r, np.float64))  # ascending
+    suffix = np.cumsum(srt)[::-1]  # suffix[k] = sum of the n-k smallest
+    return np.concatenate([suffix, [0.0]])
+
+
+# ----------------------------------------------------------------------------
+# ContourKV allocation and ragged storage (Section 4)
+# ----------------------------------------------------------------------------
+
+
+def allocate(r: np.ndarray, budget: int, floor: int) -> Dict[str, object]:
+    """One score r and one threshold tau shared by all cells.  Each cell keeps
+    its last ``floor`` positions plus its non-floor keys of score >= tau, with
+    tau set so that exactly ``budget`` entries are kept in total (floor
+    included); ties at tau go to (cell, position) ascending."""
+    r = np.asarray(r, np.float64)
+    H, n = r.shape
+    f = min(floor, n)
+    quota = budget - H * f
+    if quota < 0 or quota > H * (n - f):
+        raise ValueError("budget outside [H*floor, H*n]")
+    keep = np.zeros((H, n), bool)
+    keep[:, n - f:] = True
+    cand_h, cand_j = np.meshgrid(np.arange(H), np.arange(n - f), indexing="ij")
+    cand_h, cand_j = cand_h.ravel(), cand_j.ravel()
+    vals = r[:, : n - f].ravel()
+    order = np.lexsort((cand_j, cand_h, -vals))[:quota]
+    keep[cand_h[order], cand_j[order]] = True
+    tau = float(vals[order[-1]]) if quota > 0 else math.inf
+    counts = keep.sum(axis=1)
+    return dict(keep=keep, counts=counts, tau=tau, quota=quota,
+                dropped=np.where(keep, 0.0, r).sum(axis=1))
+
+
+def compact(K: np.ndarray, V: np.ndarray, keep: np.ndarray, heads_per_layer: int,
+            elem_bytes: int) -> Dict[str, object]:
+    """Physical per-cell eviction stored ragged: each cell's kept rows, in
+    ascending position, packed one cell after another, plus the bytes three
+    storage layouts hold (ragged, every layer padded to its widest cell, the
+    full cache under a mask)."""
+    H, n = keep.shape
+    d = K.shape[-1]
+    counts = keep.sum(axis=1)
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int64)
+    pos = [np.nonzero(keep[h])[0] for h in range(H)]
+    kept_pos = np.concatenate(pos).astype(np.int32) if H else np.zeros(0, np.int32)
+    K_out = np.concatenate([K[h][pos[h]] for h in range(H)])
+    V_out = np.concatenate([V[h][pos[h]] for h in range(H)])
+    per_row = 2 * d * elem_bytes  # one K row and one V row
+    ragged = int(counts.sum()) * per_row
+    L = H // heads_per_layer
+    padded = int(sum(counts[l * heads_per_layer:(l + 1) * heads_per_layer].max() for l in range(L))) \
+        * heads_per_layer * per_row
+    full = H * n * per_row
+    return dict(offsets=offsets, kept_pos=kept_pos, k_out=K_out, v_out=V_out,
+                bytes_held=np.array([ragged, padded, full], np.int64))

@@ -1,0 +1,130 @@
+"""Planted mistakes in the oracle must fail at least one pin.
+
+Each mutant replaces one oracle function with a plausible error (dropped
+renormalisation, wrong tie direction, wrong sign, argmax for argmin, prefix in
+place of suffix, ...) and runs the pins that should catch it.
+"""
+import numpy as np
+import pytest
+
+from oracle import fw_oracle as O
+from tests import test_oracle_pins as P
+
+
+def _fails(fn, *args):
+    try:
+        fn(*args)
+    except (AssertionError, ValueError, IndexError):
+        return True
+    return False
+
+
+def _run_all_pins():
+    """True if any pin fails under the current (mutated) oracle."""
+    checks = [
+        (P.test_example_2_3_values,), (P.test_example_2_3_swap_rule,),
+        (P.test_example_A3_table_and_tie_rule,), (P.test_example_A3_not_submodular_statements,),
+        (P.test_hardness_all_pairs_tie,), (P.test_softmax_closed_form_and_shift,),
+        (P.test_compaction_and_bytes,), (P.test_dense_topk_batch_consistency,),
+    ]
+    checks += [(P.test_hardness_family_exact, s) for s in range(4)]
+    checks += [(P.test_lemma_2_2_identities, s) for s in range(3)]
+    checks += [(P.test_closed_forms, s) for s in range(3)]
+    checks += [(P.test_top_mass_brute_force, s) for s in range(3)]
+    checks += [(P.test_swap_rule_invariants, s) for s in range(3)]
+    checks += [(P.test_dropped_mass_curve, s) for s in range(3)]
+    checks += [(P.test_allocation, s) for s in range(3)]
+    return any(_fails(*c) for c in checks)
+
+
+def _no_renorm(p, V, S):
+    S = np.asarray(S, np.int64)
+    return np.asarray(p)[S] @ np.asarray(V)[S]
+
+
+def _ties_high(z, k):
+    z = np.asarray(z, np.float64)
+    return np.lexsort((-np.arange(z.size), -z))[:k]
+
+
+def _dropped_is_kept(p, S):
+    return O.kept_mass(p, S)
+
+
+def _neg_softmax(z):
+    z = -np.asarray(z, np.float64)
+    e = np.exp(z - z.max(axis=-1, keepdims=True))
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def _argmax_best(p, V, k):
+    combos = O.combinations_table(len(p), k)
+    es = O.subset_errors(p, V, combos)
+    i = int(np.argmax(es))
+    return combos[i].copy(), float(es[i])
+
+
+def _ratio_closed(es_top, es_best):
+    return 0.0 if es_top == 0 else es_best / es_top
+
+
+def _prefix_curve(r):
+    srt = np.sort(np.asarray(r, np.float64))[::-1]
+    return np.concatenate([[0.0], np.cumsum(srt)])
+
+
+def _no_bias_logits(q, K, scale, bias=None):
+    return float(scale) * (np.asarray(q, np.float64) @ np.asarray(K, np.float64).T)
+
+
+def _gap_transposed(p, V, S):
+    # mixes up keys and dimensions of V: uses the first |S| columns
+    S = np.asarray(S, np.int64)
+    mu = np.asarray(p) @ np.asarray(V)
+    pS = np.asarray(p)[S]
+    m = (pS @ np.asarray(V)[S]) / pS.sum()
+    return float(np.linalg.norm(m - mu) + abs(m[0] - mu[0]))
+
+
+def _alloc_ties_high(r, budget, floor):
+    r = np.asarray(r, np.float64)
+    H, n = r.shape
+    f = min(floor, n)
+    quota = budget - H * f
+    if quota < 0 or quota > H * (n - f):
+        raise ValueError("budget")
+    keep = np.zeros((H, n), bool)
+    keep[:, n - f:] = True
+    hh, jj = np.meshgrid(np.arange(H), np.arange(n - f), indexing="ij")
+    hh, jj = hh.ravel(), jj.ravel()
+    vals = r[:, : n - f].ravel()
+    order = np.lexsort((-jj, -hh, -vals))[:quota]
+    keep[hh[order], jj[order]] = True
+    tau = float(vals[order[-1]]) if quota > 0 else np.inf
+    return dict(keep=keep, counts=keep.sum(1), tau=tau, quota=quota,
+                dropped=np.where(keep, 0.0, r).sum(1))
+
+
+MUTANTS = {
+    "forced_output_without_renormalisation": ("forced_output", _no_renorm),
+    "top_mass_ties_to_higher_index": ("top_mass_set", _ties_high),
+    "dropped_mass_is_kept_mass": ("dropped_mass", _dropped_is_kept),
+    "softmax_sign_flip": ("weights", _neg_softmax),
+    "best_subset_argmax": ("best_subset", _argmax_best),
+    "closed_fraction_as_ratio": ("closed_fraction", _ratio_closed),
+    "curve_as_prefix_sum": ("dropped_mass_curve", _prefix_curve),
+    "logits_drop_bias": ("logits", _no_bias_logits),
+    "gap_extra_term": ("forced_error", _gap_transposed),
+    "allocation_ties_high": ("allocate", _alloc_ties_high),
+}
+
+
+def test_unmutated_oracle_passes_all_pins():
+    assert not _run_all_pins()
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, monkeypatch):
+    attr, fn = MUTANTS[name]
+    monkeypatch.setattr(O, attr, fn)
+    assert _run_all_pins(), f"no pin catches mutant {name}"

@@ -1,0 +1,406 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test checks the oracle against something other than itself: values the
+paper prints for its worked examples (tests/golden/), exact rationals for the
+hardness construction, the identities of Lemma 2.2, closed forms, brute force
+on tiny instances and invariance under permutation of keys.
+"""
+import itertools
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import fw_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _rand_instance(rng, n, d, temp=1.0):
+    z = rng.standard_normal(n) * temp
+    V = rng.standard_normal((n, d))
+    return z, O.weights(z), V
+
+
+# ---------------------------------------------------------------------------
+# Worked examples printed in the paper
+# ---------------------------------------------------------------------------
+
+def test_example_2_3_values():
+    g = _golden("example_2_3.json")
+    v = np.array(g["v"], float)[:, None]
+    p = np.array([float(Fraction(x)) for x in g["p"]])
+    for key, val in g["es"].items():
+        A = [int(x) for x in key.split(",")]
+        assert O.forced_error(p, v, A) == pytest.approx(float(Fraction(val)), rel=1e-14)
+    best, ES = O.best_subset(p, v, g["k"])
+    assert best.tolist() == g["best_set"]
+    assert ES == pytest.approx(float(Fraction(g["ES"])), rel=1e-14)
+    top = O.top_mass_set(np.log(p), g["k"])
+    assert sorted(top.tolist()) == g["top_mass_set"]
+    es_top = O.forced_error(p, v, top)
+    assert es_top / ES == pytest.approx(float(Fraction(g["kappa"])), rel=1e-13)
+    assert O.closed_fraction(es_top, ES) == pytest.approx(float(Fraction(g["closed_fraction"])), rel=1e-13)
+
+
+def test_example_2_3_swap_rule():
+    g = _golden("example_2_3.json")
+    v = np.array(g["v"], float)[:, None]
+    p = np.array([float(Fraction(x)) for x in g["p"]])
+    for method in ("direct", "gform"):
+        S, traj, ns = O.swap_rule(p, v, g["k"], max_iters=8, method=method)
+        assert S.tolist() == g["swap_final"]
+        assert ns == g["n_swaps"]
+        want = [float(Fraction(x)) for x in g["swap_trajectory"]]
+        assert np.allclose(traj[: ns + 1], want, rtol=1e-13)
+        assert np.all(np.isnan(traj[ns + 1:]))
+
+
+def test_example_A3_table_and_tie_rule():
+    g = _golden("example_A3.json")
+    v = np.array(g["v"], float)[:, None]
+    p = np.array([float(Fraction(x)) for x in g["p"]])
+    for key, val in g["es"].items():
+        A = [int(x) for x in key.split(",")]
+        assert O.forced_error(p, v, A) == pytest.approx(float(Fraction(val)), rel=1e-14, abs=1e-15)
+    for s, want in g["lexicographic_best"].items():
+        best, ES = O.best_subset(p, v, int(s))
+        exact = g["exact_in_float64"][s]
+        if exact:
+            assert best.tolist() == want
+        else:  # tied optimum: any tied set is correct, the value is pinned
+            ties = [k for k, val in g["es"].items() if len(k.split(",")) == int(s)
+                    and Fraction(val) == min(Fraction(x) for kk, x in g["es"].items()
+                                             if len(kk.split(",")) == int(s))]
+            assert ",".join(map(str, best.tolist())) in ties
+        assert ES == pytest.approx(float(min(Fraction(x) for kk, x in g["es"].items()
+                                             if len(kk.split(",")) == int(s))), abs=1e-15)
+    # uniform masses: the top-mass set is the lowest indices
+    for s in (1, 2, 3):
+        assert O.top_mass_set(np.zeros(4), s).tolist() == list(range(s))
+
+
+def test_example_A3_not_submodular_statements():
+    """The printed increments: adding key 0 to {2} keeps es at 1/2, adding it
+    to {1,2} raises es from 0 to 1/2; adding it to {1} raises es from 1/2 to 1,
+    adding it to {1,3} lowers es from 1/2 to 1/6."""
+    v = np.arange(4.0)[:, None]
+    p = np.full(4, 0.25)
+    es = lambda A: O.forced_error(p, v, A)
+    assert es([2]) == es([0, 2]) == 0.5
+    assert es([1, 2]) == 0.0 and es([0, 1, 2]) == 0.5
+    assert es([1]) == 0.5 and es([0, 1]) == 1.0
+    assert es([1, 3]) == 0.5 and es([0, 1, 3]) == pytest.approx(1 / 6, rel=1e-14)
+
+
+# ---------------------------------------------------------------------------
+# Hardness construction (Appendix A.2) in exact rationals
+# ---------------------------------------------------------------------------
+
+def _balanced_split_exists(w):
+    """Independent subset-sum check: some half-size subset with half the sum."""
+    m, W = len(w), sum(w)
+    if W % 2:
+        return False
+    reach = {(0, 0)}
+    for x in w:
+        reach |= {(c + 1, s + x) for (c, s) in reach if c < m // 2}
+    return (m // 2, W // 2) in reach
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_hardness_family_exact(seed):
+    rng = np.random.default_rng(1000 + seed)
+    m = int(rng.choice([4, 6, 8, 10]))
+    w = [int(x) for x in rng.integers(0, 9, size=m)]
+    W = sum(w)
+    s = m // 2
+    # Lemma A.5: g_A = (m sum_A w - |A| W)/m^2; Lemma A.6: p(A) = 1/2, es = 2|g_A|
+    exact = {}
+    for A in itertools.combinations(range(m), s):
+        gA = Fraction(m * sum(w[i] for i in A) - s * W, m * m)
+        exact[A] = 2 * abs(gA)
+    ES_exact = min(exact.values())
+    p = np.full(m, 1.0 / m)
+    v = np.array(w, float)[:, None]
+    best, ES = O.best_subset(p, v, s)
+    assert ES == pytest.approx(float(ES_exact), abs=1e-12)
+    assert exact[tuple(best.tolist())] == ES_exact
+    # Proposition 2.4 / Lemma A.6: ES = 0 iff a balanced split exists, else >= 2/m^2
+    if _balanced_split_exists(w):
+        assert ES_exact == 0 and ES < 1e-12
+    else:
+        assert ES_exact >= Fraction(2, m * m) and ES >= 2.0 / m ** 2 - 1e-12
+
+
+def test_hardness_all_pairs_tie():
+    """w = (1,1,1,4): every pair has es = 3/4 exactly (dyadic), so the tie
+    rule must return the lexicographically smallest pair {0,1}."""
+    p = np.full(4, 0.25)
+    v = np.array([1, 1, 1, 4.0])[:, None]
+    es = O.subset_errors(p, v, O.combinations_table(4, 2))
+    assert np.all(es == 0.75)
+    best, ES = O.best_subset(p, v, 2)
+    assert best.tolist() == [0, 1] and ES == 0.75
+    best, ES = O.best_subset(p, np.array([1, 2, 3, 4.0])[:, None], 2)
+    assert best.tolist() == [0, 3] and ES == 0.0
+
+
+# ---------------------------------------------------------------------------
+# Lemma 2.2 identities, the 2 D mbar bound and the k = n zero
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(10))
+def test_lemma_2_2_identities(seed):
+    rng = np.random.default_rng(seed)
+    n, d = int(rng.integers(3, 40)), int(rng.integers(1, 9))
+    z, p, V = _rand_instance(rng, n, d, temp=rng.uniform(0.3, 3))
+    mu = O.dense_output(p, V)
+    assert np.allclose(mu, sum(p[j] * V[j] for j in range(n)), rtol=1e-13, atol=1e-13)
+    u = p[:, None] * (V - mu)
+    assert np.linalg.norm(u.sum(axis=0)) < 1e-13 * (1 + np.abs(u).sum())
+    for _ in range(5):
+        k = int(rng.integers(1, n))
+        A = np.sort(rng.choice(n, size=k, replace=False))
+        Ac = np.setdiff1d(np.arange(n), A)
+        es = O.forced_error(p, V, A)
+        pA = p[A].sum()
+        mA = (p[A, None] * V[A]).sum(0) / pA
+        mAc = (p[Ac, None] * V[Ac]).sum(0) / p[Ac].sum()
+        first = (1 - pA) * np.linalg.norm(mAc - mA)
+        second = np.linalg.norm(u[A].sum(0)) / pA
+        assert es == pytest.approx(first, rel=1e-10, abs=1e-13)
+        assert es == pytest.approx(second, rel=1e-10, abs=1e-13)
+        assert O.dropped_mass(p, A) == pytest.approx(1 - pA, abs=1e-14)
+        w = p[A] / O.kept_mass(p, A)
+        assert w.sum() == pytest.approx(1.0, abs=1e-14)
+    # es(A*_k) <= 2 D mbar_k
+    D = np.max(np.linalg.norm(V - mu, axis=1))
+    for k in range(1, n + 1):
+        top = O.top_mass_set(z, k)
+        es = O.forced_error(p, V, top)
+        assert es <= 2 * D * O.dropped_mass(p, top) + 1e-12
+    top = O.top_mass_set(z, n)
+    assert O.forced_error(p, V, top) < 1e-13
+    assert O.dropped_mass(p, top) == 0.0
+
+
+def test_softmax_closed_form_and_shift():
+    p = O.weights(np.array([0.0, math.log(3.0)]))
+    assert p == pytest.approx([0.25, 0.75], rel=1e-15)
+    rng = np.random.default_rng(7)
+    z = rng.standard_normal(50) * 3
+    assert O.weights(z).sum() == pytest.approx(1.0, abs=1e-14)
+    assert np.allclose(O.weights(z), O.weights(z + 123.25), rtol=1e-12)
+    q, K = rng.standard_normal(5), rng.standard_normal((7, 5))
+    bias = rng.standard_normal(7)
+    assert np.allclose(O.logits(q, K, 0.5, bias), [0.5 * q @ K[j] + bias[j] for j in range(7)])
+
+
+# ---------------------------------------------------------------------------
+# Closed forms for k = 1, k = n-1, k = n, and brute force on tiny rows
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(8))
+def test_closed_forms(seed):
+    rng = np.random.default_rng(50 + seed)
+    n, d = int(rng.integers(3, 11)), int(rng.integers(1, 6))
+    z, p, V = _rand_instance(rng, n, d)
+    mu = O.dense_output(p, V)
+    dev = np.linalg.norm(V - mu, axis=1)
+    best, ES = O.best_subset(p, V, 1)  # m_{j} = v_j
+    assert best.tolist() == [int(np.argmin(dev))]
+    assert ES == pytest.approx(dev.min(), rel=1e-12)
+    best, ES = O.best_subset(p, V, n - 1)  # dropping j: es = p_j |v_j - mu| / (1 - p_j)
+    drop = p * dev / (1 - p)
+    j = int(np.argmin(drop))
+    assert best.tolist() == [i for i in range(n) if i != j]
+    assert ES == pytest.approx(drop.min(), rel=1e-10)
+    best, ES = O.best_subset(p, V, n)
+    assert best.tolist() == list(range(n)) and ES < 1e-13
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_top_mass_brute_force(seed):
+    """pbar(A*_k) is the least achievable dropped mass over all |A| = k."""
+    rng = np.random.default_rng(90 + seed)
+    n = int(rng.integers(2, 11))
+    z = np.round(rng.standard_normal(n), 1)  # rounding creates ties
+    p = O.weights(z)
+    for k in range(1, n + 1):
+        top = O.top_mass_set(z, k)
+        brute = min(1 - p[list(A)].sum() for A in itertools.combinations(range(n), k))
+        assert O.dropped_mass(p, top) == pytest.approx(brute, abs=1e-14)
+        # ties to the lower index: the set is the first k of the (z desc, j asc) order
+        order = sorted(range(n), key=lambda j: (-z[j], j))
+        assert top.tolist() == order[:k]
+    assert O.top_mass_set(np.array([1.0, 2.0, 2.0, 0.0]), 2).tolist() == [1, 2]
+    assert O.top_mass_set(np.array([2.0, 2.0, 2.0]), 2).tolist() == [0, 1]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_best_subset_permutation_invariance(seed):
+    rng = np.random.default_rng(200 + seed)
+    n, d = int(rng.integers(4, 11)), int(rng.integers(1, 5))
+    z, p, V = _rand_instance(rng, n, d, temp=1.5)
+    k = int(rng.integers(1, n))
+    best, ES = O.best_subset(p, V, k)
+    # brute force by a different route: itertools + direct definition one by one
+    vals = {A: O.forced_error(p, V, A) for A in itertools.combinations(range(n), k)}
+    assert ES == pytest.approx(min(vals.values()), rel=1e-12)
+    perm = rng.permutation(n)
+    best2, ES2 = O.best_subset(p[perm], V[perm], k)
+    assert ES2 == pytest.approx(ES, rel=1e-12)
+    if sorted(vals.values())[1] > ES * (1 + 1e-9):  # unique optimum
+        assert sorted(perm[best2].tolist()) == best.tolist()
+
+
+# ---------------------------------------------------------------------------
+# Swap rule: ordering, local optimality, agreement of the two searches
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(8))
+def test_swap_rule_invariants(seed):
+    rng = np.random.default_rng(300 + seed)
+    n, d = int(rng.integers(5, 13)), int(rng.integers(1, 8))
+    z, p, V = _rand_instance(rng, n, d, temp=2.0)
+    k = int(rng.integers(1, n))
+    top = O.top_mass_set(z, k)
+    S, traj, ns = O.swap_rule(p, V, k, 64, start=top, method="direct")
+    S2, traj2, ns2 = O.swap_rule(p, V, k, 64, start=top, method="gform")
+    assert S.tolist() == S2.tolist() and ns == ns2
+    assert np.allclose(traj[: ns + 1], traj2[: ns + 1], rtol=1e-10)
+    es_swap = O.forced_error(p, V, S)
+    es_top = O.forced_error(p, V, top)
+    _, ES = O.best_subset(p, V, k)
+    assert ES <= es_swap * (1 + 1e-12) and es_swap <= es_top * (1 + 1e-12)
+    assert traj[0] == pytest.approx(es_top, rel=1e-14)
+    assert np.all(np.diff(traj[: ns + 1]) < 0)
+    assert traj[ns] == pytest.approx(es_swap, rel=1e-14)
+    # local optimum: no single swap decreases es (checked one pair at a time)
+    if ns < 64:
+        for i in S:
+            for j in np.setdiff1d(np.arange(n), S):
+                T = np.sort(np.concatenate([S[S != i], [j]]))
+                assert O.forced_error(p, V, T) >= es_swap * (1 - 1e-12)
+    c = O.closed_fraction(es_top, ES)
+    assert -1e-12 <= c <= 1.0
+
+
+def test_swap_rule_max_iters_and_edges():
+    rng = np.random.default_rng(5)
+    z, p, V = _rand_instance(rng, 12, 3, temp=3.0)
+    S, traj, ns = O.swap_rule(p, V, 4, 0, start=O.top_mass_set(z, 4))
+    assert ns == 0 and traj.shape == (1,)
+    S, traj, ns = O.swap_rule(p, V, 12, 5, start=O.top_mass_set(z, 12))
+    assert ns == 0 and traj[0] < 1e-13
+
+
+# ---------------------------------------------------------------------------
+# Dropped-mass curve, allocation, compaction
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(6))
+def test_dropped_mass_curve(seed):
+    rng = np.random.default_rng(400 + seed)
+    G, n, d = 4, int(rng.integers(2, 11)), 3
+    Qw, K = rng.standard_normal((G, d)), rng.standard_normal((n, d))
+    r = O.importance(Qw, K, 0.7)
+    assert r.sum() == pytest.approx(1.0, abs=1e-14)
+    assert np.allclose(r, np.mean([O.weights(O.logits(Qw[g], K, 0.7)) for g in range(G)], axis=0))
+    c = O.dropped_mass_curve(r)
+    assert c.shape == (n + 1,)
+    assert c[0] == pytest.approx(1.0, abs=1e-14) and c[n] == 0.0
+    assert np.all(np.diff(c) <= 0)
+    for k in range(n + 1):
+        brute = min(sum(r[j] for j in range(n) if j not in A) for A in itertools.combinations(range(n), k))
+        assert c[k] == pytest.approx(brute, abs=1e-15)
+
+
+def _alloc_brute(r, budget, floor):
+    H, n = r.shape
+    f = min(floor, n)
+    cand = sorted(((-r[h, j], h, j) for h in range(H) for j in range(n - f)))
+    quota = budget - H * f
+    kept = cand[:quota]
+    keep = np.zeros((H, n), bool)
+    keep[:, n - f:] = True
+    for _, h, j in kept:
+        keep[h, j] = True
+    return keep, (-kept[-1][0] if kept else math.inf)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_allocation(seed):
+    rng = np.random.default_rng(500 + seed)
+    H, n, floor = int(rng.integers(1, 6)), int(rng.integers(4, 40)), int(rng.integers(0, 5))
+    r = np.round(rng.random((H, n)), 2)  # coarse values create ties at tau
+    budget = int(rng.integers(H * min(floor, n), H * n + 1))
+    a = O.allocate(r, budget, floor)
+    keep, tau = _alloc_brute(r, budget, floor)
+    assert np.array_equal(a["keep"], keep)
+    assert a["tau"] == tau
+    assert a["counts"].sum() == budget and np.all(a["counts"] >= min(floor, n))
+    nf = np.zeros((H, n), bool)
+    nf[:, : n - min(floor, n)] = True
+    if a["quota"] > 0:
+        assert r[nf & ~a["keep"]].max(initial=-1) <= a["tau"] <= r[nf & a["keep"]].min()
+    assert np.allclose(a["dropped"], (r * ~keep).sum(1))
+
+
+def test_allocation_rejects_bad_budget():
+    with pytest.raises(ValueError):
+        O.allocate(np.ones((2, 8)), 3, 2)
+    with pytest.raises(ValueError):
+        O.allocate(np.ones((2, 8)), 17, 2)
+
+
+def test_compaction_and_bytes():
+    rng = np.random.default_rng(9)
+    H, hpl, n, d = 4, 2, 10, 3
+    K = rng.integers(0, 1 << 16, (H, n, d)).astype(np.uint16)
+    V = rng.integers(0, 1 << 16, (H, n, d)).astype(np.uint16)
+    keep = rng.random((H, n)) < 0.4
+    keep[:, -1] = True
+    c = O.compact(K, V, keep, hpl, elem_bytes=2)
+    counts = keep.sum(1)
+    assert c["offsets"].tolist() == [0] + np.cumsum(counts).tolist()
+    for h in range(H):
+        pos = [j for j in range(n) if keep[h, j]]
+        lo, hi = c["offsets"][h], c["offsets"][h + 1]
+        assert c["kept_pos"][lo:hi].tolist() == pos
+        assert np.array_equal(c["k_out"][lo:hi], K[h, pos])
+        assert np.array_equal(c["v_out"][lo:hi], V[h, pos])
+    row = 2 * d * 2
+    assert c["bytes_held"][0] == counts.sum() * row
+    assert c["bytes_held"][1] == (max(counts[0], counts[1]) + max(counts[2], counts[3])) * 2 * row
+    assert c["bytes_held"][2] == H * n * row
+
+
+def test_dense_topk_batch_consistency():
+    rng = np.random.default_rng(11)
+    H, G, n, d = 2, 3, 20, 4
+    q, K, V = rng.standard_normal((H, G, d)), rng.standard_normal((H, n, d)), rng.standard_normal((H, n, d))
+    scale = np.array([0.5, 1.5])
+    bias = np.zeros(n)
+    bias[0] = 4.0
+    out = O.dense_topk(q, K, V, scale, bias, (3, 7, 20))
+    for h in range(H):
+        for g in range(G):
+            z = scale[h] * (K[h] @ q[h, g]) + bias
+            p = np.exp(z - z.max())
+            p /= p.sum()
+            assert np.allclose(out["o"][h, g], p @ V[h])
+            for t, k in enumerate((3, 7, 20)):
+                S = out["topk_idx"][h, g, :k]
+                assert out["dropped"][t, h, g] == pytest.approx(1 - p[S].sum(), abs=1e-14)
+            assert out["gap"][2, h, g] < 1e-13
+            assert np.allclose(out["o_s"][2, h, g], out["o"][h, g])
