@@ -1,0 +1,198 @@
+/*
+ * fw.h -- C ABI of libfw: forced-weight subset evaluation over attention rows
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * The operations follow "Trust the Mass: Forced Weights in KV-Cache Eviction"
+ * (arXiv 2608.25230).  An instance (Definition 2.1) is one attention query row:
+ * weights p = softmax(z), z_j = scale * <q, k_j> + bias_j, values v_j, dense
+ * output mu = sum_j p_j v_j.  A kept set S with mass p(S) gives the forced
+ * output m_S = sum_{j in S} (p_j / p(S)) v_j, the gap es(S) = ||m_S - mu||_2 and
+ * the dropped mass 1 - p(S).
+ *
+ * Conventions shared by every entry point
+ *   - All array pointers are DEVICE pointers to contiguous row-major buffers
+ *     unless marked "host".  The caller owns every buffer; the library keeps
+ *     no pointer after a call returns and allocates no device memory: scratch
+ *     space is the caller's workspace, sized by the matching
+ *     fw_*_workspace_size() query (which returns 0 for invalid arguments).
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the default
+ *     stream).  No call synchronises the device or copies device data to the
+ *     host; results are valid once the stream reaches them.
+ *   - Validation happens before anything is enqueued: on any error status no
+ *     output has been written.  fw_last_error() returns a thread-local message
+ *     describing the last failure of the calling thread.
+ *   - Rows are grouped in units of H key/value sets with G query rows each
+ *     (grouped-query attention: the G rows of unit h share k[h], v[h]); row r
+ *     = h*G + g, R = H*G rows in total.
+ *   - Ties: the top-k set ranks keys by logit descending, then key index
+ *     ascending.  Equal-error best subsets resolve to the lexicographically
+ *     smallest ascending index tuple; equal swaps to the smallest (out, in).
+ *   - Results are bitwise repeatable across calls on the same device.
+ */
+#ifndef FW_H
+#define FW_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum fw_status {
+    FW_OK = 0,
+    FW_E_NULL = 1,        /* a required pointer is NULL                       */
+    FW_E_SHAPE = 2,       /* a size is out of range or inconsistent           */
+    FW_E_DTYPE = 3,       /* unknown element type                             */
+    FW_E_UNSUPPORTED = 4, /* valid request this build does not handle         */
+    FW_E_WORKSPACE = 5,   /* workspace NULL or smaller than the size query    */
+    FW_E_HIP = 6          /* the HIP runtime reported an error at launch      */
+} fw_status;
+
+typedef enum fw_dtype {
+    FW_F32 = 0,  /* IEEE float32                        */
+    FW_BF16 = 1  /* bfloat16 (upper half of a float32)  */
+} fw_dtype;
+
+/* A hipStream_t, passed opaquely so that C callers need no HIP headers. */
+typedef void *fw_stream;
+
+/* A batch of attention rows (Definition 2.1 in attention form).
+ *   q     [H][G][d]  query rows, element type `dtype`
+ *   k, v  [H][n][d]  keys and values of each unit, element type `dtype`;
+ *                    v may be NULL for fw_dropped_mass_curve
+ *   scale [H] float32 logit scale per unit, or NULL for 1/sqrt(d)
+ *   bias  [n] float32 additive logit bias shared by every row, or NULL
+ * Limits: H, G >= 1; 1 <= n <= 2^30; 1 <= d <= 256; H*G*n < 2^40.
+ * The paper's worked examples (a given p) are reached with q = 0 and
+ * bias = log p. */
+typedef struct fw_rows {
+    int32_t dtype;
+    const void *q;
+    const void *k;
+    const void *v;
+    int64_t H, G, n, d;
+    const float *scale;
+    const float *bias;
+} fw_rows;
+
+#define FW_MAX_KS 8
+
+/* ---------------------------------------------------------------------------
+ * fw_dense_topk -- top-k forced-weight evaluation of every row
+ * (Definition 2.1; the gap is evaluated through Lemma 2.2's first form
+ * es(S) = (1 - p(S)) * ||m_{S^c} - m_S|| so that it stays accurate when the
+ * dropped mass is small).
+ *   ks        host [n_ks] budgets, each 1 <= k <= n, 1 <= n_ks <= FW_MAX_KS,
+ *             pairwise distinct, any order; outputs follow this order
+ *   o         [H][G][d] float32 dense output mu, or NULL
+ *   o_s       [n_ks][H][G][d] float32 forced output of each top-k set, or NULL
+ *   gap       [n_ks][H][G] float32 ||o_s - o||_2 (required)
+ *   dropped   [n_ks][H][G] float32 dropped mass 1 - p(S) (required)
+ *   topk_idx  [H][G][kmax] int32 top-kmax keys in rank order (logit
+ *             descending, index ascending), kmax = max(ks); or NULL.  The
+ *             top-k set of a smaller budget is the first k entries.
+ * Errors: FW_E_NULL (rows, q, k, v, gap, dropped or ks NULL), FW_E_SHAPE,
+ * FW_E_DTYPE, FW_E_WORKSPACE, FW_E_UNSUPPORTED (topk_idx with kmax > 16384),
+ * FW_E_HIP.
+ * ------------------------------------------------------------------------- */
+size_t fw_dense_topk_workspace_size(const fw_rows *rows, const int32_t *ks, int32_t n_ks);
+fw_status fw_dense_topk(const fw_rows *rows, const int32_t *ks, int32_t n_ks,
+                        float *o, float *o_s, float *gap, float *dropped,
+                        int32_t *topk_idx, void *ws, size_t ws_bytes, fw_stream stream);
+
+/* ---------------------------------------------------------------------------
+ * fw_best_subset -- exact best kept set of size k by exhaustive enumeration
+ * (Section 2.2, Definition 2.5 with every key of the row as the candidate
+ * set), with the top-k comparison and the closed fraction
+ * c = 1 - ES(k)/es(A*_k) (0 when es(A*_k) = 0).  Arithmetic is float64.
+ *   k             budget, 1 <= k <= n
+ *   best_idx      [H][G][k] int32 best set, ascending (required)
+ *   best_gap      [H][G] float32 ES(k) (required)
+ *   topk_gap      [H][G] float32 es of the top-k set, or NULL
+ *   closed        [H][G] float32 closed fraction, or NULL
+ *   dropped_topk  [H][G] float32 dropped mass of the top-k set, or NULL
+ *   topk_idx      [H][G][k] int32 top-k set in rank order, or NULL
+ * Errors: FW_E_UNSUPPORTED when n > 64 or C(n, k) >= 2^31; FW_E_NULL,
+ * FW_E_SHAPE, FW_E_DTYPE, FW_E_WORKSPACE, FW_E_HIP.
+ * ------------------------------------------------------------------------- */
+size_t fw_best_subset_workspace_size(const fw_rows *rows, int32_t k);
+fw_status fw_best_subset(const fw_rows *rows, int32_t k, int32_t *best_idx, float *best_gap,
+                         float *topk_gap, float *closed, float *dropped_topk, int32_t *topk_idx,
+                         void *ws, size_t ws_bytes, fw_stream stream);
+
+/* ---------------------------------------------------------------------------
+ * fw_swap -- the balancing selector of Section 2.1 ("swap rule"): start at
+ * the top-k set and repeatedly apply the single (kept i, dropped j) swap that
+ * most decreases es, over the full neighbourhood, accepting only a strict
+ * decrease, for at most max_iters swaps.  Rows with n <= 64 run in float64;
+ * longer rows evaluate swaps in float32 and report gaps from a float64 sum.
+ *   k          budget, 1 <= k <= n
+ *   max_iters  0 <= max_iters <= 4096
+ *   s_idx      [H][G][k] int32 final set, ascending (required)
+ *   gap_traj   [H][G][max_iters+1] float32 es after 0, 1, ... swaps; NaN
+ *              after the last accepted swap (required)
+ *   n_swaps    [H][G] int32 swaps applied (required)
+ *   dropped    [H][G] float32 dropped mass of the final set, or NULL
+ * Errors: FW_E_NULL, FW_E_SHAPE, FW_E_DTYPE, FW_E_WORKSPACE, FW_E_HIP.
+ * ------------------------------------------------------------------------- */
+size_t fw_swap_workspace_size(const fw_rows *rows, int32_t k, int32_t max_iters);
+fw_status fw_swap(const fw_rows *rows, int32_t k, int32_t max_iters, int32_t *s_idx,
+                  float *gap_traj, int32_t *n_swaps, float *dropped,
+                  void *ws, size_t ws_bytes, fw_stream stream);
+
+/* ---------------------------------------------------------------------------
+ * fw_dropped_mass_curve -- observation-window importance and the per-unit
+ * dropped-mass curve (Section 4, "ContourKV": r_j = mean over the G window
+ * rows of the softmax weight p_{g,j}; Definition 2.1's least achievable
+ * dropped mass as a function of the budget).  v is not read.
+ *   importance [H][n] float32 r (required)
+ *   curve      [H][n+1] float32 curve[k] = sum of all but the k largest r,
+ *              accumulated from the smallest upward; curve[n] = 0 (required)
+ *   order      [H][n] int32 keys by r descending, index ascending, or NULL
+ * Errors: FW_E_NULL, FW_E_SHAPE, FW_E_DTYPE, FW_E_WORKSPACE, FW_E_HIP.
+ * ------------------------------------------------------------------------- */
+size_t fw_dropped_mass_curve_workspace_size(const fw_rows *rows);
+fw_status fw_dropped_mass_curve(const fw_rows *rows, float *importance, float *curve,
+                                int32_t *order, void *ws, size_t ws_bytes, fw_stream stream);
+
+/* ---------------------------------------------------------------------------
+ * fw_ragged_compact -- ContourKV allocation and ragged per-unit storage
+ * (Section 4, "ContourKV" and "Setup and measured memory"): one score and
+ * one threshold tau shared by all H units; each unit keeps its last
+ * recency_floor positions plus its non-floor keys of score >= tau, tau set
+ * so that exactly budget_entries entries are kept in total (floor included;
+ * ties at tau resolve by unit, then position, ascending).  Kept rows are
+ * gathered, positions ascending within a unit, unit after unit.
+ *   dtype, k, v        [H][n][d] keys/values to compact (bit copies)
+ *   heads_per_layer    units per layer (divides H), for the padded layout
+ *   importance         [H][n] float32 score r (e.g. fw_dropped_mass_curve)
+ *   budget_entries     H*min(floor,n) <= budget_entries <= H*n
+ *   offsets            [H+1] int64 exclusive prefix of kept counts (required)
+ *   kept_pos           [budget_entries] int32 kept positions (required)
+ *   k_out, v_out       [budget_entries][d] gathered rows (required)
+ *   tau                [1] float32 threshold (score of the last non-floor
+ *                      pick; +inf when no non-floor entry is kept), or NULL
+ *   dropped            [H] float32 score mass of the evicted keys, or NULL
+ *   bytes_held         [3] int64: K+V bytes held ragged, with every layer
+ *                      padded to its widest unit, and as a full cache under a
+ *                      mask; or NULL
+ * Errors: FW_E_NULL, FW_E_SHAPE, FW_E_DTYPE, FW_E_WORKSPACE, FW_E_HIP.
+ * ------------------------------------------------------------------------- */
+size_t fw_ragged_compact_workspace_size(int64_t H, int64_t n, int64_t d, int64_t budget_entries);
+fw_status fw_ragged_compact(int32_t dtype, const void *k, const void *v, int64_t H,
+                            int64_t heads_per_layer, int64_t n, int64_t d,
+                            const float *importance, int64_t budget_entries,
+                            int32_t recency_floor, int64_t *offsets, int32_t *kept_pos,
+                            void *k_out, void *v_out, float *tau, float *dropped,
+                            int64_t *bytes_held, void *ws, size_t ws_bytes, fw_stream stream);
+
+/* Thread-local description of the calling thread's last error ("" if none). */
+const char *fw_last_error(void);
+/* Library version string. */
+const char *fw_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FW_H */

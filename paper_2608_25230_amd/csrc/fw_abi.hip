@@ -1,0 +1,260 @@
+// C ABI of libfw: argument validation, workspace layout and launch order.
+// No entry point allocates device memory, synchronises or copies to the host.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "fw_internal.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+fw_status fail(fw_status s, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+fw_status hip_status(hipError_t e, const char *where) {
+    if (e == hipSuccess) return FW_OK;
+    return fail(FW_E_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+// Sequential carve-out of the caller's workspace in 256-byte aligned pieces.
+struct Carve {
+    char *base;
+    size_t off = 0;
+    explicit Carve(void *b) : base((char *)b) {}
+    template <typename T> T *take(size_t count) {
+        off = fw::align_up(off, 256);
+        T *p = base ? (T *)(base + off) : nullptr;
+        off += count * sizeof(T);
+        return p;
+    }
+    size_t size() const { return fw::align_up(off, 256); }
+};
+
+fw_status check_rows(const fw_rows *rows, bool need_v) {
+    if (!rows) return fail(FW_E_NULL, "rows is NULL");
+    if (rows->dtype != FW_F32 && rows->dtype != FW_BF16)
+        return fail(FW_E_DTYPE, "unknown dtype %d", (int)rows->dtype);
+    if (!rows->q || !rows->k) return fail(FW_E_NULL, "rows->q or rows->k is NULL");
+    if (need_v && !rows->v) return fail(FW_E_NULL, "rows->v is NULL");
+    if (rows->H < 1 || rows->G < 1 || rows->n < 1)
+        return fail(FW_E_SHAPE, "H, G, n must be >= 1 (H=%lld G=%lld n=%lld)", (long long)rows->H,
+                    (long long)rows->G, (long long)rows->n);
+    if (rows->d < 1 || rows->d > 256) return fail(FW_E_SHAPE, "d must be in [1, 256], got %lld", (long long)rows->d);
+    if (rows->n > (1ll << 30)) return fail(FW_E_SHAPE, "n must be <= 2^30");
+    if (rows->H > (1ll << 31) / rows->G) return fail(FW_E_SHAPE, "H*G must be < 2^31");
+    const double hgn = (double)rows->H * (double)rows->G * (double)rows->n;
+    if (hgn >= 1099511627776.0) return fail(FW_E_SHAPE, "H*G*n must be < 2^40");
+    return FW_OK;
+}
+
+fw_status check_ws(void *ws, size_t ws_bytes, size_t need) {
+    if (need && !ws) return fail(FW_E_WORKSPACE, "workspace is NULL, %zu bytes needed", need);
+    if (ws_bytes < need) return fail(FW_E_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, need);
+    return FW_OK;
+}
+
+// ---------------------------------------------------------------------------
+// fw_dense_topk
+// ---------------------------------------------------------------------------
+fw_status parse_ks(const fw_rows *rows, const int32_t *ks, int32_t n_ks, fw::KsArg *out) {
+    if (!ks) return fail(FW_E_NULL, "ks is NULL");
+    if (n_ks < 1 || n_ks > FW_MAX_KS) return fail(FW_E_SHAPE, "n_ks must be in [1, %d]", FW_MAX_KS);
+    int idx[FW_MAX_KS];
+    for (int i = 0; i < n_ks; ++i) {
+        if (ks[i] < 1 || ks[i] > rows->n)
+            return fail(FW_E_SHAPE, "ks[%d] = %d outside [1, n=%lld]", i, ks[i], (long long)rows->n);
+        idx[i] = i;
+    }
+    std::sort(idx, idx + n_ks, [&](int a, int b) { return ks[a] < ks[b]; });
+    out->n = n_ks;
+    for (int t = 0; t < n_ks; ++t) {
+        if (t && ks[idx[t]] == ks[idx[t - 1]]) return fail(FW_E_SHAPE, "ks must be distinct");
+        out->k[t] = ks[idx[t]];
+        out->perm[t] = idx[t];
+    }
+    for (int t = n_ks; t < FW_MAX_KS; ++t) { out->k[t] = 0; out->perm[t] = 0; }
+    return FW_OK;
+}
+
+struct DenseTopkWs {
+    float *z, *row_m, *row_l;
+    uint32_t *thr_key;
+    int32_t *thr_cut;
+    size_t bytes;
+};
+
+DenseTopkWs dense_topk_layout(const fw_rows *rows, int n_ks, void *ws) {
+    Carve c(ws);
+    const size_t R = (size_t)rows->H * rows->G;
+    DenseTopkWs w;
+    w.z = c.take<float>(R * rows->n);
+    w.row_m = c.take<float>(R);
+    w.row_l = c.take<float>(R);
+    w.thr_key = c.take<uint32_t>(R * n_ks);
+    w.thr_cut = c.take<int32_t>(R * n_ks);
+    w.bytes = c.size();
+    return w;
+}
+
+// ---------------------------------------------------------------------------
+// argument checks of the other entry points
+// ---------------------------------------------------------------------------
+fw_status check_best_subset(const fw_rows *rows, int32_t k) {
+    fw_status s = check_rows(rows, true);
+    if (s != FW_OK) return s;
+    if (k < 1 || k > rows->n) return fail(FW_E_SHAPE, "k = %d outside [1, n=%lld]", k, (long long)rows->n);
+    if (rows->n > 64) return fail(FW_E_UNSUPPORTED, "exhaustive enumeration needs n <= 64 (n=%lld)", (long long)rows->n);
+    if (fw::binom((int)rows->n, k) >= (1ull << 31))
+        return fail(FW_E_UNSUPPORTED, "C(n=%lld, k=%d) must be < 2^31", (long long)rows->n, k);
+    return FW_OK;
+}
+
+fw_status check_swap(const fw_rows *rows, int32_t k, int32_t max_iters) {
+    fw_status s = check_rows(rows, true);
+    if (s != FW_OK) return s;
+    if (k < 1 || k > rows->n) return fail(FW_E_SHAPE, "k = %d outside [1, n=%lld]", k, (long long)rows->n);
+    if (max_iters < 0 || max_iters > 4096) return fail(FW_E_SHAPE, "max_iters must be in [0, 4096]");
+    return FW_OK;
+}
+
+fw_status check_compact(int32_t dtype, const void *k, const void *v, int64_t H, int64_t hpl, int64_t n,
+                        int64_t d, const float *importance, int64_t budget, int32_t floor) {
+    if (dtype != FW_F32 && dtype != FW_BF16) return fail(FW_E_DTYPE, "unknown dtype %d", (int)dtype);
+    if (!k || !v || !importance) return fail(FW_E_NULL, "k, v and importance are required");
+    if (H < 1 || n < 1 || d < 1 || d > 4096) return fail(FW_E_SHAPE, "need H >= 1, n >= 1, 1 <= d <= 4096");
+    if (n > (1ll << 30) || (double)H * (double)n >= 1099511627776.0) return fail(FW_E_SHAPE, "H*n too large");
+    if (hpl < 1 || H % hpl != 0) return fail(FW_E_SHAPE, "heads_per_layer must divide H");
+    if (floor < 0) return fail(FW_E_SHAPE, "recency_floor must be >= 0");
+    const int64_t f = floor < n ? floor : n;
+    if (budget < H * f || budget > H * n)
+        return fail(FW_E_SHAPE, "budget_entries %lld outside [H*floor, H*n] = [%lld, %lld]", (long long)budget,
+                    (long long)(H * f), (long long)(H * n));
+    if (budget >= (1ll << 31)) return fail(FW_E_SHAPE, "budget_entries must be < 2^31");
+    return FW_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *fw_last_error(void) { return g_err; }
+const char *fw_version(void) { return "libfw 0.1 (gfx950)"; }
+
+size_t fw_dense_topk_workspace_size(const fw_rows *rows, const int32_t *ks, int32_t n_ks) {
+    fw::KsArg k;
+    if (check_rows(rows, true) != FW_OK || parse_ks(rows, ks, n_ks, &k) != FW_OK) return 0;
+    return dense_topk_layout(rows, n_ks, nullptr).bytes;
+}
+
+fw_status fw_dense_topk(const fw_rows *rows, const int32_t *ks, int32_t n_ks, float *o, float *o_s,
+                        float *gap, float *dropped, int32_t *topk_idx, void *ws, size_t ws_bytes,
+                        fw_stream stream) {
+    fw_status s = check_rows(rows, true);
+    if (s != FW_OK) return s;
+    fw::KsArg k;
+    if ((s = parse_ks(rows, ks, n_ks, &k)) != FW_OK) return s;
+    if (!gap || !dropped) return fail(FW_E_NULL, "gap and dropped are required");
+    const int kmax = k.k[k.n - 1];
+    if (topk_idx && kmax > 16384) return fail(FW_E_UNSUPPORTED, "topk_idx needs kmax <= 16384");
+    const DenseTopkWs need = dense_topk_layout(rows, n_ks, nullptr);
+    if ((s = check_ws(ws, ws_bytes, need.bytes)) != FW_OK) return s;
+    const DenseTopkWs w = dense_topk_layout(rows, n_ks, ws);
+    hipStream_t st = (hipStream_t)stream;
+    const int64_t H = rows->H, G = rows->G, n = rows->n;
+    const int d = (int)rows->d;
+    hipError_t e = fw::launch_scores(rows->dtype, rows->q, rows->k, rows->scale, rows->bias, H, G, n,
+                                     d, w.z, st);
+    if (e == hipSuccess)
+        e = fw::launch_select(w.z, H * G, n, k, w.row_m, w.row_l, w.thr_key, w.thr_cut, topk_idx,
+                              kmax, st);
+    if (e == hipSuccess)
+        e = fw::launch_tiers(rows->dtype, rows->v, w.z, w.row_m, w.row_l, w.thr_key, w.thr_cut, H,
+                             G, n, d, k, o, o_s, gap, dropped, st);
+    return hip_status(e, "fw_dense_topk");
+}
+
+// ---------------------------------------------------------------------------
+size_t fw_best_subset_workspace_size(const fw_rows *rows, int32_t k) {
+    if (check_best_subset(rows, k) != FW_OK) return 0;
+    return fw::best_subset_ws_bytes(rows->n, k);
+}
+
+fw_status fw_best_subset(const fw_rows *rows, int32_t k, int32_t *best_idx, float *best_gap,
+                         float *topk_gap, float *closed, float *dropped_topk, int32_t *topk_idx,
+                         void *ws, size_t ws_bytes, fw_stream stream) {
+    fw_status s = check_best_subset(rows, k);
+    if (s != FW_OK) return s;
+    if (!best_idx || !best_gap) return fail(FW_E_NULL, "best_idx and best_gap are required");
+    if ((s = check_ws(ws, ws_bytes, fw::best_subset_ws_bytes(rows->n, k))) != FW_OK) return s;
+    hipError_t e = fw::launch_best_subset(*rows, k, best_idx, best_gap, topk_gap, closed,
+                                          dropped_topk, topk_idx, ws, (hipStream_t)stream);
+    return hip_status(e, "fw_best_subset");
+}
+
+// ---------------------------------------------------------------------------
+size_t fw_swap_workspace_size(const fw_rows *rows, int32_t k, int32_t max_iters) {
+    if (check_swap(rows, k, max_iters) != FW_OK) return 0;
+    return fw::swap_ws_bytes(*rows, k, max_iters);
+}
+
+fw_status fw_swap(const fw_rows *rows, int32_t k, int32_t max_iters, int32_t *s_idx, float *gap_traj,
+                  int32_t *n_swaps, float *dropped, void *ws, size_t ws_bytes, fw_stream stream) {
+    fw_status s = check_swap(rows, k, max_iters);
+    if (s != FW_OK) return s;
+    if (!s_idx || !gap_traj || !n_swaps) return fail(FW_E_NULL, "s_idx, gap_traj and n_swaps are required");
+    if ((s = check_ws(ws, ws_bytes, fw::swap_ws_bytes(*rows, k, max_iters))) != FW_OK) return s;
+    hipError_t e = fw::launch_swap(*rows, k, max_iters, s_idx, gap_traj, n_swaps, dropped, ws,
+                                   (hipStream_t)stream);
+    return hip_status(e, "fw_swap");
+}
+
+// ---------------------------------------------------------------------------
+size_t fw_dropped_mass_curve_workspace_size(const fw_rows *rows) {
+    if (check_rows(rows, false) != FW_OK) return 0;
+    return fw::curve_ws_bytes(*rows);
+}
+
+fw_status fw_dropped_mass_curve(const fw_rows *rows, float *importance, float *curve, int32_t *order,
+                                void *ws, size_t ws_bytes, fw_stream stream) {
+    fw_status s = check_rows(rows, false);
+    if (s != FW_OK) return s;
+    if (!importance || !curve) return fail(FW_E_NULL, "importance and curve are required");
+    if ((s = check_ws(ws, ws_bytes, fw::curve_ws_bytes(*rows))) != FW_OK) return s;
+    hipError_t e = fw::launch_curve(*rows, importance, curve, order, ws, (hipStream_t)stream);
+    return hip_status(e, "fw_dropped_mass_curve");
+}
+
+// ---------------------------------------------------------------------------
+size_t fw_ragged_compact_workspace_size(int64_t H, int64_t n, int64_t d, int64_t budget_entries) {
+    if (H < 1 || n < 1 || d < 1 || budget_entries < 0) return 0;
+    return fw::compact_ws_bytes(H, n);
+}
+
+fw_status fw_ragged_compact(int32_t dtype, const void *k, const void *v, int64_t H, int64_t heads_per_layer,
+                            int64_t n, int64_t d, const float *importance, int64_t budget_entries,
+                            int32_t recency_floor, int64_t *offsets, int32_t *kept_pos, void *k_out,
+                            void *v_out, float *tau, float *dropped, int64_t *bytes_held, void *ws,
+                            size_t ws_bytes, fw_stream stream) {
+    fw_status s = check_compact(dtype, k, v, H, heads_per_layer, n, d, importance, budget_entries,
+                                recency_floor);
+    if (s != FW_OK) return s;
+    if (!offsets || !kept_pos || !k_out || !v_out)
+        return fail(FW_E_NULL, "offsets, kept_pos, k_out and v_out are required");
+    if ((s = check_ws(ws, ws_bytes, fw::compact_ws_bytes(H, n))) != FW_OK) return s;
+    hipError_t e = fw::launch_compact(dtype, k, v, H, heads_per_layer, n, d, importance,
+                                      budget_entries, recency_floor, offsets, kept_pos, k_out, v_out,
+                                      tau, dropped, bytes_held, ws, (hipStream_t)stream);
+    return hip_status(e, "fw_ragged_compact");
+}
+
+}  // extern "C"

@@ -1,0 +1,117 @@
+// Shared device helpers for the libfw kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "../../include/fw.h"
+
+namespace fw {
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// Element loads: float32 or bfloat16 storage, widened exactly to float.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
+    return __uint_as_float(uint32_t(b) << 16);
+}
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+    static constexpr int bytes = 4;
+    __device__ __forceinline__ static float load(const float *p, size_t i) { return p[i]; }
+};
+template <> struct Elem<uint16_t> {
+    static constexpr int bytes = 2;
+    __device__ __forceinline__ static float load(const uint16_t *p, size_t i) {
+        return bf16_bits_to_f32(p[i]);
+    }
+};
+
+// ---------------------------------------------------------------------------
+// Ordering keys.  ord_key(x) is an unsigned integer that orders like x, with
+// -0 and +0 mapped to the same key.  Top-k ranks by (key descending, index
+// ascending).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t ord_key(float x) {
+    uint32_t u = __float_as_uint(x + 0.0f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_to_float(uint32_t k) {
+    uint32_t u = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
+    return __uint_as_float(u);
+}
+__device__ __forceinline__ uint64_t ord_key64(double x) {
+    uint64_t u = (uint64_t)__double_as_longlong(x + 0.0);
+    return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+
+// Lexicographic order of two equal-size index sets given as bit masks: the
+// smallest element of the symmetric difference decides.
+__device__ __forceinline__ bool lex_less(uint64_t a, uint64_t b) {
+    uint64_t x = a ^ b;
+    return x != 0 && (a & (x & (~x + 1))) != 0;
+}
+
+// ---------------------------------------------------------------------------
+// Workgroup reductions in a fixed order (bitwise repeatable).  `red` must hold
+// blockDim.x elements; every thread must call.
+// ---------------------------------------------------------------------------
+template <typename T, typename Op>
+__device__ T block_reduce(T v, T *red, Op op) {
+    const int t = threadIdx.x, nt = blockDim.x;
+    red[t] = v;
+    __syncthreads();
+    // power-of-two tree over the (possibly non power-of-two) block
+    int pw = 1;
+    while (pw < nt) pw <<= 1;
+    for (int s = pw >> 1; s > 0; s >>= 1) {
+        if (t < s && t + s < nt) red[t] = op(red[t], red[t + s]);
+        __syncthreads();
+    }
+    T r = red[0];
+    __syncthreads();
+    return r;
+}
+
+struct OpMax { template <typename T> __device__ T operator()(T a, T b) const { return a > b ? a : b; } };
+struct OpMin { template <typename T> __device__ T operator()(T a, T b) const { return a < b ? a : b; } };
+struct OpSum { template <typename T> __device__ T operator()(T a, T b) const { return a + b; } };
+
+// Exclusive scan of one int per thread over the workgroup (Hillis-Steele in
+// LDS).  Returns the exclusive prefix; *total receives the sum.
+__device__ inline int block_exclusive_scan(int v, int *buf, int *total) {
+    const int t = threadIdx.x, nt = blockDim.x;
+    buf[t] = v;
+    __syncthreads();
+    for (int s = 1; s < nt; s <<= 1) {
+        int add = (t >= s) ? buf[t - s] : 0;
+        __syncthreads();
+        buf[t] += add;
+        __syncthreads();
+    }
+    int incl = buf[t];
+    int tot = buf[nt - 1];
+    __syncthreads();
+    if (total) *total = tot;
+    return incl - v;
+}
+
+__host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Binomial coefficient C(n, r), n <= 64, saturating at 2^62 (exact below).
+__host__ __device__ inline uint64_t binom(int n, int r) {
+    if (r < 0 || r > n) return 0;
+    if (r > n - r) r = n - r;
+    uint64_t c = 1;
+    for (int i = 1; i <= r; ++i) {
+        // c = C(n-r+i-1, i-1); C(n-r+i, i) = c * (n-r+i) / i, exact division
+        if (c > (1ull << 62) / 64) return 1ull << 62;
+        c = c * (uint64_t)(n - r + i) / (uint64_t)i;
+    }
+    return c;
+}
+
+}  // namespace fw
