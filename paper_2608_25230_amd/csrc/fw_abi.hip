@@ -124,6 +124,8 @@ fw_status check_swap(const fw_rows *rows, int32_t k, int32_t max_iters) {
     if (s != FW_OK) return s;
     if (k < 1 || k > rows->n) return fail(FW_E_SHAPE, "k = %d outside [1, n=%lld]", k, (long long)rows->n);
     if (max_iters < 0 || max_iters > 4096) return fail(FW_E_SHAPE, "max_iters must be in [0, 4096]");
+    if (rows->n > 64 && rows->H * rows->G > 65535)
+        return fail(FW_E_UNSUPPORTED, "rows longer than 64 keys: at most 65535 rows per call");
     return FW_OK;
 }
 

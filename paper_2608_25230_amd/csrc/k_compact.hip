@@ -1,0 +1,295 @@
+// ContourKV allocation and ragged per-unit storage (Section 4, "ContourKV"
+// and "Setup and measured memory").
+//
+// One threshold tau over every unit's non-floor scores: the quota = budget -
+// H*floor largest entries in the order (score desc, unit asc, position asc)
+// are kept, plus each unit's last `floor` positions.  tau is found by a
+// device-wide radix select (four 8-bit passes over order-preserving keys);
+// entries equal to tau are taken in (unit, position) order.  Kept rows are
+// then gathered unit after unit, positions ascending, as bit copies.
+#include "fw_internal.hpp"
+
+namespace fw {
+
+namespace {
+struct SelState {
+    uint32_t prefix, pmask;
+    int64_t rem;
+    uint32_t hist[256];
+};
+
+struct CompactLayout {
+    SelState *sel;
+    int64_t *cgt, *ceq, *take;
+    size_t bytes;
+};
+
+CompactLayout compact_layout(int64_t H, void *ws) {
+    CompactLayout L{};
+    size_t off = 0;
+    char *base = (char *)ws;
+    auto take = [&](size_t bytes) -> void * {
+        off = align_up(off, 256);
+        void *p = base ? base + off : nullptr;
+        off += bytes;
+        return p;
+    };
+    L.sel = (SelState *)take(sizeof(SelState));
+    L.cgt = (int64_t *)take((size_t)H * 8);
+    L.ceq = (int64_t *)take((size_t)H * 8);
+    L.take = (int64_t *)take((size_t)H * 8);
+    L.bytes = align_up(off, 256);
+    return L;
+}
+}  // namespace
+
+__global__ void sel_init_kernel(SelState *s, int64_t quota) {
+    const int t = threadIdx.x;
+    if (t < 256) s->hist[t] = 0;
+    if (t == 0) {
+        s->prefix = 0;
+        s->pmask = 0;
+        s->rem = quota;
+    }
+}
+
+// histogram of the next 8-bit digit over non-floor entries matching the prefix
+__global__ void __launch_bounds__(256)
+sel_hist_kernel(const float *__restrict__ imp, int64_t H, int64_t n, int64_t nf, int shift,
+                SelState *s) {
+    __shared__ uint32_t h[256];
+    const int t = threadIdx.x;
+    h[t] = 0;
+    __syncthreads();
+    const uint32_t prefix = s->prefix, pmask = s->pmask;
+    const int64_t total = H * nf;
+    for (int64_t e = (int64_t)blockIdx.x * 256 + t; e < total; e += (int64_t)gridDim.x * 256) {
+        const int64_t hh = e / nf, j = e % nf;
+        const uint32_t u = ord_key(imp[hh * n + j]);
+        if ((u & pmask) == prefix) atomicAdd(&h[(u >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (h[t]) atomicAdd(&s->hist[t], h[t]);
+}
+
+// choose the digit holding the rem-th largest; clear the histogram
+__global__ void sel_pick_kernel(SelState *s, int shift) {
+    if (threadIdx.x == 0) {
+        int64_t cum = 0;
+        int b = 0;
+        for (int bb = 255; bb >= 0; --bb) {
+            if (cum + (int64_t)s->hist[bb] >= s->rem) { b = bb; break; }
+            cum += s->hist[bb];
+        }
+        s->prefix |= (uint32_t)b << shift;
+        s->pmask |= 255u << shift;
+        s->rem -= cum;
+    }
+    __syncthreads();
+    if (threadIdx.x < 256) s->hist[threadIdx.x] = 0;
+}
+
+// per unit: entries above tau and equal to tau among the non-floor positions
+__global__ void __launch_bounds__(256)
+unit_counts_kernel(const float *__restrict__ imp, int64_t n, int64_t nf, const SelState *s,
+                   int64_t quota, int64_t *cgt, int64_t *ceq) {
+    __shared__ int64_t r1[256], r2[256];
+    const int64_t h = blockIdx.x;
+    const int t = threadIdx.x;
+    const uint32_t key = s->prefix;
+    int64_t a = 0, b = 0;
+    if (quota > 0)
+        for (int64_t j = t; j < nf; j += 256) {
+            const uint32_t u = ord_key(imp[h * n + j]);
+            a += (u > key);
+            b += (u == key);
+        }
+    a = block_reduce(a, r1, OpSum());
+    b = block_reduce(b, r2, OpSum());
+    if (t == 0) {
+        cgt[h] = a;
+        ceq[h] = b;
+    }
+}
+
+// ties taken per unit, offsets, tau and the bytes held (one workgroup)
+__global__ void __launch_bounds__(256)
+unit_offsets_kernel(int64_t H, int64_t hpl, int64_t n, int64_t f, int64_t quota, const SelState *s,
+                    const int64_t *cgt, const int64_t *ceq, int64_t *take, int64_t *offsets,
+                    float *tau, int64_t *bytes_held, int64_t row_bytes) {
+    if (threadIdx.x != 0) return;
+    int64_t rem = s->rem, acc = 0;
+    for (int64_t h = 0; h < H; ++h) {
+        int64_t t = 0;
+        if (quota > 0) {
+            t = rem < ceq[h] ? rem : ceq[h];
+            rem -= t;
+        }
+        take[h] = t;
+        offsets[h] = acc;
+        acc += f + (quota > 0 ? cgt[h] : 0) + t;
+    }
+    offsets[H] = acc;
+    if (tau) *tau = (quota > 0) ? key_to_float(s->prefix) : INFINITY;
+    if (bytes_held) {
+        int64_t padded = 0;
+        for (int64_t l = 0; l < H / hpl; ++l) {
+            int64_t mx = 0;
+            for (int64_t h = l * hpl; h < (l + 1) * hpl; ++h) {
+                const int64_t c = offsets[h + 1] - offsets[h];
+                mx = c > mx ? c : mx;
+            }
+            padded += mx * hpl;
+        }
+        bytes_held[0] = acc * row_bytes;
+        bytes_held[1] = padded * row_bytes;
+        bytes_held[2] = H * n * row_bytes;
+    }
+}
+
+// per unit: kept positions ascending, and the dropped score mass
+__global__ void __launch_bounds__(256)
+unit_keep_kernel(const float *__restrict__ imp, int64_t n, int64_t f, int64_t quota,
+                 const SelState *s, const int64_t *take, const int64_t *offsets, int32_t *kept_pos,
+                 float *dropped) {
+    __shared__ int scan[256];
+    __shared__ int scan2[256];
+    __shared__ double red[256];
+    const int64_t h = blockIdx.x;
+    const int t = threadIdx.x;
+    const uint32_t key = s->prefix;
+    const int64_t tk = take[h];
+    const int64_t nf = n - f;
+    const int64_t chunk = (n + 255) / 256;
+    const int64_t lo = t * chunk, hi = (lo + chunk < n) ? lo + chunk : n;
+    // ties before this thread's chunk (ascending position)
+    int c_eq = 0;
+    if (quota > 0)
+        for (int64_t j = lo; j < hi && j < nf; ++j) c_eq += (ord_key(imp[h * n + j]) == key);
+    int tot;
+    int eq_before = block_exclusive_scan(c_eq, scan2, &tot);
+    int c = 0;
+    double dm = 0.0;
+    {
+        int eq = eq_before;
+        for (int64_t j = lo; j < hi; ++j) {
+            bool keep = j >= nf;
+            if (!keep && quota > 0) {
+                const uint32_t u = ord_key(imp[h * n + j]);
+                if (u > key) keep = true;
+                else if (u == key) keep = (eq++ < tk);
+            }
+            c += keep;
+            if (!keep) dm += (double)imp[h * n + j];
+        }
+    }
+    int pos = block_exclusive_scan(c, scan, &tot) + (int)0;
+    int64_t out = offsets[h] + pos;
+    {
+        int eq = eq_before;
+        for (int64_t j = lo; j < hi; ++j) {
+            bool keep = j >= nf;
+            if (!keep && quota > 0) {
+                const uint32_t u = ord_key(imp[h * n + j]);
+                if (u > key) keep = true;
+                else if (u == key) keep = (eq++ < tk);
+            }
+            if (keep) kept_pos[out++] = (int32_t)j;
+        }
+    }
+    dm = block_reduce(dm, red, OpSum());
+    if (t == 0 && dropped) dropped[h] = (float)dm;
+}
+
+// gather kept rows: 16-byte pieces, rows located by binary search on offsets
+__global__ void __launch_bounds__(256)
+gather_rows_kernel(const char *__restrict__ k, const char *__restrict__ v, int64_t H, int64_t n,
+                   int64_t row_bytes, const int64_t *offsets, const int32_t *kept_pos, char *k_out,
+                   char *v_out, int64_t total) {
+    const int64_t pieces = row_bytes / 16;
+    const int64_t nwork = total * pieces;
+    for (int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; w < nwork;
+         w += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = w / pieces, pc = w % pieces;
+        int64_t lo = 0, hi = H;  // offsets[lo] <= row < offsets[hi]
+        while (hi - lo > 1) {
+            const int64_t mid = (lo + hi) / 2;
+            if (offsets[mid] <= row) lo = mid; else hi = mid;
+        }
+        const int64_t src = (lo * n + kept_pos[row]) * row_bytes + pc * 16;
+        const int64_t dst = row * row_bytes + pc * 16;
+        *(uint4 *)(k_out + dst) = *(const uint4 *)(k + src);
+        *(uint4 *)(v_out + dst) = *(const uint4 *)(v + src);
+    }
+}
+
+// same, any row size (byte copies), for rows that are not 16-byte multiples
+__global__ void __launch_bounds__(256)
+gather_bytes_kernel(const char *__restrict__ k, const char *__restrict__ v, int64_t H, int64_t n,
+                    int64_t row_bytes, const int64_t *offsets, const int32_t *kept_pos, char *k_out,
+                    char *v_out, int64_t total) {
+    const int64_t nwork = total * row_bytes;
+    for (int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; w < nwork;
+         w += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = w / row_bytes, b = w % row_bytes;
+        int64_t lo = 0, hi = H;
+        while (hi - lo > 1) {
+            const int64_t mid = (lo + hi) / 2;
+            if (offsets[mid] <= row) lo = mid; else hi = mid;
+        }
+        const int64_t src = (lo * n + kept_pos[row]) * row_bytes + b;
+        k_out[row * row_bytes + b] = k[src];
+        v_out[row * row_bytes + b] = v[src];
+    }
+}
+
+size_t compact_ws_bytes(int64_t H, int64_t n) {
+    (void)n;
+    return compact_layout(H, nullptr).bytes;
+}
+
+hipError_t launch_compact(int dtype, const void *k, const void *v, int64_t H, int64_t hpl, int64_t n,
+                          int64_t d, const float *importance, int64_t budget, int floor,
+                          int64_t *offsets, int32_t *kept_pos, void *k_out, void *v_out, float *tau,
+                          float *dropped, int64_t *bytes_held, void *ws, hipStream_t st) {
+    CompactLayout L = compact_layout(H, ws);
+    const int64_t f = floor < n ? floor : n;
+    const int64_t nf = n - f;
+    const int64_t quota = budget - H * f;
+    const int64_t elem = (dtype == FW_BF16) ? 2 : 4;
+    const int64_t row_bytes = d * elem;
+    hipLaunchKernelGGL(sel_init_kernel, dim3(1), dim3(256), 0, st, L.sel, quota);
+    if (quota > 0) {
+        const int64_t total = H * nf;
+        const unsigned blocks = (unsigned)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
+        for (int shift = 24; shift >= 0; shift -= 8) {
+            hipLaunchKernelGGL(sel_hist_kernel, dim3(blocks), dim3(256), 0, st, importance, H, n, nf,
+                               shift, L.sel);
+            hipLaunchKernelGGL(sel_pick_kernel, dim3(1), dim3(256), 0, st, L.sel, shift);
+        }
+    }
+    hipLaunchKernelGGL(unit_counts_kernel, dim3((unsigned)H), dim3(256), 0, st, importance, n, nf,
+                       L.sel, quota, L.cgt, L.ceq);
+    hipLaunchKernelGGL(unit_offsets_kernel, dim3(1), dim3(64), 0, st, H, hpl, n, f, quota, L.sel,
+                       L.cgt, L.ceq, L.take, offsets, tau, bytes_held, 2 * row_bytes);
+    hipLaunchKernelGGL(unit_keep_kernel, dim3((unsigned)H), dim3(256), 0, st, importance, n, f, quota,
+                       L.sel, L.take, offsets, kept_pos, dropped);
+    if (budget > 0) {
+        if (row_bytes % 16 == 0) {
+            const int64_t work = budget * (row_bytes / 16);
+            const unsigned blocks = (unsigned)((work + 255) / 256 < 65536 ? (work + 255) / 256 : 65536);
+            hipLaunchKernelGGL(gather_rows_kernel, dim3(blocks), dim3(256), 0, st, (const char *)k,
+                               (const char *)v, H, n, row_bytes, offsets, kept_pos, (char *)k_out,
+                               (char *)v_out, budget);
+        } else {
+            const int64_t work = budget * row_bytes;
+            const unsigned blocks = (unsigned)((work + 255) / 256 < 65536 ? (work + 255) / 256 : 65536);
+            hipLaunchKernelGGL(gather_bytes_kernel, dim3(blocks), dim3(256), 0, st, (const char *)k,
+                               (const char *)v, H, n, row_bytes, offsets, kept_pos, (char *)k_out,
+                               (char *)v_out, budget);
+        }
+    }
+    return hipGetLastError();
+}
+
+}  // namespace fw

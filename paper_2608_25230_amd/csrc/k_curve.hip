@@ -1,0 +1,289 @@
+// Observation-window importance and the per-unit dropped-mass curve
+// (Section 4, "ContourKV"; Definition 2.1's least achievable dropped mass as
+// a function of the budget).
+//
+//   r_j      = (1/G) sum_g softmax_j(z_g),  z_gj = scale_h <q_g, k_j> + bias_j
+//   curve[k] = sum of all but the k largest r, k = 0..n (curve[n] = 0)
+//
+// Passes: (1) per key chunk, each window row's local max and local sum of
+// exponentials; (2) combine the chunks per row in a fixed order; (3) recompute
+// the logits, weights and their window mean; (4) per unit, a stable LSD radix
+// sort of the scores (descending, ties by index); (5) a float64 suffix scan.
+#include "fw_internal.hpp"
+
+namespace fw {
+
+namespace {
+constexpr int kChunk = 512;   // keys per workgroup in the logit passes
+constexpr int kRowGrp = 16;   // window rows per LDS tile
+constexpr int kSortThreads = 1024;
+}  // namespace
+
+// Pass 1 (MODE 0) and pass 3 (MODE 1) share the logit computation: each
+// thread owns two keys of the chunk; window rows are processed 16 at a time.
+template <typename T, int MODE>
+__global__ void __launch_bounds__(256)
+window_logits_kernel(const T *__restrict__ q, const T *__restrict__ k, const float *__restrict__ scale,
+                     const float *__restrict__ bias, int64_t G, int64_t n, int d, int nchunks,
+                     float *__restrict__ part_m, float *__restrict__ part_s,
+                     const float *__restrict__ row_m, const float *__restrict__ row_il,
+                     float *__restrict__ importance) {
+    __shared__ float Qs[kRowGrp][257];
+    __shared__ float zt[kRowGrp][kChunk + 1];
+    __shared__ float red[256];
+    const int tid = threadIdx.x;
+    const int64_t h = blockIdx.x / nchunks;
+    const int ch = blockIdx.x % nchunks;
+    const int64_t j0 = (int64_t)ch * kChunk;
+    const T *qh = q + h * G * d;
+    const T *kh = k + h * n * d;
+    const float sc = scale ? scale[h] : (float)(1.0 / sqrt((double)d));
+    float racc[2] = {0.f, 0.f};
+    for (int64_t g0 = 0; g0 < G; g0 += kRowGrp) {
+        const int gn = (G - g0 < kRowGrp) ? (int)(G - g0) : kRowGrp;
+        for (int e = tid; e < kRowGrp * d; e += 256) {
+            const int rr = e / d, cc = e % d;
+            Qs[rr][cc] = (rr < gn) ? Elem<T>::load(qh, (g0 + rr) * d + cc) : 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int jl = tid + 256 * u;
+            const int64_t j = j0 + jl;
+            float acc[kRowGrp];
+#pragma unroll
+            for (int g = 0; g < kRowGrp; ++g) acc[g] = 0.f;
+            if (j < n) {
+                for (int c = 0; c < d; ++c) {
+                    const float kv = Elem<T>::load(kh, j * d + c);
+#pragma unroll
+                    for (int g = 0; g < kRowGrp; ++g) acc[g] = fmaf(Qs[g][c], kv, acc[g]);
+                }
+            }
+            const float bj = (bias && j < n) ? bias[j] : 0.f;
+#pragma unroll
+            for (int g = 0; g < kRowGrp; ++g) {
+                const float zz = sc * acc[g] + bj;
+                if (MODE == 0) {
+                    zt[g][jl] = (j < n && g < gn) ? zz : -INFINITY;
+                } else if (j < n && g < gn) {
+                    const int64_t row = h * G + g0 + g;
+                    racc[u] += expf(zz - row_m[row]) * row_il[row];
+                }
+            }
+        }
+        if (MODE == 0) {
+            __syncthreads();
+            // 16 threads per row: local max, then local sum, over 512 keys
+            const int g = tid / 16, l = tid % 16;
+            float m = -INFINITY;
+            for (int jl = l; jl < kChunk; jl += 16) m = fmaxf(m, zt[g][jl]);
+            red[tid] = m;
+            __syncthreads();
+            m = red[g * 16];
+            for (int t = 1; t < 16; ++t) m = fmaxf(m, red[g * 16 + t]);
+            __syncthreads();
+            float s = 0.f;
+            for (int jl = l; jl < kChunk; jl += 16) s += (zt[g][jl] == -INFINITY) ? 0.f : expf(zt[g][jl] - m);
+            red[tid] = s;
+            __syncthreads();
+            if (l == 0 && g < gn) {
+                float st = 0.f;
+                for (int t = 0; t < 16; ++t) st += red[g * 16 + t];
+                const int64_t row = h * G + g0 + g;
+                part_m[row * nchunks + ch] = m;
+                part_s[row * nchunks + ch] = st;
+            }
+        }
+        __syncthreads();
+    }
+    if (MODE == 1) {
+        const float invG = 1.0f / (float)G;
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int64_t j = j0 + tid + 256 * u;
+            if (j < n) importance[h * n + j] = racc[u] * invG;
+        }
+    }
+}
+
+// Pass 2: combine the per-chunk statistics of every window row.
+__global__ void window_combine_kernel(int64_t rows, int nchunks, const float *part_m,
+                                      const float *part_s, float *row_m, float *row_il) {
+    const int64_t row = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (row >= rows) return;
+    float m = -INFINITY;
+    for (int c = 0; c < nchunks; ++c) m = fmaxf(m, part_m[row * nchunks + c]);
+    double s = 0.0;
+    for (int c = 0; c < nchunks; ++c) {
+        const float pm = part_m[row * nchunks + c];
+        if (pm != -INFINITY) s += (double)part_s[row * nchunks + c] * exp((double)pm - (double)m);
+    }
+    row_m[row] = m;
+    row_il[row] = (float)(1.0 / s);
+}
+
+// Pass 4: stable LSD radix sort of one unit's scores, descending (keys are
+// the complement of the order-preserving bits), payload = key index.
+__global__ void __launch_bounds__(kSortThreads)
+unit_sort_kernel(const float *__restrict__ importance, int64_t n, uint32_t *keys_a, uint32_t *keys_b,
+                 int32_t *vals_a, int32_t *vals_b) {
+    __shared__ int hist[256];
+    __shared__ int base[256];
+    __shared__ int wcnt[kSortThreads / 64][256];
+    const int tid = threadIdx.x, lane = tid % 64, wv = tid / 64;
+    const int64_t h = blockIdx.x;
+    uint32_t *ka = keys_a + h * n, *kb = keys_b + h * n;
+    int32_t *va = vals_a + h * n, *vb = vals_b + h * n;
+    for (int64_t j = tid; j < n; j += kSortThreads) {
+        ka[j] = ~ord_key(importance[h * n + j]);
+        va[j] = (int32_t)j;
+    }
+    __syncthreads();
+    for (int shift = 0; shift < 32; shift += 8) {
+        for (int i = tid; i < 256; i += kSortThreads) hist[i] = 0;
+        __syncthreads();
+        for (int64_t j = tid; j < n; j += kSortThreads) atomicAdd(&hist[(ka[j] >> shift) & 255u], 1);
+        __syncthreads();
+        if (tid == 0) {
+            int acc = 0;
+            for (int b = 0; b < 256; ++b) { base[b] = acc; acc += hist[b]; }
+        }
+        __syncthreads();
+        for (int64_t t0 = 0; t0 < n; t0 += kSortThreads) {
+            const int64_t j = t0 + tid;
+            const bool live = j < n;
+            const uint32_t key = live ? ka[j] : 0u;
+            const int dig = live ? (int)((key >> shift) & 255u) : 256;
+            // lanes of this wave holding the same digit
+            uint64_t same = __ballot(live);
+#pragma unroll
+            for (int b = 0; b < 8; ++b) {
+                const uint64_t bal = __ballot(live && ((dig >> b) & 1));
+                same &= ((dig >> b) & 1) ? bal : ~bal;
+            }
+            const uint64_t lower = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+            const int rank = __popcll(same & lower);
+            for (int i = tid; i < (kSortThreads / 64) * 256; i += kSortThreads) (&wcnt[0][0])[i] = 0;
+            __syncthreads();
+            if (live && rank == 0) wcnt[wv][dig] = __popcll(same);
+            __syncthreads();
+            if (live) {
+                int off = base[dig];
+                for (int w = 0; w < wv; ++w) off += wcnt[w][dig];
+                kb[off + rank] = key;
+                vb[off + rank] = va[j];
+            }
+            __syncthreads();
+            if (tid < 256) {
+                int add = 0;
+                for (int w = 0; w < kSortThreads / 64; ++w) add += wcnt[w][tid];
+                base[tid] += add;
+            }
+            __syncthreads();
+        }
+        uint32_t *tk = ka; ka = kb; kb = tk;
+        int32_t *tv = va; va = vb; vb = tv;
+        __syncthreads();
+    }
+    // four passes: the result is back in keys_a / vals_a
+}
+
+// Pass 5: curve[k] = sum_{i >= k} sorted[i] (float64), and the order.
+__global__ void __launch_bounds__(kSortThreads)
+unit_curve_kernel(const float *__restrict__ importance, int64_t n, const int32_t *__restrict__ vals,
+                  float *__restrict__ curve, int32_t *__restrict__ order) {
+    __shared__ double part[kSortThreads];
+    const int tid = threadIdx.x;
+    const int64_t h = blockIdx.x;
+    const int32_t *vs = vals + h * n;
+    const float *imp = importance + h * n;
+    const int64_t chunk = (n + kSortThreads - 1) / kSortThreads;
+    const int64_t lo = tid * chunk, hi = (lo + chunk < n) ? lo + chunk : n;
+    double s = 0.0;
+    for (int64_t i = hi - 1; i >= lo; --i) s += (double)imp[vs[i]];
+    part[tid] = s;
+    __syncthreads();
+    if (tid == 0) {  // suffix sums over the chunks, last chunk first
+        double acc = 0.0;
+        for (int t = kSortThreads - 1; t >= 0; --t) {
+            const double x = part[t];
+            part[t] = acc;
+            acc += x;
+        }
+    }
+    __syncthreads();
+    double acc = part[tid];
+    for (int64_t i = hi - 1; i >= lo; --i) {
+        acc += (double)imp[vs[i]];
+        curve[h * (n + 1) + i] = (float)acc;
+        if (order) order[h * n + i] = vs[i];
+    }
+    if (tid == 0) curve[h * (n + 1) + n] = 0.f;
+}
+
+// ---------------------------------------------------------------------------
+namespace {
+struct CurveLayout {
+    float *part_m, *part_s, *row_m, *row_il;
+    uint32_t *ka, *kb;
+    int32_t *va, *vb;
+    size_t bytes;
+};
+
+CurveLayout curve_layout(const fw_rows &rows, void *ws) {
+    const size_t H = rows.H, G = rows.G, n = rows.n;
+    const size_t nch = (n + kChunk - 1) / kChunk;
+    CurveLayout L{};
+    size_t off = 0;
+    char *base = (char *)ws;
+    auto take = [&](size_t bytes) -> void * {
+        off = align_up(off, 256);
+        void *p = base ? base + off : nullptr;
+        off += bytes;
+        return p;
+    };
+    L.part_m = (float *)take(H * G * nch * 4);
+    L.part_s = (float *)take(H * G * nch * 4);
+    L.row_m = (float *)take(H * G * 4);
+    L.row_il = (float *)take(H * G * 4);
+    L.ka = (uint32_t *)take(H * n * 4);
+    L.kb = (uint32_t *)take(H * n * 4);
+    L.va = (int32_t *)take(H * n * 4);
+    L.vb = (int32_t *)take(H * n * 4);
+    L.bytes = align_up(off, 256);
+    return L;
+}
+}  // namespace
+
+size_t curve_ws_bytes(const fw_rows &rows) { return curve_layout(rows, nullptr).bytes; }
+
+template <typename T>
+static hipError_t curve_impl(const fw_rows &rows, float *importance, float *curve, int32_t *order,
+                             void *ws, hipStream_t st) {
+    CurveLayout L = curve_layout(rows, ws);
+    const int64_t H = rows.H, G = rows.G, n = rows.n;
+    const int d = (int)rows.d;
+    const int nch = (int)((n + kChunk - 1) / kChunk);
+    const dim3 grid((unsigned)(H * nch));
+    const T *q = (const T *)rows.q, *k = (const T *)rows.k;
+    hipLaunchKernelGGL((window_logits_kernel<T, 0>), grid, dim3(256), 0, st, q, k, rows.scale,
+                       rows.bias, G, n, d, nch, L.part_m, L.part_s, nullptr, nullptr, nullptr);
+    hipLaunchKernelGGL(window_combine_kernel, dim3((unsigned)((H * G + 255) / 256)), dim3(256), 0, st,
+                       H * G, nch, L.part_m, L.part_s, L.row_m, L.row_il);
+    hipLaunchKernelGGL((window_logits_kernel<T, 1>), grid, dim3(256), 0, st, q, k, rows.scale,
+                       rows.bias, G, n, d, nch, nullptr, nullptr, L.row_m, L.row_il, importance);
+    hipLaunchKernelGGL(unit_sort_kernel, dim3((unsigned)H), dim3(kSortThreads), 0, st, importance, n,
+                       L.ka, L.kb, L.va, L.vb);
+    hipLaunchKernelGGL(unit_curve_kernel, dim3((unsigned)H), dim3(kSortThreads), 0, st, importance, n,
+                       L.va, curve, order);
+    return hipGetLastError();
+}
+
+hipError_t launch_curve(const fw_rows &rows, float *importance, float *curve, int32_t *order,
+                        void *ws, hipStream_t st) {
+    if (rows.dtype == FW_BF16) return curve_impl<uint16_t>(rows, importance, curve, order, ws, st);
+    return curve_impl<float>(rows, importance, curve, order, ws, st);
+}
+
+}  // namespace fw

@@ -1,0 +1,563 @@
+// Swap rule: the balancing selector of Section 2.1.  Start at the top-k set
+// and repeatedly apply the single (kept i, dropped j) swap that most
+// decreases es, accepting only a strict decrease, for at most max_iters swaps.
+//
+// With g = sum_{a in S} u_a, u_a = p_a (v_a - mu), P = p(S) (Lemma 2.2):
+//   es(S - i + j)^2 = ||g - u_i + u_j||^2 / (P - p_i + p_j)^2
+//   ||g - u_i + u_j||^2 = ||g||^2 + ||u_i||^2 + ||u_j||^2 - 2 g.u_i + 2 g.u_j
+//                         - 2 u_i.u_j,
+// so one sweep over all pairs needs the cross terms u_i.u_j.
+//
+// Rows of at most 64 keys run entirely in float64 on the residual Gram
+// matrix, one workgroup per row.  Longer rows keep per-row state in the
+// workspace; each iteration computes g.u_x for every key, evaluates every
+// pair (cross terms from v_i.v_j: u_i.u_j = p_i p_j (v_i.v_j - v_i.mu -
+// v_j.mu + |mu|^2)) in float32 with a per-row argmin (ties to the smaller
+// (i, j)), then applies the winning swap and updates g in float64.  Gaps in
+// the trajectory are ||g|| / P from float64 sums.
+#include "fw_internal.hpp"
+#include "instance64.hpp"
+
+namespace fw {
+
+// ===========================================================================
+// rows with n <= 64: one workgroup per row, float64
+// ===========================================================================
+template <typename T>
+__global__ void __launch_bounds__(256)
+swap_small_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
+                  const float *__restrict__ scale, const float *__restrict__ bias, int64_t G,
+                  int n, int d, int kk, int max_iters, int32_t *s_idx, float *gap_traj,
+                  int32_t *n_swaps, float *dropped) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    double *Gm = (double *)smem;            // n*n
+    double *ps = Gm + n * n;                // n
+    double *zs = ps + n;                    // n
+    double *mu = zs + n;                    // d
+    double *R = mu + d;                     // n
+    double *redd = R + n;                   // NT
+    uint64_t *redm = (uint64_t *)(redd + blockDim.x);  // NT
+    int *lists = (int *)(redm + blockDim.x);           // n
+    float *Vs = (float *)(lists + n + (n & 1));        // n*d
+    const int tid = threadIdx.x, NT = blockDim.x;
+    const int64_t r = blockIdx.x, h = r / G;
+    const T *qr = q + r * d;
+    const T *kh = k + h * (int64_t)n * d;
+    const T *vh = v + h * (int64_t)n * d;
+    instance64(qr, kh, vh, scale ? scale[h] : default_scale(d), bias, n, d, Vs, zs, ps, mu, Gm);
+    uint64_t S = topk_mask64(zs, n, kk, nullptr, redm);
+    const int T_len = max_iters + 1;
+    float *traj = gap_traj + r * T_len;
+    double es = exact_gap(S, n, vh, ps, mu, d, redd);
+    if (tid == 0) traj[0] = (float)es;
+    int it = 0;
+    const int nout = n - kk;
+    while (it < max_iters && nout > 0) {
+        // R_x = g . u_x = sum_{a in S} Gm_xa; current value ||g||^2 / P^2
+        for (int x = tid; x < n; x += NT) {
+            double s = 0.0;
+            for (uint64_t a = S; a; a &= a - 1) s += Gm[x * n + (__ffsll((unsigned long long)a) - 1)];
+            R[x] = s;
+        }
+        if (tid == 0) {
+            int a = 0, b = kk;
+            for (int x = 0; x < n; ++x) lists[((S >> x) & 1ull) ? a++ : b++] = x;
+        }
+        __syncthreads();
+        double Sv = 0.0;
+        for (uint64_t a = S; a; a &= a - 1) Sv += R[__ffsll((unsigned long long)a) - 1];
+        const double P = mass64(S, ps);
+        const double cur = Sv / (P * P);
+        double bv = INFINITY;
+        int bp = 0x7FFFFFFF;
+        for (int pi = tid; pi < kk * nout; pi += NT) {
+            const int i = lists[pi / nout], j = lists[kk + pi % nout];
+            const double num = Sv + Gm[i * n + i] + Gm[j * n + j] - 2.0 * R[i] + 2.0 * R[j] - 2.0 * Gm[i * n + j];
+            const double den = P - ps[i] + ps[j];
+            const double val = num / (den * den);
+            if (val < bv) { bv = val; bp = pi; }
+        }
+        redd[tid] = bv;
+        redm[tid] = (uint64_t)(uint32_t)bp;
+        __syncthreads();
+        if (tid == 0) {
+            for (int t = 1; t < NT; ++t)
+                if (redd[t] < redd[0] || (redd[t] == redd[0] && redm[t] < redm[0])) {
+                    redd[0] = redd[t];
+                    redm[0] = redm[t];
+                }
+        }
+        __syncthreads();
+        const double best = redd[0];
+        const int pi = (int)redm[0];
+        __syncthreads();
+        if (!(best < cur)) break;
+        S ^= (1ull << lists[pi / nout]) ^ (1ull << lists[kk + pi % nout]);
+        ++it;
+        es = exact_gap(S, n, vh, ps, mu, d, redd);
+        if (tid == 0) traj[it] = (float)es;
+    }
+    if (tid == 0) {
+        for (int t = it + 1; t < T_len; ++t) traj[t] = __int_as_float(0x7fc00000);
+        n_swaps[r] = it;
+        int i = 0;
+        double dm = 0.0;
+        for (int x = 0; x < n; ++x) {
+            if ((S >> x) & 1ull) s_idx[r * kk + i++] = x;
+            else dm += ps[x];
+        }
+        if (dropped) dropped[r] = (float)dm;
+    }
+}
+
+// ===========================================================================
+// rows with n > 64: workspace state, float32 pair search
+// ===========================================================================
+struct SwapState {
+    const float *z, *row_m, *row_l;
+    const uint32_t *thr_key;
+    const int32_t *thr_cut;
+    float *p;        // [R][n]
+    uint8_t *inS;    // [R][n]
+    int32_t *Sl;     // [R][k]
+    float *w;        // [R][n]   v_j . mu
+    float *bq;       // [R][n]   ||u_j||^2
+    float *a;        // [R][n]   g . u_j
+    double *mu;      // [R][d]
+    double *g;       // [R][d]
+    double *sc;      // [R][4]   P, ||g||^2, |mu|^2, cur
+    int32_t *st;     // [R][2]   active, swaps
+    float *pv;       // [R][nblk] partial best values
+    int64_t *pp;     // [R][nblk] partial best pair index i*n + j
+    int nblk;
+};
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+swap_init_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, SwapState s,
+                 float *gap_traj, int T_len) {
+    __shared__ double redd[256];
+    __shared__ int scan[256];
+    const int tid = threadIdx.x, NT = blockDim.x;
+    const int64_t r = blockIdx.x, h = r / G;
+    const T *vh = v + h * n * d;
+    const float m = s.row_m[r], inv_l = 1.0f / s.row_l[r];
+    const uint32_t key = s.thr_key[r];
+    const int64_t cut = s.thr_cut[r];
+    float *p = s.p + r * n;
+    uint8_t *inS = s.inS + r * n;
+    const float *zr = s.z + r * n;
+    // weights and membership; kept list in ascending order
+    const int64_t chunk = (n + NT - 1) / NT;
+    const int64_t lo = tid * chunk, hi = (lo + chunk < n) ? lo + chunk : n;
+    int c = 0;
+    for (int64_t j = lo; j < hi; ++j) {
+        const float zz = zr[j];
+        p[j] = expf(zz - m) * inv_l;
+        const uint32_t u = ord_key(zz);
+        const uint8_t in = (u > key) || (u == key && j <= cut);
+        inS[j] = in;
+        c += in;
+    }
+    int total;
+    int pos = block_exclusive_scan(c, scan, &total);
+    for (int64_t j = lo; j < hi; ++j)
+        if (inS[j]) s.Sl[r * kk + pos++] = (int32_t)j;
+    __syncthreads();
+    // mu = sum_j p_j v_j, float64
+    double *mu = s.mu + r * d;
+    for (int cc = tid; cc < d; cc += NT) {
+        double acc = 0.0;
+        for (int64_t j = 0; j < n; ++j) acc = fma((double)p[j], (double)Elem<T>::load(vh, j * d + cc), acc);
+        mu[cc] = acc;
+    }
+    __syncthreads();
+    double mu2 = 0.0;
+    for (int cc = 0; cc < d; ++cc) mu2 += mu[cc] * mu[cc];
+    // w_j = v_j . mu and ||u_j||^2 = p_j^2 ||v_j - mu||^2
+    for (int64_t j = tid; j < n; j += NT) {
+        double dw = 0.0, du = 0.0;
+        for (int cc = 0; cc < d; ++cc) {
+            const double x = (double)Elem<T>::load(vh, j * d + cc);
+            dw = fma(x, mu[cc], dw);
+            du = fma(x - mu[cc], x - mu[cc], du);
+        }
+        s.w[r * n + j] = (float)dw;
+        s.bq[r * n + j] = (float)((double)p[j] * (double)p[j] * du);
+    }
+    // g = sum_{a in S} u_a, P = p(S)
+    double *g = s.g + r * d;
+    for (int cc = tid; cc < d; cc += NT) {
+        double acc = 0.0;
+        for (int i = 0; i < kk; ++i) {
+            const int64_t a = s.Sl[r * kk + i];
+            acc += (double)p[a] * ((double)Elem<T>::load(vh, a * d + cc) - mu[cc]);
+        }
+        g[cc] = acc;
+    }
+    double P = 0.0;
+    for (int i = tid; i < kk; i += NT) P += (double)p[s.Sl[r * kk + i]];
+    P = block_reduce(P, redd, OpSum());
+    double g2 = 0.0;
+    for (int cc = tid; cc < d; cc += NT) g2 += g[cc] * g[cc];
+    g2 = block_reduce(g2, redd, OpSum());
+    if (tid == 0) {
+        double *sc = s.sc + r * 4;
+        sc[0] = P;
+        sc[1] = g2;
+        sc[2] = mu2;
+        sc[3] = g2 / (P * P);
+        s.st[r * 2 + 0] = (kk < n) ? 1 : 0;
+        s.st[r * 2 + 1] = 0;
+        gap_traj[r * T_len] = (float)(sqrt(g2) / P);
+    }
+}
+
+// a_j = g . u_j = p_j (v_j . g - mu . g)
+template <typename T>
+__global__ void __launch_bounds__(256)
+swap_dots_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, SwapState s) {
+    __shared__ float gs[256];
+    __shared__ double redd[256];
+    const int64_t r = blockIdx.y;
+    if (!s.st[r * 2]) return;
+    const int tid = threadIdx.x;
+    const int64_t h = r / G;
+    const T *vh = v + h * n * d;
+    const double *g = s.g + r * d, *mu = s.mu + r * d;
+    double mg = 0.0;
+    for (int c = tid; c < d; c += blockDim.x) {
+        gs[c] = (float)g[c];
+        mg += mu[c] * g[c];
+    }
+    mg = block_reduce(mg, redd, OpSum());
+    for (int64_t j = (int64_t)blockIdx.x * blockDim.x + tid; j < n; j += (int64_t)gridDim.x * blockDim.x) {
+        float acc = 0.f;
+        for (int c = 0; c < d; ++c) acc = fmaf(Elem<T>::load(vh, j * d + c), gs[c], acc);
+        s.a[r * n + j] = s.p[r * n + j] * (float)((double)acc - mg);
+    }
+}
+
+// every (kept i, dropped j) pair of a tile: 32 kept x 128 keys per workgroup
+template <typename T>
+__global__ void __launch_bounds__(256)
+swap_pairs_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, SwapState s) {
+    constexpr int TI = 32, TJ = 128, TD = 32;
+    __shared__ float Vi[TI][TD + 1];
+    __shared__ float Vj[TJ][TD + 1];
+    __shared__ int idx_i[TI];
+    __shared__ float redv[256];
+    __shared__ int64_t redp[256];
+    const int64_t r = blockIdx.y;
+    if (!s.st[r * 2]) return;
+    const int tid = threadIdx.x;
+    const int64_t h = r / G;
+    const T *vh = v + h * n * d;
+    const int itiles = (kk + TI - 1) / TI;
+    const int it = blockIdx.x % itiles;
+    const int64_t jt = blockIdx.x / itiles;
+    const int i0 = it * TI;
+    const int64_t j0 = jt * TJ;
+    if (tid < TI) idx_i[tid] = (i0 + tid < kk) ? s.Sl[r * kk + i0 + tid] : -1;
+    __syncthreads();
+    const int ty = tid / 32, tx = tid % 32;  // rows ty*4.., keys tx + 32*c
+    float acc[4][4] = {};
+    for (int c0 = 0; c0 < d; c0 += TD) {
+        for (int e = tid; e < TI * TD; e += 256) {
+            const int rr = e / TD, cc = e % TD;
+            const int a = idx_i[rr];
+            Vi[rr][cc] = (a >= 0 && c0 + cc < d) ? Elem<T>::load(vh, (int64_t)a * d + c0 + cc) : 0.f;
+        }
+        for (int e = tid; e < TJ * TD; e += 256) {
+            const int rr = e / TD, cc = e % TD;
+            const int64_t j = j0 + rr;
+            Vj[rr][cc] = (j < n && c0 + cc < d) ? Elem<T>::load(vh, j * d + c0 + cc) : 0.f;
+        }
+        __syncthreads();
+#pragma unroll 8
+        for (int cc = 0; cc < TD; ++cc) {
+            float ai[4], bj[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) ai[u] = Vi[ty * 4 + u][cc];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) bj[u] = Vj[tx + 32 * u][cc];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int w = 0; w < 4; ++w) acc[u][w] = fmaf(ai[u], bj[w], acc[u][w]);
+        }
+        __syncthreads();
+    }
+    const double *sc = s.sc + r * 4;
+    const float P = (float)sc[0], g2 = (float)sc[1], mu2 = (float)sc[2];
+    const float *p = s.p + r * n, *w = s.w + r * n, *bq = s.bq + r * n, *a = s.a + r * n;
+    const uint8_t *inS = s.inS + r * n;
+    float bv = INFINITY;
+    int64_t bp = INT64_MAX;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int i = idx_i[ty * 4 + u];
+        if (i < 0) continue;
+        const float pi = p[i], wi = w[i], Ai = g2 + bq[i] - 2.f * a[i];
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+            const int64_t j = j0 + tx + 32 * x;
+            if (j >= n || inS[j]) continue;
+            const float pj = p[j];
+            const float cij = pi * pj * (acc[u][x] - wi - w[j] + mu2);
+            const float num = Ai + bq[j] + 2.f * a[j] - 2.f * cij;
+            const float den = P - pi + pj;
+            const float val = num / (den * den);
+            const int64_t pidx = (int64_t)i * n + j;
+            if (val < bv || (val == bv && pidx < bp)) { bv = val; bp = pidx; }
+        }
+    }
+    redv[tid] = bv;
+    redp[tid] = bp;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+        if (tid < st) {
+            const float v2 = redv[tid + st];
+            const int64_t p2 = redp[tid + st];
+            if (v2 < redv[tid] || (v2 == redv[tid] && p2 < redp[tid])) { redv[tid] = v2; redp[tid] = p2; }
+        }
+        __syncthreads();
+    }
+    if (tid == 0) {
+        s.pv[r * s.nblk + blockIdx.x] = redv[0];
+        s.pp[r * s.nblk + blockIdx.x] = redp[0];
+    }
+}
+
+// reduce the tile winners, then apply the swap (or retire the row)
+template <typename T>
+__global__ void __launch_bounds__(256)
+swap_apply_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, SwapState s,
+                  float *gap_traj, int T_len) {
+    __shared__ float redv[256];
+    __shared__ int64_t redp[256];
+    __shared__ double redd[256];
+    __shared__ int decide;
+    const int64_t r = blockIdx.x;
+    if (!s.st[r * 2]) return;
+    const int tid = threadIdx.x;
+    float bv = INFINITY;
+    int64_t bp = INT64_MAX;
+    for (int b = tid; b < s.nblk; b += blockDim.x) {
+        const float v2 = s.pv[r * s.nblk + b];
+        const int64_t p2 = s.pp[r * s.nblk + b];
+        if (v2 < bv || (v2 == bv && p2 < bp)) { bv = v2; bp = p2; }
+    }
+    redv[tid] = bv;
+    redp[tid] = bp;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+        if (tid < st) {
+            const float v2 = redv[tid + st];
+            const int64_t p2 = redp[tid + st];
+            if (v2 < redv[tid] || (v2 == redv[tid] && p2 < redp[tid])) { redv[tid] = v2; redp[tid] = p2; }
+        }
+        __syncthreads();
+    }
+    // the float32 search proposes (i, j); accept only on a strict decrease of
+    // the float64 value ||g - u_i + u_j||^2 / (P - p_i + p_j)^2
+    double *sc = s.sc + r * 4;
+    if (!(redv[0] < INFINITY) || redp[0] < 0 || redp[0] >= (int64_t)n * n) {  // no finite candidate
+        if (tid == 0) s.st[r * 2] = 0;
+        return;
+    }
+    const int64_t i = redp[0] / n, j = redp[0] % n;
+    const int64_t h = r / G;
+    const T *vh = v + h * n * d;
+    const float *p = s.p + r * n;
+    double *g = s.g + r * d;
+    const double *mu = s.mu + r * d;
+    double g2 = 0.0;
+    for (int c = tid; c < d; c += blockDim.x) {
+        const double ui = (double)p[i] * ((double)Elem<T>::load(vh, i * d + c) - mu[c]);
+        const double uj = (double)p[j] * ((double)Elem<T>::load(vh, j * d + c) - mu[c]);
+        const double gn = g[c] - ui + uj;
+        g2 += gn * gn;
+    }
+    g2 = block_reduce(g2, redd, OpSum());
+    const double P = sc[0] - (double)p[i] + (double)p[j];
+    if (tid == 0) decide = (g2 / (P * P) < sc[3]) ? 1 : 0;
+    __syncthreads();
+    if (!decide) {
+        if (tid == 0) s.st[r * 2] = 0;
+        return;
+    }
+    for (int c = tid; c < d; c += blockDim.x) {
+        const double ui = (double)p[i] * ((double)Elem<T>::load(vh, i * d + c) - mu[c]);
+        const double uj = (double)p[j] * ((double)Elem<T>::load(vh, j * d + c) - mu[c]);
+        g[c] = g[c] - ui + uj;
+    }
+    if (tid == 0) {
+        s.inS[r * n + i] = 0;
+        s.inS[r * n + j] = 1;
+        for (int t = 0; t < kk; ++t)
+            if (s.Sl[r * kk + t] == (int32_t)i) { s.Sl[r * kk + t] = (int32_t)j; break; }
+        sc[0] = P;
+        sc[1] = g2;
+        sc[3] = g2 / (P * P);
+        const int sw = ++s.st[r * 2 + 1];
+        gap_traj[r * T_len + sw] = (float)(sqrt(g2) / P);
+    }
+}
+
+__global__ void __launch_bounds__(256)
+swap_final_kernel(int64_t n, int kk, SwapState s, int32_t *s_idx, float *gap_traj, int T_len,
+                  int32_t *n_swaps, float *dropped) {
+    __shared__ int scan[256];
+    __shared__ double redd[256];
+    const int64_t r = blockIdx.x;
+    const int tid = threadIdx.x, NT = blockDim.x;
+    const uint8_t *inS = s.inS + r * n;
+    const float *p = s.p + r * n;
+    const int64_t chunk = (n + NT - 1) / NT;
+    const int64_t lo = tid * chunk, hi = (lo + chunk < n) ? lo + chunk : n;
+    int c = 0;
+    double dm = 0.0;
+    for (int64_t j = lo; j < hi; ++j) {
+        c += inS[j];
+        if (!inS[j]) dm += (double)p[j];
+    }
+    int total;
+    int pos = block_exclusive_scan(c, scan, &total);
+    for (int64_t j = lo; j < hi; ++j)
+        if (inS[j]) s_idx[r * kk + pos++] = (int32_t)j;
+    dm = block_reduce(dm, redd, OpSum());
+    const int sw = s.st[r * 2 + 1];
+    for (int t = sw + 1 + tid; t < T_len; t += NT) gap_traj[r * T_len + t] = __int_as_float(0x7fc00000);
+    if (tid == 0) {
+        n_swaps[r] = sw;
+        if (dropped) dropped[r] = (float)dm;
+    }
+}
+
+// ===========================================================================
+// host side
+// ===========================================================================
+namespace {
+
+size_t small_lds(int n, int d, int nt) {
+    size_t b = (size_t)n * n * 8 + (size_t)n * 8 * 3 + (size_t)d * 8 + (size_t)nt * 16;
+    b += (size_t)(n + (n & 1)) * 4 + (size_t)n * d * 4;
+    return b;
+}
+
+struct SwapLayout {
+    SwapState s;
+    float *z, *row_m, *row_l;
+    uint32_t *thr_key;
+    int32_t *thr_cut;
+    size_t bytes;
+};
+
+SwapLayout swap_layout(const fw_rows &rows, int k, void *ws) {
+    const size_t R = (size_t)rows.H * rows.G, n = rows.n, d = rows.d;
+    SwapLayout L{};
+    size_t off = 0;
+    char *base = (char *)ws;
+    auto take = [&](size_t bytes) -> void * {
+        off = align_up(off, 256);
+        void *p = base ? base + off : nullptr;
+        off += bytes;
+        return p;
+    };
+    const int itiles = (k + 31) / 32;
+    const int64_t jtiles = ((int64_t)n + 127) / 128;
+    L.s.nblk = (int)(itiles * jtiles);
+    L.z = (float *)take(R * n * 4);
+    L.row_m = (float *)take(R * 4);
+    L.row_l = (float *)take(R * 4);
+    L.thr_key = (uint32_t *)take(R * 4);
+    L.thr_cut = (int32_t *)take(R * 4);
+    L.s.p = (float *)take(R * n * 4);
+    L.s.inS = (uint8_t *)take(R * n);
+    L.s.Sl = (int32_t *)take(R * k * 4);
+    L.s.w = (float *)take(R * n * 4);
+    L.s.bq = (float *)take(R * n * 4);
+    L.s.a = (float *)take(R * n * 4);
+    L.s.mu = (double *)take(R * d * 8);
+    L.s.g = (double *)take(R * d * 8);
+    L.s.sc = (double *)take(R * 4 * 8);
+    L.s.st = (int32_t *)take(R * 2 * 4);
+    L.s.pv = (float *)take(R * L.s.nblk * 4);
+    L.s.pp = (int64_t *)take(R * L.s.nblk * 8);
+    L.s.z = L.z;
+    L.s.row_m = L.row_m;
+    L.s.row_l = L.row_l;
+    L.s.thr_key = L.thr_key;
+    L.s.thr_cut = L.thr_cut;
+    L.bytes = align_up(off, 256);
+    return L;
+}
+
+}  // namespace
+
+size_t swap_ws_bytes(const fw_rows &rows, int k, int max_iters) {
+    (void)max_iters;
+    if (rows.n <= 64) return 256;
+    return swap_layout(rows, k, nullptr).bytes;
+}
+
+template <typename T>
+static hipError_t swap_large(const fw_rows &rows, int k, int max_iters, int32_t *s_idx,
+                             float *gap_traj, int32_t *n_swaps, float *dropped, void *ws,
+                             hipStream_t st) {
+    SwapLayout L = swap_layout(rows, k, ws);
+    const int64_t H = rows.H, G = rows.G, n = rows.n, R = H * G;
+    const int d = (int)rows.d;
+    hipError_t e = launch_scores(rows.dtype, rows.q, rows.k, rows.scale, rows.bias, H, G, n, d, L.z, st);
+    if (e != hipSuccess) return e;
+    KsArg ks{};
+    ks.n = 1;
+    ks.k[0] = k;
+    ks.perm[0] = 0;
+    e = launch_select(L.z, R, n, ks, L.row_m, L.row_l, L.thr_key, L.thr_cut, nullptr, k, st);
+    if (e != hipSuccess) return e;
+    const T *v = (const T *)rows.v;
+    const int T_len = max_iters + 1;
+    hipLaunchKernelGGL(swap_init_kernel<T>, dim3((unsigned)R), dim3(256), 0, st, v, G, n, d, k, L.s,
+                       gap_traj, T_len);
+    const unsigned dot_blocks = (unsigned)((n + 255) / 256 < 64 ? (n + 255) / 256 : 64);
+    for (int it = 0; it < max_iters; ++it) {
+        hipLaunchKernelGGL(swap_dots_kernel<T>, dim3(dot_blocks, (unsigned)R), dim3(256), 0, st, v, G,
+                           n, d, L.s);
+        hipLaunchKernelGGL(swap_pairs_kernel<T>, dim3((unsigned)L.s.nblk, (unsigned)R), dim3(256), 0,
+                           st, v, G, n, d, k, L.s);
+        hipLaunchKernelGGL(swap_apply_kernel<T>, dim3((unsigned)R), dim3(256), 0, st, v, G, n, d, k,
+                           L.s, gap_traj, T_len);
+    }
+    hipLaunchKernelGGL(swap_final_kernel, dim3((unsigned)R), dim3(256), 0, st, n, k, L.s, s_idx,
+                       gap_traj, T_len, n_swaps, dropped);
+    return hipGetLastError();
+}
+
+hipError_t launch_swap(const fw_rows &rows, int k, int max_iters, int32_t *s_idx, float *gap_traj,
+                       int32_t *n_swaps, float *dropped, void *ws, hipStream_t st) {
+    const int64_t R = rows.H * rows.G;
+    if (rows.n <= 64) {
+        const int n = (int)rows.n, d = (int)rows.d;
+        int nt = 256;
+        while (nt > 64 && small_lds(n, d, nt) > 160 * 1024) nt >>= 1;
+        const size_t lds = small_lds(n, d, nt);
+        if (rows.dtype == FW_BF16)
+            hipLaunchKernelGGL(swap_small_kernel<uint16_t>, dim3((unsigned)R), dim3(nt), lds, st,
+                               (const uint16_t *)rows.q, (const uint16_t *)rows.k, (const uint16_t *)rows.v,
+                               rows.scale, rows.bias, rows.G, n, d, k, max_iters, s_idx, gap_traj,
+                               n_swaps, dropped);
+        else
+            hipLaunchKernelGGL(swap_small_kernel<float>, dim3((unsigned)R), dim3(nt), lds, st,
+                               (const float *)rows.q, (const float *)rows.k, (const float *)rows.v,
+                               rows.scale, rows.bias, rows.G, n, d, k, max_iters, s_idx, gap_traj,
+                               n_swaps, dropped);
+        return hipGetLastError();
+    }
+    if (rows.dtype == FW_BF16)
+        return swap_large<uint16_t>(rows, k, max_iters, s_idx, gap_traj, n_swaps, dropped, ws, st);
+    return swap_large<float>(rows, k, max_iters, s_idx, gap_traj, n_swaps, dropped, ws, st);
+}
+
+}  // namespace fw

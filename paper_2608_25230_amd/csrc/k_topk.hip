@@ -61,7 +61,7 @@ scores_kernel(const T *__restrict__ q, const T *__restrict__ k, const float *__r
         }
         __syncthreads();
     }
-    const float sc = scale ? scale[h] : rsqrtf((float)d);
+    const float sc = scale ? scale[h] : (float)(1.0 / sqrt((double)d));
 #pragma unroll
     for (int a = 0; a < 2; ++a) {
         int64_t g = g0 + ty * 2 + a;

@@ -1,0 +1,167 @@
+"""GPU parity of fw_best_subset (exhaustive enumeration, float64) against the
+oracle, including the paper's worked examples and the hardness family."""
+import itertools
+import math
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import fw_oracle as O
+from paper_2608_25230_amd import workloads as W
+from tests.parity import Tally, rel_scalar, t2np
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_fw():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2608_25230_amd import fw
+    fw.lib()
+    return torch, fw
+
+
+def _run(torch, fw, rows, k):
+    dev = fw.upload(rows)
+    out = fw.best_subset(dev["q"], dev["k"], dev["v"], k, dev["scale"], dev["bias"])
+    torch.cuda.synchronize()
+    return {key: t2np(val) for key, val in out.items() if not key.startswith("_")}
+
+
+def _check_rows(rows, k, out, hs, tol=1e-5):
+    q, K, V = rows.as_f64("q"), rows.as_f64("k"), rows.as_f64("v")
+    bias = None if rows.bias is None else rows.bias.astype(np.float64)
+    tally = Tally()
+    for h in hs:
+        for g in range(rows.G):
+            z = O.logits(q[h, g], K[h], float(rows.scale[h]), bias)
+            ref = O.row_best_subset(z, V[h], k)
+            p = O.weights(z)
+            gb = out["best_idx"][h, g]
+            exact = np.array_equal(gb, ref["best_idx"])
+            es_gpu_set = O.forced_error(p, V[h], gb)
+            tie = es_gpu_set <= ref["best_gap"] * (1 + tol) + 1e-15
+            tally.add(exact, tie, f"row {(h, g)} gpu {gb} ref {ref['best_idx']}")
+            floor = 1e-6 * np.linalg.norm(O.dense_output(p, V[h]))
+            assert rel_scalar(out["best_gap"][h, g], ref["best_gap"], floor) <= tol, (h, g)
+            assert rel_scalar(out["topk_gap"][h, g], ref["topk_gap"], floor) <= tol, (h, g)
+            assert abs(out["closed"][h, g] - max(0.0, ref["closed"])) <= 10 * tol, (h, g)
+            assert abs(out["dropped_topk"][h, g] - ref["dropped_topk"]) <= tol * max(ref["dropped_topk"], 1e-6)
+            assert np.array_equal(out["topk_idx"][h, g], ref["topk_idx"]), (h, g)
+    assert tally.fail == 0, tally
+    return tally
+
+
+def test_tiny_exhaustive_all_rows(torch_fw):
+    torch, fw = torch_fw
+    wl = W.tiny_exhaustive(seed=0)
+    out = _run(torch, fw, wl.rows, wl.k)
+    t = _check_rows(wl.rows, wl.k, out, range(wl.rows.H))
+    print("tiny exhaustive:", t)
+
+
+def _instance_rows(p, v):
+    """The paper's instances in attention form: q = 0, bias = log p."""
+    n = len(p)
+    v = np.asarray(v, np.float32).reshape(1, n, -1)
+    d = v.shape[-1]
+    return W.Rows("f32", np.zeros((1, 1, d), np.float32), np.zeros((1, n, d), np.float32), v,
+                  np.ones(1, np.float32), np.log(np.asarray(p, np.float64)).astype(np.float32))
+
+
+def test_example_2_3_on_gpu(torch_fw):
+    torch, fw = torch_fw
+    rows = _instance_rows([0.45, 0.45, 0.10], [-1, 1, 5])
+    out = _run(torch, fw, rows, 2)
+    assert out["best_idx"][0, 0].tolist() == [0, 2]
+    assert sorted(out["topk_idx"][0, 0].tolist()) == [0, 1]
+    z = rows.bias.astype(np.float64)
+    p = O.weights(z)
+    v = rows.as_f64("v")[0]
+    assert out["best_gap"][0, 0] == pytest.approx(O.forced_error(p, v, [0, 2]), rel=1e-6)
+    assert out["best_gap"][0, 0] == pytest.approx(9 / 22, rel=1e-6)
+    assert out["topk_gap"][0, 0] == pytest.approx(0.5, rel=1e-6)
+    assert out["closed"][0, 0] == pytest.approx(2 / 11, rel=1e-5)
+
+
+@pytest.mark.parametrize("s,want", [(1, [1]), (2, [0, 3]), (3, [0, 1, 3])])
+def test_example_A3_tie_rule_on_gpu(torch_fw, s, want):
+    torch, fw = torch_fw
+    rows = _instance_rows([0.25] * 4, [0, 1, 2, 3])
+    out = _run(torch, fw, rows, s)
+    assert out["best_idx"][0, 0].tolist() == want
+    exact = {1: 0.5, 2: 0.0, 3: 1 / 6}[s]
+    assert out["best_gap"][0, 0] == pytest.approx(exact, abs=1e-7)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_hardness_family_on_gpu(torch_fw, seed):
+    torch, fw = torch_fw
+    rng = np.random.default_rng(2000 + seed)
+    m = int(rng.choice([4, 8, 12, 16]))
+    w = [int(x) for x in rng.integers(0, 9, size=m)]
+    W_ = sum(w)
+    s = m // 2
+    exact = {A: 2 * abs(Fraction(m * sum(w[i] for i in A) - s * W_, m * m))
+             for A in itertools.combinations(range(m), s)}
+    ES = min(exact.values())
+    rows = _instance_rows([1.0 / m] * m, w)
+    out = _run(torch, fw, rows, s)
+    got = tuple(out["best_idx"][0, 0].tolist())
+    assert exact[got] == ES
+    if m in (4, 8, 16):  # masses 1/m and sums are dyadic: exact ties pick the smallest tuple
+        assert got == min(A for A, e in exact.items() if e == ES)
+    assert out["best_gap"][0, 0] == pytest.approx(float(ES), abs=1e-6)
+
+
+@pytest.mark.parametrize("cfg", [
+    dict(n=24, k=6, d=128, H=48),
+    dict(n=9, k=1, d=5, H=16), dict(n=9, k=8, d=5, H=16), dict(n=9, k=9, d=5, H=8),
+    dict(n=40, k=3, d=64, H=8), dict(n=64, k=2, d=32, H=4), dict(n=33, k=5, d=256, H=2),
+    dict(n=20, k=10, d=16, H=4),
+])
+def test_shapes_fp32(torch_fw, cfg):
+    torch, fw = torch_fw
+    n, k, d, H = cfg["n"], cfg["k"], cfg["d"], cfg["H"]
+    rows = W.shifted_key_rows(33, n * 100 + k, H, n, d, shift=1.5, block=64)
+    out = _run(torch, fw, rows, k)
+    _check_rows(rows, k, out, range(H))
+
+
+def test_bf16_grouped_rows(torch_fw):
+    torch, fw = torch_fw
+    wl = W.streaming_topk(seed=4, layers=1, kv_heads=2, q_per_kv=2, rows_per_q=4, n=20, d=64, ks=(5,))
+    out = _run(torch, fw, wl.rows, 5)
+    _check_rows(wl.rows, 5, out, range(wl.rows.H), tol=1e-5)
+
+
+def test_permutation_invariance_on_gpu(torch_fw):
+    torch, fw = torch_fw
+    rows = W.shifted_key_rows(34, 0, 8, 14, 16, block=64)
+    out = _run(torch, fw, rows, 4)
+    rng = np.random.default_rng(0)
+    perm = rng.permutation(14)
+    prow = W.Rows("f32", rows.q, np.ascontiguousarray(rows.k[:, perm]), np.ascontiguousarray(rows.v[:, perm]),
+                  rows.scale, None)
+    outp = _run(torch, fw, prow, 4)
+    assert np.allclose(out["best_gap"], outp["best_gap"], rtol=1e-6)
+    assert np.allclose(out["topk_gap"], outp["topk_gap"], rtol=1e-6)
+
+
+def test_full_size_exhaustive_sampled(torch_fw):
+    """168,192 rows, n = 24, k = 6 (2.26e10 subsets) in the benchmark's launch
+    configuration; sampled rows against the oracle, properties on all rows."""
+    torch, fw = torch_fw
+    wl = W.exhaustive_rows(seed=0)
+    out = _run(torch, fw, wl.rows, wl.k)
+    rng = np.random.default_rng(1)
+    hs = sorted(rng.choice(wl.rows.H, 12, replace=False).tolist())
+    t = _check_rows(wl.rows, wl.k, out, hs)
+    print("full-size sampled:", t)
+    bi = out["best_idx"].reshape(-1, wl.k)
+    assert np.all(np.diff(bi, axis=1) > 0) and bi.min() >= 0 and bi.max() < 24
+    assert np.all(out["best_gap"] <= out["topk_gap"] * (1 + 1e-6))
+    assert np.all((out["closed"] >= 0) & (out["closed"] <= 1))
