@@ -152,10 +152,15 @@ extern "C" {
 const char *fw_last_error(void) { return g_err; }
 const char *fw_version(void) { return "libfw 0.1 (gfx950)"; }
 
+size_t dense_topk_ws_bytes(const fw_rows *rows, const fw::KsArg &k) {
+    if (fw::fused_topk_supported(*rows, k)) return fw::fused_topk_ws_bytes(*rows, k.k[k.n - 1]);
+    return dense_topk_layout(rows, k.n, nullptr).bytes;
+}
+
 size_t fw_dense_topk_workspace_size(const fw_rows *rows, const int32_t *ks, int32_t n_ks) {
     fw::KsArg k;
     if (check_rows(rows, true) != FW_OK || parse_ks(rows, ks, n_ks, &k) != FW_OK) return 0;
-    return dense_topk_layout(rows, n_ks, nullptr).bytes;
+    return dense_topk_ws_bytes(rows, k);
 }
 
 fw_status fw_dense_topk(const fw_rows *rows, const int32_t *ks, int32_t n_ks, float *o, float *o_s,
@@ -168,10 +173,12 @@ fw_status fw_dense_topk(const fw_rows *rows, const int32_t *ks, int32_t n_ks, fl
     if (!gap || !dropped) return fail(FW_E_NULL, "gap and dropped are required");
     const int kmax = k.k[k.n - 1];
     if (topk_idx && kmax > 16384) return fail(FW_E_UNSUPPORTED, "topk_idx needs kmax <= 16384");
-    const DenseTopkWs need = dense_topk_layout(rows, n_ks, nullptr);
-    if ((s = check_ws(ws, ws_bytes, need.bytes)) != FW_OK) return s;
-    const DenseTopkWs w = dense_topk_layout(rows, n_ks, ws);
+    if ((s = check_ws(ws, ws_bytes, dense_topk_ws_bytes(rows, k))) != FW_OK) return s;
     hipStream_t st = (hipStream_t)stream;
+    if (fw::fused_topk_supported(*rows, k))
+        return hip_status(fw::launch_fused_topk(*rows, k, o, o_s, gap, dropped, topk_idx, ws, st),
+                          "fw_dense_topk");
+    const DenseTopkWs w = dense_topk_layout(rows, n_ks, ws);
     const int64_t H = rows->H, G = rows->G, n = rows->n;
     const int d = (int)rows->d;
     hipError_t e = fw::launch_scores(rows->dtype, rows->q, rows->k, rows->scale, rows->bias, H, G, n,

@@ -25,6 +25,12 @@ hipError_t launch_tiers(int dtype, const void *v, const float *z, const float *r
                         int64_t H, int64_t G, int64_t n, int d, const KsArg &ks, float *o,
                         float *o_s, float *gap, float *dropped, hipStream_t st);
 
+// k_topk_fused.hip -- one-kernel path for bf16, d = 128, n in {1024, 2048, 4096}
+bool fused_topk_supported(const fw_rows &rows, const KsArg &ks);
+size_t fused_topk_ws_bytes(const fw_rows &rows, int kmax);
+hipError_t launch_fused_topk(const fw_rows &rows, const KsArg &ks, float *o, float *o_s, float *gap,
+                             float *dropped, int32_t *topk_idx, void *ws, hipStream_t st);
+
 // k_subset.hip -- exhaustive best subset (float64)
 size_t best_subset_ws_bytes(int64_t n, int k);
 hipError_t launch_best_subset(const fw_rows &rows, int k, int32_t *best_idx, float *best_gap,

@@ -1,0 +1,867 @@
+// Fused top-k forced-weight evaluation for bf16 rows with d = 128 and
+// n in {1024, 2048, 4096} (Definition 2.1; gap through Lemma 2.2's first
+// form).  One workgroup takes 16 query rows of one key/value unit and every
+// key; nothing but the results leaves the chip.
+//
+//   1. logits   S^T = K Q^T on MFMA (16x16x32 bf16, fp32 accumulate); each of
+//               the 8 waves owns n/8 keys and keeps its 16 x n/8 logits in
+//               registers (lane l holds row l%16 for 4 keys of every tile)
+//   2. softmax  row max, min and sum of exp across lanes and waves
+//   3. select   per row a 1024-bin histogram of the logits over [min, max]
+//               (bins are monotone in the logit), the bin holding the k-th
+//               largest for every budget, the few logits of that bin gathered
+//               and sorted: the exact k-th key (logit desc, index asc)
+//   4. tiers    P = softmax weights rounded to bf16, split by tier (ranks
+//               [0,k_0), [k_0,k_1), ..., rest); O^T_t += V^T P^T_t on MFMA,
+//               V staged through LDS and read transposed (ds_read_tr16_b64);
+//               one pass over the keys per 32 or 64 columns of d bounds the
+//               accumulators
+//   5. epilogue partial tier sums of the eight waves combined in LDS; o, o_S,
+//               gap (1 - p(S)) ||m_{S^c} - m_S||, dropped mass.
+// Rows whose selection is degenerate (all logits equal, non-finite values, or
+// more than 128 logits sharing the threshold bin) are listed and recomputed by
+// a one-row-per-workgroup fallback that selects by radix over the exact keys.
+#include "fw_internal.hpp"
+#include "select.hpp"
+
+namespace fw {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+namespace {
+constexpr int FR = 16;        // rows per workgroup
+constexpr int FW = 8;         // waves per workgroup
+constexpr int FTH = FW * 64;  // threads per workgroup
+constexpr int FD = 128;       // head dimension
+constexpr int FBINS = 1024;   // histogram bins per row
+constexpr int FCAP = 128;     // logits gathered from the threshold bin
+constexpr float LOG2E = 1.4426950408889634f;
+// keeps the scheduler from hoisting the work of every tile of an unrolled
+// per-logit loop at once (which exhausts the register file)
+#define FW_TILE_FENCE() __builtin_amdgcn_sched_barrier(0)
+
+// An opaque copy: the compiler may not assume it equals its input, so work
+// recomputed from it in a later pass is not merged with an earlier pass
+// (keeping hundreds of per-logit compare masks alive between passes).
+template <typename T>
+__device__ __forceinline__ T opaque(T x) {
+    asm volatile("" : "+v"(x));
+    return x;
+}
+
+struct FusedLds {
+    size_t wred, thr, ssb;            // persistent
+    size_t hist, lists, cntr;         // selection
+    size_t vst;                       // V staging
+    size_t opart;                     // partial tier sums
+    size_t total;
+};
+
+__host__ __device__ constexpr int fused_dq(int nk) { return nk >= 2 ? 32 : 64; }
+
+__host__ __device__ inline FusedLds fused_lds(int nk) {
+    const int dq = fused_dq(nk);
+    FusedLds L{};
+    size_t o = 0;
+    auto take = [&](size_t bytes) { size_t at = o; o = align_up(o + bytes, 16); return at; };
+    L.wred = take((size_t)4 * FW * FR * 4);    // [quantity][wave][row]
+    L.thr = take((size_t)FR * 4 * 4 * 4);      // [row][budget][4 ints]
+    L.ssb = take((size_t)(FD / dq) * FR * 4 * 4);  // [pass][row][budget] squared norms
+    const size_t base = o;
+    L.hist = base;
+    L.lists = align_up(base + (size_t)FR * FBINS * 4, 16);
+    L.cntr = align_up(L.lists + (size_t)FR * nk * FCAP * 8, 16);
+    const size_t sel_end = L.cntr + (size_t)FR * 8 * 4;
+    L.vst = base;
+    const size_t v_end = base + (size_t)FW * 2 * 32 * (dq + 8) * 2;
+    L.opart = base;
+    const size_t o_end = base + (size_t)FW * (nk + 1) * dq * FR * 4;
+    size_t end = sel_end > v_end ? sel_end : v_end;
+    end = end > o_end ? end : o_end;
+    L.total = align_up(end, 16);
+    return L;
+}
+
+__device__ __forceinline__ uint16_t f2bf_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+// reductions over the four lanes of a wave that share a row (l, l^16, l^32, l^48)
+__device__ __forceinline__ float rmax4(float v) {
+    v = fmaxf(v, __shfl_xor(v, 16));
+    return fmaxf(v, __shfl_xor(v, 32));
+}
+__device__ __forceinline__ float rmin4(float v) {
+    v = fminf(v, __shfl_xor(v, 16));
+    return fminf(v, __shfl_xor(v, 32));
+}
+__device__ __forceinline__ float rsum4(float v) {
+    v += __shfl_xor(v, 16);
+    return v + __shfl_xor(v, 32);
+}
+
+// Buffer loads: a per-unit descriptor (wave-uniform base and size, reads past
+// the size return zero), one 32-bit lane offset and a uniform offset, so the
+// unrolled tile loops keep no 64-bit address per tile in vector registers.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ bf16x8 bload8(rsrc_t r, uint32_t voff, uint32_t soff) {
+    return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+}  // namespace
+
+struct FusedArgs {
+    const uint16_t *q, *k, *v;
+    const float *scale, *bias;
+    int64_t H, G;
+    int n;
+    KsArg ks;
+    float *o, *o_s, *gap, *dropped;
+    unsigned long long *sel;  // [R][kmax] selected keys, when indices are requested
+    int kmax;
+    int32_t *flags, *flag_list, *flag_count;
+};
+
+// ---------------------------------------------------------------------------
+template <int TILES, int NK, bool BIAS, bool SEL>
+__global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
+    constexpr int NT = NK + 1;
+    // columns of d per pass of the tier products: fewer with more tiers, so
+    // that the NT x DQ/16 accumulator tiles stay within the register budget
+    constexpr int DQ = fused_dq(NK);
+    constexpr int NPASS = FD / DQ, DT = DQ / 16, CPT = DQ / 32;
+    constexpr int VCR = DQ / 8, VLQ = DQ / 16, VP = DQ + 8;  // V staging: chunks/row, loads/lane, pitch
+    extern __shared__ __align__(16) unsigned char smem[];
+    const FusedLds L = fused_lds(NK);
+    float *wred = (float *)(smem + L.wred);
+    int *thr = (int *)(smem + L.thr);
+    float *ssb = (float *)(smem + L.ssb);
+    int *hist = (int *)(smem + L.hist);
+    unsigned long long *lists = (unsigned long long *)(smem + L.lists);
+    int *cntr = (int *)(smem + L.cntr);
+    uint16_t *vst = (uint16_t *)(smem + L.vst);
+    float *opart = (float *)(smem + L.opart);
+#define WRED(qq, ww, rr) wred[((qq) * FW + (ww)) * FR + (rr)]
+#define THR(rr, kk, ff) thr[((rr) * 4 + (kk)) * 4 + (ff)]
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int rl = lane & 15, grp = lane >> 4;
+    // workgroup -> (unit, row tile); the row tiles of a unit land on one XCD
+    // (workgroups are dealt to the 8 XCDs round-robin) so they share its L2
+    const int64_t tiles_per_unit = a.G / FR;
+    int64_t h, rt;
+    {
+        const int64_t b = blockIdx.x;
+        if ((a.H & 7) == 0) {
+            const int64_t xcd = b & 7, s = b >> 3;
+            h = (s / tiles_per_unit) * 8 + xcd;
+            rt = s % tiles_per_unit;
+        } else {
+            h = b / tiles_per_unit;
+            rt = b % tiles_per_unit;
+        }
+    }
+    const int n = a.n;
+    const int64_t row0 = h * a.G + rt * FR;
+    const float sc = a.scale ? a.scale[h] : (float)(1.0 / sqrt((double)FD));
+    const int kw0 = w * 16 * TILES;  // this wave's first key
+
+    // ---- 1. logits --------------------------------------------------------
+    float S[TILES][4];
+    {
+        bf16x8 qb[4];
+        const uint16_t *qr = a.q + (row0 + rl) * FD + 8 * grp;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) qb[s] = *(const bf16x8 *)(qr + 32 * s);
+        const rsrc_t kres = make_rsrc(a.k + h * (int64_t)n * FD, (uint32_t)n * FD * 2);
+        const uint32_t kvo = ((uint32_t)(kw0 + rl) * FD + 8 * grp) * 2;
+        const rsrc_t bres = make_rsrc(BIAS ? (const void *)a.bias : (const void *)a.k, BIAS ? (uint32_t)n * 4 : 0u);
+        const uint32_t bvo = (uint32_t)(kw0 + 4 * grp) * 4;
+        bf16x8 kn[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) kn[s] = bload8(kres, kvo, 64 * s);
+#pragma unroll
+        for (int t = 0; t < TILES; ++t) {
+            bf16x8 kc[4];
+#pragma unroll
+            for (int s = 0; s < 4; ++s) kc[s] = kn[s];
+            if (t + 1 < TILES) {
+#pragma unroll
+                for (int s = 0; s < 4; ++s) kn[s] = bload8(kres, kvo, (uint32_t)(16 * (t + 1) * FD * 2 + 64 * s));
+            }
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc[s], qb[s], acc, 0, 0, 0);
+            if (BIAS) {
+                const f32x4 bj = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(bres, bvo, 64 * t, 0));
+#pragma unroll
+                for (int i = 0; i < 4; ++i) S[t][i] = sc * acc[i] + bj[i];
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) S[t][i] = sc * acc[i];
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+
+    // ---- 2. row max / min / sum of exp -----------------------------------
+    {
+        float mx = -INFINITY, mn = INFINITY;
+#pragma unroll
+        for (int t = 0; t < TILES; ++t) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                mx = fmaxf(mx, S[t][i]);
+                mn = fminf(mn, S[t][i]);
+            }
+            FW_TILE_FENCE();
+        }
+        mx = rmax4(mx);
+        mn = rmin4(mn);
+        if (grp == 0) {
+            WRED(0, w, rl) = mx;
+            WRED(1, w, rl) = mn;
+        }
+    }
+    __syncthreads();
+    float m = WRED(0, 0, rl), zmin = WRED(1, 0, rl);
+#pragma unroll
+    for (int ww = 1; ww < FW; ++ww) {
+        m = fmaxf(m, WRED(0, ww, rl));
+        zmin = fminf(zmin, WRED(1, ww, rl));
+    }
+    {
+        // normaliser; written as exp2(S log2e - m log2e) so that it is not merged
+        // with the weights computed later (which would keep 128 values alive)
+        const float mL = -m * LOG2E;
+        float es = 0.f;
+#pragma unroll
+        for (int t = 0; t < TILES; ++t) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) es += __builtin_amdgcn_exp2f(fmaf(S[t][i], LOG2E, mL));
+            FW_TILE_FENCE();
+        }
+        es = rsum4(es);
+        if (grp == 0) WRED(2, w, rl) = es;
+    }
+    for (int e = tid; e < FR * FBINS; e += FTH) hist[e] = 0;
+    for (int e = tid; e < FR * 8; e += FTH) cntr[e] = 0;
+    __syncthreads();
+    float lsum = 0.f;
+#pragma unroll
+    for (int ww = 0; ww < FW; ++ww) lsum += WRED(2, ww, rl);
+    const float inv_l = 1.0f / lsum;
+    const float range = m - zmin;
+    const bool degenerate = !(range > 0.f) || !(range < INFINITY) || !(lsum > 0.f) || !(lsum < INFINITY);
+    const float inv_w = degenerate ? 0.f : (float)FBINS / range;
+
+    // ---- 3. selection -----------------------------------------------------
+#pragma unroll
+    for (int t = 0; t < TILES; ++t) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int bin = min(FBINS - 1, (int)((m - S[t][i]) * inv_w));
+            atomicAdd(&hist[rl * FBINS + bin], 1);
+        }
+        FW_TILE_FENCE();
+    }
+    __syncthreads();
+    // wave w scans rows 2w, 2w+1; lane owns bins [16 lane, 16 lane + 16)
+    for (int rr = 0; rr < FR / FW; ++rr) {
+        const int r = (FR / FW) * w + rr;
+        int c = 0;
+#pragma unroll
+        for (int b = 0; b < 16; ++b) c += hist[r * FBINS + 16 * lane + b];
+        int incl = c;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int y = __shfl_up(incl, off);
+            if (lane >= off) incl += y;
+        }
+        for (int kk = 0; kk < NK; ++kk) {
+            const int kv = a.ks.k[kk];
+            const unsigned long long bal = __ballot(incl >= kv);
+            const int f = __ffsll(bal) - 1;
+            if (lane == f) {
+                int cum = incl - c, bsel = 16 * lane + 15, need = 1, cnt = 0;
+                for (int b = 0; b < 16; ++b) {
+                    const int hb = hist[r * FBINS + 16 * lane + b];
+                    if (cum + hb >= kv) { bsel = 16 * lane + b; need = kv - cum; cnt = hb; break; }
+                    cum += hb;
+                }
+                THR(r, kk, 0) = bsel;
+                THR(r, kk, 1) = need;
+                THR(r, kk, 2) = cnt;
+            }
+        }
+    }
+    __syncthreads();
+    {
+        // logits in the threshold bin of each budget: count, reserve, write
+        int tb[NK], cnt[NK], pos[NK];
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) {
+            tb[kk] = THR(rl, kk, 0);
+            cnt[kk] = 0;
+        }
+        const float m1 = opaque(m), w1 = opaque(inv_w);
+#pragma unroll
+        for (int t = 0; t < TILES; ++t) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int bin = min(FBINS - 1, (int)((m1 - S[t][i]) * w1));
+#pragma unroll
+                for (int kk = 0; kk < NK; ++kk) cnt[kk] += (bin == tb[kk]) ? 1 : 0;
+            }
+            FW_TILE_FENCE();
+        }
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) pos[kk] = cnt[kk] ? atomicAdd(&cntr[rl * 8 + kk], cnt[kk]) : 0;
+        const float m2 = opaque(m1), w2 = opaque(w1);
+#pragma unroll
+        for (int t = 0; t < TILES; ++t) {
+            FW_TILE_FENCE();
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int bin = min(FBINS - 1, (int)((m2 - S[t][i]) * w2));
+#pragma unroll
+                for (int kk = 0; kk < NK; ++kk) {
+                    if (bin == tb[kk]) {
+                        if (pos[kk] < FCAP) {
+                            const uint32_t j = (uint32_t)(kw0 + 16 * t + 4 * grp + i);
+                            lists[(rl * NK + kk) * FCAP + pos[kk]] =
+                                ((unsigned long long)ord_key(S[t][i]) << 32) | (0xFFFFFFFFu - j);
+                        }
+                        ++pos[kk];
+                    }
+                }
+            }
+        }
+    }
+    __syncthreads();
+    // sort each (row, budget) list within one wave: 2 entries per lane, bitonic
+    for (int li = w; li < FR * NK; li += FW) {
+        const int r = li / NK, kk = li % NK;
+        const int cnt = cntr[r * 8 + kk];
+        unsigned long long e0 = (lane < cnt) ? lists[li * FCAP + lane] : 0ull;
+        unsigned long long e1 = (lane + 64 < cnt) ? lists[li * FCAP + lane + 64] : 0ull;
+        for (int size = 2; size <= 2 * 64; size <<= 1) {
+            for (int stride = size >> 1; stride > 0; stride >>= 1) {
+                if (stride == 64) {  // partner of element x is x ^ 64: same lane
+                    const unsigned long long hi = e0 > e1 ? e0 : e1, lo = e0 > e1 ? e1 : e0;
+                    e0 = hi;
+                    e1 = lo;
+                } else {
+                    const unsigned long long p0 = __shfl_xor(e0, stride), p1 = __shfl_xor(e1, stride);
+                    const bool upper = (lane & stride) != 0;
+                    const bool d0 = (lane & size) == 0, d1 = ((lane + 64) & size) == 0;
+                    const unsigned long long mx0 = e0 > p0 ? e0 : p0, mn0 = e0 > p0 ? p0 : e0;
+                    const unsigned long long mx1 = e1 > p1 ? e1 : p1, mn1 = e1 > p1 ? p1 : e1;
+                    e0 = (d0 != upper) ? mx0 : mn0;
+                    e1 = (d1 != upper) ? mx1 : mn1;
+                }
+            }
+        }
+        const int need = THR(r, kk, 1);
+        const int x = (need - 1) & 127;
+        const unsigned long long v0 = __shfl(e0, x & 63), v1 = __shfl(e1, x & 63);
+        const unsigned long long sel = (x < 64) ? v0 : v1;
+        if (lane == 0) {
+            THR(r, kk, 0) = (int)(uint32_t)(sel >> 32);
+            THR(r, kk, 1) = (int)(0xFFFFFFFFu - (uint32_t)(sel & 0xFFFFFFFFull));
+            THR(r, kk, 3) = (cnt > FCAP || need < 1 || need > cnt) ? 1 : 0;
+        }
+    }
+    __syncthreads();
+    uint32_t tkey[NK];
+    int tcut[NK];
+    bool bad = degenerate;
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+        tkey[kk] = (uint32_t)THR(rl, kk, 0);
+        tcut[kk] = THR(rl, kk, 1);
+        bad |= THR(rl, kk, 3) != 0;
+    }
+    if (w == 0 && grp == 0) {
+        a.flags[row0 + rl] = bad ? 1 : 0;
+        if (bad) a.flag_list[atomicAdd(a.flag_count, 1)] = (int32_t)(row0 + rl);
+    }
+    if (SEL && !bad) {  // the selected keys of the largest budget: count, reserve, write
+        int c = 0;
+        const float kf = opaque(key_to_float(tkey[NK - 1]));
+        const int kc = opaque(tcut[NK - 1]);
+#pragma unroll
+        for (int t = 0; t < TILES; ++t) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int j = kw0 + 16 * t + 4 * grp + i;
+                c += (int)(S[t][i] > kf) | ((int)(S[t][i] == kf) & (int)(j <= kc));
+            }
+            FW_TILE_FENCE();
+        }
+        int pos = c ? atomicAdd(&cntr[rl * 8 + 7], c) : 0;
+        const float kx = opaque(kf);
+        const int cx = opaque(kc);
+#pragma unroll
+        for (int t = 0; t < TILES; ++t) {
+            FW_TILE_FENCE();
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int j = kw0 + 16 * t + 4 * grp + i;
+                if ((int)(S[t][i] > kx) | ((int)(S[t][i] == kx) & (int)(j <= cx))) {
+                    const uint32_t u = ord_key(S[t][i]);
+                    if (pos < a.kmax)
+                        a.sel[(row0 + rl) * a.kmax + pos] =
+                            ((unsigned long long)u << 32) | (0xFFFFFFFFu - (uint32_t)j);
+                    ++pos;
+                }
+            }
+        }
+    }
+    // tiers (2 bits per logit, 4 tiles per word) and bf16 weights packed in
+    // pairs: from here the lane keeps 3/4 fewer registers for its keys
+    uint32_t TB[(TILES + 3) / 4];
+    uint32_t P2[TILES][2];
+    // thresholds as floats: ord_key order equals float order for finite
+    // logits (both identify -0 with +0), and compares on S itself share no
+    // work with the selection passes above
+    float tf[NK];
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+        tf[kk] = opaque(key_to_float(tkey[kk]));
+        tcut[kk] = opaque(tcut[kk]);
+    }
+    const float m3 = opaque(m), il3 = opaque(inv_l);
+    float mass[NT];
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) mass[tt] = 0.f;
+#pragma unroll
+    for (int t = 0; t < TILES; ++t) {
+        if ((t & 3) == 0) TB[t >> 2] = 0;
+        uint32_t pbits[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int j = kw0 + 16 * t + 4 * grp + i;
+            const float s = S[t][i];
+            // the budgets' sets are nested: the tier is the number of sets
+            // that leave the key out (bitwise predicates keep this branch-free)
+            int tier = NK;
+#pragma unroll
+            for (int kk = 0; kk < NK; ++kk)
+                tier -= (int)(s > tf[kk]) | ((int)(s == tf[kk]) & (int)(j <= tcut[kk]));
+            TB[t >> 2] |= (uint32_t)tier << (8 * (t & 3) + 2 * i);
+            pbits[i] = f2bf_rne(__builtin_amdgcn_exp2f((S[t][i] - m3) * LOG2E) * il3);
+            const float pr = __uint_as_float(pbits[i] << 16);
+#pragma unroll
+            for (int tt = 0; tt < NT; ++tt) mass[tt] += (tier == tt) ? pr : 0.f;
+        }
+        P2[t][0] = pbits[0] | (pbits[1] << 16);
+        P2[t][1] = pbits[2] | (pbits[3] << 16);
+        FW_TILE_FENCE();
+    }
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) mass[tt] = rsum4(mass[tt]);
+    __syncthreads();  // selection buffers are dead from here
+    if (grp == 0) {
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) WRED(tt, w, rl) = mass[tt];
+    }
+
+    // ---- 4./5. tier products per DQ columns of d, then the epilogue -------
+    const rsrc_t vres = make_rsrc(a.v + h * (int64_t)n * FD, (uint32_t)n * FD * 2);
+    const uint32_t vvo = ((uint32_t)(kw0 + lane / VCR) * FD + 8 * (lane % VCR)) * 2;
+    uint16_t *vw = vst + (size_t)w * 2 * 32 * VP;
+    const int cq = rl & 3, cr = rl >> 2;
+    const int er = tid >> 5, ec = (tid & 31) * CPT;  // epilogue: row, CPT columns of the pass
+    const int64_t R = a.H * a.G;
+    for (int pass = 0; pass < NPASS; ++pass) {
+        f32x4 acc[DT][NT];
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int tt = 0; tt < NT; ++tt) acc[dt][tt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+        s16x8 vn[VLQ];
+#pragma unroll
+        for (int qq = 0; qq < VLQ; ++qq)
+            vn[qq] = __builtin_bit_cast(s16x8, bload8(vres, vvo, (uint32_t)(((64 / VCR) * qq * FD + DQ * pass) * 2)));
+#pragma unroll
+        for (int blk = 0; blk < TILES / 2; ++blk) {
+            uint16_t *vb = vw + (blk & 1) * 32 * VP;
+#pragma unroll
+            for (int qq = 0; qq < VLQ; ++qq) {  // the block's 32 V rows x this pass's columns -> LDS
+                const int c = lane + 64 * qq;
+                *(s16x8 *)(vb + (c / VCR) * VP + 8 * (c % VCR)) = vn[qq];
+            }
+            if (blk + 1 < TILES / 2) {
+#pragma unroll
+                for (int qq = 0; qq < VLQ; ++qq)
+                    vn[qq] = __builtin_bit_cast(s16x8, bload8(vres, vvo,
+                        (uint32_t)(((32 * (blk + 1) + (64 / VCR) * qq) * FD + DQ * pass) * 2)));
+            }
+            // the staged rows belong to this wave alone and one wave's LDS
+            // operations complete in issue order: no workgroup barrier
+            __builtin_amdgcn_wave_barrier();
+            // P^T operands: slots 0..3 = tile 2 blk, slots 4..7 = tile 2 blk + 1,
+            // zero where the key is in another tier
+            uint32_t pw[NT][4];
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+                const int t = 2 * blk + hf;
+                const uint32_t tb2 = (TB[t >> 2] >> (8 * (t & 3))) & 0xFFu;
+#pragma unroll
+                for (int pr = 0; pr < 2; ++pr) {
+                    const uint32_t t0 = (tb2 >> (4 * pr)) & 3u, t1 = (tb2 >> (4 * pr + 2)) & 3u;
+#pragma unroll
+                    for (int tt = 0; tt < NT; ++tt) {
+                        const uint32_t mask = (t0 == (uint32_t)tt ? 0x0000FFFFu : 0u) | (t1 == (uint32_t)tt ? 0xFFFF0000u : 0u);
+                        pw[tt][2 * hf + pr] = P2[t][pr] & mask;
+                    }
+                }
+            }
+            s16x8 pb[NT];
+#pragma unroll
+            for (int tt = 0; tt < NT; ++tt) {
+                typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+                const u32x4 x = {pw[tt][0], pw[tt][1], pw[tt][2], pw[tt][3]};
+                pb[tt] = __builtin_bit_cast(s16x8, x);
+            }
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_s16x4 *)(vb + (4 * grp + cr) * VP + 16 * dt + 4 * cq));
+                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_s16x4 *)(vb + (16 + 4 * grp + cr) * VP + 16 * dt + 4 * cq));
+                const bf16x8 vbf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+                for (int tt = 0; tt < NT; ++tt)
+                    acc[dt][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        vbf, __builtin_bit_cast(bf16x8, pb[tt]), acc[dt][tt], 0, 0, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        __syncthreads();  // staging buffers are dead; partial sums overlay them
+        // acc[dt][tt][i] = O^T[d = DQ pass + 16 dt + 4 grp + i][row rl] over this wave's keys
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    opart[(((size_t)w * NT + tt) * DQ + 16 * dt + 4 * grp + i) * FR + rl] = acc[dt][tt][i];
+        __syncthreads();
+        {
+            float M[NT];
+            float mtot = 0.f;
+#pragma unroll
+            for (int tt = 0; tt < NT; ++tt) {
+                float s = 0.f;
+#pragma unroll
+                for (int ww = 0; ww < FW; ++ww) s += WRED(tt, ww, er);
+                M[tt] = s;
+                mtot += s;
+            }
+            float T[NT][CPT];
+#pragma unroll
+            for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+                for (int c = 0; c < CPT; ++c) {
+                    float s = 0.f;
+#pragma unroll
+                    for (int ww = 0; ww < FW; ++ww) s += opart[(((size_t)ww * NT + tt) * DQ + ec + c) * FR + er];
+                    T[tt][c] = s;
+                }
+            const int64_t row = row0 + er;
+            const float inv_tot = 1.0f / mtot;
+            const int col = DQ * pass + ec;
+            if (a.o) {
+#pragma unroll
+                for (int c = 0; c < CPT; ++c) {
+                    float s = 0.f;
+#pragma unroll
+                    for (int tt = 0; tt < NT; ++tt) s += T[tt][c];
+                    a.o[row * FD + col + c] = s * inv_tot;
+                }
+            }
+#pragma unroll
+            for (int kk = 0; kk < NK; ++kk) {
+                float km = 0.f, rm = 0.f;
+#pragma unroll
+                for (int tt = 0; tt < NT; ++tt) {
+                    if (tt <= kk) km += M[tt]; else rm += M[tt];
+                }
+                float ss = 0.f;
+#pragma unroll
+                for (int c = 0; c < CPT; ++c) {
+                    float kt = 0.f, rt2 = 0.f;
+#pragma unroll
+                    for (int tt = 0; tt < NT; ++tt) {
+                        if (tt <= kk) kt += T[tt][c]; else rt2 += T[tt][c];
+                    }
+                    const float oS = kt / km;
+                    if (a.o_s) a.o_s[((int64_t)a.ks.perm[kk] * R + row) * FD + col + c] = oS;
+                    if (rm > 0.f) {
+                        const float diff = rt2 / rm - oS;
+                        ss = fmaf(diff, diff, ss);
+                    }
+                }
+#pragma unroll
+                for (int off = 1; off < 32; off <<= 1) ss += __shfl_xor(ss, off);
+                if ((tid & 31) == 0) ssb[(pass * FR + er) * 4 + kk] = ss;
+                if (pass == NPASS - 1 && (tid & 31) == 0) {
+                    float st = ss;
+                    for (int pp = 0; pp < NPASS - 1; ++pp) st += ssb[(pp * FR + er) * 4 + kk];
+                    a.gap[(int64_t)a.ks.perm[kk] * R + row] = (rm > 0.f) ? (rm * inv_tot) * sqrtf(st) : 0.f;
+                    a.dropped[(int64_t)a.ks.perm[kk] * R + row] = rm * inv_tot;
+                }
+            }
+        }
+        __syncthreads();
+    }
+#undef WRED
+#undef THR
+}
+
+// ---------------------------------------------------------------------------
+// rank-ordered indices: sort each row's selected keys (descending)
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256)
+fused_sort_kernel(const unsigned long long *sel, const int32_t *flags, int kmax, int sort_len,
+                  int32_t *topk_idx) {
+    extern __shared__ unsigned long long sb[];
+    const int64_t r = blockIdx.x;
+    if (flags[r]) return;
+    const int tid = threadIdx.x;
+    for (int i = tid; i < sort_len; i += 256) sb[i] = (i < kmax) ? sel[r * kmax + i] : 0ull;
+    __syncthreads();
+    for (int size = 2; size <= sort_len; size <<= 1)
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int i = tid; i < sort_len / 2; i += 256) {
+                const int lo = 2 * stride * (i / stride) + (i % stride), hi = lo + stride;
+                const bool desc = (lo & size) == 0;
+                const unsigned long long x = sb[lo], y = sb[hi];
+                if (desc ? (x < y) : (x > y)) { sb[lo] = y; sb[hi] = x; }
+            }
+            __syncthreads();
+        }
+    for (int i = tid; i < kmax; i += 256)
+        topk_idx[r * kmax + i] = (int32_t)(0xFFFFFFFFu - (uint32_t)(sb[i] & 0xFFFFFFFFull));
+}
+
+__global__ void fused_clear_kernel(int32_t *flag_count) {
+    if (threadIdx.x == 0) *flag_count = 0;
+}
+
+// ---------------------------------------------------------------------------
+// fallback for listed rows: one workgroup per row, exact radix selection
+// ---------------------------------------------------------------------------
+template <int NK>
+__global__ void __launch_bounds__(256)
+fused_fixup_kernel(FusedArgs a, int32_t *topk_idx) {
+    constexpr int NT = NK + 1;
+    __shared__ float z[4096];
+    __shared__ int hist[256];
+    __shared__ int scan[256];
+    __shared__ int sh[4];
+    __shared__ float redf[256];
+    __shared__ float acc_s[NT][FD + 1];
+    __shared__ float mass_s[NT];
+    __shared__ unsigned long long sb[4096];
+    const int tid = threadIdx.x;
+    const int n = a.n;
+    const int count = *a.flag_count;
+    for (int li = blockIdx.x; li < count; li += gridDim.x) {
+        const int64_t r = a.flag_list[li];
+        const int64_t h = r / a.G;
+        const float sc = a.scale ? a.scale[h] : (float)(1.0 / sqrt((double)FD));
+        const uint16_t *qr = a.q + r * FD;
+        const uint16_t *kh = a.k + h * (int64_t)n * FD;
+        const uint16_t *vh = a.v + h * (int64_t)n * FD;
+        for (int j = tid; j < n; j += 256) {
+            float s = 0.f;
+            for (int c = 0; c < FD; ++c)
+                s = fmaf(bf16_bits_to_f32(qr[c]), bf16_bits_to_f32(kh[(int64_t)j * FD + c]), s);
+            z[j] = sc * s + (a.bias ? a.bias[j] : 0.f);
+        }
+        __syncthreads();
+        float m = -INFINITY;
+        for (int j = tid; j < n; j += 256) m = fmaxf(m, z[j]);
+        m = block_reduce(m, redf, OpMax());
+        float l = 0.f;
+        for (int j = tid; j < n; j += 256) l += expf(z[j] - m);
+        l = block_reduce(l, redf, OpSum());
+        uint32_t key[NK];
+        int64_t cut[NK];
+        for (int kk = 0; kk < NK; ++kk) {
+            int rem;
+            radix_select_desc(z, n, a.ks.k[kk], hist, sh, &key[kk], &rem);
+            cut[kk] = nth_tie(z, n, key[kk], rem, scan, sh);
+        }
+        if (tid < FD) {
+            float accl[NT], ml[NT];
+            for (int tt = 0; tt < NT; ++tt) { accl[tt] = 0.f; ml[tt] = 0.f; }
+            for (int j = 0; j < n; ++j) {
+                const uint32_t u = ord_key(z[j]);
+                int tier = NK;
+                for (int kk = NK - 1; kk >= 0; --kk)
+                    if (u > key[kk] || (u == key[kk] && j <= cut[kk])) tier = kk;
+                const float p = expf(z[j] - m) / l;
+                const float vv = bf16_bits_to_f32(vh[(int64_t)j * FD + tid]);
+                for (int tt = 0; tt < NT; ++tt)
+                    if (tt == tier) { accl[tt] = fmaf(p, vv, accl[tt]); ml[tt] += p; }
+            }
+            for (int tt = 0; tt < NT; ++tt) {
+                acc_s[tt][tid] = accl[tt];
+                if (tid == 0) mass_s[tt] = ml[tt];
+            }
+        }
+        __syncthreads();
+        if (tid < 64) {
+            const int64_t R = a.H * a.G;
+            float mtot = 0.f;
+            for (int tt = 0; tt < NT; ++tt) mtot += mass_s[tt];
+            for (int c = tid; c < FD; c += 64) {
+                float s = 0.f;
+                for (int tt = 0; tt < NT; ++tt) s += acc_s[tt][c];
+                if (a.o) a.o[r * FD + c] = s / mtot;
+            }
+            for (int kk = 0; kk < NK; ++kk) {
+                float km = 0.f, rm = 0.f;
+                for (int tt = 0; tt < NT; ++tt) { if (tt <= kk) km += mass_s[tt]; else rm += mass_s[tt]; }
+                float ss = 0.f;
+                for (int c = tid; c < FD; c += 64) {
+                    float kt = 0.f, rt2 = 0.f;
+                    for (int tt = 0; tt < NT; ++tt) { if (tt <= kk) kt += acc_s[tt][c]; else rt2 += acc_s[tt][c]; }
+                    const float oS = kt / km;
+                    if (a.o_s) a.o_s[((int64_t)a.ks.perm[kk] * R + r) * FD + c] = oS;
+                    if (rm > 0.f) { const float df = rt2 / rm - oS; ss = fmaf(df, df, ss); }
+                }
+                for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+                if (tid == 0) {
+                    a.gap[(int64_t)a.ks.perm[kk] * R + r] = (rm > 0.f) ? (rm / mtot) * sqrtf(ss) : 0.f;
+                    a.dropped[(int64_t)a.ks.perm[kk] * R + r] = rm / mtot;
+                }
+            }
+        }
+        if (topk_idx) {
+            int sort_len = 1;
+            while (sort_len < a.kmax) sort_len <<= 1;
+            for (int i = tid; i < sort_len; i += 256) sb[i] = 0ull;
+            __syncthreads();
+            const int64_t chunk = (n + 255) / 256;
+            const int64_t lo = tid * chunk, hi = (lo + chunk < n) ? lo + chunk : n;
+            int c = 0;
+            for (int64_t j = lo; j < hi; ++j) {
+                const uint32_t u = ord_key(z[j]);
+                c += (u > key[NK - 1]) || (u == key[NK - 1] && j <= cut[NK - 1]);
+            }
+            int total;
+            int pos = block_exclusive_scan(c, scan, &total);
+            for (int64_t j = lo; j < hi; ++j) {
+                const uint32_t u = ord_key(z[j]);
+                if ((u > key[NK - 1]) || (u == key[NK - 1] && j <= cut[NK - 1]))
+                    sb[pos++] = ((unsigned long long)u << 32) | (0xFFFFFFFFu - (uint32_t)j);
+            }
+            __syncthreads();
+            for (int size = 2; size <= sort_len; size <<= 1)
+                for (int stride = size >> 1; stride > 0; stride >>= 1) {
+                    for (int i = tid; i < sort_len / 2; i += 256) {
+                        const int lo2 = 2 * stride * (i / stride) + (i % stride), hi2 = lo2 + stride;
+                        const bool desc = (lo2 & size) == 0;
+                        const unsigned long long x = sb[lo2], y = sb[hi2];
+                        if (desc ? (x < y) : (x > y)) { sb[lo2] = y; sb[hi2] = x; }
+                    }
+                    __syncthreads();
+                }
+            for (int i = tid; i < a.kmax; i += 256)
+                topk_idx[r * a.kmax + i] = (int32_t)(0xFFFFFFFFu - (uint32_t)(sb[i] & 0xFFFFFFFFull));
+        }
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
+bool fused_topk_supported(const fw_rows &rows, const KsArg &ks) {
+    return rows.dtype == FW_BF16 && rows.d == FD && (rows.n == 1024 || rows.n == 2048 || rows.n == 4096) &&
+           rows.G % FR == 0 && ks.n >= 1 && ks.n <= 3;
+}
+
+size_t fused_topk_ws_bytes(const fw_rows &rows, int kmax) {
+    const size_t R = (size_t)rows.H * rows.G;
+    return align_up(R * 4, 256) * 2 + 256 + align_up(R * (size_t)kmax * 8, 256);
+}
+
+template <int TILES, int NK>
+static void launch_fused_t(const FusedArgs &a, unsigned blocks, size_t lds, hipStream_t st) {
+    if (a.bias) {
+        if (a.sel) hipLaunchKernelGGL((topk_fused_kernel<TILES, NK, true, true>), dim3(blocks), dim3(FTH), lds, st, a);
+        else hipLaunchKernelGGL((topk_fused_kernel<TILES, NK, true, false>), dim3(blocks), dim3(FTH), lds, st, a);
+    } else {
+        if (a.sel) hipLaunchKernelGGL((topk_fused_kernel<TILES, NK, false, true>), dim3(blocks), dim3(FTH), lds, st, a);
+        else hipLaunchKernelGGL((topk_fused_kernel<TILES, NK, false, false>), dim3(blocks), dim3(FTH), lds, st, a);
+    }
+}
+
+template <int NK>
+static void launch_fused_nk(const FusedArgs &a, unsigned blocks, hipStream_t st) {
+    const size_t lds = fused_lds(NK).total;
+    switch (a.n) {
+        case 1024: launch_fused_t<8, NK>(a, blocks, lds, st); break;
+        case 2048: launch_fused_t<16, NK>(a, blocks, lds, st); break;
+        default: launch_fused_t<32, NK>(a, blocks, lds, st); break;
+    }
+}
+
+hipError_t launch_fused_topk(const fw_rows &rows, const KsArg &ks, float *o, float *o_s, float *gap,
+                             float *dropped, int32_t *topk_idx, void *ws, hipStream_t st) {
+    const size_t R = (size_t)rows.H * rows.G;
+    const int kmax = ks.k[ks.n - 1];
+    char *base = (char *)ws;
+    FusedArgs a{};
+    a.q = (const uint16_t *)rows.q;
+    a.k = (const uint16_t *)rows.k;
+    a.v = (const uint16_t *)rows.v;
+    a.scale = rows.scale;
+    a.bias = rows.bias;
+    a.H = rows.H;
+    a.G = rows.G;
+    a.n = (int)rows.n;
+    a.ks = ks;
+    a.o = o;
+    a.o_s = o_s;
+    a.gap = gap;
+    a.dropped = dropped;
+    a.kmax = kmax;
+    a.flags = (int32_t *)base;
+    a.flag_list = (int32_t *)(base + align_up(R * 4, 256));
+    a.flag_count = (int32_t *)(base + 2 * align_up(R * 4, 256));
+    a.sel = topk_idx ? (unsigned long long *)(base + 2 * align_up(R * 4, 256) + 256) : nullptr;
+    hipLaunchKernelGGL(fused_clear_kernel, dim3(1), dim3(64), 0, st, a.flag_count);
+    const unsigned blocks = (unsigned)(R / FR);
+    switch (ks.n) {
+        case 1: launch_fused_nk<1>(a, blocks, st); break;
+        case 2: launch_fused_nk<2>(a, blocks, st); break;
+        default: launch_fused_nk<3>(a, blocks, st); break;
+    }
+    if (topk_idx) {
+        int sort_len = 1;
+        while (sort_len < kmax) sort_len <<= 1;
+        hipLaunchKernelGGL(fused_sort_kernel, dim3((unsigned)R), dim3(256), (size_t)sort_len * 8, st,
+                           (const unsigned long long *)a.sel, (const int32_t *)a.flags, kmax, sort_len,
+                           topk_idx);
+    }
+    switch (ks.n) {
+        case 1: hipLaunchKernelGGL(fused_fixup_kernel<1>, dim3(64), dim3(256), 0, st, a, topk_idx); break;
+        case 2: hipLaunchKernelGGL(fused_fixup_kernel<2>, dim3(64), dim3(256), 0, st, a, topk_idx); break;
+        default: hipLaunchKernelGGL(fused_fixup_kernel<3>, dim3(64), dim3(256), 0, st, a, topk_idx); break;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace fw
