@@ -30,7 +30,6 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 namespace {
 constexpr int FR = 16;        // rows per workgroup
@@ -53,17 +52,22 @@ __device__ __forceinline__ T opaque(T x) {
     return x;
 }
 
+constexpr int RING = 16384;   // bytes of streaming ring per wave
+constexpr int KD = 4;         // K tiles (16 keys x 128 d, 4 KiB) per ring
+
 struct FusedLds {
-    size_t wred, thr, ssb;            // persistent
+    size_t wred, thr, ssb, bias;      // persistent
     size_t hist, lists, cntr;         // selection
-    size_t vst;                       // V staging
+    size_t ring;                      // K tiles (phase 1), V blocks (tier products)
     size_t opart;                     // partial tier sums
     size_t total;
 };
 
-__host__ __device__ constexpr int fused_dq(int nk) { return nk >= 2 ? 32 : 64; }
+// columns of d per pass of the tier products: 64 columns are 128 bytes of a
+// V row, a whole cache line per row for the block loads
+__host__ __device__ constexpr int fused_dq(int) { return 64; }
 
-__host__ __device__ inline FusedLds fused_lds(int nk) {
+__host__ __device__ inline FusedLds fused_lds(int nk, int n) {
     const int dq = fused_dq(nk);
     FusedLds L{};
     size_t o = 0;
@@ -71,16 +75,17 @@ __host__ __device__ inline FusedLds fused_lds(int nk) {
     L.wred = take((size_t)4 * FW * FR * 4);    // [quantity][wave][row]
     L.thr = take((size_t)FR * 4 * 4 * 4);      // [row][budget][4 ints]
     L.ssb = take((size_t)(FD / dq) * FR * 4 * 4);  // [pass][row][budget] squared norms
+    L.bias = take((size_t)n * 4);              // each wave's slice of the bias
     const size_t base = o;
     L.hist = base;
     L.lists = align_up(base + (size_t)FR * FBINS * 4, 16);
     L.cntr = align_up(L.lists + (size_t)FR * nk * FCAP * 8, 16);
     const size_t sel_end = L.cntr + (size_t)FR * 8 * 4;
-    L.vst = base;
-    const size_t v_end = base + (size_t)FW * 2 * 32 * (dq + 8) * 2;
+    L.ring = base;
+    const size_t r_end = base + (size_t)FW * RING;
     L.opart = base;
-    const size_t o_end = base + (size_t)FW * (nk + 1) * dq * FR * 4;
-    size_t end = sel_end > v_end ? sel_end : v_end;
+    const size_t o_end = base + (size_t)FW * (nk + 1) * FR * (dq + 4) * 4;
+    size_t end = sel_end > r_end ? sel_end : r_end;
     end = end > o_end ? end : o_end;
     L.total = align_up(end, 16);
     return L;
@@ -115,6 +120,31 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes) {
 __device__ __forceinline__ bf16x8 bload8(rsrc_t r, uint32_t voff, uint32_t soff) {
     return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
+// Direct-to-LDS loads: lane l's 16 (or 4) bytes land at lds + 16 l (4 l); no
+// register is involved, so a wave can keep several tiles in flight.  The
+// compiler does not order these writes against later LDS reads: every
+// consumer waits explicitly (wait_vm) for the loads it needs.
+#define FW_LDS(p) ((__attribute__((address_space(3))) void *)(p))
+__device__ __forceinline__ void dma16(rsrc_t r, void *lds, uint32_t voff, uint32_t soff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, FW_LDS(lds), 16, voff, soff, 0, 0);
+}
+__device__ __forceinline__ void dma4(rsrc_t r, void *lds, uint32_t voff, uint32_t soff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, FW_LDS(lds), 4, voff, soff, 0, 0);
+}
+// wait until at most n vector memory operations of this wave are outstanding
+// (loads complete in issue order); n folds to a constant in unrolled loops
+#define FW_VM(k) case k: asm volatile("s_waitcnt vmcnt(" #k ")" ::: "memory"); break;
+__device__ __forceinline__ void wait_vm(int n) {
+    switch (n) {
+        FW_VM(0) FW_VM(1) FW_VM(2) FW_VM(3) FW_VM(4) FW_VM(5) FW_VM(6) FW_VM(7)
+        FW_VM(8) FW_VM(9) FW_VM(10) FW_VM(11) FW_VM(12) FW_VM(13) FW_VM(14) FW_VM(15)
+        FW_VM(16) FW_VM(17) FW_VM(18) FW_VM(19) FW_VM(20) FW_VM(21) FW_VM(22) FW_VM(23)
+        FW_VM(24) FW_VM(25) FW_VM(26) FW_VM(27) FW_VM(28)
+        default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    }
+}
+#undef FW_VM
+__device__ __forceinline__ void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 }  // namespace
 
 struct FusedArgs {
@@ -133,20 +163,18 @@ struct FusedArgs {
 template <int TILES, int NK, bool BIAS, bool SEL>
 __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
     constexpr int NT = NK + 1;
-    // columns of d per pass of the tier products: fewer with more tiers, so
-    // that the NT x DQ/16 accumulator tiles stay within the register budget
     constexpr int DQ = fused_dq(NK);
     constexpr int NPASS = FD / DQ, DT = DQ / 16, CPT = DQ / 32;
-    constexpr int VCR = DQ / 8, VLQ = DQ / 16, VP = DQ + 8;  // V staging: chunks/row, loads/lane, pitch
+    constexpr int VCR = DQ / 8, VLQ = DQ / 16;  // V block: 16-byte chunks per row, loads per block
+    constexpr int VD = RING / (32 * DQ * 2);      // V blocks per ring
     extern __shared__ __align__(16) unsigned char smem[];
-    const FusedLds L = fused_lds(NK);
+    const FusedLds L = fused_lds(NK, 128 * TILES);
     float *wred = (float *)(smem + L.wred);
     int *thr = (int *)(smem + L.thr);
     float *ssb = (float *)(smem + L.ssb);
     int *hist = (int *)(smem + L.hist);
     unsigned long long *lists = (unsigned long long *)(smem + L.lists);
     int *cntr = (int *)(smem + L.cntr);
-    uint16_t *vst = (uint16_t *)(smem + L.vst);
     float *opart = (float *)(smem + L.opart);
 #define WRED(qq, ww, rr) wred[((qq) * FW + (ww)) * FR + (rr)]
 #define THR(rr, kk, ff) thr[((rr) * 4 + (kk)) * 4 + (ff)]
@@ -174,33 +202,56 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
     const int kw0 = w * 16 * TILES;  // this wave's first key
 
     // ---- 1. logits --------------------------------------------------------
+    // K streams through this wave's ring, KD - 1 tiles ahead of the MFMAs.
+    // A tile (16 keys x 128 d) is 4 loads of 4 whole key rows each (1 KiB
+    // contiguous per load: few cache lines per instruction).  In LDS the
+    // 16-byte chunk c of key row r sits at chunk position c ^ r of the row, so
+    // that the MFMA operand reads (16 rows, same chunk) hit distinct banks.
     float S[TILES][4];
+    unsigned char *kring = smem + L.ring + (size_t)w * RING;
+    const float *bsl = (const float *)(smem + L.bias) + kw0;
     {
         bf16x8 qb[4];
         const uint16_t *qr = a.q + (row0 + rl) * FD + 8 * grp;
 #pragma unroll
         for (int s = 0; s < 4; ++s) qb[s] = *(const bf16x8 *)(qr + 32 * s);
-        const rsrc_t kres = make_rsrc(a.k + h * (int64_t)n * FD, (uint32_t)n * FD * 2);
-        const uint32_t kvo = ((uint32_t)(kw0 + rl) * FD + 8 * grp) * 2;
-        const rsrc_t bres = make_rsrc(BIAS ? (const void *)a.bias : (const void *)a.k, BIAS ? (uint32_t)n * 4 : 0u);
-        const uint32_t bvo = (uint32_t)(kw0 + 4 * grp) * 4;
-        bf16x8 kn[4];
+        if (BIAS) {  // this wave's bias slice, 256 bytes per load
+            const rsrc_t bres = make_rsrc(a.bias, (uint32_t)n * 4);
 #pragma unroll
-        for (int s = 0; s < 4; ++s) kn[s] = bload8(kres, kvo, 64 * s);
+            for (int c = 0; c < TILES / 4; ++c)
+                dma4(bres, (void *)(bsl + 64 * c), (uint32_t)(kw0 + lane) * 4, (uint32_t)(256 * c));
+        }
+        const rsrc_t kres = make_rsrc(a.k + h * (int64_t)n * FD, (uint32_t)n * FD * 2);
+        // load s, lane l: key row r = 4 s + l / 16, chunk position l % 16,
+        // which holds chunk (l % 16) ^ r of that row
+        uint32_t kvo[4], kro[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            const int r = 4 * s + (lane >> 4);
+            kvo[s] = ((uint32_t)(kw0 + r) * FD + 8 * ((lane & 15) ^ r)) * 2;
+            // MFMA step s, lane l: key row rl, chunk 4 s + grp
+            kro[s] = (uint32_t)(rl * 256 + (((4 * s + grp) ^ rl) * 16));
+        }
+        auto issue = [&](int t) {
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+                dma16(kres, kring + (t % KD) * 4096 + s * 1024, kvo[s], (uint32_t)(t * 16 * FD * 2));
+        };
+#pragma unroll
+        for (int t = 0; t < KD - 1 && t < TILES; ++t) issue(t);
 #pragma unroll
         for (int t = 0; t < TILES; ++t) {
-            bf16x8 kc[4];
-#pragma unroll
-            for (int s = 0; s < 4; ++s) kc[s] = kn[s];
-            if (t + 1 < TILES) {
-#pragma unroll
-                for (int s = 0; s < 4; ++s) kn[s] = bload8(kres, kvo, (uint32_t)(16 * (t + 1) * FD * 2 + 64 * s));
-            }
+            wait_lds();  // the slot refilled next was read one tile ago
+            if (t + KD - 1 < TILES) issue(t + KD - 1);
+            const int after = (TILES - 1 - t < KD - 1) ? TILES - 1 - t : KD - 1;
+            wait_vm(4 * after);
+            const unsigned char *kt = kring + (t % KD) * 4096;
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc[s], qb[s], acc, 0, 0, 0);
+            for (int s = 0; s < 4; ++s)
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8 *)(kt + kro[s]), qb[s], acc, 0, 0, 0);
             if (BIAS) {
-                const f32x4 bj = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(bres, bvo, 64 * t, 0));
+                const f32x4 bj = *(const f32x4 *)(bsl + 16 * t + 4 * grp);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) S[t][i] = sc * acc[i] + bj[i];
             } else {
@@ -304,75 +355,80 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
     }
     __syncthreads();
     {
-        // logits in the threshold bin of each budget: count, reserve, write
-        int tb[NK], cnt[NK], pos[NK];
+        // logits in the threshold bin of some budget (a few per row): one
+        // branch per logit, one LDS atomic per appended key
+        int tb[NK];
 #pragma unroll
-        for (int kk = 0; kk < NK; ++kk) {
-            tb[kk] = THR(rl, kk, 0);
-            cnt[kk] = 0;
-        }
+        for (int kk = 0; kk < NK; ++kk) tb[kk] = THR(rl, kk, 0);
         const float m1 = opaque(m), w1 = opaque(inv_w);
 #pragma unroll
         for (int t = 0; t < TILES; ++t) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int bin = min(FBINS - 1, (int)((m1 - S[t][i]) * w1));
+                int hit = 0;
 #pragma unroll
-                for (int kk = 0; kk < NK; ++kk) cnt[kk] += (bin == tb[kk]) ? 1 : 0;
-            }
-            FW_TILE_FENCE();
-        }
+                for (int kk = 0; kk < NK; ++kk) hit |= (int)(bin == tb[kk]);
+                if (hit) {
+                    const uint32_t j = (uint32_t)(kw0 + 16 * t + 4 * grp + i);
+                    const unsigned long long e = ((unsigned long long)ord_key(S[t][i]) << 32) | (0xFFFFFFFFu - j);
 #pragma unroll
-        for (int kk = 0; kk < NK; ++kk) pos[kk] = cnt[kk] ? atomicAdd(&cntr[rl * 8 + kk], cnt[kk]) : 0;
-        const float m2 = opaque(m1), w2 = opaque(w1);
-#pragma unroll
-        for (int t = 0; t < TILES; ++t) {
-            FW_TILE_FENCE();
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int bin = min(FBINS - 1, (int)((m2 - S[t][i]) * w2));
-#pragma unroll
-                for (int kk = 0; kk < NK; ++kk) {
-                    if (bin == tb[kk]) {
-                        if (pos[kk] < FCAP) {
-                            const uint32_t j = (uint32_t)(kw0 + 16 * t + 4 * grp + i);
-                            lists[(rl * NK + kk) * FCAP + pos[kk]] =
-                                ((unsigned long long)ord_key(S[t][i]) << 32) | (0xFFFFFFFFu - j);
+                    for (int kk = 0; kk < NK; ++kk)
+                        if (bin == tb[kk]) {
+                            const int p = atomicAdd(&cntr[rl * 8 + kk], 1);
+                            if (p < FCAP) lists[(rl * NK + kk) * FCAP + p] = e;
                         }
-                        ++pos[kk];
-                    }
                 }
             }
+            FW_TILE_FENCE();
         }
     }
     __syncthreads();
-    // sort each (row, budget) list within one wave: 2 entries per lane, bitonic
+    // the need-th largest entry of each (row, budget) list, within one wave:
+    // rank by counting for lists of up to 64 entries, else a bitonic sort of
+    // two entries per lane (entries are distinct: the low word is the index)
     for (int li = w; li < FR * NK; li += FW) {
         const int r = li / NK, kk = li % NK;
         const int cnt = cntr[r * 8 + kk];
-        unsigned long long e0 = (lane < cnt) ? lists[li * FCAP + lane] : 0ull;
-        unsigned long long e1 = (lane + 64 < cnt) ? lists[li * FCAP + lane + 64] : 0ull;
-        for (int size = 2; size <= 2 * 64; size <<= 1) {
-            for (int stride = size >> 1; stride > 0; stride >>= 1) {
-                if (stride == 64) {  // partner of element x is x ^ 64: same lane
-                    const unsigned long long hi = e0 > e1 ? e0 : e1, lo = e0 > e1 ? e1 : e0;
-                    e0 = hi;
-                    e1 = lo;
-                } else {
-                    const unsigned long long p0 = __shfl_xor(e0, stride), p1 = __shfl_xor(e1, stride);
-                    const bool upper = (lane & stride) != 0;
-                    const bool d0 = (lane & size) == 0, d1 = ((lane + 64) & size) == 0;
-                    const unsigned long long mx0 = e0 > p0 ? e0 : p0, mn0 = e0 > p0 ? p0 : e0;
-                    const unsigned long long mx1 = e1 > p1 ? e1 : p1, mn1 = e1 > p1 ? p1 : e1;
-                    e0 = (d0 != upper) ? mx0 : mn0;
-                    e1 = (d1 != upper) ? mx1 : mn1;
+        const int need = THR(r, kk, 1);
+        unsigned long long sel = 0ull;
+        if (cnt <= 64) {
+            const unsigned long long e = (lane < cnt) ? lists[li * FCAP + lane] : 0ull;
+            int rank = 0;
+            for (int jj = 0; jj < cnt; ++jj) {
+                const unsigned long long o =
+                    ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(e >> 32), jj) << 32) |
+                    (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)e, jj);
+                rank += (int)(o > e);
+            }
+            const unsigned long long bal = __ballot(lane < cnt && rank == need - 1);
+            const int f = bal ? __ffsll(bal) - 1 : 0;
+            sel = ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(e >> 32), f) << 32) |
+                  (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)e, f);
+        } else {
+            unsigned long long e0 = (lane < cnt) ? lists[li * FCAP + lane] : 0ull;
+            unsigned long long e1 = (lane + 64 < cnt) ? lists[li * FCAP + lane + 64] : 0ull;
+            for (int size = 2; size <= 2 * 64; size <<= 1) {
+                for (int stride = size >> 1; stride > 0; stride >>= 1) {
+                    if (stride == 64) {  // partner of element x is x ^ 64: same lane
+                        const unsigned long long hi = e0 > e1 ? e0 : e1, lo = e0 > e1 ? e1 : e0;
+                        e0 = hi;
+                        e1 = lo;
+                    } else {
+                        const unsigned long long p0 = __shfl_xor(e0, stride), p1 = __shfl_xor(e1, stride);
+                        const bool upper = (lane & stride) != 0;
+                        const bool d0 = (lane & size) == 0, d1 = ((lane + 64) & size) == 0;
+                        const unsigned long long mx0 = e0 > p0 ? e0 : p0, mn0 = e0 > p0 ? p0 : e0;
+                        const unsigned long long mx1 = e1 > p1 ? e1 : p1, mn1 = e1 > p1 ? p1 : e1;
+                        e0 = (d0 != upper) ? mx0 : mn0;
+                        e1 = (d1 != upper) ? mx1 : mn1;
+                    }
                 }
             }
+            const int x = (need - 1) & 127;
+            const unsigned long long v0 = __shfl(e0, x & 63), v1 = __shfl(e1, x & 63);
+            sel = (x < 64) ? v0 : v1;
         }
-        const int need = THR(r, kk, 1);
-        const int x = (need - 1) & 127;
-        const unsigned long long v0 = __shfl(e0, x & 63), v1 = __shfl(e1, x & 63);
-        const unsigned long long sel = (x < 64) ? v0 : v1;
         if (lane == 0) {
             THR(r, kk, 0) = (int)(uint32_t)(sel >> 32);
             THR(r, kk, 1) = (int)(0xFFFFFFFFu - (uint32_t)(sel & 0xFFFFFFFFull));
@@ -476,45 +532,57 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
 
     // ---- 4./5. tier products per DQ columns of d, then the epilogue -------
     const rsrc_t vres = make_rsrc(a.v + h * (int64_t)n * FD, (uint32_t)n * FD * 2);
-    const uint32_t vvo = ((uint32_t)(kw0 + lane / VCR) * FD + 8 * (lane % VCR)) * 2;
-    uint16_t *vw = vst + (size_t)w * 2 * 32 * VP;
+    static_assert(VCR == 8, "V block rows are 8 chunks of 16 bytes");
+    // load qq of a block, lane l: row 8 qq + l / 8, chunk position l % 8, which
+    // holds chunk (l % 8) ^ (row % 8) of the row (conflict-free transposed reads)
+    const uint32_t vvo = ((uint32_t)(kw0 + (lane >> 3)) * FD + 8 * ((lane & 7) ^ (lane >> 3))) * 2;
+    unsigned char *vring = smem + L.ring + (size_t)w * RING;
+    static_assert(DT == 4, "four 16-column tiles per pass");
     const int cq = rl & 3, cr = rl >> 2;
+    // LDS byte address of this wave's ring, and the lane's transposed-read
+    // offsets: row 4 grp + cr (= 4 (grp & 1) + cr mod 8), columns 16 dt + 4 cq
+    // .. + 4, i.e. chunk 2 dt + cq / 2 at position chunk ^ (row mod 8)
+    const uint32_t vra = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char *)vring;
+    uint32_t vrd[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+        vrd[dt] = (uint32_t)(((4 * grp + cr) * DQ + ((2 * dt + (cq >> 1)) ^ (4 * (grp & 1) + cr)) * 8 + 4 * (cq & 1)) * 2);
     const int er = tid >> 5, ec = (tid & 31) * CPT;  // epilogue: row, CPT columns of the pass
     const int64_t R = a.H * a.G;
     for (int pass = 0; pass < NPASS; ++pass) {
+        // the tier operands below do not depend on the pass; an opaque zero
+        // keeps them from being hoisted out of this loop for every block
+        // at once (256 values), which would spill
+        const uint32_t pz = opaque(0u);
         f32x4 acc[DT][NT];
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
             for (int tt = 0; tt < NT; ++tt) acc[dt][tt] = (f32x4){0.f, 0.f, 0.f, 0.f};
-        s16x8 vn[VLQ];
+        // V block b (32 keys x DQ columns, 2 DQ bytes per key, swizzled) in
+        // ring slot b % VD, VD - 1 blocks ahead of the MFMAs
+        constexpr int NB = TILES / 2;
+        auto issue = [&](int b) {
 #pragma unroll
-        for (int qq = 0; qq < VLQ; ++qq)
-            vn[qq] = __builtin_bit_cast(s16x8, bload8(vres, vvo, (uint32_t)(((64 / VCR) * qq * FD + DQ * pass) * 2)));
+            for (int qq = 0; qq < VLQ; ++qq)
+                dma16(vres, vring + (b % VD) * (32 * DQ * 2) + qq * 1024, vvo,
+                      (uint32_t)(((32 * b + (64 / VCR) * qq) * FD + DQ * pass) * 2));
+        };
 #pragma unroll
-        for (int blk = 0; blk < TILES / 2; ++blk) {
-            uint16_t *vb = vw + (blk & 1) * 32 * VP;
+        for (int b = 0; b < VD - 1 && b < NB; ++b) issue(b);
 #pragma unroll
-            for (int qq = 0; qq < VLQ; ++qq) {  // the block's 32 V rows x this pass's columns -> LDS
-                const int c = lane + 64 * qq;
-                *(s16x8 *)(vb + (c / VCR) * VP + 8 * (c % VCR)) = vn[qq];
-            }
-            if (blk + 1 < TILES / 2) {
-#pragma unroll
-                for (int qq = 0; qq < VLQ; ++qq)
-                    vn[qq] = __builtin_bit_cast(s16x8, bload8(vres, vvo,
-                        (uint32_t)(((32 * (blk + 1) + (64 / VCR) * qq) * FD + DQ * pass) * 2)));
-            }
-            // the staged rows belong to this wave alone and one wave's LDS
-            // operations complete in issue order: no workgroup barrier
-            __builtin_amdgcn_wave_barrier();
+        for (int blk = 0; blk < NB; ++blk) {
+            wait_lds();  // the slot refilled next was read one block ago
+            if (blk + VD - 1 < NB) issue(blk + VD - 1);
+            const int after = (NB - 1 - blk < VD - 1) ? NB - 1 - blk : VD - 1;
+            wait_vm(VLQ * after);
             // P^T operands: slots 0..3 = tile 2 blk, slots 4..7 = tile 2 blk + 1,
             // zero where the key is in another tier
             uint32_t pw[NT][4];
 #pragma unroll
             for (int hf = 0; hf < 2; ++hf) {
                 const int t = 2 * blk + hf;
-                const uint32_t tb2 = (TB[t >> 2] >> (8 * (t & 3))) & 0xFFu;
+                const uint32_t tb2 = ((TB[t >> 2] ^ pz) >> (8 * (t & 3))) & 0xFFu;
 #pragma unroll
                 for (int pr = 0; pr < 2; ++pr) {
                     const uint32_t t0 = (tb2 >> (4 * pr)) & 3u, t1 = (tb2 >> (4 * pr + 2)) & 3u;
@@ -532,13 +600,31 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
                 const u32x4 x = {pw[tt][0], pw[tt][1], pw[tt][2], pw[tt][3]};
                 pb[tt] = __builtin_bit_cast(s16x8, x);
             }
+            // V^T operands: transposed reads of rows 4 grp + cr (keys 0..15 of
+            // the block) and 16 + 4 grp + cr (2048 bytes on), all eight in one
+            // statement that also waits for them; the compiler would otherwise
+            // drain every outstanding ring load before each transposed read
+            s16x4 vt[DT][2];
+            {
+                const uint32_t slot = vra + (uint32_t)((blk % VD) * (32 * DQ * 2));
+                asm volatile(
+                    "ds_read_b64_tr_b16 %0, %8\n"
+                    "ds_read_b64_tr_b16 %1, %8 offset:2048\n"
+                    "ds_read_b64_tr_b16 %2, %9\n"
+                    "ds_read_b64_tr_b16 %3, %9 offset:2048\n"
+                    "ds_read_b64_tr_b16 %4, %10\n"
+                    "ds_read_b64_tr_b16 %5, %10 offset:2048\n"
+                    "ds_read_b64_tr_b16 %6, %11\n"
+                    "ds_read_b64_tr_b16 %7, %11 offset:2048\n"
+                    "s_waitcnt lgkmcnt(0)"
+                    : "=&v"(vt[0][0]), "=&v"(vt[0][1]), "=&v"(vt[1][0]), "=&v"(vt[1][1]),
+                      "=&v"(vt[2][0]), "=&v"(vt[2][1]), "=&v"(vt[3][0]), "=&v"(vt[3][1])
+                    : "v"(slot + vrd[0]), "v"(slot + vrd[1]), "v"(slot + vrd[2]), "v"(slot + vrd[3])
+                    : "memory");
+            }
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) {
-                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (lds_s16x4 *)(vb + (4 * grp + cr) * VP + 16 * dt + 4 * cq));
-                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (lds_s16x4 *)(vb + (16 + 4 * grp + cr) * VP + 16 * dt + 4 * cq));
-                const bf16x8 vbf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+                const bf16x8 vbf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(vt[dt][0], vt[dt][1], 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
                 for (int tt = 0; tt < NT; ++tt)
                     acc[dt][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
@@ -546,15 +632,16 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        __syncthreads();  // staging buffers are dead; partial sums overlay them
-        // acc[dt][tt][i] = O^T[d = DQ pass + 16 dt + 4 grp + i][row rl] over this wave's keys
+        __syncthreads();  // the rings are dead; partial sums overlay them
+        // acc[dt][tt][i] = O^T[d = DQ pass + 16 dt + 4 grp + i][row rl] over this
+        // wave's keys; stored [wave][tier][row][column], rows DQ + 4 floats
+        // apart, so that the epilogue's column reads are contiguous
+        constexpr int OP = DQ + 4;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
             for (int tt = 0; tt < NT; ++tt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    opart[(((size_t)w * NT + tt) * DQ + 16 * dt + 4 * grp + i) * FR + rl] = acc[dt][tt][i];
+                *(f32x4 *)&opart[(((size_t)w * NT + tt) * FR + rl) * OP + 16 * dt + 4 * grp] = acc[dt][tt];
         __syncthreads();
         {
             float M[NT];
@@ -574,7 +661,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
                 for (int c = 0; c < CPT; ++c) {
                     float s = 0.f;
 #pragma unroll
-                    for (int ww = 0; ww < FW; ++ww) s += opart[(((size_t)ww * NT + tt) * DQ + ec + c) * FR + er];
+                    for (int ww = 0; ww < FW; ++ww) s += opart[(((size_t)ww * NT + tt) * FR + er) * OP + ec + c];
                     T[tt][c] = s;
                 }
             const int64_t row = row0 + er;
@@ -810,7 +897,7 @@ static void launch_fused_t(const FusedArgs &a, unsigned blocks, size_t lds, hipS
 
 template <int NK>
 static void launch_fused_nk(const FusedArgs &a, unsigned blocks, hipStream_t st) {
-    const size_t lds = fused_lds(NK).total;
+    const size_t lds = fused_lds(NK, a.n).total;
     switch (a.n) {
         case 1024: launch_fused_t<8, NK>(a, blocks, lds, st); break;
         case 2048: launch_fused_t<16, NK>(a, blocks, lds, st); break;
