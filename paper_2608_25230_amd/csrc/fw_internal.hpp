@@ -47,6 +47,11 @@ size_t curve_ws_bytes(const fw_rows &rows);
 hipError_t launch_curve(const fw_rows &rows, float *importance, float *curve, int32_t *order,
                         void *ws, hipStream_t st);
 
+// k_window.hip -- window importance on MFMA (bf16, d = 128, 16..64 rows)
+bool window_mfma_supported(const fw_rows &rows);
+void launch_window_mfma(const fw_rows &rows, float *part_m, float *part_l, float *row_m, float *row_il,
+                        float *importance, hipStream_t st);
+
 // k_compact.hip -- global allocation and ragged compaction
 size_t compact_ws_bytes(int64_t H, int64_t n);
 hipError_t launch_compact(int dtype, const void *k, const void *v, int64_t H, int64_t hpl,

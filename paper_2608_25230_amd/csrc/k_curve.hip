@@ -267,12 +267,17 @@ static hipError_t curve_impl(const fw_rows &rows, float *importance, float *curv
     const int nch = (int)((n + kChunk - 1) / kChunk);
     const dim3 grid((unsigned)(H * nch));
     const T *q = (const T *)rows.q, *k = (const T *)rows.k;
-    hipLaunchKernelGGL((window_logits_kernel<T, 0>), grid, dim3(256), 0, st, q, k, rows.scale,
-                       rows.bias, G, n, d, nch, L.part_m, L.part_s, nullptr, nullptr, nullptr);
-    hipLaunchKernelGGL(window_combine_kernel, dim3((unsigned)((H * G + 255) / 256)), dim3(256), 0, st,
-                       H * G, nch, L.part_m, L.part_s, L.row_m, L.row_il);
-    hipLaunchKernelGGL((window_logits_kernel<T, 1>), grid, dim3(256), 0, st, q, k, rows.scale,
-                       rows.bias, G, n, d, nch, nullptr, nullptr, L.row_m, L.row_il, importance);
+    if (window_mfma_supported(rows)) {
+        // bf16, d = 128, up to 64 window rows: MFMA scores (k_window.hip)
+        launch_window_mfma(rows, L.part_m, L.part_s, L.row_m, L.row_il, importance, st);
+    } else {
+        hipLaunchKernelGGL((window_logits_kernel<T, 0>), grid, dim3(256), 0, st, q, k, rows.scale,
+                           rows.bias, G, n, d, nch, L.part_m, L.part_s, nullptr, nullptr, nullptr);
+        hipLaunchKernelGGL(window_combine_kernel, dim3((unsigned)((H * G + 255) / 256)), dim3(256), 0, st,
+                           H * G, nch, L.part_m, L.part_s, L.row_m, L.row_il);
+        hipLaunchKernelGGL((window_logits_kernel<T, 1>), grid, dim3(256), 0, st, q, k, rows.scale,
+                           rows.bias, G, n, d, nch, nullptr, nullptr, L.row_m, L.row_il, importance);
+    }
     hipLaunchKernelGGL(unit_sort_kernel, dim3((unsigned)H), dim3(kSortThreads), 0, st, importance, n,
                        L.ka, L.kb, L.va, L.vb);
     hipLaunchKernelGGL(unit_curve_kernel, dim3((unsigned)H), dim3(kSortThreads), 0, st, importance, n,

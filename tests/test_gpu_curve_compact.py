@@ -60,6 +60,28 @@ def test_curve_small_shapes(torch_fw):
         assert np.all(np.diff(out["curve"], axis=1) <= 0)
 
 
+@pytest.mark.parametrize("shape", [
+    dict(H=3, G=64, n=5000, bias=False),   # ragged last chunk
+    dict(H=2, G=16, n=4096, bias=True),
+    dict(H=2, G=32, n=777, bias=True),
+    dict(H=1, G=48, n=9000, bias=False),
+])
+def test_curve_window_mfma_shapes(torch_fw, shape):
+    """bf16, d = 128, 16..64 window rows: the MFMA importance path."""
+    torch, fw = torch_fw
+    H, G, n = shape["H"], shape["G"], shape["n"]
+    rows = W.window_rows(56, n + G, H, G, n, 128, "bf16")
+    if shape["bias"]:
+        rng = np.random.default_rng(n)
+        bias = (rng.standard_normal(n) * 2.0).astype(np.float32)
+        bias[0] = 4.0
+        rows = W.Rows(rows.dtype, rows.q, rows.k, rows.v, rows.scale, bias)
+    dev, out = _curve(torch, fw, rows)
+    _check_curve(rows, out, range(H))
+    assert np.allclose(out["curve"][:, 0], 1.0, atol=1e-4)
+    assert np.all(out["curve"][:, n] == 0.0)
+
+
 def _compact(torch, fw, k, v, imp, budget, floor, hpl):
     out = fw.ragged_compact(k, v, imp, budget, floor, hpl)
     torch.cuda.synchronize()
