@@ -116,6 +116,8 @@ fw_status check_best_subset(const fw_rows *rows, int32_t k) {
     if (rows->n > 64) return fail(FW_E_UNSUPPORTED, "exhaustive enumeration needs n <= 64 (n=%lld)", (long long)rows->n);
     if (fw::binom((int)rows->n, k) >= (1ull << 31))
         return fail(FW_E_UNSUPPORTED, "C(n=%lld, k=%d) must be < 2^31", (long long)rows->n, k);
+    if (!fw::best_subset_plannable(rows->n, k))
+        return fail(FW_E_UNSUPPORTED, "no enumeration plan fits for n=%lld, k=%d", (long long)rows->n, k);
     return FW_OK;
 }
 

@@ -33,6 +33,7 @@ hipError_t launch_fused_topk(const fw_rows &rows, const KsArg &ks, float *o, flo
 
 // k_subset.hip -- exhaustive best subset (float64)
 size_t best_subset_ws_bytes(int64_t n, int k);
+bool best_subset_plannable(int64_t n, int k);
 hipError_t launch_best_subset(const fw_rows &rows, int k, int32_t *best_idx, float *best_gap,
                               float *topk_gap, float *closed, float *dropped_topk,
                               int32_t *topk_idx, void *ws, hipStream_t st);
