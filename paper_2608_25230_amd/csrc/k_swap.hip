@@ -129,6 +129,7 @@ struct SwapState {
     int32_t *st;     // [R][2]   active, swaps
     float *pv;       // [R][nblk] partial best values
     int64_t *pp;     // [R][nblk] partial best pair index i*n + j
+    float4 *jd;      // [R][n]   per key: (B_j or +inf if kept, p_j, 2 w_j, P + p_j)
     int nblk;
 };
 
@@ -231,10 +232,17 @@ swap_dots_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, SwapState
         mg += mu[c] * g[c];
     }
     mg = block_reduce(mg, redd, OpSum());
+    const float P = (float)s.sc[r * 4 + 0];
     for (int64_t j = (int64_t)blockIdx.x * blockDim.x + tid; j < n; j += (int64_t)gridDim.x * blockDim.x) {
         float acc = 0.f;
         for (int c = 0; c < d; ++c) acc = fmaf(Elem<T>::load(vh, j * d + c), gs[c], acc);
-        s.a[r * n + j] = s.p[r * n + j] * (float)((double)acc - mg);
+        const float pj = s.p[r * n + j];
+        const float aj = pj * (float)((double)acc - mg);
+        s.a[r * n + j] = aj;
+        if (s.jd) {
+            const float bj = s.inS[r * n + j] ? INFINITY : s.bq[r * n + j] + 2.f * aj;
+            s.jd[r * n + j] = make_float4(bj, pj, 2.f * s.w[r * n + j], P + pj);
+        }
     }
 }
 
@@ -326,6 +334,189 @@ swap_pairs_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, 
     if (tid == 0) {
         s.pv[r * s.nblk + blockIdx.x] = redv[0];
         s.pp[r * s.nblk + blockIdx.x] = redp[0];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// every (kept i, key j) pair on MFMA: bf16 rows, d = 128, n a multiple of 16.
+// A workgroup (8 waves) takes 512 consecutive kept keys of one row -- each
+// wave 64 of them as the MFMA's A operand in registers -- and a chunk of
+// SPJ keys, streamed as 16-key tiles through a double-buffered LDS stage
+// shared by the waves (whole key rows per load, 16-byte chunk c of row r at
+// position c ^ r).  The cross term v_i . v_j is the MFMA output; the
+// epilogue keeps, per (lane, kept key), the smallest pair value and the tile
+// where it was first reached, so ties resolve to the smaller (i, j).
+//   num = (A_i + B_j) + p_i p_j (2 w_i - 2|mu|^2 + 2 w_j - 2 v_i.v_j)
+//   A_i = ||g||^2 + ||u_i||^2 - 2 g.u_i,  B_j = ||u_j||^2 + 2 g.u_j
+//   den = P - p_i + p_j,  value = num / den^2
+// ---------------------------------------------------------------------------
+namespace {
+typedef __bf16 sbf16x8 __attribute__((ext_vector_type(8)));
+typedef float sf32x4 __attribute__((ext_vector_type(4)));
+constexpr int SPI = 512;        // kept keys per workgroup
+constexpr int SPJ = 2048;       // keys per workgroup
+constexpr int SPT = 8;          // tiles per stage
+constexpr int SPD = 128;        // head dimension
+constexpr int SP_STAGE = SPT * 16 * SPD * 2;  // bytes of V per stage
+#define SP_LDS(ptr) ((__attribute__((address_space(3))) void *)(ptr))
+#define SP_VM(k) case k: asm volatile("s_waitcnt vmcnt(" #k ")" ::: "memory"); break;
+__device__ __forceinline__ void sp_wait_vm(int n) {
+    switch (n) {
+        SP_VM(0) SP_VM(1) SP_VM(4) SP_VM(5)
+        default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    }
+}
+#undef SP_VM
+}  // namespace
+
+__global__ void __launch_bounds__(512)
+swap_pairs_mfma_kernel(const uint16_t *__restrict__ v, int64_t G, int64_t n, int kk, SwapState s) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    unsigned char *vbuf = smem;                                   // [2][SP_STAGE]
+    float4 *jbuf = (float4 *)(smem + 2 * SP_STAGE);               // [2][SPT * 16]
+    float *redv = (float *)(smem + 2 * SP_STAGE + 2 * SPT * 16 * 16);  // [8]
+    int64_t *redp = (int64_t *)(redv + 8);                        // [8]
+    const int64_t r = blockIdx.y;
+    if (!s.st[r * 2]) return;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, rl = lane & 15, grp = lane >> 4;
+    const int64_t nchunk = (n + SPJ - 1) / SPJ;
+    const int ib = (int)(blockIdx.x / nchunk);
+    const int64_t jc = blockIdx.x % nchunk;
+    const int64_t h = r / G;
+    const uint16_t *vh = v + h * n * SPD;
+    const int32_t *Sl = s.Sl + r * kk;
+    const float4 *jd = s.jd + r * n;
+    const int ibase = ib * SPI + w * 64;  // this wave's first kept-list position
+    // A operand: kept keys ibase + 16 it + rl, columns 32 s + 8 grp
+    sbf16x8 qa[4][4];
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+        const int ip = ibase + 16 * it + rl;
+        const int a = ip < kk ? Sl[ip] : 0;
+#pragma unroll
+        for (int st = 0; st < 4; ++st) qa[it][st] = *(const sbf16x8 *)(vh + (int64_t)a * SPD + 32 * st + 8 * grp);
+    }
+    // per kept-key slot (it, e): list position ibase + 16 it + 4 grp + e
+    const double *sc = s.sc + r * 4;
+    const float g2 = (float)sc[1], mu2 = (float)sc[2];
+    float Ai[4][4], pi[4][4], Xi[4][4];
+#pragma unroll
+    for (int it = 0; it < 4; ++it)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int ip = ibase + 16 * it + 4 * grp + e;
+            const int a = ip < kk ? Sl[ip] : 0;
+            const float pa = s.p[r * n + a];
+            Ai[it][e] = ip < kk ? g2 + s.bq[r * n + a] - 2.f * s.a[r * n + a] : INFINITY;
+            pi[it][e] = pa;
+            Xi[it][e] = 2.f * s.w[r * n + a] - 2.f * mu2;
+        }
+    float bv[4][4];
+    int bt[4][4];
+#pragma unroll
+    for (int it = 0; it < 4; ++it)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) { bv[it][e] = INFINITY; bt[it][e] = -1; }
+
+    // stage loads: wave w < SPT fetches tile w of the stage (4 loads of 4 key
+    // rows); waves 0..1 fetch the stage's per-key data (64 keys each)
+    const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(vh), (short)0, (int)(n * SPD * 2), 0x00020000);
+    const __amdgpu_buffer_rsrc_t jres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float4 *>(jd), (short)0, (int)(n * 16), 0x00020000);
+    uint32_t kvo[4], kro[4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+        const int rr = 4 * st + grp;
+        kvo[st] = ((uint32_t)rr * SPD + 8 * ((lane & 15) ^ rr)) * 2;
+        kro[st] = (uint32_t)(rl * 256 + (((4 * st + grp) ^ rl) * 16));
+    }
+    const int64_t j0 = jc * SPJ;
+    const int jn = (int)((n - j0) < SPJ ? (n - j0) : SPJ);  // keys of this chunk (multiple of 16)
+    const int nst = (jn / 16 + SPT - 1) / SPT;
+    auto issue = [&](int stg) {
+        const int64_t sj = j0 + (int64_t)stg * SPT * 16;
+        unsigned char *vb = vbuf + (stg & 1) * SP_STAGE;
+        if (w < SPT && sj + 16 * w < j0 + jn) {
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(vres, SP_LDS(vb + w * 4096 + st * 1024), 16, kvo[st],
+                                                         (uint32_t)((sj + 16 * w) * SPD * 2), 0, 0);
+        }
+        if (w < 2)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(jres, SP_LDS(jbuf + (stg & 1) * SPT * 16 + 64 * w), 16,
+                                                     (uint32_t)lane * 16, (uint32_t)((sj + 64 * w) * 16), 0, 0);
+    };
+    issue(0);
+    for (int stg = 0; stg < nst; ++stg) {
+        if (stg + 1 < nst) issue(stg + 1);
+        // this wave's loads of stage stg have landed once at most those of
+        // stage stg + 1 are outstanding; the barrier makes every wave's visible
+        int mine = 0;
+        if (stg + 1 < nst) {
+            const int64_t nj = j0 + (int64_t)(stg + 1) * SPT * 16;
+            mine = ((w < SPT && nj + 16 * w < j0 + jn) ? 4 : 0) + (w < 2 ? 1 : 0);
+        }
+        sp_wait_vm(mine);
+        __syncthreads();
+        const unsigned char *vb = vbuf + (stg & 1) * SP_STAGE;
+        const float4 *jb = jbuf + (stg & 1) * SPT * 16;
+        const int tiles = min(SPT, jn / 16 - stg * SPT);
+        for (int t = 0; t < tiles; ++t) {
+            const unsigned char *kt = vb + t * 4096;
+            sbf16x8 kb[4];
+#pragma unroll
+            for (int st = 0; st < 4; ++st) kb[st] = *(const sbf16x8 *)(kt + kro[st]);
+            sf32x4 acc[4];
+#pragma unroll
+            for (int it = 0; it < 4; ++it) {
+                acc[it] = (sf32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int st = 0; st < 4; ++st)
+                    acc[it] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[it][st], kb[st], acc[it], 0, 0, 0);
+            }
+            const float4 jv = jb[t * 16 + rl];  // this lane's key
+            const int tg = stg * SPT + t;       // tile index within the chunk
+#pragma unroll
+            for (int it = 0; it < 4; ++it)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float tt = fmaf(-2.f, acc[it][e], Xi[it][e] + jv.z);
+                    const float num = fmaf(pi[it][e] * jv.y, tt, Ai[it][e] + jv.x);
+                    const float den = jv.w - pi[it][e];
+                    const float val = num * __builtin_amdgcn_rcpf(den * den);
+                    const bool better = val < bv[it][e];
+                    bv[it][e] = better ? val : bv[it][e];
+                    bt[it][e] = better ? tg : bt[it][e];
+                }
+        }
+        __syncthreads();  // the stage buffer is refilled two stages on
+    }
+    // lane winner (value, i, j) with ties to the smaller i, then j
+    float lv = INFINITY;
+    int64_t lp = INT64_MAX;
+#pragma unroll
+    for (int it = 0; it < 4; ++it)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            if (bt[it][e] < 0 || !(bv[it][e] < INFINITY)) continue;
+            const int ip = ibase + 16 * it + 4 * grp + e;
+            const int64_t pidx = (int64_t)Sl[ip] * n + (j0 + 16 * (int64_t)bt[it][e] + rl);
+            if (bv[it][e] < lv || (bv[it][e] == lv && pidx < lp)) { lv = bv[it][e]; lp = pidx; }
+        }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const float ov = __shfl_xor(lv, off);
+        const int64_t op = __shfl_xor(lp, off);
+        if (ov < lv || (ov == lv && op < lp)) { lv = ov; lp = op; }
+    }
+    if (lane == 0) { redv[w] = lv; redp[w] = lp; }
+    __syncthreads();
+    if (tid == 0) {
+        for (int ww = 1; ww < 8; ++ww)
+            if (redv[ww] < lv || (redv[ww] == lv && redp[ww] < lp)) { lv = redv[ww]; lp = redp[ww]; }
+        s.pv[r * s.nblk + blockIdx.x] = lv;
+        s.pp[r * s.nblk + blockIdx.x] = lp;
     }
 }
 
@@ -440,6 +631,11 @@ swap_final_kernel(int64_t n, int kk, SwapState s, int32_t *s_idx, float *gap_tra
 // ===========================================================================
 namespace {
 
+// the MFMA pair sweep: bf16, d = 128, whole 16-key tiles
+bool swap_mfma_ok(const fw_rows &rows) {
+    return rows.dtype == FW_BF16 && rows.d == SPD && rows.n % 16 == 0 && rows.n * SPD * 2 < ((int64_t)1 << 31);
+}
+
 size_t small_lds(int n, int d, int nt) {
     size_t b = (size_t)n * n * 8 + (size_t)n * 8 * 3 + (size_t)d * 8 + (size_t)nt * 16;
     b += (size_t)(n + (n & 1)) * 4 + (size_t)n * d * 4;
@@ -465,9 +661,13 @@ SwapLayout swap_layout(const fw_rows &rows, int k, void *ws) {
         off += bytes;
         return p;
     };
-    const int itiles = (k + 31) / 32;
-    const int64_t jtiles = ((int64_t)n + 127) / 128;
-    L.s.nblk = (int)(itiles * jtiles);
+    if (swap_mfma_ok(rows)) {
+        L.s.nblk = (int)(((k + SPI - 1) / SPI) * (((int64_t)n + SPJ - 1) / SPJ));
+    } else {
+        const int itiles = (k + 31) / 32;
+        const int64_t jtiles = ((int64_t)n + 127) / 128;
+        L.s.nblk = (int)(itiles * jtiles);
+    }
     L.z = (float *)take(R * n * 4);
     L.row_m = (float *)take(R * 4);
     L.row_l = (float *)take(R * 4);
@@ -485,6 +685,7 @@ SwapLayout swap_layout(const fw_rows &rows, int k, void *ws) {
     L.s.st = (int32_t *)take(R * 2 * 4);
     L.s.pv = (float *)take(R * L.s.nblk * 4);
     L.s.pp = (int64_t *)take(R * L.s.nblk * 8);
+    L.s.jd = swap_mfma_ok(rows) ? (float4 *)take(R * n * 16) : nullptr;
     L.s.z = L.z;
     L.s.row_m = L.row_m;
     L.s.row_l = L.row_l;
@@ -525,8 +726,13 @@ static hipError_t swap_large(const fw_rows &rows, int k, int max_iters, int32_t 
     for (int it = 0; it < max_iters; ++it) {
         hipLaunchKernelGGL(swap_dots_kernel<T>, dim3(dot_blocks, (unsigned)R), dim3(256), 0, st, v, G,
                            n, d, L.s);
-        hipLaunchKernelGGL(swap_pairs_kernel<T>, dim3((unsigned)L.s.nblk, (unsigned)R), dim3(256), 0,
-                           st, v, G, n, d, k, L.s);
+        if (swap_mfma_ok(rows))
+            hipLaunchKernelGGL(swap_pairs_mfma_kernel, dim3((unsigned)L.s.nblk, (unsigned)R), dim3(512),
+                               (size_t)(2 * SP_STAGE + 2 * SPT * 16 * 16 + 8 * 4 + 8 * 8), st,
+                               (const uint16_t *)rows.v, G, n, k, L.s);
+        else
+            hipLaunchKernelGGL(swap_pairs_kernel<T>, dim3((unsigned)L.s.nblk, (unsigned)R), dim3(256), 0,
+                               st, v, G, n, d, k, L.s);
         hipLaunchKernelGGL(swap_apply_kernel<T>, dim3((unsigned)R), dim3(256), 0, st, v, G, n, d, k,
                            L.s, gap_traj, T_len);
     }

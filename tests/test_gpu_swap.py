@@ -80,6 +80,10 @@ def test_tiny_rows_all(torch_fw):
     dict(kv_heads=2, q_per_kv=2, rows_per_q=4, n=1000, d=128, k=48, max_iters=12),
     dict(kv_heads=1, q_per_kv=3, rows_per_q=3, n=333, d=64, k=100, max_iters=30),
     dict(kv_heads=1, q_per_kv=1, rows_per_q=5, n=130, d=16, k=1, max_iters=5),
+    # bf16, d = 128, n a multiple of 16: the MFMA pair sweep
+    dict(kv_heads=2, q_per_kv=2, rows_per_q=4, n=1024, d=128, k=100, max_iters=12),
+    dict(kv_heads=1, q_per_kv=2, rows_per_q=3, n=2064, d=128, k=600, max_iters=8),
+    dict(kv_heads=1, q_per_kv=1, rows_per_q=4, n=4096, d=128, k=1030, max_iters=6),
 ])
 def test_long_rows_bf16(torch_fw, shape):
     torch, fw = torch_fw
