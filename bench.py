@@ -31,7 +31,7 @@ def _args():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--only", default="", help="comma list: topk,exhaustive,swap,curve,tiny")
+    ap.add_argument("--only", default="", help="comma list: topk,exhaustive,swap,curve,tiny,copy")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     return ap.parse_args()
@@ -57,6 +57,30 @@ def _time(torch, fn, steps, warmup):
 def _roofline(bound, achieved, peak, unit, traffic=None):
     return {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": unit,
             "frac": round(achieved / peak, 4), "traffic": traffic}
+
+
+def _traffic(name, source):
+    """HBM bytes per launch from the committed counter summary
+    profiles/traffic_<name>.txt (FETCH_SIZE and WRITE_SIZE, scaled by a plain
+    copy of known size), or None when the kernel source has changed since the
+    counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic_%s.txt" % name)
+    src = os.path.join(ROOT, "paper_2608_25230_amd", "csrc", source)
+    if not (os.path.exists(path) and os.path.exists(src)):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                key, val = line.split(":", 1)
+                kv[key.strip()] = val.strip()
+    if kv.get("source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+        return None
+    try:
+        return int(float(kv["hbm_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
 
 
 # ---------------------------------------------------------------------------
@@ -181,11 +205,17 @@ def main():
         R = r.H * r.G
         sweeps = int(holder["n_swaps"].sum().item()) + R  # the last sweep of each row finds nothing
         pairs = sweeps * wl.k * (r.n - wl.k)
+        # the pair sweep's cross terms: every kept key against every key, per
+        # row and iteration, d multiply-adds each on bf16 MFMA
+        iters = int(holder["n_swaps"].max().item()) + 1
+        mfma_flop = iters * R * wl.k * r.n * r.d * 2
         components.append({"workload": wl.name, "metric": "swap pairs evaluated/s",
                            "value": round(pairs / (ms / 1e3), 1), "unit": "pairs/s", "ms": round(ms, 3),
                            "rows_per_s": round(R / (ms / 1e3), 2),
                            "median_swaps": float(holder["n_swaps"].float().median().item()),
-                           "dtype": "f32"})
+                           "dtype": "bf16",
+                           "roofline": dict(_roofline("mfma", mfma_flop / (ms / 1e3) / 1e12, MFMA_BF16_TFLOPS,
+                                                      "TFLOP/s"), kernel="fw_swap (all launches)")})
         del dev, holder
         torch.cuda.empty_cache()
 
@@ -233,6 +263,17 @@ def main():
                            "value": round(subsets / (ms / 1e3), 1), "unit": "subsets/s",
                            "ms": round(ms, 4), "dtype": "f64", "note": "launch-bound"})
 
+    # ---- plain device copy (calibrates the HBM byte counters) -------------------
+    if want("copy"):
+        nbytes = 1 << 31
+        src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").uniform_()
+        dst = torch.empty_like(src)
+        ms, _ = _time(torch, lambda: dst.copy_(src), a.steps, a.warmup)
+        components.append({"workload": "device copy 2 GiB", "metric": "GB/s",
+                           "value": round(2 * nbytes / (ms / 1e3) / 1e9, 1), "unit": "GB/s",
+                           "ms": round(ms, 4), "bytes_read": nbytes, "bytes_written": nbytes})
+        del src, dst
+
     if head is None:
         print(json.dumps({"components": components}))
         return
@@ -247,12 +288,15 @@ def main():
         "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
         "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "bf16",
         "data": "synthetic (seeded bf16 N(0,1) rows shaped like the paper's grouped-query heads)",
         "config": {"workload": wl.name, "units": r.H, "rows_per_unit": r.G, "n": r.n, "d": r.d,
                    "ks": list(wl.ks), "rows": head["R"], "outputs": "o, o_S, gap, dropped"},
-        "roofline": dict(_roofline("hbm", gbs, HBM_PEAK_GBS, "GB/s"), kernel="fw_dense_topk (all launches)",
-                         algorithmic_bytes=head["alg_bytes"]),
+        "roofline": dict(_roofline("hbm", gbs, HBM_PEAK_GBS, "GB/s", _traffic("streaming_topk_n4096",
+                                                                               "k_topk_fused.hip")),
+                         kernel="topk_fused_kernel (fw_dense_topk: one launch plus a flag clear and the "
+                                "fallback pass)",
+                         algorithmic_bytes=head["alg_bytes"], launches_per_step=1),
         "components": components,
     }
     if not a.no_cpu_baseline:
