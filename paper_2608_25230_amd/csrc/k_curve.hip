@@ -127,7 +127,7 @@ __global__ void window_combine_kernel(int64_t rows, int nchunks, const float *pa
 // the complement of the order-preserving bits), payload = key index.
 __global__ void __launch_bounds__(kSortThreads)
 unit_sort_kernel(const float *__restrict__ importance, int64_t n, uint32_t *keys_a, uint32_t *keys_b,
-                 int32_t *vals_a, int32_t *vals_b) {
+                 int32_t *vals_a, int32_t *vals_b, int with_vals) {
     __shared__ int hist[256];
     __shared__ int base[256];
     __shared__ int wcnt[kSortThreads / 64][256];
@@ -137,7 +137,7 @@ unit_sort_kernel(const float *__restrict__ importance, int64_t n, uint32_t *keys
     int32_t *va = vals_a + h * n, *vb = vals_b + h * n;
     for (int64_t j = tid; j < n; j += kSortThreads) {
         ka[j] = ~ord_key(importance[h * n + j]);
-        va[j] = (int32_t)j;
+        if (with_vals) va[j] = (int32_t)j;
     }
     __syncthreads();
     for (int shift = 0; shift < 32; shift += 8) {
@@ -172,7 +172,7 @@ unit_sort_kernel(const float *__restrict__ importance, int64_t n, uint32_t *keys
                 int off = base[dig];
                 for (int w = 0; w < wv; ++w) off += wcnt[w][dig];
                 kb[off + rank] = key;
-                vb[off + rank] = va[j];
+                if (with_vals) vb[off + rank] = va[j];
             }
             __syncthreads();
             if (tid < 256) {
@@ -189,37 +189,67 @@ unit_sort_kernel(const float *__restrict__ importance, int64_t n, uint32_t *keys
     // four passes: the result is back in keys_a / vals_a
 }
 
-// Pass 5: curve[k] = sum_{i >= k} sorted[i] (float64), and the order.
+// Pass 5: curve[k] = sum_{i >= k} sorted[i] (float64) read from the sorted
+// keys themselves, and the order.  Tiles of 8192 positions from the end: a
+// coalesced load into LDS, per-thread sums of 8 consecutive positions, a
+// suffix scan of the thread sums (wave shuffles, then across waves), and a
+// coalesced store.
+constexpr int kCurveTile = 8 * kSortThreads;
 __global__ void __launch_bounds__(kSortThreads)
-unit_curve_kernel(const float *__restrict__ importance, int64_t n, const int32_t *__restrict__ vals,
+unit_curve_kernel(const uint32_t *__restrict__ keys, int64_t n, const int32_t *__restrict__ vals,
                   float *__restrict__ curve, int32_t *__restrict__ order) {
-    __shared__ double part[kSortThreads];
-    const int tid = threadIdx.x;
+    __shared__ float tile[kCurveTile];
+    __shared__ double wsum[kSortThreads / 64];
+    __shared__ double carry_s;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int64_t h = blockIdx.x;
-    const int32_t *vs = vals + h * n;
-    const float *imp = importance + h * n;
-    const int64_t chunk = (n + kSortThreads - 1) / kSortThreads;
-    const int64_t lo = tid * chunk, hi = (lo + chunk < n) ? lo + chunk : n;
-    double s = 0.0;
-    for (int64_t i = hi - 1; i >= lo; --i) s += (double)imp[vs[i]];
-    part[tid] = s;
-    __syncthreads();
-    if (tid == 0) {  // suffix sums over the chunks, last chunk first
-        double acc = 0.0;
-        for (int t = kSortThreads - 1; t >= 0; --t) {
-            const double x = part[t];
-            part[t] = acc;
-            acc += x;
+    const uint32_t *kh = keys + h * n;
+    float *ch = curve + h * (n + 1);
+    if (tid == 0) carry_s = 0.0;
+    for (int64_t t0 = ((n - 1) / kCurveTile) * kCurveTile; t0 >= 0; t0 -= kCurveTile) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int64_t e = t0 + i * kSortThreads + tid;
+            tile[i * kSortThreads + tid] = e < n ? key_to_float(~kh[e]) : 0.f;
         }
+        __syncthreads();
+        double part = 0.0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) part += (double)tile[8 * tid + q];
+        // inclusive suffix sum over the lanes of this wave
+        double suf = part;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const double y = __shfl_down(suf, off);
+            if (lane + off < 64) suf += y;
+        }
+        if (lane == 0) wsum[wv] = suf;  // the wave's total
+        __syncthreads();
+        double after = carry_s;  // everything right of this wave
+        for (int w2 = wv + 1; w2 < kSortThreads / 64; ++w2) after += wsum[w2];
+        double acc = after + (suf - part);  // right of this thread's 8 positions
+#pragma unroll
+        for (int q = 7; q >= 0; --q) {
+            acc += (double)tile[8 * tid + q];
+            tile[8 * tid + q] = (float)acc;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            double tot = 0.0;
+            for (int w2 = 0; w2 < kSortThreads / 64; ++w2) tot += wsum[w2];
+            carry_s += tot;
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int64_t e = t0 + i * kSortThreads + tid;
+            if (e < n) {
+                ch[e] = tile[i * kSortThreads + tid];
+                if (order) order[h * n + e] = vals[h * n + e];
+            }
+        }
+        __syncthreads();
     }
-    __syncthreads();
-    double acc = part[tid];
-    for (int64_t i = hi - 1; i >= lo; --i) {
-        acc += (double)imp[vs[i]];
-        curve[h * (n + 1) + i] = (float)acc;
-        if (order) order[h * n + i] = vs[i];
-    }
-    if (tid == 0) curve[h * (n + 1) + n] = 0.f;
+    if (tid == 0) ch[n] = 0.f;
 }
 
 // ---------------------------------------------------------------------------
@@ -279,9 +309,9 @@ static hipError_t curve_impl(const fw_rows &rows, float *importance, float *curv
                            rows.bias, G, n, d, nch, nullptr, nullptr, L.row_m, L.row_il, importance);
     }
     hipLaunchKernelGGL(unit_sort_kernel, dim3((unsigned)H), dim3(kSortThreads), 0, st, importance, n,
-                       L.ka, L.kb, L.va, L.vb);
-    hipLaunchKernelGGL(unit_curve_kernel, dim3((unsigned)H), dim3(kSortThreads), 0, st, importance, n,
-                       L.va, curve, order);
+                       L.ka, L.kb, L.va, L.vb, order ? 1 : 0);
+    hipLaunchKernelGGL(unit_curve_kernel, dim3((unsigned)H), dim3(kSortThreads), 0, st,
+                       (const uint32_t *)L.ka, n, (const int32_t *)L.va, curve, order);
     return hipGetLastError();
 }
 
