@@ -11,42 +11,53 @@ namespace fw {
 // The documented default scale 1/sqrt(d), as the float32 value callers pass.
 __device__ __forceinline__ float default_scale(int d) { return (float)(1.0 / sqrt((double)d)); }
 
-// Whole workgroup; n <= 64 <= blockDim.x.  Vs [n][d] float (LDS) receives the
-// values; zs, ps [n], mu [d], Gm [n][n] (LDS) receive the instance.
+// Row pitch (floats) of the values staged in LDS: d + 1 keeps the column
+// reads of different rows on different banks.
+__host__ __device__ inline int instance_pitch(int d) { return d + 1; }
+
+// Whole workgroup; n <= 64 <= blockDim.x.  Vs [n][d + 1] float (LDS) stages
+// the keys, then the values; zs, ps [n], mu [d], Gm [n][n] (LDS) receive the
+// instance.  Global reads are coalesced (whole rows); the logits, weights,
+// dense output and Gram are formed from LDS.
 template <typename T>
 __device__ void instance64(const T *qr, const T *kh, const T *vh, float scale, const float *bias,
                            int n, int d, float *Vs, double *zs, double *ps, double *mu, double *Gm) {
     const int tid = threadIdx.x, NT = blockDim.x;
-    for (int e = tid; e < n * d; e += NT) Vs[e] = Elem<T>::load(vh, e);
+    const int pitch = instance_pitch(d);
+    float *qs = (float *)mu;  // the query, in the dense output's space until that is formed
+    for (int e = tid; e < n * d; e += NT) Vs[(e / d) * pitch + e % d] = Elem<T>::load(kh, e);
+    for (int c = tid; c < d; c += NT) qs[c] = Elem<T>::load(qr, c);
+    __syncthreads();
     if (tid < n) {
         double dot = 0.0;
-        for (int c = 0; c < d; ++c)
-            dot = fma((double)Elem<T>::load(qr, c), (double)Elem<T>::load(kh, (size_t)tid * d + c), dot);
+        for (int c = 0; c < d; ++c) dot = fma((double)qs[c], (double)Vs[tid * pitch + c], dot);
         zs[tid] = (double)scale * dot + (bias ? (double)bias[tid] : 0.0);
     }
     __syncthreads();
-    if (tid == 0) {
-        double m = zs[0];
-        for (int j = 1; j < n; ++j) m = zs[j] > m ? zs[j] : m;
-        double l = 0.0;
-        for (int j = 0; j < n; ++j) {
-            ps[j] = exp(zs[j] - m);
-            l += ps[j];
-        }
-        for (int j = 0; j < n; ++j) ps[j] /= l;
+    for (int e = tid; e < n * d; e += NT) Vs[(e / d) * pitch + e % d] = Elem<T>::load(vh, e);
+    if (tid < 64) {  // softmax on one wave, fixed reduction order
+        const double z = tid < n ? zs[tid] : -INFINITY;
+        double m = z;
+        for (int off = 32; off > 0; off >>= 1) m = fmax(m, __shfl_xor(m, off));
+        const double ez = tid < n ? exp(z - m) : 0.0;
+        double l = ez;
+        for (int off = 32; off > 0; off >>= 1) l += __shfl_xor(l, off);
+        if (tid < n) ps[tid] = ez / l;
     }
     __syncthreads();
     for (int c = tid; c < d; c += NT) {
         double s = 0.0;
-        for (int j = 0; j < n; ++j) s = fma(ps[j], (double)Vs[j * d + c], s);
+        for (int j = 0; j < n; ++j) s = fma(ps[j], (double)Vs[j * pitch + c], s);
         mu[c] = s;
     }
     __syncthreads();
-    for (int e = tid; e < n * n; e += NT) {
-        const int i = e / n, j = e % n;
-        if (i > j) continue;
+    for (int e = tid; e < n * (n + 1) / 2; e += NT) {
+        // e -> (i, j), i <= j, row-major over the upper triangle
+        int i = 0, rem = e;
+        while (rem >= n - i) { rem -= n - i; ++i; }
+        const int j = i + rem;
         double s = 0.0;
-        for (int c = 0; c < d; ++c) s = fma((double)Vs[i * d + c] - mu[c], (double)Vs[j * d + c] - mu[c], s);
+        for (int c = 0; c < d; ++c) s = fma((double)Vs[i * pitch + c] - mu[c], (double)Vs[j * pitch + c] - mu[c], s);
         const double gij = ps[i] * ps[j] * s;
         Gm[i * n + j] = gij;
         Gm[j * n + i] = gij;

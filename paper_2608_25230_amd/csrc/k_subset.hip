@@ -9,23 +9,26 @@
 //
 // Enumeration.  The keys split into a low range [0, m) and a high range
 // [m, n); every k-subset is a high part H (|H| = h) plus a low part L
-// (|L| = k - h).  A lane owns one H; the lanes of a wave, all with the same h,
-// walk every L in the same revolving-door order over [0, m), so each step's
-// entering and leaving keys are wave-uniform and the shared per-step values
-// (S_L = sum_{x,y in L} Gm_xy and p(L)^2) come from per-row tables.  Against
-// the wave's best ratio beta the test
+// (|L| = k - h).  For each h one of the two parts is owned by a lane and the
+// other is walked: the lanes of a wave, all with the same h, walk every
+// walked part in the same revolving-door order over its range (at most 16
+// keys), so each step's entering and leaving keys are wave-uniform and the
+// shared per-step values (S_W = sum_{x,y in W} Gm_xy and p(W)^2 of the walked
+// part W) come from per-row tables.  With O the lane's own part, against the
+// wave's best ratio beta the test
 //     f = S(A) - beta p(A)^2 <= 0
 // is linear in the walk:
-//     S(A) - beta p(A)^2 = K1 + sum_{x in L} e[x] + S_L - beta p(L)^2,
-//     K1 = S_H - beta p(H)^2,   e[x] = 2 sum_{a in H} Gm_xa - 2 beta p(H) p_x,
+//     S(A) - beta p(A)^2 = K1 + sum_{x in W} e[x] + S_W - beta p(W)^2,
+//     K1 = S_O - beta p(O)^2,   e[x] = 2 sum_{a in O} Gm_xa - 2 beta p(O) p_x,
 // so one step is two register reads of e (indexed by the uniform keys), two
 // adds, one multiply-add and a compare.  Subsets that pass are scored exactly
 // (S / p^2 from the Gram, ties to the lexicographically smaller set), lower
 // beta for the wave and rescale e.  The top-k set seeds every lane, so the
-// answer is never worse than top-k.  Work items (h, a run of up to 64 high
-// parts) are taken by the waves of the row's workgroup from a shared counter,
-// longest walks first.  Reported gaps are recomputed from the d-dimensional
-// residual sums of the chosen sets.
+// answer is never worse than top-k.  The plan picks m and, per h, which part
+// the lanes own, to minimise walk steps plus per-lane set-up.  Work items
+// (h, a run of up to 64 owned parts) are taken by the waves of the row's
+// workgroup from a shared counter, longest first.  Reported gaps are
+// recomputed from the d-dimensional residual sums of the chosen sets.
 #include "fw_internal.hpp"
 #include "instance64.hpp"
 #include "revdoor.hpp"
@@ -35,65 +38,92 @@ namespace fw {
 namespace {
 
 constexpr int kSubsetThreads = 256;
-constexpr int kMaxLow = 16;       // low range size (per-lane e[] in registers)
-constexpr int kMaxEntries = 2048; // walk-table entries per row (LDS)
+constexpr int kMaxWalk = 16;      // walked range size (per-lane e[] in registers)
+constexpr int kMaxEntries = 4096; // walk-table entries per row (LDS)
+constexpr int kMaxClass = 17;     // values of h with work (min(m, n - m) + 1)
+
+// One value of h: which part the lanes own and which is walked.
+struct EnumClass {
+    int h;
+    int wb, wn, ws;  // walked part: range [wb, wb + wn), size ws
+    int lb, ln, ls;  // owned part: range [lb, lb + ln), size ls
+    int toff;        // first walk-table entry
+};
 
 // Enumeration plan shared by host (sizes) and device (tables, jobs).
 struct EnumPlan {
     int n, k, d, G;
-    int m;             // low range [0, m)
-    int hlo, hhi;      // high part sizes with work
-    int nent;          // walk-table entries: sum over used walk sizes of C(m, kw)
+    int m;
+    int ncls;
+    EnumClass cls[kMaxClass];
+    int nent;  // walk-table entries
     int njobs;
-    int toff[kMaxLow + 1];  // first entry of the walk of size kw (-1 if unused)
 };
 
 __host__ __device__ inline int ceil64(uint64_t x) { return (int)((x + 63) / 64); }
+// walks run in rounds of four steps; tables are padded with neutral steps
+__host__ __device__ inline uint64_t pad4(uint64_t x) { return (x + 3) & ~(uint64_t)3; }
+constexpr uint64_t kPadMask = ~(uint64_t)0;  // walk-table mask of a padding step
 
-__host__ __device__ inline bool plan_for(int n, int k, int m, EnumPlan *P) {
+// Estimated instructions of one wave job: set-up of the owned part plus the
+// walk.
+__host__ __device__ inline double job_cost(int wn, int ws, int ln, int ls) {
+    const double steps = (double)binom(wn, ws);
+    double setup = 40.0 + 6.0 * ln + 6.0 * ls * ls;
+    if (ws > 0) setup += ls * (1.5 * wn + 8.0) + 3.0 * wn;
+    return setup + 10.0 * steps;
+}
+
+__host__ __device__ inline bool plan_for(int n, int k, int m, EnumPlan *P, double *cost) {
     EnumPlan p{};
     p.n = n;
     p.k = k;
     p.m = m;
-    p.hlo = k - m > 0 ? k - m : 0;
-    p.hhi = k < n - m ? k : n - m;
-    if (p.hlo > p.hhi) return false;
-    for (int kw = 0; kw <= kMaxLow; ++kw) p.toff[kw] = -1;
+    const int N = n - m;
+    const int hlo = k - m > 0 ? k - m : 0, hhi = k < N ? k : N;
+    if (hlo > hhi || hhi - hlo + 1 > kMaxClass) return false;
+    double total = 0.0;
     uint64_t nent = 0, njobs = 0;
-    for (int h = p.hlo; h <= p.hhi; ++h) {
+    int toffA[kMaxWalk + 1], toffB[kMaxWalk + 1];
+    for (int q = 0; q <= kMaxWalk; ++q) toffA[q] = toffB[q] = -1;
+    for (int h = hlo; h <= hhi; ++h) {
         const int kw = k - h;
-        p.toff[kw] = (int)nent;
-        nent += binom(m, kw);
-        njobs += (uint64_t)ceil64(binom(n - m, h));
+        // A: lanes own the high part, walk the low range; B: the reverse
+        const bool okA = m <= kMaxWalk, okB = N <= kMaxWalk;
+        if (!okA && !okB) return false;
+        const double cA = okA ? ceil64(binom(N, h)) * job_cost(m, kw, N, h) : 0.0;
+        const double cB = okB ? ceil64(binom(m, kw)) * job_cost(N, h, m, kw) : 0.0;
+        const bool useA = okA && (!okB || cA <= cB);
+        EnumClass c;
+        c.h = h;
+        if (useA) {
+            c.wb = 0; c.wn = m; c.ws = kw; c.lb = m; c.ln = N; c.ls = h;
+            if (toffA[kw] < 0) { toffA[kw] = (int)nent; nent += pad4(binom(m, kw)); }
+            c.toff = toffA[kw];
+        } else {
+            c.wb = m; c.wn = N; c.ws = h; c.lb = 0; c.ln = m; c.ls = kw;
+            if (toffB[h] < 0) { toffB[h] = (int)nent; nent += pad4(binom(N, h)); }
+            c.toff = toffB[h];
+        }
+        total += useA ? cA : cB;
+        njobs += (uint64_t)ceil64(binom(c.ln, c.ls));
+        p.cls[p.ncls++] = c;
     }
     if (nent > (uint64_t)kMaxEntries || njobs > (1u << 22)) return false;
     p.nent = (int)nent;
     p.njobs = (int)njobs;
     *P = p;
+    *cost = total;
     return true;
-}
-
-// Estimated cost in wave-steps: walk steps of every job plus the per-lane
-// set-up of its high part (about one step per nine instructions).
-__host__ inline double plan_cost(const EnumPlan &p) {
-    double c = 0.0;
-    for (int h = p.hlo; h <= p.hhi; ++h) {
-        const double jobs = (double)ceil64(binom(p.n - p.m, h));
-        const double steps = (double)binom(p.m, p.k - h);
-        const double setup = (double)(p.m * h + h * h + 3 * (p.n - p.m)) / 9.0;
-        c += jobs * (steps + setup);
-    }
-    return c;
 }
 
 __host__ inline bool choose_plan(int64_t n, int k, EnumPlan *out) {
     bool found = false;
     double best = 0.0;
-    const int mmax = n < kMaxLow ? (int)n : kMaxLow;
-    for (int m = 1; m <= mmax; ++m) {
+    for (int m = 1; m <= (int)n; ++m) {
         EnumPlan p;
-        if (!plan_for((int)n, k, m, &p)) continue;
-        const double c = plan_cost(p);
+        double c;
+        if (!plan_for((int)n, k, m, &p, &c)) continue;
         if (!found || c < best) {
             best = c;
             *out = p;
@@ -103,9 +133,9 @@ __host__ inline bool choose_plan(int64_t n, int k, EnumPlan *out) {
     return found;
 }
 
-// Job descriptor: h, kw, first high-part rank, lanes, steps, table offset.
+// Job descriptor: the class and a run of owned parts (colex ranks).
 struct EnumJob {
-    int32_t h, kw, start, lanes, steps, toff;
+    int32_t cls, start, lanes, steps;
 };
 
 struct SubsetLds {
@@ -121,7 +151,7 @@ __host__ __device__ inline SubsetLds subset_lds(int n, int d, int k, int nent, i
     L.mu = take((size_t)d * 8);
     // walk tables overlay the values staged for the instance (dead by then)
     const size_t tab = (size_t)nent * 16 + (size_t)nent * 8;
-    const size_t vsb = (size_t)n * d * 4;
+    const size_t vsb = (size_t)n * instance_pitch(d) * 4;
     const size_t region = take(tab > vsb ? tab : vsb);
     L.ent = region;
     L.pl = region + (size_t)nent * 16;
@@ -135,50 +165,62 @@ __host__ __device__ inline SubsetLds subset_lds(int n, int d, int k, int nent, i
 
 }  // namespace
 
-// Walk tables (row independent): for every used walk size kw the
-// revolving-door sequence over [0, m) -- entry t holds the keys entering and
-// leaving at step t (in | out << 8) and the mask of L_t -- and the job list,
-// longest walks first.
-__global__ void enum_plan_kernel(EnumPlan p, uint32_t *io, uint32_t *lmk, EnumJob *jobs) {
+// Walk tables (row independent): for every walked (range, size) the
+// revolving-door sequence -- entry t holds the keys entering and leaving at
+// step t relative to the range (in | out << 8) and the mask of the walked
+// part (absolute key positions) -- and the job list, longest jobs first.
+__global__ void enum_plan_kernel(EnumPlan p, uint2 *io, uint64_t *wmk, EnumJob *jobs) {
     if (threadIdx.x != 0 || blockIdx.x != 0) return;
-    int c[kMaxLow + 2];
-    for (int h = p.hlo; h <= p.hhi; ++h) {
-        const int kw = p.k - h;
-        int t = p.toff[kw];
-        uint32_t mask = kw == 0 ? 0u : ((kw >= 32) ? 0xFFFFFFFFu : ((1u << kw) - 1u));
-        io[t] = 0;
-        lmk[t] = mask;
-        if (kw > 0 && kw < p.m) {
-            revdoor_init(c, kw, p.m);
+    int c[kMaxWalk + 2];
+    for (int q = 0; q < p.ncls; ++q) {
+        const EnumClass &C = p.cls[q];
+        bool first = true;  // tables are shared by classes with the same walk
+        for (int q2 = 0; q2 < q; ++q2)
+            if (p.cls[q2].toff == C.toff) first = false;
+        if (!first) continue;
+        int t = C.toff;
+        uint32_t rel = C.ws == 0 ? 0u : ((1u << C.ws) - 1u);
+        io[t] = make_uint2(0u, 0u);
+        wmk[t] = (uint64_t)rel << C.wb;
+        if (C.ws > 0 && C.ws < C.wn) {
+            revdoor_init(c, C.ws, C.wn);
             int in, out;
-            while (revdoor_next(c, kw, &in, &out)) {
+            while (revdoor_next(c, C.ws, &in, &out)) {
                 ++t;
-                mask ^= (1u << in) ^ (1u << out);
-                io[t] = (uint32_t)in | ((uint32_t)out << 8);
-                lmk[t] = mask;
+                rel ^= (1u << in) ^ (1u << out);
+                io[t] = make_uint2((uint32_t)in, (uint32_t)out);
+                wmk[t] = (uint64_t)rel << C.wb;
             }
         }
+        const int end = C.toff + (int)pad4(binom(C.wn, C.ws));
+        for (++t; t < end; ++t) {  // neutral steps: no key moves, never a candidate
+            io[t] = make_uint2(0u, 0u);
+            wmk[t] = kPadMask;
+        }
     }
-    // jobs, grouped by h in order of decreasing walk length
+    // jobs: classes in order of decreasing job cost
     int nj = 0;
-    bool done[kMaxLow + 48];
-    for (int h = 0; h <= p.hhi; ++h) done[h] = h < p.hlo;
-    for (int round = p.hlo; round <= p.hhi; ++round) {
-        int hb = -1;
-        uint64_t best = 0;
-        for (int h = p.hlo; h <= p.hhi; ++h)
-            if (!done[h] && (hb < 0 || binom(p.m, p.k - h) > best)) { hb = h; best = binom(p.m, p.k - hb); }
-        done[hb] = true;
-        const uint64_t tot = binom(p.n - p.m, hb);
-        for (uint64_t s = 0; s < tot; s += 64) {
-            EnumJob j;
-            j.h = hb;
-            j.kw = p.k - hb;
-            j.start = (int32_t)s;
-            j.lanes = (int32_t)((tot - s) < 64 ? (tot - s) : 64);
-            j.steps = (int32_t)binom(p.m, p.k - hb);
-            j.toff = p.toff[p.k - hb];
-            jobs[nj++] = j;
+    bool done[kMaxClass];
+    for (int q = 0; q < p.ncls; ++q) done[q] = false;
+    for (int round = 0; round < p.ncls; ++round) {
+        int qb = -1;
+        double best = 0.0;
+        for (int q = 0; q < p.ncls; ++q) {
+            const EnumClass &C = p.cls[q];
+            const double cq = job_cost(C.wn, C.ws, C.ln, C.ls);
+            if (!done[q] && (qb < 0 || cq > best)) { qb = q; best = cq; }
+        }
+        done[qb] = true;
+        const EnumClass &C = p.cls[qb];
+        const uint64_t tot = binom(C.ln, C.ls);
+        const int steps = (int)pad4(binom(C.wn, C.ws));
+        for (uint64_t s0 = 0; s0 < tot; s0 += 64) {
+            EnumJob jb;
+            jb.cls = qb;
+            jb.start = (int32_t)s0;
+            jb.lanes = (int32_t)((tot - s0) < 64 ? (tot - s0) : 64);
+            jb.steps = steps;
+            jobs[nj++] = jb;
         }
     }
 }
@@ -187,7 +229,7 @@ template <typename T>
 __global__ void __launch_bounds__(kSubsetThreads)
 best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
                    const float *__restrict__ scale, const float *__restrict__ bias, EnumPlan pl,
-                   const uint32_t *__restrict__ g_io, const uint32_t *__restrict__ g_lmk,
+                   const uint2 *__restrict__ g_io, const uint64_t *__restrict__ g_wmk,
                    const EnumJob *__restrict__ g_jobs, int32_t *best_idx, float *best_gap,
                    float *topk_gap, float *closed, float *dropped_topk, int32_t *topk_idx) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -218,12 +260,17 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
     const uint64_t top_mask = topk_mask64(zs, n, kk, topk_idx ? topk_idx + r * kk : nullptr, redm);
     // per-row walk tables (Vs is dead: instance64 ends with a barrier)
     for (int t = tid; t < pl.nent; t += NT) {
-        const uint32_t lm = g_lmk[t];
+        const uint64_t lm = g_wmk[t];
+        if (lm == kPadMask) {  // neutral step
+            ent[t] = make_double2(INFINITY, 0.0);
+            PLt[t] = 0.0;
+            continue;
+        }
         double P = 0.0, S = 0.0;
-        for (uint32_t a = lm; a; a &= a - 1) {
-            const int x = __ffs(a) - 1;
+        for (uint64_t a = lm; a; a &= a - 1) {
+            const int x = __ffsll((unsigned long long)a) - 1;
             P += ps[x];
-            for (uint32_t b2 = lm; b2; b2 &= b2 - 1) S += Gm[x * n + (__ffs(b2) - 1)];
+            for (uint64_t b2 = lm; b2; b2 &= b2 - 1) S += Gm[x * n + (__ffsll((unsigned long long)b2) - 1)];
         }
         ent[t] = make_double2(S, P * P);
         PLt[t] = P;
@@ -245,65 +292,74 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
     double best_val = S_top / (P_top * P_top);
     uint64_t best_mask = top_mask;
     double beta = best_val;  // wave-uniform
-    const int N = n - m;
-
     for (;;) {
         int jn = 0;
         if (lane == 0) jn = atomicAdd(ctr, 1);
         jn = __builtin_amdgcn_readfirstlane(__shfl(jn, 0));
         if (jn >= pl.njobs) break;
         const EnumJob jb = g_jobs[jn];
-        const int h = jb.h, kw = jb.kw;
+        const EnumClass C = pl.cls[jb.cls];
+        const int wb = C.wb, wn = C.wn, ls = C.ls;
         const bool act = lane < jb.lanes;
-        // high part of this lane: colex rank start + lane among h-subsets of [m, n)
-        uint64_t Hm = 0;
+        // owned part of this lane: colex rank start + lane among ls-subsets of
+        // [lb, lb + ln)
+        uint64_t Om = 0;
         if (act) {
             uint32_t rr = (uint32_t)(jb.start + lane);
-            int c = N - 1;
-            for (int s = h; s >= 1; --s) {
-                while (pas[c * (kk + 1) + s] > rr) --c;
-                Hm |= 1ull << (m + c);
-                rr -= pas[c * (kk + 1) + s];
+            int c = C.ln - 1;
+            for (int sz = ls; sz >= 1; --sz) {
+                while (pas[c * (kk + 1) + sz] > rr) --c;
+                Om |= 1ull << (C.lb + c);
+                rr -= pas[c * (kk + 1) + sz];
                 --c;
             }
         }
-        double PH = 0.0, SH = 0.0;
-        for (uint64_t a = Hm; a; a &= a - 1) {
+        double PO = 0.0, SO = 0.0;
+        for (uint64_t a = Om; a; a &= a - 1) {
             const int x = __ffsll((unsigned long long)a) - 1;
-            PH += ps[x];
-            for (uint64_t b2 = Hm; b2; b2 &= b2 - 1) SH += Gm[x * n + (__ffsll((unsigned long long)b2) - 1)];
+            PO += ps[x];
+            const double *row = Gm + x * n;
+            for (uint64_t b2 = Om; b2; b2 &= b2 - 1) SO += row[__ffsll((unsigned long long)b2) - 1];
         }
-        double e[kMaxLow];
+        // e[x] over the walked range, from contiguous Gram rows
+        double e[kMaxWalk];
 #pragma unroll
-        for (int x = 0; x < kMaxLow; ++x) {
-            double E = 0.0;
-            if (x < m)
-                for (uint64_t a = Hm; a; a &= a - 1) E += Gm[x * n + (__ffsll((unsigned long long)a) - 1)];
-            e[x] = (x < m) ? 2.0 * E - 2.0 * beta * PH * ps[x] : 0.0;
+        for (int x = 0; x < kMaxWalk; ++x) e[x] = 0.0;
+        if (C.ws > 0) {
+            for (uint64_t a = Om; a; a &= a - 1) {
+                const double *row = Gm + (__ffsll((unsigned long long)a) - 1) * n + wb;
+#pragma unroll
+                for (int x = 0; x < kMaxWalk; ++x)
+                    if (x < wn) e[x] += row[x];
+            }
+#pragma unroll
+            for (int x = 0; x < kMaxWalk; ++x)
+                if (x < wn) e[x] = 2.0 * e[x] - 2.0 * beta * PO * ps[wb + x];
         }
-        double K1 = SH - beta * PH * PH;
-        double Y = K1;
-        for (int x = 0; x < kw; ++x) Y += e[x];
+        double Y = SO - beta * PO * PO;
+#pragma unroll
+        for (int x = 0; x < kMaxWalk; ++x)
+            if (x < C.ws) Y += e[x];
         if (!act) Y = INFINITY;
-        const uint32_t *io = g_io + jb.toff;
-        const uint32_t *lmk = g_lmk + jb.toff;
-        const double2 *en = ent + jb.toff;
-        const double *plt = PLt + jb.toff;
-        const int steps = jb.steps;
+        const uint2 *io = g_io + C.toff;
+        const uint64_t *wmk = g_wmk + C.toff;
+        const double2 *en = ent + C.toff;
+        const double *plt = PLt + C.toff;
+        const int steps = jb.steps;  // a multiple of 4 (padded with neutral steps)
         double thr = 1e-12 * beta;
         // exact score of walk step t for this lane (a candidate)
         auto exact = [&](int t) {
-            const uint32_t lm = lmk[t];
-            double S = SH + en[t].x;
-            for (uint32_t a = lm; a; a &= a - 1) {
-                const int x = __ffs(a) - 1;
+            const uint64_t wm = wmk[t];
+            double S = SO + en[t].x;
+            for (uint64_t a = wm; a; a &= a - 1) {
+                const double *row = Gm + (__ffsll((unsigned long long)a) - 1) * n;
                 double E = 0.0;
-                for (uint64_t b2 = Hm; b2; b2 &= b2 - 1) E += Gm[x * n + (__ffsll((unsigned long long)b2) - 1)];
+                for (uint64_t b2 = Om; b2; b2 &= b2 - 1) E += row[__ffsll((unsigned long long)b2) - 1];
                 S += 2.0 * E;
             }
-            const double P = PH + plt[t];
+            const double P = PO + plt[t];
             const double val = S / (P * P);
-            const uint64_t mask = Hm | (uint64_t)lm;
+            const uint64_t mask = Om | wm;
             if (val < best_val || (val == best_val && lex_less(mask, best_mask))) {
                 best_val = val;
                 best_mask = mask;
@@ -313,44 +369,43 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
         // rare candidates handled after the four tests (a beta lowered within
         // the round only widens the filter of the remaining steps)
         for (int t0 = 0; t0 < steps; t0 += 4) {
-            uint32_t w[4];
+            uint2 w[4];
             double2 c[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                const int t = t0 + u;
-                w[u] = (t > 0 && t < steps) ? io[t] : 0u;
-                c[u] = (t < steps) ? en[t] : make_double2(INFINITY, 0.0);
+                w[u] = io[t0 + u];
+                c[u] = en[t0 + u];
             }
             bool cand[4];
-            bool any = false;
+            uint64_t any = 0;
             double y = Y;
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                y += e[w[u] & 255u] - e[(w[u] >> 8) & 255u];
+                y += e[w[u].x] - e[w[u].y];
                 const double f = y + fma(-beta, c[u].y, c[u].x);
                 cand[u] = f <= thr;
-                any |= cand[u];
+                any |= __ballot(cand[u]);  // wave masks: or-ed on the scalar unit
             }
             Y = y;
-            if (__ballot(any)) {  // rare: exact scores, then the wave's new beta
+            if (any) {  // rare: exact scores, then the wave's new beta
 #pragma unroll
                 for (int u = 0; u < 4; ++u)
                     if (cand[u]) exact(t0 + u);
-                double wb = best_val;
+                double wbst = best_val;
 #pragma unroll
-                for (int off = 32; off > 0; off >>= 1) wb = fmin(wb, __shfl_xor(wb, off));
-                if (wb < beta) {
-                    const double dB = wb - beta;
+                for (int off = 32; off > 0; off >>= 1) wbst = fmin(wbst, __shfl_xor(wbst, off));
+                if (wbst < beta) {
+                    const double dB = wbst - beta;
 #pragma unroll
-                    for (int x = 0; x < kMaxLow; ++x)
-                        if (x < m) e[x] -= 2.0 * dB * PH * ps[x];
-                    beta = wb;
+                    for (int x = 0; x < kMaxWalk; ++x)
+                        if (x < wn) e[x] -= 2.0 * dB * PO * ps[wb + x];
+                    beta = wbst;
                     thr = 1e-12 * beta;
-                    K1 = SH - beta * PH * PH;
-                    // Y for the round's last step from the rescaled e
-                    const int tl = (t0 + 3 < steps) ? t0 + 3 : steps - 1;
-                    double yy = K1;
-                    for (uint32_t a = lmk[tl]; a; a &= a - 1) yy += e[__ffs(a) - 1];
+                    // Y for the round's last real step from the rescaled e
+                    int tl = t0 + 3;
+                    while (wmk[tl] == kPadMask) --tl;
+                    double yy = SO - beta * PO * PO;
+                    for (uint64_t a = wmk[tl]; a; a &= a - 1) yy += e[__ffsll((unsigned long long)a) - 1 - wb];
                     Y = act ? yy : INFINITY;
                 }
             }
@@ -395,7 +450,8 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
 
 namespace {
 struct SubsetWs {
-    uint32_t *io, *lmk;
+    uint2 *io;
+    uint64_t *wmk;
     EnumJob *jobs;
     size_t bytes;
 };
@@ -410,8 +466,8 @@ SubsetWs subset_ws(const EnumPlan &p, void *ws) {
         off += bytes;
         return ptr;
     };
-    W.io = (uint32_t *)take((size_t)p.nent * 4);
-    W.lmk = (uint32_t *)take((size_t)p.nent * 4);
+    W.io = (uint2 *)take((size_t)p.nent * 8);
+    W.wmk = (uint64_t *)take((size_t)p.nent * 8);
     W.jobs = (EnumJob *)take((size_t)p.njobs * sizeof(EnumJob));
     W.bytes = align_up(off, 256);
     return W;
@@ -437,7 +493,7 @@ hipError_t launch_best_subset(const fw_rows &rows, int k, int32_t *best_idx, flo
     p.d = (int)rows.d;
     p.G = (int)rows.G;
     const SubsetWs W = subset_ws(p, ws);
-    hipLaunchKernelGGL(enum_plan_kernel, dim3(1), dim3(64), 0, st, p, W.io, W.lmk, W.jobs);
+    hipLaunchKernelGGL(enum_plan_kernel, dim3(1), dim3(64), 0, st, p, W.io, W.wmk, W.jobs);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int nt = kSubsetThreads;
@@ -447,12 +503,12 @@ hipError_t launch_best_subset(const fw_rows &rows, int k, int32_t *best_idx, flo
     if (rows.dtype == FW_BF16)
         hipLaunchKernelGGL(best_subset_kernel<uint16_t>, dim3(R), dim3(nt), L.total, st,
                            (const uint16_t *)rows.q, (const uint16_t *)rows.k, (const uint16_t *)rows.v,
-                           rows.scale, rows.bias, p, W.io, W.lmk, W.jobs, best_idx, best_gap, topk_gap,
+                           rows.scale, rows.bias, p, W.io, W.wmk, W.jobs, best_idx, best_gap, topk_gap,
                            closed, dropped_topk, topk_idx);
     else
         hipLaunchKernelGGL(best_subset_kernel<float>, dim3(R), dim3(nt), L.total, st,
                            (const float *)rows.q, (const float *)rows.k, (const float *)rows.v,
-                           rows.scale, rows.bias, p, W.io, W.lmk, W.jobs, best_idx, best_gap, topk_gap,
+                           rows.scale, rows.bias, p, W.io, W.wmk, W.jobs, best_idx, best_gap, topk_gap,
                            closed, dropped_topk, topk_idx);
     return hipGetLastError();
 }

@@ -38,7 +38,7 @@ swap_small_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__r
     double *redd = R + n;                   // NT
     uint64_t *redm = (uint64_t *)(redd + blockDim.x);  // NT
     int *lists = (int *)(redm + blockDim.x);           // n
-    float *Vs = (float *)(lists + n + (n & 1));        // n*d
+    float *Vs = (float *)(lists + n + (n & 1));        // n*(d+1)
     const int tid = threadIdx.x, NT = blockDim.x;
     const int64_t r = blockIdx.x, h = r / G;
     const T *qr = q + r * d;
@@ -638,7 +638,7 @@ bool swap_mfma_ok(const fw_rows &rows) {
 
 size_t small_lds(int n, int d, int nt) {
     size_t b = (size_t)n * n * 8 + (size_t)n * 8 * 3 + (size_t)d * 8 + (size_t)nt * 16;
-    b += (size_t)(n + (n & 1)) * 4 + (size_t)n * d * 4;
+    b += (size_t)(n + (n & 1)) * 4 + (size_t)n * instance_pitch(d) * 4;
     return b;
 }
 
