@@ -69,7 +69,8 @@ constexpr uint64_t kPadMask = ~(uint64_t)0;  // walk-table mask of a padding ste
 // walk.
 __host__ __device__ inline double job_cost(int wn, int ws, int ln, int ls) {
     const double steps = (double)binom(wn, ws);
-    double setup = 40.0 + 6.0 * ln + 6.0 * ls * ls;
+    double setup = 40.0 + 6.0 * ls * ls;  // the owned part comes from a table
+    (void)ln;
     if (ws > 0) setup += ls * (1.5 * wn + 8.0) + 3.0 * wn;
     return setup + 10.0 * steps;
 }
@@ -109,7 +110,7 @@ __host__ __device__ inline bool plan_for(int n, int k, int m, EnumPlan *P, doubl
         njobs += (uint64_t)ceil64(binom(c.ln, c.ls));
         p.cls[p.ncls++] = c;
     }
-    if (nent > (uint64_t)kMaxEntries || njobs > (1u << 22)) return false;
+    if (nent > (uint64_t)kMaxEntries || njobs > (1u << 17)) return false;
     p.nent = (int)nent;
     p.njobs = (int)njobs;
     *P = p;
@@ -139,7 +140,7 @@ struct EnumJob {
 };
 
 struct SubsetLds {
-    size_t gm, pz, mu, ent, pl, vs, pas, red, ctr, total;
+    size_t gm, pz, mu, ent, pl, vs, red, ctr, total;
 };
 
 __host__ __device__ inline SubsetLds subset_lds(int n, int d, int k, int nent, int nt) {
@@ -156,7 +157,6 @@ __host__ __device__ inline SubsetLds subset_lds(int n, int d, int k, int nent, i
     L.ent = region;
     L.pl = region + (size_t)nent * 16;
     L.vs = region;
-    L.pas = take((size_t)(n + 1) * (k + 1) * 4);
     L.red = take((size_t)nt * 16);
     L.ctr = take(16);
     L.total = o;
@@ -225,12 +225,33 @@ __global__ void enum_plan_kernel(EnumPlan p, uint2 *io, uint64_t *wmk, EnumJob *
     }
 }
 
+// Owned parts (row independent): job j, lane l holds the colex rank
+// start + l among the ls-subsets of [lb, lb + ln), as a key mask.
+__global__ void __launch_bounds__(64) enum_owned_kernel(EnumPlan p, const EnumJob *jobs, uint64_t *omk) {
+    const int j = blockIdx.x, lane = threadIdx.x;
+    const EnumJob jb = jobs[j];
+    const EnumClass &C = p.cls[jb.cls];
+    uint64_t m = 0;
+    if (lane < jb.lanes) {
+        uint64_t rr = (uint64_t)jb.start + lane;
+        int c = C.ln - 1;
+        for (int sz = C.ls; sz >= 1; --sz) {
+            while (binom(c, sz) > rr) --c;
+            m |= 1ull << (C.lb + c);
+            rr -= binom(c, sz);
+            --c;
+        }
+    }
+    omk[(size_t)j * 64 + lane] = m;
+}
+
 template <typename T>
 __global__ void __launch_bounds__(kSubsetThreads)
 best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
                    const float *__restrict__ scale, const float *__restrict__ bias, EnumPlan pl,
                    const uint2 *__restrict__ g_io, const uint64_t *__restrict__ g_wmk,
-                   const EnumJob *__restrict__ g_jobs, int32_t *best_idx, float *best_gap,
+                   const EnumJob *__restrict__ g_jobs, const uint64_t *__restrict__ g_omk,
+                   int32_t *best_idx, float *best_gap,
                    float *topk_gap, float *closed, float *dropped_topk, int32_t *topk_idx) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int NT = blockDim.x;
@@ -243,7 +264,6 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
     double2 *ent = (double2 *)(smem + L.ent);  // (S_L, p(L)^2)
     double *PLt = (double *)(smem + L.pl);     // p(L)
     float *Vs = (float *)(smem + L.vs);
-    uint32_t *pas = (uint32_t *)(smem + L.pas);  // C(c, s), c <= n, s <= k (saturated)
     double *redd = (double *)(smem + L.red);
     uint64_t *redm = (uint64_t *)(redd + NT);
     int *ctr = (int *)(smem + L.ctr);
@@ -275,10 +295,6 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
         ent[t] = make_double2(S, P * P);
         PLt[t] = P;
     }
-    for (int e = tid; e < (n + 1) * (kk + 1); e += NT) {
-        const uint64_t b = binom(e / (kk + 1), e % (kk + 1));
-        pas[e] = b > 0x7FFFFFFFull ? 0x7FFFFFFFu : (uint32_t)b;
-    }
     if (tid == 0) ctr[0] = 0;
     __syncthreads();
 
@@ -299,21 +315,10 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
         if (jn >= pl.njobs) break;
         const EnumJob jb = g_jobs[jn];
         const EnumClass C = pl.cls[jb.cls];
-        const int wb = C.wb, wn = C.wn, ls = C.ls;
+        const int wb = C.wb, wn = C.wn;
         const bool act = lane < jb.lanes;
-        // owned part of this lane: colex rank start + lane among ls-subsets of
-        // [lb, lb + ln)
-        uint64_t Om = 0;
-        if (act) {
-            uint32_t rr = (uint32_t)(jb.start + lane);
-            int c = C.ln - 1;
-            for (int sz = ls; sz >= 1; --sz) {
-                while (pas[c * (kk + 1) + sz] > rr) --c;
-                Om |= 1ull << (C.lb + c);
-                rr -= pas[c * (kk + 1) + sz];
-                --c;
-            }
-        }
+        // owned part of this lane (precomputed key mask; 0 on idle lanes)
+        const uint64_t Om = g_omk[(size_t)jn * 64 + lane];
         double PO = 0.0, SO = 0.0;
         for (uint64_t a = Om; a; a &= a - 1) {
             const int x = __ffsll((unsigned long long)a) - 1;
@@ -411,12 +416,24 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
             }
         }
     }
-    // workgroup argmin with the lexicographic tie rule
-    redd[tid] = best_val;
-    redm[tid] = best_mask;
+    // workgroup argmin with the lexicographic tie rule: within each wave by
+    // shuffles, then over the waves
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const double ov = __shfl_xor(best_val, off);
+        const uint64_t om = __shfl_xor(best_mask, off);
+        if (ov < best_val || (ov == best_val && lex_less(om, best_mask))) {
+            best_val = ov;
+            best_mask = om;
+        }
+    }
+    if (lane == 0) {
+        redd[tid >> 6] = best_val;
+        redm[tid >> 6] = best_mask;
+    }
     __syncthreads();
     if (tid == 0) {
-        for (int i = 1; i < NT; ++i) {
+        for (int i = 1; i < NT / 64; ++i) {
             if (redd[i] < redd[0] || (redd[i] == redd[0] && lex_less(redm[i], redm[0]))) {
                 redd[0] = redd[i];
                 redm[0] = redm[i];
@@ -453,6 +470,7 @@ struct SubsetWs {
     uint2 *io;
     uint64_t *wmk;
     EnumJob *jobs;
+    uint64_t *omk;
     size_t bytes;
 };
 
@@ -469,6 +487,7 @@ SubsetWs subset_ws(const EnumPlan &p, void *ws) {
     W.io = (uint2 *)take((size_t)p.nent * 8);
     W.wmk = (uint64_t *)take((size_t)p.nent * 8);
     W.jobs = (EnumJob *)take((size_t)p.njobs * sizeof(EnumJob));
+    W.omk = (uint64_t *)take((size_t)p.njobs * 64 * 8);
     W.bytes = align_up(off, 256);
     return W;
 }
@@ -494,6 +513,8 @@ hipError_t launch_best_subset(const fw_rows &rows, int k, int32_t *best_idx, flo
     p.G = (int)rows.G;
     const SubsetWs W = subset_ws(p, ws);
     hipLaunchKernelGGL(enum_plan_kernel, dim3(1), dim3(64), 0, st, p, W.io, W.wmk, W.jobs);
+    hipLaunchKernelGGL(enum_owned_kernel, dim3((unsigned)p.njobs), dim3(64), 0, st, p,
+                       (const EnumJob *)W.jobs, W.omk);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int nt = kSubsetThreads;
@@ -503,12 +524,12 @@ hipError_t launch_best_subset(const fw_rows &rows, int k, int32_t *best_idx, flo
     if (rows.dtype == FW_BF16)
         hipLaunchKernelGGL(best_subset_kernel<uint16_t>, dim3(R), dim3(nt), L.total, st,
                            (const uint16_t *)rows.q, (const uint16_t *)rows.k, (const uint16_t *)rows.v,
-                           rows.scale, rows.bias, p, W.io, W.wmk, W.jobs, best_idx, best_gap, topk_gap,
+                           rows.scale, rows.bias, p, W.io, W.wmk, W.jobs, W.omk, best_idx, best_gap, topk_gap,
                            closed, dropped_topk, topk_idx);
     else
         hipLaunchKernelGGL(best_subset_kernel<float>, dim3(R), dim3(nt), L.total, st,
                            (const float *)rows.q, (const float *)rows.k, (const float *)rows.v,
-                           rows.scale, rows.bias, p, W.io, W.wmk, W.jobs, best_idx, best_gap, topk_gap,
+                           rows.scale, rows.bias, p, W.io, W.wmk, W.jobs, W.omk, best_idx, best_gap, topk_gap,
                            closed, dropped_topk, topk_idx);
     return hipGetLastError();
 }
