@@ -179,12 +179,19 @@ def main():
         ms, _ = _time(torch, step, max(1, a.steps // 5), 1)
         subsets = r.H * r.G * math.comb(r.n, wl.k)
         sps = subsets / (ms / 1e3)
-        ops = 4 * sps  # four VALU lane-ops per subset in the walk's inner step
+        # the walk's work per subset: two adds for the running sum, one
+        # multiply-add and one add for the test value, one compare (float64
+        # VALU lane-ops); peak = 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+        ops = 5 * sps
         components.append({"workload": wl.name, "metric": "subsets evaluated/s", "value": round(sps, 1),
                            "unit": "subsets/s", "ms": round(ms, 3), "subsets": subsets,
                            "dtype": "f64",
-                           "roofline": _roofline("alu", ops / 1e12, round(VALU_LANE_OPS / 1e12, 2),
-                                                 "TOP/s")})
+                           "roofline": dict(_roofline("alu", ops / 1e12, round(VALU_LANE_OPS / 1e12, 2),
+                                                      "TOP/s"), kernel="best_subset_kernel",
+                                            ops_per_subset=5),
+                           # context: the direct d-dimensional update costs 3d + 6 flops
+                           # per subset; the Gram form does the same search in 5 ops
+                           "d_dim_equivalent_tflops": round(sps * (3 * r.d + 6) / 1e12, 1)})
         del dev, ws
         torch.cuda.empty_cache()
 
