@@ -30,6 +30,13 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+template <bool B>
+struct BoolTag {
+    static constexpr bool value = B;
+};
 
 namespace {
 constexpr int FR = 16;        // rows per workgroup
@@ -91,10 +98,12 @@ __host__ __device__ inline FusedLds fused_lds(int nk, int n) {
     return L;
 }
 
-__device__ __forceinline__ uint16_t f2bf_rne(float f) {
-    uint32_t u = __float_as_uint(f);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
+// 0xFFFF in each 16-bit half of x (two 2-bit tier codes) whose code is at
+// most kk, else 0: packed 16-bit subtract, then the sign spread by an
+// arithmetic shift
+__device__ __forceinline__ uint32_t codes_le(uint32_t x, int kk) {
+    const s16x2 d = __builtin_bit_cast(s16x2, x) - (s16x2)(short)(kk + 1);
+    return __builtin_bit_cast(uint32_t, d >> (s16x2)(short)15);
 }
 // reductions over the four lanes of a wave that share a row (l, l^16, l^32, l^48)
 __device__ __forceinline__ float rmax4(float v) {
@@ -145,6 +154,15 @@ __device__ __forceinline__ void wait_vm(int n) {
 }
 #undef FW_VM
 __device__ __forceinline__ void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Workgroup barrier that orders LDS only.  Every barrier of the fused kernel
+// separates LDS writes from LDS reads (the direct-to-LDS loads are per wave
+// and waited for by that wave); a full __syncthreads would also wait for every
+// outstanding global store of the wave, exposing write latency at each one.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 }  // namespace
 
 struct FusedArgs {
@@ -281,7 +299,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
             WRED(1, w, rl) = mn;
         }
     }
-    __syncthreads();
+    lds_barrier();
     float m = WRED(0, 0, rl), zmin = WRED(1, 0, rl);
 #pragma unroll
     for (int ww = 1; ww < FW; ++ww) {
@@ -304,7 +322,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
     }
     for (int e = tid; e < FR * FBINS; e += FTH) hist[e] = 0;
     for (int e = tid; e < FR * 8; e += FTH) cntr[e] = 0;
-    __syncthreads();
+    lds_barrier();
     float lsum = 0.f;
 #pragma unroll
     for (int ww = 0; ww < FW; ++ww) lsum += WRED(2, ww, rl);
@@ -323,7 +341,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
         }
         FW_TILE_FENCE();
     }
-    __syncthreads();
+    lds_barrier();
     // wave w scans rows 2w, 2w+1; lane owns bins [16 lane, 16 lane + 16)
     for (int rr = 0; rr < FR / FW; ++rr) {
         const int r = (FR / FW) * w + rr;
@@ -353,7 +371,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
             }
         }
     }
-    __syncthreads();
+    lds_barrier();
     {
         // logits in the threshold bin of some budget (a few per row): one
         // branch per logit, one LDS atomic per appended key
@@ -383,7 +401,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
             FW_TILE_FENCE();
         }
     }
-    __syncthreads();
+    lds_barrier();
     // the need-th largest entry of each (row, budget) list, within one wave:
     // rank by counting for lists of up to 64 entries, else a bitonic sort of
     // two entries per lane (entries are distinct: the low word is the index)
@@ -392,6 +410,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
         const int cnt = cntr[r * 8 + kk];
         const int need = THR(r, kk, 1);
         unsigned long long sel = 0ull;
+        bool tied = false;  // another logit of the row equals the threshold logit
         if (cnt <= 64) {
             const unsigned long long e = (lane < cnt) ? lists[li * FCAP + lane] : 0ull;
             int rank = 0;
@@ -405,6 +424,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
             const int f = bal ? __ffsll(bal) - 1 : 0;
             sel = ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(e >> 32), f) << 32) |
                   (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)e, f);
+            tied = __popcll(__ballot(lane < cnt && (uint32_t)(e >> 32) == (uint32_t)(sel >> 32))) > 1;
         } else {
             unsigned long long e0 = (lane < cnt) ? lists[li * FCAP + lane] : 0ull;
             unsigned long long e1 = (lane + 64 < cnt) ? lists[li * FCAP + lane + 64] : 0ull;
@@ -428,14 +448,18 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
             const int x = (need - 1) & 127;
             const unsigned long long v0 = __shfl(e0, x & 63), v1 = __shfl(e1, x & 63);
             sel = (x < 64) ? v0 : v1;
+            // finite logits have keys above zero, so the zero padding never matches
+            const uint32_t sk = (uint32_t)(sel >> 32);
+            tied = __popcll(__ballot((uint32_t)(e0 >> 32) == sk)) + __popcll(__ballot((uint32_t)(e1 >> 32) == sk)) > 1;
         }
         if (lane == 0) {
             THR(r, kk, 0) = (int)(uint32_t)(sel >> 32);
+            THR(r, kk, 2) = tied ? 1 : 0;
             THR(r, kk, 1) = (int)(0xFFFFFFFFu - (uint32_t)(sel & 0xFFFFFFFFull));
             THR(r, kk, 3) = (cnt > FCAP || need < 1 || need > cnt) ? 1 : 0;
         }
     }
-    __syncthreads();
+    lds_barrier();
     uint32_t tkey[NK];
     int tcut[NK];
     bool bad = degenerate;
@@ -481,54 +505,61 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
             }
         }
     }
-    // tiers (2 bits per logit, 4 tiles per word) and bf16 weights packed in
-    // pairs: from here the lane keeps 3/4 fewer registers for its keys
+    // tiers (2 bits per logit) and bf16 weights packed in pairs: from here
+    // the lane keeps 3/4 fewer registers for its keys.  Word TB[t / 4] holds
+    // tiles 4 (t / 4) .. + 3; key i of tile t sits at bit
+    // 16 (i % 2) + 2 (2 (t % 4) + i / 2), so one shift brings the codes of a
+    // pair of keys to the low bits of the two 16-bit halves.
     uint32_t TB[(TILES + 3) / 4];
     uint32_t P2[TILES][2];
     // thresholds as floats: ord_key order equals float order for finite
     // logits (both identify -0 with +0), and compares on S itself share no
     // work with the selection passes above
     float tf[NK];
+    int tied = 0;
 #pragma unroll
     for (int kk = 0; kk < NK; ++kk) {
         tf[kk] = opaque(key_to_float(tkey[kk]));
         tcut[kk] = opaque(tcut[kk]);
+        tied |= THR(rl, kk, 2);
     }
-    const float m3 = opaque(m), il3 = opaque(inv_l);
-    float mass[NT];
+    const float mL3 = -opaque(m) * LOG2E, il3 = opaque(inv_l);
+    // The budgets' sets are nested: a key's tier is the number of sets that
+    // leave it out.  Where no other logit of the row equals a threshold logit
+    // (the usual case), membership is one compare, logit >= threshold;
+    // otherwise the index decides among the equal logits.
+    auto tier_pass = [&](auto exact_tag) {
+        constexpr bool EXACT = decltype(exact_tag)::value;
 #pragma unroll
-    for (int tt = 0; tt < NT; ++tt) mass[tt] = 0.f;
+        for (int t = 0; t < TILES; ++t) {
+            if ((t & 3) == 0) TB[t >> 2] = 0;
+            float pv[4];
 #pragma unroll
-    for (int t = 0; t < TILES; ++t) {
-        if ((t & 3) == 0) TB[t >> 2] = 0;
-        uint32_t pbits[4];
+            for (int i = 0; i < 4; ++i) {
+                const float s = S[t][i];
+                int tier = NK;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int j = kw0 + 16 * t + 4 * grp + i;
-            const float s = S[t][i];
-            // the budgets' sets are nested: the tier is the number of sets
-            // that leave the key out (bitwise predicates keep this branch-free)
-            int tier = NK;
-#pragma unroll
-            for (int kk = 0; kk < NK; ++kk)
-                tier -= (int)(s > tf[kk]) | ((int)(s == tf[kk]) & (int)(j <= tcut[kk]));
-            TB[t >> 2] |= (uint32_t)tier << (8 * (t & 3) + 2 * i);
-            pbits[i] = f2bf_rne(__builtin_amdgcn_exp2f((S[t][i] - m3) * LOG2E) * il3);
-            const float pr = __uint_as_float(pbits[i] << 16);
-#pragma unroll
-            for (int tt = 0; tt < NT; ++tt) mass[tt] += (tier == tt) ? pr : 0.f;
+                for (int kk = 0; kk < NK; ++kk) {
+                    if (EXACT) {
+                        const int j = kw0 + 16 * t + 4 * grp + i;
+                        tier -= (int)(s > tf[kk]) | ((int)(s == tf[kk]) & (int)(j <= tcut[kk]));
+                    } else {
+                        tier -= (int)(s >= tf[kk]);
+                    }
+                }
+                TB[t >> 2] |= (uint32_t)tier << (16 * (i & 1) + 2 * (2 * (t & 3) + (i >> 1)));
+                pv[i] = __builtin_amdgcn_exp2f(fmaf(s, LOG2E, mL3)) * il3;
+            }
+            // round to bf16 (nearest even) in pairs: the weights the tier
+            // products and masses use
+            P2[t][0] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){pv[0], pv[1]}, bf16x2));
+            P2[t][1] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){pv[2], pv[3]}, bf16x2));
+            FW_TILE_FENCE();
         }
-        P2[t][0] = pbits[0] | (pbits[1] << 16);
-        P2[t][1] = pbits[2] | (pbits[3] << 16);
-        FW_TILE_FENCE();
-    }
-#pragma unroll
-    for (int tt = 0; tt < NT; ++tt) mass[tt] = rsum4(mass[tt]);
-    __syncthreads();  // selection buffers are dead from here
-    if (grp == 0) {
-#pragma unroll
-        for (int tt = 0; tt < NT; ++tt) WRED(tt, w, rl) = mass[tt];
-    }
+    };
+    if (__ballot(tied != 0)) tier_pass(BoolTag<true>{});
+    else tier_pass(BoolTag<false>{});
+    lds_barrier();  // selection buffers are dead from here
 
     // ---- 4./5. tier products per DQ columns of d, then the epilogue -------
     const rsrc_t vres = make_rsrc(a.v + h * (int64_t)n * FD, (uint32_t)n * FD * 2);
@@ -547,6 +578,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
         vrd[dt] = (uint32_t)(((4 * grp + cr) * DQ + ((2 * dt + (cq >> 1)) ^ (4 * (grp & 1) + cr)) * 8 + 4 * (cq & 1)) * 2);
+    const bf16x8 ones = __builtin_bit_cast(bf16x8, (s16x8){0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80});
     const int er = tid >> 5, ec = (tid & 31) * CPT;  // epilogue: row, CPT columns of the pass
     const int64_t R = a.H * a.G;
     for (int pass = 0; pass < NPASS; ++pass) {
@@ -554,11 +586,13 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
         // keeps them from being hoisted out of this loop for every block
         // at once (256 values), which would spill
         const uint32_t pz = opaque(0u);
-        f32x4 acc[DT][NT];
+        f32x4 acc[DT][NT], accm[NT];
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
+        for (int tt = 0; tt < NT; ++tt) {
+            accm[tt] = (f32x4){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int tt = 0; tt < NT; ++tt) acc[dt][tt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+            for (int dt = 0; dt < DT; ++dt) acc[dt][tt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+        }
         // V block b (32 keys x DQ columns, 2 DQ bytes per key, swizzled) in
         // ring slot b % VD, VD - 1 blocks ahead of the MFMAs
         constexpr int NB = TILES / 2;
@@ -577,20 +611,26 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
             const int after = (NB - 1 - blk < VD - 1) ? NB - 1 - blk : VD - 1;
             wait_vm(VLQ * after);
             // P^T operands: slots 0..3 = tile 2 blk, slots 4..7 = tile 2 blk + 1,
-            // zero where the key is in another tier
+            // zero where the key is in another tier.  The nested sets' copies
+            // N_kk (keys of tier <= kk) are masks of the packed pair; the tiers
+            // are their differences, exact as 32-bit integers since each half
+            // of a word is either the weight or zero in all of them
             uint32_t pw[NT][4];
 #pragma unroll
             for (int hf = 0; hf < 2; ++hf) {
                 const int t = 2 * blk + hf;
-                const uint32_t tb2 = ((TB[t >> 2] ^ pz) >> (8 * (t & 3))) & 0xFFu;
 #pragma unroll
                 for (int pr = 0; pr < 2; ++pr) {
-                    const uint32_t t0 = (tb2 >> (4 * pr)) & 3u, t1 = (tb2 >> (4 * pr + 2)) & 3u;
+                    const uint32_t x = ((TB[t >> 2] ^ pz) >> (2 * (2 * (t & 3) + pr))) & 0x00030003u;
+                    const uint32_t pp = P2[t][pr];
+                    uint32_t prev = 0u;
 #pragma unroll
-                    for (int tt = 0; tt < NT; ++tt) {
-                        const uint32_t mask = (t0 == (uint32_t)tt ? 0x0000FFFFu : 0u) | (t1 == (uint32_t)tt ? 0xFFFF0000u : 0u);
-                        pw[tt][2 * hf + pr] = P2[t][pr] & mask;
+                    for (int kk = 0; kk < NK; ++kk) {
+                        const uint32_t nk = pp & codes_le(x, kk);
+                        pw[kk][2 * hf + pr] = nk - prev;
+                        prev = nk;
                     }
+                    pw[NK][2 * hf + pr] = pp - prev;
                 }
             }
             s16x8 pb[NT];
@@ -630,9 +670,18 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
                     acc[dt][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                         vbf, __builtin_bit_cast(bf16x8, pb[tt]), acc[dt][tt], 0, 0, 0);
             }
+            // tier masses: the same operands against a block of ones
+#pragma unroll
+            for (int tt = 0; tt < NT; ++tt)
+                accm[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, __builtin_bit_cast(bf16x8, pb[tt]), accm[tt], 0, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
         }
-        __syncthreads();  // the rings are dead; partial sums overlay them
+        // every lane of a row holds that row's masses over this wave's keys
+        if (pass == 0 && grp == 0) {
+#pragma unroll
+            for (int tt = 0; tt < NT; ++tt) WRED(tt, w, rl) = accm[tt][0];
+        }
+        lds_barrier();  // the rings are dead; partial sums overlay them
         // acc[dt][tt][i] = O^T[d = DQ pass + 16 dt + 4 grp + i][row rl] over this
         // wave's keys; stored [wave][tier][row][column], rows DQ + 4 floats
         // apart, so that the epilogue's column reads are contiguous
@@ -642,7 +691,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
 #pragma unroll
             for (int tt = 0; tt < NT; ++tt)
                 *(f32x4 *)&opart[(((size_t)w * NT + tt) * FR + rl) * OP + 16 * dt + 4 * grp] = acc[dt][tt];
-        __syncthreads();
+        lds_barrier();
         {
             float M[NT];
             float mtot = 0.f;
@@ -664,17 +713,22 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
                     for (int ww = 0; ww < FW; ++ww) s += opart[(((size_t)ww * NT + tt) * FR + er) * OP + ec + c];
                     T[tt][c] = s;
                 }
-            const int64_t row = row0 + er;
             const float inv_tot = 1.0f / mtot;
+            // outputs through a wave-uniform base (this tile's first row) and a
+            // 32-bit byte offset: no per-lane 64-bit addresses to keep alive
+            static_assert(CPT == 2, "two columns per lane and pass");
             const int col = DQ * pass + ec;
+            const uint32_t eo = (uint32_t)((er * FD + col) * 4);
             if (a.o) {
+                f32x2 ov;
 #pragma unroll
                 for (int c = 0; c < CPT; ++c) {
                     float s = 0.f;
 #pragma unroll
                     for (int tt = 0; tt < NT; ++tt) s += T[tt][c];
-                    a.o[row * FD + col + c] = s * inv_tot;
+                    ov[c] = s * inv_tot;
                 }
+                *(f32x2 *)((char *)(a.o + row0 * FD) + eo) = ov;
             }
 #pragma unroll
             for (int kk = 0; kk < NK; ++kk) {
@@ -683,7 +737,9 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
                 for (int tt = 0; tt < NT; ++tt) {
                     if (tt <= kk) km += M[tt]; else rm += M[tt];
                 }
+                const float ikm = 1.0f / km, irm = (rm > 0.f) ? 1.0f / rm : 0.f;
                 float ss = 0.f;
+                f32x2 osv;
 #pragma unroll
                 for (int c = 0; c < CPT; ++c) {
                     float kt = 0.f, rt2 = 0.f;
@@ -691,25 +747,27 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
                     for (int tt = 0; tt < NT; ++tt) {
                         if (tt <= kk) kt += T[tt][c]; else rt2 += T[tt][c];
                     }
-                    const float oS = kt / km;
-                    if (a.o_s) a.o_s[((int64_t)a.ks.perm[kk] * R + row) * FD + col + c] = oS;
+                    const float oS = kt * ikm;
+                    osv[c] = oS;
                     if (rm > 0.f) {
-                        const float diff = rt2 / rm - oS;
+                        const float diff = rt2 * irm - oS;
                         ss = fmaf(diff, diff, ss);
                     }
                 }
+                const int64_t plane = (int64_t)a.ks.perm[kk] * R + row0;
+                if (a.o_s) *(f32x2 *)((char *)(a.o_s + plane * FD) + eo) = osv;
 #pragma unroll
                 for (int off = 1; off < 32; off <<= 1) ss += __shfl_xor(ss, off);
                 if ((tid & 31) == 0) ssb[(pass * FR + er) * 4 + kk] = ss;
                 if (pass == NPASS - 1 && (tid & 31) == 0) {
                     float st = ss;
                     for (int pp = 0; pp < NPASS - 1; ++pp) st += ssb[(pp * FR + er) * 4 + kk];
-                    a.gap[(int64_t)a.ks.perm[kk] * R + row] = (rm > 0.f) ? (rm * inv_tot) * sqrtf(st) : 0.f;
-                    a.dropped[(int64_t)a.ks.perm[kk] * R + row] = rm * inv_tot;
+                    a.gap[plane + er] = (rm > 0.f) ? (rm * inv_tot) * sqrtf(st) : 0.f;
+                    a.dropped[plane + er] = rm * inv_tot;
                 }
             }
         }
-        __syncthreads();
+        lds_barrier();
     }
 #undef WRED
 #undef THR

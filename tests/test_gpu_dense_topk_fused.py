@@ -107,3 +107,32 @@ def test_fused_matches_general_path(torch_fw):
     ia, ib = t2np(a["topk_idx"]), t2np(b["topk_idx"])[..., :1024]
     same = np.mean([len(np.intersect1d(x, y)) / 1024 for x, y in zip(ia.reshape(-1, 1024), ib.reshape(-1, 1024))])
     assert same > 0.995
+
+
+def test_fused_tied_threshold_logits(torch_fw):
+    """Unit 0 stores every key twice (keys 2j and 2j + 1 equal), so with odd
+    budgets the threshold logit's equal twin is left out by index alone (the
+    exact tier rule); unit 1 keeps distinct logits (one compare per budget).
+    Both stay on the fused path (a threshold bin holds a few dozen logits).
+    Channel 0 of V is +64 on even keys and -64 on odd ones, so a twin wrongly
+    kept or dropped moves o_S far beyond tolerance; and a selected key 2j + 1
+    implies that its twin 2j, equal in logit and lower in index, is selected."""
+    torch, fw = torch_fw
+    ks = (127, 511, 999)
+    wl = W.streaming_topk(seed=15, layers=1, kv_heads=2, q_per_kv=2, rows_per_q=8, n=2048, d=128, ks=ks)
+    r = wl.rows
+    k, v = r.k.copy(), r.v.copy()
+    k[0, 1::2] = k[0, 0::2]
+    v[0, 0::2, 0] = W.bf16_bits(np.float32(64.0))
+    v[0, 1::2, 0] = W.bf16_bits(np.float32(-64.0))
+    rows = W.Rows(r.dtype, r.q, k, v, r.scale, r.bias)
+    out = _run(torch, fw, rows, ks)
+    ref = _oracle_rows(rows, ks)
+    t = _compare(rows, ks, out, ref, torch)
+    print("tied thresholds:", t)
+    idx = t2np(out["topk_idx"])
+    for g in range(rows.G):
+        for kv in ks:
+            sel = set(idx[0, g, :kv].tolist())
+            odd = [j for j in sel if j % 2 == 1 and j > 1]
+            assert all(j - 1 in sel for j in odd), (g, kv)
