@@ -33,10 +33,6 @@ typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef short s16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-template <bool B>
-struct BoolTag {
-    static constexpr bool value = B;
-};
 
 namespace {
 constexpr int FR = 16;        // rows per workgroup
@@ -45,6 +41,7 @@ constexpr int FTH = FW * 64;  // threads per workgroup
 constexpr int FD = 128;       // head dimension
 constexpr int FBINS = 1024;   // histogram bins per row
 constexpr int FCAP = 128;     // logits gathered from the threshold bin
+constexpr int FIXCAP = 32;    // per row: logits equal to a threshold logit, past its index
 constexpr float LOG2E = 1.4426950408889634f;
 // keeps the scheduler from hoisting the work of every tile of an unrolled
 // per-logit loop at once (which exhausts the register file)
@@ -64,7 +61,7 @@ constexpr int KD = 4;         // K tiles (16 keys x 128 d, 4 KiB) per ring
 
 struct FusedLds {
     size_t wred, thr, ssb, bias;      // persistent
-    size_t hist, lists, cntr;         // selection
+    size_t hist, lists, cntr, fix;    // selection
     size_t ring;                      // K tiles (phase 1), V blocks (tier products)
     size_t opart;                     // partial tier sums
     size_t total;
@@ -87,7 +84,8 @@ __host__ __device__ inline FusedLds fused_lds(int nk, int n) {
     L.hist = base;
     L.lists = align_up(base + (size_t)FR * FBINS * 4, 16);
     L.cntr = align_up(L.lists + (size_t)FR * nk * FCAP * 8, 16);
-    const size_t sel_end = L.cntr + (size_t)FR * 8 * 4;
+    L.fix = align_up(L.cntr + (size_t)FR * 8 * 4, 16);
+    const size_t sel_end = L.fix + (size_t)FR * FIXCAP * 8;
     L.ring = base;
     const size_t r_end = base + (size_t)FW * RING;
     L.opart = base;
@@ -193,6 +191,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
     int *hist = (int *)(smem + L.hist);
     unsigned long long *lists = (unsigned long long *)(smem + L.lists);
     int *cntr = (int *)(smem + L.cntr);
+    unsigned long long *fixl = (unsigned long long *)(smem + L.fix);
     float *opart = (float *)(smem + L.opart);
 #define WRED(qq, ww, rr) wred[((qq) * FW + (ww)) * FR + (rr)]
 #define THR(rr, kk, ff) thr[((rr) * 4 + (kk)) * 4 + (ff)]
@@ -410,7 +409,25 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
         const int cnt = cntr[r * 8 + kk];
         const int need = THR(r, kk, 1);
         unsigned long long sel = 0ull;
-        bool tied = false;  // another logit of the row equals the threshold logit
+        // Logits equal to the threshold logit but past its index are out of
+        // the set, yet the one-compare tier rule below counts them in: they
+        // are listed per row (entry = key, inverted index) and their tiers
+        // recomputed by the exact rule.  A full list sends the row to the
+        // exact fallback.
+        bool fix_over = false;
+        auto fix_out = [&](unsigned long long e, bool valid) {
+            const uint32_t sk = (uint32_t)(sel >> 32), jc = 0xFFFFFFFFu - (uint32_t)sel;
+            const bool x = valid && (uint32_t)(e >> 32) == sk && (0xFFFFFFFFu - (uint32_t)e) > jc;
+            const unsigned long long bx = __ballot(x);
+            if (bx) {
+                int base = 0;
+                if (lane == 0) base = atomicAdd(&cntr[r * 8 + 6], __popcll(bx));
+                base = __shfl(base, 0);
+                const int pos = base + __popcll(bx & ((1ull << lane) - 1ull));
+                if (x && pos < FIXCAP) fixl[r * FIXCAP + pos] = e;
+                fix_over |= base + __popcll(bx) > FIXCAP;
+            }
+        };
         if (cnt <= 64) {
             const unsigned long long e = (lane < cnt) ? lists[li * FCAP + lane] : 0ull;
             int rank = 0;
@@ -424,7 +441,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
             const int f = bal ? __ffsll(bal) - 1 : 0;
             sel = ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(e >> 32), f) << 32) |
                   (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)e, f);
-            tied = __popcll(__ballot(lane < cnt && (uint32_t)(e >> 32) == (uint32_t)(sel >> 32))) > 1;
+            fix_out(e, lane < cnt);
         } else {
             unsigned long long e0 = (lane < cnt) ? lists[li * FCAP + lane] : 0ull;
             unsigned long long e1 = (lane + 64 < cnt) ? lists[li * FCAP + lane + 64] : 0ull;
@@ -449,14 +466,13 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
             const unsigned long long v0 = __shfl(e0, x & 63), v1 = __shfl(e1, x & 63);
             sel = (x < 64) ? v0 : v1;
             // finite logits have keys above zero, so the zero padding never matches
-            const uint32_t sk = (uint32_t)(sel >> 32);
-            tied = __popcll(__ballot((uint32_t)(e0 >> 32) == sk)) + __popcll(__ballot((uint32_t)(e1 >> 32) == sk)) > 1;
+            fix_out(e0, true);
+            fix_out(e1, true);
         }
         if (lane == 0) {
             THR(r, kk, 0) = (int)(uint32_t)(sel >> 32);
-            THR(r, kk, 2) = tied ? 1 : 0;
             THR(r, kk, 1) = (int)(0xFFFFFFFFu - (uint32_t)(sel & 0xFFFFFFFFull));
-            THR(r, kk, 3) = (cnt > FCAP || need < 1 || need > cnt) ? 1 : 0;
+            THR(r, kk, 3) = (cnt > FCAP || need < 1 || need > cnt || fix_over) ? 1 : 0;
         }
     }
     lds_barrier();
@@ -516,49 +532,61 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
     // logits (both identify -0 with +0), and compares on S itself share no
     // work with the selection passes above
     float tf[NK];
-    int tied = 0;
 #pragma unroll
     for (int kk = 0; kk < NK; ++kk) {
         tf[kk] = opaque(key_to_float(tkey[kk]));
         tcut[kk] = opaque(tcut[kk]);
-        tied |= THR(rl, kk, 2);
     }
     const float mL3 = -opaque(m) * LOG2E, il3 = opaque(inv_l);
     // The budgets' sets are nested: a key's tier is the number of sets that
-    // leave it out.  Where no other logit of the row equals a threshold logit
-    // (the usual case), membership is one compare, logit >= threshold;
-    // otherwise the index decides among the equal logits.
-    auto tier_pass = [&](auto exact_tag) {
-        constexpr bool EXACT = decltype(exact_tag)::value;
+    // leave it out.  Membership is one compare, logit >= threshold; the keys
+    // for which the index decides (listed above) are corrected afterwards.
 #pragma unroll
-        for (int t = 0; t < TILES; ++t) {
-            if ((t & 3) == 0) TB[t >> 2] = 0;
-            float pv[4];
+    for (int t = 0; t < TILES; ++t) {
+        if ((t & 3) == 0) TB[t >> 2] = 0;
+        float pv[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float s = S[t][i];
-                int tier = NK;
+        for (int i = 0; i < 4; ++i) {
+            const float s = S[t][i];
+            int tier = NK;
 #pragma unroll
-                for (int kk = 0; kk < NK; ++kk) {
-                    if (EXACT) {
-                        const int j = kw0 + 16 * t + 4 * grp + i;
-                        tier -= (int)(s > tf[kk]) | ((int)(s == tf[kk]) & (int)(j <= tcut[kk]));
-                    } else {
-                        tier -= (int)(s >= tf[kk]);
-                    }
-                }
-                TB[t >> 2] |= (uint32_t)tier << (16 * (i & 1) + 2 * (2 * (t & 3) + (i >> 1)));
-                pv[i] = __builtin_amdgcn_exp2f(fmaf(s, LOG2E, mL3)) * il3;
-            }
-            // round to bf16 (nearest even) in pairs: the weights the tier
-            // products and masses use
-            P2[t][0] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){pv[0], pv[1]}, bf16x2));
-            P2[t][1] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){pv[2], pv[3]}, bf16x2));
-            FW_TILE_FENCE();
+            for (int kk = 0; kk < NK; ++kk) tier -= (int)(s >= tf[kk]);
+            TB[t >> 2] |= (uint32_t)tier << (16 * (i & 1) + 2 * (2 * (t & 3) + (i >> 1)));
+            pv[i] = __builtin_amdgcn_exp2f(fmaf(s, LOG2E, mL3)) * il3;
         }
-    };
-    if (__ballot(tied != 0)) tier_pass(BoolTag<true>{});
-    else tier_pass(BoolTag<false>{});
+        // round to bf16 (nearest even) in pairs: the weights the tier
+        // products and masses use
+        P2[t][0] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){pv[0], pv[1]}, bf16x2));
+        P2[t][1] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){pv[2], pv[3]}, bf16x2));
+        FW_TILE_FENCE();
+    }
+    {
+        // listed keys: the lane holding key j recomputes its tier with the
+        // index rule (logit above the threshold, or equal and at most its index)
+        const int nf = min(cntr[rl * 8 + 6], FIXCAP);
+        int nmax = nf;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) nmax = max(nmax, __shfl_xor(nmax, off));
+        for (int f = 0; f < nmax; ++f) {
+            if (f < nf) {
+                const unsigned long long e = fixl[rl * FIXCAP + f];
+                const int j = (int)(0xFFFFFFFFu - (uint32_t)e);
+                const int jj = j - kw0 - 4 * grp;  // 16 t + i for a key of this lane
+                if (jj >= 0 && jj < 16 * TILES && (jj & 15) < 4) {
+                    const float s = key_to_float((uint32_t)(e >> 32));
+                    int tier = NK;
+#pragma unroll
+                    for (int kk = 0; kk < NK; ++kk)
+                        tier -= (int)(s > tf[kk]) | ((int)(s == tf[kk]) & (int)(j <= tcut[kk]));
+                    const int t = jj >> 4, i = jj & 3;
+                    const int sh = 16 * (i & 1) + 2 * (2 * (t & 3) + (i >> 1));
+#pragma unroll
+                    for (int x = 0; x < (TILES + 3) / 4; ++x)
+                        if (x == (t >> 2)) TB[x] = (TB[x] & ~(3u << sh)) | ((uint32_t)tier << sh);
+                }
+            }
+        }
+    }
     lds_barrier();  // selection buffers are dead from here
 
     // ---- 4./5. tier products per DQ columns of d, then the epilogue -------
@@ -579,7 +607,6 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
     for (int dt = 0; dt < DT; ++dt)
         vrd[dt] = (uint32_t)(((4 * grp + cr) * DQ + ((2 * dt + (cq >> 1)) ^ (4 * (grp & 1) + cr)) * 8 + 4 * (cq & 1)) * 2);
     const bf16x8 ones = __builtin_bit_cast(bf16x8, (s16x8){0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80});
-    const int er = tid >> 5, ec = (tid & 31) * CPT;  // epilogue: row, CPT columns of the pass
     const int64_t R = a.H * a.G;
     for (int pass = 0; pass < NPASS; ++pass) {
         // the tier operands below do not depend on the pass; an opaque zero
@@ -693,6 +720,11 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
                 *(f32x4 *)&opart[(((size_t)w * NT + tt) * FR + rl) * OP + 16 * dt + 4 * grp] = acc[dt][tt];
         lds_barrier();
         {
+            // epilogue lane: row er, CPT columns from ec; derived from an opaque
+            // copy of the thread index so that nothing here is hoisted out of
+            // the pass loop (and spilled across the products)
+            const int etid = opaque(tid);
+            const int er = etid >> 5, ec = (etid & 31) * CPT;
             float M[NT];
             float mtot = 0.f;
 #pragma unroll
@@ -762,8 +794,9 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
                 if (pass == NPASS - 1 && (tid & 31) == 0) {
                     float st = ss;
                     for (int pp = 0; pp < NPASS - 1; ++pp) st += ssb[(pp * FR + er) * 4 + kk];
-                    a.gap[plane + er] = (rm > 0.f) ? (rm * inv_tot) * sqrtf(st) : 0.f;
-                    a.dropped[plane + er] = rm * inv_tot;
+                    const uint32_t go = (uint32_t)er * 4u;
+                    *(float *)((char *)(a.gap + plane) + go) = (rm > 0.f) ? (rm * inv_tot) * sqrtf(st) : 0.f;
+                    *(float *)((char *)(a.dropped + plane) + go) = rm * inv_tot;
                 }
             }
         }

@@ -130,6 +130,10 @@ def test_fused_tied_threshold_logits(torch_fw):
     ref = _oracle_rows(rows, ks)
     t = _compare(rows, ks, out, ref, torch)
     print("tied thresholds:", t)
+    # the fused workspace starts with one fallback flag per row: none is set
+    R = rows.H * rows.G
+    flags = out["_ws"][: R * 4].view(torch.int32).cpu().numpy()
+    assert not flags.any(), np.nonzero(flags)
     idx = t2np(out["topk_idx"])
     for g in range(rows.G):
         for kv in ks:
