@@ -31,6 +31,15 @@ template <> struct Elem<uint16_t> {
 };
 
 // ---------------------------------------------------------------------------
+// Workgroup barrier that orders LDS accesses only (no wait for outstanding
+// global loads or stores): for barriers that separate LDS writes from LDS
+// reads, where __syncthreads would expose global write latency.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Ordering keys.  ord_key(x) is an unsigned integer that orders like x, with
 // -0 and +0 mapped to the same key.  Top-k ranks by (key descending, index
 // ascending).

@@ -124,67 +124,166 @@ __global__ void window_combine_kernel(int64_t rows, int nchunks, const float *pa
 }
 
 // Pass 4: stable LSD radix sort of one unit's scores, descending (keys are
-// the complement of the order-preserving bits), payload = key index.
+// the complement of the order-preserving bits), payload = key index.  One
+// workgroup per unit; four 8-bit passes.  The digit histograms of all four
+// passes come from one read.  Each pass takes tiles of kSortTile keys, 8 per
+// thread in index order (wave, slot, lane): a key's rank among the equal
+// digits of its wave comes from ballots slot by slot with running per-wave
+// counters, the tile is placed digit-ordered in LDS, and then written out as
+// contiguous runs (coalesced) at the digit's running global offset.
+constexpr int kSortWaves = kSortThreads / 64;
+constexpr int kSortE = 8;
+constexpr int kSortTile = kSortThreads * kSortE;
 __global__ void __launch_bounds__(kSortThreads)
 unit_sort_kernel(const float *__restrict__ importance, int64_t n, uint32_t *keys_a, uint32_t *keys_b,
                  int32_t *vals_a, int32_t *vals_b, int with_vals) {
-    __shared__ int hist[256];
-    __shared__ int base[256];
-    __shared__ int wcnt[kSortThreads / 64][256];
-    const int tid = threadIdx.x, lane = tid % 64, wv = tid / 64;
+    __shared__ int gb[4][256];             // per pass: running global offset of each digit
+    __shared__ int wc[kSortWaves][256];    // per wave: digit counts, then their cross-wave prefix
+    __shared__ int tdp[256], ttot[256];    // tile: digit prefix, digit totals
+    __shared__ uint32_t stk[kSortTile];
+    __shared__ int32_t stv[kSortTile];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int64_t h = blockIdx.x;
+    const float *imp = importance + h * n;
     uint32_t *ka = keys_a + h * n, *kb = keys_b + h * n;
     int32_t *va = vals_a + h * n, *vb = vals_b + h * n;
-    for (int64_t j = tid; j < n; j += kSortThreads) {
-        ka[j] = ~ord_key(importance[h * n + j]);
-        if (with_vals) va[j] = (int32_t)j;
+    const uint64_t below_mask = (1ull << lane) - 1ull;
+    for (int i = tid; i < 4 * 256; i += kSortThreads) (&gb[0][0])[i] = 0;
+    __syncthreads();
+    // (scores of a unit often share their top bytes: a digit common to every
+    // live lane of the wave is added once)
+    for (int64_t j0 = (int64_t)wv * 64; j0 < n; j0 += kSortThreads) {
+        const int64_t j = j0 + lane;
+        const bool live = j < n;
+        const uint32_t key = live ? ~ord_key(imp[j]) : 0u;
+        const uint64_t lv = __ballot(live);
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            const uint32_t d = (key >> (8 * p)) & 255u;
+            const uint32_t d0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)d);
+            if (__ballot(live && d == d0) == lv) {
+                if (lane == 0) atomicAdd(&gb[p][d0], __popcll(lv));
+            } else if (live) {
+                atomicAdd(&gb[p][d], 1);
+            }
+        }
     }
     __syncthreads();
-    for (int shift = 0; shift < 32; shift += 8) {
-        for (int i = tid; i < 256; i += kSortThreads) hist[i] = 0;
-        __syncthreads();
-        for (int64_t j = tid; j < n; j += kSortThreads) atomicAdd(&hist[(ka[j] >> shift) & 255u], 1);
-        __syncthreads();
-        if (tid == 0) {
-            int acc = 0;
-            for (int b = 0; b < 256; ++b) { base[b] = acc; acc += hist[b]; }
-        }
-        __syncthreads();
-        for (int64_t t0 = 0; t0 < n; t0 += kSortThreads) {
-            const int64_t j = t0 + tid;
-            const bool live = j < n;
-            const uint32_t key = live ? ka[j] : 0u;
-            const int dig = live ? (int)((key >> shift) & 255u) : 256;
-            // lanes of this wave holding the same digit
-            uint64_t same = __ballot(live);
+    if (wv < 4) {  // exclusive prefix over the digits, one wave per pass
+        int v[4], sum = 0;
 #pragma unroll
-            for (int b = 0; b < 8; ++b) {
-                const uint64_t bal = __ballot(live && ((dig >> b) & 1));
-                same &= ((dig >> b) & 1) ? bal : ~bal;
-            }
-            const uint64_t lower = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-            const int rank = __popcll(same & lower);
-            for (int i = tid; i < (kSortThreads / 64) * 256; i += kSortThreads) (&wcnt[0][0])[i] = 0;
-            __syncthreads();
-            if (live && rank == 0) wcnt[wv][dig] = __popcll(same);
-            __syncthreads();
-            if (live) {
-                int off = base[dig];
-                for (int w = 0; w < wv; ++w) off += wcnt[w][dig];
-                kb[off + rank] = key;
-                if (with_vals) vb[off + rank] = va[j];
-            }
-            __syncthreads();
-            if (tid < 256) {
-                int add = 0;
-                for (int w = 0; w < kSortThreads / 64; ++w) add += wcnt[w][tid];
-                base[tid] += add;
-            }
-            __syncthreads();
+        for (int q = 0; q < 4; ++q) { v[q] = gb[wv][4 * lane + q]; sum += v[q]; }
+        int incl = sum;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int y = __shfl_up(incl, off);
+            if (lane >= off) incl += y;
         }
-        uint32_t *tk = ka; ka = kb; kb = tk;
-        int32_t *tv = va; va = vb; vb = tv;
-        __syncthreads();
+        int run = incl - sum;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) { gb[wv][4 * lane + q] = run; run += v[q]; }
+    }
+    __syncthreads();
+    for (int p = 0; p < 4; ++p) {
+        const int shift = 8 * p;
+        const uint32_t *sk = (p & 1) ? kb : ka;
+        const int32_t *sv = (p & 1) ? vb : va;
+        uint32_t *dk = (p & 1) ? ka : kb;
+        int32_t *dv = (p & 1) ? va : vb;
+        // the keys of tile t0 + kSortTile load while tile t0 is ranked and written
+        uint32_t nkey[kSortE];
+        int32_t nval[kSortE];
+        auto load_tile = [&](int64_t t0) {
+#pragma unroll
+            for (int s = 0; s < kSortE; ++s) {
+                const int64_t e = t0 + (int64_t)wv * 64 * kSortE + s * 64 + lane;
+                const bool live = e < n;
+                if (p == 0) {
+                    nkey[s] = live ? ~ord_key(imp[e]) : 0u;
+                    nval[s] = (int32_t)e;
+                } else {
+                    nkey[s] = live ? sk[e] : 0u;
+                    nval[s] = (with_vals && live) ? sv[e] : 0;
+                }
+            }
+        };
+        load_tile(0);
+        for (int64_t t0 = 0; t0 < n; t0 += kSortTile) {
+            for (int i = lane; i < 256; i += 64) wc[wv][i] = 0;
+            uint32_t key[kSortE];
+            int32_t val[kSortE];
+            int dg[kSortE], lr[kSortE];
+#pragma unroll
+            for (int s = 0; s < kSortE; ++s) {
+                const int64_t e = t0 + (int64_t)wv * 64 * kSortE + s * 64 + lane;
+                key[s] = nkey[s];
+                val[s] = nval[s];
+                dg[s] = (e < n) ? (int)((key[s] >> shift) & 255u) : 256;
+            }
+            if (t0 + kSortTile < n) load_tile(t0 + kSortTile);
+#pragma unroll
+            for (int s = 0; s < kSortE; ++s) {
+                // lanes of this wave holding the same digit in this slot
+                uint64_t same = __ballot(dg[s] < 256);
+#pragma unroll
+                for (int b = 0; b < 8; ++b) {
+                    const uint64_t bal = __ballot((dg[s] >> b) & 1);
+                    same &= ((dg[s] >> b) & 1) ? bal : ~bal;
+                }
+                const int below = __popcll(same & below_mask);
+                int pre = 0;
+                if (dg[s] < 256) pre = wc[wv][dg[s]];
+                lr[s] = pre + below;
+                if (dg[s] < 256 && below == 0) wc[wv][dg[s]] = pre + __popcll(same);
+            }
+            lds_barrier();
+            if (tid < 256) {
+                int c[kSortWaves];
+#pragma unroll
+                for (int w = 0; w < kSortWaves; ++w) c[w] = wc[w][tid];
+                int run = 0;
+#pragma unroll
+                for (int w = 0; w < kSortWaves; ++w) { wc[w][tid] = run; run += c[w]; }
+                ttot[tid] = run;
+            }
+            lds_barrier();
+            if (wv == 0) {
+                int v[4], sum = 0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) { v[q] = ttot[4 * lane + q]; sum += v[q]; }
+                int incl = sum;
+#pragma unroll
+                for (int off = 1; off < 64; off <<= 1) {
+                    const int y = __shfl_up(incl, off);
+                    if (lane >= off) incl += y;
+                }
+                int run = incl - sum;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) { tdp[4 * lane + q] = run; run += v[q]; }
+            }
+            lds_barrier();
+#pragma unroll
+            for (int s = 0; s < kSortE; ++s) {
+                if (dg[s] < 256) {
+                    const int lp = tdp[dg[s]] + wc[wv][dg[s]] + lr[s];
+                    stk[lp] = key[s];
+                    if (with_vals) stv[lp] = val[s];
+                }
+            }
+            lds_barrier();
+            const int cnt = (int)((n - t0 < kSortTile) ? n - t0 : kSortTile);
+            for (int i = tid; i < cnt; i += kSortThreads) {
+                const uint32_t kk = stk[i];
+                const int d = (int)((kk >> shift) & 255u);
+                const int64_t gp = (int64_t)gb[p][d] + (i - tdp[d]);
+                dk[gp] = kk;
+                if (with_vals) dv[gp] = stv[i];
+            }
+            lds_barrier();
+            if (tid < 256) gb[p][tid] += ttot[tid];
+            lds_barrier();
+        }
+        __syncthreads();  // this pass's global writes are the next pass's input
     }
     // four passes: the result is back in keys_a / vals_a
 }

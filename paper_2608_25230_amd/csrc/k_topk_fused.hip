@@ -152,15 +152,10 @@ __device__ __forceinline__ void wait_vm(int n) {
 }
 #undef FW_VM
 __device__ __forceinline__ void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-// Workgroup barrier that orders LDS only.  Every barrier of the fused kernel
-// separates LDS writes from LDS reads (the direct-to-LDS loads are per wave
-// and waited for by that wave); a full __syncthreads would also wait for every
-// outstanding global store of the wave, exposing write latency at each one.
-__device__ __forceinline__ void lds_barrier() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
+// Every barrier of the fused kernel separates LDS writes from LDS reads (the
+// direct-to-LDS loads are per wave and waited for by that wave), so it uses
+// lds_barrier: a full __syncthreads would also wait for every outstanding
+// global store of the wave, exposing write latency at each one.
 }  // namespace
 
 struct FusedArgs {

@@ -82,6 +82,23 @@ def test_curve_window_mfma_shapes(torch_fw, shape):
     assert np.all(out["curve"][:, n] == 0.0)
 
 
+def test_curve_tied_scores_across_sort_tiles(torch_fw):
+    """Unit 0 has zero window queries and an integer bias, so its scores take
+    five values over 20000 keys (bitwise ties spread over three tiles of the
+    sort); the order must keep equal scores by index.  Unit 1 is ordinary."""
+    torch, fw = torch_fw
+    H, G, n = 2, 16, 20000
+    rows = W.window_rows(57, 7, H, G, n, 128, "bf16")
+    q = rows.q.copy()
+    q[0] = W.bf16_bits(np.zeros((G, 128), np.float32))
+    rng = np.random.default_rng(3)
+    bias = np.clip(np.round(rng.standard_normal(n)), -2, 2).astype(np.float32)
+    rows = W.Rows(rows.dtype, q, rows.k, rows.v, rows.scale, bias)
+    dev, out = _curve(torch, fw, rows)
+    _check_curve(rows, out, range(H))
+    assert len(np.unique(out["importance"][0])) <= 5
+
+
 def _compact(torch, fw, k, v, imp, budget, floor, hpl):
     out = fw.ragged_compact(k, v, imp, budget, floor, hpl)
     torch.cuda.synchronize()
