@@ -212,6 +212,13 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
     const int64_t row0 = h * a.G + rt * FR;
     const float sc = a.scale ? a.scale[h] : (float)(1.0 / sqrt((double)FD));
     const int kw0 = w * 16 * TILES;  // this wave's first key
+    // The row tiles of a unit read the same keys.  Each starts its walk over
+    // them at a different tile (logit tile t holds keys kw0 + 16 tk(t) ..),
+    // so that at any moment they ask the L2 for different lines, and the
+    // later readers of a line find it there.  The shift is even, so the two
+    // tiles of a value block stay adjacent.
+    const int trot = (int)((rt * 2) & (TILES - 1));
+    auto tk = [&](int t) { return (t + trot) & (TILES - 1); };
 
     // ---- 1. logits --------------------------------------------------------
     // K streams through this wave's ring, KD - 1 tiles ahead of the MFMAs.
@@ -247,7 +254,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
         auto issue = [&](int t) {
 #pragma unroll
             for (int s = 0; s < 4; ++s)
-                dma16(kres, kring + (t % KD) * 4096 + s * 1024, kvo[s], (uint32_t)(t * 16 * FD * 2));
+                dma16(kres, kring + (t % KD) * 4096 + s * 1024, kvo[s], (uint32_t)(tk(t) * 16 * FD * 2));
         };
 #pragma unroll
         for (int t = 0; t < KD - 1 && t < TILES; ++t) issue(t);
@@ -263,7 +270,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
             for (int s = 0; s < 4; ++s)
                 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8 *)(kt + kro[s]), qb[s], acc, 0, 0, 0);
             if (BIAS) {
-                const f32x4 bj = *(const f32x4 *)(bsl + 16 * t + 4 * grp);
+                const f32x4 bj = *(const f32x4 *)(bsl + 16 * tk(t) + 4 * grp);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) S[t][i] = sc * acc[i] + bj[i];
             } else {
@@ -326,22 +333,35 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
     const float inv_w = degenerate ? 0.f : (float)FBINS / range;
 
     // ---- 3. selection -----------------------------------------------------
+    // bin(z) = min(FBINS - 1, int(fma(z, -inv_w, m inv_w))): non-increasing in
+    // z (a rounded affine map), so bins are ordered by logit, highest first.
+    // The histogram and the threshold-bin pass below evaluate the same
+    // expression on the same operands and agree bit for bit.
+    const float bnw = -inv_w, bmw = m * inv_w;
 #pragma unroll
     for (int t = 0; t < TILES; ++t) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int bin = min(FBINS - 1, (int)((m - S[t][i]) * inv_w));
+            const int bin = min(FBINS - 1, (int)fmaf(S[t][i], bnw, bmw));
             atomicAdd(&hist[rl * FBINS + bin], 1);
         }
         FW_TILE_FENCE();
     }
     lds_barrier();
-    // wave w scans rows 2w, 2w+1; lane owns bins [16 lane, 16 lane + 16)
+    // wave w scans rows 2w, 2w+1; lane owns bins [16 lane, 16 lane + 16),
+    // read once into registers
     for (int rr = 0; rr < FR / FW; ++rr) {
         const int r = (FR / FW) * w + rr;
+        int hv[16];
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+            typedef int i32x4 __attribute__((ext_vector_type(4)));
+            const i32x4 x = *(const i32x4 *)&hist[r * FBINS + 16 * lane + 4 * q4];
+            hv[4 * q4] = x[0]; hv[4 * q4 + 1] = x[1]; hv[4 * q4 + 2] = x[2]; hv[4 * q4 + 3] = x[3];
+        }
         int c = 0;
 #pragma unroll
-        for (int b = 0; b < 16; ++b) c += hist[r * FBINS + 16 * lane + b];
+        for (int b = 0; b < 16; ++b) c += hv[b];
         int incl = c;
 #pragma unroll
         for (int off = 1; off < 64; off <<= 1) {
@@ -354,10 +374,15 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
             const int f = __ffsll(bal) - 1;
             if (lane == f) {
                 int cum = incl - c, bsel = 16 * lane + 15, need = 1, cnt = 0;
+                bool found = false;
+#pragma unroll
                 for (int b = 0; b < 16; ++b) {
-                    const int hb = hist[r * FBINS + 16 * lane + b];
-                    if (cum + hb >= kv) { bsel = 16 * lane + b; need = kv - cum; cnt = hb; break; }
-                    cum += hb;
+                    const bool here = !found && cum + hv[b] >= kv;
+                    bsel = here ? 16 * lane + b : bsel;
+                    need = here ? kv - cum : need;
+                    cnt = here ? hv[b] : cnt;
+                    found |= here;
+                    cum += hv[b];
                 }
                 THR(r, kk, 0) = bsel;
                 THR(r, kk, 1) = need;
@@ -372,17 +397,17 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
         int tb[NK];
 #pragma unroll
         for (int kk = 0; kk < NK; ++kk) tb[kk] = THR(rl, kk, 0);
-        const float m1 = opaque(m), w1 = opaque(inv_w);
+        const float m1 = opaque(bmw), w1 = opaque(bnw);
 #pragma unroll
         for (int t = 0; t < TILES; ++t) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int bin = min(FBINS - 1, (int)((m1 - S[t][i]) * w1));
+                const int bin = min(FBINS - 1, (int)fmaf(S[t][i], w1, m1));
                 int hit = 0;
 #pragma unroll
                 for (int kk = 0; kk < NK; ++kk) hit |= (int)(bin == tb[kk]);
                 if (hit) {
-                    const uint32_t j = (uint32_t)(kw0 + 16 * t + 4 * grp + i);
+                    const uint32_t j = (uint32_t)(kw0 + 16 * tk(t) + 4 * grp + i);
                     const unsigned long long e = ((unsigned long long)ord_key(S[t][i]) << 32) | (0xFFFFFFFFu - j);
 #pragma unroll
                     for (int kk = 0; kk < NK; ++kk)
@@ -425,12 +450,13 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
         };
         if (cnt <= 64) {
             const unsigned long long e = (lane < cnt) ? lists[li * FCAP + lane] : 0ull;
+            // rank = entries above e, read as LDS broadcasts (every lane the
+            // same address), four independent reads per step
+            const unsigned long long *lp = lists + li * FCAP;
             int rank = 0;
-            for (int jj = 0; jj < cnt; ++jj) {
-                const unsigned long long o =
-                    ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(e >> 32), jj) << 32) |
-                    (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)e, jj);
-                rank += (int)(o > e);
+            for (int jj = 0; jj < cnt; jj += 4) {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) rank += (int)(jj + u < cnt) & (int)(lp[jj + u] > e);
             }
             const unsigned long long bal = __ballot(lane < cnt && rank == need - 1);
             const int f = bal ? __ffsll(bal) - 1 : 0;
@@ -492,7 +518,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
         for (int t = 0; t < TILES; ++t) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int j = kw0 + 16 * t + 4 * grp + i;
+                const int j = kw0 + 16 * tk(t) + 4 * grp + i;
                 c += (int)(S[t][i] > kf) | ((int)(S[t][i] == kf) & (int)(j <= kc));
             }
             FW_TILE_FENCE();
@@ -505,7 +531,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
             FW_TILE_FENCE();
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int j = kw0 + 16 * t + 4 * grp + i;
+                const int j = kw0 + 16 * tk(t) + 4 * grp + i;
                 if ((int)(S[t][i] > kx) | ((int)(S[t][i] == kx) & (int)(j <= cx))) {
                     const uint32_t u = ord_key(S[t][i]);
                     if (pos < a.kmax)
@@ -566,14 +592,14 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
             if (f < nf) {
                 const unsigned long long e = fixl[rl * FIXCAP + f];
                 const int j = (int)(0xFFFFFFFFu - (uint32_t)e);
-                const int jj = j - kw0 - 4 * grp;  // 16 t + i for a key of this lane
+                const int jj = j - kw0 - 4 * grp;  // 16 tk(t) + i for a key of this lane
                 if (jj >= 0 && jj < 16 * TILES && (jj & 15) < 4) {
                     const float s = key_to_float((uint32_t)(e >> 32));
                     int tier = NK;
 #pragma unroll
                     for (int kk = 0; kk < NK; ++kk)
                         tier -= (int)(s > tf[kk]) | ((int)(s == tf[kk]) & (int)(j <= tcut[kk]));
-                    const int t = jj >> 4, i = jj & 3;
+                    const int t = ((jj >> 4) - trot) & (TILES - 1), i = jj & 3;
                     const int sh = 16 * (i & 1) + 2 * (2 * (t & 3) + (i >> 1));
 #pragma unroll
                     for (int x = 0; x < (TILES + 3) / 4; ++x)
@@ -622,7 +648,7 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
 #pragma unroll
             for (int qq = 0; qq < VLQ; ++qq)
                 dma16(vres, vring + (b % VD) * (32 * DQ * 2) + qq * 1024, vvo,
-                      (uint32_t)(((32 * b + (64 / VCR) * qq) * FD + DQ * pass) * 2));
+                      (uint32_t)(((32 * ((b + trot / 2) & (NB - 1)) + (64 / VCR) * qq) * FD + DQ * pass) * 2));
         };
 #pragma unroll
         for (int b = 0; b < VD - 1 && b < NB; ++b) issue(b);
@@ -692,10 +718,13 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
                     acc[dt][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                         vbf, __builtin_bit_cast(bf16x8, pb[tt]), acc[dt][tt], 0, 0, 0);
             }
-            // tier masses: the same operands against a block of ones
+            // tier masses (first pass only): the same operands against a
+            // block of ones
+            if (pass == 0) {
 #pragma unroll
-            for (int tt = 0; tt < NT; ++tt)
-                accm[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, __builtin_bit_cast(bf16x8, pb[tt]), accm[tt], 0, 0, 0);
+                for (int tt = 0; tt < NT; ++tt)
+                    accm[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, __builtin_bit_cast(bf16x8, pb[tt]), accm[tt], 0, 0, 0);
+            }
             __builtin_amdgcn_sched_barrier(0);
         }
         // every lane of a row holds that row's masses over this wave's keys
