@@ -360,3 +360,158 @@ def compact(K: np.ndarray, V: np.ndarray, keep: np.ndarray, heads_per_layer: int
     full = H * n * per_row
     return dict(offsets=offsets, kept_pos=kept_pos, k_out=K_out, v_out=V_out,
                 bytes_held=np.array([ragged, padded, full], np.int64))
+
+
+# ----------------------------------------------------------------------------
+# Candidate set, ES_pool and the pool-restricted balancing selector
+# (Section 2.2, Definition 2.5; the appendix's enumeration protocol), and the
+# per-row certificate statistics (Lemma 2.2; Section 2.3 "Dropped mass
+# certificate"; the appendix's "Absolute forms")
+# ----------------------------------------------------------------------------
+
+
+def single_key_errors(p: np.ndarray, V: np.ndarray) -> np.ndarray:
+    """p_j ||v_j - mu||: the error a key contributes on its own (Definition 2.5)."""
+    p = np.asarray(p, np.float64)
+    V = np.asarray(V, np.float64)
+    mu = dense_output(p, V)
+    return p * np.linalg.norm(V - mu, axis=1)
+
+
+def candidate_pool(z: np.ndarray, V: np.ndarray, s: int, extra: int) -> Tuple[np.ndarray, np.ndarray]:
+    """The candidate set of Definition 2.5: the top-mass set A*_s plus the
+    ``extra`` keys outside it of largest single-key error (ties to the lower
+    index).  Returns (A*_s in rank order, the extra keys in error order)."""
+    z = np.asarray(z, np.float64)
+    p = weights(z)
+    top = top_mass_set(z, s)
+    e = single_key_errors(p, V)
+    rest = np.setdiff1d(np.arange(z.size), top)
+    order = np.lexsort((rest, -e[rest]))
+    return top, rest[order[:extra]]
+
+
+def pool_subset_errors(p: np.ndarray, V: np.ndarray, combos: np.ndarray, chunk: int = 1 << 15) -> np.ndarray:
+    """es(A) from its definition for every row A of ``combos`` (key indices of
+    the full row): the masses p_j and the dense output mu are the full row's,
+    and m_A renormalises by p(A).  Only the keys that occur in ``combos`` enter
+    the kept sums."""
+    p = np.asarray(p, np.float64)
+    V = np.asarray(V, np.float64)
+    mu = p @ V
+    keys = np.unique(combos)
+    col = np.searchsorted(keys, combos)
+    pk = p[keys]
+    pV = pk[:, None] * V[keys]
+    out = np.empty(len(combos))
+    for lo in range(0, len(combos), chunk):
+        c = col[lo:lo + chunk]
+        ind = np.zeros((len(c), keys.size))
+        np.put_along_axis(ind, c, 1.0, axis=1)
+        out[lo:lo + chunk] = np.linalg.norm((ind @ pV) / (ind @ pk)[:, None] - mu, axis=1)
+    return out
+
+
+def pool_best_subset(p: np.ndarray, V: np.ndarray, pool: Sequence[int], s: int) -> Tuple[np.ndarray, float]:
+    """ES_pool(s): the exact minimum of es over the size-s subsets of the
+    candidate set (Definition 2.5), by enumeration of the pool's keys in
+    ascending order; the lexicographically smallest ascending tuple of key
+    indices wins exact ties.  Returns (ascending key indices, ES_pool)."""
+    keys = np.sort(np.asarray(pool, np.int64))
+    combos = keys[combinations_table(keys.size, s)]
+    es = pool_subset_errors(p, V, combos)
+    best = combos[int(np.argmin(es))].copy()
+    return best, forced_error(p, V, best)
+
+
+def pool_swap(p: np.ndarray, V: np.ndarray, pool: Sequence[int], s: int, max_iters: int,
+              start: Sequence[int]) -> Tuple[np.ndarray, np.ndarray, int]:
+    """The balancing selector drawing from the candidate set: from ``start``
+    (the top-mass set) take the swap of one kept key for one dropped key of
+    the pool that most decreases es (ties to the smallest (out, in)), accept
+    only a strict decrease, stop after ``max_iters`` swaps.  Returns
+    (ascending set, trajectory padded with NaN, number of swaps)."""
+    p = np.asarray(p, np.float64)
+    V = np.asarray(V, np.float64)
+    pool = np.sort(np.asarray(pool, np.int64))
+    S = np.sort(np.asarray(start, np.int64))
+    traj = np.full(max_iters + 1, np.nan)
+    cur = forced_error(p, V, S)
+    traj[0] = cur
+    it = 0
+    while it < max_iters:
+        out_keys = np.setdiff1d(pool, S)
+        if out_keys.size == 0:
+            break
+        cands, pairs = [], []
+        for i in S:
+            for j in out_keys:
+                cands.append(np.sort(np.concatenate([S[S != i], [j]])))
+                pairs.append((int(i), int(j)))
+        es = pool_subset_errors(p, V, np.array(cands, np.int64))
+        t = int(np.argmin(es))
+        if not es[t] < cur:
+            break
+        i, j = pairs[t]
+        S = np.sort(np.concatenate([S[S != i], [j]]))
+        it += 1
+        cur = forced_error(p, V, S)
+        traj[it] = cur
+    return S, traj, it
+
+
+def certificate(p: np.ndarray, V: np.ndarray, S: Sequence[int]) -> Dict[str, float]:
+    """Per-row statistics of a kept set S (the top-mass set in the paper):
+    dropped mass pbar(S); Phi = ||g_S|| with g_S = sum_{j in S} p_j (v_j - mu)
+    (Lemma 2.2); the radius D = max_j ||v_j - mu||; sigma with
+    sigma^2 = sum_j p_j ||v_j - mu||^2; and the two absolute upper bounds on
+    es(S): the diameter form 2 D pbar (Lemma 2.2, for the top-mass set) and
+    the variance form sqrt(pbar / (1 - pbar)) sigma."""
+    p = np.asarray(p, np.float64)
+    V = np.asarray(V, np.float64)
+    S = np.asarray(S, np.int64)
+    mu = dense_output(p, V)
+    dev = np.linalg.norm(V - mu, axis=1)
+    g = (p[S][:, None] * (V[S] - mu)).sum(axis=0)
+    drop = dropped_mass(p, S)
+    sigma = float(math.sqrt(float(np.sum(p * dev ** 2))))
+    D = float(dev.max())
+    var_bound = math.sqrt(drop / (1.0 - drop)) * sigma if drop < 1.0 else math.inf
+    return dict(dropped=drop, phi=float(np.linalg.norm(g)), diam=D, sigma=sigma,
+                bound_diam=2.0 * D * drop, bound_var=var_bound)
+
+
+def ratio(num: float, den: float) -> float:
+    """num / den for the kappa statistics: 1 when both are 0, +inf when only
+    the denominator is."""
+    if den > 0.0:
+        return num / den
+    return 1.0 if num == 0.0 else math.inf
+
+
+def row_pool(z: np.ndarray, V: np.ndarray, s: int, extra: int, max_iters: int) -> Dict[str, object]:
+    """Everything Definition 2.5 and the enumeration protocol report for one
+    row: the candidate set, ES_pool and its argmin, the pool-restricted
+    balancing set, kappa_hat = es(A*_s)/ES_pool, c_hat = 1 - ES_pool/es(A*_s),
+    kappa_bal = es(A_bal)/ES_pool and the certificate statistics of A*_s."""
+    z = np.asarray(z, np.float64)
+    p = weights(z)
+    top, extras = candidate_pool(z, V, s, extra)
+    pool = np.concatenate([top, extras])
+    # every set's error through one evaluator on its ascending indices, so a
+    # top-mass set that is also the pool optimum gives c_hat = 0 exactly
+    es_top = forced_error(p, V, np.sort(top))
+    best, es_pool = pool_best_subset(p, V, pool, s)
+    bal, traj, n_swaps = pool_swap(p, V, pool, s, max_iters, top)
+    es_bal = forced_error(p, V, bal)
+    cert = certificate(p, V, top)
+    return dict(top=top, extras=extras, best_idx=best, bal_idx=bal, es_top=es_top, es_pool=es_pool,
+                es_bal=es_bal, kappa_hat=ratio(es_top, es_pool), c_hat=closed_fraction(es_top, es_pool),
+                kappa_bal=ratio(es_bal, es_pool), n_swaps=n_swaps, traj=traj, **cert)
+
+
+def cell_median(dropped: np.ndarray) -> float:
+    """Median dropped mass over a cell's rows (a cell is flat when this, at
+    s = 8, exceeds 0.25: Definition 2.5).  An even count averages the two
+    middle values."""
+    return float(np.median(np.asarray(dropped, np.float64)))

@@ -34,6 +34,11 @@ def _run_all_pins():
     checks += [(P.test_swap_rule_invariants, s) for s in range(3)]
     checks += [(P.test_dropped_mass_curve, s) for s in range(3)]
     checks += [(P.test_allocation, s) for s in range(3)]
+    checks += [(P.test_pool_example_2_3,), (P.test_cell_median,)]
+    checks += [(P.test_pool_brute_force, s) for s in range(4)]
+    checks += [(P.test_pool_of_every_key_is_the_full_search, s) for s in range(3)]
+    checks += [(P.test_pool_swap_invariants, s) for s in range(3)]
+    checks += [(P.test_certificate_identities_and_bounds, s) for s in range(3)]
     return any(_fails(*c) for c in checks)
 
 
@@ -105,7 +110,50 @@ def _alloc_ties_high(r, budget, floor):
                 dropped=np.where(keep, 0.0, r).sum(1))
 
 
+def _extras_by_mass(z, V, s, extra):
+    z = np.asarray(z, np.float64)
+    top = O.top_mass_set(z, s)
+    rest = np.setdiff1d(np.arange(z.size), top)
+    return top, rest[np.lexsort((rest, -z[rest]))[:extra]]
+
+
+def _extras_may_repeat_top(z, V, s, extra):
+    z = np.asarray(z, np.float64)
+    e = O.single_key_errors(O.weights(z), V)
+    allk = np.arange(z.size)
+    return O.top_mass_set(z, s), allk[np.lexsort((allk, -e))[:extra]]
+
+
+def _pool_renormalised(p, V, pool, s):
+    keys = np.sort(np.asarray(pool, np.int64))
+    q = np.asarray(p)[keys] / np.asarray(p)[keys].sum()
+    Vk = np.asarray(V)[keys]
+    best, es = O.best_subset(q, Vk, s)
+    return keys[best], es
+
+
+def _sigma_unweighted(p, V, S):
+    c = _ORIG_CERT(p, V, S)
+    mu = np.asarray(p) @ np.asarray(V)
+    c["sigma"] = float(np.sqrt(np.mean(np.linalg.norm(np.asarray(V) - mu, axis=1) ** 2)))
+    return c
+
+
+def _var_bound_inverted(p, V, S):
+    c = _ORIG_CERT(p, V, S)
+    m = c["dropped"]
+    c["bound_var"] = float(np.sqrt((1 - m) / m) * c["sigma"]) if m > 0 else np.inf
+    return c
+
+
+_ORIG_CERT = O.certificate
+
 MUTANTS = {
+    "pool_extras_by_mass": ("candidate_pool", _extras_by_mass),
+    "pool_extras_repeat_top": ("candidate_pool", _extras_may_repeat_top),
+    "pool_renormalised_within_pool": ("pool_best_subset", _pool_renormalised),
+    "certificate_sigma_unweighted": ("certificate", _sigma_unweighted),
+    "certificate_variance_bound_inverted": ("certificate", _var_bound_inverted),
     "forced_output_without_renormalisation": ("forced_output", _no_renorm),
     "top_mass_ties_to_higher_index": ("top_mass_set", _ties_high),
     "dropped_mass_is_kept_mass": ("dropped_mass", _dropped_is_kept),

@@ -404,3 +404,127 @@ def test_dense_topk_batch_consistency():
                 assert out["dropped"][t, h, g] == pytest.approx(1 - p[S].sum(), abs=1e-14)
             assert out["gap"][2, h, g] < 1e-13
             assert np.allclose(out["o_s"][2, h, g], out["o"][h, g])
+
+
+# ---------------------------------------------------------------------------
+# Candidate set, ES_pool, pool-restricted balancing, certificate statistics
+# (Definition 2.5, Lemma 2.2, the appendix's absolute forms)
+# ---------------------------------------------------------------------------
+
+def test_pool_example_2_3():
+    g = _golden("example_2_3_pool.json")
+    v = np.array(g["v"], float)[:, None]
+    p = np.array([float(Fraction(x)) for x in g["p"]])
+    F = lambda x: float(Fraction(x))
+    e = O.single_key_errors(p, v)
+    assert e == pytest.approx([F(x) for x in g["single_key_errors"]], rel=1e-13)
+    r = O.row_pool(np.log(p), v, g["s"], g["extra"], max_iters=8)
+    assert r["top"].tolist() == g["top"] and r["extras"].tolist() == g["extras"]
+    assert r["best_idx"].tolist() == g["best_set"] and r["bal_idx"].tolist() == g["bal_set"]
+    assert r["es_pool"] == pytest.approx(F(g["ES_pool"]), rel=1e-13)
+    assert r["kappa_hat"] == pytest.approx(F(g["kappa_hat"]), rel=1e-13)
+    assert r["c_hat"] == pytest.approx(F(g["c_hat"]), rel=1e-12)
+    assert r["n_swaps"] == g["n_swaps"]
+    assert r["dropped"] == pytest.approx(F(g["dropped"]), rel=1e-13)
+    assert r["phi"] == pytest.approx(F(g["phi"]), rel=1e-13)
+    assert r["diam"] == pytest.approx(F(g["diam"]), rel=1e-13)
+    assert r["sigma"] ** 2 == pytest.approx(F(g["sigma_sq"]), rel=1e-13)
+    assert r["bound_diam"] == pytest.approx(F(g["bound_diam"]), rel=1e-13)
+    assert r["bound_var"] ** 2 == pytest.approx(F(g["bound_var_sq"]), rel=1e-13)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_pool_brute_force(seed):
+    """The candidate set and ES_pool against plain loops over the definitions
+    on small rows: extras are the largest p_j ||v_j - mu|| outside A*_s (ties to
+    the lower index), and ES_pool is the smallest es over the pool's s-subsets
+    with the full row's masses and dense output; ES <= ES_pool <= es(A*_s)."""
+    rng = np.random.default_rng(700 + seed)
+    n, d, s, extra = 9, 3, 3, 3
+    z, p, V = _rand_instance(rng, n, d, temp=1.5)
+    if seed == 3:  # equal single-key errors: the lower index must win
+        V[5] = V[6]
+        z[5] = z[6]
+        p = O.weights(z)
+    top, extras = O.candidate_pool(z, V, s, extra)
+    mu = sum(p[j] * V[j] for j in range(n))
+    err = [p[j] * math.sqrt(sum((V[j][c] - mu[c]) ** 2 for c in range(d))) for j in range(n)]
+    ranked = sorted(range(n), key=lambda j: (-z[j], j))
+    assert top.tolist() == ranked[:s]
+    rest = sorted((j for j in range(n) if j not in ranked[:s]), key=lambda j: (-err[j], j))
+    assert extras.tolist() == rest[:extra]
+    pool = sorted(ranked[:s] + rest[:extra])
+    brute = min((O.forced_error(p, V, list(A)), A) for A in itertools.combinations(pool, s))
+    best, es_pool = O.pool_best_subset(p, V, np.concatenate([top, extras]), s)
+    assert best.tolist() == list(brute[1])
+    assert es_pool == pytest.approx(brute[0], rel=1e-12)
+    _, ES = O.best_subset(p, V, s)
+    assert ES <= es_pool * (1 + 1e-12)
+    assert es_pool <= O.forced_error(p, V, top) * (1 + 1e-12)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_pool_of_every_key_is_the_full_search(seed):
+    """With every key in the candidate set, ES_pool is ES and the
+    pool-restricted balancing selector is the full one (both pinned above)."""
+    rng = np.random.default_rng(710 + seed)
+    n, d, s = 8, 2, 3
+    z, p, V = _rand_instance(rng, n, d, temp=2.0)
+    r = O.row_pool(z, V, s, n - s, max_iters=16)
+    best, ES = O.best_subset(p, V, s)
+    assert r["best_idx"].tolist() == best.tolist()
+    assert r["es_pool"] == pytest.approx(ES, rel=1e-12)
+    S, traj, ns = O.swap_rule(p, V, s, max_iters=16, method="direct")
+    assert r["bal_idx"].tolist() == S.tolist() and r["n_swaps"] == ns
+    np.testing.assert_allclose(r["traj"], traj, rtol=1e-12)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_pool_swap_invariants(seed):
+    """The pool-restricted trajectory decreases strictly, its set stays in the
+    pool, no single in-pool swap improves the final set, and it lies between
+    ES_pool and es(A*_s)."""
+    rng = np.random.default_rng(720 + seed)
+    n, d, s, extra = 12, 4, 4, 4
+    z, p, V = _rand_instance(rng, n, d, temp=2.5)
+    r = O.row_pool(z, V, s, extra, max_iters=20)
+    pool = set(r["top"].tolist()) | set(r["extras"].tolist())
+    S = r["bal_idx"]
+    assert set(S.tolist()) <= pool
+    t = r["traj"][: r["n_swaps"] + 1]
+    assert np.all(np.diff(t) < 0)
+    for i in S:
+        for j in pool - set(S.tolist()):
+            A = sorted(set(S.tolist()) - {int(i)} | {j})
+            assert O.forced_error(p, V, A) >= r["es_bal"] * (1 - 1e-12)
+    assert r["es_pool"] <= r["es_bal"] * (1 + 1e-12)
+    assert r["es_bal"] <= r["es_top"] * (1 + 1e-12)
+    assert r["kappa_hat"] >= 1 - 1e-12 and 0 <= r["c_hat"] <= 1
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_certificate_identities_and_bounds(seed):
+    """Phi = es(S) p(S) = ||g_S|| (Lemma 2.2); sigma^2 = sum_j p_j ||v_j||^2 -
+    ||mu||^2; D bounds every deviation; es(A*_s) <= 2 D pbar (Lemma 2.2) and
+    every kept set satisfies es(S) <= sqrt(pbar / (1 - pbar)) sigma."""
+    rng = np.random.default_rng(730 + seed)
+    n, d, s = 8, 3, 3
+    z, p, V = _rand_instance(rng, n, d, temp=1.0 + seed)
+    top = O.top_mass_set(z, s)
+    c = O.certificate(p, V, top)
+    es_top = O.forced_error(p, V, top)
+    assert c["phi"] == pytest.approx(es_top * O.kept_mass(p, top), rel=1e-12)
+    mu = p @ V
+    assert c["sigma"] ** 2 == pytest.approx(float(p @ (V * V).sum(1) - mu @ mu), rel=1e-10)
+    assert c["diam"] == pytest.approx(max(math.dist(V[j], mu) for j in range(n)), rel=1e-13)
+    assert es_top <= c["bound_diam"] * (1 + 1e-12)
+    for k in range(1, n):
+        for A in itertools.combinations(range(n), k):
+            cA = O.certificate(p, V, list(A))
+            assert O.forced_error(p, V, list(A)) <= cA["bound_var"] * (1 + 1e-12)
+
+
+def test_cell_median():
+    assert O.cell_median(np.array([0.1, 0.3, 0.2])) == pytest.approx(0.2)
+    assert O.cell_median(np.array([0.1, 0.4, 0.2, 0.3])) == pytest.approx(0.25)
+    assert O.ratio(0.0, 0.0) == 1.0 and O.ratio(1.0, 0.0) == math.inf
