@@ -32,112 +32,13 @@
 #include "fw_internal.hpp"
 #include "instance64.hpp"
 #include "revdoor.hpp"
+#include "enum_walk.hpp"
 
 namespace fw {
 
 namespace {
 
 constexpr int kSubsetThreads = 256;
-constexpr int kMaxWalk = 16;      // walked range size (per-lane e[] in registers)
-constexpr int kMaxEntries = 4096; // walk-table entries per row (LDS)
-constexpr int kMaxClass = 17;     // values of h with work (min(m, n - m) + 1)
-
-// One value of h: which part the lanes own and which is walked.
-struct EnumClass {
-    int h;
-    int wb, wn, ws;  // walked part: range [wb, wb + wn), size ws
-    int lb, ln, ls;  // owned part: range [lb, lb + ln), size ls
-    int toff;        // first walk-table entry
-};
-
-// Enumeration plan shared by host (sizes) and device (tables, jobs).
-struct EnumPlan {
-    int n, k, d, G;
-    int m;
-    int ncls;
-    EnumClass cls[kMaxClass];
-    int nent;  // walk-table entries
-    int njobs;
-};
-
-__host__ __device__ inline int ceil64(uint64_t x) { return (int)((x + 63) / 64); }
-// walks run in rounds of four steps; tables are padded with neutral steps
-__host__ __device__ inline uint64_t pad4(uint64_t x) { return (x + 3) & ~(uint64_t)3; }
-constexpr uint64_t kPadMask = ~(uint64_t)0;  // walk-table mask of a padding step
-
-// Estimated instructions of one wave job: set-up of the owned part plus the
-// walk.
-__host__ __device__ inline double job_cost(int wn, int ws, int ln, int ls) {
-    const double steps = (double)binom(wn, ws);
-    double setup = 40.0 + 6.0 * ls * ls;  // the owned part comes from a table
-    (void)ln;
-    if (ws > 0) setup += ls * (1.5 * wn + 8.0) + 3.0 * wn;
-    return setup + 10.0 * steps;
-}
-
-__host__ __device__ inline bool plan_for(int n, int k, int m, EnumPlan *P, double *cost) {
-    EnumPlan p{};
-    p.n = n;
-    p.k = k;
-    p.m = m;
-    const int N = n - m;
-    const int hlo = k - m > 0 ? k - m : 0, hhi = k < N ? k : N;
-    if (hlo > hhi || hhi - hlo + 1 > kMaxClass) return false;
-    double total = 0.0;
-    uint64_t nent = 0, njobs = 0;
-    int toffA[kMaxWalk + 1], toffB[kMaxWalk + 1];
-    for (int q = 0; q <= kMaxWalk; ++q) toffA[q] = toffB[q] = -1;
-    for (int h = hlo; h <= hhi; ++h) {
-        const int kw = k - h;
-        // A: lanes own the high part, walk the low range; B: the reverse
-        const bool okA = m <= kMaxWalk, okB = N <= kMaxWalk;
-        if (!okA && !okB) return false;
-        const double cA = okA ? ceil64(binom(N, h)) * job_cost(m, kw, N, h) : 0.0;
-        const double cB = okB ? ceil64(binom(m, kw)) * job_cost(N, h, m, kw) : 0.0;
-        const bool useA = okA && (!okB || cA <= cB);
-        EnumClass c;
-        c.h = h;
-        if (useA) {
-            c.wb = 0; c.wn = m; c.ws = kw; c.lb = m; c.ln = N; c.ls = h;
-            if (toffA[kw] < 0) { toffA[kw] = (int)nent; nent += pad4(binom(m, kw)); }
-            c.toff = toffA[kw];
-        } else {
-            c.wb = m; c.wn = N; c.ws = h; c.lb = 0; c.ln = m; c.ls = kw;
-            if (toffB[h] < 0) { toffB[h] = (int)nent; nent += pad4(binom(N, h)); }
-            c.toff = toffB[h];
-        }
-        total += useA ? cA : cB;
-        njobs += (uint64_t)ceil64(binom(c.ln, c.ls));
-        p.cls[p.ncls++] = c;
-    }
-    if (nent > (uint64_t)kMaxEntries || njobs > (1u << 17)) return false;
-    p.nent = (int)nent;
-    p.njobs = (int)njobs;
-    *P = p;
-    *cost = total;
-    return true;
-}
-
-__host__ inline bool choose_plan(int64_t n, int k, EnumPlan *out) {
-    bool found = false;
-    double best = 0.0;
-    for (int m = 1; m <= (int)n; ++m) {
-        EnumPlan p;
-        double c;
-        if (!plan_for((int)n, k, m, &p, &c)) continue;
-        if (!found || c < best) {
-            best = c;
-            *out = p;
-            found = true;
-        }
-    }
-    return found;
-}
-
-// Job descriptor: the class and a run of owned parts (colex ranks).
-struct EnumJob {
-    int32_t cls, start, lanes, steps;
-};
 
 struct SubsetLds {
     size_t gm, pz, mu, ent, pl, vs, red, ctr, total;
@@ -255,7 +156,7 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
                    float *topk_gap, float *closed, float *dropped_topk, int32_t *topk_idx) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int NT = blockDim.x;
-    const int n = pl.n, d = pl.d, kk = pl.k, m = pl.m;
+    const int n = pl.n, d = pl.d, kk = pl.k;
     const SubsetLds L = subset_lds(n, d, kk, pl.nent, NT);
     double *Gm = (double *)(smem + L.gm);
     double *ps = (double *)(smem + L.pz);
@@ -278,171 +179,8 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
     instance64(qr, kh, vh, scale ? scale[hh] : default_scale(d), bias, n, d, Vs, zs, ps, mu, Gm);
     // top-k set: rank by (z desc, index asc)
     const uint64_t top_mask = topk_mask64(zs, n, kk, topk_idx ? topk_idx + r * kk : nullptr, redm);
-    // per-row walk tables (Vs is dead: instance64 ends with a barrier)
-    for (int t = tid; t < pl.nent; t += NT) {
-        const uint64_t lm = g_wmk[t];
-        if (lm == kPadMask) {  // neutral step
-            ent[t] = make_double2(INFINITY, 0.0);
-            PLt[t] = 0.0;
-            continue;
-        }
-        double P = 0.0, S = 0.0;
-        for (uint64_t a = lm; a; a &= a - 1) {
-            const int x = __ffsll((unsigned long long)a) - 1;
-            P += ps[x];
-            for (uint64_t b2 = lm; b2; b2 &= b2 - 1) S += Gm[x * n + (__ffsll((unsigned long long)b2) - 1)];
-        }
-        ent[t] = make_double2(S, P * P);
-        PLt[t] = P;
-    }
-    if (tid == 0) ctr[0] = 0;
-    __syncthreads();
-
-    // seed: the top-k set, scored from the Gram
-    double S_top = 0.0, P_top = 0.0;
-    for (uint64_t a = top_mask; a; a &= a - 1) {
-        const int x = __ffsll((unsigned long long)a) - 1;
-        P_top += ps[x];
-        for (uint64_t b2 = top_mask; b2; b2 &= b2 - 1) S_top += Gm[x * n + (__ffsll((unsigned long long)b2) - 1)];
-    }
-    double best_val = S_top / (P_top * P_top);
-    uint64_t best_mask = top_mask;
-    double beta = best_val;  // wave-uniform
-    for (;;) {
-        int jn = 0;
-        if (lane == 0) jn = atomicAdd(ctr, 1);
-        jn = __builtin_amdgcn_readfirstlane(__shfl(jn, 0));
-        if (jn >= pl.njobs) break;
-        const EnumJob jb = g_jobs[jn];
-        const EnumClass C = pl.cls[jb.cls];
-        const int wb = C.wb, wn = C.wn;
-        const bool act = lane < jb.lanes;
-        // owned part of this lane (precomputed key mask; 0 on idle lanes)
-        const uint64_t Om = g_omk[(size_t)jn * 64 + lane];
-        double PO = 0.0, SO = 0.0;
-        for (uint64_t a = Om; a; a &= a - 1) {
-            const int x = __ffsll((unsigned long long)a) - 1;
-            PO += ps[x];
-            const double *row = Gm + x * n;
-            for (uint64_t b2 = Om; b2; b2 &= b2 - 1) SO += row[__ffsll((unsigned long long)b2) - 1];
-        }
-        // e[x] over the walked range, from contiguous Gram rows
-        double e[kMaxWalk];
-#pragma unroll
-        for (int x = 0; x < kMaxWalk; ++x) e[x] = 0.0;
-        if (C.ws > 0) {
-            for (uint64_t a = Om; a; a &= a - 1) {
-                const double *row = Gm + (__ffsll((unsigned long long)a) - 1) * n + wb;
-#pragma unroll
-                for (int x = 0; x < kMaxWalk; ++x)
-                    if (x < wn) e[x] += row[x];
-            }
-#pragma unroll
-            for (int x = 0; x < kMaxWalk; ++x)
-                if (x < wn) e[x] = 2.0 * e[x] - 2.0 * beta * PO * ps[wb + x];
-        }
-        double Y = SO - beta * PO * PO;
-#pragma unroll
-        for (int x = 0; x < kMaxWalk; ++x)
-            if (x < C.ws) Y += e[x];
-        if (!act) Y = INFINITY;
-        const uint2 *io = g_io + C.toff;
-        const uint64_t *wmk = g_wmk + C.toff;
-        const double2 *en = ent + C.toff;
-        const double *plt = PLt + C.toff;
-        const int steps = jb.steps;  // a multiple of 4 (padded with neutral steps)
-        double thr = 1e-12 * beta;
-        // exact score of walk step t for this lane (a candidate)
-        auto exact = [&](int t) {
-            const uint64_t wm = wmk[t];
-            double S = SO + en[t].x;
-            for (uint64_t a = wm; a; a &= a - 1) {
-                const double *row = Gm + (__ffsll((unsigned long long)a) - 1) * n;
-                double E = 0.0;
-                for (uint64_t b2 = Om; b2; b2 &= b2 - 1) E += row[__ffsll((unsigned long long)b2) - 1];
-                S += 2.0 * E;
-            }
-            const double P = PO + plt[t];
-            const double val = S / (P * P);
-            const uint64_t mask = Om | wm;
-            if (val < best_val || (val == best_val && lex_less(mask, best_mask))) {
-                best_val = val;
-                best_mask = mask;
-            }
-        };
-        // four steps per round: the step tables are loaded together and the
-        // rare candidates handled after the four tests (a beta lowered within
-        // the round only widens the filter of the remaining steps)
-        for (int t0 = 0; t0 < steps; t0 += 4) {
-            uint2 w[4];
-            double2 c[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                w[u] = io[t0 + u];
-                c[u] = en[t0 + u];
-            }
-            bool cand[4];
-            uint64_t any = 0;
-            double y = Y;
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                y += e[w[u].x] - e[w[u].y];
-                const double f = y + fma(-beta, c[u].y, c[u].x);
-                cand[u] = f <= thr;
-                any |= __ballot(cand[u]);  // wave masks: or-ed on the scalar unit
-            }
-            Y = y;
-            if (any) {  // rare: exact scores, then the wave's new beta
-#pragma unroll
-                for (int u = 0; u < 4; ++u)
-                    if (cand[u]) exact(t0 + u);
-                double wbst = best_val;
-#pragma unroll
-                for (int off = 32; off > 0; off >>= 1) wbst = fmin(wbst, __shfl_xor(wbst, off));
-                if (wbst < beta) {
-                    const double dB = wbst - beta;
-#pragma unroll
-                    for (int x = 0; x < kMaxWalk; ++x)
-                        if (x < wn) e[x] -= 2.0 * dB * PO * ps[wb + x];
-                    beta = wbst;
-                    thr = 1e-12 * beta;
-                    // Y for the round's last real step from the rescaled e
-                    int tl = t0 + 3;
-                    while (wmk[tl] == kPadMask) --tl;
-                    double yy = SO - beta * PO * PO;
-                    for (uint64_t a = wmk[tl]; a; a &= a - 1) yy += e[__ffsll((unsigned long long)a) - 1 - wb];
-                    Y = act ? yy : INFINITY;
-                }
-            }
-        }
-    }
-    // workgroup argmin with the lexicographic tie rule: within each wave by
-    // shuffles, then over the waves
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        const double ov = __shfl_xor(best_val, off);
-        const uint64_t om = __shfl_xor(best_mask, off);
-        if (ov < best_val || (ov == best_val && lex_less(om, best_mask))) {
-            best_val = ov;
-            best_mask = om;
-        }
-    }
-    if (lane == 0) {
-        redd[tid >> 6] = best_val;
-        redm[tid >> 6] = best_mask;
-    }
-    __syncthreads();
-    if (tid == 0) {
-        for (int i = 1; i < NT / 64; ++i) {
-            if (redd[i] < redd[0] || (redd[i] == redd[0] && lex_less(redm[i], redm[0]))) {
-                redd[0] = redd[i];
-                redm[0] = redm[i];
-            }
-        }
-    }
-    __syncthreads();
-    const uint64_t best = redm[0];
-    __syncthreads();
+    // (Vs is dead: instance64 ends with a barrier)
+    const uint64_t best = enum_best(pl, Gm, ps, top_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd, redm, ctr);
     if (tid == 0) {
         int i = 0;
         for (uint64_t a = best; a; a &= a - 1) best_idx[r * kk + i++] = __ffsll((unsigned long long)a) - 1;
@@ -465,38 +203,17 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
     }
 }
 
-namespace {
-struct SubsetWs {
-    uint2 *io;
-    uint64_t *wmk;
-    EnumJob *jobs;
-    uint64_t *omk;
-    size_t bytes;
-};
-
-SubsetWs subset_ws(const EnumPlan &p, void *ws) {
-    SubsetWs W{};
-    size_t off = 0;
-    char *base = (char *)ws;
-    auto take = [&](size_t bytes) -> void * {
-        off = align_up(off, 256);
-        void *ptr = base ? base + off : nullptr;
-        off += bytes;
-        return ptr;
-    };
-    W.io = (uint2 *)take((size_t)p.nent * 8);
-    W.wmk = (uint64_t *)take((size_t)p.nent * 8);
-    W.jobs = (EnumJob *)take((size_t)p.njobs * sizeof(EnumJob));
-    W.omk = (uint64_t *)take((size_t)p.njobs * 64 * 8);
-    W.bytes = align_up(off, 256);
-    return W;
+hipError_t launch_enum_tables(const EnumPlan &p, const EnumTables &W, hipStream_t st) {
+    hipLaunchKernelGGL(enum_plan_kernel, dim3(1), dim3(64), 0, st, p, W.io, W.wmk, W.jobs);
+    hipLaunchKernelGGL(enum_owned_kernel, dim3((unsigned)p.njobs), dim3(64), 0, st, p,
+                       (const EnumJob *)W.jobs, W.omk);
+    return hipGetLastError();
 }
-}  // namespace
 
 size_t best_subset_ws_bytes(int64_t n, int k) {
     EnumPlan p;
     if (!choose_plan(n, k, &p)) return 0;
-    return subset_ws(p, nullptr).bytes;
+    return enum_tables(p, nullptr).bytes;
 }
 
 bool best_subset_plannable(int64_t n, int k) {
@@ -511,11 +228,8 @@ hipError_t launch_best_subset(const fw_rows &rows, int k, int32_t *best_idx, flo
     if (!choose_plan(rows.n, k, &p)) return hipErrorInvalidConfiguration;
     p.d = (int)rows.d;
     p.G = (int)rows.G;
-    const SubsetWs W = subset_ws(p, ws);
-    hipLaunchKernelGGL(enum_plan_kernel, dim3(1), dim3(64), 0, st, p, W.io, W.wmk, W.jobs);
-    hipLaunchKernelGGL(enum_owned_kernel, dim3((unsigned)p.njobs), dim3(64), 0, st, p,
-                       (const EnumJob *)W.jobs, W.omk);
-    hipError_t e = hipGetLastError();
+    const EnumTables W = enum_tables(p, ws);
+    hipError_t e = launch_enum_tables(p, W, st);
     if (e != hipSuccess) return e;
     const int nt = kSubsetThreads;
     const SubsetLds L = subset_lds(p.n, p.d, k, p.nent, nt);

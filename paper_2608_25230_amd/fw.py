@@ -18,7 +18,10 @@ FW_F32, FW_BF16 = 0, 1
 STATUS = {0: "FW_OK", 1: "FW_E_NULL", 2: "FW_E_SHAPE", 3: "FW_E_DTYPE", 4: "FW_E_UNSUPPORTED",
           5: "FW_E_WORKSPACE", 6: "FW_E_HIP"}
 ENTRY_POINTS = ("fw_dense_topk", "fw_best_subset", "fw_swap", "fw_dropped_mass_curve",
-                "fw_ragged_compact")
+                "fw_ragged_compact", "fw_pool_subset")
+# columns of fw_pool_subset's stats (FW_POOL_* in include/fw.h)
+POOL_STATS = ("es_top", "es_pool", "es_bal", "kappa_hat", "c_hat", "kappa_bal", "dropped", "phi",
+              "diam", "sigma", "bound_diam", "bound_var")
 
 
 class FwError(RuntimeError):
@@ -51,6 +54,8 @@ _SIGS = {
     "fw_ragged_compact_workspace_size": (SZ, [I64, I64, I64, I64]),
     "fw_ragged_compact": (I32, [I32, P, P, I64, I64, I64, I64, P, I64, I32, P, P, P, P, P, P, P,
                                 P, SZ, P]),
+    "fw_pool_subset_workspace_size": (SZ, [RP, I32, I32]),
+    "fw_pool_subset": (I32, [RP, I32, I32, I32, P, P, P, P, P, ctypes.c_float, P, P, P, SZ, P]),
     "fw_last_error": (ctypes.c_char_p, []),
     "fw_version": (ctypes.c_char_p, []),
 }
@@ -185,6 +190,31 @@ def swap(q, k, v, kb: int, max_iters: int, scale=None, bias=None, *, ws=None) ->
     _check(L.fw_swap(ctypes.byref(rows), kb, max_iters, _ptr(out["s_idx"]), _ptr(out["gap_traj"]),
                      _ptr(out["n_swaps"]), _ptr(out["dropped"]), ws.data_ptr(), ws.numel(),
                      _stream()))
+    out["_ws"] = ws
+    return out
+
+
+def pool_subset(q, k, v, s: int, extra: int, max_swaps: int, scale=None, bias=None, *,
+                flat_threshold: float = 0.25, want_cells=True, ws=None) -> Dict[str, object]:
+    torch = _torch()
+    rows = _rows(q, k, v, scale, bias)
+    H, G = rows.H, rows.G
+    dev = q.device
+    out = {"pool_idx": torch.empty((H, G, s + extra), dtype=torch.int32, device=dev),
+           "best_idx": torch.empty((H, G, s), dtype=torch.int32, device=dev),
+           "bal_idx": torch.empty((H, G, s), dtype=torch.int32, device=dev),
+           "n_swaps": torch.empty((H, G), dtype=torch.int32, device=dev),
+           "stats": torch.empty((H, G, len(POOL_STATS)), dtype=torch.float32, device=dev),
+           "cell_median": torch.empty(H, dtype=torch.float32, device=dev) if want_cells else None,
+           "cell_flat": torch.empty(H, dtype=torch.uint8, device=dev) if want_cells else None}
+    L = lib()
+    need = L.fw_pool_subset_workspace_size(ctypes.byref(rows), s, extra)
+    if ws is None or ws.numel() < need:
+        ws = _workspace(need, dev)
+    _check(L.fw_pool_subset(ctypes.byref(rows), s, extra, max_swaps, _ptr(out["pool_idx"]),
+                            _ptr(out["best_idx"]), _ptr(out["bal_idx"]), _ptr(out["n_swaps"]),
+                            _ptr(out["stats"]), float(flat_threshold), _ptr(out["cell_median"]),
+                            _ptr(out["cell_flat"]), ws.data_ptr(), ws.numel(), _stream()))
     out["_ws"] = ws
     return out
 

@@ -29,7 +29,7 @@ from __future__ import annotations
 import math
 from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
-from typing import Optional, Sequence
+from typing import Optional, Sequence, Tuple
 
 import numpy as np
 
@@ -270,6 +270,26 @@ def swap_long_rows(seed: int = 0, kv_heads: int = 8, q_per_kv: int = 4,
     return Workload(f"swap_kv{kv_heads}_n{n}_k{k}", r, ks=(k,), k=k,
                     max_iters=max_iters, heads_per_layer=kv_heads,
                     recipe="bf16 N(0,1); bias[0]=+4; %d heavy keys x3" % heavy)
+
+
+def pool_rows(seed: int = 0, layers: int = 32, kv_heads: int = 8, q_per_kv: int = 4,
+              rows_per_q: int = 6, n: int = 4096, d: int = 128,
+              budgets: Sequence[Tuple[int, int]] = ((4, 24), (8, 12), (16, 6), (32, 4)),
+              max_swaps: int = 64) -> Workload:
+    """Candidate-set search at the enumeration protocol's shape: layers x
+    kv_heads units of q_per_kv x rows_per_q sampled rows (six per query head),
+    n keys, bf16 N(0,1) with 4 outlier key channels x8 and +4 logit on key 0
+    (the streaming recipe, drawn independently); budgets s with their extra
+    keys beyond the top-mass set; at most max_swaps balancing swaps."""
+    ch = outlier_channels(seed, d, wid=6)
+    r = sink_rows(6, seed, layers * kv_heads, q_per_kv * rows_per_q, n, d, BF16,
+                  sink=4.0, outlier_channels=ch)
+    return Workload(f"pool_L{layers}_kv{kv_heads}_r{q_per_kv * rows_per_q}_n{n}", r,
+                    ks=tuple(b for b, _ in budgets), max_iters=max_swaps,
+                    heads_per_layer=kv_heads,
+                    recipe="bf16 N(0,1); k channels %s x8; bias[0]=+4; (s, extra) %s"
+                    % (list(ch), list(budgets)),
+                    meta={"budgets": [tuple(b) for b in budgets], "outlier_channels": ch.tolist()})
 
 
 def curve_ragged(seed: int = 0, layers: int = 32, kv_heads: int = 8, window: int = 64,

@@ -26,7 +26,7 @@ def L():
     return fw.lib()
 
 
-def test_header_declares_the_five_entry_points():
+def test_header_declares_every_entry_point():
     names = _declared()
     for ep in fw.ENTRY_POINTS:
         assert ep in names and ep + "_workspace_size" in names
@@ -124,3 +124,28 @@ def test_compact_validation(L):
     assert call(floor=-1) == 2
     assert call(outs=None) == 1
     assert L.fw_ragged_compact_workspace_size(4, 64, 8, 100) > 0
+
+
+def test_pool_subset_validation(L):
+    r = _rows(n=64, d=8)
+    call = lambda rows, s, extra, ms=4, best=1, stats=1, ws=1, wsb=1 << 40: L.fw_pool_subset(
+        rows, s, extra, ms, None, best, None, None, stats, 0.25, None, None, ws, wsb, None)
+    assert call(None, 4, 4) == 1
+    assert call(ctypes.byref(_rows(dtype=7)), 4, 4) == 3
+    assert call(ctypes.byref(_rows(v=None)), 4, 4) == 1
+    assert call(ctypes.byref(r), 0, 4) == 2            # s < 1
+    assert call(ctypes.byref(r), 4, -1) == 2           # extra < 0
+    assert call(ctypes.byref(_rows(n=6)), 4, 4) == 2   # s + extra > n
+    assert call(ctypes.byref(r), 4, 4, ms=-1) == 2
+    assert call(ctypes.byref(r), 4, 4, ms=5000) == 2
+    assert call(ctypes.byref(_rows(n=200)), 40, 30) == 4   # more than 64 pool keys
+    assert call(ctypes.byref(_rows(n=9000)), 4, 4) == 4    # row longer than 8192
+    assert call(ctypes.byref(r), 4, 4, best=None) == 1
+    assert call(ctypes.byref(r), 4, 4, stats=None) == 1
+    assert call(ctypes.byref(r), 4, 4, ws=None) == 5
+    assert call(ctypes.byref(r), 4, 4, wsb=0) == 5
+    assert L.fw_pool_subset_workspace_size(ctypes.byref(r), 4, 4) > 0
+    assert L.fw_pool_subset_workspace_size(ctypes.byref(_rows(n=200)), 40, 30) == 0
+    # the paper's four (s, extra) settings are all plannable
+    for s, e in ((4, 24), (8, 12), (16, 6), (32, 4)):
+        assert L.fw_pool_subset_workspace_size(ctypes.byref(_rows(n=4096, d=128)), s, e) > 0

@@ -1,0 +1,209 @@
+"""GPU parity of fw_pool_subset (candidate set, ES_pool, pool-restricted
+balancing, certificate statistics; Definition 2.5, Lemma 2.2, Section 2.3)
+against the oracle: the paper's Example 2.3, small rows on every row, model-
+shaped bf16 rows, degenerate pools and the benchmark's full size on sampled
+rows with properties on all rows."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import fw_oracle as O
+from paper_2608_25230_amd import workloads as W
+from tests.parity import Tally, rel_scalar, t2np
+
+pytestmark = pytest.mark.gpu
+
+STATS = ("es_top", "es_pool", "es_bal", "kappa_hat", "c_hat", "kappa_bal", "dropped", "phi",
+         "diam", "sigma", "bound_diam", "bound_var")
+
+
+@pytest.fixture(scope="module")
+def torch_fw():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2608_25230_amd import fw
+    fw.lib()
+    assert tuple(fw.POOL_STATS) == STATS
+    return torch, fw
+
+
+def _run(torch, fw, rows, s, extra, max_swaps, threshold=0.25):
+    dev = fw.upload(rows)
+    out = fw.pool_subset(dev["q"], dev["k"], dev["v"], s, extra, max_swaps, dev["scale"], dev["bias"],
+                         flat_threshold=threshold)
+    torch.cuda.synchronize()
+    return {key: t2np(val) for key, val in out.items() if not key.startswith("_")}
+
+
+def _check_rows(rows, s, extra, max_swaps, out, hs, tol, gs=None):
+    """Every row of units hs against the oracle.  Index sets must match or be
+    tie cases: top-mass keys whose logits are within tol of the s-th logit,
+    extra keys whose single-key errors are within tol of the last one taken,
+    and chosen sets whose float64 error is within tol of the oracle's."""
+    q, K, V = rows.as_f64("q"), rows.as_f64("k"), rows.as_f64("v")
+    bias = None if rows.bias is None else rows.bias.astype(np.float64)
+    tally = Tally()
+    for h in hs:
+        for g in (range(rows.G) if gs is None else gs):
+            z = O.logits(q[h, g], K[h], float(rows.scale[h]), bias)
+            ref = O.row_pool(z, V[h], s, extra, max_swaps)
+            p = O.weights(z)
+            pid = out["pool_idx"][h, g]
+            top_ok = np.array_equal(pid[:s], ref["top"])
+            zs = np.sort(z)[::-1]
+            top_tie = set(pid[:s].tolist()) ^ set(ref["top"].tolist()) <= set(
+                np.nonzero(np.abs(z - zs[s - 1]) <= tol * max(1.0, abs(zs[s - 1])))[0].tolist())
+            ex_ok = np.array_equal(pid[s:], ref["extras"])
+            e = O.single_key_errors(p, V[h])
+            last = e[ref["extras"][-1]] if extra else 0.0
+            ex_tie = (not top_ok) or set(pid[s:].tolist()) ^ set(ref["extras"].tolist()) <= set(
+                np.nonzero(np.abs(e - last) <= tol * max(last, 1e-300))[0].tolist())
+            tally.add(top_ok and ex_ok, top_tie and ex_tie, f"pool row {(h, g)}")
+            same_pool = top_ok and ex_ok
+            gb, gbal = out["best_idx"][h, g], out["bal_idx"][h, g]
+            if same_pool:
+                exact = np.array_equal(gb, ref["best_idx"])
+                tie = O.forced_error(p, V[h], gb) <= ref["es_pool"] * (1 + tol) + 1e-15
+                tally.add(exact, tie, f"best row {(h, g)} gpu {gb} ref {ref['best_idx']}")
+                exact = np.array_equal(gbal, ref["bal_idx"]) and out["n_swaps"][h, g] == ref["n_swaps"]
+                tie = abs(O.forced_error(p, V[h], gbal) - ref["es_bal"]) <= tol * ref["es_bal"] + 1e-15
+                tally.add(exact, tie, f"bal row {(h, g)} gpu {gbal} ref {ref['bal_idx']}")
+            floor = 1e-6 * np.linalg.norm(O.dense_output(p, V[h]))
+            st = out["stats"][h, g]
+            for c, name in enumerate(STATS):
+                if not same_pool and name in ("es_pool", "es_bal", "kappa_hat", "c_hat", "kappa_bal"):
+                    continue
+                refv = ref[name]
+                if name == "c_hat":
+                    assert abs(st[c] - refv) <= 10 * tol, (h, g, name, st[c], refv)
+                elif math.isinf(refv):
+                    assert math.isinf(st[c]), (h, g, name)
+                else:
+                    fl = floor if name.startswith(("es", "phi", "bound")) else 1e-12
+                    assert rel_scalar(st[c], refv, fl) <= 10 * tol, (h, g, name, st[c], refv)
+    assert tally.fail == 0, tally
+    return tally
+
+
+def _cells(out, G, threshold=0.25):
+    drop = out["stats"][..., STATS.index("dropped")].astype(np.float64)
+    med = np.array([np.median(drop[h]) for h in range(drop.shape[0])])
+    np.testing.assert_allclose(out["cell_median"], med, rtol=1e-6, atol=1e-9)
+    assert np.array_equal(out["cell_flat"].astype(bool), out["cell_median"] > threshold)
+
+
+def _fp32_rows(seed, H, G, n, d, temp=1.0, sink=0.0):
+    rng = np.random.default_rng(seed)
+    q = (rng.standard_normal((H, G, d)) * temp).astype(np.float32)
+    K = rng.standard_normal((H, n, d)).astype(np.float32)
+    V = rng.standard_normal((H, n, d)).astype(np.float32)
+    bias = None
+    if sink:
+        bias = np.zeros(n, np.float32)
+        bias[0] = sink
+    return W.Rows(W.F32, q, K, V, np.full(H, 1.0 / math.sqrt(d), np.float32), bias)
+
+
+def test_example_2_3_pool_on_gpu(torch_fw):
+    """Example 2.3 as an instance (q = 0, bias = log p): the candidate set with
+    one extra key is every key, ES_pool = 9/22 at {0, 2}, kappa_hat = 11/9,
+    c_hat = 2/11, Phi = 9/20, D = 9/2, sigma^2 = 63/20, one balancing swap."""
+    torch, fw = torch_fw
+    p = np.array([0.45, 0.45, 0.10])
+    rows = W.Rows(W.F32, np.zeros((1, 1, 1), np.float32), np.zeros((1, 3, 1), np.float32),
+                  np.array([[[-1.0], [1.0], [5.0]]], np.float32), np.ones(1, np.float32),
+                  np.log(p).astype(np.float32))
+    out = _run(torch, fw, rows, 2, 1, 8)
+    st = out["stats"][0, 0]
+    assert out["pool_idx"][0, 0].tolist() == [0, 1, 2]
+    assert out["best_idx"][0, 0].tolist() == [0, 2] and out["bal_idx"][0, 0].tolist() == [0, 2]
+    assert out["n_swaps"][0, 0] == 1
+    want = dict(es_top=0.5, es_pool=9 / 22, es_bal=9 / 22, kappa_hat=11 / 9, c_hat=2 / 11, kappa_bal=1.0,
+                dropped=0.1, phi=0.45, diam=4.5, sigma=math.sqrt(3.15), bound_diam=0.9,
+                bound_var=math.sqrt(0.35))
+    for c, name in enumerate(STATS):
+        assert st[c] == pytest.approx(want[name], rel=1e-5), name
+
+
+@pytest.mark.parametrize("cfg", [
+    # (H, G, n, d, s, extra, temp, sink)
+    (3, 7, 48, 16, 4, 8, 2.0, 0.0),     # vectorised rows, odd G (median of one value)
+    (2, 8, 61, 12, 3, 9, 3.0, 4.0),     # ragged n, d not a multiple of 8: one element per lane
+    (2, 6, 40, 64, 8, 12, 1.5, 4.0),    # the s = 8 setting
+    (2, 5, 33, 8, 6, 0, 2.0, 0.0),      # no extra keys: the pool is A*_s
+])
+def test_small_rows_fp32_all(torch_fw, cfg):
+    torch, fw = torch_fw
+    H, G, n, d, s, extra, temp, sink = cfg
+    rows = _fp32_rows(100 + H * n + d, H, G, n, d, temp, sink)
+    out = _run(torch, fw, rows, s, extra, 16)
+    t = _check_rows(rows, s, extra, 16, out, range(H), tol=1e-5)
+    _cells(out, G)
+    print(cfg, t)
+    if extra == 0:
+        assert np.all(out["n_swaps"] == 0)
+        assert np.array_equal(np.sort(out["pool_idx"], axis=-1), out["best_idx"])
+
+
+def test_pool_of_every_key_matches_exhaustive(torch_fw):
+    """s + extra = n: the candidate set is every key, so ES_pool is the full
+    ES that fw_best_subset computes on the same rows."""
+    torch, fw = torch_fw
+    H, G, n, d, s = 2, 8, 16, 32, 4
+    rows = _fp32_rows(9, H, G, n, d, 2.0, 4.0)
+    out = _run(torch, fw, rows, s, n - s, 32)
+    dev = fw.upload(rows)
+    ex = fw.best_subset(dev["q"], dev["k"], dev["v"], s, dev["scale"], dev["bias"])
+    torch.cuda.synchronize()
+    assert np.array_equal(out["best_idx"], t2np(ex["best_idx"]))
+    np.testing.assert_allclose(out["stats"][..., STATS.index("es_pool")], t2np(ex["best_gap"]), rtol=1e-6)
+    _check_rows(rows, s, n - s, 32, out, range(H), tol=1e-5)
+
+
+@pytest.mark.parametrize("budget", [(4, 24), (8, 12), (16, 6), (32, 4)])
+def test_model_rows_bf16(torch_fw, budget):
+    """Model-shaped bf16 rows (outlier channels, sink) at n = 1024, every row."""
+    torch, fw = torch_fw
+    s, extra = budget
+    wl = W.pool_rows(seed=3, layers=1, kv_heads=2, q_per_kv=2, rows_per_q=3, n=1024)
+    out = _run(torch, fw, wl.rows, s, extra, 64)
+    t = _check_rows(wl.rows, s, extra, 64, out, range(wl.rows.H), tol=2e-2)
+    _cells(out, wl.rows.G)
+    print(budget, t)
+
+
+def test_full_size_pool_sampled(torch_fw):
+    """The benchmark's workload (256 units x 24 rows, n = 4096) at every budget
+    in its launch configuration: sampled rows against the oracle, properties
+    of the statistics on all rows."""
+    torch, fw = torch_fw
+    wl = W.pool_rows(seed=0)
+    dev = fw.upload(wl.rows)
+    rng = np.random.default_rng(5)
+    for s, extra in wl.meta["budgets"]:
+        o = fw.pool_subset(dev["q"], dev["k"], dev["v"], s, extra, wl.max_iters, dev["scale"], dev["bias"])
+        torch.cuda.synchronize()
+        out = {key: t2np(val) for key, val in o.items() if not key.startswith("_")}
+        hs = sorted(rng.choice(wl.rows.H, 1, replace=False).tolist())
+        sub = {k2: v2[hs] for k2, v2 in out.items() if v2 is not None and v2.shape[0] == wl.rows.H}
+        unit = wl.rows.unit(hs[0])
+        gs = sorted(rng.choice(wl.rows.G, 4, replace=False).tolist())
+        t = _check_rows(unit, s, extra, wl.max_iters, sub, [0], tol=2e-2, gs=gs)
+        print((s, extra), t)
+        st = out["stats"].reshape(-1, len(STATS))
+        col = {name: st[:, c].astype(np.float64) for c, name in enumerate(STATS)}
+        eps = 1e-5
+        assert np.all(col["kappa_hat"] >= 1 - eps) and np.all((col["c_hat"] >= 0) & (col["c_hat"] <= 1))
+        assert np.all(col["es_pool"] <= col["es_bal"] * (1 + eps) + 1e-12)
+        assert np.all(col["es_bal"] <= col["es_top"] * (1 + eps) + 1e-12)
+        assert np.all(col["es_top"] <= col["bound_diam"] * (1 + eps))
+        assert np.all(col["es_top"] <= col["bound_var"] * (1 + eps))
+        np.testing.assert_allclose(col["phi"], col["es_top"] * (1 - col["dropped"]), rtol=1e-4)
+        assert np.all((out["n_swaps"] >= 0) & (out["n_swaps"] <= wl.max_iters))
+        pid = out["pool_idx"].reshape(-1, s + extra)
+        assert np.all([np.unique(r).size == s + extra for r in pid[:64]]) and pid.min() >= 0 and pid.max() < 4096
+        bi = out["best_idx"].reshape(-1, s)
+        assert np.all(np.diff(bi, axis=1) > 0)
+        _cells(out, wl.rows.G)
