@@ -31,7 +31,7 @@ def _args():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--only", default="", help="comma list: topk,exhaustive,swap,curve,tiny,copy")
+    ap.add_argument("--only", default="", help="comma list: topk,exhaustive,swap,pool,curve,tiny,copy")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     return ap.parse_args()
@@ -223,6 +223,32 @@ def main():
                            "dtype": "bf16",
                            "roofline": dict(_roofline("mfma", mfma_flop / (ms / 1e3) / 1e12, MFMA_BF16_TFLOPS,
                                                       "TFLOP/s"), kernel="fw_swap (all launches)")})
+        del dev, holder
+        torch.cuda.empty_cache()
+
+    # ---- candidate-set search (ES_pool, pool balancing, certificate) -------------
+    if want("pool"):
+        wl = W.pool_rows(seed=0)
+        r = wl.rows
+        dev = fw.upload(r)
+        holder = {}
+
+        def step():
+            o = fw.pool_subset(dev["q"], dev["k"], dev["v"], wl.meta["budgets"], wl.max_iters, dev["scale"],
+                               dev["bias"], ws=holder.get("ws"))
+            holder["ws"] = o["_ws"]
+            holder["n_swaps"] = o["n_swaps"]
+
+        ms, _ = _time(torch, step, max(1, a.steps // 2), 1)
+        R = r.H * r.G
+        subsets = R * sum(math.comb(s_ + e_, s_) for s_, e_ in wl.meta["budgets"])
+        components.append({"workload": wl.name, "metric": "pool subsets evaluated/s",
+                           "value": round(subsets / (ms / 1e3), 1), "unit": "subsets/s", "ms": round(ms, 3),
+                           "rows_per_s": round(R / (ms / 1e3), 1), "subsets": subsets,
+                           "budgets": [list(b) for b in wl.meta["budgets"]],
+                           "median_swaps": {str(s_): float(holder["n_swaps"][b].float().median().item())
+                                            for b, (s_, _) in enumerate(wl.meta["budgets"])},
+                           "dtype": "f64"})
         del dev, holder
         torch.cuda.empty_cache()
 

@@ -125,7 +125,9 @@ fw_status fw_best_subset(const fw_rows *rows, int32_t k, int32_t *best_idx, floa
  * fw_pool_subset -- the candidate-set search of Section 2.2 (Definition 2.5
  * and the appendix's enumeration protocol) on rows of any length, with the
  * per-row certificate statistics of Section 2.3 and the appendix's absolute
- * forms.  Per row, with the full row's masses p and dense output mu:
+ * forms, for up to FW_POOL_MAX_BUDGETS budgets per call (the row's weights,
+ * dense output and key deviations are formed once for all of them).  Per row
+ * and budget (s, extra), with the full row's masses p and dense output mu:
  *   - the candidate set: the top-mass set A*_s (logit desc, index asc) and
  *     the `extra` keys outside it of largest single-key error
  *     p_j ||v_j - mu|| (error desc, index asc);
@@ -136,27 +138,34 @@ fw_status fw_best_subset(const fw_rows *rows, int32_t k, int32_t *best_idx, floa
  *     (kept, dropped) pool swap that most decreases es (ties to the smallest
  *     (out, in)), strict decrease only, at most max_swaps swaps.
  * Arithmetic is float64 throughout.
- *   s, extra       1 <= s, 0 <= extra, s + extra <= min(64, n), with the
- *                  enumeration of C(s + extra, s) subsets plannable
- *                  (it is for every s + extra <= 24, and for the paper's
- *                  (4, 24), (8, 12), (16, 6), (32, 4)); n <= 8192
+ *   n_budgets      1 <= n_budgets <= FW_POOL_MAX_BUDGETS
+ *   s, extra       host [n_budgets]: 1 <= s[b], 0 <= extra[b],
+ *                  s[b] + extra[b] <= min(64, n); pools dropping more than
+ *                  4 keys need a plannable enumeration of C(s + extra, s)
+ *                  subsets (every pool of at most 24 keys is, and the
+ *                  paper's (4, 24), (8, 12), (16, 6), (32, 4)); n <= 8192
  *   max_swaps      0 <= max_swaps <= 4096
- *   pool_idx       [H][G][s+extra] int32 A*_s in rank order, then the extra
- *                  keys in error order, or NULL
- *   best_idx       [H][G][s] int32 the ES_pool argmin, ascending (required)
- *   bal_idx        [H][G][s] int32 the balancing set, ascending, or NULL
- *   n_swaps        [H][G] int32 swaps the balancing selector applied, or NULL
- *   stats          [H][G][FW_POOL_NSTATS] float32 (required), columns
- *                  FW_POOL_* below
- *   flat_threshold, cell_median [H], cell_flat [H] uint8: per unit, the
- *                  median of the rows' dropped mass of A*_s (the mean of the
- *                  two middle values for even G) and whether it exceeds
- *                  flat_threshold (a flat cell at s = 8, threshold 0.25);
- *                  either may be NULL
+ * With P_b = s[b] + extra[b], the budgets' lists are concatenated per row in
+ * the caller's budget order:
+ *   pool_idx       [H][G][sum_b P_b] int32: per budget, A*_s in rank order,
+ *                  then the extra keys in error order, or NULL
+ *   best_idx       [H][G][sum_b s[b]] int32: per budget, the ES_pool argmin,
+ *                  ascending (required)
+ *   bal_idx        [H][G][sum_b s[b]] int32: per budget, the balancing set,
+ *                  ascending, or NULL
+ *   n_swaps        [n_budgets][H][G] int32 balancing swaps applied, or NULL
+ *   stats          [n_budgets][H][G][FW_POOL_NSTATS] float32 (required),
+ *                  columns FW_POOL_* below
+ *   flat_threshold, cell_median [n_budgets][H], cell_flat [n_budgets][H]
+ *                  uint8: per budget and unit, the median of the rows'
+ *                  dropped mass of A*_s (the mean of the two middle values
+ *                  for even G) and whether it exceeds flat_threshold (a flat
+ *                  cell at s = 8, threshold 0.25); either may be NULL
  * kappa values are num/den, 1 when both are 0 and +inf when only den is.
- * Errors: FW_E_UNSUPPORTED when the pool or its enumeration is out of the
+ * Errors: FW_E_UNSUPPORTED when a pool or its enumeration is out of the
  * limits above; FW_E_NULL, FW_E_SHAPE, FW_E_DTYPE, FW_E_WORKSPACE, FW_E_HIP.
  * ------------------------------------------------------------------------- */
+#define FW_POOL_MAX_BUDGETS 4
 #define FW_POOL_NSTATS 12
 #define FW_POOL_ES_TOP 0     /* es(A*_s)                                  */
 #define FW_POOL_ES_POOL 1    /* ES_pool(s)                                */
@@ -170,11 +179,12 @@ fw_status fw_best_subset(const fw_rows *rows, int32_t k, int32_t *best_idx, floa
 #define FW_POOL_SIGMA 9      /* sigma, sigma^2 = sum_j p_j ||v_j - mu||^2 */
 #define FW_POOL_BOUND_DIAM 10 /* 2 D pbar (Lemma 2.2)                     */
 #define FW_POOL_BOUND_VAR 11  /* sqrt(pbar / (1 - pbar)) sigma            */
-size_t fw_pool_subset_workspace_size(const fw_rows *rows, int32_t s, int32_t extra);
-fw_status fw_pool_subset(const fw_rows *rows, int32_t s, int32_t extra, int32_t max_swaps,
-                         int32_t *pool_idx, int32_t *best_idx, int32_t *bal_idx, int32_t *n_swaps,
-                         float *stats, float flat_threshold, float *cell_median, uint8_t *cell_flat,
-                         void *ws, size_t ws_bytes, fw_stream stream);
+size_t fw_pool_subset_workspace_size(const fw_rows *rows, int32_t n_budgets, const int32_t *s,
+                                     const int32_t *extra);
+fw_status fw_pool_subset(const fw_rows *rows, int32_t n_budgets, const int32_t *s, const int32_t *extra,
+                         int32_t max_swaps, int32_t *pool_idx, int32_t *best_idx, int32_t *bal_idx,
+                         int32_t *n_swaps, float *stats, float flat_threshold, float *cell_median,
+                         uint8_t *cell_flat, void *ws, size_t ws_bytes, fw_stream stream);
 
 /* ---------------------------------------------------------------------------
  * fw_swap -- the balancing selector of Section 2.1 ("swap rule"): start at

@@ -147,17 +147,23 @@ fw_status check_compact(int32_t dtype, const void *k, const void *v, int64_t H, 
     return FW_OK;
 }
 
-fw_status check_pool(const fw_rows *rows, int32_t s, int32_t extra, int32_t max_swaps) {
+fw_status check_pool(const fw_rows *rows, int32_t n_budgets, const int32_t *s, const int32_t *extra,
+                     int32_t max_swaps) {
     fw_status st = check_rows(rows, true);
     if (st != FW_OK) return st;
-    if (s < 1 || extra < 0 || (int64_t)s + extra > rows->n)
-        return fail(FW_E_SHAPE, "need 1 <= s, 0 <= extra, s + extra <= n (s=%d extra=%d n=%lld)", s, extra,
-                    (long long)rows->n);
+    if (!s || !extra) return fail(FW_E_NULL, "s and extra are required");
+    if (n_budgets < 1 || n_budgets > FW_POOL_MAX_BUDGETS)
+        return fail(FW_E_SHAPE, "n_budgets must be in [1, %d]", FW_POOL_MAX_BUDGETS);
+    for (int b = 0; b < n_budgets; ++b) {
+        if (s[b] < 1 || extra[b] < 0 || (int64_t)s[b] + extra[b] > rows->n)
+            return fail(FW_E_SHAPE, "budget %d: need 1 <= s, 0 <= extra, s + extra <= n (s=%d extra=%d n=%lld)", b,
+                        s[b], extra[b], (long long)rows->n);
+        if (s[b] + extra[b] > 64) return fail(FW_E_UNSUPPORTED, "budget %d: s + extra = %d > 64 pool keys", b, s[b] + extra[b]);
+    }
     if (max_swaps < 0 || max_swaps > 4096) return fail(FW_E_SHAPE, "max_swaps must be in [0, 4096]");
-    if (s + extra > 64) return fail(FW_E_UNSUPPORTED, "s + extra = %d > 64 pool keys", s + extra);
     if (rows->n > 8192) return fail(FW_E_UNSUPPORTED, "n = %lld > 8192 for the candidate-set search", (long long)rows->n);
-    if (!fw::pool_plan(rows->n, (int)rows->d, s, extra, nullptr, nullptr))
-        return fail(FW_E_UNSUPPORTED, "no enumeration plan for C(%d, %d) within the limits", s + extra, s);
+    if (!fw::pool_plannable(rows->n, (int)rows->d, n_budgets, s, extra))
+        return fail(FW_E_UNSUPPORTED, "no enumeration plan for these budgets within the limits");
     return FW_OK;
 }
 
@@ -227,21 +233,22 @@ fw_status fw_best_subset(const fw_rows *rows, int32_t k, int32_t *best_idx, floa
 }
 
 // ---------------------------------------------------------------------------
-size_t fw_pool_subset_workspace_size(const fw_rows *rows, int32_t s, int32_t extra) {
-    if (check_pool(rows, s, extra, 0) != FW_OK) return 0;
-    return fw::pool_ws_bytes(*rows, s, extra);
+size_t fw_pool_subset_workspace_size(const fw_rows *rows, int32_t n_budgets, const int32_t *s,
+                                     const int32_t *extra) {
+    if (check_pool(rows, n_budgets, s, extra, 0) != FW_OK) return 0;
+    return fw::pool_ws_bytes(*rows, n_budgets, s, extra);
 }
 
-fw_status fw_pool_subset(const fw_rows *rows, int32_t s, int32_t extra, int32_t max_swaps,
-                         int32_t *pool_idx, int32_t *best_idx, int32_t *bal_idx, int32_t *n_swaps,
-                         float *stats, float flat_threshold, float *cell_median, uint8_t *cell_flat,
-                         void *ws, size_t ws_bytes, fw_stream stream) {
-    fw_status st = check_pool(rows, s, extra, max_swaps);
+fw_status fw_pool_subset(const fw_rows *rows, int32_t n_budgets, const int32_t *s, const int32_t *extra,
+                         int32_t max_swaps, int32_t *pool_idx, int32_t *best_idx, int32_t *bal_idx,
+                         int32_t *n_swaps, float *stats, float flat_threshold, float *cell_median,
+                         uint8_t *cell_flat, void *ws, size_t ws_bytes, fw_stream stream) {
+    fw_status st = check_pool(rows, n_budgets, s, extra, max_swaps);
     if (st != FW_OK) return st;
     if (!best_idx || !stats) return fail(FW_E_NULL, "best_idx and stats are required");
-    if ((st = check_ws(ws, ws_bytes, fw::pool_ws_bytes(*rows, s, extra))) != FW_OK) return st;
-    hipError_t e = fw::launch_pool(*rows, s, extra, max_swaps, pool_idx, best_idx, bal_idx, n_swaps, stats,
-                                   flat_threshold, cell_median, cell_flat, ws, (hipStream_t)stream);
+    if ((st = check_ws(ws, ws_bytes, fw::pool_ws_bytes(*rows, n_budgets, s, extra))) != FW_OK) return st;
+    hipError_t e = fw::launch_pool(*rows, n_budgets, s, extra, max_swaps, pool_idx, best_idx, bal_idx, n_swaps,
+                                   stats, flat_threshold, cell_median, cell_flat, ws, (hipStream_t)stream);
     return hip_status(e, "fw_pool_subset");
 }
 

@@ -39,13 +39,11 @@ hipError_t launch_best_subset(const fw_rows &rows, int k, int32_t *best_idx, flo
                               int32_t *topk_idx, void *ws, hipStream_t st);
 
 // k_pool.hip -- candidate-set search (ES_pool, pool balancing, certificate)
-struct EnumPlan;
-bool pool_plan(int64_t N, int d, int s, int extra, EnumPlan *pl, size_t *lds);
-size_t pool_ws_bytes(const fw_rows &rows, int s, int extra);
-hipError_t launch_pool(const fw_rows &rows, int s, int extra, int max_swaps, int32_t *pool_idx,
-                       int32_t *best_idx, int32_t *bal_idx, int32_t *n_swaps, float *stats,
-                       float flat_threshold, float *cell_median, uint8_t *cell_flat, void *ws,
-                       hipStream_t st);
+bool pool_plannable(int64_t N, int d, int nb, const int32_t *s, const int32_t *extra);
+size_t pool_ws_bytes(const fw_rows &rows, int nb, const int32_t *s, const int32_t *extra);
+hipError_t launch_pool(const fw_rows &rows, int nb, const int32_t *s, const int32_t *extra, int max_swaps,
+                       int32_t *pool_idx, int32_t *best_idx, int32_t *bal_idx, int32_t *n_swaps, float *stats,
+                       float flat_threshold, float *cell_median, uint8_t *cell_flat, void *ws, hipStream_t st);
 
 // k_swap.hip -- swap rule
 size_t swap_ws_bytes(const fw_rows &rows, int k, int max_iters);

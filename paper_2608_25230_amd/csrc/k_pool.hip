@@ -31,14 +31,18 @@ namespace {
 constexpr int PT = 256;       // threads per row workgroup
 constexpr int kPoolMax = 64;  // pool keys (one 64-bit mask)
 
+constexpr int kMaxBudgets = FW_POOL_MAX_BUDGETS;
+
 struct PoolLds {
-    size_t xq, mu, red, ctr, pid, ps, sc;  // persistent
-    size_t zz, ee, bits;                   // row phase
-    size_t gm, vs, ent, pl, cv;            // pool phase (overlays the row phase)
+    size_t xq, mu, red, ctr, rank, tmp, plist, pps, sc, seed;  // persistent
+    size_t zz, ee, rk;                                   // row phase
+    size_t gm, vs, cv, ent, pl;                          // pool phase (overlays the row phase)
     size_t total;
 };
 
-__host__ __device__ inline PoolLds pool_lds(int64_t N, int d, int P, int nent) {
+// The pool phase is sized for the largest pool (Pmax keys) and the largest
+// walk table (nentmax entries) of the call's budgets.
+__host__ __device__ inline PoolLds pool_lds(int64_t N, int d, int Pmax, int nentmax) {
     PoolLds L{};
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t at = o; o = align_up(o + bytes, 16); return at; };
@@ -46,20 +50,23 @@ __host__ __device__ inline PoolLds pool_lds(int64_t N, int d, int P, int nent) {
     L.mu = take((size_t)d * 8);
     L.red = take((size_t)PT * 16);
     L.ctr = take(16);
-    L.pid = take((size_t)kPoolMax * 4 * 2);  // pool keys ascending, then in output order
-    L.ps = take((size_t)kPoolMax * 8);
-    L.sc = take((size_t)16 * 8);
+    L.rank = take((size_t)kPoolMax * 4);                // top keys in rank order
+    L.tmp = take((size_t)kPoolMax * 4);                 // a pool in output order
+    L.plist = take((size_t)kMaxBudgets * kPoolMax * 4);  // each pool, ascending keys
+    L.pps = take((size_t)kMaxBudgets * kPoolMax * 8);    // their masses
+    L.sc = take((size_t)(kMaxBudgets + 2) * 8);
+    L.seed = take((size_t)kMaxBudgets * 8);        // each A*_s as a pool mask
     const size_t base = o;
     L.zz = base;
     L.ee = align_up(L.zz + (size_t)N * 8, 16);
-    L.bits = align_up(L.ee + (size_t)N * 8, 16);
-    const size_t row_end = L.bits + (size_t)((N + 63) / 64) * 8;
+    L.rk = align_up(L.ee + (size_t)N * 8, 16);
+    const size_t row_end = L.rk + (size_t)N;
     L.gm = base;
-    L.vs = align_up(L.gm + (size_t)P * P * 8, 16);
-    L.cv = align_up(L.vs + (size_t)P * (d + 1) * 4, 16);
-    L.ent = align_up(L.cv + (size_t)P * 8, 16);
-    L.pl = L.ent + (size_t)nent * 16;
-    const size_t pool_end = L.pl + (size_t)nent * 8;
+    L.vs = align_up(L.gm + (size_t)Pmax * Pmax * 8, 16);
+    L.cv = align_up(L.vs + (size_t)Pmax * (d + 1) * 4, 16);
+    L.ent = align_up(L.cv + (size_t)Pmax * 8, 16);
+    L.pl = L.ent + (size_t)nentmax * 16;
+    const size_t pool_end = L.pl + (size_t)nentmax * 8;
     L.total = align_up(row_end > pool_end ? row_end : pool_end, 16);
     return L;
 }
@@ -69,8 +76,8 @@ __host__ __device__ inline PoolLds pool_lds(int64_t N, int d, int P, int nent) {
 template <typename T> struct RowVec;
 template <> struct RowVec<uint16_t> {
     static constexpr int VEC = 8;
-    __device__ static void load(const uint16_t *row, int c0, float (&x)[8]) {
-        const uint4 w = *(const uint4 *)(row + c0);
+    __device__ static uint4 raw(const uint16_t *row, int c0) { return *(const uint4 *)(row + c0); }
+    __device__ static void unpack(const uint4 &w, float (&x)[8]) {
         const uint32_t u[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -81,9 +88,10 @@ template <> struct RowVec<uint16_t> {
 };
 template <> struct RowVec<float> {
     static constexpr int VEC = 4;
-    __device__ static void load(const float *row, int c0, float (&x)[4]) {
-        const float4 w = *(const float4 *)(row + c0);
-        x[0] = w.x; x[1] = w.y; x[2] = w.z; x[3] = w.w;
+    __device__ static uint4 raw(const float *row, int c0) { return *(const uint4 *)(row + c0); }
+    __device__ static void unpack(const uint4 &w, float (&x)[4]) {
+        x[0] = __uint_as_float(w.x); x[1] = __uint_as_float(w.y);
+        x[2] = __uint_as_float(w.z); x[3] = __uint_as_float(w.w);
     }
 };
 
@@ -103,47 +111,85 @@ __device__ __forceinline__ double group_sum(double v, int GL) {
 
 // For every key j of M [N][d]: f(j, lane_in_group, GL, walk), where
 // walk(g) calls g(c, slot, x) for the lane's elements x = M[j][c]; slot
-// (< 32) numbers them within the lane, the same for every key.  The GL lanes
+// numbers them within the lane (< VEC), the same for every key.  The GL lanes
 // of a group share a key (j = -1 on lanes past the end, which still take part
-// in the group's shuffles).  VEC-wide loads when d is a multiple of VEC, else
-// one element per lane.  d <= 256: at most four chunks (elements) per lane.
+// in the group's shuffles).  With VEC-wide loads (d a multiple of VEC) a
+// group covers a row with one 16-byte chunk per lane (d <= 256 gives at most
+// 64 chunks); otherwise a wave takes one key with up to four elements per
+// lane.  Every lane keeps U keys' loads in flight (raw 16-byte words) before
+// it uses the first: the passes over a row are bound by load latency.
 template <typename T, typename F>
 __device__ void for_keys(const T *M, int64_t N, int d, F &&f) {
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, NW = blockDim.x >> 6;
     constexpr int VEC = RowVec<T>::VEC;
     if (d % VEC == 0) {
+        constexpr int U = 16;
         const int GL = group_lanes(d, VEC), KPW = 64 / GL;  // keys per wave step
         const int gi = lane % GL, gk = lane / GL;
-        const int chunks = d / VEC;
-        for (int64_t j0 = (int64_t)w * KPW; j0 < N; j0 += (int64_t)NW * KPW) {
-            const int64_t j = j0 + gk;
-            const bool ok = j < N;
-            f(ok ? j : -1, gi, GL, [&](auto &&g) {
-                if (!ok) return;
-                const T *row = M + j * d;
+        const bool has = gi < d / VEC;  // GL >= d / VEC: one chunk per lane at most
+        const int64_t stride = (int64_t)NW * KPW;
+        for (int64_t j0 = (int64_t)w * KPW; j0 < N; j0 += stride * U) {
+            uint4 raw[U];
 #pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const int ch = gi + GL * t;
-                    if (ch < chunks) {
-                        float x[VEC];
-                        RowVec<T>::load(row, ch * VEC, x);
+            for (int u = 0; u < U; ++u) {
+                const int64_t j = j0 + u * stride + gk;
+                raw[u] = (j < N && has) ? RowVec<T>::raw(M + j * d, gi * VEC) : make_uint4(0u, 0u, 0u, 0u);
+            }
 #pragma unroll
-                        for (int i = 0; i < VEC; ++i) g(ch * VEC + i, t * VEC + i, x[i]);
-                    }
-                }
-            });
+            for (int u = 0; u < U; ++u) {
+                const int64_t j = j0 + u * stride + gk;
+                const bool ok = j < N;
+                f(ok ? j : -1, gi, GL, [&](auto &&g) {
+                    if (!ok || !has) return;
+                    float x[VEC];
+                    RowVec<T>::unpack(raw[u], x);
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) g(gi * VEC + i, i, x[i]);
+                });
+            }
         }
     } else {
-        for (int64_t j = w; j < N; j += NW) {
-            f(j, lane, 64, [&](auto &&g) {
-                const T *row = M + j * d;
+        constexpr int U = 4;
+        for (int64_t j0 = w; j0 < N; j0 += (int64_t)NW * U) {
+            float x[U][4];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t j = j0 + (int64_t)u * NW;
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
                     const int c = lane + 64 * t;
-                    if (c < d) g(c, t, Elem<T>::load(row, c));
+                    x[u][t] = (j < N && c < d) ? Elem<T>::load(M + j * d, c) : 0.f;
                 }
-            });
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t j = j0 + (int64_t)u * NW;
+                if (j >= N) break;  // uniform across the wave
+                f(j, lane, 64, [&](auto &&g) {
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        if (lane + 64 * t < d) g(lane + 64 * t, t, x[u][t]);
+                });
+            }
         }
+    }
+}
+
+// The columns for_keys hands this lane, by slot: fn(c, slot) once per column.
+template <typename T, typename F>
+__device__ void lane_columns(int d, F &&fn) {
+    const int lane = threadIdx.x & 63;
+    constexpr int VEC = RowVec<T>::VEC;
+    if (d % VEC == 0) {
+        const int gi = lane % group_lanes(d, VEC);
+        if (gi < d / VEC) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) fn(gi * VEC + i, i);
+        }
+    } else {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            if (lane + 64 * t < d) fn(lane + 64 * t, t);
     }
 }
 
@@ -173,13 +219,107 @@ __device__ inline void block_argmax(double &val, int64_t &idx, double *redv, int
 
 __device__ inline double block_sum(double v, double *red) { return block_reduce(v, red, OpSum()); }
 
+// Pools that drop at most this many keys are enumerated through the dropped
+// set: owned parts of the walk would hold nearly every key.
+constexpr int kDirectDrop = 4;
+
+// Every s-subset A of the pool as the complement of a dropped set D of
+// q = P - s keys: with c_i = sum_j Gm_ij over the pool, S_U = sum_i c_i and
+// p_U = p(pool), ||g_A||^2 = S_U - 2 sum_{i in D} c_i + sum_{i,j in D} Gm_ij
+// and p(A) = p_U - p(D).  The colex ranks of D are split into one run per
+// thread, each stepping to the next mask of the same size; ties go to the
+// lexicographically smallest A.  Returns A's mask, block-uniform.
+__device__ inline uint64_t enum_complement(const double *Gm, const double *ps, int P, int q, double *cv,
+                                           double *redd, uint64_t *redm) {
+    const int tid = threadIdx.x, NT = blockDim.x, lane = tid & 63, w = tid >> 6;
+    const uint64_t all = P == 64 ? ~0ull : ((1ull << P) - 1ull);
+    if (q == 0) return all;
+    for (int x = tid; x < P; x += NT) {
+        double c = 0.0;
+        for (int y = 0; y < P; ++y) c += Gm[x * P + y];
+        cv[x] = c;
+    }
+    __syncthreads();
+    double SU = 0.0, pU = 0.0;
+    for (int x = 0; x < P; ++x) {
+        SU += cv[x];
+        pU += ps[x];
+    }
+    const uint64_t total = binom(P, q);
+    const uint64_t lo = total * (uint64_t)tid / (uint64_t)NT, hi = total * (uint64_t)(tid + 1) / (uint64_t)NT;
+    double best = INFINITY;
+    uint64_t bestA = 0;
+    if (lo < hi) {
+        // unrank lo (combinatorial number system, colex)
+        uint64_t D = 0, rr = lo;
+        int c = P - 1;
+        for (int sz = q; sz >= 1; --sz) {
+            while (binom(c, sz) > rr) --c;
+            D |= 1ull << c;
+            rr -= binom(c, sz);
+            --c;
+        }
+        for (uint64_t r = lo; r < hi; ++r) {
+            double S = SU, pD = 0.0;
+            for (uint64_t m = D; m; m &= m - 1) {
+                const int i = __ffsll((unsigned long long)m) - 1;
+                S -= 2.0 * cv[i];
+                pD += ps[i];
+                for (uint64_t m2 = D; m2; m2 &= m2 - 1) S += Gm[i * P + (__ffsll((unsigned long long)m2) - 1)];
+            }
+            const double PA = pU - pD;
+            const double val = fmax(S, 0.0) / (PA * PA);
+            const uint64_t A = all & ~D;
+            if (val < best || (val == best && lex_less(A, bestA))) {
+                best = val;
+                bestA = A;
+            }
+            // next mask of the same size (colex successor)
+            const uint64_t u = D & (~D + 1ull), v = D + u;
+            D = v | (((v ^ D) >> 2) >> (__ffsll((unsigned long long)D) - 1));
+        }
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+        const double ov = __shfl_xor(best, off);
+        const uint64_t om = __shfl_xor(bestA, off);
+        if (ov < best || (ov == best && om != 0 && (bestA == 0 || lex_less(om, bestA)))) {
+            best = ov;
+            bestA = om;
+        }
+    }
+    __syncthreads();
+    if (lane == 0) {
+        redd[w] = best;
+        redm[w] = bestA;
+    }
+    __syncthreads();
+    best = redd[0];
+    bestA = redm[0];
+    for (int i = 1; i < NT / 64; ++i)
+        if (redd[i] < best || (redd[i] == best && redm[i] != 0 && (bestA == 0 || lex_less(redm[i], bestA)))) {
+            best = redd[i];
+            bestA = redm[i];
+        }
+    __syncthreads();
+    return bestA;
+}
+
+// One budget of a call: s kept keys, `extra` keys beyond A*_s, offsets of the
+// row's index lists, and how its pool is enumerated.
+struct PoolBudget {
+    int s, extra, P, pool_off, set_off;
+    int direct;  // through the dropped set (enum_complement), else the walk
+    size_t tab_off;  // the walk tables' offset in the workspace
+    EnumPlan pl;
+    EnumTables tab;
+};
+
 struct PoolArgs {
     const void *q, *k, *v;
     const float *scale, *bias;
     int64_t H, G, N;
-    int d, s, extra, max_swaps;
-    EnumPlan pl;
-    EnumTables tab;
+    int d, nb, max_swaps, Smax, Ptot, Stot, Pmax, nentmax;
+    PoolBudget b[kMaxBudgets];
     int32_t *pool_idx, *best_idx, *bal_idx, *n_swaps;
     float *stats;
 };
@@ -191,20 +331,24 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int tid = threadIdx.x, NT = blockDim.x;
     const int64_t N = a.N;
-    const int d = a.d, s = a.s, P = a.s + a.extra;
-    const PoolLds L = pool_lds(N, d, P, a.pl.nent);
+    const int d = a.d, nb = a.nb;
+    const int64_t R = a.H * a.G;
+    const PoolLds L = pool_lds(N, d, a.Pmax, a.nentmax);
     double *xq = (double *)(smem + L.xq);
     double *mu = (double *)(smem + L.mu);
     double *redd = (double *)(smem + L.red);
     uint64_t *redm = (uint64_t *)(redd + NT);
     int64_t *redi = (int64_t *)(redd + NT);
     int *ctr = (int *)(smem + L.ctr);
-    int *pid = (int *)(smem + L.pid);  // [0, P): ascending keys; [64, 64 + P): output order
-    double *ps = (double *)(smem + L.ps);
-    double *sc = (double *)(smem + L.sc);
+    int *rank = (int *)(smem + L.rank);
+    int *tmp = (int *)(smem + L.tmp);
+    int *plist = (int *)(smem + L.plist);
+    double *pps = (double *)(smem + L.pps);
+    double *sc = (double *)(smem + L.sc);  // [0, nb): dropped masses; nb: sigma^2; nb + 1: D
     double *zz = (double *)(smem + L.zz);
     double *ee = (double *)(smem + L.ee);
-    uint64_t *bits = (uint64_t *)(smem + L.bits);
+    unsigned char *rk = smem + L.rk;  // rank among the top keys, 255 beyond them
+    uint64_t *seeds = (uint64_t *)(smem + L.seed);
 
     const int64_t r = blockIdx.x;
     const int64_t h = r / a.G;
@@ -213,13 +357,17 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
     const T *vh = (const T *)a.v + h * N * d;
     const double scale = a.scale ? (double)a.scale[h] : (double)default_scale(d);
 
-    // ---- 1. the row ---------------------------------------------------------
+    // ---- 1. the row, once for every budget -------------------------------------
     for (int c = tid; c < d; c += NT) xq[c] = (double)Elem<T>::load(qr, c);
-    for (int64_t e = tid; e < (N + 63) / 64; e += NT) bits[e] = 0ull;
+    for (int64_t j = tid; j < N; j += NT) rk[j] = 255;
     __syncthreads();
+    double xr[8];  // this lane's columns of the query (then of mu), in registers
+#pragma unroll
+    for (int i = 0; i < 8; ++i) xr[i] = 0.0;
+    lane_columns<T>(d, [&](int c, int slot) { xr[slot] = xq[c]; });
     for_keys(kh, N, d, [&](int64_t j, int gi, int GL, auto &&walk) {
         double acc = 0.0;
-        walk([&](int c, int, float x) { acc = fma(xq[c], (double)x, acc); });
+        walk([&](int, int slot, float x) { acc = fma(xr[slot], (double)x, acc); });
         acc = group_sum(acc, GL);
         if (j >= 0 && gi == 0) zz[j] = scale * acc + (a.bias ? (double)a.bias[j] : 0.0);
     });
@@ -228,11 +376,12 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
     for (int64_t j = tid; j < N; j += NT) zmax = fmax(zmax, zz[j]);
     zmax = block_reduce(zmax, redd, OpMax());
 
-    // ---- 2a. top-mass set: s rounds, each the next key in (z desc, j asc) ---
+    // top keys in rank order: Smax rounds, each the next key in (z desc, j asc);
+    // every budget's A*_s is a prefix
     {
         double pv = INFINITY;
         int64_t pi = -1;
-        for (int t = 0; t < s; ++t) {
+        for (int t = 0; t < a.Smax; ++t) {
             double bv = 0.0;
             int64_t bi = -1;
             for (int64_t j = tid; j < N; j += NT) {
@@ -241,56 +390,60 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
                 if (after && (bi < 0 || z > bv || (z == bv && j < bi))) { bv = z; bi = j; }
             }
             block_argmax(bv, bi, redd, redi);
-            if (tid == 0 && bi >= 0) {  // s <= n: a key is always found
-                pid[64 + t] = (int)bi;
-                bits[bi >> 6] |= 1ull << (bi & 63);
+            if (tid == 0 && bi >= 0) {  // Smax <= n: a key is always found
+                rank[t] = (int)bi;
+                rk[bi] = (unsigned char)t;
             }
             pv = bv;
             pi = bi;
         }
     }
-    // weights in place of the logits; the dropped mass of A*_s summed over the
-    // dropped keys themselves
+    // weights in place of the logits; each budget's dropped mass summed over
+    // its dropped keys themselves
     double lsum = 0.0;
     for (int64_t j = tid; j < N; j += NT) lsum += exp(zz[j] - zmax);
     lsum = block_sum(lsum, redd);
-    double drop = 0.0;
+    double drop[kMaxBudgets];
+#pragma unroll
+    for (int b = 0; b < kMaxBudgets; ++b) drop[b] = 0.0;
     for (int64_t j = tid; j < N; j += NT) {
         const double p = exp(zz[j] - zmax) / lsum;
         zz[j] = p;
-        if (!((bits[j >> 6] >> (j & 63)) & 1ull)) drop += p;
+        const int rj = rk[j];
+#pragma unroll
+        for (int b = 0; b < kMaxBudgets; ++b)
+            if (b < nb && rj >= a.b[b].s) drop[b] += p;
     }
-    drop = block_sum(drop, redd);  // ends with a barrier: zz holds p
+#pragma unroll
+    for (int b = 0; b < kMaxBudgets; ++b)
+        if (b < nb) drop[b] = block_sum(drop[b], redd);  // barriers: zz holds p
 
     // dense output: each lane accumulates its columns over the keys it visits
     {
         constexpr int VEC = RowVec<T>::VEC;
-        double part[8 * 4];  // up to 4 chunks of VEC columns per lane (d <= 256)
+        double part[8];  // the lane's columns: VEC of one chunk, or up to 4 single ones
 #pragma unroll
-        for (int i = 0; i < 32; ++i) part[i] = 0.0;
+        for (int i = 0; i < 8; ++i) part[i] = 0.0;
         const bool vec = d % VEC == 0;
         const int GL = vec ? group_lanes(d, VEC) : 64;
-        for_keys(vh, N, d, [&](int64_t j, int gi, int, auto &&walk) {
+        for_keys(vh, N, d, [&](int64_t j, int, int, auto &&walk) {
             if (j < 0) return;
             const double p = zz[j];
             walk([&](int, int slot, float x) { part[slot] = fma(p, (double)x, part[slot]); });
         });
-        // combine: partial sums per column through LDS, one column per thread
+        // combine: the (wave, group) partial sums through LDS, one group per round
         for (int c = tid; c < d; c += NT) mu[c] = 0.0;
         __syncthreads();
         const int lane = tid & 63, gi = vec ? lane % GL : lane;
         for (int rnd = 0; rnd < NT / 64 * (64 / GL); ++rnd) {
-            // round rnd: the lanes whose (wave, group) index is rnd add their partials
             const int me = (tid >> 6) * (64 / GL) + lane / GL;
             if (me == rnd) {
                 if (vec) {
 #pragma unroll
-                    for (int t = 0; t < 4; ++t)
-#pragma unroll
-                        for (int i = 0; i < VEC; ++i) {
-                            const int c = (gi + GL * t) * VEC + i;
-                            if (c < d) mu[c] += part[t * VEC + i];
-                        }
+                    for (int i = 0; i < VEC; ++i) {
+                        const int c = gi * VEC + i;
+                        if (c < d) mu[c] += part[i];
+                    }
                 } else {
 #pragma unroll
                     for (int t = 0; t < 4; ++t) {
@@ -305,10 +458,11 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
 
     // deviations: single-key errors, sigma^2 and D
     double s2 = 0.0, dmax = 0.0;
+    lane_columns<T>(d, [&](int c, int slot) { xr[slot] = mu[c]; });
     for_keys(vh, N, d, [&](int64_t j, int gi, int GL, auto &&walk) {
         double acc = 0.0;
-        walk([&](int c, int, float x) {
-            const double t = (double)x - mu[c];
+        walk([&](int, int slot, float x) {
+            const double t = (double)x - xr[slot];
             acc = fma(t, t, acc);
         });
         acc = group_sum(acc, GL);
@@ -322,206 +476,219 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
     s2 = block_sum(s2, redd);
     dmax = block_reduce(dmax, redd, OpMax());
 
-    // ---- 2b. extras: the largest single-key errors outside A*_s ------------
-    {
+    // ---- 2. each budget's candidate set ------------------------------------------
+    for (int b = 0; b < nb; ++b) {
+        const PoolBudget &B = a.b[b];
+        const int s = B.s, P = B.P;
+        // the extra keys: largest single-key errors outside A*_s
         double pv = INFINITY;
         int64_t pi = -1;
-        for (int t = 0; t < a.extra; ++t) {
+        for (int t = 0; t < B.extra; ++t) {
             double bv = 0.0;
             int64_t bi = -1;
             for (int64_t j = tid; j < N; j += NT) {
-                if ((bits[j >> 6] >> (j & 63)) & 1ull) continue;
+                if (rk[j] < s) continue;
                 const double e = ee[j];
                 const bool after = e < pv || (e == pv && j > pi);
                 if (after && (bi < 0 || e > bv || (e == bv && j < bi))) { bv = e; bi = j; }
             }
             block_argmax(bv, bi, redd, redi);
-            if (tid == 0) pid[64 + s + t] = bi >= 0 ? (int)bi : 0;  // s + extra <= n
+            if (tid == 0) tmp[s + t] = bi >= 0 ? (int)bi : 0;  // s + extra <= n
             pv = bv;
             pi = bi;
         }
-    }
-    // pool keys ascending, their masses; the seed (A*_s) as a pool-position mask
-    if (tid < P) {
-        const int key = pid[64 + tid];
-        int rank = 0;
-        for (int u = 0; u < P; ++u) rank += pid[64 + u] < key;
-        pid[rank] = key;
-        ps[rank] = zz[key];
-        if (a.pool_idx) a.pool_idx[r * P + tid] = key;
+        if (tid < s) tmp[tid] = rank[tid];
+        __syncthreads();
+        // output order, then ascending keys with their masses
+        if (tid < P) {
+            const int key = tmp[tid];
+            int pos = 0;
+            for (int u = 0; u < P; ++u) pos += tmp[u] < key;
+            plist[b * kPoolMax + pos] = key;
+            pps[b * kPoolMax + pos] = zz[key];
+            if (a.pool_idx) a.pool_idx[r * a.Ptot + B.pool_off + tid] = key;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            uint64_t seed = 0;
+            for (int i = 0; i < P; ++i)
+                if (rk[plist[b * kPoolMax + i]] < s) seed |= 1ull << i;
+            seeds[b] = seed;
+        }
+        __syncthreads();  // tmp is reused by the next budget
     }
     if (tid == 0) {
-        sc[0] = drop;
-        sc[1] = s2;
-        sc[2] = sqrt(dmax);
+        for (int b = 0; b < nb; ++b) sc[b] = drop[b];
+        sc[nb] = s2;
+        sc[nb + 1] = sqrt(dmax);
     }
     __syncthreads();  // the row arrays are dead from here
-    uint64_t seed = 0;
-    for (int i = 0; i < P; ++i)
-        if ((bits[pid[i] >> 6] >> (pid[i] & 63)) & 1ull) seed |= 1ull << i;
-    __syncthreads();
 
-    // ---- 3. the pool instance -------------------------------------------------
+    // ---- 3.-6. each budget's pool: instance, ES_pool, balancing, statistics -----
     double *Gm = (double *)(smem + L.gm);
     float *Vs = (float *)(smem + L.vs);
     double *cv = (double *)(smem + L.cv);
     double2 *ent = (double2 *)(smem + L.ent);
     double *PLt = (double *)(smem + L.pl);
     const int pitch = d + 1;
-    for (int e = tid; e < P * d; e += NT) {
-        const int i = e / d, c = e % d;
-        Vs[i * pitch + c] = Elem<T>::load(vh, (int64_t)pid[i] * d + c);
-    }
-    __syncthreads();
-    for (int e = tid; e < P * (P + 1) / 2; e += NT) {
-        int i = 0, rem = e;
-        while (rem >= P - i) { rem -= P - i; ++i; }
-        const int j = i + rem;
-        double acc = 0.0;
-        for (int c = 0; c < d; ++c) acc = fma((double)Vs[i * pitch + c] - mu[c], (double)Vs[j * pitch + c] - mu[c], acc);
-        const double g = ps[i] * ps[j] * acc;
-        Gm[i * P + j] = g;
-        Gm[j * P + i] = g;
-    }
-    if (tid == 0) ctr[0] = 0;
-    __syncthreads();
+    for (int b = 0; b < nb; ++b) {
+        const PoolBudget &B = a.b[b];
+        const int s = B.s, P = B.P;
+        const int *pid = plist + b * kPoolMax;
+        const double *ps = pps + b * kPoolMax;
+        const uint64_t seed = seeds[b];
+        // the pool instance
+        for (int e = tid; e < P * d; e += NT) {
+            const int i = e / d, c = e % d;
+            Vs[i * pitch + c] = Elem<T>::load(vh, (int64_t)pid[i] * d + c);
+        }
+        __syncthreads();
+        for (int e = tid; e < P * (P + 1) / 2; e += NT) {
+            int i = 0, rem = e;
+            while (rem >= P - i) { rem -= P - i; ++i; }
+            const int j = i + rem;
+            double acc = 0.0;
+            for (int c = 0; c < d; ++c)
+                acc = fma((double)Vs[i * pitch + c] - mu[c], (double)Vs[j * pitch + c] - mu[c], acc);
+            const double g = ps[i] * ps[j] * acc;
+            Gm[i * P + j] = g;
+            Gm[j * P + i] = g;
+        }
+        if (tid == 0) ctr[0] = 0;
+        __syncthreads();
 
-    // ---- 4. ES_pool --------------------------------------------------------------
-    const uint64_t best = enum_best(a.pl, Gm, ps, seed, a.tab.io, a.tab.wmk, a.tab.jobs, a.tab.omk, ent, PLt,
-                                    redd, redm, ctr);
+        // ES_pool
+        const uint64_t best = B.direct ? enum_complement(Gm, ps, P, P - s, cv, redd, redm)
+                                       : enum_best(B.pl, Gm, ps, seed, B.tab.io, B.tab.wmk, B.tab.jobs, B.tab.omk,
+                                                   ent, PLt, redd, redm, ctr);
 
-    // ---- 5. balancing within the pool --------------------------------------------
-    const uint64_t all = P == 64 ? ~0ull : ((1ull << P) - 1ull);
-    uint64_t A = seed;
-    int swaps = 0;
-    if (s < P) {
-        // Gram value of the current set, recomputed exactly after every swap
-        auto gram_of = [&](uint64_t M, double &S, double &PA) {
-            double v = 0.0, pm = 0.0;
-            for (int e = tid; e < P * P; e += NT) {
-                const int i = e / P, j = e % P;
-                if (((M >> i) & 1ull) && ((M >> j) & 1ull)) v += Gm[e];
-            }
-            for (int i = tid; i < P; i += NT)
-                if ((M >> i) & 1ull) pm += ps[i];
-            S = block_sum(v, redd);
-            PA = block_sum(pm, redd);
-        };
-        double S, PA;
-        gram_of(A, S, PA);
-        double cur = S / (PA * PA);
-        const int nout = P - s;
-        while (swaps < a.max_swaps) {
-            for (int x = tid; x < P; x += NT) {
-                double c = 0.0;
-                for (int y = 0; y < P; ++y)
-                    if ((A >> y) & 1ull) c += Gm[x * P + y];
-                cv[x] = c;
-            }
-            __syncthreads();
-            double bv = 0.0;
-            int64_t bi = -1;
-            for (int t = tid; t < s * nout; t += NT) {
-                const int ii = t / nout, jj = t % nout;
-                // ii-th member and jj-th non-member of A, ascending
-                int i = -1, j = -1;
-                {
-                    int ci = 0, cj = 0;
-                    for (int x = 0; x < P; ++x) {
-                        if ((A >> x) & 1ull) { if (ci++ == ii) i = x; }
-                        else if (cj++ == jj) j = x;
-                    }
+        // balancing within the pool
+        uint64_t A = seed;
+        int swaps = 0;
+        if (s < P) {
+            // Gram value of the current set, recomputed exactly after every swap
+            auto gram_of = [&](uint64_t M, double &S, double &PA) {
+                double v = 0.0, pm = 0.0;
+                for (int e = tid; e < P * P; e += NT) {
+                    const int i = e / P, j = e % P;
+                    if (((M >> i) & 1ull) && ((M >> j) & 1ull)) v += Gm[e];
                 }
-                if (i < 0 || j < 0) continue;  // A always holds s of the P keys
-                const double Sn = S - 2.0 * cv[i] + Gm[i * P + i] + 2.0 * (cv[j] - Gm[i * P + j]) + Gm[j * P + j];
-                const double Pn = PA - ps[i] + ps[j];
-                const double val = fmax(Sn, 0.0) / (Pn * Pn);
-                // argmax of -val; ties to the smallest (out, in) = smallest t
-                if (bi < 0 || -val > bv) { bv = -val; bi = t; }
-            }
-            block_argmax(bv, bi, redd, redi);
-            if (bi < 0 || !(-bv < cur)) break;
-            const int ii = (int)(bi / nout), jj = (int)(bi % nout);
-            int i = -1, j = -1;
-            {
+                for (int i = tid; i < P; i += NT)
+                    if ((M >> i) & 1ull) pm += ps[i];
+                S = block_sum(v, redd);
+                PA = block_sum(pm, redd);
+            };
+            double S, PA;
+            gram_of(A, S, PA);
+            double cur = S / (PA * PA);
+            const int nout = P - s;
+            // ii-th member and jj-th non-member of A, ascending
+            auto pick = [&](int ii, int jj, int &i, int &j) {
                 int ci = 0, cj = 0;
+                i = j = -1;
                 for (int x = 0; x < P; ++x) {
                     if ((A >> x) & 1ull) { if (ci++ == ii) i = x; }
                     else if (cj++ == jj) j = x;
                 }
+            };
+            while (swaps < a.max_swaps) {
+                for (int x = tid; x < P; x += NT) {
+                    double c = 0.0;
+                    for (int y = 0; y < P; ++y)
+                        if ((A >> y) & 1ull) c += Gm[x * P + y];
+                    cv[x] = c;
+                }
+                __syncthreads();
+                double bv = 0.0;
+                int64_t bi = -1;
+                for (int t = tid; t < s * nout; t += NT) {
+                    int i, j;
+                    pick(t / nout, t % nout, i, j);
+                    if (i < 0 || j < 0) continue;  // A always holds s of the P keys
+                    const double Sn = S - 2.0 * cv[i] + Gm[i * P + i] + 2.0 * (cv[j] - Gm[i * P + j]) + Gm[j * P + j];
+                    const double Pn = PA - ps[i] + ps[j];
+                    const double val = fmax(Sn, 0.0) / (Pn * Pn);
+                    // argmax of -val; ties to the smallest (out, in) = smallest t
+                    if (bi < 0 || -val > bv) { bv = -val; bi = t; }
+                }
+                block_argmax(bv, bi, redd, redi);
+                if (bi < 0 || !(-bv < cur)) break;
+                int i, j;
+                pick((int)(bi / nout), (int)(bi % nout), i, j);
+                if (i < 0 || j < 0) break;
+                A = (A & ~(1ull << i)) | (1ull << j);
+                ++swaps;
+                gram_of(A, S, PA);
+                cur = S / (PA * PA);
             }
-            if (i < 0 || j < 0) break;
-            A = (A & ~(1ull << i)) | (1ull << j);
-            ++swaps;
-            gram_of(A, S, PA);
-            cur = S / (PA * PA);
         }
-        (void)all;
-    }
 
-    // ---- 6. reported errors and statistics -------------------------------------
-    // es(M) = ||sum_{i in M} p_i (v_i - mu)|| / p(M) over the pool's staged rows
-    auto es_of = [&](uint64_t M) {
-        if ((int64_t)__popcll(M) == N) return 0.0;
-        double g2 = 0.0;
-        for (int c = tid; c < d; c += NT) {
-            double g = 0.0;
-            for (uint64_t m = M; m; m &= m - 1) {
-                const int i = __ffsll((unsigned long long)m) - 1;
-                g = fma(ps[i], (double)Vs[i * pitch + c] - mu[c], g);
+        // reported errors: es(M) = ||sum_{i in M} p_i (v_i - mu)|| / p(M)
+        auto es_of = [&](uint64_t M) {
+            if ((int64_t)__popcll(M) == N) return 0.0;
+            double g2 = 0.0;
+            for (int c = tid; c < d; c += NT) {
+                double g = 0.0;
+                for (uint64_t m = M; m; m &= m - 1) {
+                    const int i = __ffsll((unsigned long long)m) - 1;
+                    g = fma(ps[i], (double)Vs[i * pitch + c] - mu[c], g);
+                }
+                g2 = fma(g, g, g2);
             }
-            g2 = fma(g, g, g2);
-        }
-        g2 = block_sum(g2, redd);
-        double pm = 0.0;
-        for (uint64_t m = M; m; m &= m - 1) pm += ps[__ffsll((unsigned long long)m) - 1];
-        return sqrt(g2) / pm;
-    };
-    const double es_top = es_of(seed);
-    const double es_pool = es_of(best);
-    const double es_bal = es_of(A);
-    if (tid == 0) {
-        int t = 0, u = 0;
-        for (int i = 0; i < P; ++i) {
-            if (((best >> i) & 1ull) && t < s) a.best_idx[r * s + t++] = pid[i];
-            if (a.bal_idx && ((A >> i) & 1ull) && u < s) a.bal_idx[r * s + u++] = pid[i];
-        }
-        if (a.n_swaps) a.n_swaps[r] = swaps;
-        const double m = sc[0], sigma = sqrt(sc[1]), D = sc[2];
-        double ptop = 0.0;
-        for (int i = 0; i < P; ++i)
-            if ((seed >> i) & 1ull) ptop += ps[i];
-        auto ratio = [](double num, double den) {
-            return den > 0.0 ? num / den : (num == 0.0 ? 1.0 : (double)INFINITY);
+            g2 = block_sum(g2, redd);
+            double pm = 0.0;
+            for (uint64_t m = M; m; m &= m - 1) pm += ps[__ffsll((unsigned long long)m) - 1];
+            return sqrt(g2) / pm;
         };
-        float *o = a.stats + r * FW_POOL_NSTATS;
-        o[0] = (float)es_top;
-        o[1] = (float)es_pool;
-        o[2] = (float)es_bal;
-        o[3] = (float)ratio(es_top, es_pool);
-        o[4] = (float)(es_top > 0.0 ? 1.0 - es_pool / es_top : 0.0);
-        o[5] = (float)ratio(es_bal, es_pool);
-        o[6] = (float)m;
-        o[7] = (float)(es_top * ptop);
-        o[8] = (float)D;
-        o[9] = (float)sigma;
-        o[10] = (float)(2.0 * D * m);
-        o[11] = (float)(m < 1.0 ? sqrt(m / (1.0 - m)) * sigma : (double)INFINITY);
+        const double es_top = es_of(seed);
+        const double es_pool = es_of(best);
+        const double es_bal = es_of(A);
+        if (tid == 0) {
+            int t = 0, u = 0;
+            for (int i = 0; i < P; ++i) {
+                if (((best >> i) & 1ull) && t < s) a.best_idx[r * a.Stot + B.set_off + t++] = pid[i];
+                if (a.bal_idx && ((A >> i) & 1ull) && u < s) a.bal_idx[r * a.Stot + B.set_off + u++] = pid[i];
+            }
+            if (a.n_swaps) a.n_swaps[b * R + r] = swaps;
+            const double m = sc[b], sigma = sqrt(sc[nb]), D = sc[nb + 1];
+            double ptop = 0.0;
+            for (int i = 0; i < P; ++i)
+                if ((seed >> i) & 1ull) ptop += ps[i];
+            auto ratio = [](double num, double den) {
+                return den > 0.0 ? num / den : (num == 0.0 ? 1.0 : (double)INFINITY);
+            };
+            float *o = a.stats + (b * R + r) * FW_POOL_NSTATS;
+            o[0] = (float)es_top;
+            o[1] = (float)es_pool;
+            o[2] = (float)es_bal;
+            o[3] = (float)ratio(es_top, es_pool);
+            o[4] = (float)(es_top > 0.0 ? 1.0 - es_pool / es_top : 0.0);
+            o[5] = (float)ratio(es_bal, es_pool);
+            o[6] = (float)m;
+            o[7] = (float)(es_top * ptop);
+            o[8] = (float)D;
+            o[9] = (float)sigma;
+            o[10] = (float)(2.0 * D * m);
+            o[11] = (float)(m < 1.0 ? sqrt(m / (1.0 - m)) * sigma : (double)INFINITY);
+        }
+        __syncthreads();  // the next budget overwrites the pool arrays
     }
 }
 
-// Per cell: the median of the dropped mass over its G rows (the mean of the
-// two middle values for even G), and the flat label median > threshold.
-__global__ void __launch_bounds__(256) pool_cell_kernel(const float *stats, int64_t G, float threshold,
+// Per cell and budget: the median of the dropped mass over the cell's G rows
+// (the mean of the two middle values for even G), and the flat label
+// median > threshold.  Grid: (H, budgets).
+__global__ void __launch_bounds__(256) pool_cell_kernel(const float *stats, int64_t H, int64_t G, float threshold,
                                                         float *cell_median, uint8_t *cell_flat) {
     __shared__ float lo_hi[2];
-    const int64_t h = blockIdx.x;
+    const int64_t h = blockIdx.x, b = blockIdx.y;
+    const float *st = stats + (b * H * G + h * G) * FW_POOL_NSTATS + FW_POOL_DROPPED;
     const int64_t lo = (G - 1) / 2, hi = G / 2;
     for (int64_t g = threadIdx.x; g < G; g += blockDim.x) {
-        const float x = stats[(h * G + g) * FW_POOL_NSTATS + 6];
+        const float x = st[g * FW_POOL_NSTATS];
         int64_t rank = 0;
         for (int64_t u = 0; u < G; ++u) {
-            const float y = stats[(h * G + u) * FW_POOL_NSTATS + 6];
+            const float y = st[u * FW_POOL_NSTATS];
             rank += (y < x) || (y == x && u < g);
         }
         if (rank == lo) lo_hi[0] = x;
@@ -530,43 +697,85 @@ __global__ void __launch_bounds__(256) pool_cell_kernel(const float *stats, int6
     __syncthreads();
     if (threadIdx.x == 0) {
         const float med = (float)(0.5 * ((double)lo_hi[0] + (double)lo_hi[1]));
-        if (cell_median) cell_median[h] = med;
-        if (cell_flat) cell_flat[h] = med > threshold ? 1 : 0;
+        if (cell_median) cell_median[b * H + h] = med;
+        if (cell_flat) cell_flat[b * H + h] = med > threshold ? 1 : 0;
     }
 }
 
 // ---------------------------------------------------------------------------
-bool pool_plan(int64_t N, int d, int s, int extra, EnumPlan *pl, size_t *lds) {
-    const int P = s + extra;
-    if (P > kPoolMax || P > N || s < 1) return false;
-    if (binom(P, s) >= (1ull << 31)) return false;
-    EnumPlan p;
-    if (!choose_plan(P, s, &p)) return false;
-    p.d = d;
-    p.G = 1;
-    const size_t L = pool_lds(N, d, P, p.nent).total;
-    if (L > 160 * 1024) return false;
-    if (pl) *pl = p;
-    if (lds) *lds = L;
+// Host: plans of every budget, launch configuration.
+namespace {
+struct PoolPlan {
+    int nb, Smax, Ptot, Stot, Pmax, nentmax;
+    PoolBudget b[kMaxBudgets];
+    size_t lds, ws;
+};
+
+bool make_pool_plan(int64_t N, int d, int nb, const int32_t *s, const int32_t *extra, PoolPlan *out) {
+    if (nb < 1 || nb > kMaxBudgets) return false;
+    PoolPlan pp{};
+    pp.nb = nb;
+    size_t ws = 0;
+    for (int b = 0; b < nb; ++b) {
+        const int sb = s[b], eb = extra[b], P = sb + eb;
+        if (sb < 1 || eb < 0 || P > kPoolMax || P > N) return false;
+        PoolBudget &B = pp.b[b];
+        B.s = sb;
+        B.extra = eb;
+        B.P = P;
+        B.pool_off = pp.Ptot;
+        B.set_off = pp.Stot;
+        pp.Ptot += P;
+        pp.Stot += sb;
+        pp.Smax = sb > pp.Smax ? sb : pp.Smax;
+        pp.Pmax = P > pp.Pmax ? P : pp.Pmax;
+        B.direct = eb <= kDirectDrop;
+        if (!B.direct) {
+            if (binom(P, sb) >= (1ull << 31)) return false;
+            if (!choose_plan(P, sb, &B.pl)) return false;
+            B.pl.d = d;
+            B.pl.G = 1;
+            pp.nentmax = B.pl.nent > pp.nentmax ? B.pl.nent : pp.nentmax;
+            ws = align_up(ws, 256);
+            B.tab_off = ws;
+            ws += enum_tables(B.pl, nullptr).bytes;
+        }
+    }
+    pp.lds = pool_lds(N, d, pp.Pmax, pp.nentmax).total;
+    if (pp.lds > 160 * 1024) return false;
+    // 0 is the size query's answer for invalid arguments: a call whose pools
+    // are all enumerated directly asks for a token 256 bytes it does not use
+    pp.ws = ws ? align_up(ws, 256) : 256;
+    *out = pp;
     return true;
 }
+}  // namespace
 
-size_t pool_ws_bytes(const fw_rows &rows, int s, int extra) {
-    EnumPlan p;
-    if (!pool_plan(rows.n, (int)rows.d, s, extra, &p, nullptr)) return 0;
-    return enum_tables(p, nullptr).bytes;
+bool pool_plannable(int64_t N, int d, int nb, const int32_t *s, const int32_t *extra) {
+    PoolPlan pp;
+    return make_pool_plan(N, d, nb, s, extra, &pp);
 }
 
-hipError_t launch_pool(const fw_rows &rows, int s, int extra, int max_swaps, int32_t *pool_idx,
-                       int32_t *best_idx, int32_t *bal_idx, int32_t *n_swaps, float *stats,
-                       float flat_threshold, float *cell_median, uint8_t *cell_flat, void *ws,
-                       hipStream_t st) {
+size_t pool_ws_bytes(const fw_rows &rows, int nb, const int32_t *s, const int32_t *extra) {
+    PoolPlan pp;
+    if (!make_pool_plan(rows.n, (int)rows.d, nb, s, extra, &pp)) return 0;
+    return pp.ws;
+}
+
+hipError_t launch_pool(const fw_rows &rows, int nb, const int32_t *s, const int32_t *extra, int max_swaps,
+                       int32_t *pool_idx, int32_t *best_idx, int32_t *bal_idx, int32_t *n_swaps, float *stats,
+                       float flat_threshold, float *cell_median, uint8_t *cell_flat, void *ws, hipStream_t st) {
+    PoolPlan pp;
+    if (!make_pool_plan(rows.n, (int)rows.d, nb, s, extra, &pp)) return hipErrorInvalidConfiguration;
     PoolArgs a{};
-    size_t lds = 0;
-    if (!pool_plan(rows.n, (int)rows.d, s, extra, &a.pl, &lds)) return hipErrorInvalidConfiguration;
-    a.tab = enum_tables(a.pl, ws);
-    hipError_t e = launch_enum_tables(a.pl, a.tab, st);
-    if (e != hipSuccess) return e;
+    hipError_t e = hipSuccess;
+    for (int b = 0; b < nb; ++b) {
+        a.b[b] = pp.b[b];
+        if (!a.b[b].direct) {
+            a.b[b].tab = enum_tables(a.b[b].pl, (char *)ws + a.b[b].tab_off);
+            if ((e = launch_enum_tables(a.b[b].pl, a.b[b].tab, st)) != hipSuccess) return e;
+        }
+    }
     a.q = rows.q;
     a.k = rows.k;
     a.v = rows.v;
@@ -576,9 +785,13 @@ hipError_t launch_pool(const fw_rows &rows, int s, int extra, int max_swaps, int
     a.G = rows.G;
     a.N = rows.n;
     a.d = (int)rows.d;
-    a.s = s;
-    a.extra = extra;
+    a.nb = nb;
     a.max_swaps = max_swaps;
+    a.Smax = pp.Smax;
+    a.Ptot = pp.Ptot;
+    a.Stot = pp.Stot;
+    a.Pmax = pp.Pmax;
+    a.nentmax = pp.nentmax;
     a.pool_idx = pool_idx;
     a.best_idx = best_idx;
     a.bal_idx = bal_idx;
@@ -586,13 +799,13 @@ hipError_t launch_pool(const fw_rows &rows, int s, int extra, int max_swaps, int
     a.stats = stats;
     const unsigned R = (unsigned)(rows.H * rows.G);
     if (rows.dtype == FW_BF16)
-        hipLaunchKernelGGL(pool_row_kernel<uint16_t>, dim3(R), dim3(PT), lds, st, a);
+        hipLaunchKernelGGL(pool_row_kernel<uint16_t>, dim3(R), dim3(PT), pp.lds, st, a);
     else
-        hipLaunchKernelGGL(pool_row_kernel<float>, dim3(R), dim3(PT), lds, st, a);
+        hipLaunchKernelGGL(pool_row_kernel<float>, dim3(R), dim3(PT), pp.lds, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (cell_median || cell_flat)
-        hipLaunchKernelGGL(pool_cell_kernel, dim3((unsigned)rows.H), dim3(256), 0, st, stats, rows.G,
-                           flat_threshold, cell_median, cell_flat);
+        hipLaunchKernelGGL(pool_cell_kernel, dim3((unsigned)rows.H, (unsigned)nb), dim3(256), 0, st, stats, rows.H,
+                           rows.G, flat_threshold, cell_median, cell_flat);
     return hipGetLastError();
 }
 

@@ -54,8 +54,8 @@ _SIGS = {
     "fw_ragged_compact_workspace_size": (SZ, [I64, I64, I64, I64]),
     "fw_ragged_compact": (I32, [I32, P, P, I64, I64, I64, I64, P, I64, I32, P, P, P, P, P, P, P,
                                 P, SZ, P]),
-    "fw_pool_subset_workspace_size": (SZ, [RP, I32, I32]),
-    "fw_pool_subset": (I32, [RP, I32, I32, I32, P, P, P, P, P, ctypes.c_float, P, P, P, SZ, P]),
+    "fw_pool_subset_workspace_size": (SZ, [RP, I32, P, P]),
+    "fw_pool_subset": (I32, [RP, I32, P, P, I32, P, P, P, P, P, ctypes.c_float, P, P, P, SZ, P]),
     "fw_last_error": (ctypes.c_char_p, []),
     "fw_version": (ctypes.c_char_p, []),
 }
@@ -194,27 +194,45 @@ def swap(q, k, v, kb: int, max_iters: int, scale=None, bias=None, *, ws=None) ->
     return out
 
 
-def pool_subset(q, k, v, s: int, extra: int, max_swaps: int, scale=None, bias=None, *,
+def pool_subset(q, k, v, budgets: Sequence, max_swaps: int, scale=None, bias=None, *,
                 flat_threshold: float = 0.25, want_cells=True, ws=None) -> Dict[str, object]:
+    """budgets: a sequence of (s, extra).  Returns, per budget b (lists in the
+    same order): pool_idx[b] [H][G][s+extra], best_idx[b] and bal_idx[b]
+    [H][G][s] (views of the concatenated per-row lists the library writes),
+    and stacked n_swaps [nb][H][G], stats [nb][H][G][12], cell_median and
+    cell_flat [nb][H]."""
     torch = _torch()
     rows = _rows(q, k, v, scale, bias)
     H, G = rows.H, rows.G
     dev = q.device
-    out = {"pool_idx": torch.empty((H, G, s + extra), dtype=torch.int32, device=dev),
-           "best_idx": torch.empty((H, G, s), dtype=torch.int32, device=dev),
-           "bal_idx": torch.empty((H, G, s), dtype=torch.int32, device=dev),
-           "n_swaps": torch.empty((H, G), dtype=torch.int32, device=dev),
-           "stats": torch.empty((H, G, len(POOL_STATS)), dtype=torch.float32, device=dev),
-           "cell_median": torch.empty(H, dtype=torch.float32, device=dev) if want_cells else None,
-           "cell_flat": torch.empty(H, dtype=torch.uint8, device=dev) if want_cells else None}
+    nb = len(budgets)
+    sv = (ctypes.c_int32 * nb)(*[int(b[0]) for b in budgets])
+    ev = (ctypes.c_int32 * nb)(*[int(b[1]) for b in budgets])
+    Ptot = sum(int(b[0]) + int(b[1]) for b in budgets)
+    Stot = sum(int(b[0]) for b in budgets)
+    pool = torch.empty((H, G, Ptot), dtype=torch.int32, device=dev)
+    best = torch.empty((H, G, Stot), dtype=torch.int32, device=dev)
+    bal = torch.empty((H, G, Stot), dtype=torch.int32, device=dev)
+    out = {"n_swaps": torch.empty((nb, H, G), dtype=torch.int32, device=dev),
+           "stats": torch.empty((nb, H, G, len(POOL_STATS)), dtype=torch.float32, device=dev),
+           "cell_median": torch.empty((nb, H), dtype=torch.float32, device=dev) if want_cells else None,
+           "cell_flat": torch.empty((nb, H), dtype=torch.uint8, device=dev) if want_cells else None}
     L = lib()
-    need = L.fw_pool_subset_workspace_size(ctypes.byref(rows), s, extra)
+    need = L.fw_pool_subset_workspace_size(ctypes.byref(rows), nb, sv, ev)
     if ws is None or ws.numel() < need:
         ws = _workspace(need, dev)
-    _check(L.fw_pool_subset(ctypes.byref(rows), s, extra, max_swaps, _ptr(out["pool_idx"]),
-                            _ptr(out["best_idx"]), _ptr(out["bal_idx"]), _ptr(out["n_swaps"]),
-                            _ptr(out["stats"]), float(flat_threshold), _ptr(out["cell_median"]),
-                            _ptr(out["cell_flat"]), ws.data_ptr(), ws.numel(), _stream()))
+    _check(L.fw_pool_subset(ctypes.byref(rows), nb, sv, ev, max_swaps, pool.data_ptr(), best.data_ptr(),
+                            bal.data_ptr(), _ptr(out["n_swaps"]), _ptr(out["stats"]), float(flat_threshold),
+                            _ptr(out["cell_median"]), _ptr(out["cell_flat"]), ws.data_ptr(), ws.numel(),
+                            _stream()))
+    po = so = 0
+    out["pool_idx"], out["best_idx"], out["bal_idx"] = [], [], []
+    for s_, e_ in budgets:
+        out["pool_idx"].append(pool[..., po:po + s_ + e_])
+        out["best_idx"].append(best[..., so:so + s_])
+        out["bal_idx"].append(bal[..., so:so + s_])
+        po += s_ + e_
+        so += s_
     out["_ws"] = ws
     return out
 

@@ -128,24 +128,30 @@ def test_compact_validation(L):
 
 def test_pool_subset_validation(L):
     r = _rows(n=64, d=8)
-    call = lambda rows, s, extra, ms=4, best=1, stats=1, ws=1, wsb=1 << 40: L.fw_pool_subset(
-        rows, s, extra, ms, None, best, None, None, stats, 0.25, None, None, ws, wsb, None)
-    assert call(None, 4, 4) == 1
-    assert call(ctypes.byref(_rows(dtype=7)), 4, 4) == 3
-    assert call(ctypes.byref(_rows(v=None)), 4, 4) == 1
-    assert call(ctypes.byref(r), 0, 4) == 2            # s < 1
-    assert call(ctypes.byref(r), 4, -1) == 2           # extra < 0
-    assert call(ctypes.byref(_rows(n=6)), 4, 4) == 2   # s + extra > n
-    assert call(ctypes.byref(r), 4, 4, ms=-1) == 2
-    assert call(ctypes.byref(r), 4, 4, ms=5000) == 2
-    assert call(ctypes.byref(_rows(n=200)), 40, 30) == 4   # more than 64 pool keys
-    assert call(ctypes.byref(_rows(n=9000)), 4, 4) == 4    # row longer than 8192
-    assert call(ctypes.byref(r), 4, 4, best=None) == 1
-    assert call(ctypes.byref(r), 4, 4, stats=None) == 1
-    assert call(ctypes.byref(r), 4, 4, ws=None) == 5
-    assert call(ctypes.byref(r), 4, 4, wsb=0) == 5
-    assert L.fw_pool_subset_workspace_size(ctypes.byref(r), 4, 4) > 0
-    assert L.fw_pool_subset_workspace_size(ctypes.byref(_rows(n=200)), 40, 30) == 0
-    # the paper's four (s, extra) settings are all plannable
-    for s, e in ((4, 24), (8, 12), (16, 6), (32, 4)):
-        assert L.fw_pool_subset_workspace_size(ctypes.byref(_rows(n=4096, d=128)), s, e) > 0
+    def call(rows, s=(4,), e=(8,), ms=4, best=1, stats=1, ws=1, wsb=1 << 40, nb=None):
+        sv, ev = _ks(*s), _ks(*e)
+        return L.fw_pool_subset(rows, len(s) if nb is None else nb, sv, ev, ms, None, best, None, None, stats,
+                                0.25, None, None, ws, wsb, None)
+    assert call(None) == 1
+    assert call(ctypes.byref(_rows(dtype=7))) == 3
+    assert call(ctypes.byref(_rows(v=None))) == 1
+    assert call(ctypes.byref(r), s=(0,)) == 2                 # s < 1
+    assert call(ctypes.byref(r), e=(-1,)) == 2                # extra < 0
+    assert call(ctypes.byref(_rows(n=6))) == 2                # s + extra > n
+    assert call(ctypes.byref(r), ms=-1) == 2
+    assert call(ctypes.byref(r), ms=5000) == 2
+    assert call(ctypes.byref(r), s=(4, 8), e=(8, 4), nb=0) == 2
+    assert call(ctypes.byref(r), s=(1,) * 5, e=(1,) * 5) == 2   # more than FW_POOL_MAX_BUDGETS
+    assert call(ctypes.byref(_rows(n=200)), s=(40,), e=(30,)) == 4   # more than 64 pool keys
+    assert call(ctypes.byref(_rows(n=9000))) == 4             # row longer than 8192
+    assert call(ctypes.byref(r), best=None) == 1
+    assert call(ctypes.byref(r), stats=None) == 1
+    assert call(ctypes.byref(r), ws=None) == 5
+    assert call(ctypes.byref(r), wsb=0) == 5
+    ws = lambda rows, s, e: L.fw_pool_subset_workspace_size(rows, len(s), _ks(*s), _ks(*e))
+    assert ws(ctypes.byref(r), (4,), (8,)) > 0
+    assert ws(ctypes.byref(r), (4,), (2,)) > 0                # dropped-set enumeration: a token size
+    assert ws(ctypes.byref(_rows(n=200)), (40,), (30,)) == 0
+    # the paper's four (s, extra) settings in one call
+    big = _rows(n=4096, d=128)
+    assert ws(ctypes.byref(big), (4, 8, 16, 32), (24, 12, 6, 4)) > 0

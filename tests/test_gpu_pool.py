@@ -29,12 +29,16 @@ def torch_fw():
     return torch, fw
 
 
-def _run(torch, fw, rows, s, extra, max_swaps, threshold=0.25):
+def _run(torch, fw, rows, budgets, max_swaps, threshold=0.25):
+    """One call for every budget; a numpy dict per budget."""
     dev = fw.upload(rows)
-    out = fw.pool_subset(dev["q"], dev["k"], dev["v"], s, extra, max_swaps, dev["scale"], dev["bias"],
-                         flat_threshold=threshold)
+    o = fw.pool_subset(dev["q"], dev["k"], dev["v"], budgets, max_swaps, dev["scale"], dev["bias"],
+                       flat_threshold=threshold)
     torch.cuda.synchronize()
-    return {key: t2np(val) for key, val in out.items() if not key.startswith("_")}
+    return [{"pool_idx": t2np(o["pool_idx"][b]), "best_idx": t2np(o["best_idx"][b]),
+             "bal_idx": t2np(o["bal_idx"][b]), "n_swaps": t2np(o["n_swaps"][b]), "stats": t2np(o["stats"][b]),
+             "cell_median": t2np(o["cell_median"][b]), "cell_flat": t2np(o["cell_flat"][b])}
+            for b in range(len(budgets))]
 
 
 def _check_rows(rows, s, extra, max_swaps, out, hs, tol, gs=None):
@@ -115,7 +119,7 @@ def test_example_2_3_pool_on_gpu(torch_fw):
     rows = W.Rows(W.F32, np.zeros((1, 1, 1), np.float32), np.zeros((1, 3, 1), np.float32),
                   np.array([[[-1.0], [1.0], [5.0]]], np.float32), np.ones(1, np.float32),
                   np.log(p).astype(np.float32))
-    out = _run(torch, fw, rows, 2, 1, 8)
+    out = _run(torch, fw, rows, [(2, 1)], 8)[0]
     st = out["stats"][0, 0]
     assert out["pool_idx"][0, 0].tolist() == [0, 1, 2]
     assert out["best_idx"][0, 0].tolist() == [0, 2] and out["bal_idx"][0, 0].tolist() == [0, 2]
@@ -133,12 +137,14 @@ def test_example_2_3_pool_on_gpu(torch_fw):
     (2, 8, 61, 12, 3, 9, 3.0, 4.0),     # ragged n, d not a multiple of 8: one element per lane
     (2, 6, 40, 64, 8, 12, 1.5, 4.0),    # the s = 8 setting
     (2, 5, 33, 8, 6, 0, 2.0, 0.0),      # no extra keys: the pool is A*_s
+    (2, 6, 50, 16, 30, 3, 2.5, 4.0),    # few dropped keys: enumeration through the dropped set
+    (2, 6, 20, 16, 2, 4, 3.0, 0.0),     # dropped set larger than the kept set, still direct
 ])
 def test_small_rows_fp32_all(torch_fw, cfg):
     torch, fw = torch_fw
     H, G, n, d, s, extra, temp, sink = cfg
     rows = _fp32_rows(100 + H * n + d, H, G, n, d, temp, sink)
-    out = _run(torch, fw, rows, s, extra, 16)
+    out = _run(torch, fw, rows, [(s, extra)], 16)[0]
     t = _check_rows(rows, s, extra, 16, out, range(H), tol=1e-5)
     _cells(out, G)
     print(cfg, t)
@@ -147,13 +153,31 @@ def test_small_rows_fp32_all(torch_fw, cfg):
         assert np.array_equal(np.sort(out["pool_idx"], axis=-1), out["best_idx"])
 
 
+def test_several_budgets_in_one_call(torch_fw):
+    """Walk and dropped-set enumerations, an empty extra set and a repeated
+    budget in one call: each budget's lists and statistics match the oracle
+    and a call with that budget alone."""
+    torch, fw = torch_fw
+    H, G, n, d = 2, 6, 40, 32
+    rows = _fp32_rows(77, H, G, n, d, 2.0, 4.0)
+    budgets = [(4, 8), (10, 3), (2, 0), (4, 8)]
+    outs = _run(torch, fw, rows, budgets, 16)
+    for (s, extra), out in zip(budgets, outs):
+        t = _check_rows(rows, s, extra, 16, out, range(H), tol=1e-5)
+        _cells(out, G)
+        alone = _run(torch, fw, rows, [(s, extra)], 16)[0]
+        for key in ("pool_idx", "best_idx", "bal_idx", "n_swaps", "stats"):
+            assert np.array_equal(out[key], alone[key]), (s, extra, key)
+        print((s, extra), t)
+
+
 def test_pool_of_every_key_matches_exhaustive(torch_fw):
     """s + extra = n: the candidate set is every key, so ES_pool is the full
     ES that fw_best_subset computes on the same rows."""
     torch, fw = torch_fw
     H, G, n, d, s = 2, 8, 16, 32, 4
     rows = _fp32_rows(9, H, G, n, d, 2.0, 4.0)
-    out = _run(torch, fw, rows, s, n - s, 32)
+    out = _run(torch, fw, rows, [(s, n - s)], 32)[0]
     dev = fw.upload(rows)
     ex = fw.best_subset(dev["q"], dev["k"], dev["v"], s, dev["scale"], dev["bias"])
     torch.cuda.synchronize()
@@ -162,35 +186,33 @@ def test_pool_of_every_key_matches_exhaustive(torch_fw):
     _check_rows(rows, s, n - s, 32, out, range(H), tol=1e-5)
 
 
-@pytest.mark.parametrize("budget", [(4, 24), (8, 12), (16, 6), (32, 4)])
-def test_model_rows_bf16(torch_fw, budget):
-    """Model-shaped bf16 rows (outlier channels, sink) at n = 1024, every row."""
+def test_model_rows_bf16(torch_fw):
+    """Model-shaped bf16 rows (outlier channels, sink) at n = 1024, every row,
+    the paper's four budgets in one call."""
     torch, fw = torch_fw
-    s, extra = budget
     wl = W.pool_rows(seed=3, layers=1, kv_heads=2, q_per_kv=2, rows_per_q=3, n=1024)
-    out = _run(torch, fw, wl.rows, s, extra, 64)
-    t = _check_rows(wl.rows, s, extra, 64, out, range(wl.rows.H), tol=2e-2)
-    _cells(out, wl.rows.G)
-    print(budget, t)
+    budgets = wl.meta["budgets"]
+    outs = _run(torch, fw, wl.rows, budgets, 64)
+    for (s, extra), out in zip(budgets, outs):
+        t = _check_rows(wl.rows, s, extra, 64, out, range(wl.rows.H), tol=2e-2)
+        _cells(out, wl.rows.G)
+        print((s, extra), t)
 
 
 def test_full_size_pool_sampled(torch_fw):
-    """The benchmark's workload (256 units x 24 rows, n = 4096) at every budget
-    in its launch configuration: sampled rows against the oracle, properties
-    of the statistics on all rows."""
+    """The benchmark's workload (256 units x 24 rows, n = 4096, the paper's
+    four budgets in one call): sampled rows against the oracle, properties of
+    the statistics on all rows."""
     torch, fw = torch_fw
     wl = W.pool_rows(seed=0)
-    dev = fw.upload(wl.rows)
+    budgets = wl.meta["budgets"]
+    outs = _run(torch, fw, wl.rows, budgets, wl.max_iters)
     rng = np.random.default_rng(5)
-    for s, extra in wl.meta["budgets"]:
-        o = fw.pool_subset(dev["q"], dev["k"], dev["v"], s, extra, wl.max_iters, dev["scale"], dev["bias"])
-        torch.cuda.synchronize()
-        out = {key: t2np(val) for key, val in o.items() if not key.startswith("_")}
+    for (s, extra), out in zip(budgets, outs):
         hs = sorted(rng.choice(wl.rows.H, 1, replace=False).tolist())
         sub = {k2: v2[hs] for k2, v2 in out.items() if v2 is not None and v2.shape[0] == wl.rows.H}
-        unit = wl.rows.unit(hs[0])
         gs = sorted(rng.choice(wl.rows.G, 4, replace=False).tolist())
-        t = _check_rows(unit, s, extra, wl.max_iters, sub, [0], tol=2e-2, gs=gs)
+        t = _check_rows(wl.rows.unit(hs[0]), s, extra, wl.max_iters, sub, [0], tol=2e-2, gs=gs)
         print((s, extra), t)
         st = out["stats"].reshape(-1, len(STATS))
         col = {name: st[:, c].astype(np.float64) for c, name in enumerate(STATS)}
@@ -203,7 +225,7 @@ def test_full_size_pool_sampled(torch_fw):
         np.testing.assert_allclose(col["phi"], col["es_top"] * (1 - col["dropped"]), rtol=1e-4)
         assert np.all((out["n_swaps"] >= 0) & (out["n_swaps"] <= wl.max_iters))
         pid = out["pool_idx"].reshape(-1, s + extra)
-        assert np.all([np.unique(r).size == s + extra for r in pid[:64]]) and pid.min() >= 0 and pid.max() < 4096
+        assert all(np.unique(r).size == s + extra for r in pid[:64]) and pid.min() >= 0 and pid.max() < 4096
         bi = out["best_idx"].reshape(-1, s)
         assert np.all(np.diff(bi, axis=1) > 0)
         _cells(out, wl.rows.G)
