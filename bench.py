@@ -4,8 +4,9 @@
 Default run: the streaming top-k workload (32 layers x 8 kv heads x 256 query
 rows, n = 4096, d = 128, bf16, budgets 128/512/1024) timed as the headline
 (attention rows per second), plus one pass of every other entry point on its
-own workload as components (exhaustive subsets/s, swap pairs/s, curve and
-compaction GB/s, and the tiny exhaustive case).  Prints ONE JSON line.
+own workload as components (exhaustive subsets/s, swap pairs/s, candidate-set
+subsets/s, curve and compaction GB/s, and the tiny exhaustive case).  Prints
+ONE JSON line.
 
 Timing: W warm-up passes, then K timed passes bracketed by device
 synchronisation, with HIP events recorded on the stream the library launches
@@ -242,9 +243,17 @@ def main():
         ms, _ = _time(torch, step, max(1, a.steps // 2), 1)
         R = r.H * r.G
         subsets = R * sum(math.comb(s_ + e_, s_) for s_, e_ in wl.meta["budgets"])
+        # float64 lane-ops of the method: per row the logits, the dense output
+        # and the deviations (4 n d: one multiply-add per element, plus the
+        # subtraction of the deviations), and per pool subset the walk's five
+        # (as for the exhaustive search); peak = 256 CUs x 4 SIMDs x 16 lanes
+        lane_ops = R * 4 * r.n * r.d + 5 * subsets
         components.append({"workload": wl.name, "metric": "pool subsets evaluated/s",
                            "value": round(subsets / (ms / 1e3), 1), "unit": "subsets/s", "ms": round(ms, 3),
                            "rows_per_s": round(R / (ms / 1e3), 1), "subsets": subsets,
+                           "roofline": dict(_roofline("alu", lane_ops / (ms / 1e3) / 1e12,
+                                                      round(VALU_LANE_OPS / 1e12, 2), "TOP/s"),
+                                            kernel="pool_row_kernel", lane_ops=lane_ops),
                            "budgets": [list(b) for b in wl.meta["budgets"]],
                            "median_swaps": {str(s_): float(holder["n_swaps"][b].float().median().item())
                                             for b, (s_, _) in enumerate(wl.meta["budgets"])},

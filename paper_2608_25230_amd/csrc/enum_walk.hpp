@@ -25,7 +25,7 @@ namespace fw {
 // the answer is never worse than it.  ent [nent] (double2), PLt [nent],
 // redd [NT] (double), redm [NT] (uint64) and ctr[1] are LDS scratch.
 // Returns the best mask, block-uniform.
-__device__ inline uint64_t enum_best(const EnumPlan &pl, const double *Gm, const double *ps, uint64_t seed_mask,
+__device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const double *Gm, const double *ps, uint64_t seed_mask,
                                      const uint2 *__restrict__ g_io, const uint64_t *__restrict__ g_wmk,
                                      const EnumJob *__restrict__ g_jobs, const uint64_t *__restrict__ g_omk,
                                      double2 *ent, double *PLt, double *redd, uint64_t *redm, int *ctr) {
@@ -199,6 +199,16 @@ __device__ inline uint64_t enum_best(const EnumPlan &pl, const double *Gm, const
     const uint64_t best = redm[0];
     __syncthreads();
     return best;
+}
+
+// The same walk, inlined or called at the compiler's choice (the candidate-set
+// kernel, whose row phase already holds many registers); the exhaustive
+// kernel calls the body inlined, which keeps it at four waves per SIMD.
+__device__ inline uint64_t enum_best(const EnumPlan &pl, const double *Gm, const double *ps, uint64_t seed_mask,
+                                     const uint2 *__restrict__ g_io, const uint64_t *__restrict__ g_wmk,
+                                     const EnumJob *__restrict__ g_jobs, const uint64_t *__restrict__ g_omk,
+                                     double2 *ent, double *PLt, double *redd, uint64_t *redm, int *ctr) {
+    return enum_best_body(pl, Gm, ps, seed_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd, redm, ctr);
 }
 
 }  // namespace fw

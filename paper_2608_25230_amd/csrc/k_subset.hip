@@ -180,7 +180,7 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
     // top-k set: rank by (z desc, index asc)
     const uint64_t top_mask = topk_mask64(zs, n, kk, topk_idx ? topk_idx + r * kk : nullptr, redm);
     // (Vs is dead: instance64 ends with a barrier)
-    const uint64_t best = enum_best(pl, Gm, ps, top_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd, redm, ctr);
+    const uint64_t best = enum_best_body(pl, Gm, ps, top_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd, redm, ctr);
     if (tid == 0) {
         int i = 0;
         for (uint64_t a = best; a; a &= a - 1) best_idx[r * kk + i++] = __ffsll((unsigned long long)a) - 1;
