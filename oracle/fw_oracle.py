@@ -515,3 +515,33 @@ def cell_median(dropped: np.ndarray) -> float:
     s = 8, exceeds 0.25: Definition 2.5).  An even count averages the two
     middle values."""
     return float(np.median(np.asarray(dropped, np.float64)))
+
+
+# ----------------------------------------------------------------------------
+# Group vote (Section 2.1, the paragraph on deployment's one kept set per KV
+# head): the s keys of largest mass summed over the group's rows, and what it
+# costs each row against its own top-mass set
+# ----------------------------------------------------------------------------
+
+
+def group_vote(Z: np.ndarray, V: np.ndarray, s: int) -> Dict[str, object]:
+    """Z [m][n] holds the logits of the m query rows that share one key/value
+    head (the group), V [n][d] its values.  The vote keeps the s keys of
+    largest mass summed over the group's rows (ties to the lower index); each
+    row is then evaluated with the vote's set under its own forced weights.
+    Returns the vote set in rank order and, per row, es(vote), es(A*_s) of the
+    row's own top-mass set, their ratio (kappa conventions of ``ratio``) and
+    the vote's dropped mass."""
+    Z = np.asarray(Z, np.float64)
+    P = weights(Z)
+    score = P.sum(axis=0)
+    vote = np.lexsort((np.arange(score.size), -score))[:s]
+    vs = np.sort(vote)
+    es_vote, es_top, drop = [], [], []
+    for r in range(Z.shape[0]):
+        es_vote.append(forced_error(P[r], V, vs))
+        es_top.append(forced_error(P[r], V, np.sort(top_mass_set(Z[r], s))))
+        drop.append(dropped_mass(P[r], vs))
+    es_vote, es_top = np.array(es_vote), np.array(es_top)
+    return dict(vote=vote, score=score, es_vote=es_vote, es_top=es_top,
+                ratio=np.array([ratio(a, b) for a, b in zip(es_vote, es_top)]), dropped=np.array(drop))

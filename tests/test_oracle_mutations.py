@@ -39,6 +39,8 @@ def _run_all_pins():
     checks += [(P.test_pool_of_every_key_is_the_full_search, s) for s in range(3)]
     checks += [(P.test_pool_swap_invariants, s) for s in range(3)]
     checks += [(P.test_certificate_identities_and_bounds, s) for s in range(3)]
+    checks += [(P.test_group_vote_of_one_row_is_its_top_mass_set, s) for s in range(3)]
+    checks += [(P.test_group_vote_brute_force, s) for s in range(3)]
     return any(_fails(*c) for c in checks)
 
 
@@ -148,7 +150,24 @@ def _var_bound_inverted(p, V, S):
 
 _ORIG_CERT = O.certificate
 
+
+def _vote_by_max(Z, V, s):
+    # votes on the largest single-row mass instead of the summed mass
+    Z = np.asarray(Z, np.float64)
+    P = O.weights(Z)
+    score = P.max(axis=0)
+    vote = np.lexsort((np.arange(score.size), -score))[:s]
+    r = _ORIG_VOTE(Z, V, s)
+    r["vote"] = vote
+    vs = np.sort(vote)
+    r["es_vote"] = np.array([O.forced_error(P[i], V, vs) for i in range(Z.shape[0])])
+    return r
+
+
+_ORIG_VOTE = O.group_vote
+
 MUTANTS = {
+    "group_vote_by_max_mass": ("group_vote", _vote_by_max),
     "pool_extras_by_mass": ("candidate_pool", _extras_by_mass),
     "pool_extras_repeat_top": ("candidate_pool", _extras_may_repeat_top),
     "pool_renormalised_within_pool": ("pool_best_subset", _pool_renormalised),

@@ -528,3 +528,42 @@ def test_cell_median():
     assert O.cell_median(np.array([0.1, 0.3, 0.2])) == pytest.approx(0.2)
     assert O.cell_median(np.array([0.1, 0.4, 0.2, 0.3])) == pytest.approx(0.25)
     assert O.ratio(0.0, 0.0) == 1.0 and O.ratio(1.0, 0.0) == math.inf
+
+
+# ---------------------------------------------------------------------------
+# Group vote (Section 2.1)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(3))
+def test_group_vote_of_one_row_is_its_top_mass_set(seed):
+    """A group of one row (the multi-head family of the paper) votes exactly
+    that row's top-mass set, at ratio 1."""
+    rng = np.random.default_rng(800 + seed)
+    z, p, V = _rand_instance(rng, 12, 3, temp=2.0)
+    r = O.group_vote(z[None, :], V, 4)
+    assert r["vote"].tolist() == O.top_mass_set(z, 4).tolist()
+    assert r["es_vote"][0] == r["es_top"][0] and r["ratio"][0] == 1.0
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_group_vote_brute_force(seed):
+    """The vote set holds the most summed mass of all s-subsets (ties to the
+    lexicographically first), each row's error is the forced-weight error of
+    that set, and identical rows vote their common top-mass set."""
+    rng = np.random.default_rng(810 + seed)
+    m, n, d, s = 3, 8, 2, 3
+    Z = rng.standard_normal((m, n)) * 2.0
+    V = rng.standard_normal((n, d))
+    if seed == 2:
+        Z[:, 6] = Z[:, 5]  # tied summed masses: the lower index first
+    r = O.group_vote(Z, V, s)
+    P = np.exp(Z - Z.max(1, keepdims=True))
+    P /= P.sum(1, keepdims=True)
+    best = max(itertools.combinations(range(n), s), key=lambda A: (round(P[:, list(A)].sum(), 12), [-a for a in A]))
+    assert sorted(r["vote"].tolist()) == list(best)
+    for i in range(m):
+        assert r["es_vote"][i] == pytest.approx(O.forced_error(P[i], V, list(best)), rel=1e-12)
+        assert r["dropped"][i] == pytest.approx(1.0 - P[i, list(best)].sum(), rel=1e-10)
+    same = O.group_vote(np.repeat(Z[:1], 4, axis=0), V, s)
+    assert same["vote"].tolist() == O.top_mass_set(Z[0], s).tolist()
+    assert np.all(same["ratio"] == 1.0)
