@@ -5,7 +5,8 @@ Default run: the streaming top-k workload (32 layers x 8 kv heads x 256 query
 rows, n = 4096, d = 128, bf16, budgets 128/512/1024) timed as the headline
 (attention rows per second), plus one pass of every other entry point on its
 own workload as components (exhaustive subsets/s, swap pairs/s, candidate-set
-subsets/s, curve and compaction GB/s, and the tiny exhaustive case).  Prints
+subsets/s, group-vote rows/s, curve and compaction GB/s, and the tiny
+exhaustive case).  Prints
 ONE JSON line.
 
 Timing: W warm-up passes, then K timed passes bracketed by device
@@ -32,7 +33,7 @@ def _args():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--only", default="", help="comma list: topk,exhaustive,swap,pool,curve,tiny,copy")
+    ap.add_argument("--only", default="", help="comma list: topk,exhaustive,swap,pool,vote,curve,tiny,copy")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     return ap.parse_args()
@@ -257,6 +258,34 @@ def main():
                            "budgets": [list(b) for b in wl.meta["budgets"]],
                            "median_swaps": {str(s_): float(holder["n_swaps"][b].float().median().item())
                                             for b, (s_, _) in enumerate(wl.meta["budgets"])},
+                           "dtype": "f64"})
+        del dev, holder
+        torch.cuda.empty_cache()
+
+    # ---- group vote ------------------------------------------------------------------
+    if want("vote"):
+        wl = W.pool_rows(seed=0)
+        r = wl.rows
+        dev = fw.upload(r)
+        holder = {}
+        gs, sv = 4, 8  # the 4 query heads of a key/value head, at s = 8
+
+        def step():
+            holder["out"] = fw.group_vote(dev["q"], dev["k"], dev["v"], sv, gs, dev["scale"], dev["bias"])
+
+        ms, _ = _time(torch, step, max(1, a.steps // 2), 1)
+        R = r.H * r.G
+        o = holder["out"]
+        ratio = (o["es_vote"] / o["es_top"].clamp_min(1e-30)).float().median().item()
+        # float64 lane-ops of the method: per row the logits and the dense
+        # output (one multiply-add per element each)
+        lane_ops = R * 2 * r.n * r.d
+        components.append({"workload": wl.name + "_vote", "metric": "group-vote rows/s",
+                           "value": round(R / (ms / 1e3), 1), "unit": "rows/s", "ms": round(ms, 3),
+                           "group_size": gs, "s": sv, "median_es_vote_over_es_top": round(ratio, 4),
+                           "roofline": dict(_roofline("alu", lane_ops / (ms / 1e3) / 1e12,
+                                                      round(VALU_LANE_OPS / 1e12, 2), "TOP/s"),
+                                            kernel="vote_group_kernel", lane_ops=lane_ops),
                            "dtype": "f64"})
         del dev, holder
         torch.cuda.empty_cache()

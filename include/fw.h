@@ -187,6 +187,31 @@ fw_status fw_pool_subset(const fw_rows *rows, int32_t n_budgets, const int32_t *
                          uint8_t *cell_flat, void *ws, size_t ws_bytes, fw_stream stream);
 
 /* ---------------------------------------------------------------------------
+ * fw_group_vote -- the group vote of Section 2.1: deployment keeps one set
+ * per key/value head for the group of query rows that share it; the vote
+ * keeps the s keys of largest mass summed over the group's rows (ties to the
+ * lower index).  Each unit's G rows are ordered (query head) x (position),
+ * G = group_size x T; the group of position t is the group_size rows
+ * qh*T + t.  Per row, its forced-weight error under the vote's set and under
+ * its own top-mass set (logit desc, index asc), from float64 sums.
+ *   s           1 <= s <= min(n, 256)
+ *   group_size  query heads per key/value head, dividing G
+ *   vote_idx    [H][T][s] int32 the vote's keys by summed mass, descending
+ *               (required)
+ *   es_vote     [H][G] float32 es of the vote's set (required)
+ *   es_top      [H][G] float32 es of the row's own top-mass set (required)
+ *   dropped     [H][G] float32 the row's dropped mass under the vote's set,
+ *               1 - p(vote), or NULL
+ * The workspace query returns 0: no workspace is used (ws may be NULL).
+ * Errors: FW_E_UNSUPPORTED when n, d and the group size need more than
+ * 160 KiB of LDS (n <= 8192 always fits at d <= 256 and group_size <= 16);
+ * FW_E_NULL, FW_E_SHAPE, FW_E_DTYPE, FW_E_HIP.
+ * ------------------------------------------------------------------------- */
+size_t fw_group_vote_workspace_size(const fw_rows *rows, int32_t s, int32_t group_size);
+fw_status fw_group_vote(const fw_rows *rows, int32_t s, int32_t group_size, int32_t *vote_idx, float *es_vote,
+                        float *es_top, float *dropped, void *ws, size_t ws_bytes, fw_stream stream);
+
+/* ---------------------------------------------------------------------------
  * fw_swap -- the balancing selector of Section 2.1 ("swap rule"): start at
  * the top-k set and repeatedly apply the single (kept i, dropped j) swap that
  * most decreases es, over the full neighbourhood, accepting only a strict

@@ -309,3 +309,28 @@ fw_status fw_ragged_compact(int32_t dtype, const void *k, const void *v, int64_t
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+size_t fw_group_vote_workspace_size(const fw_rows *rows, int32_t s, int32_t group_size) {
+    (void)rows;
+    (void)s;
+    (void)group_size;
+    return 0;
+}
+
+fw_status fw_group_vote(const fw_rows *rows, int32_t s, int32_t group_size, int32_t *vote_idx, float *es_vote,
+                        float *es_top, float *dropped, void *ws, size_t ws_bytes, fw_stream stream) {
+    (void)ws;
+    (void)ws_bytes;
+    fw_status st = check_rows(rows, true);
+    if (st != FW_OK) return st;
+    if (group_size < 1 || rows->G % group_size != 0)
+        return fail(FW_E_SHAPE, "group_size must divide G (G=%lld group_size=%d)", (long long)rows->G, group_size);
+    if (s < 1 || s > rows->n) return fail(FW_E_SHAPE, "s must be in [1, n=%lld], got %d", (long long)rows->n, s);
+    if (s > 256) return fail(FW_E_UNSUPPORTED, "s = %d > 256", s);
+    if (!fw::vote_supported(*rows, s, group_size))
+        return fail(FW_E_UNSUPPORTED, "n, d and the group size need more than 160 KiB of LDS");
+    if (!vote_idx || !es_vote || !es_top) return fail(FW_E_NULL, "vote_idx, es_vote and es_top are required");
+    hipError_t e = fw::launch_vote(*rows, s, group_size, vote_idx, es_vote, es_top, dropped, (hipStream_t)stream);
+    return hip_status(e, "fw_group_vote");
+}

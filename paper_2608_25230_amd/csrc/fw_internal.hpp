@@ -45,6 +45,11 @@ hipError_t launch_pool(const fw_rows &rows, int nb, const int32_t *s, const int3
                        int32_t *pool_idx, int32_t *best_idx, int32_t *bal_idx, int32_t *n_swaps, float *stats,
                        float flat_threshold, float *cell_median, uint8_t *cell_flat, void *ws, hipStream_t st);
 
+// k_vote.hip -- group vote
+bool vote_supported(const fw_rows &rows, int s, int gs);
+hipError_t launch_vote(const fw_rows &rows, int s, int gs, int32_t *vote_idx, float *es_vote, float *es_top,
+                       float *dropped, hipStream_t st);
+
 // k_swap.hip -- swap rule
 size_t swap_ws_bytes(const fw_rows &rows, int k, int max_iters);
 hipError_t launch_swap(const fw_rows &rows, int k, int max_iters, int32_t *s_idx, float *gap_traj,

@@ -1,0 +1,159 @@
+// Passes over the key or value rows of one attention row, for kernels that
+// run one workgroup per row (or per group of rows) in float64: vector loads
+// of whole key rows by groups of lanes with many rows' loads in flight, and
+// workgroup reductions.
+#pragma once
+
+#include "fw_common.hpp"
+
+namespace fw {
+
+// Key rows are read by groups of lanes: a group of GL lanes covers one key,
+// each lane VEC consecutive columns per load (whole rows per instruction).
+template <typename T> struct RowVec;
+template <> struct RowVec<uint16_t> {
+    static constexpr int VEC = 8;
+    __device__ static uint4 raw(const uint16_t *row, int c0) { return *(const uint4 *)(row + c0); }
+    __device__ static void unpack(const uint4 &w, float (&x)[8]) {
+        const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[2 * i] = __uint_as_float(u[i] << 16);
+            x[2 * i + 1] = __uint_as_float(u[i] & 0xFFFF0000u);
+        }
+    }
+};
+template <> struct RowVec<float> {
+    static constexpr int VEC = 4;
+    __device__ static uint4 raw(const float *row, int c0) { return *(const uint4 *)(row + c0); }
+    __device__ static void unpack(const uint4 &w, float (&x)[4]) {
+        x[0] = __uint_as_float(w.x); x[1] = __uint_as_float(w.y);
+        x[2] = __uint_as_float(w.z); x[3] = __uint_as_float(w.w);
+    }
+};
+
+// lanes per key for rows of d elements: a power of two covering d / VEC chunks
+__host__ __device__ inline int group_lanes(int d, int vec) {
+    const int chunks = (d + vec - 1) / vec;
+    int g = 1;
+    while (g < chunks && g < 64) g <<= 1;
+    return g;
+}
+
+// Sum over the GL lanes of a group (GL a power of two <= 64).
+__device__ __forceinline__ double group_sum(double v, int GL) {
+    for (int off = 1; off < GL; off <<= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
+// For every key j of M [N][d]: f(j, lane_in_group, GL, walk), where
+// walk(g) calls g(c, slot, x) for the lane's elements x = M[j][c]; slot
+// numbers them within the lane (< VEC), the same for every key.  The GL lanes
+// of a group share a key (j = -1 on lanes past the end, which still take part
+// in the group's shuffles).  With VEC-wide loads (d a multiple of VEC) a
+// group covers a row with one 16-byte chunk per lane (d <= 256 gives at most
+// 64 chunks); otherwise a wave takes one key with up to four elements per
+// lane.  Every lane keeps U keys' loads in flight (raw 16-byte words) before
+// it uses the first: the passes over a row are bound by load latency.
+template <typename T, typename F>
+__device__ void for_keys(const T *M, int64_t N, int d, F &&f) {
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, NW = blockDim.x >> 6;
+    constexpr int VEC = RowVec<T>::VEC;
+    if (d % VEC == 0) {
+        constexpr int U = 16;
+        const int GL = group_lanes(d, VEC), KPW = 64 / GL;  // keys per wave step
+        const int gi = lane % GL, gk = lane / GL;
+        const bool has = gi < d / VEC;  // GL >= d / VEC: one chunk per lane at most
+        const int64_t stride = (int64_t)NW * KPW;
+        for (int64_t j0 = (int64_t)w * KPW; j0 < N; j0 += stride * U) {
+            uint4 raw[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t j = j0 + u * stride + gk;
+                raw[u] = (j < N && has) ? RowVec<T>::raw(M + j * d, gi * VEC) : make_uint4(0u, 0u, 0u, 0u);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t j = j0 + u * stride + gk;
+                const bool ok = j < N;
+                f(ok ? j : -1, gi, GL, [&](auto &&g) {
+                    if (!ok || !has) return;
+                    float x[VEC];
+                    RowVec<T>::unpack(raw[u], x);
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) g(gi * VEC + i, i, x[i]);
+                });
+            }
+        }
+    } else {
+        constexpr int U = 4;
+        for (int64_t j0 = w; j0 < N; j0 += (int64_t)NW * U) {
+            float x[U][4];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t j = j0 + (int64_t)u * NW;
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const int c = lane + 64 * t;
+                    x[u][t] = (j < N && c < d) ? Elem<T>::load(M + j * d, c) : 0.f;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t j = j0 + (int64_t)u * NW;
+                if (j >= N) break;  // uniform across the wave
+                f(j, lane, 64, [&](auto &&g) {
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        if (lane + 64 * t < d) g(lane + 64 * t, t, x[u][t]);
+                });
+            }
+        }
+    }
+}
+
+// The columns for_keys hands this lane, by slot: fn(c, slot) once per column.
+template <typename T, typename F>
+__device__ void lane_columns(int d, F &&fn) {
+    const int lane = threadIdx.x & 63;
+    constexpr int VEC = RowVec<T>::VEC;
+    if (d % VEC == 0) {
+        const int gi = lane % group_lanes(d, VEC);
+        if (gi < d / VEC) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) fn(gi * VEC + i, i);
+        }
+    } else {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            if (lane + 64 * t < d) fn(lane + 64 * t, t);
+    }
+}
+
+// Workgroup argmax of (key desc, index asc) over per-thread candidates
+// (idx < 0: none).  Returns the winner on every thread.
+__device__ inline void block_argmax(double &val, int64_t &idx, double *redv, int64_t *redi) {
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, NW = blockDim.x >> 6;
+    auto better = [](double v1, int64_t i1, double v2, int64_t i2) {
+        if (i1 < 0) return false;
+        if (i2 < 0) return true;
+        return v1 > v2 || (v1 == v2 && i1 < i2);
+    };
+    for (int off = 32; off > 0; off >>= 1) {
+        const double ov = __shfl_xor(val, off);
+        const int64_t oi = __shfl_xor(idx, off);
+        if (better(ov, oi, val, idx)) { val = ov; idx = oi; }
+    }
+    __syncthreads();
+    if (lane == 0) { redv[w] = val; redi[w] = idx; }
+    __syncthreads();
+    val = redv[0];
+    idx = redi[0];
+    for (int i = 1; i < NW; ++i)
+        if (better(redv[i], redi[i], val, idx)) { val = redv[i]; idx = redi[i]; }
+    __syncthreads();
+}
+
+__device__ inline double block_sum(double v, double *red) { return block_reduce(v, red, OpSum()); }
+
+}  // namespace fw

@@ -18,7 +18,7 @@ FW_F32, FW_BF16 = 0, 1
 STATUS = {0: "FW_OK", 1: "FW_E_NULL", 2: "FW_E_SHAPE", 3: "FW_E_DTYPE", 4: "FW_E_UNSUPPORTED",
           5: "FW_E_WORKSPACE", 6: "FW_E_HIP"}
 ENTRY_POINTS = ("fw_dense_topk", "fw_best_subset", "fw_swap", "fw_dropped_mass_curve",
-                "fw_ragged_compact", "fw_pool_subset")
+                "fw_ragged_compact", "fw_pool_subset", "fw_group_vote")
 # columns of fw_pool_subset's stats (FW_POOL_* in include/fw.h)
 POOL_STATS = ("es_top", "es_pool", "es_bal", "kappa_hat", "c_hat", "kappa_bal", "dropped", "phi",
               "diam", "sigma", "bound_diam", "bound_var")
@@ -56,6 +56,8 @@ _SIGS = {
                                 P, SZ, P]),
     "fw_pool_subset_workspace_size": (SZ, [RP, I32, P, P]),
     "fw_pool_subset": (I32, [RP, I32, P, P, I32, P, P, P, P, P, ctypes.c_float, P, P, P, SZ, P]),
+    "fw_group_vote_workspace_size": (SZ, [RP, I32, I32]),
+    "fw_group_vote": (I32, [RP, I32, I32, P, P, P, P, P, SZ, P]),
     "fw_last_error": (ctypes.c_char_p, []),
     "fw_version": (ctypes.c_char_p, []),
 }
@@ -234,6 +236,21 @@ def pool_subset(q, k, v, budgets: Sequence, max_swaps: int, scale=None, bias=Non
         po += s_ + e_
         so += s_
     out["_ws"] = ws
+    return out
+
+
+def group_vote(q, k, v, s: int, group_size: int, scale=None, bias=None) -> Dict[str, object]:
+    """Rows of a unit ordered (query head) x (position); returns vote_idx
+    [H][T][s] (T = G / group_size) and per row es_vote, es_top, dropped."""
+    torch = _torch()
+    rows = _rows(q, k, v, scale, bias)
+    H, G = rows.H, rows.G
+    dev = q.device
+    f = lambda: torch.empty((H, G), dtype=torch.float32, device=dev)
+    out = {"vote_idx": torch.empty((H, max(G // max(group_size, 1), 1), s), dtype=torch.int32, device=dev),
+           "es_vote": f(), "es_top": f(), "dropped": f()}
+    _check(lib().fw_group_vote(ctypes.byref(rows), s, group_size, _ptr(out["vote_idx"]), _ptr(out["es_vote"]),
+                               _ptr(out["es_top"]), _ptr(out["dropped"]), None, 0, _stream()))
     return out
 
 

@@ -155,3 +155,20 @@ def test_pool_subset_validation(L):
     # the paper's four (s, extra) settings in one call
     big = _rows(n=4096, d=128)
     assert ws(ctypes.byref(big), (4, 8, 16, 32), (24, 12, 6, 4)) > 0
+
+
+def test_group_vote_validation(L):
+    call = lambda rows, s=4, gs=2, vote=1, ev=1, et=1: L.fw_group_vote(rows, s, gs, vote, ev, et, None, None, 0, None)
+    r = _rows(G=4, n=64, d=8)
+    assert call(None) == 1
+    assert call(ctypes.byref(_rows(dtype=7))) == 3
+    assert call(ctypes.byref(_rows(v=None))) == 1
+    assert call(ctypes.byref(r), gs=3) == 2          # does not divide G
+    assert call(ctypes.byref(r), gs=0) == 2
+    assert call(ctypes.byref(r), s=0) == 2
+    assert call(ctypes.byref(r), s=65) == 2          # s > n
+    assert call(ctypes.byref(_rows(G=4, n=1000)), s=300) == 4
+    assert call(ctypes.byref(_rows(G=4, n=20000)), s=4) == 4   # more LDS than a workgroup has
+    assert call(ctypes.byref(r), vote=None) == 1
+    assert call(ctypes.byref(r), ev=None) == 1
+    assert L.fw_group_vote_workspace_size(ctypes.byref(r), 4, 2) == 0
