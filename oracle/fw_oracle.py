@@ -314,28 +314,52 @@ def dropped_mass_curve(r: np.ndarray) -> np.ndarray:
 # ----------------------------------------------------------------------------
 
 
-def allocate(r: np.ndarray, budget: int, floor: int) -> Dict[str, object]:
+def allocate(r: np.ndarray, budget: int, floor: int, cap: Optional[int] = None) -> Dict[str, object]:
     """One score r and one threshold tau shared by all cells.  Each cell keeps
     its last ``floor`` positions plus its non-floor keys of score >= tau, with
     tau set so that exactly ``budget`` entries are kept in total (floor
-    included); ties at tau go to (cell, position) ascending."""
+    included); ties at tau go to (cell, position) ascending.  With ``cap``
+    (budget enforcement), no cell keeps more than ``cap`` entries: each cell
+    offers only its cap - floor best non-floor keys (score desc, position
+    asc) to the shared threshold."""
     r = np.asarray(r, np.float64)
     H, n = r.shape
     f = min(floor, n)
     quota = budget - H * f
-    if quota < 0 or quota > H * (n - f):
-        raise ValueError("budget outside [H*floor, H*n]")
+    per_cell = n - f if cap is None else max(0, min(cap, n) - f)
+    if quota < 0 or quota > H * per_cell:
+        raise ValueError("budget outside [H*floor, H*min(cap, n)]")
     keep = np.zeros((H, n), bool)
     keep[:, n - f:] = True
-    cand_h, cand_j = np.meshgrid(np.arange(H), np.arange(n - f), indexing="ij")
-    cand_h, cand_j = cand_h.ravel(), cand_j.ravel()
-    vals = r[:, : n - f].ravel()
+    cand_h, cand_j = [], []
+    for h in range(H):
+        js = np.arange(n - f)
+        order = np.lexsort((js, -r[h, : n - f]))[:per_cell]
+        cand_h.append(np.full(order.size, h))
+        cand_j.append(js[order])
+    cand_h = np.concatenate(cand_h) if H else np.zeros(0, np.int64)
+    cand_j = np.concatenate(cand_j) if H else np.zeros(0, np.int64)
+    vals = r[cand_h, cand_j]
     order = np.lexsort((cand_j, cand_h, -vals))[:quota]
     keep[cand_h[order], cand_j[order]] = True
     tau = float(vals[order[-1]]) if quota > 0 else math.inf
     counts = keep.sum(axis=1)
     return dict(keep=keep, counts=counts, tau=tau, quota=quota,
                 dropped=np.where(keep, 0.0, r).sum(axis=1))
+
+
+def maxpool_scores(r: np.ndarray, kernel: int) -> np.ndarray:
+    """SnapKV's pooling of the observation-window score (the appendix's audit
+    runs it with kernel 7): each position takes the largest score within
+    kernel // 2 positions on either side, positions outside the cell
+    ignored."""
+    r = np.asarray(r, np.float64)
+    half = kernel // 2
+    n = r.shape[-1]
+    out = np.empty_like(r)
+    for j in range(n):
+        out[..., j] = r[..., max(0, j - half): j + half + 1].max(axis=-1)
+    return out
 
 
 def compact(K: np.ndarray, V: np.ndarray, keep: np.ndarray, heads_per_layer: int,

@@ -41,6 +41,9 @@ def _run_all_pins():
     checks += [(P.test_certificate_identities_and_bounds, s) for s in range(3)]
     checks += [(P.test_group_vote_of_one_row_is_its_top_mass_set, s) for s in range(3)]
     checks += [(P.test_group_vote_brute_force, s) for s in range(3)]
+    checks += [(P.test_allocation_with_cap, s) for s in range(3)]
+    checks += [(P.test_allocation_uniform_cap_is_per_cell_top,)]
+    checks += [(P.test_maxpool_scores, k) for k in (1, 3, 7)]
     return any(_fails(*c) for c in checks)
 
 
@@ -166,8 +169,26 @@ def _vote_by_max(Z, V, s):
 
 _ORIG_VOTE = O.group_vote
 
+
+def _cap_counts_floor_twice(r, budget, floor, cap=None):
+    # caps the non-floor part at cap instead of cap - floor
+    return _ORIG_ALLOC(r, budget, floor, None if cap is None else cap + floor)
+
+
+def _maxpool_one_sided(r, kernel):
+    r = np.asarray(r, np.float64)
+    out = np.empty_like(r)
+    for j in range(r.shape[-1]):
+        out[..., j] = r[..., j: j + kernel].max(axis=-1)
+    return out
+
+
+_ORIG_ALLOC = O.allocate
+
 MUTANTS = {
     "group_vote_by_max_mass": ("group_vote", _vote_by_max),
+    "allocation_cap_ignores_floor": ("allocate", _cap_counts_floor_twice),
+    "maxpool_one_sided_window": ("maxpool_scores", _maxpool_one_sided),
     "pool_extras_by_mass": ("candidate_pool", _extras_by_mass),
     "pool_extras_repeat_top": ("candidate_pool", _extras_may_repeat_top),
     "pool_renormalised_within_pool": ("pool_best_subset", _pool_renormalised),

@@ -567,3 +567,68 @@ def test_group_vote_brute_force(seed):
     same = O.group_vote(np.repeat(Z[:1], 4, axis=0), V, s)
     assert same["vote"].tolist() == O.top_mass_set(Z[0], s).tolist()
     assert np.all(same["ratio"] == 1.0)
+
+
+
+# ---------------------------------------------------------------------------
+# Budget-enforced ContourKV and SnapKV's max-pooled score (Section 4; the
+# appendix's audit of SnapKV)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(3))
+def test_allocation_with_cap(seed):
+    """A cap of n changes nothing; with a cap every cell keeps at most cap
+    entries, the total is exact, and the result equals a greedy fill in the
+    global order (score desc, cell asc, position asc) that skips full cells."""
+    rng = np.random.default_rng(900 + seed)
+    H, n, f = 5, 30, 3
+    r = rng.random((H, n))
+    if seed == 2:
+        r[:, 4] = r[:, 5] = 0.5  # ties inside and across cells
+        r[1, 10:14] = 0.5
+    for budget, cap in ((60, 14), (40, 8), (H * 14, 14)):
+        a = O.allocate(r, budget, f, cap)
+        assert a["counts"].sum() == budget and a["counts"].max() <= cap and a["counts"].min() >= f
+        keep = np.zeros((H, n), bool)
+        keep[:, n - f:] = True
+        order = sorted(((-r[h, j], h, j) for h in range(H) for j in range(n - f)))
+        left = budget - H * f
+        for _, h, j in order:
+            if left == 0:
+                break
+            if keep[h].sum() < cap:
+                keep[h, j] = True
+                left -= 1
+        assert np.array_equal(a["keep"], keep)
+    nocap = O.allocate(r, 50, f)
+    assert np.array_equal(O.allocate(r, 50, f, n)["keep"], nocap["keep"])
+    with pytest.raises(ValueError):
+        O.allocate(r, H * 8 + 1, f, 8)
+
+
+def test_allocation_uniform_cap_is_per_cell_top():
+    """budget = H * cap forces every cell to keep exactly its floor plus its
+    cap - floor best keys (a uniform per-head budget)."""
+    rng = np.random.default_rng(910)
+    H, n, f, cap = 4, 25, 2, 7
+    r = rng.random((H, n))
+    a = O.allocate(r, H * cap, f, cap)
+    for h in range(H):
+        best = np.lexsort((np.arange(n - f), -r[h, : n - f]))[: cap - f]
+        assert set(np.nonzero(a["keep"][h, : n - f])[0].tolist()) == set(best.tolist())
+
+
+@pytest.mark.parametrize("kernel", [1, 3, 7])
+def test_maxpool_scores(kernel):
+    """Kernel 1 is the identity; otherwise the pooled score equals scipy's
+    maximum filter (edge replication adds no new maximum) and bounds the score
+    from above."""
+    scipy_nd = pytest.importorskip("scipy.ndimage")
+    rng = np.random.default_rng(920 + kernel)
+    r = rng.random((3, 40))
+    out = O.maxpool_scores(r, kernel)
+    if kernel == 1:
+        assert np.array_equal(out, r)
+    ref = scipy_nd.maximum_filter1d(r, size=kernel, axis=1, mode="nearest")
+    assert np.array_equal(out, ref)
+    assert np.all(out >= r)
