@@ -252,12 +252,18 @@ fw_status fw_dropped_mass_curve(const fw_rows *rows, float *importance, float *c
  * one threshold tau shared by all H units; each unit keeps its last
  * recency_floor positions plus its non-floor keys of score >= tau, tau set
  * so that exactly budget_entries entries are kept in total (floor included;
- * ties at tau resolve by unit, then position, ascending).  Kept rows are
- * gathered, positions ascending within a unit, unit after unit.
+ * ties at tau resolve by unit, then position, ascending).  With cap > 0 the
+ * budget is enforced per unit (Section 4: enforcement caps every head):
+ * each unit offers only its cap - floor best non-floor keys (score desc,
+ * position asc) to the shared threshold, so no unit keeps more than cap.
+ * Kept rows are gathered, positions ascending within a unit, unit after
+ * unit.
  *   dtype, k, v        [H][n][d] keys/values to compact (bit copies)
  *   heads_per_layer    units per layer (divides H), for the padded layout
- *   importance         [H][n] float32 score r (e.g. fw_dropped_mass_curve)
- *   budget_entries     H*min(floor,n) <= budget_entries <= H*n
+ *   importance         [H][n] float32 score r (e.g. fw_dropped_mass_curve,
+ *                      or its fw_maxpool_scores pooling)
+ *   budget_entries     H*min(floor,n) <= budget_entries <= H*min(cap,n)
+ *   cap                0 (no per-unit cap) or min(floor, n) <= cap
  *   offsets            [H+1] int64 exclusive prefix of kept counts (required)
  *   kept_pos           [budget_entries] int32 kept positions (required)
  *   k_out, v_out       [budget_entries][d] gathered rows (required)
@@ -273,9 +279,20 @@ size_t fw_ragged_compact_workspace_size(int64_t H, int64_t n, int64_t d, int64_t
 fw_status fw_ragged_compact(int32_t dtype, const void *k, const void *v, int64_t H,
                             int64_t heads_per_layer, int64_t n, int64_t d,
                             const float *importance, int64_t budget_entries,
-                            int32_t recency_floor, int64_t *offsets, int32_t *kept_pos,
+                            int32_t recency_floor, int64_t cap, int64_t *offsets, int32_t *kept_pos,
                             void *k_out, void *v_out, float *tau, float *dropped,
                             int64_t *bytes_held, void *ws, size_t ws_bytes, fw_stream stream);
+
+/* ---------------------------------------------------------------------------
+ * fw_maxpool_scores -- SnapKV's pooling of an observation-window score, as
+ * the appendix's audit runs it (kernel 7): out[h][j] = max of scores[h][i]
+ * over |i - j| <= kernel / 2, positions outside [0, n) ignored.
+ *   scores, out  [H][n] float32 (out must not alias scores unless kernel = 1)
+ *   kernel       odd, 1 <= kernel <= 1023
+ * Errors: FW_E_NULL, FW_E_SHAPE, FW_E_HIP.
+ * ------------------------------------------------------------------------- */
+fw_status fw_maxpool_scores(const float *scores, int64_t H, int64_t n, int32_t kernel, float *out,
+                            fw_stream stream);
 
 /* Thread-local description of the calling thread's last error ("" if none). */
 const char *fw_last_error(void);

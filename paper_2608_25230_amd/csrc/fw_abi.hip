@@ -132,7 +132,7 @@ fw_status check_swap(const fw_rows *rows, int32_t k, int32_t max_iters) {
 }
 
 fw_status check_compact(int32_t dtype, const void *k, const void *v, int64_t H, int64_t hpl, int64_t n,
-                        int64_t d, const float *importance, int64_t budget, int32_t floor) {
+                        int64_t d, const float *importance, int64_t budget, int32_t floor, int64_t cap) {
     if (dtype != FW_F32 && dtype != FW_BF16) return fail(FW_E_DTYPE, "unknown dtype %d", (int)dtype);
     if (!k || !v || !importance) return fail(FW_E_NULL, "k, v and importance are required");
     if (H < 1 || n < 1 || d < 1 || d > 4096) return fail(FW_E_SHAPE, "need H >= 1, n >= 1, 1 <= d <= 4096");
@@ -140,9 +140,12 @@ fw_status check_compact(int32_t dtype, const void *k, const void *v, int64_t H, 
     if (hpl < 1 || H % hpl != 0) return fail(FW_E_SHAPE, "heads_per_layer must divide H");
     if (floor < 0) return fail(FW_E_SHAPE, "recency_floor must be >= 0");
     const int64_t f = floor < n ? floor : n;
-    if (budget < H * f || budget > H * n)
-        return fail(FW_E_SHAPE, "budget_entries %lld outside [H*floor, H*n] = [%lld, %lld]", (long long)budget,
-                    (long long)(H * f), (long long)(H * n));
+    if (cap < 0 || (cap > 0 && cap < f))
+        return fail(FW_E_SHAPE, "cap must be 0 (none) or >= min(recency_floor, n), got %lld", (long long)cap);
+    const int64_t per_cell = (cap > 0 && cap < n) ? cap : n;
+    if (budget < H * f || budget > H * per_cell)
+        return fail(FW_E_SHAPE, "budget_entries %lld outside [H*floor, H*min(cap, n)] = [%lld, %lld]",
+                    (long long)budget, (long long)(H * f), (long long)(H * per_cell));
     if (budget >= (1ll << 31)) return fail(FW_E_SHAPE, "budget_entries must be < 2^31");
     return FW_OK;
 }
@@ -293,22 +296,29 @@ size_t fw_ragged_compact_workspace_size(int64_t H, int64_t n, int64_t d, int64_t
 
 fw_status fw_ragged_compact(int32_t dtype, const void *k, const void *v, int64_t H, int64_t heads_per_layer,
                             int64_t n, int64_t d, const float *importance, int64_t budget_entries,
-                            int32_t recency_floor, int64_t *offsets, int32_t *kept_pos, void *k_out,
-                            void *v_out, float *tau, float *dropped, int64_t *bytes_held, void *ws,
+                            int32_t recency_floor, int64_t cap, int64_t *offsets, int32_t *kept_pos,
+                            void *k_out, void *v_out, float *tau, float *dropped, int64_t *bytes_held, void *ws,
                             size_t ws_bytes, fw_stream stream) {
     fw_status s = check_compact(dtype, k, v, H, heads_per_layer, n, d, importance, budget_entries,
-                                recency_floor);
+                                recency_floor, cap);
     if (s != FW_OK) return s;
     if (!offsets || !kept_pos || !k_out || !v_out)
         return fail(FW_E_NULL, "offsets, kept_pos, k_out and v_out are required");
     if ((s = check_ws(ws, ws_bytes, fw::compact_ws_bytes(H, n))) != FW_OK) return s;
     hipError_t e = fw::launch_compact(dtype, k, v, H, heads_per_layer, n, d, importance,
-                                      budget_entries, recency_floor, offsets, kept_pos, k_out, v_out,
+                                      budget_entries, recency_floor, cap, offsets, kept_pos, k_out, v_out,
                                       tau, dropped, bytes_held, ws, (hipStream_t)stream);
     return hip_status(e, "fw_ragged_compact");
 }
 
-}  // extern "C"
+fw_status fw_maxpool_scores(const float *scores, int64_t H, int64_t n, int32_t kernel, float *out,
+                            fw_stream stream) {
+    if (!scores || !out) return fail(FW_E_NULL, "scores and out are required");
+    if (H < 1 || n < 1 || (double)H * (double)n >= 1099511627776.0) return fail(FW_E_SHAPE, "need H, n >= 1, H*n < 2^40");
+    if (kernel < 1 || kernel % 2 == 0 || kernel > 1023) return fail(FW_E_SHAPE, "kernel must be odd, 1..1023");
+    if (scores == out && kernel > 1) return fail(FW_E_SHAPE, "out must not alias scores");
+    return hip_status(fw::launch_maxpool(scores, H, n, kernel, out, (hipStream_t)stream), "fw_maxpool_scores");
+}
 
 // ---------------------------------------------------------------------------
 size_t fw_group_vote_workspace_size(const fw_rows *rows, int32_t s, int32_t group_size) {
@@ -334,3 +344,6 @@ fw_status fw_group_vote(const fw_rows *rows, int32_t s, int32_t group_size, int3
     hipError_t e = fw::launch_vote(*rows, s, group_size, vote_idx, es_vote, es_top, dropped, (hipStream_t)stream);
     return hip_status(e, "fw_group_vote");
 }
+
+}  // extern "C"
+

@@ -69,8 +69,9 @@ void launch_window_mfma(const fw_rows &rows, float *part_m, float *part_l, float
 size_t compact_ws_bytes(int64_t H, int64_t n);
 hipError_t launch_compact(int dtype, const void *k, const void *v, int64_t H, int64_t hpl,
                           int64_t n, int64_t d, const float *importance, int64_t budget,
-                          int floor, int64_t *offsets, int32_t *kept_pos, void *k_out,
+                          int floor, int64_t cap, int64_t *offsets, int32_t *kept_pos, void *k_out,
                           void *v_out, float *tau, float *dropped, int64_t *bytes_held, void *ws,
                           hipStream_t st);
+hipError_t launch_maxpool(const float *scores, int64_t H, int64_t n, int kernel, float *out, hipStream_t st);
 
 }  // namespace fw

@@ -7,6 +7,11 @@
 // device-wide radix select (four 8-bit passes over order-preserving keys);
 // entries equal to tau are taken in (unit, position) order.  Kept rows are
 // then gathered unit after unit, positions ascending, as bit copies.
+//
+// With a per-unit cap (budget enforcement), each unit first finds its
+// (cap - floor)-th best non-floor key in the order (score desc, position asc)
+// by a radix select of its own; only keys up to that one are candidates for
+// the shared threshold.
 #include "fw_internal.hpp"
 
 namespace fw {
@@ -21,6 +26,8 @@ struct SelState {
 struct CompactLayout {
     SelState *sel;
     int64_t *cgt, *ceq, *take;
+    uint32_t *ckey;  // per unit: key of its last candidate (cap only)
+    int64_t *ccut;   // per unit: position of its last candidate among equal keys
     size_t bytes;
 };
 
@@ -38,10 +45,102 @@ CompactLayout compact_layout(int64_t H, void *ws) {
     L.cgt = (int64_t *)take((size_t)H * 8);
     L.ceq = (int64_t *)take((size_t)H * 8);
     L.take = (int64_t *)take((size_t)H * 8);
+    L.ckey = (uint32_t *)take((size_t)H * 4);
+    L.ccut = (int64_t *)take((size_t)H * 8);
     L.bytes = align_up(off, 256);
     return L;
 }
+// Whether non-floor key j of unit h (order key u) is offered to the shared
+// threshold: every key without a cap, else the keys up to the unit's last
+// candidate in the order (key desc, position asc).
+__device__ __forceinline__ bool offered(const uint32_t *ckey, const int64_t *ccut, int64_t h, int64_t j,
+                                        uint32_t u) {
+    if (!ckey) return true;
+    const uint32_t k = ckey[h];
+    return u > k || (u == k && j <= ccut[h]);
+}
 }  // namespace
+
+// Per unit (one workgroup): its capnf-th best non-floor key (capnf < nf) by a
+// radix select over order keys, then the position cut among equal keys
+// (ascending positions).  capnf = 0 offers no key.
+__global__ void __launch_bounds__(256)
+unit_cap_kernel(const float *__restrict__ imp, int64_t n, int64_t nf, int64_t capnf, uint32_t *ckey,
+                int64_t *ccut) {
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t s_prefix, s_mask;
+    __shared__ int64_t s_rem;
+    __shared__ int scan[256];
+    const int64_t h = blockIdx.x;
+    const int t = threadIdx.x;
+    const float *r = imp + h * n;
+    if (capnf == 0) {
+        if (t == 0) {
+            ckey[h] = 0xFFFFFFFFu;
+            ccut[h] = -1;
+        }
+        return;
+    }
+    if (t == 0) {
+        s_prefix = 0;
+        s_mask = 0;
+        s_rem = capnf;
+    }
+    for (int shift = 24; shift >= 0; shift -= 8) {
+        hist[t] = 0;
+        __syncthreads();
+        const uint32_t prefix = s_prefix, mask = s_mask;
+        for (int64_t j = t; j < nf; j += 256) {
+            const uint32_t u = ord_key(r[j]);
+            if ((u & mask) == prefix) atomicAdd(&hist[(u >> shift) & 255u], 1u);
+        }
+        __syncthreads();
+        if (t == 0) {
+            int64_t cum = 0;
+            int b = 0;
+            for (int bb = 255; bb >= 0; --bb) {
+                if (cum + (int64_t)hist[bb] >= s_rem) { b = bb; break; }
+                cum += hist[bb];
+            }
+            s_prefix |= (uint32_t)b << shift;
+            s_mask |= 255u << shift;
+            s_rem -= cum;
+        }
+        __syncthreads();
+    }
+    // the s_rem-th key equal to the cut key, positions ascending
+    const uint32_t key = s_prefix;
+    const int64_t need = s_rem;
+    const int64_t chunk = (nf + 255) / 256;
+    const int64_t lo = t * chunk, hi = (lo + chunk < nf) ? lo + chunk : nf;
+    int c = 0;
+    for (int64_t j = lo; j < hi; ++j) c += ord_key(r[j]) == key;
+    int tot;
+    const int before = block_exclusive_scan(c, scan, &tot);
+    if (before < need && need <= before + c) {
+        int64_t seen = before;
+        for (int64_t j = lo; j < hi; ++j)
+            if (ord_key(r[j]) == key && ++seen == need) {
+                ckey[h] = key;
+                ccut[h] = j;
+                break;
+            }
+    }
+}
+
+// SnapKV's pooling of a window score: the largest score within kernel / 2
+// positions on either side (positions outside the unit ignored).
+__global__ void __launch_bounds__(256)
+maxpool_kernel(const float *__restrict__ r, int64_t H, int64_t n, int half, float *out) {
+    const int64_t total = H * n;
+    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+        const int64_t h = e / n, j = e % n;
+        const int64_t lo = j - half < 0 ? 0 : j - half, hi = j + half + 1 < n ? j + half + 1 : n;
+        float m = r[h * n + lo];
+        for (int64_t i = lo + 1; i < hi; ++i) m = fmaxf(m, r[h * n + i]);
+        out[e] = m;
+    }
+}
 
 __global__ void sel_init_kernel(SelState *s, int64_t quota) {
     const int t = threadIdx.x;
@@ -56,7 +155,7 @@ __global__ void sel_init_kernel(SelState *s, int64_t quota) {
 // histogram of the next 8-bit digit over non-floor entries matching the prefix
 __global__ void __launch_bounds__(256)
 sel_hist_kernel(const float *__restrict__ imp, int64_t H, int64_t n, int64_t nf, int shift,
-                SelState *s) {
+                SelState *s, const uint32_t *ckey, const int64_t *ccut) {
     __shared__ uint32_t h[256];
     const int t = threadIdx.x;
     h[t] = 0;
@@ -66,7 +165,7 @@ sel_hist_kernel(const float *__restrict__ imp, int64_t H, int64_t n, int64_t nf,
     for (int64_t e = (int64_t)blockIdx.x * 256 + t; e < total; e += (int64_t)gridDim.x * 256) {
         const int64_t hh = e / nf, j = e % nf;
         const uint32_t u = ord_key(imp[hh * n + j]);
-        if ((u & pmask) == prefix) atomicAdd(&h[(u >> shift) & 255u], 1u);
+        if ((u & pmask) == prefix && offered(ckey, ccut, hh, j, u)) atomicAdd(&h[(u >> shift) & 255u], 1u);
     }
     __syncthreads();
     if (h[t]) atomicAdd(&s->hist[t], h[t]);
@@ -92,7 +191,7 @@ __global__ void sel_pick_kernel(SelState *s, int shift) {
 // per unit: entries above tau and equal to tau among the non-floor positions
 __global__ void __launch_bounds__(256)
 unit_counts_kernel(const float *__restrict__ imp, int64_t n, int64_t nf, const SelState *s,
-                   int64_t quota, int64_t *cgt, int64_t *ceq) {
+                   int64_t quota, int64_t *cgt, int64_t *ceq, const uint32_t *ckey, const int64_t *ccut) {
     __shared__ int64_t r1[256], r2[256];
     const int64_t h = blockIdx.x;
     const int t = threadIdx.x;
@@ -101,8 +200,9 @@ unit_counts_kernel(const float *__restrict__ imp, int64_t n, int64_t nf, const S
     if (quota > 0)
         for (int64_t j = t; j < nf; j += 256) {
             const uint32_t u = ord_key(imp[h * n + j]);
-            a += (u > key);
-            b += (u == key);
+            const bool o = offered(ckey, ccut, h, j, u);
+            a += o && (u > key);
+            b += o && (u == key);
         }
     a = block_reduce(a, r1, OpSum());
     b = block_reduce(b, r2, OpSum());
@@ -151,7 +251,7 @@ unit_offsets_kernel(int64_t H, int64_t hpl, int64_t n, int64_t f, int64_t quota,
 __global__ void __launch_bounds__(256)
 unit_keep_kernel(const float *__restrict__ imp, int64_t n, int64_t f, int64_t quota,
                  const SelState *s, const int64_t *take, const int64_t *offsets, int32_t *kept_pos,
-                 float *dropped) {
+                 float *dropped, const uint32_t *ckey, const int64_t *ccut) {
     __shared__ int scan[256];
     __shared__ int scan2[256];
     __shared__ double red[256];
@@ -165,7 +265,10 @@ unit_keep_kernel(const float *__restrict__ imp, int64_t n, int64_t f, int64_t qu
     // ties before this thread's chunk (ascending position)
     int c_eq = 0;
     if (quota > 0)
-        for (int64_t j = lo; j < hi && j < nf; ++j) c_eq += (ord_key(imp[h * n + j]) == key);
+        for (int64_t j = lo; j < hi && j < nf; ++j) {
+            const uint32_t u = ord_key(imp[h * n + j]);
+            c_eq += (u == key) && offered(ckey, ccut, h, j, u);
+        }
     int tot;
     int eq_before = block_exclusive_scan(c_eq, scan2, &tot);
     int c = 0;
@@ -176,8 +279,10 @@ unit_keep_kernel(const float *__restrict__ imp, int64_t n, int64_t f, int64_t qu
             bool keep = j >= nf;
             if (!keep && quota > 0) {
                 const uint32_t u = ord_key(imp[h * n + j]);
-                if (u > key) keep = true;
-                else if (u == key) keep = (eq++ < tk);
+                if (offered(ckey, ccut, h, j, u)) {
+                    if (u > key) keep = true;
+                    else if (u == key) keep = (eq++ < tk);
+                }
             }
             c += keep;
             if (!keep) dm += (double)imp[h * n + j];
@@ -191,8 +296,10 @@ unit_keep_kernel(const float *__restrict__ imp, int64_t n, int64_t f, int64_t qu
             bool keep = j >= nf;
             if (!keep && quota > 0) {
                 const uint32_t u = ord_key(imp[h * n + j]);
-                if (u > key) keep = true;
-                else if (u == key) keep = (eq++ < tk);
+                if (offered(ckey, ccut, h, j, u)) {
+                    if (u > key) keep = true;
+                    else if (u == key) keep = (eq++ < tk);
+                }
             }
             if (keep) kept_pos[out++] = (int32_t)j;
         }
@@ -249,13 +356,22 @@ size_t compact_ws_bytes(int64_t H, int64_t n) {
 }
 
 hipError_t launch_compact(int dtype, const void *k, const void *v, int64_t H, int64_t hpl, int64_t n,
-                          int64_t d, const float *importance, int64_t budget, int floor,
+                          int64_t d, const float *importance, int64_t budget, int floor, int64_t cap,
                           int64_t *offsets, int32_t *kept_pos, void *k_out, void *v_out, float *tau,
                           float *dropped, int64_t *bytes_held, void *ws, hipStream_t st) {
     CompactLayout L = compact_layout(H, ws);
     const int64_t f = floor < n ? floor : n;
     const int64_t nf = n - f;
     const int64_t quota = budget - H * f;
+    // the per-unit candidate cut, when a cap leaves some non-floor key out
+    const uint32_t *ckey = nullptr;
+    const int64_t *ccut = nullptr;
+    if (cap > 0 && cap - f < nf) {
+        hipLaunchKernelGGL(unit_cap_kernel, dim3((unsigned)H), dim3(256), 0, st, importance, n, nf, cap - f, L.ckey,
+                           L.ccut);
+        ckey = L.ckey;
+        ccut = L.ccut;
+    }
     const int64_t elem = (dtype == FW_BF16) ? 2 : 4;
     const int64_t row_bytes = d * elem;
     hipLaunchKernelGGL(sel_init_kernel, dim3(1), dim3(256), 0, st, L.sel, quota);
@@ -264,16 +380,16 @@ hipError_t launch_compact(int dtype, const void *k, const void *v, int64_t H, in
         const unsigned blocks = (unsigned)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
         for (int shift = 24; shift >= 0; shift -= 8) {
             hipLaunchKernelGGL(sel_hist_kernel, dim3(blocks), dim3(256), 0, st, importance, H, n, nf,
-                               shift, L.sel);
+                               shift, L.sel, ckey, ccut);
             hipLaunchKernelGGL(sel_pick_kernel, dim3(1), dim3(256), 0, st, L.sel, shift);
         }
     }
     hipLaunchKernelGGL(unit_counts_kernel, dim3((unsigned)H), dim3(256), 0, st, importance, n, nf,
-                       L.sel, quota, L.cgt, L.ceq);
+                       L.sel, quota, L.cgt, L.ceq, ckey, ccut);
     hipLaunchKernelGGL(unit_offsets_kernel, dim3(1), dim3(64), 0, st, H, hpl, n, f, quota, L.sel,
                        L.cgt, L.ceq, L.take, offsets, tau, bytes_held, 2 * row_bytes);
     hipLaunchKernelGGL(unit_keep_kernel, dim3((unsigned)H), dim3(256), 0, st, importance, n, f, quota,
-                       L.sel, L.take, offsets, kept_pos, dropped);
+                       L.sel, L.take, offsets, kept_pos, dropped, ckey, ccut);
     if (budget > 0) {
         if (row_bytes % 16 == 0) {
             const int64_t work = budget * (row_bytes / 16);
@@ -289,6 +405,13 @@ hipError_t launch_compact(int dtype, const void *k, const void *v, int64_t H, in
                                (char *)v_out, budget);
         }
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_maxpool(const float *scores, int64_t H, int64_t n, int kernel, float *out, hipStream_t st) {
+    const int64_t total = H * n;
+    const unsigned blocks = (unsigned)((total + 255) / 256 < 65536 ? (total + 255) / 256 : 65536);
+    hipLaunchKernelGGL(maxpool_kernel, dim3(blocks), dim3(256), 0, st, scores, H, n, kernel / 2, out);
     return hipGetLastError();
 }
 

@@ -18,7 +18,7 @@ FW_F32, FW_BF16 = 0, 1
 STATUS = {0: "FW_OK", 1: "FW_E_NULL", 2: "FW_E_SHAPE", 3: "FW_E_DTYPE", 4: "FW_E_UNSUPPORTED",
           5: "FW_E_WORKSPACE", 6: "FW_E_HIP"}
 ENTRY_POINTS = ("fw_dense_topk", "fw_best_subset", "fw_swap", "fw_dropped_mass_curve",
-                "fw_ragged_compact", "fw_pool_subset", "fw_group_vote")
+                "fw_ragged_compact", "fw_pool_subset", "fw_group_vote", "fw_maxpool_scores")
 # columns of fw_pool_subset's stats (FW_POOL_* in include/fw.h)
 POOL_STATS = ("es_top", "es_pool", "es_bal", "kappa_hat", "c_hat", "kappa_bal", "dropped", "phi",
               "diam", "sigma", "bound_diam", "bound_var")
@@ -52,7 +52,8 @@ _SIGS = {
     "fw_dropped_mass_curve_workspace_size": (SZ, [RP]),
     "fw_dropped_mass_curve": (I32, [RP, P, P, P, P, SZ, P]),
     "fw_ragged_compact_workspace_size": (SZ, [I64, I64, I64, I64]),
-    "fw_ragged_compact": (I32, [I32, P, P, I64, I64, I64, I64, P, I64, I32, P, P, P, P, P, P, P,
+    "fw_maxpool_scores": (I32, [P, I64, I64, I32, P, P]),
+    "fw_ragged_compact": (I32, [I32, P, P, I64, I64, I64, I64, P, I64, I32, I64, P, P, P, P, P, P, P,
                                 P, SZ, P]),
     "fw_pool_subset_workspace_size": (SZ, [RP, I32, P, P]),
     "fw_pool_subset": (I32, [RP, I32, P, P, I32, P, P, P, P, P, ctypes.c_float, P, P, P, SZ, P]),
@@ -272,7 +273,19 @@ def dropped_mass_curve(q, k, scale=None, bias=None, *, want_order=True, ws=None)
     return out
 
 
-def ragged_compact(k, v, importance, budget: int, floor: int, heads_per_layer: int, *,
+def maxpool_scores(scores, kernel: int):
+    """SnapKV's max pooling of [H][n] scores over kernel // 2 positions on
+    either side."""
+    torch = _torch()
+    if not (scores.is_cuda and scores.is_contiguous() and scores.dtype == torch.float32 and scores.dim() == 2):
+        raise FwError(2, "scores must be a contiguous [H][n] float32 device tensor")
+    out = torch.empty_like(scores)
+    _check(lib().fw_maxpool_scores(scores.data_ptr(), scores.shape[0], scores.shape[1], kernel, out.data_ptr(),
+                                   _stream()))
+    return out
+
+
+def ragged_compact(k, v, importance, budget: int, floor: int, heads_per_layer: int, *, cap: int = 0,
                    ws=None) -> Dict[str, object]:
     torch = _torch()
     for name, t in (("k", k), ("v", v), ("importance", importance)):
@@ -292,7 +305,7 @@ def ragged_compact(k, v, importance, budget: int, floor: int, heads_per_layer: i
     if ws is None or ws.numel() < need:
         ws = _workspace(need, dev)
     _check(L.fw_ragged_compact(_dtype_code(k), k.data_ptr(), v.data_ptr(), H, heads_per_layer, n, d,
-                               importance.data_ptr(), budget, floor, out["offsets"].data_ptr(),
+                               importance.data_ptr(), budget, floor, cap, out["offsets"].data_ptr(),
                                out["kept_pos"].data_ptr(), out["k_out"].data_ptr(),
                                out["v_out"].data_ptr(), out["tau"].data_ptr(),
                                out["dropped"].data_ptr(), out["bytes_held"].data_ptr(),

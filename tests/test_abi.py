@@ -29,7 +29,9 @@ def L():
 def test_header_declares_every_entry_point():
     names = _declared()
     for ep in fw.ENTRY_POINTS:
-        assert ep in names and ep + "_workspace_size" in names
+        assert ep in names
+        if ep != "fw_maxpool_scores":  # the one entry point without a workspace
+            assert ep + "_workspace_size" in names
 
 
 def test_every_declared_symbol_is_exported(L):
@@ -114,16 +116,28 @@ def test_curve_validation(L):
 
 
 def test_compact_validation(L):
-    def call(dtype=1, H=4, hpl=2, n=64, d=8, budget=100, floor=8, outs=1):
-        return L.fw_ragged_compact(dtype, 1, 1, H, hpl, n, d, 1, budget, floor, outs, outs, outs,
+    def call(dtype=1, H=4, hpl=2, n=64, d=8, budget=100, floor=8, cap=0, outs=1):
+        return L.fw_ragged_compact(dtype, 1, 1, H, hpl, n, d, 1, budget, floor, cap, outs, outs, outs,
                                    outs, None, None, None, 1, 1 << 40, None)
     assert call(dtype=5) == 3
     assert call(hpl=3) == 2
     assert call(budget=31) == 2  # below H*floor
     assert call(budget=257) == 2  # above H*n
     assert call(floor=-1) == 2
+    assert call(cap=4) == 2       # cap below the floor
+    assert call(cap=-1) == 2
+    assert call(cap=20) == 2      # budget 100 above H*cap = 80
     assert call(outs=None) == 1
     assert L.fw_ragged_compact_workspace_size(4, 64, 8, 100) > 0
+
+
+def test_maxpool_validation(L):
+    assert L.fw_maxpool_scores(None, 2, 8, 7, 1, None) == 1
+    assert L.fw_maxpool_scores(1, 2, 8, 7, None, None) == 1
+    assert L.fw_maxpool_scores(1, 0, 8, 7, 2, None) == 2
+    assert L.fw_maxpool_scores(1, 2, 8, 6, 2, None) == 2     # even kernel
+    assert L.fw_maxpool_scores(1, 2, 8, 7, 1, None) == 2     # aliasing
+    assert L.fw_maxpool_scores(1, 2, 8, 0, 2, None) == 2
 
 
 def test_pool_subset_validation(L):

@@ -99,8 +99,8 @@ def test_curve_tied_scores_across_sort_tiles(torch_fw):
     assert len(np.unique(out["importance"][0])) <= 5
 
 
-def _compact(torch, fw, k, v, imp, budget, floor, hpl):
-    out = fw.ragged_compact(k, v, imp, budget, floor, hpl)
+def _compact(torch, fw, k, v, imp, budget, floor, hpl, cap=0):
+    out = fw.ragged_compact(k, v, imp, budget, floor, hpl, cap=cap)
     torch.cuda.synchronize()
     res = {}
     for key, val in out.items():
@@ -113,8 +113,8 @@ def _compact(torch, fw, k, v, imp, budget, floor, hpl):
     return res
 
 
-def _check_compact(Knp, Vnp, imp, out, budget, floor, hpl, elem):
-    a = O.allocate(imp.astype(np.float64), budget, floor)
+def _check_compact(Knp, Vnp, imp, out, budget, floor, hpl, elem, cap=0):
+    a = O.allocate(imp.astype(np.float64), budget, floor, cap if cap else None)
     c = O.compact(Knp, Vnp, a["keep"], hpl, elem)
     assert np.array_equal(out["offsets"], c["offsets"])
     assert np.array_equal(out["kept_pos"][:budget], c["kept_pos"])
@@ -132,6 +132,12 @@ def _check_compact(Knp, Vnp, imp, out, budget, floor, hpl, elem):
     dict(H=4, hpl=4, n=50, d=3, floor=60, frac=1.0, dt="f32", ties=True),  # floor > n, keep all
     dict(H=5, hpl=1, n=70, d=16, floor=10, frac=0.0, dt="bf16", ties=True),  # floor only
     dict(H=16, hpl=8, n=1000, d=128, floor=0, frac=0.02, dt="bf16", ties=True),
+    # budget enforcement: a per-unit cap
+    dict(H=8, hpl=4, n=300, d=64, floor=32, frac=0.2, dt="bf16", ties=True, cap=60),
+    dict(H=6, hpl=2, n=100, d=8, floor=5, frac=0.5, dt="f32", ties=False, cap=40),
+    dict(H=5, hpl=5, n=200, d=16, floor=8, frac=1.0, dt="f32", ties=True, cap=30),   # every unit at its cap
+    dict(H=4, hpl=2, n=64, d=8, floor=8, frac=0.5, dt="f32", ties=True, cap=8),      # cap = floor
+    dict(H=4, hpl=2, n=64, d=8, floor=4, frac=0.3, dt="f32", ties=True, cap=100),    # cap above n
 ])
 def test_compact_exact(torch_fw, case):
     torch, fw = torch_fw
@@ -154,8 +160,13 @@ def test_compact_exact(torch_fw, case):
         Vnp = rng.standard_normal((H, n, d)).astype(np.float32)
         k, v = torch.from_numpy(Knp).cuda(), torch.from_numpy(Vnp).cuda()
         elem = 4
-    out = _compact(torch, fw, k, v, torch.from_numpy(imp).cuda(), budget, case["floor"], case["hpl"])
-    _check_compact(Knp, Vnp, imp, out, budget, case["floor"], case["hpl"], elem)
+    cap = case.get("cap", 0)
+    if cap:
+        budget = min(budget, H * min(cap, n))
+    out = _compact(torch, fw, k, v, torch.from_numpy(imp).cuda(), budget, case["floor"], case["hpl"], cap)
+    a = _check_compact(Knp, Vnp, imp, out, budget, case["floor"], case["hpl"], elem, cap)
+    if cap:
+        assert a["counts"].max() <= cap
 
 
 def test_full_size_curve_and_compact(torch_fw):
@@ -189,3 +200,35 @@ def test_full_size_curve_and_compact(torch_fw):
     assert bh[0] == wl.budget * 2 * 128 * 2 and bh[2] == rows.H * rows.n * 2 * 128 * 2
     assert bh[0] <= bh[1] <= bh[2]
     print("bytes held ragged/padded/full:", bh.tolist(), "tau", t2np(co["tau"])[0])
+
+
+@pytest.mark.parametrize("kernel", [1, 3, 7])
+def test_maxpool_scores(torch_fw, kernel):
+    """SnapKV's pooling against the oracle, bit for bit (a max of float32
+    values), including windows cut by both ends of a unit."""
+    torch, fw = torch_fw
+    rng = np.random.default_rng(kernel)
+    r = rng.random((5, 333)).astype(np.float32)
+    out = t2np(fw.maxpool_scores(torch.from_numpy(r).cuda(), kernel))
+    assert np.array_equal(out, O.maxpool_scores(r.astype(np.float64), kernel).astype(np.float32))
+
+
+def test_full_size_enforced_allocation(torch_fw):
+    """The full-size cells with SnapKV's pooled score and the uniform per-head
+    budget as the cap (enforcement caps every head at SnapKV's count): the
+    allocation checked exactly against the oracle on the GPU's own scores."""
+    torch, fw = torch_fw
+    wl = W.curve_ragged(seed=0)
+    rows = wl.rows
+    dev, out = _curve(torch, fw, rows)
+    pooled = fw.maxpool_scores(torch.from_numpy(out["importance"]).cuda(), 7)
+    cap = int(math.ceil(wl.budget / rows.H))
+    co = fw.ragged_compact(dev["k"], dev["v"], pooled, wl.budget, wl.floor, wl.heads_per_layer, cap=cap)
+    torch.cuda.synchronize()
+    a = O.allocate(t2np(pooled).astype(np.float64), wl.budget, wl.floor, cap)
+    assert np.array_equal(t2np(co["offsets"]), np.concatenate([[0], np.cumsum(a["counts"])]))
+    assert a["counts"].max() <= cap
+    kept = t2np(co["kept_pos"])
+    offsets = t2np(co["offsets"])
+    for h in (0, 77, 255):
+        assert np.array_equal(kept[offsets[h]:offsets[h + 1]], np.nonzero(a["keep"][h])[0])
