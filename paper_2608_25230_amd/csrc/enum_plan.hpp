@@ -15,6 +15,8 @@ namespace fw {
 constexpr int kMaxWalk = 16;      // walked range size (per-lane e[] in registers)
 constexpr int kMaxEntries = 4096; // walk-table entries per row (LDS)
 constexpr int kMaxClass = 17;     // values of h with work (min(m, n - m) + 1)
+constexpr int kColexMax = 3;      // walked parts of at most this many keys run in colex order
+constexpr int kFastOwned = 8;     // owned parts of at most this many keys take the unrolled set-up
 
 // One value of h: which part the lanes own and which is walked.
 struct EnumClass {
@@ -27,6 +29,7 @@ struct EnumClass {
 // Enumeration plan shared by host (sizes) and device (tables, jobs).
 struct EnumPlan {
     int n, k, d, G;
+    int gp;  // Gram row pitch (doubles), >= n
     int m;
     int ncls;
     EnumClass cls[kMaxClass];
@@ -53,6 +56,7 @@ __host__ __device__ inline bool plan_for(int n, int k, int m, EnumPlan *P, doubl
     EnumPlan p{};
     p.n = n;
     p.k = k;
+    p.gp = n;
     p.m = m;
     const int N = n - m;
     const int hlo = k - m > 0 ? k - m : 0, hhi = k < N ? k : N;

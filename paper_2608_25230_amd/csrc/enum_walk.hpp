@@ -20,7 +20,7 @@
 
 namespace fw {
 
-// Whole workgroup (a multiple of 64 threads).  Gm [n][n] and ps [n] (LDS,
+// Whole workgroup (a multiple of 64 threads).  Gm [n][pl.gp] and ps [n] (LDS,
 // float64) hold the instance; seed_mask (block-uniform) is scored first, so
 // the answer is never worse than it.  ent [nent] (double2), PLt [nent],
 // redd [NT] (double), redm [NT] (uint64) and ctr[1] are LDS scratch.
@@ -30,7 +30,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                                      const EnumJob *__restrict__ g_jobs, const uint64_t *__restrict__ g_omk,
                                      double2 *ent, double *PLt, double *redd, uint64_t *redm, int *ctr) {
     const int NT = blockDim.x;
-    const int n = pl.n;
+    const int gp = pl.gp;
     const int tid = threadIdx.x, lane = tid & 63;
     const uint64_t top_mask = seed_mask;
     // per-row walk tables
@@ -45,7 +45,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
         for (uint64_t a = lm; a; a &= a - 1) {
             const int x = __ffsll((unsigned long long)a) - 1;
             P += ps[x];
-            for (uint64_t b2 = lm; b2; b2 &= b2 - 1) S += Gm[x * n + (__ffsll((unsigned long long)b2) - 1)];
+            for (uint64_t b2 = lm; b2; b2 &= b2 - 1) S += Gm[x * gp + (__ffsll((unsigned long long)b2) - 1)];
         }
         ent[t] = make_double2(S, P * P);
         PLt[t] = P;
@@ -58,7 +58,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
     for (uint64_t a = top_mask; a; a &= a - 1) {
         const int x = __ffsll((unsigned long long)a) - 1;
         P_top += ps[x];
-        for (uint64_t b2 = top_mask; b2; b2 &= b2 - 1) S_top += Gm[x * n + (__ffsll((unsigned long long)b2) - 1)];
+        for (uint64_t b2 = top_mask; b2; b2 &= b2 - 1) S_top += Gm[x * gp + (__ffsll((unsigned long long)b2) - 1)];
     }
     double best_val = S_top / (P_top * P_top);
     uint64_t best_mask = top_mask;
@@ -70,49 +70,70 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
         if (jn >= pl.njobs) break;
         const EnumJob jb = g_jobs[jn];
         const EnumClass C = pl.cls[jb.cls];
-        const int wb = C.wb, wn = C.wn;
+        const int wb = C.wb, wn = C.wn, ws = C.ws, ls = C.ls;
         const bool act = lane < jb.lanes;
-        // owned part of this lane (precomputed key mask; 0 on idle lanes)
+        // owned part of this lane (precomputed key mask; 0 on idle lanes):
+        // p(O), S(O) and E[x] = sum_{a in O} Gm_{a, wb + x} over the walked range
         const uint64_t Om = g_omk[(size_t)jn * 64 + lane];
         double PO = 0.0, SO = 0.0;
-        for (uint64_t a = Om; a; a &= a - 1) {
-            const int x = __ffsll((unsigned long long)a) - 1;
-            PO += ps[x];
-            const double *row = Gm + x * n;
-            for (uint64_t b2 = Om; b2; b2 &= b2 - 1) SO += row[__ffsll((unsigned long long)b2) - 1];
-        }
-        // e[x] over the walked range, from contiguous Gram rows
         double e[kMaxWalk];
 #pragma unroll
         for (int x = 0; x < kMaxWalk; ++x) e[x] = 0.0;
-        if (C.ws > 0) {
-            for (uint64_t a = Om; a; a &= a - 1) {
-                const double *row = Gm + (__ffsll((unsigned long long)a) - 1) * n + wb;
+        if (kFastOwned > 1 && ls <= kFastOwned) {
+            // the owned keys in registers, then independent Gram reads (no
+            // loop-carried address chains); idle lanes read key 0
+            int kx[kFastOwned];
+            uint64_t a = Om;
 #pragma unroll
-                for (int x = 0; x < kMaxWalk; ++x)
-                    if (x < wn) e[x] += row[x];
+            for (int i = 0; i < kFastOwned; ++i) {
+                kx[i] = a ? __ffsll((unsigned long long)a) - 1 : 0;
+                a &= a - 1;
             }
 #pragma unroll
-            for (int x = 0; x < kMaxWalk; ++x)
-                if (x < wn) e[x] = 2.0 * e[x] - 2.0 * beta * PO * ps[wb + x];
-        }
-        double Y = SO - beta * PO * PO;
+            for (int i = 0; i < kFastOwned; ++i) {
+                if (i < ls) {
+                    const double *ri = Gm + kx[i] * gp;
+                    PO += ps[kx[i]];
+                    double sv = ri[kx[i]];
 #pragma unroll
-        for (int x = 0; x < kMaxWalk; ++x)
-            if (x < C.ws) Y += e[x];
-        if (!act) Y = INFINITY;
-        const uint2 *io = g_io + C.toff;
-        const uint64_t *wmk = g_wmk + C.toff;
+                    for (int j = 0; j < i; ++j) sv = fma(2.0, ri[kx[j]], sv);
+                    SO += sv;
+                    if (ws > 0) {
+#pragma unroll
+                        for (int x = 0; x < kMaxWalk; ++x)
+                            if (x < wn) e[x] += ri[wb + x];
+                    }
+                }
+            }
+        } else {
+            for (uint64_t a = Om; a; a &= a - 1) {
+                const int x = __ffsll((unsigned long long)a) - 1;
+                PO += ps[x];
+                const double *row = Gm + x * gp;
+                for (uint64_t b2 = Om; b2; b2 &= b2 - 1) SO += row[__ffsll((unsigned long long)b2) - 1];
+                if (ws > 0) {
+#pragma unroll
+                    for (int y = 0; y < kMaxWalk; ++y)
+                        if (y < wn) e[y] += row[wb + y];
+                }
+            }
+        }
+        if (ws > 0) {
+            const double b2p = 2.0 * beta * PO;
+#pragma unroll
+            for (int x = 0; x < kMaxWalk; ++x)
+                if (x < wn) e[x] = fma(2.0, e[x], -b2p * ps[wb + x]);
+        }
         const double2 *en = ent + C.toff;
         const double *plt = PLt + C.toff;
-        const int steps = jb.steps;  // a multiple of 4 (padded with neutral steps)
+        const uint64_t *wmk = g_wmk + C.toff;
         double thr = 1e-12 * beta;
         // exact score of walk step t for this lane (a candidate)
-        auto exact = [&](int t) {
+        auto exact = [&](int t) __attribute__((always_inline)) {
             const uint64_t wm = wmk[t];
             double S = SO + en[t].x;
             for (uint64_t a = wm; a; a &= a - 1) {
-                const double *row = Gm + (__ffsll((unsigned long long)a) - 1) * n;
+                const double *row = Gm + (__ffsll((unsigned long long)a) - 1) * gp;
                 double E = 0.0;
                 for (uint64_t b2 = Om; b2; b2 &= b2 - 1) E += row[__ffsll((unsigned long long)b2) - 1];
                 S += 2.0 * E;
@@ -125,6 +146,132 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                 best_mask = mask;
             }
         };
+        // after exact scores: the wave's best ratio becomes the new beta;
+        // returns the change (0 when none), by which the caller rescales e
+        auto lower_beta = [&]() __attribute__((always_inline)) -> double {
+            double wbst = best_val;
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) wbst = fmin(wbst, __shfl_xor(wbst, off));
+            if (!(wbst < beta)) return 0.0;
+            const double dB = wbst - beta;
+            beta = wbst;
+            thr = 1e-12 * beta;
+            return dB;
+        };
+
+        if (kColexMax >= 0 && ws <= kColexMax) {
+            // Colex walk of the walked part W = {i < j < l}: the outer keys'
+            // terms are summed once per run of the innermost key, and the
+            // innermost key indexes e at a compile-time position, so a step is
+            // one add, one fused multiply-add and a compare.  Consecutive
+            // steps of a run differ by one key (i -> i + 1).
+            auto run = [&](double base, int t0, int lim) __attribute__((always_inline)) {
+                const double nb = thr - base;  // test: e[i] + S_W - beta p(W)^2 <= thr - base
+                uint64_t any = 0;
+                // chunks of four steps: one batch of table reads per chunk
+#pragma unroll
+                for (int i0 = 0; i0 < kMaxWalk; i0 += 4) {
+                    if (i0 < lim) {
+                        double2 c[4];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) c[u] = en[t0 + i0 + u];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) any |= __ballot(e[i0 + u] + fma(-beta, c[u].y, c[u].x) <= nb);
+                    }
+                }
+                if (any) {  // rare: the same tests again (steps of the run only), exact scores, new beta
+                    uint32_t cm = 0;
+#pragma unroll
+                    for (int i = 0; i < kMaxWalk; ++i) {
+                        if (i < lim) {
+                            const double2 c = en[t0 + i];
+                            if (e[i] + fma(-beta, c.y, c.x) <= nb) cm |= 1u << i;
+                        }
+                    }
+                    for (; cm; cm &= cm - 1) exact(t0 + __ffs(cm) - 1);
+                    const double dB = lower_beta();
+#pragma unroll
+                    for (int x = 0; x < kMaxWalk; ++x)
+                        if (x < wn) e[x] -= 2.0 * dB * PO * ps[wb + x];
+                }
+            };
+            if (ws == 0) {
+                const double YO = act ? SO - beta * PO * PO : INFINITY;
+                if (__ballot(YO <= thr)) {
+                    if (YO <= thr) exact(0);
+                    lower_beta();  // nothing is walked: e is unused
+                }
+            } else if (ws == 1) {
+                run(act ? SO - beta * PO * PO : INFINITY, 0, wn);
+            } else {
+                // Walked pairs {i < j} below a limit L, after an outer base B
+                // (walked triples {i < j < l}: one block per l with
+                // B = K1 + e[l], L = l).  Both pair keys index e at
+                // compile-time positions.  e at the wave-uniform l comes from
+                // selects written out here (a helper taking e by reference
+                // would be folded into an indexed load, keeping e out of
+                // registers).
+                for (int l = ws == 2 ? wn : 2; l < wn || (ws == 2 && l == wn); ++l) {
+                    double el = 0.0;
+                    if (ws == 3) {
+#pragma unroll
+                        for (int x = 2; x < kMaxWalk; ++x) el = l == x ? e[x] : el;
+                    }
+                    const double B = act ? SO - beta * PO * PO + el : INFINITY;
+                    const int tl = ws == 3 ? l * (l - 1) * (l - 2) / 6 : 0;
+                    uint64_t any = 0;
+#pragma unroll
+                    for (int j = 1; j < kMaxWalk; ++j) {
+                        if (j < l) {
+                            const double nb = thr - (B + e[j]);
+                            const double2 *cj = en + tl + j * (j - 1) / 2;
+#pragma unroll
+                            for (int i = 0; i < j; ++i) {
+                                const double2 c = cj[i];
+                                any |= __ballot(e[i] + fma(-beta, c.y, c.x) <= nb);
+                            }
+                        }
+                    }
+                    if (any) {  // rare: the same tests again, exact scores, new beta
+                        for (int j = 1; j < l; ++j) {
+                            double ej = e[1];
+#pragma unroll
+                            for (int x = 2; x < kMaxWalk; ++x) ej = j == x ? e[x] : ej;
+                            const double nb = thr - (B + ej);
+                            const int tj = tl + j * (j - 1) / 2;
+                            uint32_t cm = 0;
+#pragma unroll
+                            for (int i = 0; i < kMaxWalk; ++i) {
+                                if (i < j) {
+                                    const double2 c = en[tj + i];
+                                    if (e[i] + fma(-beta, c.y, c.x) <= nb) cm |= 1u << i;
+                                }
+                            }
+                            for (; cm; cm &= cm - 1) exact(tj + __ffs(cm) - 1);
+                        }
+                        const double dB = lower_beta();
+#pragma unroll
+                        for (int x = 0; x < kMaxWalk; ++x)
+                            if (x < wn) e[x] -= 2.0 * dB * PO * ps[wb + x];
+                    }
+                }
+            }
+            continue;
+        }
+
+        // Revolving-door walk (walked parts of more than kColexMax keys): one
+        // key leaves and one enters per step, both wave-uniform, so e is read
+        // at uniform register positions (its own copy: only indexed here).
+        double er[kMaxWalk];
+#pragma unroll
+        for (int x = 0; x < kMaxWalk; ++x) er[x] = e[x];
+        double Y = SO - beta * PO * PO;
+#pragma unroll
+        for (int x = 0; x < kMaxWalk; ++x)
+            if (x < ws) Y += er[x];
+        if (!act) Y = INFINITY;
+        const uint2 *io = g_io + C.toff;
+        const int steps = jb.steps;  // a multiple of 4 (padded with neutral steps)
         // four steps per round: the step tables are loaded together and the
         // rare candidates handled after the four tests (a beta lowered within
         // the round only widens the filter of the remaining steps)
@@ -141,7 +288,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
             double y = Y;
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                y += e[w[u].x] - e[w[u].y];
+                y += er[w[u].x] - er[w[u].y];
                 const double f = y + fma(-beta, c[u].y, c[u].x);
                 cand[u] = f <= thr;
                 any |= __ballot(cand[u]);  // wave masks: or-ed on the scalar unit
@@ -151,21 +298,16 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
 #pragma unroll
                 for (int u = 0; u < 4; ++u)
                     if (cand[u]) exact(t0 + u);
-                double wbst = best_val;
-#pragma unroll
-                for (int off = 32; off > 0; off >>= 1) wbst = fmin(wbst, __shfl_xor(wbst, off));
-                if (wbst < beta) {
-                    const double dB = wbst - beta;
+                const double dB = lower_beta();
+                if (dB != 0.0) {
 #pragma unroll
                     for (int x = 0; x < kMaxWalk; ++x)
-                        if (x < wn) e[x] -= 2.0 * dB * PO * ps[wb + x];
-                    beta = wbst;
-                    thr = 1e-12 * beta;
+                        if (x < wn) er[x] -= 2.0 * dB * PO * ps[wb + x];
                     // Y for the round's last real step from the rescaled e
                     int tl = t0 + 3;
                     while (wmk[tl] == kPadMask) --tl;
                     double yy = SO - beta * PO * PO;
-                    for (uint64_t a = wmk[tl]; a; a &= a - 1) yy += e[__ffsll((unsigned long long)a) - 1 - wb];
+                    for (uint64_t a = wmk[tl]; a; a &= a - 1) yy += er[__ffsll((unsigned long long)a) - 1 - wb];
                     Y = act ? yy : INFINITY;
                 }
             }

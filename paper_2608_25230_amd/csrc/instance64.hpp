@@ -16,12 +16,12 @@ __device__ __forceinline__ float default_scale(int d) { return (float)(1.0 / sqr
 __host__ __device__ inline int instance_pitch(int d) { return d + 1; }
 
 // Whole workgroup; n <= 64 <= blockDim.x.  Vs [n][d + 1] float (LDS) stages
-// the keys, then the values; zs, ps [n], mu [d], Gm [n][n] (LDS) receive the
-// instance.  Global reads are coalesced (whole rows); the logits, weights,
+// the keys, then the values; zs, ps [n], mu [d], Gm [n][gp] (LDS, row pitch
+// gp >= n) receive the instance.  Global reads are coalesced (whole rows); the logits, weights,
 // dense output and Gram are formed from LDS.
 template <typename T>
 __device__ void instance64(const T *qr, const T *kh, const T *vh, float scale, const float *bias,
-                           int n, int d, float *Vs, double *zs, double *ps, double *mu, double *Gm) {
+                           int n, int d, float *Vs, double *zs, double *ps, double *mu, double *Gm, int gp) {
     const int tid = threadIdx.x, NT = blockDim.x;
     const int pitch = instance_pitch(d);
     float *qs = (float *)mu;  // the query, in the dense output's space until that is formed
@@ -59,8 +59,8 @@ __device__ void instance64(const T *qr, const T *kh, const T *vh, float scale, c
         double s = 0.0;
         for (int c = 0; c < d; ++c) s = fma((double)Vs[i * pitch + c] - mu[c], (double)Vs[j * pitch + c] - mu[c], s);
         const double gij = ps[i] * ps[j] * s;
-        Gm[i * n + j] = gij;
-        Gm[j * n + i] = gij;
+        Gm[i * gp + j] = gij;
+        Gm[j * gp + i] = gij;
     }
     __syncthreads();
 }

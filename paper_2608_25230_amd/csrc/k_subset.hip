@@ -40,6 +40,10 @@ namespace {
 
 constexpr int kSubsetThreads = 256;
 
+// Gram row pitch: odd, so that lanes reading different rows at one column
+// fall on different LDS banks.
+__host__ __device__ inline int gram_pitch(int n) { return n | 1; }
+
 struct SubsetLds {
     size_t gm, pz, mu, ent, pl, vs, red, ctr, total;
 };
@@ -48,7 +52,7 @@ __host__ __device__ inline SubsetLds subset_lds(int n, int d, int k, int nent, i
     SubsetLds L{};
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t at = o; o = align_up(o + bytes, 16); return at; };
-    L.gm = take((size_t)n * n * 8);
+    L.gm = take((size_t)n * gram_pitch(n) * 8);
     L.pz = take((size_t)n * 8 * 2);
     L.mu = take((size_t)d * 8);
     // walk tables overlay the values staged for the instance (dead by then)
@@ -66,10 +70,11 @@ __host__ __device__ inline SubsetLds subset_lds(int n, int d, int k, int nent, i
 
 }  // namespace
 
-// Walk tables (row independent): for every walked (range, size) the
-// revolving-door sequence -- entry t holds the keys entering and leaving at
-// step t relative to the range (in | out << 8) and the mask of the walked
-// part (absolute key positions) -- and the job list, longest jobs first.
+// Walk tables (row independent): for every walked (range, size) the walk's
+// sequence -- colex order for parts of at most kColexMax keys, else the
+// revolving-door order, where entry t also holds the keys entering and
+// leaving at step t relative to the range -- as masks of the walked part
+// (absolute key positions), and the job list, longest jobs first.
 __global__ void enum_plan_kernel(EnumPlan p, uint2 *io, uint64_t *wmk, EnumJob *jobs) {
     if (threadIdx.x != 0 || blockIdx.x != 0) return;
     int c[kMaxWalk + 2];
@@ -83,7 +88,18 @@ __global__ void enum_plan_kernel(EnumPlan p, uint2 *io, uint64_t *wmk, EnumJob *
         uint32_t rel = C.ws == 0 ? 0u : ((1u << C.ws) - 1u);
         io[t] = make_uint2(0u, 0u);
         wmk[t] = (uint64_t)rel << C.wb;
-        if (C.ws > 0 && C.ws < C.wn) {
+        if (C.ws <= kColexMax) {
+            // colex order: Gosper's successor (the next larger integer with
+            // the same number of bits)
+            const int cnt = (int)binom(C.wn, C.ws);
+            for (int q = 1; q < cnt; ++q) {
+                const uint32_t low = rel & (~rel + 1u), r = rel + low;
+                rel = (((r ^ rel) >> 2) / low) | r;
+                ++t;
+                io[t] = make_uint2(0u, 0u);
+                wmk[t] = (uint64_t)rel << C.wb;
+            }
+        } else if (C.ws > 0 && C.ws < C.wn) {
             revdoor_init(c, C.ws, C.wn);
             int in, out;
             while (revdoor_next(c, C.ws, &in, &out)) {
@@ -147,7 +163,7 @@ __global__ void __launch_bounds__(64) enum_owned_kernel(EnumPlan p, const EnumJo
 }
 
 template <typename T>
-__global__ void __launch_bounds__(kSubsetThreads)
+__global__ void __launch_bounds__(kSubsetThreads, 4)
 best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
                    const float *__restrict__ scale, const float *__restrict__ bias, EnumPlan pl,
                    const uint2 *__restrict__ g_io, const uint64_t *__restrict__ g_wmk,
@@ -176,7 +192,7 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
     const T *kh = k + hh * (int64_t)n * d;
     const T *vh = v + hh * (int64_t)n * d;
 
-    instance64(qr, kh, vh, scale ? scale[hh] : default_scale(d), bias, n, d, Vs, zs, ps, mu, Gm);
+    instance64(qr, kh, vh, scale ? scale[hh] : default_scale(d), bias, n, d, Vs, zs, ps, mu, Gm, pl.gp);
     // top-k set: rank by (z desc, index asc)
     const uint64_t top_mask = topk_mask64(zs, n, kk, topk_idx ? topk_idx + r * kk : nullptr, redm);
     // (Vs is dead: instance64 ends with a barrier)
@@ -228,6 +244,7 @@ hipError_t launch_best_subset(const fw_rows &rows, int k, int32_t *best_idx, flo
     if (!choose_plan(rows.n, k, &p)) return hipErrorInvalidConfiguration;
     p.d = (int)rows.d;
     p.G = (int)rows.G;
+    p.gp = gram_pitch(p.n);
     const EnumTables W = enum_tables(p, ws);
     hipError_t e = launch_enum_tables(p, W, st);
     if (e != hipSuccess) return e;

@@ -44,7 +44,7 @@ swap_small_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__r
     const T *qr = q + r * d;
     const T *kh = k + h * (int64_t)n * d;
     const T *vh = v + h * (int64_t)n * d;
-    instance64(qr, kh, vh, scale ? scale[h] : default_scale(d), bias, n, d, Vs, zs, ps, mu, Gm);
+    instance64(qr, kh, vh, scale ? scale[h] : default_scale(d), bias, n, d, Vs, zs, ps, mu, Gm, n);
     uint64_t S = topk_mask64(zs, n, kk, nullptr, redm);
     const int T_len = max_iters + 1;
     float *traj = gap_traj + r * T_len;
