@@ -66,21 +66,20 @@ __device__ __forceinline__ bool lex_less(uint64_t a, uint64_t b) {
 
 // ---------------------------------------------------------------------------
 // Workgroup reductions in a fixed order (bitwise repeatable).  `red` must hold
-// blockDim.x elements; every thread must call.
+// blockDim.x / 64 elements; every thread must call.
 // ---------------------------------------------------------------------------
 template <typename T, typename Op>
 __device__ T block_reduce(T v, T *red, Op op) {
-    const int t = threadIdx.x, nt = blockDim.x;
-    red[t] = v;
+    // butterfly within each wave (every lane ends with the wave's value,
+    // the same bits on each since op is commutative), then the waves'
+    // values in wave order; blockDim.x is a multiple of 64
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v = op(v, __shfl_xor(v, off));
+    if (lane == 0) red[w] = v;
     __syncthreads();
-    // power-of-two tree over the (possibly non power-of-two) block
-    int pw = 1;
-    while (pw < nt) pw <<= 1;
-    for (int s = pw >> 1; s > 0; s >>= 1) {
-        if (t < s && t + s < nt) red[t] = op(red[t], red[t + s]);
-        __syncthreads();
-    }
     T r = red[0];
+    for (int i = 1; i < nw; ++i) r = op(r, red[i]);
     __syncthreads();
     return r;
 }

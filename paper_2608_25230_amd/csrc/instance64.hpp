@@ -15,26 +15,88 @@ __device__ __forceinline__ float default_scale(int d) { return (float)(1.0 / sqr
 // reads of different rows on different banks.
 __host__ __device__ inline int instance_pitch(int d) { return d + 1; }
 
-// Whole workgroup; n <= 64 <= blockDim.x.  Vs [n][d + 1] float (LDS) stages
-// the keys, then the values; zs, ps [n], mu [d], Gm [n][gp] (LDS, row pitch
-// gp >= n) receive the instance.  Global reads are coalesced (whole rows); the logits, weights,
-// dense output and Gram are formed from LDS.
+// Elements [first, n d) of a row-major [n][d] matrix into LDS at row pitch
+// `pitch` (floats), every thread of the workgroup taking elements NT apart
+// (first a multiple of NT), eight global loads in flight per thread.
+template <typename T>
+__device__ __forceinline__ void stage_rows_from(const T *src, int n, int d, float *dst, int pitch, int first) {
+    const int NT = blockDim.x;
+    const int rstep = NT / d, cstep = NT - rstep * d;
+    const int e = first + threadIdx.x;
+    int r = e / d, c = e - (e / d) * d;
+    const int tot = n * d;
+    for (int e0 = e; e0 < tot; e0 += 8 * NT) {
+        float buf[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (e0 + u * NT < tot) buf[u] = Elem<T>::load(src, e0 + u * NT);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            if (e0 + u * NT < tot) dst[r * pitch + c] = buf[u];
+            r += rstep;
+            c += cstep;
+            if (c >= d) {
+                c -= d;
+                ++r;
+            }
+        }
+    }
+}
+
+template <typename T>
+__device__ __forceinline__ void stage_rows(const T *src, int n, int d, float *dst, int pitch) {
+    stage_rows_from(src, n, d, dst, pitch, 0);
+}
+
+// Whole workgroup; n <= 64 <= blockDim.x, blockDim.x a multiple of 64.
+// Vs [n][d + 1] float (LDS) stages the keys, then the values; zs, ps [n],
+// mu [d], Gm [n][gp] (LDS, row pitch gp >= n) receive the instance.  Global
+// reads are coalesced (whole rows); the logits, weights, dense output and
+// Gram are formed from LDS, each sum in a fixed order.
 template <typename T>
 __device__ void instance64(const T *qr, const T *kh, const T *vh, float scale, const float *bias,
                            int n, int d, float *Vs, double *zs, double *ps, double *mu, double *Gm, int gp) {
     const int tid = threadIdx.x, NT = blockDim.x;
     const int pitch = instance_pitch(d);
     float *qs = (float *)mu;  // the query, in the dense output's space until that is formed
-    for (int e = tid; e < n * d; e += NT) Vs[(e / d) * pitch + e % d] = Elem<T>::load(kh, e);
+    stage_rows(kh, n, d, Vs, pitch);
     for (int c = tid; c < d; c += NT) qs[c] = Elem<T>::load(qr, c);
+    // the first 16 values per thread are loaded now and land in LDS after
+    // the logits (their loads overlap that phase)
+    const int tot = n * d;
+    float vpre[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+        if (tid + u * NT < tot) vpre[u] = Elem<T>::load(vh, tid + u * NT);
     __syncthreads();
-    if (tid < n) {
+    {
+        // logits: lpk adjacent lanes per key (a power of two dividing 64),
+        // strided partial sums combined by a fixed butterfly
+        int lpk = 8;
+        while (lpk > 1 && lpk * n > NT) lpk >>= 1;
+        const int key = tid / lpk, part = tid & (lpk - 1);
         double dot = 0.0;
-        for (int c = 0; c < d; ++c) dot = fma((double)qs[c], (double)Vs[tid * pitch + c], dot);
-        zs[tid] = (double)scale * dot + (bias ? (double)bias[tid] : 0.0);
+        if (key < n)
+            for (int c = part; c < d; c += lpk) dot = fma((double)qs[c], (double)Vs[key * pitch + c], dot);
+        for (int off = 1; off < lpk; off <<= 1) dot += __shfl_xor(dot, off);
+        if (key < n && part == 0) zs[key] = (double)scale * dot + (bias ? (double)bias[key] : 0.0);
     }
     __syncthreads();
-    for (int e = tid; e < n * d; e += NT) Vs[(e / d) * pitch + e % d] = Elem<T>::load(vh, e);
+    {
+        const int rstep = NT / d, cstep = NT - rstep * d;
+        int r = tid / d, c = tid - (tid / d) * d;
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+            if (tid + u * NT < tot) Vs[r * pitch + c] = vpre[u];
+            r += rstep;
+            c += cstep;
+            if (c >= d) {
+                c -= d;
+                ++r;
+            }
+        }
+        if (tot > 16 * NT) stage_rows_from(vh, n, d, Vs, pitch, 16 * NT);
+    }
     if (tid < 64) {  // softmax on one wave, fixed reduction order
         const double z = tid < n ? zs[tid] : -INFINITY;
         double m = z;
@@ -51,38 +113,60 @@ __device__ void instance64(const T *qr, const T *kh, const T *vh, float scale, c
         mu[c] = s;
     }
     __syncthreads();
-    for (int e = tid; e < n * (n + 1) / 2; e += NT) {
-        // e -> (i, j), i <= j, row-major over the upper triangle
-        int i = 0, rem = e;
-        while (rem >= n - i) { rem -= n - i; ++i; }
-        const int j = i + rem;
-        double s = 0.0;
-        for (int c = 0; c < d; ++c) s = fma((double)Vs[i * pitch + c] - mu[c], (double)Vs[j * pitch + c] - mu[c], s);
-        const double gij = ps[i] * ps[j] * s;
-        Gm[i * gp + j] = gij;
-        Gm[j * gp + i] = gij;
+    // Gram: 2 x 2 blocks of rows (2A, 2A + 1) x (2B, 2B + 1), A <= B, each on
+    // two adjacent lanes that split the columns (even / odd) and add their
+    // sums; rows past n (odd n) read row n - 1 and are not written
+    const int nb = (n + 1) >> 1, nblk = nb * (nb + 1) / 2;
+    for (int task = tid; task < 2 * ((nblk + 31) / 32) * 32; task += NT) {
+        const int blk = task >> 1, half = task & 1;
+        int A = 0, rem = blk < nblk ? blk : 0;
+        while (rem >= nb - A) { rem -= nb - A; ++A; }
+        const int B = A + rem;
+        const int i0 = 2 * A, j0 = 2 * B;
+        const int i1 = min(i0 + 1, n - 1), j1 = min(j0 + 1, n - 1);
+        const float *ra0 = Vs + i0 * pitch, *ra1 = Vs + i1 * pitch, *rb0 = Vs + j0 * pitch, *rb1 = Vs + j1 * pitch;
+        double s00 = 0.0, s01 = 0.0, s10 = 0.0, s11 = 0.0;
+        for (int c = half; c < d; c += 2) {
+            const double m = mu[c];
+            const double a0 = (double)ra0[c] - m, a1 = (double)ra1[c] - m;
+            const double b0 = (double)rb0[c] - m, b1 = (double)rb1[c] - m;
+            s00 = fma(a0, b0, s00);
+            s01 = fma(a0, b1, s01);
+            s10 = fma(a1, b0, s10);
+            s11 = fma(a1, b1, s11);
+        }
+        s00 += __shfl_xor(s00, 1);
+        s01 += __shfl_xor(s01, 1);
+        s10 += __shfl_xor(s10, 1);
+        s11 += __shfl_xor(s11, 1);
+        if (blk < nblk && half == 0) {
+            auto put = [&](int i, int j, double sv) {
+                const double g = ps[i] * ps[j] * sv;
+                Gm[i * gp + j] = g;
+                Gm[j * gp + i] = g;
+            };
+            put(i0, j0, s00);
+            if (j0 + 1 < n) put(i0, j0 + 1, s01);
+            if (i0 + 1 < n) put(i0 + 1, j0, s10);
+            if (i0 + 1 < n && j0 + 1 < n) put(i0 + 1, j0 + 1, s11);
+        }
     }
     __syncthreads();
 }
 
 // Top-k set of the row as a bit mask: rank by (logit desc, index asc).  When
-// idx is given, idx[rank] = key for the k best.  `scratch` holds blockDim.x
-// 64-bit words.
-__device__ inline uint64_t topk_mask64(const double *zs, int n, int k, int32_t *idx,
-                                       uint64_t *scratch) {
-    const int tid = threadIdx.x;
+// idx is given, idx[rank] = key for the k best.  Every wave forms the mask
+// itself from zs (no barrier); n <= 64.
+__device__ inline uint64_t topk_mask64(const double *zs, int n, int k, int32_t *idx) {
+    const int lane = threadIdx.x & 63;
     int rank = n;
-    if (tid < n) {
+    if (lane < n) {
+        const double z = zs[lane];
         rank = 0;
-        for (int i = 0; i < n; ++i) rank += (zs[i] > zs[tid]) || (zs[i] == zs[tid] && i < tid);
-        if (rank < k && idx) idx[rank] = tid;
+        for (int i = 0; i < n; ++i) rank += (zs[i] > z) || (zs[i] == z && i < lane);
+        if (rank < k && idx && threadIdx.x < 64) idx[rank] = lane;
     }
-    scratch[tid] = (tid < n && rank < k) ? (1ull << tid) : 0ull;
-    __syncthreads();
-    uint64_t m = 0;
-    for (int i = 0; i < n; ++i) m |= scratch[i];
-    __syncthreads();
-    return m;
+    return __ballot(rank < k);
 }
 
 // es(A) = ||sum_{j in A} p_j (v_j - mu)|| / p(A) from the d-dimensional sums
@@ -107,10 +191,66 @@ __device__ double exact_gap(uint64_t A, int n, const T *vh, const double *ps, co
     return sqrt(g2) / P;
 }
 
+// The same error from values staged in LDS (Vs [n][pitch] floats).
+__device__ inline double exact_gap_lds(uint64_t A, int n, const float *Vs, int pitch, const double *ps,
+                                       const double *mu, int d, double *red) {
+    if (__popcll(A) == n) return 0.0;
+    double g2 = 0.0;
+    for (int c = threadIdx.x; c < d; c += blockDim.x) {
+        double gc = 0.0;
+        for (uint64_t m = A; m; m &= m - 1) {
+            const int j = __ffsll((unsigned long long)m) - 1;
+            gc += ps[j] * ((double)Vs[j * pitch + c] - mu[c]);
+        }
+        g2 += gc * gc;
+    }
+    g2 = block_reduce(g2, red, OpSum());
+    double P = 0.0;
+    for (uint64_t m = A; m; m &= m - 1) P += ps[__ffsll((unsigned long long)m) - 1];
+    return sqrt(g2) / P;
+}
+
 __device__ inline double mass64(uint64_t A, const double *ps) {
     double P = 0.0;
     for (uint64_t m = A; m; m &= m - 1) P += ps[__ffsll((unsigned long long)m) - 1];
     return P;
 }
+
+// es of two sets at once from values staged in LDS (one workgroup
+// reduction for both).
+__device__ inline double2 exact_gap2_lds(uint64_t A, uint64_t B, int n, const float *Vs, int pitch,
+                                         const double *ps, const double *mu, int d, double *red) {
+    double ga = 0.0, gb = 0.0;
+    for (int c = threadIdx.x; c < d; c += blockDim.x) {
+        double sa = 0.0, sb = 0.0;
+        for (int j = 0; j < n; ++j) {
+            const double u = ps[j] * ((double)Vs[j * pitch + c] - mu[c]);
+            if ((A >> j) & 1ull) sa += u;
+            if ((B >> j) & 1ull) sb += u;
+        }
+        ga += sa * sa;
+        gb += sb * sb;
+    }
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        ga += __shfl_xor(ga, off);
+        gb += __shfl_xor(gb, off);
+    }
+    if (lane == 0) {
+        red[2 * w] = ga;
+        red[2 * w + 1] = gb;
+    }
+    __syncthreads();
+    double ta = red[0], tb = red[1];
+    for (int i = 1; i < nw; ++i) {
+        ta += red[2 * i];
+        tb += red[2 * i + 1];
+    }
+    __syncthreads();
+    const double pa = mass64(A, ps), pb = mass64(B, ps);
+    return make_double2(__popcll(A) == n ? 0.0 : sqrt(ta) / pa, __popcll(B) == n ? 0.0 : sqrt(tb) / pb);
+}
+
 
 }  // namespace fw

@@ -44,8 +44,11 @@ constexpr int kSubsetThreads = 256;
 // fall on different LDS banks.
 __host__ __device__ inline int gram_pitch(int n) { return n | 1; }
 
+constexpr size_t kSubsetLdsKeep = 40 * 1024;  // four workgroups per CU
+
 struct SubsetLds {
     size_t gm, pz, mu, ent, pl, vs, red, ctr, total;
+    bool keep_vs;
 };
 
 __host__ __device__ inline SubsetLds subset_lds(int n, int d, int k, int nent, int nt) {
@@ -55,15 +58,18 @@ __host__ __device__ inline SubsetLds subset_lds(int n, int d, int k, int nent, i
     L.gm = take((size_t)n * gram_pitch(n) * 8);
     L.pz = take((size_t)n * 8 * 2);
     L.mu = take((size_t)d * 8);
-    // walk tables overlay the values staged for the instance (dead by then)
     const size_t tab = (size_t)nent * 16 + (size_t)nent * 8;
     const size_t vsb = (size_t)n * instance_pitch(d) * 4;
-    const size_t region = take(tab > vsb ? tab : vsb);
-    L.ent = region;
-    L.pl = region + (size_t)nent * 16;
-    L.vs = region;
     L.red = take((size_t)nt * 16);
     L.ctr = take(16);
+    // the values stay staged through the walk when that keeps four
+    // workgroups per CU; otherwise the walk tables overlay them and they
+    // are staged again for the reported errors
+    L.keep_vs = o + tab + vsb + 32 <= kSubsetLdsKeep;
+    const size_t region = take(L.keep_vs ? tab : (tab > vsb ? tab : vsb));
+    L.ent = region;
+    L.pl = region + (size_t)nent * 16;
+    L.vs = L.keep_vs ? take(vsb) : region;
     L.total = o;
     return L;
 }
@@ -194,8 +200,8 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
 
     instance64(qr, kh, vh, scale ? scale[hh] : default_scale(d), bias, n, d, Vs, zs, ps, mu, Gm, pl.gp);
     // top-k set: rank by (z desc, index asc)
-    const uint64_t top_mask = topk_mask64(zs, n, kk, topk_idx ? topk_idx + r * kk : nullptr, redm);
-    // (Vs is dead: instance64 ends with a barrier)
+    const uint64_t top_mask = topk_mask64(zs, n, kk, topk_idx ? topk_idx + r * kk : nullptr);
+    // (instance64 ends with a barrier: the walk tables may overlay Vs)
     const uint64_t best = enum_best_body(pl, Gm, ps, top_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd, redm, ctr);
     if (tid == 0) {
         int i = 0;
@@ -207,8 +213,12 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
             dropped_topk[r] = (float)dm;
         }
     }
-    const double es_best = exact_gap(best, n, vh, ps, mu, d, redd);
-    const double es_top = exact_gap(top_mask, n, vh, ps, mu, d, redd);
+    if (!L.keep_vs) {  // the values again (the walk tables that overlaid them are dead)
+        stage_rows(vh, n, d, Vs, instance_pitch(d));
+        __syncthreads();
+    }
+    const double2 es = exact_gap2_lds(best, top_mask, n, Vs, instance_pitch(d), ps, mu, d, redd);
+    const double es_best = es.x, es_top = es.y;
     if (tid == 0) {
         best_gap[r] = (float)es_best;
         if (topk_gap) topk_gap[r] = (float)es_top;

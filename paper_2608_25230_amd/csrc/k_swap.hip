@@ -45,7 +45,7 @@ swap_small_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__r
     const T *kh = k + h * (int64_t)n * d;
     const T *vh = v + h * (int64_t)n * d;
     instance64(qr, kh, vh, scale ? scale[h] : default_scale(d), bias, n, d, Vs, zs, ps, mu, Gm, n);
-    uint64_t S = topk_mask64(zs, n, kk, nullptr, redm);
+    uint64_t S = topk_mask64(zs, n, kk, nullptr);
     const int T_len = max_iters + 1;
     float *traj = gap_traj + r * T_len;
     double es = exact_gap(S, n, vh, ps, mu, d, redd);
