@@ -20,11 +20,13 @@
 
 namespace fw {
 
-// Whole workgroup (a multiple of 64 threads).  Gm [n][pl.gp] and ps [n] (LDS,
+// Whole workgroup (a multiple of 64 threads); every walked range of the plan
+// holds at most WMAX keys.  Gm [n][pl.gp] and ps [n] (LDS,
 // float64) hold the instance; seed_mask (block-uniform) is scored first, so
 // the answer is never worse than it.  ent [nent] (double2), PLt [nent],
 // redd [NT] (double), redm [NT] (uint64) and ctr[1] are LDS scratch.
 // Returns the best mask, block-uniform.
+template <int WMAX>
 __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const double *Gm, const double *ps, uint64_t seed_mask,
                                      const uint2 *__restrict__ g_io, const uint64_t *__restrict__ g_wmk,
                                      const EnumJob *__restrict__ g_jobs, const uint64_t *__restrict__ g_omk,
@@ -76,9 +78,9 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
         // p(O), S(O) and E[x] = sum_{a in O} Gm_{a, wb + x} over the walked range
         const uint64_t Om = g_omk[(size_t)jn * 64 + lane];
         double PO = 0.0, SO = 0.0;
-        double e[kMaxWalk];
+        double e[WMAX];
 #pragma unroll
-        for (int x = 0; x < kMaxWalk; ++x) e[x] = 0.0;
+        for (int x = 0; x < WMAX; ++x) e[x] = 0.0;
         if (kFastOwned > 1 && ls <= kFastOwned) {
             // the owned keys in registers, then independent Gram reads (no
             // loop-carried address chains); idle lanes read key 0
@@ -100,7 +102,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                     SO += sv;
                     if (ws > 0) {
 #pragma unroll
-                        for (int x = 0; x < kMaxWalk; ++x)
+                        for (int x = 0; x < WMAX; ++x)
                             if (x < wn) e[x] += ri[wb + x];
                     }
                 }
@@ -113,7 +115,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                 for (uint64_t b2 = Om; b2; b2 &= b2 - 1) SO += row[__ffsll((unsigned long long)b2) - 1];
                 if (ws > 0) {
 #pragma unroll
-                    for (int y = 0; y < kMaxWalk; ++y)
+                    for (int y = 0; y < WMAX; ++y)
                         if (y < wn) e[y] += row[wb + y];
                 }
             }
@@ -121,7 +123,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
         if (ws > 0) {
             const double b2p = 2.0 * beta * PO;
 #pragma unroll
-            for (int x = 0; x < kMaxWalk; ++x)
+            for (int x = 0; x < WMAX; ++x)
                 if (x < wn) e[x] = fma(2.0, e[x], -b2p * ps[wb + x]);
         }
         const double2 *en = ent + C.toff;
@@ -170,7 +172,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                 uint64_t any = 0;
                 // chunks of four steps: one batch of table reads per chunk
 #pragma unroll
-                for (int i0 = 0; i0 < kMaxWalk; i0 += 4) {
+                for (int i0 = 0; i0 < WMAX; i0 += 4) {
                     if (i0 < lim) {
                         double2 c[4];
 #pragma unroll
@@ -182,7 +184,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                 if (any) {  // rare: the same tests again (steps of the run only), exact scores, new beta
                     uint32_t cm = 0;
 #pragma unroll
-                    for (int i = 0; i < kMaxWalk; ++i) {
+                    for (int i = 0; i < WMAX; ++i) {
                         if (i < lim) {
                             const double2 c = en[t0 + i];
                             if (e[i] + fma(-beta, c.y, c.x) <= nb) cm |= 1u << i;
@@ -191,7 +193,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                     for (; cm; cm &= cm - 1) exact(t0 + __ffs(cm) - 1);
                     const double dB = lower_beta();
 #pragma unroll
-                    for (int x = 0; x < kMaxWalk; ++x)
+                    for (int x = 0; x < WMAX; ++x)
                         if (x < wn) e[x] -= 2.0 * dB * PO * ps[wb + x];
                 }
             };
@@ -215,13 +217,13 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                     double el = 0.0;
                     if (ws == 3) {
 #pragma unroll
-                        for (int x = 2; x < kMaxWalk; ++x) el = l == x ? e[x] : el;
+                        for (int x = 2; x < WMAX; ++x) el = l == x ? e[x] : el;
                     }
                     const double B = act ? SO - beta * PO * PO + el : INFINITY;
                     const int tl = ws == 3 ? l * (l - 1) * (l - 2) / 6 : 0;
                     uint64_t any = 0;
 #pragma unroll
-                    for (int j = 1; j < kMaxWalk; ++j) {
+                    for (int j = 1; j < WMAX; ++j) {
                         if (j < l) {
                             const double nb = thr - (B + e[j]);
                             const double2 *cj = en + tl + j * (j - 1) / 2;
@@ -236,12 +238,12 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                         for (int j = 1; j < l; ++j) {
                             double ej = e[1];
 #pragma unroll
-                            for (int x = 2; x < kMaxWalk; ++x) ej = j == x ? e[x] : ej;
+                            for (int x = 2; x < WMAX; ++x) ej = j == x ? e[x] : ej;
                             const double nb = thr - (B + ej);
                             const int tj = tl + j * (j - 1) / 2;
                             uint32_t cm = 0;
 #pragma unroll
-                            for (int i = 0; i < kMaxWalk; ++i) {
+                            for (int i = 0; i < WMAX; ++i) {
                                 if (i < j) {
                                     const double2 c = en[tj + i];
                                     if (e[i] + fma(-beta, c.y, c.x) <= nb) cm |= 1u << i;
@@ -251,7 +253,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                         }
                         const double dB = lower_beta();
 #pragma unroll
-                        for (int x = 0; x < kMaxWalk; ++x)
+                        for (int x = 0; x < WMAX; ++x)
                             if (x < wn) e[x] -= 2.0 * dB * PO * ps[wb + x];
                     }
                 }
@@ -262,12 +264,12 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
         // Revolving-door walk (walked parts of more than kColexMax keys): one
         // key leaves and one enters per step, both wave-uniform, so e is read
         // at uniform register positions (its own copy: only indexed here).
-        double er[kMaxWalk];
+        double er[WMAX];
 #pragma unroll
-        for (int x = 0; x < kMaxWalk; ++x) er[x] = e[x];
+        for (int x = 0; x < WMAX; ++x) er[x] = e[x];
         double Y = SO - beta * PO * PO;
 #pragma unroll
-        for (int x = 0; x < kMaxWalk; ++x)
+        for (int x = 0; x < WMAX; ++x)
             if (x < ws) Y += er[x];
         if (!act) Y = INFINITY;
         const uint2 *io = g_io + C.toff;
@@ -301,7 +303,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                 const double dB = lower_beta();
                 if (dB != 0.0) {
 #pragma unroll
-                    for (int x = 0; x < kMaxWalk; ++x)
+                    for (int x = 0; x < WMAX; ++x)
                         if (x < wn) er[x] -= 2.0 * dB * PO * ps[wb + x];
                     // Y for the round's last real step from the rescaled e
                     int tl = t0 + 3;
@@ -350,7 +352,7 @@ __device__ inline uint64_t enum_best(const EnumPlan &pl, const double *Gm, const
                                      const uint2 *__restrict__ g_io, const uint64_t *__restrict__ g_wmk,
                                      const EnumJob *__restrict__ g_jobs, const uint64_t *__restrict__ g_omk,
                                      double2 *ent, double *PLt, double *redd, uint64_t *redm, int *ctr) {
-    return enum_best_body(pl, Gm, ps, seed_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd, redm, ctr);
+    return enum_best_body<kMaxWalk>(pl, Gm, ps, seed_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd, redm, ctr);
 }
 
 }  // namespace fw

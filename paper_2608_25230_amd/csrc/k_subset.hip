@@ -168,7 +168,7 @@ __global__ void __launch_bounds__(64) enum_owned_kernel(EnumPlan p, const EnumJo
     omk[(size_t)j * 64 + lane] = m;
 }
 
-template <typename T>
+template <typename T, int WMAX>
 __global__ void __launch_bounds__(kSubsetThreads, 4)
 best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
                    const float *__restrict__ scale, const float *__restrict__ bias, EnumPlan pl,
@@ -202,7 +202,7 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
     // top-k set: rank by (z desc, index asc)
     const uint64_t top_mask = topk_mask64(zs, n, kk, topk_idx ? topk_idx + r * kk : nullptr);
     // (instance64 ends with a barrier: the walk tables may overlay Vs)
-    const uint64_t best = enum_best_body(pl, Gm, ps, top_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd, redm, ctr);
+    const uint64_t best = enum_best_body<WMAX>(pl, Gm, ps, top_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd, redm, ctr);
     if (tid == 0) {
         int i = 0;
         for (uint64_t a = best; a; a &= a - 1) best_idx[r * kk + i++] = __ffsll((unsigned long long)a) - 1;
@@ -262,16 +262,22 @@ hipError_t launch_best_subset(const fw_rows &rows, int k, int32_t *best_idx, flo
     const SubsetLds L = subset_lds(p.n, p.d, k, p.nent, nt);
     if (L.total > 160 * 1024) return hipErrorInvalidConfiguration;
     const unsigned R = (unsigned)(rows.H * rows.G);
-    if (rows.dtype == FW_BF16)
-        hipLaunchKernelGGL(best_subset_kernel<uint16_t>, dim3(R), dim3(nt), L.total, st,
-                           (const uint16_t *)rows.q, (const uint16_t *)rows.k, (const uint16_t *)rows.v,
-                           rows.scale, rows.bias, p, W.io, W.wmk, W.jobs, W.omk, best_idx, best_gap, topk_gap,
-                           closed, dropped_topk, topk_idx);
-    else
-        hipLaunchKernelGGL(best_subset_kernel<float>, dim3(R), dim3(nt), L.total, st,
-                           (const float *)rows.q, (const float *)rows.k, (const float *)rows.v,
-                           rows.scale, rows.bias, p, W.io, W.wmk, W.jobs, W.omk, best_idx, best_gap, topk_gap,
-                           closed, dropped_topk, topk_idx);
+    // a narrower walk register file when every walked range allows it
+    int wmax = 0;
+    for (int q = 0; q < p.ncls; ++q) wmax = p.cls[q].wn > wmax ? p.cls[q].wn : wmax;
+    auto go = [&](auto kern, const auto *q, const auto *k, const auto *v) {
+        hipLaunchKernelGGL(kern, dim3(R), dim3(nt), L.total, st, q, k, v, rows.scale, rows.bias, p, W.io, W.wmk,
+                           W.jobs, W.omk, best_idx, best_gap, topk_gap, closed, dropped_topk, topk_idx);
+    };
+    if (rows.dtype == FW_BF16) {
+        const uint16_t *q = (const uint16_t *)rows.q, *k = (const uint16_t *)rows.k, *v = (const uint16_t *)rows.v;
+        if (wmax <= 12) go(best_subset_kernel<uint16_t, 12>, q, k, v);
+        else go(best_subset_kernel<uint16_t, kMaxWalk>, q, k, v);
+    } else {
+        const float *q = (const float *)rows.q, *k = (const float *)rows.k, *v = (const float *)rows.v;
+        if (wmax <= 12) go(best_subset_kernel<float, 12>, q, k, v);
+        else go(best_subset_kernel<float, kMaxWalk>, q, k, v);
+    }
     return hipGetLastError();
 }
 

@@ -20,6 +20,8 @@ int main(){
     // count
     double C=1; for(int i=1;i<=t;++i) C=C*(n-t+i)/i;
     if ((double)seq.size()!= C){printf("count n=%d t=%d got %zu want %.0f\n",n,t,seq.size(),C);return 1;}
+    // unranking gives every position of the walk
+    for(size_t i=0;i<seq.size();++i) if (fw::revdoor_unrank(i,n,t)!=seq[i]) {printf("unrank n=%d t=%d r=%zu\n",n,t,i);return 1;}
     // prefix property
     for(int b=t;b<=n;++b){ double Cb=1; for(int i=1;i<=t;++i) Cb=Cb*(b-t+i)/i;
       for(size_t i=0;i<(size_t)Cb;++i) if (seq[i]>>b) {printf("prefix n=%d t=%d b=%d\n",n,t,b);return 1;} }
