@@ -15,6 +15,17 @@
 // v_j.mu + |mu|^2)) in float32 with a per-row argmin (ties to the smaller
 // (i, j)), then applies the winning swap and updates g in float64.  Gaps in
 // the trajectory are ||g|| / P from float64 sums.
+//
+// Pruned pair search (long rows).  By Cauchy-Schwarz, |u_i.u_j| <= r_i r_j
+// with r_x = ||u_x||, so every pair's numerator is at least
+//     A_i + B_j - 2 r_i r_j,   A_i = ||g - u_i||^2,  B_j = ||u_j||^2 + 2 g.u_j,
+// and its denominator is (P - p_i + p_j)^2.  An upper
+// bound UB on the best value (the best of the 8 x 8 pairs of smallest A_i and
+// B_j, evaluated exactly) leaves only the pairs whose lower bound reaches UB:
+// two fused multiply-adds and a compare per pair, no cross terms.  Those few
+// are evaluated exactly in float64 (||g - u_i + u_j||^2 / (P - p_i + p_j)^2,
+// ties to the smaller i n + j).  A row whose survivors overflow the list
+// falls back to the full sweep.
 #include "fw_internal.hpp"
 #include "instance64.hpp"
 
@@ -130,8 +141,18 @@ struct SwapState {
     float *pv;       // [R][nblk] partial best values
     int64_t *pp;     // [R][nblk] partial best pair index i*n + j
     float4 *jd;      // [R][n]   per key: (B_j or +inf if kept, p_j, 2 w_j, P + p_j)
+    float2 *br;      // [R][n]   per key: (B_j or +inf if kept, ||u_j||) for the pruned search
+    double *ub;      // [R][2]   upper bound on the best pair value (and a spare slot)
+    int64_t *ubp;    // [R]      the pair that gave the upper bound
+    int32_t *cnt;    // [R]      surviving pairs
+    int32_t *fb;     // [R]      1: survivors overflowed, the full sweep runs
+    int64_t *cand;   // [R][kSwapCand] surviving pairs i n + j
+    int32_t *ord;    // [R][k]    kept keys in the bound pass's order (k <= kSwapSort)
     int nblk;
 };
+
+constexpr int kSwapCand = 4096;  // surviving pairs kept per row
+constexpr int kSwapSort = 2048;  // kept keys ordered for the bound pass
 
 template <typename T>
 __global__ void __launch_bounds__(256)
@@ -165,12 +186,32 @@ swap_init_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, S
     for (int64_t j = lo; j < hi; ++j)
         if (inS[j]) s.Sl[r * kk + pos++] = (int32_t)j;
     __syncthreads();
-    // mu = sum_j p_j v_j, float64
+    // mu = sum_j p_j v_j, float64: 16 key lanes x 16 column groups (a
+    // column group per thread and pass), the key lanes' sums added in order
     double *mu = s.mu + r * d;
-    for (int cc = tid; cc < d; cc += NT) {
-        double acc = 0.0;
-        for (int64_t j = 0; j < n; ++j) acc = fma((double)p[j], (double)Elem<T>::load(vh, j * d + cc), acc);
-        mu[cc] = acc;
+    {
+        const int jl = tid & 15, cg = tid >> 4;
+        for (int c0 = 8 * cg; c0 < d; c0 += 128) {
+            double acc[8];
+#pragma unroll
+            for (int x = 0; x < 8; ++x) acc[x] = 0.0;
+            for (int64_t j = jl; j < n; j += 16) {
+                const double pj = (double)p[j];
+#pragma unroll
+                for (int x = 0; x < 8; ++x)
+                    if (c0 + x < d) acc[x] = fma(pj, (double)Elem<T>::load(vh, j * d + c0 + x), acc[x]);
+            }
+#pragma unroll
+            for (int x = 0; x < 8; ++x) {
+#pragma unroll
+                for (int off = 1; off < 16; off <<= 1) acc[x] += __shfl_xor(acc[x], off);
+            }
+            if (jl == 0) {
+#pragma unroll
+                for (int x = 0; x < 8; ++x)
+                    if (c0 + x < d) mu[c0 + x] = acc[x];
+            }
+        }
     }
     __syncthreads();
     double mu2 = 0.0;
@@ -239,9 +280,62 @@ swap_dots_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, SwapState
         const float pj = s.p[r * n + j];
         const float aj = pj * (float)((double)acc - mg);
         s.a[r * n + j] = aj;
-        if (s.jd) {
+        const float bj = s.inS[r * n + j] ? INFINITY : s.bq[r * n + j] + 2.f * aj;
+        if (s.jd) s.jd[r * n + j] = make_float4(bj, pj, 2.f * s.w[r * n + j], P + pj);
+        if (s.br) s.br[r * n + j] = make_float2(bj, sqrtf(s.bq[r * n + j]));
+    }
+}
+
+// The same dots for RB rows of one key/value unit at once (G % RB == 0,
+// d <= 256): each key's values are read once for the RB rows, whose g
+// vectors sit in LDS.  Per row the same float32 sum in column order.
+template <typename T, int RB>
+__global__ void __launch_bounds__(256)
+swap_dots_group_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, SwapState s) {
+    __shared__ float gs[RB][256];
+    __shared__ double mgs[RB];
+    __shared__ float Ps[RB];
+    const int tid = threadIdx.x;
+    const int64_t r0 = (int64_t)blockIdx.y * RB;
+    const int64_t h = r0 / G;
+    const T *vh = v + h * n * d;
+    for (int e = tid; e < RB * d; e += blockDim.x) {
+        const int rr = e / d, c = e - rr * d;
+        gs[rr][c] = (float)s.g[(r0 + rr) * d + c];
+    }
+    // mu . g per row: 16 lanes per row, their partial sums added by a butterfly
+    for (int rr0 = 0; rr0 < RB; rr0 += 16) {
+        const int rr = rr0 + (tid >> 4), ln = tid & 15;
+        double mg = 0.0;
+        if (rr < RB)
+            for (int c = ln; c < d; c += 16) mg += s.mu[(r0 + rr) * d + c] * s.g[(r0 + rr) * d + c];
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) mg += __shfl_xor(mg, off);
+        if (rr < RB && ln == 0) {
+            mgs[rr] = mg;
+            Ps[rr] = (float)s.sc[(r0 + rr) * 4 + 0];
+        }
+    }
+    __syncthreads();
+    for (int64_t j = (int64_t)blockIdx.x * blockDim.x + tid; j < n; j += (int64_t)gridDim.x * blockDim.x) {
+        float acc[RB];
+#pragma unroll
+        for (int rr = 0; rr < RB; ++rr) acc[rr] = 0.f;
+        for (int c = 0; c < d; ++c) {
+            const float x = Elem<T>::load(vh, j * d + c);
+#pragma unroll
+            for (int rr = 0; rr < RB; ++rr) acc[rr] = fmaf(x, gs[rr][c], acc[rr]);
+        }
+#pragma unroll
+        for (int rr = 0; rr < RB; ++rr) {
+            const int64_t r = r0 + rr;
+            if (!s.st[r * 2]) continue;
+            const float pj = s.p[r * n + j];
+            const float aj = pj * (float)((double)acc[rr] - mgs[rr]);
+            s.a[r * n + j] = aj;
             const float bj = s.inS[r * n + j] ? INFINITY : s.bq[r * n + j] + 2.f * aj;
-            s.jd[r * n + j] = make_float4(bj, pj, 2.f * s.w[r * n + j], P + pj);
+            if (s.jd) s.jd[r * n + j] = make_float4(bj, pj, 2.f * s.w[r * n + j], Ps[rr] + pj);
+            if (s.br) s.br[r * n + j] = make_float2(bj, sqrtf(s.bq[r * n + j]));
         }
     }
 }
@@ -257,7 +351,7 @@ swap_pairs_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, 
     __shared__ float redv[256];
     __shared__ int64_t redp[256];
     const int64_t r = blockIdx.y;
-    if (!s.st[r * 2]) return;
+    if (!s.st[r * 2] || (s.fb && !s.fb[r])) return;
     const int tid = threadIdx.x;
     const int64_t h = r / G;
     const T *vh = v + h * n * d;
@@ -377,7 +471,7 @@ swap_pairs_mfma_kernel(const uint16_t *__restrict__ v, int64_t G, int64_t n, int
     float *redv = (float *)(smem + 2 * SP_STAGE + 2 * SPT * 16 * 16);  // [8]
     int64_t *redp = (int64_t *)(redv + 8);                        // [8]
     const int64_t r = blockIdx.y;
-    if (!s.st[r * 2]) return;
+    if (!s.st[r * 2] || (s.fb && !s.fb[r])) return;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, rl = lane & 15, grp = lane >> 4;
     const int64_t nchunk = (n + SPJ - 1) / SPJ;
     const int ib = (int)(blockIdx.x / nchunk);
@@ -520,6 +614,304 @@ swap_pairs_mfma_kernel(const uint16_t *__restrict__ v, int64_t G, int64_t n, int
     }
 }
 
+// (value, index) minimum over the workgroup, ties to the smaller index
+__device__ inline void block_argmin_vi(double &v, int64_t &i, double *redv, int64_t *redi) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const double ov = __shfl_xor(v, off);
+        const int64_t oi = __shfl_xor(i, off);
+        if (ov < v || (ov == v && oi < i)) { v = ov; i = oi; }
+    }
+    if (lane == 0) { redv[w] = v; redi[w] = i; }
+    __syncthreads();
+    v = redv[0];
+    i = redi[0];
+    for (int x = 1; x < nw; ++x)
+        if (redv[x] < v || (redv[x] == v && redi[x] < i)) { v = redv[x]; i = redi[x]; }
+    __syncthreads();
+}
+
+// exact value of the swap (i out, j in): ||g - u_i + u_j||^2 / (P - p_i + p_j)^2,
+// float64, over the columns c = c0, c0 + step, ... (a partial numerator)
+template <typename T>
+__device__ inline double swap_num_part(const T *vh, int d, int64_t i, int64_t j, double pi, double pj,
+                                       const double *g, const double *mu, int c0, int step) {
+    double acc = 0.0;
+    for (int c = c0; c < d; c += step) {
+        const double x = g[c] - pi * ((double)Elem<T>::load(vh, i * d + c) - mu[c]) +
+                         pj * ((double)Elem<T>::load(vh, j * d + c) - mu[c]);
+        acc = fma(x, x, acc);
+    }
+    return acc;
+}
+
+// per row: the 8 smallest A_i (kept) and B_j (dropped), the exact values of
+// their 64 pairs, and from them the upper bound
+template <typename T>
+__global__ void __launch_bounds__(256)
+swap_ub_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, SwapState s) {
+    __shared__ double redv[4];
+    __shared__ int64_t redi[4];
+    __shared__ double gs[256], ms[256];
+    __shared__ int64_t topi[8], topj[8];
+    const int64_t r = blockIdx.x;
+    if (!s.st[r * 2]) return;
+    const int tid = threadIdx.x, NT = blockDim.x;
+    const double *sc = s.sc + r * 4;
+    const double P = sc[0], g2 = sc[1];
+    const float *p = s.p + r * n, *a = s.a + r * n, *bq = s.bq + r * n;
+    const int32_t *Sl = s.Sl + r * kk;
+    const float2 *br = s.br + r * n;
+    for (int c = tid; c < d; c += NT) {
+        gs[c] = s.g[r * d + c];
+        ms[c] = s.mu[r * d + c];
+    }
+    // eight smallest B_j and A_i, each round after the previous (value, index)
+    double pvj = -INFINITY, pvi = -INFINITY;
+    int64_t pij = -1, pii = -1;
+    for (int u = 0; u < 8; ++u) {
+        double bv = INFINITY;
+        int64_t bi = INT64_MAX;
+        for (int64_t j = tid; j < n; j += NT) {
+            const double x = (double)br[j].x;
+            if (!(x < INFINITY)) continue;
+            const bool after = x > pvj || (x == pvj && j > pij);
+            if (after && (x < bv || (x == bv && j < bi))) { bv = x; bi = j; }
+        }
+        block_argmin_vi(bv, bi, redv, redi);
+        if (tid == 0) topj[u] = bi < INT64_MAX ? bi : -1;
+        pvj = bv;
+        pij = bi;
+        double av = INFINITY;
+        int64_t ai = INT64_MAX;
+        for (int t = tid; t < kk; t += NT) {
+            const int64_t i = Sl[t];
+            const double x = g2 + (double)bq[i] - 2.0 * (double)a[i];
+            const bool after = x > pvi || (x == pvi && i > pii);
+            if (after && (x < av || (x == av && i < ai))) { av = x; ai = i; }
+        }
+        block_argmin_vi(av, ai, redv, redi);
+        if (tid == 0) topi[u] = ai < INT64_MAX ? ai : -1;
+        pvi = av;
+        pii = ai;
+    }
+    __syncthreads();
+    // the 64 pairs: four lanes per pair, each a quarter of the columns
+    const int pr = tid >> 2, qt = tid & 3;
+    const int64_t i = topi[pr >> 3], j = topj[pr & 7];
+    const T *vh = v + (r / G) * n * d;
+    double num = 0.0;
+    if (i >= 0 && j >= 0) num = swap_num_part(vh, d, i, j, (double)p[i], (double)p[j], gs, ms, qt, 4);
+    num += __shfl_xor(num, 1);
+    num += __shfl_xor(num, 2);
+    double val = INFINITY;
+    int64_t pidx = INT64_MAX;
+    if (i >= 0 && j >= 0 && qt == 0) {
+        const double den = P - (double)p[i] + (double)p[j];
+        val = num / (den * den);
+        pidx = i * n + j;
+    }
+    block_argmin_vi(val, pidx, redv, redi);
+    if (tid == 0) {
+        s.ub[r * 2 + 0] = val;
+        s.ub[r * 2 + 1] = 0.0;
+        s.ubp[r] = pidx;
+        s.cnt[r] = 0;
+    }
+    if (!s.ord) return;
+    // Order the kept keys for the bound pass by how readily their pairs pass
+    // a slice test (largest first), so that the few that do share waves and
+    // the other waves skip whole slices: kappa_i = c_i + 2 r_i rt + 2 UB Pi pt
+    // with rt, pt four times the mean r_j and p_j of the dropped keys.
+    double sr = 0.0, sp = 0.0, nd = 0.0;
+    for (int64_t j = tid; j < n; j += NT) {
+        const float2 b = br[j];
+        if (b.x < INFINITY) {
+            sr += (double)b.y;
+            sp += (double)p[j];
+            nd += 1.0;
+        }
+    }
+    sr = block_reduce(sr, redv, OpSum());
+    sp = block_reduce(sp, redv, OpSum());
+    nd = block_reduce(nd, redv, OpSum());
+    const double rt = 4.0 * sr / fmax(nd, 1.0), pt = 4.0 * sp / fmax(nd, 1.0);
+    __shared__ float skey[kSwapSort];
+    __shared__ int32_t sval[kSwapSort];
+    int np2 = 1;
+    while (np2 < kk) np2 <<= 1;
+    for (int t = tid; t < np2; t += NT) {
+        float key = INFINITY;
+        int32_t iv = -1;
+        if (t < kk) {
+            iv = Sl[t];
+            const double bqi = (double)bq[iv];
+            const double Ai = g2 + bqi - 2.0 * (double)a[iv];
+            const double Pi = P - (double)p[iv];
+            const double kap = val * Pi * Pi - Ai + 2.0 * sqrt(bqi) * rt + 2.0 * val * Pi * pt;
+            key = (float)(-kap);
+        }
+        skey[t] = key;
+        sval[t] = iv;
+    }
+    __syncthreads();
+    for (int size = 2; size <= np2; size <<= 1) {
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int t = tid; t < np2; t += NT) {
+                const int u = t ^ stride;
+                if (u > t) {
+                    const bool up = (t & size) == 0;
+                    const float kt = skey[t], ku = skey[u];
+                    if ((kt > ku) == up && kt != ku) {
+                        skey[t] = ku;
+                        skey[u] = kt;
+                        const int32_t vt = sval[t];
+                        sval[t] = sval[u];
+                        sval[u] = vt;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    }
+    for (int t = tid; t < kk; t += NT) s.ord[r * kk + t] = sval[t];
+}
+
+// every (kept i, dropped j) pair of a tile against the lower bound: 256
+// kept keys (one per thread) x JC keys per workgroup.  With Pi = P - p_i the
+// test  A_i + B_j - 2 r_i r_j <= UB (Pi + p_j)^2  is, expanded,
+//     (B_j - UB p_j^2) - 2 r_i r_j - 2 UB Pi p_j <= UB Pi^2 - A_i,
+// two fused multiply-adds and a compare per pair; the keys' terms are staged
+// in LDS per tile and read by all threads alike.  Each 64-key slice of a tile
+// is first tested as a whole, with its smallest B_j - UB p_j^2 and largest
+// r_j and p_j (a lower bound for every pair of the slice): a wave whose lanes
+// all fail skips the slice.
+template <int JC>
+__global__ void __launch_bounds__(256)
+swap_bound_kernel(int64_t n, int kk, SwapState s) {
+    __shared__ float4 tile[256];
+    __shared__ float4 slice[4];
+    const int64_t r = blockIdx.y;
+    if (!s.st[r * 2]) return;
+    const int tid = threadIdx.x;
+    const int nic = (kk + 255) / 256, ic = blockIdx.x % nic, jc = blockIdx.x / nic;
+    const double *sc = s.sc + r * 4;
+    const double P = sc[0], g2 = sc[1], UB = s.ub[r * 2 + 0];
+    const int t = ic * 256 + tid;
+    int64_t i = -1;
+    float ci = -INFINITY, m2r = 0.f, m2u = 0.f;
+    if (t < kk) {
+        i = s.ord ? s.ord[r * kk + t] : s.Sl[r * kk + t];
+        const double bqi = (double)s.bq[r * n + i];
+        const double Ai = g2 + bqi - 2.0 * (double)s.a[r * n + i];
+        const double Pi = P - (double)s.p[r * n + i];
+        // margins cover the float32 rounding of A, B and the test itself
+        ci = (float)(UB * (1.0 + 1e-5) * Pi * Pi - Ai + 1e-4 * g2);
+        m2r = (float)(-2.0 * sqrt(bqi));
+        m2u = (float)(-2.0 * UB * (1.0 + 1e-5) * Pi);
+    }
+    const float ubf = (float)(UB * (1.0 + 1e-5));
+    const float2 *br = s.br + r * n;
+    const float *pr = s.p + r * n;
+    const int64_t j0 = (int64_t)jc * JC, j1 = j0 + JC < n ? j0 + JC : n;
+    for (int64_t jt = j0; jt < j1; jt += 256) {
+        __syncthreads();
+        {
+            float4 e = make_float4(INFINITY, 0.f, 0.f, 0.f);
+            if (jt + tid < j1) {
+                const float2 b = br[jt + tid];
+                const float pj = pr[jt + tid];
+                e = make_float4(b.x - ubf * pj * pj, b.y, pj, 0.f);
+            }
+            tile[tid] = e;
+            float mb = e.x, mr = e.x < INFINITY ? e.y : 0.f, mp = e.x < INFINITY ? e.z : 0.f;
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) {
+                mb = fminf(mb, __shfl_xor(mb, off));
+                mr = fmaxf(mr, __shfl_xor(mr, off));
+                mp = fmaxf(mp, __shfl_xor(mp, off));
+            }
+            if ((tid & 63) == 0) slice[tid >> 6] = make_float4(mb, mr, mp, 0.f);
+        }
+        __syncthreads();
+        for (int u0 = 0; u0 < 256; u0 += 32) {
+            const float4 sl = slice[u0 >> 6];
+            if (!__ballot(fmaf(m2u, sl.z, fmaf(m2r, sl.y, sl.x)) <= ci)) continue;
+            uint64_t any = 0;
+#pragma unroll
+            for (int u = 0; u < 32; ++u) {
+                const float4 b = tile[u0 + u];
+                any |= __ballot(fmaf(m2u, b.z, fmaf(m2r, b.y, b.x)) <= ci);
+            }
+            if (any) {  // rare: this lane's survivors of the 32, one list slot range per wave
+                uint32_t m = 0;
+#pragma unroll
+                for (int u = 0; u < 32; ++u) {
+                    const float4 b = tile[u0 + u];
+                    m |= (fmaf(m2u, b.z, fmaf(m2r, b.y, b.x)) <= ci ? 1u : 0u) << u;
+                }
+                const int lane = tid & 63, c = __popc(m);
+                int incl = c;
+#pragma unroll
+                for (int off = 1; off < 64; off <<= 1) {
+                    const int y = __shfl_up(incl, off);
+                    if (lane >= off) incl += y;
+                }
+                int base = 0;
+                if (lane == 63) base = atomicAdd(&s.cnt[r], incl);
+                base = __shfl(base, 63);
+                int pos = base + incl - c;
+                for (; m; m &= m - 1, ++pos)
+                    if (pos < kSwapCand) s.cand[r * kSwapCand + pos] = i * n + (jt + u0 + __ffs(m) - 1);
+            }
+        }
+    }
+}
+
+// the survivors (and the upper bound's own pair) evaluated exactly; the
+// winner goes to the first partial slot of the row, the others are cleared
+template <typename T>
+__global__ void __launch_bounds__(256)
+swap_cand_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, SwapState s) {
+    __shared__ double redv[4];
+    __shared__ int64_t redi[4];
+    __shared__ double gs[256], ms[256];
+    const int64_t r = blockIdx.x;
+    if (!s.st[r * 2]) return;
+    const int tid = threadIdx.x, NT = blockDim.x;
+    const int cnt = s.cnt[r];
+    if (cnt > kSwapCand) {  // overflow: the full sweep decides this row
+        if (tid == 0) s.fb[r] = 1;
+        return;
+    }
+    if (tid == 0) s.fb[r] = 0;
+    for (int c = tid; c < d; c += NT) {
+        gs[c] = s.g[r * d + c];
+        ms[c] = s.mu[r * d + c];
+    }
+    __syncthreads();
+    const double P = s.sc[r * 4 + 0];
+    const float *p = s.p + r * n;
+    const T *vh = v + (r / G) * n * d;
+    double bv = INFINITY;
+    int64_t bp = INT64_MAX;
+    for (int c = tid; c <= cnt; c += NT) {
+        const int64_t pidx = c < cnt ? s.cand[r * kSwapCand + c] : s.ubp[r];
+        if (pidx < 0 || pidx >= n * n) continue;
+        const int64_t i = pidx / n, j = pidx % n;
+        const double num = swap_num_part(vh, d, i, j, (double)p[i], (double)p[j], gs, ms, 0, 1);
+        const double den = P - (double)p[i] + (double)p[j];
+        const double val = num / (den * den);
+        if (val < bv || (val == bv && pidx < bp)) { bv = val; bp = pidx; }
+    }
+    block_argmin_vi(bv, bp, redv, redi);
+    for (int b = tid; b < s.nblk; b += NT) {
+        s.pv[r * s.nblk + b] = b == 0 ? (float)bv : INFINITY;
+        s.pp[r * s.nblk + b] = b == 0 ? bp : INT64_MAX;
+    }
+}
+
 // reduce the tile winners, then apply the swap (or retire the row)
 template <typename T>
 __global__ void __launch_bounds__(256)
@@ -631,6 +1023,9 @@ swap_final_kernel(int64_t n, int kk, SwapState s, int32_t *s_idx, float *gap_tra
 // ===========================================================================
 namespace {
 
+constexpr int kSwapJC = 4096;  // keys per workgroup of the bound pass
+constexpr int kSwapRB = 16;    // rows of one unit per workgroup of the dots pass
+
 // the MFMA pair sweep: bf16, d = 128, whole 16-key tiles
 bool swap_mfma_ok(const fw_rows &rows) {
     return rows.dtype == FW_BF16 && rows.d == SPD && rows.n % 16 == 0 && rows.n * SPD * 2 < ((int64_t)1 << 31);
@@ -686,6 +1081,15 @@ SwapLayout swap_layout(const fw_rows &rows, int k, void *ws) {
     L.s.pv = (float *)take(R * L.s.nblk * 4);
     L.s.pp = (int64_t *)take(R * L.s.nblk * 8);
     L.s.jd = swap_mfma_ok(rows) ? (float4 *)take(R * n * 16) : nullptr;
+    if (d <= 256) {  // the pruned search stages g and mu (float64) per workgroup
+        L.s.br = (float2 *)take(R * n * 8);
+        L.s.ub = (double *)take(R * 2 * 8);
+        L.s.ubp = (int64_t *)take(R * 8);
+        L.s.cnt = (int32_t *)take(R * 4);
+        L.s.fb = (int32_t *)take(R * 4);
+        L.s.cand = (int64_t *)take(R * (size_t)kSwapCand * 8);
+        if (k <= kSwapSort) L.s.ord = (int32_t *)take(R * (size_t)k * 4);
+    }
     L.s.z = L.z;
     L.s.row_m = L.row_m;
     L.s.row_l = L.row_l;
@@ -724,8 +1128,19 @@ static hipError_t swap_large(const fw_rows &rows, int k, int max_iters, int32_t 
                        gap_traj, T_len);
     const unsigned dot_blocks = (unsigned)((n + 255) / 256 < 64 ? (n + 255) / 256 : 64);
     for (int it = 0; it < max_iters; ++it) {
-        hipLaunchKernelGGL(swap_dots_kernel<T>, dim3(dot_blocks, (unsigned)R), dim3(256), 0, st, v, G,
-                           n, d, L.s);
+        if (G % kSwapRB == 0 && d <= 256)
+            hipLaunchKernelGGL((swap_dots_group_kernel<T, kSwapRB>), dim3(dot_blocks, (unsigned)(R / kSwapRB)),
+                               dim3(256), 0, st, v, G, n, d, L.s);
+        else
+            hipLaunchKernelGGL(swap_dots_kernel<T>, dim3(dot_blocks, (unsigned)R), dim3(256), 0, st, v, G,
+                               n, d, L.s);
+        if (L.s.br) {  // pruned search; the sweep below then runs only for overflowing rows
+            hipLaunchKernelGGL(swap_ub_kernel<T>, dim3((unsigned)R), dim3(256), 0, st, v, G, n, d, k, L.s);
+            hipLaunchKernelGGL(swap_bound_kernel<kSwapJC>,
+                               dim3((unsigned)(((k + 255) / 256) * ((n + kSwapJC - 1) / kSwapJC)), (unsigned)R),
+                               dim3(256), 0, st, n, k, L.s);
+            hipLaunchKernelGGL(swap_cand_kernel<T>, dim3((unsigned)R), dim3(256), 0, st, v, G, n, d, L.s);
+        }
         if (swap_mfma_ok(rows))
             hipLaunchKernelGGL(swap_pairs_mfma_kernel, dim3((unsigned)L.s.nblk, (unsigned)R), dim3(512),
                                (size_t)(2 * SP_STAGE + 2 * SPT * 16 * 16 + 8 * 4 + 8 * 8), st,
