@@ -169,18 +169,19 @@ swap_init_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, S
     float *p = s.p + r * n;
     uint8_t *inS = s.inS + r * n;
     const float *zr = s.z + r * n;
-    // weights and membership; kept list in ascending order
-    const int64_t chunk = (n + NT - 1) / NT;
-    const int64_t lo = tid * chunk, hi = (lo + chunk < n) ? lo + chunk : n;
-    int c = 0;
-    for (int64_t j = lo; j < hi; ++j) {
+    // weights and membership (coalesced), then the kept list in ascending
+    // order from per-thread chunks of the membership bytes
+    for (int64_t j = tid; j < n; j += NT) {
         const float zz = zr[j];
         p[j] = expf(zz - m) * inv_l;
         const uint32_t u = ord_key(zz);
-        const uint8_t in = (u > key) || (u == key && j <= cut);
-        inS[j] = in;
-        c += in;
+        inS[j] = (uint8_t)((u > key) || (u == key && j <= cut));
     }
+    __syncthreads();
+    const int64_t chunk = (n + NT - 1) / NT;
+    const int64_t lo = tid * chunk, hi = (lo + chunk < n) ? lo + chunk : n;
+    int c = 0;
+    for (int64_t j = lo; j < hi; ++j) c += inS[j];
     int total;
     int pos = block_exclusive_scan(c, scan, &total);
     for (int64_t j = lo; j < hi; ++j)
@@ -216,27 +217,59 @@ swap_init_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, S
     __syncthreads();
     double mu2 = 0.0;
     for (int cc = 0; cc < d; ++cc) mu2 += mu[cc] * mu[cc];
-    // w_j = v_j . mu and ||u_j||^2 = p_j^2 ||v_j - mu||^2
-    for (int64_t j = tid; j < n; j += NT) {
-        double dw = 0.0, du = 0.0;
-        for (int cc = 0; cc < d; ++cc) {
-            const double x = (double)Elem<T>::load(vh, j * d + cc);
-            dw = fma(x, mu[cc], dw);
-            du = fma(x - mu[cc], x - mu[cc], du);
+    // w_j = v_j . mu and ||u_j||^2 = p_j^2 ||v_j - mu||^2: 16 lanes per key
+    // (columns lane, lane + 16, ...: coalesced), partial sums by a butterfly
+    {
+        const int jl = tid >> 4, cl = tid & 15;
+        for (int64_t j0 = 0; j0 < n; j0 += NT / 16) {
+            const int64_t j = j0 + jl;
+            double dw = 0.0, du = 0.0;
+            if (j < n)
+                for (int cc = cl; cc < d; cc += 16) {
+                    const double x = (double)Elem<T>::load(vh, j * d + cc), m = mu[cc];
+                    dw = fma(x, m, dw);
+                    du = fma(x - m, x - m, du);
+                }
+#pragma unroll
+            for (int off = 1; off < 16; off <<= 1) {
+                dw += __shfl_xor(dw, off);
+                du += __shfl_xor(du, off);
+            }
+            if (j < n && cl == 0) {
+                s.w[r * n + j] = (float)dw;
+                s.bq[r * n + j] = (float)((double)p[j] * (double)p[j] * du);
+            }
         }
-        s.w[r * n + j] = (float)dw;
-        s.bq[r * n + j] = (float)((double)p[j] * (double)p[j] * du);
     }
-    // g = sum_{a in S} u_a, P = p(S)
+    // g = sum_{a in S} u_a, P = p(S): 16 kept-key lanes x 16 column groups,
+    // the key lanes' sums added by a butterfly
     double *g = s.g + r * d;
-    for (int cc = tid; cc < d; cc += NT) {
-        double acc = 0.0;
-        for (int i = 0; i < kk; ++i) {
-            const int64_t a = s.Sl[r * kk + i];
-            acc += (double)p[a] * ((double)Elem<T>::load(vh, a * d + cc) - mu[cc]);
+    {
+        const int kl = tid & 15, cg = tid >> 4;
+        for (int c0 = 8 * cg; c0 < d; c0 += 128) {
+            double acc[8];
+#pragma unroll
+            for (int x = 0; x < 8; ++x) acc[x] = 0.0;
+            for (int i = kl; i < kk; i += 16) {
+                const int64_t a = s.Sl[r * kk + i];
+                const double pa = (double)p[a];
+#pragma unroll
+                for (int x = 0; x < 8; ++x)
+                    if (c0 + x < d) acc[x] = fma(pa, (double)Elem<T>::load(vh, a * d + c0 + x) - mu[c0 + x], acc[x]);
+            }
+#pragma unroll
+            for (int x = 0; x < 8; ++x) {
+#pragma unroll
+                for (int off = 1; off < 16; off <<= 1) acc[x] += __shfl_xor(acc[x], off);
+            }
+            if (kl == 0) {
+#pragma unroll
+                for (int x = 0; x < 8; ++x)
+                    if (c0 + x < d) g[c0 + x] = acc[x];
+            }
         }
-        g[cc] = acc;
     }
+    __syncthreads();
     double P = 0.0;
     for (int i = tid; i < kk; i += NT) P += (double)p[s.Sl[r * kk + i]];
     P = block_reduce(P, redd, OpSum());
@@ -667,35 +700,60 @@ swap_ub_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, Swa
         gs[c] = s.g[r * d + c];
         ms[c] = s.mu[r * d + c];
     }
-    // eight smallest B_j and A_i, each round after the previous (value, index)
-    double pvj = -INFINITY, pvi = -INFINITY;
-    int64_t pij = -1, pii = -1;
-    for (int u = 0; u < 8; ++u) {
-        double bv = INFINITY;
-        int64_t bi = INT64_MAX;
-        for (int64_t j = tid; j < n; j += NT) {
-            const double x = (double)br[j].x;
-            if (!(x < INFINITY)) continue;
-            const bool after = x > pvj || (x == pvj && j > pij);
-            if (after && (x < bv || (x == bv && j < bi))) { bv = x; bi = j; }
+    // eight smallest B_j and A_i: each thread keeps its own eight (value,
+    // index ascending) in one pass, then eight rounds over the threads' lists
+    // in LDS pick the workgroup's, each after the previous (value, index)
+    __shared__ double lv[256 * 8];
+    __shared__ int64_t li[256 * 8];
+    auto top8 = [&](auto &&get, int64_t cnt, int64_t *dst) __attribute__((always_inline)) {
+        double tv[8];
+        int64_t ti[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) { tv[q] = INFINITY; ti[q] = INT64_MAX; }
+        for (int64_t e = tid; e < cnt; e += NT) {
+            int64_t id;
+            const double x = get(e, id);
+            if (!(x < tv[7] || (x == tv[7] && id < ti[7]))) continue;
+            tv[7] = x;
+            ti[7] = id;
+#pragma unroll
+            for (int q = 7; q > 0; --q) {
+                const bool sw = tv[q] < tv[q - 1] || (tv[q] == tv[q - 1] && ti[q] < ti[q - 1]);
+                const double v0 = tv[q - 1];
+                const int64_t i0 = ti[q - 1];
+                tv[q - 1] = sw ? tv[q] : v0;
+                ti[q - 1] = sw ? ti[q] : i0;
+                tv[q] = sw ? v0 : tv[q];
+                ti[q] = sw ? i0 : ti[q];
+            }
         }
-        block_argmin_vi(bv, bi, redv, redi);
-        if (tid == 0) topj[u] = bi < INT64_MAX ? bi : -1;
-        pvj = bv;
-        pij = bi;
-        double av = INFINITY;
-        int64_t ai = INT64_MAX;
-        for (int t = tid; t < kk; t += NT) {
-            const int64_t i = Sl[t];
-            const double x = g2 + (double)bq[i] - 2.0 * (double)a[i];
-            const bool after = x > pvi || (x == pvi && i > pii);
-            if (after && (x < av || (x == av && i < ai))) { av = x; ai = i; }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) { lv[tid * 8 + q] = tv[q]; li[tid * 8 + q] = ti[q]; }
+        __syncthreads();
+        double pv = -INFINITY;
+        int64_t pi = -1;
+        for (int u = 0; u < 8; ++u) {
+            double bv = INFINITY;
+            int64_t bi = INT64_MAX;
+            for (int q = 0; q < 8; ++q) {
+                const double x = lv[tid * 8 + q];
+                const int64_t id = li[tid * 8 + q];
+                if (!(x < INFINITY)) continue;
+                const bool after = x > pv || (x == pv && id > pi);
+                if (after && (x < bv || (x == bv && id < bi))) { bv = x; bi = id; }
+            }
+            block_argmin_vi(bv, bi, redv, redi);
+            if (tid == 0) dst[u] = bi < INT64_MAX ? bi : -1;
+            pv = bv;
+            pi = bi;
         }
-        block_argmin_vi(av, ai, redv, redi);
-        if (tid == 0) topi[u] = ai < INT64_MAX ? ai : -1;
-        pvi = av;
-        pii = ai;
-    }
+    };
+    top8([&](int64_t j, int64_t &id) { id = j; return (double)br[j].x; }, n, topj);
+    top8([&](int64_t t, int64_t &id) {
+        const int64_t i = Sl[t];
+        id = i;
+        return g2 + (double)bq[i] - 2.0 * (double)a[i];
+    }, (int64_t)kk, topi);
     __syncthreads();
     // the 64 pairs: four lanes per pair, each a quarter of the columns
     const int pr = tid >> 2, qt = tid & 3;
@@ -790,15 +848,18 @@ swap_ub_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, Swa
 template <int JC>
 __global__ void __launch_bounds__(256)
 swap_bound_kernel(int64_t n, int kk, SwapState s) {
-    __shared__ float4 tile[256];
-    __shared__ float4 slice[4];
+    __shared__ float4 tile[2][256];
+    __shared__ float4 slice[2][4];
     const int64_t r = blockIdx.y;
     if (!s.st[r * 2]) return;
     const int tid = threadIdx.x;
     const int nic = (kk + 255) / 256, ic = blockIdx.x % nic, jc = blockIdx.x / nic;
     const double *sc = s.sc + r * 4;
     const double P = sc[0], g2 = sc[1], UB = s.ub[r * 2 + 0];
-    const int t = ic * 256 + tid;
+    // the kept keys most likely to pass (first in the order) fill one wave
+    // per workgroup; which wave rotates with the key chunk, so that those
+    // waves of the workgroups on a CU sit on different SIMDs
+    const int t = ic * 256 + (((tid >> 6) + jc) & 3) * 64 + (tid & 63);
     int64_t i = -1;
     float ci = -INFINITY, m2r = 0.f, m2u = 0.f;
     if (t < kk) {
@@ -815,16 +876,27 @@ swap_bound_kernel(int64_t n, int kk, SwapState s) {
     const float2 *br = s.br + r * n;
     const float *pr = s.p + r * n;
     const int64_t j0 = (int64_t)jc * JC, j1 = j0 + JC < n ? j0 + JC : n;
-    for (int64_t jt = j0; jt < j1; jt += 256) {
-        __syncthreads();
+    // the next tile's keys are loaded while this one is tested; two LDS
+    // buffers, one barrier per tile
+    float2 nb = make_float2(INFINITY, 0.f);
+    float np = 0.f;
+    if (j0 + tid < j1) {
+        nb = br[j0 + tid];
+        np = pr[j0 + tid];
+    }
+    int buf = 0;
+    for (int64_t jt = j0; jt < j1; jt += 256, buf ^= 1) {
+        float4 (&tile_b)[256] = tile[buf];
         {
-            float4 e = make_float4(INFINITY, 0.f, 0.f, 0.f);
-            if (jt + tid < j1) {
-                const float2 b = br[jt + tid];
-                const float pj = pr[jt + tid];
-                e = make_float4(b.x - ubf * pj * pj, b.y, pj, 0.f);
+            const float2 b = nb;
+            const float pj = np;
+            if (jt + 256 + tid < j1) {
+                nb = br[jt + 256 + tid];
+                np = pr[jt + 256 + tid];
             }
-            tile[tid] = e;
+            float4 e = make_float4(INFINITY, 0.f, 0.f, 0.f);
+            if (jt + tid < j1) e = make_float4(b.x - ubf * pj * pj, b.y, pj, 0.f);
+            tile_b[tid] = e;
             float mb = e.x, mr = e.x < INFINITY ? e.y : 0.f, mp = e.x < INFINITY ? e.z : 0.f;
 #pragma unroll
             for (int off = 32; off > 0; off >>= 1) {
@@ -832,23 +904,23 @@ swap_bound_kernel(int64_t n, int kk, SwapState s) {
                 mr = fmaxf(mr, __shfl_xor(mr, off));
                 mp = fmaxf(mp, __shfl_xor(mp, off));
             }
-            if ((tid & 63) == 0) slice[tid >> 6] = make_float4(mb, mr, mp, 0.f);
+            if ((tid & 63) == 0) slice[buf][tid >> 6] = make_float4(mb, mr, mp, 0.f);
         }
         __syncthreads();
         for (int u0 = 0; u0 < 256; u0 += 32) {
-            const float4 sl = slice[u0 >> 6];
+            const float4 sl = slice[buf][u0 >> 6];
             if (!__ballot(fmaf(m2u, sl.z, fmaf(m2r, sl.y, sl.x)) <= ci)) continue;
             uint64_t any = 0;
 #pragma unroll
             for (int u = 0; u < 32; ++u) {
-                const float4 b = tile[u0 + u];
+                const float4 b = tile_b[u0 + u];
                 any |= __ballot(fmaf(m2u, b.z, fmaf(m2r, b.y, b.x)) <= ci);
             }
             if (any) {  // rare: this lane's survivors of the 32, one list slot range per wave
                 uint32_t m = 0;
 #pragma unroll
                 for (int u = 0; u < 32; ++u) {
-                    const float4 b = tile[u0 + u];
+                    const float4 b = tile_b[u0 + u];
                     m |= (fmaf(m2u, b.z, fmaf(m2r, b.y, b.x)) <= ci ? 1u : 0u) << u;
                 }
                 const int lane = tid & 63, c = __popc(m);
