@@ -35,7 +35,7 @@ constexpr int kPoolMax = 64;  // pool keys (one 64-bit mask)
 constexpr int kMaxBudgets = FW_POOL_MAX_BUDGETS;
 
 struct PoolLds {
-    size_t xq, mu, red, ctr, rank, tmp, plist, pps, sc, seed;  // persistent
+    size_t xq, mu, red, ctr, rank, eord, tmp, plist, pps, sc, seed;  // persistent
     size_t zz, ee, rk;                                   // row phase
     size_t gm, vs, cv, ent, pl;                          // pool phase (overlays the row phase)
     size_t total;
@@ -52,6 +52,7 @@ __host__ __device__ inline PoolLds pool_lds(int64_t N, int d, int Pmax, int nent
     L.red = take((size_t)PT * 16);
     L.ctr = take(16);
     L.rank = take((size_t)kPoolMax * 4);                // top keys in rank order
+    L.eord = take((size_t)kPoolMax * 4);                // keys of largest single-key error, in order
     L.tmp = take((size_t)kPoolMax * 4);                 // a pool in output order
     L.plist = take((size_t)kMaxBudgets * kPoolMax * 4);  // each pool, ascending keys
     L.pps = take((size_t)kMaxBudgets * kPoolMax * 8);    // their masses
@@ -179,6 +180,56 @@ struct PoolArgs {
 
 }  // namespace
 
+// The M (<= kPoolMax) largest values of vals[0, N) in the order (value desc,
+// index asc), keys with skip[j] < smin left out (no skip: all keys), their
+// indices into out[0, M).  Each wave takes the next best of its own keys M
+// times (shuffles only, no workgroup barrier), then the waves' lists are
+// merged by counting ranks.  cv, ci: LDS scratch of (blockDim.x / 64) M
+// entries.
+__device__ inline void wave_top(const double *vals, int64_t N, int M, int *out, double *cv, int64_t *ci,
+                                const unsigned char *skip = nullptr, int smin = 0) {
+    const int tid = threadIdx.x, NT = blockDim.x, lane = tid & 63, w = tid >> 6, nw = NT >> 6;
+    double pv = INFINITY;
+    int64_t pi = -1;
+    for (int t = 0; t < M; ++t) {
+        double bv = 0.0;
+        int64_t bi = -1;
+        for (int64_t j = tid; j < N; j += NT) {
+            if (skip && skip[j] < smin) continue;
+            const double x = vals[j];
+            const bool after = x < pv || (x == pv && j > pi);
+            if (after && (bi < 0 || x > bv || (x == bv && j < bi))) { bv = x; bi = j; }
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            const double ov = __shfl_xor(bv, off);
+            const int64_t oi = __shfl_xor(bi, off);
+            if (oi >= 0 && (bi < 0 || ov > bv || (ov == bv && oi < bi))) { bv = ov; bi = oi; }
+        }
+        if (lane == 0) {
+            cv[w * M + t] = bv;
+            ci[w * M + t] = bi;
+        }
+        if (bi >= 0) {  // none left: the later rounds find none either
+            pv = bv;
+            pi = bi;
+        }
+    }
+    __syncthreads();
+    for (int c = tid; c < nw * M; c += NT) {
+        const int64_t i = ci[c];
+        if (i < 0) continue;
+        const double v = cv[c];
+        int rank = 0;
+        for (int e = 0; e < nw * M; ++e) {
+            const int64_t oi = ci[e];
+            rank += oi >= 0 && (cv[e] > v || (cv[e] == v && oi < i));
+        }
+        if (rank < M) out[rank] = (int)i;
+    }
+    __syncthreads();
+}
+
 template <typename T>
 __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -194,6 +245,7 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
     int64_t *redi = (int64_t *)(redd + NT);
     int *ctr = (int *)(smem + L.ctr);
     int *rank = (int *)(smem + L.rank);
+    int *eord = (int *)(smem + L.eord);
     int *tmp = (int *)(smem + L.tmp);
     int *plist = (int *)(smem + L.plist);
     double *pps = (double *)(smem + L.pps);
@@ -229,28 +281,9 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
     for (int64_t j = tid; j < N; j += NT) zmax = fmax(zmax, zz[j]);
     zmax = block_reduce(zmax, redd, OpMax());
 
-    // top keys in rank order: Smax rounds, each the next key in (z desc, j asc);
-    // every budget's A*_s is a prefix
-    {
-        double pv = INFINITY;
-        int64_t pi = -1;
-        for (int t = 0; t < a.Smax; ++t) {
-            double bv = 0.0;
-            int64_t bi = -1;
-            for (int64_t j = tid; j < N; j += NT) {
-                const double z = zz[j];
-                const bool after = z < pv || (z == pv && j > pi);
-                if (after && (bi < 0 || z > bv || (z == bv && j < bi))) { bv = z; bi = j; }
-            }
-            block_argmax(bv, bi, redd, redi);
-            if (tid == 0 && bi >= 0) {  // Smax <= n: a key is always found
-                rank[t] = (int)bi;
-                rk[bi] = (unsigned char)t;
-            }
-            pv = bv;
-            pi = bi;
-        }
-    }
+    // top keys in rank order (z desc, j asc); every budget's A*_s is a prefix
+    wave_top(zz, N, a.Smax, rank, redd, redi);
+    for (int t = tid; t < a.Smax; t += NT) rk[rank[t]] = (unsigned char)t;
     // weights in place of the logits; each budget's dropped mass summed over
     // its dropped keys themselves
     double lsum = 0.0;
@@ -330,25 +363,23 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
     dmax = block_reduce(dmax, redd, OpMax());
 
     // ---- 2. each budget's candidate set ------------------------------------------
+    // keys outside the smallest budget's A*_s in order of single-key error
+    // (e desc, j asc): the first extra + s - smin hold a budget's extra keys
+    // (at most s - smin of them are in its A*_s)
+    int smin = a.b[0].s, me = 0;
+    for (int b = 1; b < nb; ++b) smin = a.b[b].s < smin ? a.b[b].s : smin;
+    for (int b = 0; b < nb; ++b) me = a.b[b].extra + a.b[b].s - smin > me ? a.b[b].extra + a.b[b].s - smin : me;
+    wave_top(ee, N, me, eord, redd, redi, rk, smin);
     for (int b = 0; b < nb; ++b) {
         const PoolBudget &B = a.b[b];
         const int s = B.s, P = B.P;
         // the extra keys: largest single-key errors outside A*_s
-        double pv = INFINITY;
-        int64_t pi = -1;
-        for (int t = 0; t < B.extra; ++t) {
-            double bv = 0.0;
-            int64_t bi = -1;
-            for (int64_t j = tid; j < N; j += NT) {
-                if (rk[j] < s) continue;
-                const double e = ee[j];
-                const bool after = e < pv || (e == pv && j > pi);
-                if (after && (bi < 0 || e > bv || (e == bv && j < bi))) { bv = e; bi = j; }
+        if (tid == 0) {
+            int t = 0;
+            for (int u = 0; u < me && t < B.extra; ++u) {
+                const int j = eord[u];
+                if (rk[j] >= s) tmp[s + t++] = j;
             }
-            block_argmax(bv, bi, redd, redi);
-            if (tid == 0) tmp[s + t] = bi >= 0 ? (int)bi : 0;  // s + extra <= n
-            pv = bv;
-            pi = bi;
         }
         if (tid < s) tmp[tid] = rank[tid];
         __syncthreads();
