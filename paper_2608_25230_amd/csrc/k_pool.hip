@@ -113,20 +113,42 @@ __device__ inline uint64_t enum_complement(const double *Gm, const double *ps, i
             rr -= binom(c, sz);
             --c;
         }
+        // the keys of D in registers, every term from independent reads;
+        // against the thread's best ratio beta the test S - beta p(A)^2 <= 0
+        // is one fused multiply-add, and only passing sets take the division
+        double beta = INFINITY;
         for (uint64_t r = lo; r < hi; ++r) {
+            int kd[kDirectDrop];
+            uint64_t m = D;
+#pragma unroll
+            for (int x = 0; x < kDirectDrop; ++x) {
+                kd[x] = m ? __ffsll((unsigned long long)m) - 1 : 0;
+                m &= m - 1;
+            }
             double S = SU, pD = 0.0;
-            for (uint64_t m = D; m; m &= m - 1) {
-                const int i = __ffsll((unsigned long long)m) - 1;
-                S -= 2.0 * cv[i];
-                pD += ps[i];
-                for (uint64_t m2 = D; m2; m2 &= m2 - 1) S += Gm[i * P + (__ffsll((unsigned long long)m2) - 1)];
+#pragma unroll
+            for (int x = 0; x < kDirectDrop; ++x) {
+                if (x < q) {
+                    const double *rx = Gm + kd[x] * P;
+                    pD += ps[kd[x]];
+                    double t = rx[kd[x]] - 2.0 * cv[kd[x]];
+#pragma unroll
+                    for (int y = 0; y < x; ++y) t = fma(2.0, rx[kd[y]], t);
+                    S += t;
+                }
             }
             const double PA = pU - pD;
+            if (!(fma(-beta, PA * PA, fmax(S, 0.0)) <= 1e-12 * beta) && beta < INFINITY) {
+                const uint64_t u = D & (~D + 1ull), v = D + u;
+                D = v | (((v ^ D) >> 2) >> (__ffsll((unsigned long long)D) - 1));
+                continue;
+            }
             const double val = fmax(S, 0.0) / (PA * PA);
             const uint64_t A = all & ~D;
             if (val < best || (val == best && lex_less(A, bestA))) {
                 best = val;
                 bestA = A;
+                beta = val;
             }
             // next mask of the same size (colex successor)
             const uint64_t u = D & (~D + 1ull), v = D + u;
