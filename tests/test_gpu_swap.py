@@ -123,3 +123,23 @@ def test_full_size_swap_sampled(torch_fw):
             seg = gt[h, g, : ns[h, g] + 1]
             assert np.all(np.diff(seg) < 0) and np.all(np.isnan(gt[h, g, ns[h, g] + 1:]))
     assert np.all((out["dropped"] >= 0) & (out["dropped"] <= 1))
+
+
+def test_long_rows_tied_pairs_fall_back_to_full_sweep(torch_fw):
+    """Uniform weights over keys whose values repeat 8 distinct rows: every
+    pair of the same two value kinds ties, so thousands of pairs survive the
+    pruned search's lower bound and the row falls back to the full sweep.
+    The sets must still match the oracle (ties to the smaller (i, j))."""
+    torch, fw = torch_fw
+    rng = np.random.default_rng(11)
+    n, d, k = 2048, 128, 512
+    base = rng.standard_normal((8, d)).astype(np.float32)
+    V = base[rng.integers(0, 8, n)][None]
+    K = rng.standard_normal((1, n, d)).astype(np.float32)
+    q = np.zeros((1, 2, d), np.float32)
+    rows = W.Rows("bf16", W.bf16_bits(q), W.bf16_bits(K), W.bf16_bits(V),
+                  np.full(1, 1.0 / np.sqrt(d), np.float32))
+    out = _run(torch, fw, rows, k, 4)
+    t = _check(rows, k, 4, out, [(0, 0), (0, 1)], method="gform")
+    assert np.all(out["n_swaps"] >= 1)
+    print("tied pairs:", t)
