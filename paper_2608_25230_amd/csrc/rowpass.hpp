@@ -156,4 +156,54 @@ __device__ inline void block_argmax(double &val, int64_t &idx, double *redv, int
 
 __device__ inline double block_sum(double v, double *red) { return block_reduce(v, red, OpSum()); }
 
+// The M (<= 64) largest values of vals[0, N) in the order (value desc,
+// index asc), keys with skip[j] < smin left out (no skip: all keys), their
+// indices into out[0, M).  Each wave takes the next best of its own keys M
+// times (shuffles only, no workgroup barrier), then the waves' lists are
+// merged by counting ranks.  cv, ci: LDS scratch of (blockDim.x / 64) M
+// entries.
+__device__ inline void wave_top(const double *vals, int64_t N, int M, int *out, double *cv, int64_t *ci,
+                                const unsigned char *skip = nullptr, int smin = 0) {
+    const int tid = threadIdx.x, NT = blockDim.x, lane = tid & 63, w = tid >> 6, nw = NT >> 6;
+    double pv = INFINITY;
+    int64_t pi = -1;
+    for (int t = 0; t < M; ++t) {
+        double bv = 0.0;
+        int64_t bi = -1;
+        for (int64_t j = tid; j < N; j += NT) {
+            if (skip && skip[j] < smin) continue;
+            const double x = vals[j];
+            const bool after = x < pv || (x == pv && j > pi);
+            if (after && (bi < 0 || x > bv || (x == bv && j < bi))) { bv = x; bi = j; }
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            const double ov = __shfl_xor(bv, off);
+            const int64_t oi = __shfl_xor(bi, off);
+            if (oi >= 0 && (bi < 0 || ov > bv || (ov == bv && oi < bi))) { bv = ov; bi = oi; }
+        }
+        if (lane == 0) {
+            cv[w * M + t] = bv;
+            ci[w * M + t] = bi;
+        }
+        if (bi >= 0) {  // none left: the later rounds find none either
+            pv = bv;
+            pi = bi;
+        }
+    }
+    __syncthreads();
+    for (int c = tid; c < nw * M; c += NT) {
+        const int64_t i = ci[c];
+        if (i < 0) continue;
+        const double v = cv[c];
+        int rank = 0;
+        for (int e = 0; e < nw * M; ++e) {
+            const int64_t oi = ci[e];
+            rank += oi >= 0 && (cv[e] > v || (cv[e] == v && oi < i));
+        }
+        if (rank < M) out[rank] = (int)i;
+    }
+    __syncthreads();
+}
+
 }  // namespace fw

@@ -83,6 +83,7 @@ def test_group_of_one_votes_its_own_top_mass_set(torch_fw):
     (2, 6, 40, 16, 4, 3, 2.0, 0.0),    # vector loads
     (2, 8, 37, 12, 6, 4, 3.0, 4.0),    # ragged n, one element per lane
     (3, 4, 64, 64, 8, 2, 1.5, 4.0),
+    (2, 4, 300, 16, 80, 2, 1.0, 0.0),  # s > 64: one workgroup argmax per pick
 ])
 def test_small_groups_fp32(torch_fw, cfg):
     torch, fw = torch_fw
