@@ -152,6 +152,7 @@ struct SwapState {
 };
 
 constexpr int kSwapCand = 4096;  // surviving pairs kept per row
+constexpr int kSwapSL = 16;      // keys per slice of the bound pass's whole-slice test (<= 32)
 constexpr int kSwapSort = 2048;  // kept keys ordered for the bound pass
 
 template <typename T>
@@ -841,25 +842,25 @@ swap_ub_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, Swa
 // test  A_i + B_j - 2 r_i r_j <= UB (Pi + p_j)^2  is, expanded,
 //     (B_j - UB p_j^2) - 2 r_i r_j - 2 UB Pi p_j <= UB Pi^2 - A_i,
 // two fused multiply-adds and a compare per pair; the keys' terms are staged
-// in LDS per tile and read by all threads alike.  Each 64-key slice of a tile
+// in LDS per tile and read by all threads alike.  Each 16-key slice of a tile
 // is first tested as a whole, with its smallest B_j - UB p_j^2 and largest
 // r_j and p_j (a lower bound for every pair of the slice): a wave whose lanes
 // all fail skips the slice.
-template <int JC>
-__global__ void __launch_bounds__(256)
+template <int JC, int BT>
+__global__ void __launch_bounds__(BT)
 swap_bound_kernel(int64_t n, int kk, SwapState s) {
-    __shared__ float4 tile[2][256];
-    __shared__ float4 slice[2][4];
+    __shared__ float4 tile[2][BT];
+    __shared__ float4 slice[2][BT / kSwapSL];
     const int64_t r = blockIdx.y;
     if (!s.st[r * 2]) return;
     const int tid = threadIdx.x;
-    const int nic = (kk + 255) / 256, ic = blockIdx.x % nic, jc = blockIdx.x / nic;
+    const int nic = (kk + BT - 1) / BT, ic = blockIdx.x % nic, jc = blockIdx.x / nic;
     const double *sc = s.sc + r * 4;
     const double P = sc[0], g2 = sc[1], UB = s.ub[r * 2 + 0];
     // the kept keys most likely to pass (first in the order) fill one wave
     // per workgroup; which wave rotates with the key chunk, so that those
     // waves of the workgroups on a CU sit on different SIMDs
-    const int t = ic * 256 + (((tid >> 6) + jc) & 3) * 64 + (tid & 63);
+    const int t = ic * BT + (((tid >> 6) + jc) % (BT / 64)) * 64 + (tid & 63);
     int64_t i = -1;
     float ci = -INFINITY, m2r = 0.f, m2u = 0.f;
     if (t < kk) {
@@ -885,41 +886,41 @@ swap_bound_kernel(int64_t n, int kk, SwapState s) {
         np = pr[j0 + tid];
     }
     int buf = 0;
-    for (int64_t jt = j0; jt < j1; jt += 256, buf ^= 1) {
-        float4 (&tile_b)[256] = tile[buf];
+    for (int64_t jt = j0; jt < j1; jt += BT, buf ^= 1) {
+        float4 (&tile_b)[BT] = tile[buf];
         {
             const float2 b = nb;
             const float pj = np;
-            if (jt + 256 + tid < j1) {
-                nb = br[jt + 256 + tid];
-                np = pr[jt + 256 + tid];
+            if (jt + BT + tid < j1) {
+                nb = br[jt + BT + tid];
+                np = pr[jt + BT + tid];
             }
             float4 e = make_float4(INFINITY, 0.f, 0.f, 0.f);
             if (jt + tid < j1) e = make_float4(b.x - ubf * pj * pj, b.y, pj, 0.f);
             tile_b[tid] = e;
             float mb = e.x, mr = e.x < INFINITY ? e.y : 0.f, mp = e.x < INFINITY ? e.z : 0.f;
 #pragma unroll
-            for (int off = 32; off > 0; off >>= 1) {
+            for (int off = kSwapSL / 2; off > 0; off >>= 1) {
                 mb = fminf(mb, __shfl_xor(mb, off));
                 mr = fmaxf(mr, __shfl_xor(mr, off));
                 mp = fmaxf(mp, __shfl_xor(mp, off));
             }
-            if ((tid & 63) == 0) slice[buf][tid >> 6] = make_float4(mb, mr, mp, 0.f);
+            if ((tid & (kSwapSL - 1)) == 0) slice[buf][tid / kSwapSL] = make_float4(mb, mr, mp, 0.f);
         }
         __syncthreads();
-        for (int u0 = 0; u0 < 256; u0 += 32) {
-            const float4 sl = slice[buf][u0 >> 6];
+        for (int u0 = 0; u0 < BT; u0 += kSwapSL) {
+            const float4 sl = slice[buf][u0 / kSwapSL];
             if (!__ballot(fmaf(m2u, sl.z, fmaf(m2r, sl.y, sl.x)) <= ci)) continue;
             uint64_t any = 0;
 #pragma unroll
-            for (int u = 0; u < 32; ++u) {
+            for (int u = 0; u < kSwapSL; ++u) {
                 const float4 b = tile_b[u0 + u];
                 any |= __ballot(fmaf(m2u, b.z, fmaf(m2r, b.y, b.x)) <= ci);
             }
-            if (any) {  // rare: this lane's survivors of the 32, one list slot range per wave
+            if (any) {  // rare: this lane's survivors of the slice, one list slot range per wave
                 uint32_t m = 0;
 #pragma unroll
-                for (int u = 0; u < 32; ++u) {
+                for (int u = 0; u < kSwapSL; ++u) {
                     const float4 b = tile_b[u0 + u];
                     m |= (fmaf(m2u, b.z, fmaf(m2r, b.y, b.x)) <= ci ? 1u : 0u) << u;
                 }
@@ -1096,6 +1097,7 @@ swap_final_kernel(int64_t n, int kk, SwapState s, int32_t *s_idx, float *gap_tra
 namespace {
 
 constexpr int kSwapJC = 4096;  // keys per workgroup of the bound pass
+constexpr int kSwapBT = 256;   // kept keys (threads) per workgroup of the bound pass
 constexpr int kSwapRB = 16;    // rows of one unit per workgroup of the dots pass
 
 // the MFMA pair sweep: bf16, d = 128, whole 16-key tiles
@@ -1208,9 +1210,10 @@ static hipError_t swap_large(const fw_rows &rows, int k, int max_iters, int32_t 
                                n, d, L.s);
         if (L.s.br) {  // pruned search; the sweep below then runs only for overflowing rows
             hipLaunchKernelGGL(swap_ub_kernel<T>, dim3((unsigned)R), dim3(256), 0, st, v, G, n, d, k, L.s);
-            hipLaunchKernelGGL(swap_bound_kernel<kSwapJC>,
-                               dim3((unsigned)(((k + 255) / 256) * ((n + kSwapJC - 1) / kSwapJC)), (unsigned)R),
-                               dim3(256), 0, st, n, k, L.s);
+            hipLaunchKernelGGL((swap_bound_kernel<kSwapJC, kSwapBT>),
+                               dim3((unsigned)(((k + kSwapBT - 1) / kSwapBT) * ((n + kSwapJC - 1) / kSwapJC)),
+                                    (unsigned)R),
+                               dim3(kSwapBT), 0, st, n, k, L.s);
             hipLaunchKernelGGL(swap_cand_kernel<T>, dim3((unsigned)R), dim3(256), 0, st, v, G, n, d, L.s);
         }
         if (swap_mfma_ok(rows))
