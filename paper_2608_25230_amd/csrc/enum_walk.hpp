@@ -101,9 +101,10 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                     for (int j = 0; j < i; ++j) sv = fma(2.0, ri[kx[j]], sv);
                     SO += sv;
                     if (ws > 0) {
+                        // all WMAX positions, unguarded: those past the walked
+                        // range read neighbouring LDS words and are never used
 #pragma unroll
-                        for (int x = 0; x < WMAX; ++x)
-                            if (x < wn) e[x] += ri[wb + x];
+                        for (int x = 0; x < WMAX; ++x) e[x] += ri[wb + x];
                     }
                 }
             }
@@ -123,8 +124,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
         if (ws > 0) {
             const double b2p = 2.0 * beta * PO;
 #pragma unroll
-            for (int x = 0; x < WMAX; ++x)
-                if (x < wn) e[x] = fma(2.0, e[x], -b2p * ps[wb + x]);
+            for (int x = 0; x < WMAX; ++x) e[x] = fma(2.0, e[x], -b2p * ps[wb + x]);
         }
         const double2 *en = ent + C.toff;
         const double *plt = PLt + C.toff;
