@@ -116,8 +116,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                 for (uint64_t b2 = Om; b2; b2 &= b2 - 1) SO += row[__ffsll((unsigned long long)b2) - 1];
                 if (ws > 0) {
 #pragma unroll
-                    for (int y = 0; y < WMAX; ++y)
-                        if (y < wn) e[y] += row[wb + y];
+                    for (int y = 0; y < WMAX; ++y) e[y] += row[wb + y];
                 }
             }
         }
@@ -194,7 +193,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                     const double dB = lower_beta();
 #pragma unroll
                     for (int x = 0; x < WMAX; ++x)
-                        if (x < wn) e[x] -= 2.0 * dB * PO * ps[wb + x];
+                        e[x] -= 2.0 * dB * PO * ps[wb + x];
                 }
             };
             if (ws == 0) {
@@ -254,7 +253,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                         const double dB = lower_beta();
 #pragma unroll
                         for (int x = 0; x < WMAX; ++x)
-                            if (x < wn) e[x] -= 2.0 * dB * PO * ps[wb + x];
+                            e[x] -= 2.0 * dB * PO * ps[wb + x];
                     }
                 }
             }
@@ -304,7 +303,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                 if (dB != 0.0) {
 #pragma unroll
                     for (int x = 0; x < WMAX; ++x)
-                        if (x < wn) er[x] -= 2.0 * dB * PO * ps[wb + x];
+                        er[x] -= 2.0 * dB * PO * ps[wb + x];
                     // Y for the round's last real step from the rescaled e
                     int tl = t0 + 3;
                     while (wmk[tl] == kPadMask) --tl;
