@@ -242,12 +242,9 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) xr[i] = 0.0;
     lane_columns<T>(d, [&](int c, int slot) { xr[slot] = xq[c]; });
-    for_keys(kh, N, d, [&](int64_t j, int gi, int GL, auto &&walk) {
-        double acc = 0.0;
-        walk([&](int, int slot, float x) { acc = fma(xr[slot], (double)x, acc); });
-        acc = group_sum(acc, GL);
-        if (j >= 0 && gi == 0) zz[j] = scale * acc + (a.bias ? (double)a.bias[j] : 0.0);
-    });
+    for_key_sums(
+        kh, N, d, [&](int, int slot, float x, double acc) { return fma(xr[slot], (double)x, acc); },
+        [&](int64_t j, double acc) { zz[j] = scale * acc + (a.bias ? (double)a.bias[j] : 0.0); });
     __syncthreads();
     double zmax = -INFINITY;
     for (int64_t j = tid; j < N; j += NT) zmax = fmax(zmax, zz[j]);
@@ -317,20 +314,18 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
     // deviations: single-key errors, sigma^2 and D
     double s2 = 0.0, dmax = 0.0;
     lane_columns<T>(d, [&](int c, int slot) { xr[slot] = mu[c]; });
-    for_keys(vh, N, d, [&](int64_t j, int gi, int GL, auto &&walk) {
-        double acc = 0.0;
-        walk([&](int, int slot, float x) {
+    for_key_sums(
+        vh, N, d,
+        [&](int, int slot, float x, double acc) {
             const double t = (double)x - xr[slot];
-            acc = fma(t, t, acc);
-        });
-        acc = group_sum(acc, GL);
-        if (j >= 0 && gi == 0) {
+            return fma(t, t, acc);
+        },
+        [&](int64_t j, double acc) {
             const double p = zz[j];
             ee[j] = p * sqrt(acc);
             s2 = fma(p, acc, s2);
             dmax = fmax(dmax, acc);
-        }
-    });
+        });
     s2 = block_sum(s2, redd);
     dmax = block_reduce(dmax, redd, OpMax());
 

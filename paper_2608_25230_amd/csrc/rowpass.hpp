@@ -112,6 +112,63 @@ __device__ void for_keys(const T *M, int64_t N, int d, F &&f) {
     }
 }
 
+// For every key j of M [N][d]: h(j, s_j) on one lane, with s_j the key's
+// elements folded by acc = term(c, slot, x, acc) from 0 on each lane and
+// summed over the lanes.  Rows of 16 lanes per key (d = 128 in bf16, say)
+// sum the 16 keys a lane has in flight by a transposed reduction: at each
+// of four exchanges a lane gives away half of its partial sums and adds
+// the partner's half of its own, so after 15 shuffles (not 64) lane i of
+// the group holds the whole sum of the group's i-th key.  Other widths
+// reduce every key over its group.
+template <typename T, typename Term, typename H>
+__device__ void for_key_sums(const T *M, int64_t N, int d, Term &&term, H &&h) {
+    constexpr int VEC = RowVec<T>::VEC, U = 16;
+    if (d % VEC == 0 && group_lanes(d, VEC) == U) {
+        const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, NW = blockDim.x >> 6;
+        constexpr int KPW = 64 / U;
+        const int gi = lane % U, gk = lane / U;
+        const bool has = gi < d / VEC;
+        const int64_t stride = (int64_t)NW * KPW;
+        for (int64_t j0 = (int64_t)w * KPW; j0 < N; j0 += stride * U) {
+            uint4 raw[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t j = j0 + u * stride + gk;
+                raw[u] = (j < N && has) ? RowVec<T>::raw(M + j * d, gi * VEC) : make_uint4(0u, 0u, 0u, 0u);
+            }
+            double acc[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                float x[VEC];
+                RowVec<T>::unpack(raw[u], x);
+                double a = 0.0;
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) a = term(gi * VEC + i, i, x[i], a);
+                acc[u] = has ? a : 0.0;
+            }
+#pragma unroll
+            for (int half = U / 2; half > 0; half >>= 1) {
+                const bool upper = (gi & half) != 0;
+#pragma unroll
+                for (int i = 0; i < half; ++i) {
+                    const double give = upper ? acc[i] : acc[i + half];
+                    const double keep = upper ? acc[i + half] : acc[i];
+                    acc[i] = keep + __shfl_xor(give, half);
+                }
+            }
+            const int64_t j = j0 + (int64_t)gi * stride + gk;
+            if (j < N) h(j, acc[0]);
+        }
+    } else {
+        for_keys(M, N, d, [&](int64_t j, int gi, int GL, auto &&walk) {
+            double a = 0.0;
+            walk([&](int c, int slot, float x) { a = term(c, slot, x, a); });
+            a = group_sum(a, GL);
+            if (j >= 0 && gi == 0) h(j, a);
+        });
+    }
+}
+
 // The columns for_keys hands this lane, by slot: fn(c, slot) once per column.
 template <typename T, typename F>
 __device__ void lane_columns(int d, F &&fn) {
@@ -156,15 +213,20 @@ __device__ inline void block_argmax(double &val, int64_t &idx, double *redv, int
 
 __device__ inline double block_sum(double v, double *red) { return block_reduce(v, red, OpSum()); }
 
-// The M (<= 64) largest values of vals[0, N) in the order (value desc,
-// index asc), keys with skip[j] < smin left out (no skip: all keys), their
-// indices into out[0, M).  Each wave takes the next best of its own keys M
-// times (shuffles only, no workgroup barrier), then the waves' lists are
-// merged by counting ranks.  cv, ci: LDS scratch of (blockDim.x / 64) M
-// entries.
-__device__ inline void wave_top(const double *vals, int64_t N, int M, int *out, double *cv, int64_t *ci,
-                                const unsigned char *skip = nullptr, int smin = 0) {
-    const int tid = threadIdx.x, NT = blockDim.x, lane = tid & 63, w = tid >> 6, nw = NT >> 6;
+// Keys per thread that wave_top holds in registers.
+constexpr int kTopRegs = 16;
+
+// (a, ia) ahead of (b, ib) in the order (value desc, index asc); index -1
+// marks no key, behind every key.
+__device__ __forceinline__ bool top_ahead(double a, int ia, double b, int ib) {
+    return ia >= 0 && (ib < 0 || a > b || (a == b && ia < ib));
+}
+
+// wave_top's per-wave picks for rows too long for registers: every pick
+// rescans the thread's keys in LDS for the best one after the last pick.
+__device__ inline void wave_top_scan(const double *vals, int64_t N, int M, double *cv, int64_t *ci,
+                                     const unsigned char *skip, int smin) {
+    const int tid = threadIdx.x, NT = blockDim.x, lane = tid & 63, w = tid >> 6;
     double pv = INFINITY;
     int64_t pi = -1;
     for (int t = 0; t < M; ++t) {
@@ -190,6 +252,84 @@ __device__ inline void wave_top(const double *vals, int64_t N, int M, int *out, 
             pv = bv;
             pi = bi;
         }
+    }
+}
+
+// The M (<= 64) largest values of vals[0, N) in the order (value desc,
+// index asc), keys with skip[j] < smin left out (no skip: all keys), their
+// indices into out[0, M).  Each wave takes the next best of its own keys M
+// times (shuffles only, no workgroup barrier), then the waves' lists are
+// merged by counting ranks.  cv, ci: LDS scratch of (blockDim.x / 64) M
+// entries.
+//
+// Rows of up to kTopRegs keys per thread: each thread sorts its keys in
+// registers once (a bitonic network), so a pick is one wave reduction of
+// the threads' heads and a shift in the thread that held the winner.
+// Longer rows rescan the thread's keys in LDS for every pick.
+__device__ inline void wave_top(const double *vals, int64_t N, int M, int *out, double *cv, int64_t *ci,
+                                const unsigned char *skip = nullptr, int smin = 0) {
+    const int tid = threadIdx.x, NT = blockDim.x, lane = tid & 63, w = tid >> 6, nw = NT >> 6;
+    if (N <= (int64_t)kTopRegs * NT) {
+        double v[kTopRegs];
+        int id[kTopRegs];
+#pragma unroll
+        for (int i = 0; i < kTopRegs; ++i) {
+            const int j = tid + NT * i;
+            v[i] = 0.0;
+            id[i] = -1;
+            if (j < N && !(skip && skip[j] < smin)) {
+                v[i] = vals[j];
+                id[i] = j;
+            }
+        }
+#pragma unroll
+        for (int k = 2; k <= kTopRegs; k <<= 1) {
+#pragma unroll
+            for (int jj = k >> 1; jj > 0; jj >>= 1) {
+#pragma unroll
+                for (int i = 0; i < kTopRegs; ++i) {
+                    const int l = i ^ jj;
+                    if (l > i) {
+                        // blocks with (i & k) == 0 put the better key first
+                        const bool sw = (i & k) == 0 ? top_ahead(v[l], id[l], v[i], id[i])
+                                                     : top_ahead(v[i], id[i], v[l], id[l]);
+                        const double tv = v[i];
+                        const int ti = id[i];
+                        v[i] = sw ? v[l] : tv;
+                        id[i] = sw ? id[l] : ti;
+                        v[l] = sw ? tv : v[l];
+                        id[l] = sw ? ti : id[l];
+                    }
+                }
+            }
+        }
+        for (int t = 0; t < M; ++t) {
+            double bv = v[0];
+            int bi = id[0];
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) {
+                const double ov = __shfl_xor(bv, off);
+                const int oi = __shfl_xor(bi, off);
+                if (top_ahead(ov, oi, bv, bi)) {
+                    bv = ov;
+                    bi = oi;
+                }
+            }
+            if (lane == 0) {
+                cv[w * M + t] = bv;
+                ci[w * M + t] = bi;
+            }
+            if (bi >= 0 && id[0] == bi) {  // keys are distinct: one thread
+#pragma unroll
+                for (int i = 0; i + 1 < kTopRegs; ++i) {
+                    v[i] = v[i + 1];
+                    id[i] = id[i + 1];
+                }
+                id[kTopRegs - 1] = -1;
+            }
+        }
+    } else {
+        wave_top_scan(vals, N, M, cv, ci, skip, smin);
     }
     __syncthreads();
     for (int c = tid; c < nw * M; c += NT) {

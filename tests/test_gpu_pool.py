@@ -139,6 +139,7 @@ def test_example_2_3_pool_on_gpu(torch_fw):
     (2, 5, 33, 8, 6, 0, 2.0, 0.0),      # no extra keys: the pool is A*_s
     (2, 6, 50, 16, 30, 3, 2.5, 4.0),    # few dropped keys: enumeration through the dropped set
     (2, 6, 20, 16, 2, 4, 3.0, 0.0),     # dropped set larger than the kept set, still direct
+    (1, 3, 4500, 16, 6, 10, 2.0, 4.0),  # over 16 keys per thread: the top-key picks rescan LDS
 ])
 def test_small_rows_fp32_all(torch_fw, cfg):
     torch, fw = torch_fw
