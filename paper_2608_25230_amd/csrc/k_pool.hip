@@ -413,72 +413,15 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
                                        : enum_best(B.pl, Gm, ps, seed, B.tab.io, B.tab.wmk, B.tab.jobs, B.tab.omk,
                                                    ent, PLt, redd, redm, ctr);
 
-        // balancing within the pool
-        uint64_t A = seed;
-        int swaps = 0;
-        if (s < P) {
-            // Gram value of the current set, recomputed exactly after every swap
-            auto gram_of = [&](uint64_t M, double &S, double &PA) {
-                double v = 0.0, pm = 0.0;
-                for (int e = tid; e < P * P; e += NT) {
-                    const int i = e / P, j = e % P;
-                    if (((M >> i) & 1ull) && ((M >> j) & 1ull)) v += Gm[e];
-                }
-                for (int i = tid; i < P; i += NT)
-                    if ((M >> i) & 1ull) pm += ps[i];
-                S = block_sum(v, redd);
-                PA = block_sum(pm, redd);
-            };
-            double S, PA;
-            gram_of(A, S, PA);
-            double cur = S / (PA * PA);
-            const int nout = P - s;
-            // ii-th member and jj-th non-member of A, ascending
-            auto pick = [&](int ii, int jj, int &i, int &j) {
-                int ci = 0, cj = 0;
-                i = j = -1;
-                for (int x = 0; x < P; ++x) {
-                    if ((A >> x) & 1ull) { if (ci++ == ii) i = x; }
-                    else if (cj++ == jj) j = x;
-                }
-            };
-            while (swaps < a.max_swaps) {
-                for (int x = tid; x < P; x += NT) {
-                    double c = 0.0;
-                    for (int y = 0; y < P; ++y)
-                        if ((A >> y) & 1ull) c += Gm[x * P + y];
-                    cv[x] = c;
-                }
-                __syncthreads();
-                double bv = 0.0;
-                int64_t bi = -1;
-                for (int t = tid; t < s * nout; t += NT) {
-                    int i, j;
-                    pick(t / nout, t % nout, i, j);
-                    if (i < 0 || j < 0) continue;  // A always holds s of the P keys
-                    const double Sn = S - 2.0 * cv[i] + Gm[i * P + i] + 2.0 * (cv[j] - Gm[i * P + j]) + Gm[j * P + j];
-                    const double Pn = PA - ps[i] + ps[j];
-                    const double val = fmax(Sn, 0.0) / (Pn * Pn);
-                    // argmax of -val; ties to the smallest (out, in) = smallest t
-                    if (bi < 0 || -val > bv) { bv = -val; bi = t; }
-                }
-                block_argmax(bv, bi, redd, redi);
-                if (bi < 0 || !(-bv < cur)) break;
-                int i, j;
-                pick((int)(bi / nout), (int)(bi % nout), i, j);
-                if (i < 0 || j < 0) break;
-                A = (A & ~(1ull << i)) | (1ull << j);
-                ++swaps;
-                gram_of(A, S, PA);
-                cur = S / (PA * PA);
-            }
-        }
-
-        // reported errors: es(M) = ||sum_{i in M} p_i (v_i - mu)|| / p(M)
-        auto es_of = [&](uint64_t M) {
+        // Balancing within the pool on wave 0 alone (P <= 64 keys, one per
+        // lane, no workgroup barrier), while waves 1 and 2 take the reported
+        // errors of A*_s and the ES_pool set.
+        const int lane = tid & 63, w = tid >> 6;
+        // es(M) = ||sum_{i in M} p_i (v_i - mu)|| / p(M), within one wave
+        auto wave_es = [&](uint64_t M) {
             if ((int64_t)__popcll(M) == N) return 0.0;
             double g2 = 0.0;
-            for (int c = tid; c < d; c += NT) {
+            for (int c = lane; c < d; c += 64) {
                 double g = 0.0;
                 for (uint64_t m = M; m; m &= m - 1) {
                     const int i = __ffsll((unsigned long long)m) - 1;
@@ -486,14 +429,72 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
                 }
                 g2 = fma(g, g, g2);
             }
-            g2 = block_sum(g2, redd);
+            g2 = wave_sum(g2);
             double pm = 0.0;
             for (uint64_t m = M; m; m &= m - 1) pm += ps[__ffsll((unsigned long long)m) - 1];
             return sqrt(g2) / pm;
         };
-        const double es_top = es_of(seed);
-        const double es_pool = es_of(best);
-        const double es_bal = es_of(A);
+        uint64_t A = seed;
+        int swaps = 0;
+        double es_bal = 0.0;
+        if (w == 0) {
+            if (s < P) {
+                const int x = lane;
+                const bool inP = x < P;
+                const double px = inP ? ps[x] : 0.0, gxx = inP ? Gm[x * P + x] : 0.0;
+                const int nout = P - s;
+                while (swaps < a.max_swaps) {
+                    // c_x = sum_{y in A} Gm_xy, and the set's Gram value S and
+                    // mass, recomputed from the Gram matrix every round
+                    double cx = 0.0;
+                    if (inP)
+                        for (uint64_t m = A; m; m &= m - 1) cx += Gm[(__ffsll((unsigned long long)m) - 1) * P + x];
+                    const bool mem = inP && ((A >> x) & 1ull);
+                    const double S = wave_sum(mem ? cx : 0.0), PA = wave_sum(mem ? px : 0.0);
+                    const double cur = S / (PA * PA);
+                    // lane j (a non-member) against every member i, ascending;
+                    // pair t = (member rank) nout + (non-member rank)
+                    const bool out = inP && !mem;
+                    double bv = 0.0;
+                    int bii = -1, ii = 0;
+                    for (uint64_t m = A; m; m &= m - 1, ++ii) {
+                        const int i = __ffsll((unsigned long long)m) - 1;
+                        const double ci = lane_value(cx, i), gii = lane_value(gxx, i), pi = lane_value(px, i);
+                        if (out) {
+                            const double Sn = S - 2.0 * ci + gii + 2.0 * (cx - Gm[i * P + x]) + gxx;
+                            const double Pn = PA - pi + px;
+                            const double val = fmax(Sn, 0.0) / (Pn * Pn);
+                            if (bii < 0 || -val > bv) {
+                                bv = -val;
+                                bii = ii;
+                            }
+                        }
+                    }
+                    // argmax of -val over the wave; ties to the smallest t
+                    int bt = bii < 0 ? -1 : bii * nout + (x - __popcll(A & ((1ull << x) - 1ull)));
+#pragma unroll
+                    for (int off = 32; off > 0; off >>= 1) {
+                        const double ov = __shfl_xor(bv, off);
+                        const int ot = __shfl_xor(bt, off);
+                        if (ot >= 0 && (bt < 0 || ov > bv || (ov == bv && ot < bt))) {
+                            bv = ov;
+                            bt = ot;
+                        }
+                    }
+                    if (bt < 0 || !(-bv < cur)) break;
+                    const int i = nth_bit(A, bt / nout);
+                    const int j = nth_bit(~A & (P == 64 ? ~0ull : (1ull << P) - 1ull), bt % nout);
+                    A = (A & ~(1ull << i)) | (1ull << j);
+                    ++swaps;
+                }
+            }
+            es_bal = wave_es(A);
+        } else if (w <= 2) {
+            const double e = wave_es(w == 1 ? seed : best);
+            if (lane == 0) redd[w] = e;
+        }
+        __syncthreads();
+        const double es_top = redd[1], es_pool = redd[2];
         if (tid == 0) {
             int t = 0, u = 0;
             for (int i = 0; i < P; ++i) {

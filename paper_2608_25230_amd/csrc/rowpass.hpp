@@ -213,6 +213,27 @@ __device__ inline void block_argmax(double &val, int64_t &idx, double *redv, int
 
 __device__ inline double block_sum(double v, double *red) { return block_reduce(v, red, OpSum()); }
 
+// Sum over the 64 lanes of a wave, on every lane.
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
+// Lane l's v (l wave-uniform), on every lane.
+__device__ __forceinline__ double lane_value(double v, int l) {
+    const uint64_t b = __double_as_longlong(v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), l);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// Position of the k-th (from 0) set bit of m; m holds more than k bits.
+__device__ __forceinline__ int nth_bit(uint64_t m, int k) {
+    for (; k > 0; --k) m &= m - 1;
+    return __ffsll((unsigned long long)m) - 1;
+}
+
 // Keys per thread that wave_top holds in registers.
 constexpr int kTopRegs = 16;
 
