@@ -54,7 +54,7 @@ __device__ __forceinline__ void stage_rows(const T *src, int n, int d, float *ds
 // reads are coalesced (whole rows); the logits, weights, dense output and
 // Gram are formed from LDS, each sum in a fixed order.
 template <typename T>
-__device__ void instance64(const T *qr, const T *kh, const T *vh, float scale, const float *bias,
+__device__ __forceinline__ void instance64(const T *qr, const T *kh, const T *vh, float scale, const float *bias,
                            int n, int d, float *Vs, double *zs, double *ps, double *mu, double *Gm, int gp) {
     const int tid = threadIdx.x, NT = blockDim.x;
     const int pitch = instance_pitch(d);
@@ -113,42 +113,61 @@ __device__ void instance64(const T *qr, const T *kh, const T *vh, float scale, c
         mu[c] = s;
     }
     __syncthreads();
-    // Gram: 2 x 2 blocks of rows (2A, 2A + 1) x (2B, 2B + 1), A <= B, each on
-    // two adjacent lanes that split the columns (even / odd) and add their
-    // sums; rows past n (odd n) read row n - 1 and are not written
-    const int nb = (n + 1) >> 1, nblk = nb * (nb + 1) / 2;
-    for (int task = tid; task < 2 * ((nblk + 31) / 32) * 32; task += NT) {
-        const int blk = task >> 1, half = task & 1;
+    // Gram: 4 x 4 blocks of rows (4A .. 4A + 3) x (4B .. 4B + 3), A <= B, each
+    // on L adjacent lanes that split the columns (c = part mod L) and add
+    // their sums by a butterfly; rows past n read row n - 1 and are not
+    // written.  Whole waves take part, so every butterfly sees its group.
+    const int nb = (n + 3) >> 2, nblk = nb * (nb + 1) / 2;
+    int lgL = 3;
+    while (lgL > 0 && (nblk << lgL) > NT) --lgL;
+    const int L = 1 << lgL;
+    const int ntask = ((nblk * L + 63) / 64) * 64;
+    for (int task = tid; task < ntask; task += NT) {
+        const int blk = task >> lgL, part = task & (L - 1);
         int A = 0, rem = blk < nblk ? blk : 0;
         while (rem >= nb - A) { rem -= nb - A; ++A; }
         const int B = A + rem;
-        const int i0 = 2 * A, j0 = 2 * B;
-        const int i1 = min(i0 + 1, n - 1), j1 = min(j0 + 1, n - 1);
-        const float *ra0 = Vs + i0 * pitch, *ra1 = Vs + i1 * pitch, *rb0 = Vs + j0 * pitch, *rb1 = Vs + j1 * pitch;
-        double s00 = 0.0, s01 = 0.0, s10 = 0.0, s11 = 0.0;
-        for (int c = half; c < d; c += 2) {
-            const double m = mu[c];
-            const double a0 = (double)ra0[c] - m, a1 = (double)ra1[c] - m;
-            const double b0 = (double)rb0[c] - m, b1 = (double)rb1[c] - m;
-            s00 = fma(a0, b0, s00);
-            s01 = fma(a0, b1, s01);
-            s10 = fma(a1, b0, s10);
-            s11 = fma(a1, b1, s11);
+        const float *ra[4], *rb[4];
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+            ra[x] = Vs + min(4 * A + x, n - 1) * pitch;
+            rb[x] = Vs + min(4 * B + x, n - 1) * pitch;
         }
-        s00 += __shfl_xor(s00, 1);
-        s01 += __shfl_xor(s01, 1);
-        s10 += __shfl_xor(s10, 1);
-        s11 += __shfl_xor(s11, 1);
-        if (blk < nblk && half == 0) {
-            auto put = [&](int i, int j, double sv) {
-                const double g = ps[i] * ps[j] * sv;
-                Gm[i * gp + j] = g;
-                Gm[j * gp + i] = g;
-            };
-            put(i0, j0, s00);
-            if (j0 + 1 < n) put(i0, j0 + 1, s01);
-            if (i0 + 1 < n) put(i0 + 1, j0, s10);
-            if (i0 + 1 < n && j0 + 1 < n) put(i0 + 1, j0 + 1, s11);
+        double sg[4][4];
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+#pragma unroll
+            for (int y = 0; y < 4; ++y) sg[x][y] = 0.0;
+#pragma unroll 1
+        for (int c = part; c < d; c += L) {
+            const double m = mu[c];
+            double va[4], vb[4];
+#pragma unroll
+            for (int x = 0; x < 4; ++x) {
+                va[x] = (double)ra[x][c] - m;
+                vb[x] = (double)rb[x][c] - m;
+            }
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+#pragma unroll
+                for (int y = 0; y < 4; ++y) sg[x][y] = fma(va[x], vb[y], sg[x][y]);
+        }
+        for (int off = 1; off < L; off <<= 1)
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+#pragma unroll
+                for (int y = 0; y < 4; ++y) sg[x][y] += __shfl_xor(sg[x][y], off);
+        if (blk < nblk) {
+            // lane `part` of the group writes entries part, part + L, .. of 16
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int i = 4 * A + e / 4, j = 4 * B + e % 4;
+                if ((e & (L - 1)) == part && i < n && j < n) {
+                    const double g = ps[i] * ps[j] * sg[e / 4][e % 4];
+                    Gm[i * gp + j] = g;
+                    Gm[j * gp + i] = g;
+                }
+            }
         }
     }
     __syncthreads();
