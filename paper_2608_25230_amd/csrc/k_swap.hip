@@ -28,6 +28,7 @@
 // falls back to the full sweep.
 #include "fw_internal.hpp"
 #include "instance64.hpp"
+#include "rowpass.hpp"
 
 namespace fw {
 
@@ -322,7 +323,9 @@ swap_dots_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, SwapState
 
 // The same dots for RB rows of one key/value unit at once (G % RB == 0,
 // d <= 256): each key's values are read once for the RB rows, whose g
-// vectors sit in LDS.  Per row the same float32 sum in column order.
+// vectors sit in LDS.  Per row the same float32 sum in column order.  Rows
+// of whole 16-byte chunks are read a chunk per load (8 bf16 or 4 float
+// values), and g by vector LDS reads of the same columns.
 template <typename T, int RB>
 __global__ void __launch_bounds__(256)
 swap_dots_group_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, SwapState s) {
@@ -355,10 +358,23 @@ swap_dots_group_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, Swa
         float acc[RB];
 #pragma unroll
         for (int rr = 0; rr < RB; ++rr) acc[rr] = 0.f;
-        for (int c = 0; c < d; ++c) {
-            const float x = Elem<T>::load(vh, j * d + c);
+        constexpr int VEC = RowVec<T>::VEC;
+        if (d % VEC == 0) {
+            const T *row = vh + j * d;
+            for (int c0 = 0; c0 < d; c0 += VEC) {
+                float x[VEC];
+                RowVec<T>::unpack(RowVec<T>::raw(row, c0), x);
 #pragma unroll
-            for (int rr = 0; rr < RB; ++rr) acc[rr] = fmaf(x, gs[rr][c], acc[rr]);
+                for (int rr = 0; rr < RB; ++rr)
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) acc[rr] = fmaf(x[i], gs[rr][c0 + i], acc[rr]);
+            }
+        } else {
+            for (int c = 0; c < d; ++c) {
+                const float x = Elem<T>::load(vh, j * d + c);
+#pragma unroll
+                for (int rr = 0; rr < RB; ++rr) acc[rr] = fmaf(x, gs[rr][c], acc[rr]);
+            }
         }
 #pragma unroll
         for (int rr = 0; rr < RB; ++rr) {
