@@ -1114,7 +1114,7 @@ namespace {
 
 constexpr int kSwapJC = 4096;  // keys per workgroup of the bound pass
 constexpr int kSwapBT = 256;   // kept keys (threads) per workgroup of the bound pass
-constexpr int kSwapRB = 16;    // rows of one unit per workgroup of the dots pass
+constexpr int kSwapRB = 32;    // rows of one unit per workgroup of the dots pass
 
 // the MFMA pair sweep: bf16, d = 128, whole 16-key tiles
 bool swap_mfma_ok(const fw_rows &rows) {
