@@ -147,12 +147,15 @@ struct SwapState {
     int64_t *ubp;    // [R]      the pair that gave the upper bound
     int32_t *cnt;    // [R]      surviving pairs
     int32_t *fb;     // [R]      1: survivors overflowed, the full sweep runs
+    int32_t *fbl;    // [R]      the rows whose survivors overflowed, in any order
+    int32_t *fbn;    // [1]      their count (cleared by the init and apply passes)
     int64_t *cand;   // [R][kSwapCand] surviving pairs i n + j
     int32_t *ord;    // [R][k]    kept keys in the bound pass's order (k <= kSwapSort)
     int nblk;
 };
 
 constexpr int kSwapCand = 4096;  // surviving pairs kept per row
+constexpr int kSwapSweepRows = 64;  // rows a fallback sweep takes at a time
 constexpr int kSwapSL = 16;      // keys per slice of the bound pass's whole-slice test (<= 32)
 constexpr int kSwapSort = 2048;  // kept keys ordered for the bound pass
 
@@ -164,6 +167,7 @@ swap_init_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, S
     __shared__ int scan[256];
     const int tid = threadIdx.x, NT = blockDim.x;
     const int64_t r = blockIdx.x, h = r / G;
+    if (s.fbn && r == 0 && tid == 0) *s.fbn = 0;
     const T *vh = v + h * n * d;
     const float m = s.row_m[r], inv_l = 1.0f / s.row_l[r];
     const uint32_t key = s.thr_key[r];
@@ -390,18 +394,35 @@ swap_dots_group_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, Swa
     }
 }
 
+// The rows a sweep workgroup takes: blockIdx.y over every active row, or,
+// under the pruned search, the listed rows whose survivors overflowed,
+// gridDim.y of them at a time (so that a sweep with no such row costs a
+// small grid, not one workgroup per tile of every row).
+template <typename F>
+__device__ __forceinline__ void sweep_rows(const SwapState &s, F &&body) {
+    if (!s.fbl) {
+        const int64_t r = blockIdx.y;
+        if (s.st[r * 2]) body(r);
+        return;
+    }
+    const int nfb = *s.fbn;
+    for (int yy = blockIdx.y; yy < nfb; yy += gridDim.y) {
+        const int64_t r = s.fbl[yy];
+        if (s.st[r * 2]) body(r);
+        __syncthreads();  // LDS is reused by the next row
+    }
+}
+
 // every (kept i, dropped j) pair of a tile: 32 kept x 128 keys per workgroup
 template <typename T>
-__global__ void __launch_bounds__(256)
-swap_pairs_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, SwapState s) {
+__device__ __forceinline__ void pairs_row(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk,
+                                          const SwapState &s, int64_t r) {
     constexpr int TI = 32, TJ = 128, TD = 32;
     __shared__ float Vi[TI][TD + 1];
     __shared__ float Vj[TJ][TD + 1];
     __shared__ int idx_i[TI];
     __shared__ float redv[256];
     __shared__ int64_t redp[256];
-    const int64_t r = blockIdx.y;
-    if (!s.st[r * 2] || (s.fb && !s.fb[r])) return;
     const int tid = threadIdx.x;
     const int64_t h = r / G;
     const T *vh = v + h * n * d;
@@ -481,6 +502,12 @@ swap_pairs_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, 
     }
 }
 
+template <typename T>
+__global__ void __launch_bounds__(256)
+swap_pairs_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, SwapState s) {
+    sweep_rows(s, [&](int64_t r) { pairs_row<T>(v, G, n, d, kk, s, r); });
+}
+
 // ---------------------------------------------------------------------------
 // every (kept i, key j) pair on MFMA: bf16 rows, d = 128, n a multiple of 16.
 // A workgroup (8 waves) takes 512 consecutive kept keys of one row -- each
@@ -513,15 +540,13 @@ __device__ __forceinline__ void sp_wait_vm(int n) {
 #undef SP_VM
 }  // namespace
 
-__global__ void __launch_bounds__(512)
-swap_pairs_mfma_kernel(const uint16_t *__restrict__ v, int64_t G, int64_t n, int kk, SwapState s) {
+__device__ __forceinline__ void pairs_mfma_row(const uint16_t *__restrict__ v, int64_t G, int64_t n, int kk,
+                                               const SwapState &s, int64_t r) {
     extern __shared__ __align__(16) unsigned char smem[];
     unsigned char *vbuf = smem;                                   // [2][SP_STAGE]
     float4 *jbuf = (float4 *)(smem + 2 * SP_STAGE);               // [2][SPT * 16]
     float *redv = (float *)(smem + 2 * SP_STAGE + 2 * SPT * 16 * 16);  // [8]
     int64_t *redp = (int64_t *)(redv + 8);                        // [8]
-    const int64_t r = blockIdx.y;
-    if (!s.st[r * 2] || (s.fb && !s.fb[r])) return;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, rl = lane & 15, grp = lane >> 4;
     const int64_t nchunk = (n + SPJ - 1) / SPJ;
     const int ib = (int)(blockIdx.x / nchunk);
@@ -662,6 +687,11 @@ swap_pairs_mfma_kernel(const uint16_t *__restrict__ v, int64_t G, int64_t n, int
         s.pv[r * s.nblk + blockIdx.x] = lv;
         s.pp[r * s.nblk + blockIdx.x] = lp;
     }
+}
+
+__global__ void __launch_bounds__(512)
+swap_pairs_mfma_kernel(const uint16_t *__restrict__ v, int64_t G, int64_t n, int kk, SwapState s) {
+    sweep_rows(s, [&](int64_t r) { pairs_mfma_row(v, G, n, kk, s, r); });
 }
 
 // (value, index) minimum over the workgroup, ties to the smaller index
@@ -971,7 +1001,10 @@ swap_cand_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, SwapState
     const int tid = threadIdx.x, NT = blockDim.x;
     const int cnt = s.cnt[r];
     if (cnt > kSwapCand) {  // overflow: the full sweep decides this row
-        if (tid == 0) s.fb[r] = 1;
+        if (tid == 0) {
+            s.fb[r] = 1;
+            s.fbl[atomicAdd(s.fbn, 1)] = (int32_t)r;
+        }
         return;
     }
     if (tid == 0) s.fb[r] = 0;
@@ -1011,6 +1044,7 @@ swap_apply_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, 
     __shared__ double redd[256];
     __shared__ int decide;
     const int64_t r = blockIdx.x;
+    if (s.fbn && r == 0 && threadIdx.x == 0) *s.fbn = 0;  // the sweep that read it is done
     if (!s.st[r * 2]) return;
     const int tid = threadIdx.x;
     float bv = INFINITY;
@@ -1177,6 +1211,8 @@ SwapLayout swap_layout(const fw_rows &rows, int k, void *ws) {
         L.s.ubp = (int64_t *)take(R * 8);
         L.s.cnt = (int32_t *)take(R * 4);
         L.s.fb = (int32_t *)take(R * 4);
+        L.s.fbl = (int32_t *)take(R * 4);
+        L.s.fbn = (int32_t *)take(16);
         L.s.cand = (int64_t *)take(R * (size_t)kSwapCand * 8);
         if (k <= kSwapSort) L.s.ord = (int32_t *)take(R * (size_t)k * 4);
     }
@@ -1232,12 +1268,14 @@ static hipError_t swap_large(const fw_rows &rows, int k, int max_iters, int32_t 
                                dim3(kSwapBT), 0, st, n, k, L.s);
             hipLaunchKernelGGL(swap_cand_kernel<T>, dim3((unsigned)R), dim3(256), 0, st, v, G, n, d, L.s);
         }
+        // under the pruned search the sweep takes only the listed rows
+        const unsigned sweep_y = L.s.fbl ? (unsigned)(R < kSwapSweepRows ? R : kSwapSweepRows) : (unsigned)R;
         if (swap_mfma_ok(rows))
-            hipLaunchKernelGGL(swap_pairs_mfma_kernel, dim3((unsigned)L.s.nblk, (unsigned)R), dim3(512),
+            hipLaunchKernelGGL(swap_pairs_mfma_kernel, dim3((unsigned)L.s.nblk, sweep_y), dim3(512),
                                (size_t)(2 * SP_STAGE + 2 * SPT * 16 * 16 + 8 * 4 + 8 * 8), st,
                                (const uint16_t *)rows.v, G, n, k, L.s);
         else
-            hipLaunchKernelGGL(swap_pairs_kernel<T>, dim3((unsigned)L.s.nblk, (unsigned)R), dim3(256), 0,
+            hipLaunchKernelGGL(swap_pairs_kernel<T>, dim3((unsigned)L.s.nblk, sweep_y), dim3(256), 0,
                                st, v, G, n, d, k, L.s);
         hipLaunchKernelGGL(swap_apply_kernel<T>, dim3((unsigned)R), dim3(256), 0, st, v, G, n, d, k,
                            L.s, gap_traj, T_len);
