@@ -82,45 +82,48 @@ __host__ __device__ inline SubsetLds subset_lds(int n, int d, int k, int nent, i
 // leaving at step t relative to the range -- as masks of the walked part
 // (absolute key positions), and the job list, longest jobs first.
 __global__ void enum_plan_kernel(EnumPlan p, uint2 *io, uint64_t *wmk, EnumJob *jobs) {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    if (blockIdx.x != 0) return;
     int c[kMaxWalk + 2];
-    for (int q = 0; q < p.ncls; ++q) {
+    // one lane per class (the tables are independent)
+    if (const int q = threadIdx.x; q < p.ncls) {
         const EnumClass &C = p.cls[q];
         bool first = true;  // tables are shared by classes with the same walk
         for (int q2 = 0; q2 < q; ++q2)
             if (p.cls[q2].toff == C.toff) first = false;
-        if (!first) continue;
-        int t = C.toff;
-        uint32_t rel = C.ws == 0 ? 0u : ((1u << C.ws) - 1u);
-        io[t] = make_uint2(0u, 0u);
-        wmk[t] = (uint64_t)rel << C.wb;
-        if (C.ws <= kColexMax) {
-            // colex order: Gosper's successor (the next larger integer with
-            // the same number of bits)
-            const int cnt = (int)binom(C.wn, C.ws);
-            for (int q = 1; q < cnt; ++q) {
-                const uint32_t low = rel & (~rel + 1u), r = rel + low;
-                rel = (((r ^ rel) >> 2) / low) | r;
-                ++t;
-                io[t] = make_uint2(0u, 0u);
-                wmk[t] = (uint64_t)rel << C.wb;
-            }
-        } else if (C.ws > 0 && C.ws < C.wn) {
-            revdoor_init(c, C.ws, C.wn);
-            int in, out;
-            while (revdoor_next(c, C.ws, &in, &out)) {
-                ++t;
-                rel ^= (1u << in) ^ (1u << out);
-                io[t] = make_uint2((uint32_t)in, (uint32_t)out);
-                wmk[t] = (uint64_t)rel << C.wb;
-            }
-        }
-        const int end = C.toff + (int)pad4(binom(C.wn, C.ws));
-        for (++t; t < end; ++t) {  // neutral steps: no key moves, never a candidate
+        if (first) {
+            int t = C.toff;
+            uint32_t rel = C.ws == 0 ? 0u : ((1u << C.ws) - 1u);
             io[t] = make_uint2(0u, 0u);
-            wmk[t] = kPadMask;
+            wmk[t] = (uint64_t)rel << C.wb;
+            if (C.ws <= kColexMax) {
+                // colex order: Gosper's successor (the next larger integer with
+                // the same number of bits)
+                const int cnt = (int)binom(C.wn, C.ws);
+                for (int e = 1; e < cnt; ++e) {
+                    const uint32_t low = rel & (~rel + 1u), r = rel + low;
+                    rel = (((r ^ rel) >> 2) >> (__ffs(low) - 1)) | r;
+                    ++t;
+                    io[t] = make_uint2(0u, 0u);
+                    wmk[t] = (uint64_t)rel << C.wb;
+                }
+            } else if (C.ws > 0 && C.ws < C.wn) {
+                revdoor_init(c, C.ws, C.wn);
+                int in, out;
+                while (revdoor_next(c, C.ws, &in, &out)) {
+                    ++t;
+                    rel ^= (1u << in) ^ (1u << out);
+                    io[t] = make_uint2((uint32_t)in, (uint32_t)out);
+                    wmk[t] = (uint64_t)rel << C.wb;
+                }
+            }
+            const int end = C.toff + (int)pad4(binom(C.wn, C.ws));
+            for (++t; t < end; ++t) {  // neutral steps: no key moves, never a candidate
+                io[t] = make_uint2(0u, 0u);
+                wmk[t] = kPadMask;
+            }
         }
     }
+    if (threadIdx.x != 0) return;
     // jobs: classes in order of decreasing job cost
     int nj = 0;
     bool done[kMaxClass];
