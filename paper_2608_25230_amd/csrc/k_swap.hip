@@ -750,8 +750,12 @@ swap_ub_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, Swa
     // eight smallest B_j and A_i: each thread keeps its own eight (value,
     // index ascending) in one pass, then eight rounds over the threads' lists
     // in LDS pick the workgroup's, each after the previous (value, index)
-    __shared__ double lv[256 * 8];
-    __shared__ int64_t li[256 * 8];
+    // one buffer for the threads' eight-entry lists and, once those are
+    // merged, the kept keys' sort (four workgroups per CU fit)
+    __shared__ __align__(16) unsigned char ubuf[256 * 8 * 16];
+    static_assert(kSwapSort * 8 <= 256 * 8 * 16, "sort keys fit the list buffer");
+    double *lv = (double *)ubuf;
+    int64_t *li = (int64_t *)(ubuf + 256 * 8 * 8);
     auto top8 = [&](auto &&get, int64_t cnt, int64_t *dst) __attribute__((always_inline)) {
         double tv[8];
         int64_t ti[8];
@@ -842,8 +846,8 @@ swap_ub_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, Swa
     sp = block_reduce(sp, redv, OpSum());
     nd = block_reduce(nd, redv, OpSum());
     const double rt = 4.0 * sr / fmax(nd, 1.0), pt = 4.0 * sp / fmax(nd, 1.0);
-    __shared__ float skey[kSwapSort];
-    __shared__ int32_t sval[kSwapSort];
+    float *skey = (float *)ubuf;  // the lists are dead: their merges ended with a barrier
+    int32_t *sval = (int32_t *)(ubuf + kSwapSort * 4);
     int np2 = 1;
     while (np2 < kk) np2 <<= 1;
     for (int t = tid; t < np2; t += NT) {
