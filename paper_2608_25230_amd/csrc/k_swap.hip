@@ -159,6 +159,18 @@ constexpr int kSwapSweepRows = 64;  // rows a fallback sweep takes at a time
 constexpr int kSwapSL = 16;      // keys per slice of the bound pass's whole-slice test (<= 32)
 constexpr int kSwapSort = 2048;  // kept keys ordered for the bound pass
 
+// Elements [c0, c0 + 8) of a row of d (those below d), as floats: one
+// 16-byte load for bf16 rows with d a multiple of 8, else one load each.
+template <typename T>
+__device__ __forceinline__ void load8(const T *row, int c0, int d, float (&x)[8]) {
+    if (sizeof(T) == 2 && d % 8 == 0) {
+        RowVec<uint16_t>::unpack(RowVec<uint16_t>::raw((const uint16_t *)row, c0), x);
+        return;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = c0 + e < d ? Elem<T>::load(row, c0 + e) : 0.f;
+}
+
 template <typename T>
 __global__ void __launch_bounds__(256)
 swap_init_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, SwapState s,
@@ -204,9 +216,11 @@ swap_init_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, S
             for (int x = 0; x < 8; ++x) acc[x] = 0.0;
             for (int64_t j = jl; j < n; j += 16) {
                 const double pj = (double)p[j];
+                float xv[8];
+                load8(vh + j * d, c0, d, xv);
 #pragma unroll
                 for (int x = 0; x < 8; ++x)
-                    if (c0 + x < d) acc[x] = fma(pj, (double)Elem<T>::load(vh, j * d + c0 + x), acc[x]);
+                    if (c0 + x < d) acc[x] = fma(pj, (double)xv[x], acc[x]);
             }
 #pragma unroll
             for (int x = 0; x < 8; ++x) {
@@ -259,9 +273,11 @@ swap_init_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, S
             for (int i = kl; i < kk; i += 16) {
                 const int64_t a = s.Sl[r * kk + i];
                 const double pa = (double)p[a];
+                float xv[8];
+                load8(vh + a * d, c0, d, xv);
 #pragma unroll
                 for (int x = 0; x < 8; ++x)
-                    if (c0 + x < d) acc[x] = fma(pa, (double)Elem<T>::load(vh, a * d + c0 + x) - mu[c0 + x], acc[x]);
+                    if (c0 + x < d) acc[x] = fma(pa, (double)xv[x] - mu[c0 + x], acc[x]);
             }
 #pragma unroll
             for (int x = 0; x < 8; ++x) {
