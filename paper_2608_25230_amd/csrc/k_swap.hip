@@ -237,19 +237,34 @@ swap_init_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, S
     __syncthreads();
     double mu2 = 0.0;
     for (int cc = 0; cc < d; ++cc) mu2 += mu[cc] * mu[cc];
-    // w_j = v_j . mu and ||u_j||^2 = p_j^2 ||v_j - mu||^2: 16 lanes per key
-    // (columns lane, lane + 16, ...: coalesced), partial sums by a butterfly
+    // w_j = v_j . mu and ||u_j||^2 = p_j^2 ||v_j - mu||^2: 16 lanes per key,
+    // partial sums by a butterfly.  bf16 rows with d a multiple of 8: lane l
+    // takes the 8-column chunks l, l + 16, .. (a 16-byte load each); other
+    // rows: columns lane, lane + 16, ...
     {
         const int jl = tid >> 4, cl = tid & 15;
+        const bool chunks = sizeof(T) == 2 && d % 8 == 0;
         for (int64_t j0 = 0; j0 < n; j0 += NT / 16) {
             const int64_t j = j0 + jl;
             double dw = 0.0, du = 0.0;
-            if (j < n)
+            if (j < n && chunks) {
+                for (int c0 = 8 * cl; c0 < d; c0 += 128) {
+                    float xv[8];
+                    load8(vh + j * d, c0, d, xv);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const double x = (double)xv[e], m = mu[c0 + e];
+                        dw = fma(x, m, dw);
+                        du = fma(x - m, x - m, du);
+                    }
+                }
+            } else if (j < n) {
                 for (int cc = cl; cc < d; cc += 16) {
                     const double x = (double)Elem<T>::load(vh, j * d + cc), m = mu[cc];
                     dw = fma(x, m, dw);
                     du = fma(x - m, x - m, du);
                 }
+            }
 #pragma unroll
             for (int off = 1; off < 16; off <<= 1) {
                 dw += __shfl_xor(dw, off);
