@@ -400,18 +400,24 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
         const float m1 = opaque(bmw), w1 = opaque(bnw);
 #pragma unroll
         for (int t = 0; t < TILES; ++t) {
+            // the tile's four logits tested together: one branch per tile
+            int bin[4], hit[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int bin = min(FBINS - 1, (int)fmaf(S[t][i], w1, m1));
-                int hit = 0;
+                bin[i] = min(FBINS - 1, (int)fmaf(S[t][i], w1, m1));
+                hit[i] = 0;
 #pragma unroll
-                for (int kk = 0; kk < NK; ++kk) hit |= (int)(bin == tb[kk]);
-                if (hit) {
+                for (int kk = 0; kk < NK; ++kk) hit[i] |= (int)(bin[i] == tb[kk]);
+            }
+            if (hit[0] | hit[1] | hit[2] | hit[3]) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    if (!hit[i]) continue;
                     const uint32_t j = (uint32_t)(kw0 + 16 * tk(t) + 4 * grp + i);
                     const unsigned long long e = ((unsigned long long)ord_key(S[t][i]) << 32) | (0xFFFFFFFFu - j);
 #pragma unroll
                     for (int kk = 0; kk < NK; ++kk)
-                        if (bin == tb[kk]) {
+                        if (bin[i] == tb[kk]) {
                             const int p = atomicAdd(&cntr[rl * 8 + kk], 1);
                             if (p < FCAP) lists[(rl * NK + kk) * FCAP + p] = e;
                         }
