@@ -140,6 +140,7 @@ def test_example_2_3_pool_on_gpu(torch_fw):
     (2, 6, 50, 16, 30, 3, 2.5, 4.0),    # few dropped keys: enumeration through the dropped set
     (2, 6, 20, 16, 2, 4, 3.0, 0.0),     # dropped set larger than the kept set, still direct
     (1, 3, 4500, 16, 6, 10, 2.0, 4.0),  # over 16 keys per thread: the top-key picks rescan LDS
+    (1, 3, 100, 16, 62, 2, 2.0, 0.0),   # a pool of 64 keys: the full mask, one balancing lane per key
 ])
 def test_small_rows_fp32_all(torch_fw, cfg):
     torch, fw = torch_fw
