@@ -84,6 +84,8 @@ def test_tiny_rows_all(torch_fw):
     dict(kv_heads=2, q_per_kv=2, rows_per_q=4, n=1024, d=128, k=100, max_iters=12),
     dict(kv_heads=1, q_per_kv=2, rows_per_q=3, n=2064, d=128, k=600, max_iters=8),
     dict(kv_heads=1, q_per_kv=1, rows_per_q=4, n=4096, d=128, k=1030, max_iters=6),
+    # d not a multiple of 8: the element-wise loads beside the 16-byte chunks
+    dict(kv_heads=1, q_per_kv=2, rows_per_q=2, n=300, d=20, k=30, max_iters=6),
 ])
 def test_long_rows_bf16(torch_fw, shape):
     torch, fw = torch_fw
