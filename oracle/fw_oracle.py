@@ -27,9 +27,13 @@ Readings where the paper is silent (each also listed in the design notes):
   * the ContourKV budget counts the recency floor, is exact (ties at the
     threshold broken by (cell, position) ascending) and has no per-cell cap.
 
-Parity status: every function here is pinned by the not-gpu tests (worked
-examples of the paper, closed forms, identities, brute force, permutation
-invariance, the hardness family in exact rationals); none is "parity unpinned".
+Parity status: every function here is pinned by the not-gpu tests against
+something other than itself: worked examples of the paper and constructed
+instances in exact rationals (tests/golden/), closed forms, Lemma 2.2's
+identities, brute force over all subsets, permutation invariance and the
+hardness family.  Each pin was checked by planting plausible mistakes in a
+copy of this module (tests/test_oracle_mutations.py); no function is
+"parity unpinned".
 """
 from __future__ import annotations
 
@@ -123,9 +127,8 @@ def row_dense_topk(z: np.ndarray, V: np.ndarray, ks: Sequence[int]) -> Dict[str,
     o_s, gap, drop = [], [], []
     for k in ks:
         S = top[:k]
-        oS = forced_output(p, V, S)
-        o_s.append(oS)
-        gap.append(float(np.linalg.norm(oS - o)))
+        o_s.append(forced_output(p, V, S))
+        gap.append(forced_error(p, V, S))
         drop.append(dropped_mass(p, S))
     return dict(p=p, o=o, o_s=np.array(o_s), gap=np.array(gap), dropped=np.array(drop),
                 topk_idx=top)

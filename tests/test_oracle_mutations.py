@@ -2,7 +2,9 @@
 
 Each mutant replaces one oracle function with a plausible error (dropped
 renormalisation, wrong tie direction, wrong sign, argmax for argmin, prefix in
-place of suffix, ...) and runs the pins that should catch it.
+place of suffix, Phi reported for es, one budget's set used for every budget,
+an inverted ratio, a non-strict stopping rule, ...) and runs the pins that
+should catch it.
 """
 import numpy as np
 import pytest
@@ -44,6 +46,9 @@ def _run_all_pins():
     checks += [(P.test_allocation_with_cap, s) for s in range(3)]
     checks += [(P.test_allocation_uniform_cap_is_per_cell_top,)]
     checks += [(P.test_maxpool_scores, k) for k in (1, 3, 7)]
+    checks += [(P.test_row_dense_topk_example_2_3,), (P.test_row_best_subset_example_2_3,),
+               (P.test_balancing_stops_at_a_local_optimum,), (P.test_swap_rule_stops_on_a_tie,)]
+    checks += [(P.test_row_dense_topk_per_budget_first_form, s) for s in range(4)]
     return any(_fails(*c) for c in checks)
 
 
@@ -184,6 +189,62 @@ def _maxpool_one_sided(r, kernel):
 
 
 _ORIG_ALLOC = O.allocate
+_ORIG_ROW_DENSE = O.row_dense_topk
+_ORIG_ROW_BEST = O.row_best_subset
+_ORIG_ROW_POOL = O.row_pool
+
+
+def _dense_gap_times_kept_mass(z, V, ks):
+    # reports Phi = p(S) es(S) instead of es(S)
+    r = _ORIG_ROW_DENSE(z, V, ks)
+    r["gap"] = r["gap"] * (1.0 - r["dropped"])
+    return r
+
+
+def _dense_kmax_set_for_every_budget(z, V, ks):
+    # evaluates every budget on the largest budget's set
+    r = _ORIG_ROW_DENSE(z, V, ks)
+    i = int(np.argmax(ks))
+    for t in range(len(ks)):
+        r["o_s"][t], r["gap"][t], r["dropped"][t] = r["o_s"][i], r["gap"][i], r["dropped"][i]
+    return r
+
+
+def _best_dropped_is_kept(z, V, k):
+    r = _ORIG_ROW_BEST(z, V, k)
+    r["dropped_topk"] = 1.0 - r["dropped_topk"]
+    return r
+
+
+def _pool_kappa_bal_inverted(z, V, s, extra, max_iters):
+    r = _ORIG_ROW_POOL(z, V, s, extra, max_iters)
+    r["kappa_bal"] = O.ratio(r["es_pool"], r["es_bal"])
+    return r
+
+
+def _swap_non_strict(p, V, k, max_iters, start=None, method="auto"):
+    # accepts a swap that only ties the current error
+    p = np.asarray(p, np.float64)
+    V = np.asarray(V, np.float64)
+    if start is None:
+        start = O.top_mass_set(np.log(p), k)
+    S = np.sort(np.asarray(start, np.int64))
+    search = O._best_swap_direct if (method == "direct" or (method == "auto" and p.size <= 32)) else O._best_swap_gform
+    traj = np.full(max_iters + 1, np.nan)
+    cur = O.forced_error(p, V, S)
+    traj[0] = cur
+    it = 0
+    if k == 0 or k == p.size:
+        return S, traj, 0
+    while it < max_iters:
+        es_new, i, j = search(p, V, S)
+        if not es_new <= cur:
+            break
+        S = np.sort(np.concatenate([S[S != i], [j]]))
+        it += 1
+        cur = O.forced_error(p, V, S)
+        traj[it] = cur
+    return S, traj, it
 
 MUTANTS = {
     "group_vote_by_max_mass": ("group_vote", _vote_by_max),
@@ -204,6 +265,11 @@ MUTANTS = {
     "logits_drop_bias": ("logits", _no_bias_logits),
     "gap_extra_term": ("forced_error", _gap_transposed),
     "allocation_ties_high": ("allocate", _alloc_ties_high),
+    "dense_topk_gap_times_kept_mass": ("row_dense_topk", _dense_gap_times_kept_mass),
+    "dense_topk_kmax_set_for_every_budget": ("row_dense_topk", _dense_kmax_set_for_every_budget),
+    "best_subset_dropped_is_kept": ("row_best_subset", _best_dropped_is_kept),
+    "pool_kappa_bal_inverted": ("row_pool", _pool_kappa_bal_inverted),
+    "swap_rule_non_strict_stop": ("swap_rule", _swap_non_strict),
 }
 
 

@@ -101,6 +101,95 @@ def test_example_A3_not_submodular_statements():
     assert es([1, 3]) == 0.5 and es([0, 1, 3]) == pytest.approx(1 / 6, rel=1e-14)
 
 
+def test_row_dense_topk_example_2_3():
+    """Example 2.3 through the batched top-k evaluator, budgets given out of
+    order: mu = 1/2; the top-1 set is {0} (keys 0 and 1 tie in mass, the lower
+    index wins), m = -1, gap 3/2, dropped 11/20; the top-2 set {0,1} has m = 0,
+    gap 1/2 (the example's value), dropped 1/10; keeping all three keys gives
+    m = mu, gap 0, dropped 0."""
+    g = _golden("example_2_3.json")
+    v = np.array(g["v"], float)[:, None]
+    p = np.array([float(Fraction(x)) for x in g["p"]])
+    r = O.row_dense_topk(np.log(p), v, (3, 1, 2))
+    assert r["o"][0] == pytest.approx(0.5, rel=1e-14)
+    assert r["topk_idx"].tolist() == [0, 1, 2]
+    np.testing.assert_allclose(r["o_s"][:, 0], [0.5, -1.0, 0.0], rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(r["gap"], [0.0, 1.5, float(Fraction(g["es"]["0,1"]))], rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(r["dropped"], [0.0, 0.55, 0.1], rtol=1e-13, atol=1e-15)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_row_dense_topk_per_budget_first_form(seed):
+    """Every budget's forced output, gap and dropped mass come from that
+    budget's own top-mass set: checked against plain loops over the set
+    ranked by (logit desc, index asc) and against Lemma 2.2's first form
+    es(S) = (1 - p(S)) ||m_{S^c} - m_S||."""
+    rng = np.random.default_rng(1200 + seed)
+    n, d = 17, 4
+    z = np.round(rng.standard_normal(n) * 2.0, 1)  # rounding creates logit ties
+    V = rng.standard_normal((n, d))
+    ks = (11, 3, 7, n)
+    r = O.row_dense_topk(z, V, ks)
+    e = [math.exp(z[j] - max(z)) for j in range(n)]
+    p = [x / sum(e) for x in e]
+    order = sorted(range(n), key=lambda j: (-z[j], j))
+    assert r["topk_idx"].tolist() == order[: max(ks)]
+    for t, k in enumerate(ks):
+        S, Sc = order[:k], order[k:]
+        pS = sum(p[j] for j in S)
+        mS = [sum(p[j] * V[j][c] for j in S) / pS for c in range(d)]
+        np.testing.assert_allclose(r["o_s"][t], mS, rtol=1e-12, atol=1e-14)
+        assert r["dropped"][t] == pytest.approx(sum(p[j] for j in Sc), rel=1e-12, abs=1e-15)
+        if not Sc:
+            assert r["gap"][t] == 0.0
+            continue
+        pSc = sum(p[j] for j in Sc)
+        mSc = [sum(p[j] * V[j][c] for j in Sc) / pSc for c in range(d)]
+        first = (1.0 - pS) * math.sqrt(sum((mSc[c] - mS[c]) ** 2 for c in range(d)))
+        assert r["gap"][t] == pytest.approx(first, rel=1e-10)
+
+
+def test_row_best_subset_example_2_3():
+    """Example 2.3 through the per-row exhaustive evaluator: best set {0,2}
+    (the paper's {1,3}) at 9/22, top-mass set {0,1} at 1/2, closed fraction
+    2/11, and the top-mass set drops mass 1/10."""
+    g = _golden("example_2_3.json")
+    v = np.array(g["v"], float)[:, None]
+    p = np.array([float(Fraction(x)) for x in g["p"]])
+    r = O.row_best_subset(np.log(p), v, g["k"])
+    assert r["best_idx"].tolist() == g["best_set"]
+    assert r["topk_idx"].tolist() == g["top_mass_set"]
+    assert r["best_gap"] == pytest.approx(float(Fraction(g["ES"])), rel=1e-14)
+    assert r["topk_gap"] == pytest.approx(float(Fraction(g["es"]["0,1"])), rel=1e-14)
+    assert r["closed"] == pytest.approx(float(Fraction(g["closed_fraction"])), rel=1e-13)
+    assert r["dropped_topk"] == pytest.approx(0.1, rel=1e-13)
+
+
+def test_balancing_stops_at_a_local_optimum():
+    """A row on which the balancing selector stops above the candidate-set
+    optimum (exact rationals in the fixture): no swap improves A*_s, so it
+    returns A*_s with zero swaps, while ES_pool is lower; kappa_bal =
+    es(A_bal) / ES_pool = 22/7, and never below 1."""
+    g = _golden("balancing_local_optimum.json")
+    F = lambda x: float(Fraction(x))
+    v = np.array(g["v"], float)[:, None]
+    p = np.array([F(x) for x in g["p"]])
+    for key, val in g["swap_es"].items():
+        assert O.forced_error(p, v, [int(x) for x in key.split(",")]) == pytest.approx(F(val), rel=1e-13)
+    r = O.row_pool(np.log(p), v, g["s"], g["extra"], max_iters=8)
+    assert r["top"].tolist() == g["top"]
+    assert r["bal_idx"].tolist() == g["bal_set"] and r["n_swaps"] == g["n_swaps"]
+    assert r["best_idx"].tolist() == g["best_set"]
+    assert r["es_top"] == pytest.approx(F(g["es_top"]), rel=1e-13)
+    assert r["es_bal"] == pytest.approx(F(g["es_top"]), rel=1e-13)
+    assert r["es_pool"] == pytest.approx(F(g["ES_pool"]), rel=1e-12)
+    assert r["kappa_hat"] == pytest.approx(F(g["kappa_hat"]), rel=1e-12)
+    assert r["kappa_bal"] == pytest.approx(F(g["kappa_bal"]), rel=1e-12)
+    assert r["c_hat"] == pytest.approx(F(g["c_hat"]), rel=1e-12)
+    S, traj, ns = O.swap_rule(p, v, g["s"], 8, method="direct")
+    assert S.tolist() == sorted(g["bal_set"]) and ns == 0
+
+
 # ---------------------------------------------------------------------------
 # Hardness construction (Appendix A.2) in exact rationals
 # ---------------------------------------------------------------------------
@@ -152,6 +241,23 @@ def test_hardness_all_pairs_tie():
     assert best.tolist() == [0, 1] and ES == 0.75
     best, ES = O.best_subset(p, np.array([1, 2, 3, 4.0])[:, None], 2)
     assert best.tolist() == [0, 3] and ES == 0.0
+
+
+def test_swap_rule_stops_on_a_tie():
+    """The balancing selector stops when no swap strictly decreases es
+    (Section 2.1).  On the hardness instance w = (1,1,1,4) with uniform
+    masses every pair has es = 3/4 exactly, so every swap ties the current
+    set: no swap is taken, the trajectory is [3/4] and the set stays the
+    top-mass set {0,1}; the same holds inside a candidate set of every key."""
+    p = np.full(4, 0.25)
+    v = np.array([1, 1, 1, 4.0])[:, None]
+    for method in ("direct", "gform"):
+        S, traj, ns = O.swap_rule(p, v, 2, 6, method=method)
+        assert ns == 0 and S.tolist() == [0, 1]
+        assert traj[0] == 0.75 and np.all(np.isnan(traj[1:]))
+    r = O.row_pool(np.log(p), v, 2, 2, max_iters=6)
+    assert r["n_swaps"] == 0 and r["bal_idx"].tolist() == [0, 1]
+    assert r["kappa_bal"] == 1.0 and r["kappa_hat"] == 1.0
 
 
 # ---------------------------------------------------------------------------
