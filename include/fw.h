@@ -12,9 +12,10 @@
  * Conventions shared by every entry point
  *   - All array pointers are DEVICE pointers to contiguous row-major buffers
  *     unless marked "host".  The caller owns every buffer; the library keeps
- *     no pointer after a call returns and allocates no device memory: scratch
- *     space is the caller's workspace, sized by the matching
- *     fw_*_workspace_size() query (which returns 0 for invalid arguments).
+ *     no pointer after a call returns and no call allocates device memory:
+ *     scratch space is the caller's workspace, sized by the matching
+ *     fw_*_workspace_size() query (which returns 0 for invalid arguments),
+ *     or, for fw_dense_topk_noalloc, a static per-device array.
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = the default
  *     stream).  No call synchronises the device or copies device data to the
  *     host; results are valid once the stream reaches them.
@@ -100,6 +101,29 @@ size_t fw_dense_topk_workspace_size(const fw_rows *rows, const int32_t *ks, int3
 fw_status fw_dense_topk(const fw_rows *rows, const int32_t *ks, int32_t n_ks,
                         float *o, float *o_s, float *gap, float *dropped,
                         int32_t *topk_idx, void *ws, size_t ws_bytes, fw_stream stream);
+
+/* ---------------------------------------------------------------------------
+ * fw_dense_topk_noalloc -- fw_dense_topk for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Same operation, arguments, outputs, kernels and
+ * results as fw_dense_topk, without the workspace arguments.  Its scratch
+ * space is a static device array of FW_NOALLOC_SCRATCH_BYTES bytes that the
+ * library holds on every GPU it runs on until the process ends; the call
+ * allocates nothing, and it clears what must start at zero with a kernel (no
+ * memset).  `stream` must belong to the current device.
+ * Calls on one GPU share that GPU's array, which keeps the last call's
+ * contents: calls that overlap on one GPU (several streams or host threads)
+ * race and must be serialised by the caller.
+ * Errors: those of fw_dense_topk other than FW_E_WORKSPACE; FW_E_UNSUPPORTED
+ * when the call needs more scratch than FW_NOALLOC_SCRATCH_BYTES (the size
+ * fw_dense_topk_workspace_size reports for the same arguments) or when the
+ * stream belongs to another device; FW_E_HIP when the device or the scratch
+ * address cannot be queried.
+ * ------------------------------------------------------------------------- */
+#define FW_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+fw_status fw_dense_topk_noalloc(const fw_rows *rows, const int32_t *ks, int32_t n_ks,
+                                float *o, float *o_s, float *gap, float *dropped,
+                                int32_t *topk_idx, fw_stream stream);
 
 /* ---------------------------------------------------------------------------
  * fw_best_subset -- exact best kept set of size k by exhaustive enumeration

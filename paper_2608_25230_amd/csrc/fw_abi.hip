@@ -6,8 +6,15 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "fw_internal.hpp"
+
+// Scratch space of fw_dense_topk_noalloc: one copy per GPU, allocated with the
+// code object and held until the process ends.  In host code this name only
+// stands in for the symbol; kernels and copies use the per-device address
+// taken from hipGetSymbolAddress below, never the name itself.
+static __device__ __align__(256) unsigned char scratch[FW_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -188,18 +195,25 @@ size_t fw_dense_topk_workspace_size(const fw_rows *rows, const int32_t *ks, int3
     return dense_topk_ws_bytes(rows, k);
 }
 
-fw_status fw_dense_topk(const fw_rows *rows, const int32_t *ks, int32_t n_ks, float *o, float *o_s,
-                        float *gap, float *dropped, int32_t *topk_idx, void *ws, size_t ws_bytes,
-                        fw_stream stream) {
+}  // extern "C"
+
+namespace {
+
+fw_status check_dense_topk(const fw_rows *rows, const int32_t *ks, int32_t n_ks, const float *gap,
+                           const float *dropped, const int32_t *topk_idx, fw::KsArg *k) {
     fw_status s = check_rows(rows, true);
     if (s != FW_OK) return s;
-    fw::KsArg k;
-    if ((s = parse_ks(rows, ks, n_ks, &k)) != FW_OK) return s;
+    if ((s = parse_ks(rows, ks, n_ks, k)) != FW_OK) return s;
     if (!gap || !dropped) return fail(FW_E_NULL, "gap and dropped are required");
+    if (topk_idx && k->k[k->n - 1] > 16384) return fail(FW_E_UNSUPPORTED, "topk_idx needs kmax <= 16384");
+    return FW_OK;
+}
+
+// Launches of fw_dense_topk once the arguments and the workspace are checked.
+fw_status dense_topk_launch(const fw_rows *rows, const fw::KsArg &k, float *o, float *o_s, float *gap,
+                            float *dropped, int32_t *topk_idx, void *ws, hipStream_t st) {
     const int kmax = k.k[k.n - 1];
-    if (topk_idx && kmax > 16384) return fail(FW_E_UNSUPPORTED, "topk_idx needs kmax <= 16384");
-    if ((s = check_ws(ws, ws_bytes, dense_topk_ws_bytes(rows, k))) != FW_OK) return s;
-    hipStream_t st = (hipStream_t)stream;
+    const int n_ks = k.n;
     if (fw::fused_topk_supported(*rows, k))
         return hip_status(fw::launch_fused_topk(*rows, k, o, o_s, gap, dropped, topk_idx, ws, st),
                           "fw_dense_topk");
@@ -215,6 +229,69 @@ fw_status fw_dense_topk(const fw_rows *rows, const int32_t *ks, int32_t n_ks, fl
         e = fw::launch_tiers(rows->dtype, rows->v, w.z, w.row_m, w.row_l, w.thr_key, w.thr_cut, H,
                              G, n, d, k, o, o_s, gap, dropped, st);
     return hip_status(e, "fw_dense_topk");
+}
+
+// Per-device address of `scratch`, taken once per device with that device
+// current (every GPU holds its own copy at its own address).
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kScratchDevices];
+
+fw_status scratch_address(hipStream_t st, void **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_status(e, "fw_dense_topk_noalloc: hipGetDevice");
+    if (st) {
+        int sdev = -1;
+        if ((e = hipStreamGetDevice(st, &sdev)) != hipSuccess)
+            return hip_status(e, "fw_dense_topk_noalloc: hipStreamGetDevice");
+        if (sdev != dev)
+            return fail(FW_E_UNSUPPORTED, "stream belongs to device %d but device %d is current", sdev, dev);
+    }
+    if (dev < 0 || dev >= kScratchDevices)
+        return fail(FW_E_UNSUPPORTED, "device %d is beyond the %d devices the scratch table holds", dev,
+                    kScratchDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess)
+            return hip_status(e, "fw_dense_topk_noalloc: hipGetSymbolAddress");
+        if (!p) return fail(FW_E_HIP, "fw_dense_topk_noalloc: no device address for the scratch array");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return FW_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+fw_status fw_dense_topk(const fw_rows *rows, const int32_t *ks, int32_t n_ks, float *o, float *o_s,
+                        float *gap, float *dropped, int32_t *topk_idx, void *ws, size_t ws_bytes,
+                        fw_stream stream) {
+    fw::KsArg k;
+    fw_status s = check_dense_topk(rows, ks, n_ks, gap, dropped, topk_idx, &k);
+    if (s != FW_OK) return s;
+    if ((s = check_ws(ws, ws_bytes, dense_topk_ws_bytes(rows, k))) != FW_OK) return s;
+    return dense_topk_launch(rows, k, o, o_s, gap, dropped, topk_idx, ws, (hipStream_t)stream);
+}
+
+fw_status fw_dense_topk_noalloc(const fw_rows *rows, const int32_t *ks, int32_t n_ks, float *o, float *o_s,
+                                float *gap, float *dropped, int32_t *topk_idx, fw_stream stream) {
+    fw::KsArg k;
+    fw_status s = check_dense_topk(rows, ks, n_ks, gap, dropped, topk_idx, &k);
+    if (s != FW_OK) return s;
+    const size_t need = dense_topk_ws_bytes(rows, k);
+    if (need > FW_NOALLOC_SCRATCH_BYTES)
+        return fail(FW_E_UNSUPPORTED,
+                    "fw_dense_topk_noalloc: this call needs %zu bytes of scratch, more than the %zu the "
+                    "library holds per device (use fw_dense_topk with a workspace)",
+                    need, (size_t)FW_NOALLOC_SCRATCH_BYTES);
+    hipStream_t st = (hipStream_t)stream;
+    void *ws = nullptr;
+    if ((s = scratch_address(st, &ws)) != FW_OK) return s;
+    return dense_topk_launch(rows, k, o, o_s, gap, dropped, topk_idx, ws, st);
 }
 
 // ---------------------------------------------------------------------------

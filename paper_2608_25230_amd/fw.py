@@ -19,6 +19,8 @@ STATUS = {0: "FW_OK", 1: "FW_E_NULL", 2: "FW_E_SHAPE", 3: "FW_E_DTYPE", 4: "FW_E
           5: "FW_E_WORKSPACE", 6: "FW_E_HIP"}
 ENTRY_POINTS = ("fw_dense_topk", "fw_best_subset", "fw_swap", "fw_dropped_mass_curve",
                 "fw_ragged_compact", "fw_pool_subset", "fw_group_vote", "fw_maxpool_scores")
+# entry points that take no workspace: their scratch is a static device array
+NOALLOC_ENTRY_POINTS = ("fw_dense_topk_noalloc",)
 # columns of fw_pool_subset's stats (FW_POOL_* in include/fw.h)
 POOL_STATS = ("es_top", "es_pool", "es_bal", "kappa_hat", "c_hat", "kappa_bal", "dropped", "phi",
               "diam", "sigma", "bound_diam", "bound_var")
@@ -45,6 +47,7 @@ RP = ctypes.POINTER(Rows)
 _SIGS = {
     "fw_dense_topk_workspace_size": (SZ, [RP, P, I32]),
     "fw_dense_topk": (I32, [RP, P, I32, P, P, P, P, P, P, SZ, P]),
+    "fw_dense_topk_noalloc": (I32, [RP, P, I32, P, P, P, P, P, P]),
     "fw_best_subset_workspace_size": (SZ, [RP, I32]),
     "fw_best_subset": (I32, [RP, I32, P, P, P, P, P, P, P, SZ, P]),
     "fw_swap_workspace_size": (SZ, [RP, I32, I32]),
@@ -154,6 +157,29 @@ def dense_topk(q, k, v, ks: Sequence[int], scale=None, bias=None, *, want_o=True
                            _ptr(out["gap"]), _ptr(out["dropped"]), _ptr(out["topk_idx"]),
                            ws.data_ptr(), ws.numel(), _stream()))
     out["_ws"] = ws
+    return out
+
+
+def dense_topk_noalloc(q, k, v, ks: Sequence[int], scale=None, bias=None, *, want_o=True, want_os=True,
+                       want_idx=True) -> Dict[str, object]:
+    """``dense_topk`` through fw_dense_topk_noalloc: the library's static
+    per-device scratch array in place of a workspace."""
+    torch = _torch()
+    rows = _rows(q, k, v, scale, bias)
+    ks_arr = (ctypes.c_int32 * len(ks))(*[int(x) for x in ks])
+    H, G, n, d = rows.H, rows.G, rows.n, rows.d
+    dev = q.device
+    nk = len(ks)
+    out = {
+        "o": torch.empty((H, G, d), dtype=torch.float32, device=dev) if want_o else None,
+        "o_s": torch.empty((nk, H, G, d), dtype=torch.float32, device=dev) if want_os else None,
+        "gap": torch.empty((nk, H, G), dtype=torch.float32, device=dev),
+        "dropped": torch.empty((nk, H, G), dtype=torch.float32, device=dev),
+        "topk_idx": torch.empty((H, G, max(ks)), dtype=torch.int32, device=dev) if want_idx else None,
+    }
+    _check(lib().fw_dense_topk_noalloc(ctypes.byref(rows), ks_arr, nk, _ptr(out["o"]), _ptr(out["o_s"]),
+                                       _ptr(out["gap"]), _ptr(out["dropped"]), _ptr(out["topk_idx"]),
+                                       _stream()))
     return out
 
 

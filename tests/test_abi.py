@@ -34,6 +34,31 @@ def test_header_declares_every_entry_point():
             assert ep + "_workspace_size" in names
 
 
+def test_header_declares_the_noalloc_entry_point():
+    names = _declared()
+    for ep in fw.NOALLOC_ENTRY_POINTS:
+        assert ep in names and ep + "_workspace_size" not in names
+
+
+def test_dense_topk_noalloc_validation(L):
+    """Argument errors and a request beyond the static scratch size are
+    rejected on the host, before any device is queried."""
+    ks = _ks(4, 8)
+    call = lambda rows, ks, nk, gap=1, dropped=1: L.fw_dense_topk_noalloc(
+        rows, ks, nk, None, None, gap, dropped, None, None)
+    assert call(None, ks, 2) == 1
+    assert call(_rows(), ks, 2, gap=None) == 1
+    assert call(_rows(), _ks(4, 4), 2) == 2
+    assert call(_rows(dtype=9), ks, 2) == 3
+    # fp32 rows take the general path, whose workspace holds every logit:
+    # 4096 rows x 8192 keys x 4 bytes = 128 MiB > the 64 MiB scratch array
+    big = _rows(H=1, G=4096, n=8192, d=8)
+    need = L.fw_dense_topk_workspace_size(big, ks, 2)
+    assert need > 64 << 20
+    assert call(big, ks, 2) == 4
+    assert b"scratch" in L.fw_last_error()
+
+
 def test_every_declared_symbol_is_exported(L):
     for name in _declared():
         assert hasattr(L, name), name
