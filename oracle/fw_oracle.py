@@ -218,33 +218,28 @@ def row_best_subset(z: np.ndarray, V: np.ndarray, k: int) -> Dict[str, object]:
 # ----------------------------------------------------------------------------
 
 
-def _best_swap_direct(p: np.ndarray, V: np.ndarray, S: np.ndarray) -> Tuple[float, int, int]:
-    """Evaluate es(S - i + j) from the definition for every kept i and dropped
-    j; return (min es, i, j), ties to the smallest (i, j)."""
+def swap_values(p: np.ndarray, V: np.ndarray, S: Sequence[int], method: str = "direct"
+                ) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """es(S - i + j) for every kept key i and dropped key j, as an array
+    [|S|][n - |S|] over the kept keys ascending (rows) and the dropped keys
+    ascending (columns); returns (values, kept keys, dropped keys).
+
+    ``direct`` evaluates every candidate set from the definition.  ``gform``
+    uses Lemma 2.2's second form es(A) = ||g_A|| / p(A) with
+    g_A = sum_{j in A} p_j (v_j - mu): ||g - u_i + u_j||^2 expands into norms,
+    inner products with g and the cross terms u_i . u_j, taken as one float64
+    matrix product."""
+    p = np.asarray(p, np.float64)
+    V = np.asarray(V, np.float64)
     n = p.size
-    Sin = np.sort(S)
+    Sin = np.sort(np.asarray(S, np.int64))
     Sout = np.setdiff1d(np.arange(n), Sin)
-    cands = []
-    pairs = []
-    for i in Sin:
-        for j in Sout:
-            cands.append(np.sort(np.concatenate([Sin[Sin != i], [j]])))
-            pairs.append((int(i), int(j)))
-    es = subset_errors(p, V, np.array(cands, np.int64))
-    t = int(np.argmin(es))
-    return float(es[t]), pairs[t][0], pairs[t][1]
-
-
-def _best_swap_gform(p: np.ndarray, V: np.ndarray, S: np.ndarray) -> Tuple[float, int, int]:
-    """Same as ``_best_swap_direct`` through Lemma 2.2's second form
-    es(A) = ||g_A|| / p(A), g_A = sum_{j in A} p_j (v_j - mu):
-    ||g - u_i + u_j||^2 expands into norms, inner products with g and the
-    cross terms u_i . u_j (one float64 matrix product per call)."""
-    n = p.size
+    if method == "direct":
+        cands = [np.sort(np.concatenate([Sin[Sin != i], [j]])) for i in Sin for j in Sout]
+        vals = subset_errors(p, V, np.array(cands, np.int64)).reshape(Sin.size, Sout.size)
+        return vals, Sin, Sout
     mu = p @ V
     U = p[:, None] * (V - mu)
-    Sin = np.sort(S)
-    Sout = np.setdiff1d(np.arange(n), Sin)
     g = U[Sin].sum(axis=0)
     P = p[Sin].sum()
     a_in, a_out = U[Sin] @ g, U[Sout] @ g
@@ -252,10 +247,16 @@ def _best_swap_gform(p: np.ndarray, V: np.ndarray, S: np.ndarray) -> Tuple[float
     cross = U[Sin] @ U[Sout].T
     num = (g @ g) + b_in[:, None] + b_out[None, :] - 2.0 * a_in[:, None] + 2.0 * a_out[None, :] - 2.0 * cross
     den = (P - p[Sin][:, None] + p[Sout][None, :]) ** 2
-    val = np.maximum(num, 0.0) / den
-    t = int(np.argmin(val))
-    i, j = divmod(t, len(Sout))
-    return float(math.sqrt(val.flat[t])), int(Sin[i]), int(Sout[j])
+    return np.sqrt(np.maximum(num, 0.0) / den), Sin, Sout
+
+
+def _best_swap(p: np.ndarray, V: np.ndarray, S: np.ndarray, method: str) -> Tuple[float, int, int]:
+    """(min es over all single swaps, kept key i, dropped key j); ties to the
+    smallest (i, j): the first minimum in (i asc, j asc) order."""
+    vals, Sin, Sout = swap_values(p, V, S, method)
+    t = int(np.argmin(vals))
+    i, j = divmod(t, Sout.size)
+    return float(vals.flat[t]), int(Sin[i]), int(Sout[j])
 
 
 def swap_rule(p: np.ndarray, V: np.ndarray, k: int, max_iters: int,
@@ -274,7 +275,6 @@ def swap_rule(p: np.ndarray, V: np.ndarray, k: int, max_iters: int,
     S = np.sort(np.asarray(start, np.int64))
     if method == "auto":
         method = "direct" if p.size <= 32 else "gform"
-    search = _best_swap_direct if method == "direct" else _best_swap_gform
     traj = np.full(max_iters + 1, np.nan)
     cur = forced_error(p, V, S)
     traj[0] = cur
@@ -282,7 +282,7 @@ def swap_rule(p: np.ndarray, V: np.ndarray, k: int, max_iters: int,
     if k == 0 or k == p.size:
         return S, traj, 0
     while it < max_iters:
-        es_new, i, j = search(p, V, S)
+        es_new, i, j = _best_swap(p, V, S, method)
         if not es_new < cur:
             break
         S = np.sort(np.concatenate([S[S != i], [j]]))
@@ -487,6 +487,101 @@ def pool_swap(p: np.ndarray, V: np.ndarray, pool: Sequence[int], s: int, max_ite
     return S, traj, it
 
 
+# ----------------------------------------------------------------------------
+# Free weights (Section 2.1, the definitions after Definition 2.1, and
+# Proposition A.1; the appendix's "Penalty" subsection): ef(A) is the distance
+# from mu to the convex hull of A's values, EF(s) its least value over size-s
+# sets, EF_FW its Frank-Wolfe estimate over the candidate set
+# ----------------------------------------------------------------------------
+
+
+def hull_distance(V: np.ndarray, mu: np.ndarray, S: Sequence[int]) -> float:
+    """ef(S) = dist(mu, conv{v_j : j in S}), exactly, by brute force over the
+    faces.  The point of the hull nearest mu lies in the relative interior of
+    some face and is a positive combination of affinely independent vertices F
+    of that face, where it is also the point of aff F nearest mu.  So for every
+    nonempty F subset of S take the point of aff F nearest mu (least squares
+    with weights summing to one); it is in the hull when its weights are
+    nonnegative, and the least distance among those points is ef(S).
+    Exponential in |S|: small sets only."""
+    V = np.asarray(V, np.float64)
+    mu = np.asarray(mu, np.float64)
+    S = [int(j) for j in S]
+    best = math.inf
+    for size in range(1, len(S) + 1):
+        for F in itertools.combinations(S, size):
+            v0 = V[F[0]]
+            if size == 1:
+                w = np.ones(1)
+            else:
+                B = (V[list(F[1:])] - v0).T
+                t = np.linalg.lstsq(B, mu - v0, rcond=None)[0]
+                w = np.concatenate([[1.0 - t.sum()], t])
+            if w.min() < -1e-12:
+                continue
+            best = min(best, float(np.linalg.norm(w @ V[list(F)] - mu)))
+    return best
+
+
+def exact_free_error(V: np.ndarray, mu: np.ndarray, keys: Sequence[int], s: int) -> float:
+    """EF(s) restricted to ``keys``: the least ef(A) over the size-s subsets A
+    of ``keys``.  A larger set only widens the hull, so this is the least
+    distance from mu to the hull of at most s of the keys; brute force over
+    those faces (small instances only)."""
+    keys = [int(j) for j in keys]
+    return min(hull_distance(V, mu, F) for F in itertools.combinations(keys, min(s, len(keys))))
+
+
+def frank_wolfe(V: np.ndarray, mu: np.ndarray, keys: Sequence[int], s: int, max_iters: int) -> Dict[str, object]:
+    """The Frank-Wolfe estimate EF_FW of EF(s) over the points v_j, j in
+    ``keys``: minimise ||x - mu||^2 over x in their convex hull, holding x as
+    weights w over the keys.  Start at the key nearest mu (ties to the lower
+    key index).  Each step takes the vertex j minimising the linearised
+    objective <v_j, x - mu> (ties to the lower key index) and the duality gap
+    <x - mu, x - v_j>; it stops when that gap is not positive, when j would be
+    an (s+1)-th key of the support, or after ``max_iters`` steps; otherwise it
+    moves to x + eta (v_j - x) with the exact line search
+    eta = min(1, gap / ||v_j - x||^2).  Returns ef = ||x - mu|| (an upper bound
+    on EF(s) over ``keys``: x lies in the hull of at most s of them), the
+    support (keys of positive weight, ascending), the weights and the number of
+    steps taken."""
+    V = np.asarray(V, np.float64)
+    mu = np.asarray(mu, np.float64)
+    keys = np.sort(np.asarray(keys, np.int64))
+    P = V[keys]
+    w = np.zeros(keys.size)
+    w[int(np.argmin(np.linalg.norm(P - mu, axis=1)))] = 1.0
+    steps = 0
+    while steps < max_iters:
+        x = w @ P
+        r = x - mu
+        j = int(np.argmin(P @ r))
+        dvec = P[j] - x
+        gap = -float(r @ dvec)
+        if not gap > 0.0:
+            break
+        if w[j] == 0.0 and np.count_nonzero(w) >= s:
+            break
+        eta = min(1.0, gap / float(dvec @ dvec))
+        w = (1.0 - eta) * w
+        w[j] += eta
+        steps += 1
+    support = keys[w > 0.0]
+    return dict(ef=float(np.linalg.norm(w @ P - mu)), support=support, weights=w[w > 0.0], steps=steps)
+
+
+def geometric_set(support: Sequence[int], top: Sequence[int], s: int) -> np.ndarray:
+    """A^geo_s: the Frank-Wolfe support padded to s keys with the top-mass
+    keys it lacks, taken in rank order (appendix, "Penalty").  Ascending."""
+    out = [int(j) for j in support]
+    for j in top:
+        if len(out) >= s:
+            break
+        if int(j) not in out:
+            out.append(int(j))
+    return np.sort(np.asarray(out, np.int64))
+
+
 def certificate(p: np.ndarray, V: np.ndarray, S: Sequence[int]) -> Dict[str, float]:
     """Per-row statistics of a kept set S (the top-mass set in the paper):
     dropped mass pbar(S); Phi = ||g_S|| with g_S = sum_{j in S} p_j (v_j - mu)
@@ -516,11 +611,15 @@ def ratio(num: float, den: float) -> float:
     return 1.0 if num == 0.0 else math.inf
 
 
-def row_pool(z: np.ndarray, V: np.ndarray, s: int, extra: int, max_iters: int) -> Dict[str, object]:
+def row_pool(z: np.ndarray, V: np.ndarray, s: int, extra: int, max_iters: int,
+             fw_iters: int = 64) -> Dict[str, object]:
     """Everything Definition 2.5 and the enumeration protocol report for one
     row: the candidate set, ES_pool and its argmin, the pool-restricted
     balancing set, kappa_hat = es(A*_s)/ES_pool, c_hat = 1 - ES_pool/es(A*_s),
-    kappa_bal = es(A_bal)/ES_pool and the certificate statistics of A*_s."""
+    kappa_bal = es(A_bal)/ES_pool and the certificate statistics of A*_s;
+    and, over the same candidate set, the Frank-Wolfe estimate EF_FW(s)
+    (``fw_iters`` steps at most), the geometric set A^geo_s with its error and
+    the penalty estimate pi_hat = ES_pool / EF_FW."""
     z = np.asarray(z, np.float64)
     p = weights(z)
     top, extras = candidate_pool(z, V, s, extra)
@@ -532,9 +631,13 @@ def row_pool(z: np.ndarray, V: np.ndarray, s: int, extra: int, max_iters: int) -
     bal, traj, n_swaps = pool_swap(p, V, pool, s, max_iters, top)
     es_bal = forced_error(p, V, bal)
     cert = certificate(p, V, top)
+    fw = frank_wolfe(V, dense_output(p, V), pool, s, fw_iters)
+    geo = geometric_set(fw["support"], top, s)
     return dict(top=top, extras=extras, best_idx=best, bal_idx=bal, es_top=es_top, es_pool=es_pool,
                 es_bal=es_bal, kappa_hat=ratio(es_top, es_pool), c_hat=closed_fraction(es_top, es_pool),
-                kappa_bal=ratio(es_bal, es_pool), n_swaps=n_swaps, traj=traj, **cert)
+                kappa_bal=ratio(es_bal, es_pool), n_swaps=n_swaps, traj=traj,
+                ef_fw=fw["ef"], fw_support=fw["support"], fw_steps=fw["steps"], geo_idx=geo,
+                es_geo=forced_error(p, V, geo), pi_hat=ratio(es_pool, fw["ef"]), **cert)
 
 
 def cell_median(dropped: np.ndarray) -> float:

@@ -6,6 +6,9 @@ place of suffix, Phi reported for es, one budget's set used for every budget,
 an inverted ratio, a non-strict stopping rule, ...) and runs the pins that
 should catch it.
 """
+import itertools
+import math
+
 import numpy as np
 import pytest
 
@@ -47,8 +50,15 @@ def _run_all_pins():
     checks += [(P.test_allocation_uniform_cap_is_per_cell_top,)]
     checks += [(P.test_maxpool_scores, k) for k in (1, 3, 7)]
     checks += [(P.test_row_dense_topk_example_2_3,), (P.test_row_best_subset_example_2_3,),
-               (P.test_balancing_stops_at_a_local_optimum,), (P.test_swap_rule_stops_on_a_tie,)]
+               (P.test_balancing_stops_at_a_local_optimum,), (P.test_swap_rule_stops_on_a_tie,),
+               (P.test_swap_values_example_2_3,)]
     checks += [(P.test_row_dense_topk_per_budget_first_form, s) for s in range(4)]
+    checks += [(P.test_hull_distance_constructed,), (P.test_frank_wolfe_example_2_3,),
+               (P.test_geometric_set_pads_in_rank_order,)]
+    checks += [(P.test_free_error_brute_force_and_bounds, s) for s in range(4)]
+    checks += [(P.test_frank_wolfe_one_dimension_closed_form, s) for s in range(3)]
+    checks += [(P.test_frank_wolfe_convergence_rate_and_descent, s) for s in range(3)]
+    checks += [(P.test_frank_wolfe_permutation, s) for s in range(2)]
     return any(_fails(*c) for c in checks)
 
 
@@ -216,8 +226,8 @@ def _best_dropped_is_kept(z, V, k):
     return r
 
 
-def _pool_kappa_bal_inverted(z, V, s, extra, max_iters):
-    r = _ORIG_ROW_POOL(z, V, s, extra, max_iters)
+def _pool_kappa_bal_inverted(z, V, s, extra, max_iters, fw_iters=64):
+    r = _ORIG_ROW_POOL(z, V, s, extra, max_iters, fw_iters)
     r["kappa_bal"] = O.ratio(r["es_pool"], r["es_bal"])
     return r
 
@@ -229,7 +239,7 @@ def _swap_non_strict(p, V, k, max_iters, start=None, method="auto"):
     if start is None:
         start = O.top_mass_set(np.log(p), k)
     S = np.sort(np.asarray(start, np.int64))
-    search = O._best_swap_direct if (method == "direct" or (method == "auto" and p.size <= 32)) else O._best_swap_gform
+    method = "direct" if (method == "direct" or (method == "auto" and p.size <= 32)) else "gform"
     traj = np.full(max_iters + 1, np.nan)
     cur = O.forced_error(p, V, S)
     traj[0] = cur
@@ -237,7 +247,7 @@ def _swap_non_strict(p, V, k, max_iters, start=None, method="auto"):
     if k == 0 or k == p.size:
         return S, traj, 0
     while it < max_iters:
-        es_new, i, j = search(p, V, S)
+        es_new, i, j = O._best_swap(p, V, S, method)
         if not es_new <= cur:
             break
         S = np.sort(np.concatenate([S[S != i], [j]]))
@@ -246,7 +256,93 @@ def _swap_non_strict(p, V, k, max_iters, start=None, method="auto"):
         traj[it] = cur
     return S, traj, it
 
+_ORIG_FW = O.frank_wolfe
+_ORIG_HULL = O.hull_distance
+_ORIG_ROW_POOL_FW = O.row_pool
+
+
+def _fw_variant(vertex="argmin", step="square", start="nearest", cap=0):
+    def fw(V, mu, keys, s, max_iters):
+        V = np.asarray(V, np.float64)
+        mu = np.asarray(mu, np.float64)
+        keys = np.sort(np.asarray(keys, np.int64))
+        P = V[keys]
+        w = np.zeros(keys.size)
+        w[0 if start == "first" else int(np.argmin(np.linalg.norm(P - mu, axis=1)))] = 1.0
+        steps = 0
+        while steps < max_iters:
+            x = w @ P
+            r = x - mu
+            j = int(np.argmin(P @ r)) if vertex == "argmin" else int(np.argmax(P @ r))
+            dvec = P[j] - x
+            gap = -float(r @ dvec)
+            if vertex == "argmin" and not gap > 0.0:
+                break
+            if w[j] == 0.0 and np.count_nonzero(w) >= s + cap:
+                break
+            nrm = float(dvec @ dvec)
+            if nrm == 0.0:
+                break
+            eta = min(1.0, gap / (nrm if step == "square" else math.sqrt(nrm)))
+            if vertex != "argmin":
+                eta = min(1.0, abs(eta))
+            w = (1.0 - eta) * w
+            w[j] += eta
+            steps += 1
+        return dict(ef=float(np.linalg.norm(w @ P - mu)), support=keys[w > 0.0], weights=w[w > 0.0], steps=steps)
+    return fw
+
+
+def _hull_negative_weights(V, mu, S):
+    # accepts affine projections outside the hull
+    V = np.asarray(V, np.float64)
+    mu = np.asarray(mu, np.float64)
+    S = [int(j) for j in S]
+    best = math.inf
+    for size in range(1, len(S) + 1):
+        for F in itertools.combinations(S, size):
+            v0 = V[F[0]]
+            if size == 1:
+                w = np.ones(1)
+            else:
+                B = (V[list(F[1:])] - v0).T
+                t = np.linalg.lstsq(B, mu - v0, rcond=None)[0]
+                w = np.concatenate([[1.0 - t.sum()], t])
+            best = min(best, float(np.linalg.norm(w @ V[list(F)] - mu)))
+    return best
+
+
+def _exact_free_one_fewer(V, mu, keys, s):
+    keys = [int(j) for j in keys]
+    m = max(1, min(s, len(keys)) - 1)
+    return min(O.hull_distance(V, mu, F) for F in itertools.combinations(keys, m))
+
+
+def _geo_pads_ascending(support, top, s):
+    out = [int(j) for j in support]
+    for j in sorted(int(t) for t in top):
+        if len(out) >= s:
+            break
+        if j not in out:
+            out.append(j)
+    return np.sort(np.asarray(out, np.int64))
+
+
+def _pool_pi_inverted(z, V, s, extra, max_iters, fw_iters=64):
+    r = _ORIG_ROW_POOL_FW(z, V, s, extra, max_iters, fw_iters)
+    r["pi_hat"] = O.ratio(r["ef_fw"], r["es_pool"])
+    return r
+
+
 MUTANTS = {
+    "frank_wolfe_vertex_argmax": ("frank_wolfe", _fw_variant(vertex="argmax")),
+    "frank_wolfe_step_over_norm": ("frank_wolfe", _fw_variant(step="norm")),
+    "frank_wolfe_starts_at_first_key": ("frank_wolfe", _fw_variant(start="first")),
+    "frank_wolfe_support_cap_plus_one": ("frank_wolfe", _fw_variant(cap=1)),
+    "hull_distance_negative_weights": ("hull_distance", _hull_negative_weights),
+    "exact_free_error_one_key_fewer": ("exact_free_error", _exact_free_one_fewer),
+    "geometric_set_pads_ascending": ("geometric_set", _geo_pads_ascending),
+    "pool_pi_hat_inverted": ("row_pool", _pool_pi_inverted),
     "group_vote_by_max_mass": ("group_vote", _vote_by_max),
     "allocation_cap_ignores_floor": ("allocate", _cap_counts_floor_twice),
     "maxpool_one_sided_window": ("maxpool_scores", _maxpool_one_sided),

@@ -243,6 +243,20 @@ def test_hardness_all_pairs_tie():
     assert best.tolist() == [0, 3] and ES == 0.0
 
 
+def test_swap_values_example_2_3():
+    """Every single swap from Example 2.3's top-mass set {0,1}: dropping 0
+    for 2 gives {1,2} at 27/22, dropping 1 for 2 gives {0,2} at 9/22 (the
+    example's optimum); both evaluators agree."""
+    g = _golden("example_2_3.json")
+    v = np.array(g["v"], float)[:, None]
+    p = np.array([float(Fraction(x)) for x in g["p"]])
+    for method in ("direct", "gform"):
+        vals, Sin, Sout = O.swap_values(p, v, [1, 0], method)
+        assert Sin.tolist() == [0, 1] and Sout.tolist() == [2]
+        np.testing.assert_allclose(vals[:, 0], [float(Fraction(g["es"]["1,2"])), float(Fraction(g["es"]["0,2"]))],
+                                   rtol=1e-13)
+
+
 def test_swap_rule_stops_on_a_tie():
     """The balancing selector stops when no swap strictly decreases es
     (Section 2.1).  On the hardness instance w = (1,1,1,4) with uniform
@@ -738,3 +752,137 @@ def test_maxpool_scores(kernel):
     ref = scipy_nd.maximum_filter1d(r, size=kernel, axis=1, mode="nearest")
     assert np.array_equal(out, ref)
     assert np.all(out >= r)
+
+
+# ---------------------------------------------------------------------------
+# Free weights: ef, EF and the Frank-Wolfe estimate (Section 2.1, the
+# definitions after Definition 2.1; Proposition A.1; the appendix's "Penalty")
+# ---------------------------------------------------------------------------
+
+def _frac_vec(xs):
+    return np.array([float(Fraction(str(x))) for x in xs])
+
+
+def test_hull_distance_constructed():
+    g = _golden("frank_wolfe.json")
+    V = np.array(g["triangle"]["V"], float)
+    for c in g["triangle"]["cases"]:
+        dist = O.hull_distance(V, _frac_vec(c["mu"]), [0, 1, 2])
+        assert dist ** 2 == pytest.approx(float(Fraction(c["dist_sq"])), rel=1e-13, abs=1e-26), c["note"]
+    c = g["collinear"]
+    V = np.array(c["V"], float)
+    assert O.hull_distance(V, _frac_vec(c["mu"]), range(4)) ** 2 == pytest.approx(float(Fraction(c["dist_sq"])), rel=1e-13)
+
+
+def test_frank_wolfe_example_2_3():
+    """Example 2.3: EF(2) = 0 although ES(2) = 9/22, so pi = +inf; EF(1) is the
+    distance to the nearest value, 1/2."""
+    g = _golden("frank_wolfe.json")["example_2_3"]
+    F = lambda x: float(Fraction(x))
+    v = np.array(g["v"], float)[:, None]
+    p = _frac_vec(g["p"])
+    mu = O.dense_output(p, v)
+    assert O.exact_free_error(v, mu, range(3), 2) == pytest.approx(F(g["EF_2"]), abs=1e-15)
+    assert O.exact_free_error(v, mu, range(3), 1) == pytest.approx(F(g["EF_1"]), rel=1e-13)
+    fw1 = O.frank_wolfe(v, mu, range(3), 1, 16)
+    assert fw1["ef"] == pytest.approx(F(g["EF_1"]), rel=1e-13) and fw1["support"].tolist() == [1]
+    r = O.row_pool(np.log(p), v, g["s"], g["extra"], max_iters=8, fw_iters=16)
+    assert r["ef_fw"] <= 1e-15
+    assert r["fw_support"].tolist() == g["fw_support_2"]
+    assert r["geo_idx"].tolist() == g["geo_2"]
+    assert r["es_geo"] == pytest.approx(F(g["es_geo_2"]), rel=1e-13)
+    assert r["es_pool"] == pytest.approx(F(g["ES_pool_2"]), rel=1e-13)
+    assert r["pi_hat"] > 1e12
+
+
+def test_geometric_set_pads_in_rank_order():
+    g = _golden("frank_wolfe.json")["geo_padding"]
+    v = np.array(g["v"], float)[:, None]
+    p = _frac_vec(g["p"])
+    mu = np.array([float(Fraction(g["mu"]))])
+    assert O.dense_output(p, v)[0] == mu[0]  # dyadic: exact
+    top = O.top_mass_set(np.log(p), 4)
+    assert top.tolist() == g["rank_order"]
+    fw = O.frank_wolfe(v, mu, range(4), g["s"], 16)
+    assert fw["support"].tolist() == g["fw_support"] and fw["steps"] == g["fw_steps"] and fw["ef"] == 0.0
+    geo = O.geometric_set(fw["support"], top, g["s"])
+    assert geo.tolist() == g["geo"]
+    assert O.forced_error(p, v, geo) == pytest.approx(float(Fraction(g["es_geo"])), rel=1e-13)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_free_error_brute_force_and_bounds(seed):
+    """On small rows with every key a candidate: EF(s) <= sigma / sqrt(s)
+    (Proposition A.1), EF(s) <= ES(s) (es >= ef, Lemma 2.2's proof), EF(d+1) = 0
+    (Caratheodory), EF nonincreasing in s, EF(1) = min_j ||v_j - mu||; the
+    Frank-Wolfe estimate is an upper bound on EF(s) and exact at s = 1."""
+    rng = np.random.default_rng(900 + seed)
+    n, d = 6, 1 + seed % 3
+    z, p, V = _rand_instance(rng, n, d, temp=1.0 + seed)
+    mu = O.dense_output(p, V)
+    dev = np.linalg.norm(V - mu, axis=1)
+    sigma = math.sqrt(float(np.sum(p * dev ** 2)))
+    ef = [O.exact_free_error(V, mu, range(n), s) for s in range(1, n + 1)]
+    for s in range(1, n + 1):
+        assert ef[s - 1] <= sigma / math.sqrt(s) + 1e-12
+        assert ef[s - 1] <= O.best_subset(p, V, s)[1] + 1e-12
+        fw = O.frank_wolfe(V, mu, range(n), s, 200)
+        assert fw["ef"] >= ef[s - 1] - 1e-12
+        assert fw["support"].size <= s and abs(fw["weights"].sum() - 1.0) < 1e-12
+        assert np.all(fw["weights"] > 0)
+    assert np.all(np.diff(ef) <= 1e-12)
+    assert ef[d] <= 1e-12
+    assert ef[0] == pytest.approx(dev.min(), rel=1e-13)
+    assert O.frank_wolfe(V, mu, range(n), 1, 50)["ef"] == pytest.approx(dev.min(), rel=1e-13)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_frank_wolfe_one_dimension_closed_form(seed):
+    """d = 1 with every key a candidate: mu lies between the smallest and the
+    largest value, and one step from the nearest value toward the farthest
+    value on the other side of mu lands on mu, so EF_FW(s) = 0 for s >= 2."""
+    rng = np.random.default_rng(950 + seed)
+    n = 5 + seed
+    z, p, V = _rand_instance(rng, n, 1, temp=2.0)
+    mu = O.dense_output(p, V)
+    D = float(np.abs(V - mu).max())
+    for s in range(2, n + 1):
+        fw = O.frank_wolfe(V, mu, range(n), s, 1)
+        assert fw["steps"] == 1 and fw["ef"] <= 1e-14 * D
+        near = int(np.argmin(np.abs(V[:, 0] - mu[0])))
+        far = int(np.argmin(V[:, 0])) if V[near, 0] > mu[0] else int(np.argmax(V[:, 0]))
+        assert sorted(fw["support"].tolist()) == sorted([near, far])
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_frank_wolfe_convergence_rate_and_descent(seed):
+    """Without the support cap (s = number of keys) the iterates descend and
+    obey the Frank-Wolfe rate with exact line search:
+    ||x_t - mu||^2 - dist(mu, hull)^2 <= 4 diam^2 / (t + 2)."""
+    rng = np.random.default_rng(980 + seed)
+    n, d = 6, 4
+    V = rng.standard_normal((n, d))
+    mu = rng.standard_normal(d) * (0.3 if seed == 0 else 2.0)  # inside / outside the hull
+    dist = O.hull_distance(V, mu, range(n))
+    diam = max(np.linalg.norm(V[i] - V[j]) for i in range(n) for j in range(n))
+    prev = math.inf
+    for t in range(0, 40):
+        fw = O.frank_wolfe(V, mu, range(n), n, t)
+        e2 = fw["ef"] ** 2
+        assert e2 - dist ** 2 <= 4 * diam ** 2 / (t + 2) + 1e-12
+        assert fw["ef"] <= prev + 1e-12 and fw["ef"] >= dist - 1e-12
+        prev = fw["ef"]
+
+
+@pytest.mark.parametrize("seed", range(2))
+def test_frank_wolfe_permutation(seed):
+    """Relabelling the keys relabels the support and keeps EF_FW."""
+    rng = np.random.default_rng(990 + seed)
+    n, d, s = 8, 5, 3
+    z, p, V = _rand_instance(rng, n, d)
+    mu = O.dense_output(p, V)
+    perm = rng.permutation(n)
+    a = O.frank_wolfe(V, mu, range(n), s, 30)
+    b = O.frank_wolfe(V[perm], mu, range(n), s, 30)
+    assert b["ef"] == pytest.approx(a["ef"], rel=1e-10, abs=1e-14)
+    assert sorted(perm[b["support"]].tolist()) == a["support"].tolist()
