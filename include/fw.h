@@ -160,7 +160,16 @@ fw_status fw_best_subset(const fw_rows *rows, int32_t k, int32_t *best_idx, floa
  *     ascending index tuple);
  *   - the balancing selector drawing from the candidate set: from A*_s, the
  *     (kept, dropped) pool swap that most decreases es (ties to the smallest
- *     (out, in)), strict decrease only, at most max_swaps swaps.
+ *     (out, in)), strict decrease only, at most max_swaps swaps;
+ *   - the free-weight side (Section 2.1's ef(A) = dist(mu, conv{v_j : j in
+ *     A}) and EF(s); the appendix's penalty estimate): the Frank-Wolfe
+ *     estimate EF_FW of EF(s) over the candidate set's values, from the key
+ *     nearest mu (ties to the lower index), each step toward the vertex of
+ *     least <v_j, x - mu> (ties to the lower index) with the exact line
+ *     search, stopping at a non-positive duality gap, at a vertex that would
+ *     be the (s+1)-th key of the support, or after fw_iters steps; the
+ *     geometric set A^geo_s (the support padded to s keys with top-mass keys
+ *     in rank order), its es, and pi_hat = ES_pool / EF_FW.
  * Arithmetic is float64 throughout.
  *   n_budgets      1 <= n_budgets <= FW_POOL_MAX_BUDGETS
  *   s, extra       host [n_budgets]: 1 <= s[b], 0 <= extra[b],
@@ -169,6 +178,7 @@ fw_status fw_best_subset(const fw_rows *rows, int32_t k, int32_t *best_idx, floa
  *                  subsets (every pool of at most 24 keys is, and the
  *                  paper's (4, 24), (8, 12), (16, 6), (32, 4)); n <= 8192
  *   max_swaps      0 <= max_swaps <= 4096
+ *   fw_iters       0 <= fw_iters <= 4096 Frank-Wolfe steps at most
  * With P_b = s[b] + extra[b], the budgets' lists are concatenated per row in
  * the caller's budget order:
  *   pool_idx       [H][G][sum_b P_b] int32: per budget, A*_s in rank order,
@@ -176,6 +186,8 @@ fw_status fw_best_subset(const fw_rows *rows, int32_t k, int32_t *best_idx, floa
  *   best_idx       [H][G][sum_b s[b]] int32: per budget, the ES_pool argmin,
  *                  ascending (required)
  *   bal_idx        [H][G][sum_b s[b]] int32: per budget, the balancing set,
+ *                  ascending, or NULL
+ *   geo_idx        [H][G][sum_b s[b]] int32: per budget, the geometric set,
  *                  ascending, or NULL
  *   n_swaps        [n_budgets][H][G] int32 balancing swaps applied, or NULL
  *   stats          [n_budgets][H][G][FW_POOL_NSTATS] float32 (required),
@@ -185,12 +197,13 @@ fw_status fw_best_subset(const fw_rows *rows, int32_t k, int32_t *best_idx, floa
  *                  dropped mass of A*_s (the mean of the two middle values
  *                  for even G) and whether it exceeds flat_threshold (a flat
  *                  cell at s = 8, threshold 0.25); either may be NULL
- * kappa values are num/den, 1 when both are 0 and +inf when only den is.
+ * kappa and pi values are num/den, 1 when both are 0 and +inf when only den
+ * is.
  * Errors: FW_E_UNSUPPORTED when a pool or its enumeration is out of the
  * limits above; FW_E_NULL, FW_E_SHAPE, FW_E_DTYPE, FW_E_WORKSPACE, FW_E_HIP.
  * ------------------------------------------------------------------------- */
 #define FW_POOL_MAX_BUDGETS 4
-#define FW_POOL_NSTATS 12
+#define FW_POOL_NSTATS 16
 #define FW_POOL_ES_TOP 0     /* es(A*_s)                                  */
 #define FW_POOL_ES_POOL 1    /* ES_pool(s)                                */
 #define FW_POOL_ES_BAL 2     /* es of the balancing set                   */
@@ -203,12 +216,16 @@ fw_status fw_best_subset(const fw_rows *rows, int32_t k, int32_t *best_idx, floa
 #define FW_POOL_SIGMA 9      /* sigma, sigma^2 = sum_j p_j ||v_j - mu||^2 */
 #define FW_POOL_BOUND_DIAM 10 /* 2 D pbar (Lemma 2.2)                     */
 #define FW_POOL_BOUND_VAR 11  /* sqrt(pbar / (1 - pbar)) sigma            */
+#define FW_POOL_EF_FW 12      /* EF_FW(s): Frank-Wolfe estimate of EF(s)  */
+#define FW_POOL_ES_GEO 13     /* es of the geometric set A^geo_s          */
+#define FW_POOL_PI_HAT 14     /* pi_hat = ES_pool / EF_FW                 */
+#define FW_POOL_FW_STEPS 15   /* Frank-Wolfe steps taken                  */
 size_t fw_pool_subset_workspace_size(const fw_rows *rows, int32_t n_budgets, const int32_t *s,
                                      const int32_t *extra);
 fw_status fw_pool_subset(const fw_rows *rows, int32_t n_budgets, const int32_t *s, const int32_t *extra,
-                         int32_t max_swaps, int32_t *pool_idx, int32_t *best_idx, int32_t *bal_idx,
-                         int32_t *n_swaps, float *stats, float flat_threshold, float *cell_median,
-                         uint8_t *cell_flat, void *ws, size_t ws_bytes, fw_stream stream);
+                         int32_t max_swaps, int32_t fw_iters, int32_t *pool_idx, int32_t *best_idx,
+                         int32_t *bal_idx, int32_t *geo_idx, int32_t *n_swaps, float *stats, float flat_threshold,
+                         float *cell_median, uint8_t *cell_flat, void *ws, size_t ws_bytes, fw_stream stream);
 
 /* ---------------------------------------------------------------------------
  * fw_group_vote -- the group vote of Section 2.1: deployment keeps one set

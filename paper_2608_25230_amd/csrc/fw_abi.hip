@@ -185,7 +185,8 @@ const char *fw_last_error(void) { return g_err; }
 const char *fw_version(void) { return "libfw 0.1 (gfx950)"; }
 
 size_t dense_topk_ws_bytes(const fw_rows *rows, const fw::KsArg &k) {
-    if (fw::fused_topk_supported(*rows, k)) return fw::fused_topk_ws_bytes(*rows, k.k[k.n - 1]);
+    if (fw::mp_topk_supported(*rows, k) || fw::fused_topk_supported(*rows, k))
+        return fw::fused_topk_ws_bytes(*rows, k.k[k.n - 1]);
     return dense_topk_layout(rows, k.n, nullptr).bytes;
 }
 
@@ -214,6 +215,8 @@ fw_status dense_topk_launch(const fw_rows *rows, const fw::KsArg &k, float *o, f
                             float *dropped, int32_t *topk_idx, void *ws, hipStream_t st) {
     const int kmax = k.k[k.n - 1];
     const int n_ks = k.n;
+    if (fw::mp_topk_supported(*rows, k))
+        return hip_status(fw::launch_mp_topk(*rows, k, o, o_s, gap, dropped, topk_idx, ws, st), "fw_dense_topk");
     if (fw::fused_topk_supported(*rows, k))
         return hip_status(fw::launch_fused_topk(*rows, k, o, o_s, gap, dropped, topk_idx, ws, st),
                           "fw_dense_topk");
@@ -320,15 +323,17 @@ size_t fw_pool_subset_workspace_size(const fw_rows *rows, int32_t n_budgets, con
 }
 
 fw_status fw_pool_subset(const fw_rows *rows, int32_t n_budgets, const int32_t *s, const int32_t *extra,
-                         int32_t max_swaps, int32_t *pool_idx, int32_t *best_idx, int32_t *bal_idx,
-                         int32_t *n_swaps, float *stats, float flat_threshold, float *cell_median,
-                         uint8_t *cell_flat, void *ws, size_t ws_bytes, fw_stream stream) {
+                         int32_t max_swaps, int32_t fw_iters, int32_t *pool_idx, int32_t *best_idx,
+                         int32_t *bal_idx, int32_t *geo_idx, int32_t *n_swaps, float *stats, float flat_threshold,
+                         float *cell_median, uint8_t *cell_flat, void *ws, size_t ws_bytes, fw_stream stream) {
     fw_status st = check_pool(rows, n_budgets, s, extra, max_swaps);
     if (st != FW_OK) return st;
+    if (fw_iters < 0 || fw_iters > 4096) return fail(FW_E_SHAPE, "fw_iters must be in [0, 4096]");
     if (!best_idx || !stats) return fail(FW_E_NULL, "best_idx and stats are required");
     if ((st = check_ws(ws, ws_bytes, fw::pool_ws_bytes(*rows, n_budgets, s, extra))) != FW_OK) return st;
-    hipError_t e = fw::launch_pool(*rows, n_budgets, s, extra, max_swaps, pool_idx, best_idx, bal_idx, n_swaps,
-                                   stats, flat_threshold, cell_median, cell_flat, ws, (hipStream_t)stream);
+    hipError_t e = fw::launch_pool(*rows, n_budgets, s, extra, max_swaps, fw_iters, pool_idx, best_idx, bal_idx,
+                                   geo_idx, n_swaps, stats, flat_threshold, cell_median, cell_flat, ws,
+                                   (hipStream_t)stream);
     return hip_status(e, "fw_pool_subset");
 }
 

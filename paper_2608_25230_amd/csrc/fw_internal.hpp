@@ -31,6 +31,12 @@ size_t fused_topk_ws_bytes(const fw_rows &rows, int kmax);
 hipError_t launch_fused_topk(const fw_rows &rows, const KsArg &ks, float *o, float *o_s, float *gap,
                              float *dropped, int32_t *topk_idx, void *ws, hipStream_t st);
 
+// k_topk_mp.hip -- multi-pass one-kernel path for bf16, d = 128, n a multiple
+// of 32 up to 4096, 128 rows per unit tile (same workspace as the fused path)
+bool mp_topk_supported(const fw_rows &rows, const KsArg &ks);
+hipError_t launch_mp_topk(const fw_rows &rows, const KsArg &ks, float *o, float *o_s, float *gap,
+                          float *dropped, int32_t *topk_idx, void *ws, hipStream_t st);
+
 // k_subset.hip -- exhaustive best subset (float64)
 size_t best_subset_ws_bytes(int64_t n, int k);
 bool best_subset_plannable(int64_t n, int k);
@@ -42,7 +48,8 @@ hipError_t launch_best_subset(const fw_rows &rows, int k, int32_t *best_idx, flo
 bool pool_plannable(int64_t N, int d, int nb, const int32_t *s, const int32_t *extra);
 size_t pool_ws_bytes(const fw_rows &rows, int nb, const int32_t *s, const int32_t *extra);
 hipError_t launch_pool(const fw_rows &rows, int nb, const int32_t *s, const int32_t *extra, int max_swaps,
-                       int32_t *pool_idx, int32_t *best_idx, int32_t *bal_idx, int32_t *n_swaps, float *stats,
+                       int fw_iters, int32_t *pool_idx, int32_t *best_idx, int32_t *bal_idx, int32_t *geo_idx,
+                       int32_t *n_swaps, float *stats,
                        float flat_threshold, float *cell_median, uint8_t *cell_flat, void *ws, hipStream_t st);
 
 // k_vote.hip -- group vote

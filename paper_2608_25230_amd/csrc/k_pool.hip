@@ -18,7 +18,12 @@
 //      pair of the pool scored from the Gram each round, ties to the smallest
 //      (out, in) key pair, accepted only on a strict decrease;
 //   6. the reported errors of A*_s, the ES_pool argmin and the balancing set
-//      from d-dimensional residual sums, and the certificate statistics.
+//      from d-dimensional residual sums, and the certificate statistics;
+//   7. beside the balancing (another wave), the Frank-Wolfe estimate of the
+//      free-weight error EF(s) over the pool's values (Section 2.1's ef and
+//      EF; the appendix's penalty estimate), run on the Gram matrix of the
+//      deviations v_i - mu and reported from a d-dimensional sum, with the
+//      geometric set (its support padded with top-mass keys in rank order).
 // A second kernel takes each cell's median dropped mass over its rows.
 #include "fw_internal.hpp"
 #include "instance64.hpp"
@@ -37,7 +42,7 @@ constexpr int kMaxBudgets = FW_POOL_MAX_BUDGETS;
 struct PoolLds {
     size_t xq, mu, red, ctr, rank, eord, tmp, plist, pps, sc, seed;  // persistent
     size_t zz, ee, rk;                                   // row phase
-    size_t gm, vs, cv, ent, pl;                          // pool phase (overlays the row phase)
+    size_t gm, vs, cv, ent, pl, yd, wf;                  // pool phase (overlays the row phase)
     size_t total;
 };
 
@@ -68,7 +73,9 @@ __host__ __device__ inline PoolLds pool_lds(int64_t N, int d, int Pmax, int nent
     L.cv = align_up(L.vs + (size_t)Pmax * (d + 1) * 4, 16);
     L.ent = align_up(L.cv + (size_t)Pmax * 8, 16);
     L.pl = L.ent + (size_t)nentmax * 16;
-    const size_t pool_end = L.pl + (size_t)nentmax * 8;
+    L.yd = align_up(L.pl + (size_t)nentmax * 8, 16);   // Gram matrix of v_i - mu
+    L.wf = align_up(L.yd + (size_t)Pmax * Pmax * 8, 16);  // Frank-Wolfe weights
+    const size_t pool_end = L.wf + (size_t)Pmax * 8;
     L.total = align_up(row_end > pool_end ? row_end : pool_end, 16);
     return L;
 }
@@ -194,9 +201,9 @@ struct PoolArgs {
     const void *q, *k, *v;
     const float *scale, *bias;
     int64_t H, G, N;
-    int d, nb, max_swaps, Smax, Ptot, Stot, Pmax, nentmax;
+    int d, nb, max_swaps, fw_iters, Smax, Ptot, Stot, Pmax, nentmax;
     PoolBudget b[kMaxBudgets];
-    int32_t *pool_idx, *best_idx, *bal_idx, *n_swaps;
+    int32_t *pool_idx, *best_idx, *bal_idx, *geo_idx, *n_swaps;
     float *stats;
 };
 
@@ -381,6 +388,8 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
     double *cv = (double *)(smem + L.cv);
     double2 *ent = (double2 *)(smem + L.ent);
     double *PLt = (double *)(smem + L.pl);
+    double *Yd = (double *)(smem + L.yd);
+    double *wf = (double *)(smem + L.wf);
     const int pitch = d + 1;
     for (int b = 0; b < nb; ++b) {
         const PoolBudget &B = a.b[b];
@@ -404,6 +413,8 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
             const double g = ps[i] * ps[j] * acc;
             Gm[i * P + j] = g;
             Gm[j * P + i] = g;
+            Yd[i * P + j] = acc;
+            Yd[j * P + i] = acc;
         }
         if (tid == 0) ctr[0] = 0;
         __syncthreads();
@@ -492,14 +503,88 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
         } else if (w <= 2) {
             const double e = wave_es(w == 1 ? seed : best);
             if (lane == 0) redd[w] = e;
+        } else if (w == 3) {
+            // Frank-Wolfe over the pool's values, one lane per pool key: with
+            // y_x = v_x - mu and the iterate's residual r = sum_i w_i y_i, lane
+            // x holds w_x and t_x = <y_x, r>; the vertex is the least t_x
+            // (ties to the lower key), the duality gap |r|^2 - t_j, and the
+            // exact line search eta = min(1, gap / |y_j - r|^2)
+            const int x = lane;
+            const bool inP = x < P;
+            const uint64_t lanes = P == 64 ? ~0ull : (1ull << P) - 1ull;
+            auto wave_argmin = [&](double v, int &at) {
+                int j = inP ? x : 64;
+                v = inP ? v : INFINITY;
+#pragma unroll
+                for (int off = 32; off > 0; off >>= 1) {
+                    const double ov = __shfl_xor(v, off);
+                    const int oj = __shfl_xor(j, off);
+                    if (ov < v || (ov == v && oj < j)) {
+                        v = ov;
+                        j = oj;
+                    }
+                }
+                at = j;
+                return v;
+            };
+            int j0;
+            wave_argmin(inP ? Yd[x * P + x] : 0.0, j0);  // the key nearest mu
+            double wx = x == j0 ? 1.0 : 0.0;
+            double tx = inP ? Yd[j0 * P + x] : 0.0;
+            uint64_t sup = 1ull << j0;
+            int steps = 0;
+            while (steps < a.fw_iters) {
+                int j;
+                const double tj = wave_argmin(tx, j);
+                const double q = wave_sum(wx * tx);
+                const double gap = q - tj;
+                if (!(gap > 0.0)) break;
+                if (!((sup >> j) & 1ull) && __popcll(sup) >= s) break;
+                const double nrm = Yd[j * P + j] - 2.0 * tj + q;
+                if (!(nrm > 0.0)) break;
+                const double eta = fmin(1.0, gap / nrm);
+                wx *= 1.0 - eta;
+                if (x == j) wx += eta;
+                tx = inP ? fma(eta, Yd[j * P + x], (1.0 - eta) * tx) : 0.0;
+                sup = __ballot(wx > 0.0) & lanes;
+                ++steps;
+            }
+            if (inP) wf[x] = wx;
+            // ||sum_i w_i (v_i - mu)|| over the support, columns across lanes
+            double e2 = 0.0;
+            for (int c = lane; c < d; c += 64) {
+                double g = 0.0;
+                for (uint64_t m = sup; m; m &= m - 1) {
+                    const int i = __ffsll((unsigned long long)m) - 1;
+                    g = fma(wf[i], (double)Vs[i * pitch + c] - mu[c], g);
+                }
+                e2 = fma(g, g, e2);
+            }
+            e2 = wave_sum(e2);
+            // the geometric set: the support, then top-mass keys in rank order
+            uint64_t geo = sup;
+            for (int t = 0; t < s && __popcll(geo) < s; ++t) {
+                const int key = rank[t];
+                geo |= __ballot(inP && pid[x] == key) & lanes;
+            }
+            const double eg = wave_es(geo);
+            if (lane == 0) {
+                redd[3] = sqrt(e2);
+                redd[4] = eg;
+                redd[5] = (double)steps;
+                redm[3] = geo;
+            }
         }
         __syncthreads();
         const double es_top = redd[1], es_pool = redd[2];
+        const double ef_fw = redd[3], es_geo = redd[4], fw_steps = redd[5];
+        const uint64_t geo = redm[3];
         if (tid == 0) {
-            int t = 0, u = 0;
+            int t = 0, u = 0, v = 0;
             for (int i = 0; i < P; ++i) {
                 if (((best >> i) & 1ull) && t < s) a.best_idx[r * a.Stot + B.set_off + t++] = pid[i];
                 if (a.bal_idx && ((A >> i) & 1ull) && u < s) a.bal_idx[r * a.Stot + B.set_off + u++] = pid[i];
+                if (a.geo_idx && ((geo >> i) & 1ull) && v < s) a.geo_idx[r * a.Stot + B.set_off + v++] = pid[i];
             }
             if (a.n_swaps) a.n_swaps[b * R + r] = swaps;
             const double m = sc[b], sigma = sqrt(sc[nb]), D = sc[nb + 1];
@@ -522,6 +607,10 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
             o[9] = (float)sigma;
             o[10] = (float)(2.0 * D * m);
             o[11] = (float)(m < 1.0 ? sqrt(m / (1.0 - m)) * sigma : (double)INFINITY);
+            o[12] = (float)ef_fw;
+            o[13] = (float)es_geo;
+            o[14] = (float)ratio(es_pool, ef_fw);
+            o[15] = (float)fw_steps;
         }
         __syncthreads();  // the next budget overwrites the pool arrays
     }
@@ -615,7 +704,8 @@ size_t pool_ws_bytes(const fw_rows &rows, int nb, const int32_t *s, const int32_
 }
 
 hipError_t launch_pool(const fw_rows &rows, int nb, const int32_t *s, const int32_t *extra, int max_swaps,
-                       int32_t *pool_idx, int32_t *best_idx, int32_t *bal_idx, int32_t *n_swaps, float *stats,
+                       int fw_iters, int32_t *pool_idx, int32_t *best_idx, int32_t *bal_idx, int32_t *geo_idx,
+                       int32_t *n_swaps, float *stats,
                        float flat_threshold, float *cell_median, uint8_t *cell_flat, void *ws, hipStream_t st) {
     PoolPlan pp;
     if (!make_pool_plan(rows.n, (int)rows.d, nb, s, extra, &pp)) return hipErrorInvalidConfiguration;
@@ -639,6 +729,7 @@ hipError_t launch_pool(const fw_rows &rows, int nb, const int32_t *s, const int3
     a.d = (int)rows.d;
     a.nb = nb;
     a.max_swaps = max_swaps;
+    a.fw_iters = fw_iters;
     a.Smax = pp.Smax;
     a.Ptot = pp.Ptot;
     a.Stot = pp.Stot;
@@ -647,6 +738,7 @@ hipError_t launch_pool(const fw_rows &rows, int nb, const int32_t *s, const int3
     a.pool_idx = pool_idx;
     a.best_idx = best_idx;
     a.bal_idx = bal_idx;
+    a.geo_idx = geo_idx;
     a.n_swaps = n_swaps;
     a.stats = stats;
     const unsigned R = (unsigned)(rows.H * rows.G);

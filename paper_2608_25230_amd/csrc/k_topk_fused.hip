@@ -23,16 +23,9 @@
 // a one-row-per-workgroup fallback that selects by radix over the exact keys.
 #include "fw_internal.hpp"
 #include "select.hpp"
+#include "topk_fused.hpp"
 
 namespace fw {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef short s16x8 __attribute__((ext_vector_type(8)));
-typedef short s16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 namespace {
 constexpr int FR = 16;        // rows per workgroup
@@ -46,15 +39,6 @@ constexpr float LOG2E = 1.4426950408889634f;
 // keeps the scheduler from hoisting the work of every tile of an unrolled
 // per-logit loop at once (which exhausts the register file)
 #define FW_TILE_FENCE() __builtin_amdgcn_sched_barrier(0)
-
-// An opaque copy: the compiler may not assume it equals its input, so work
-// recomputed from it in a later pass is not merged with an earlier pass
-// (keeping hundreds of per-logit compare masks alive between passes).
-template <typename T>
-__device__ __forceinline__ T opaque(T x) {
-    asm volatile("" : "+v"(x));
-    return x;
-}
 
 constexpr int RING = 16384;   // bytes of streaming ring per wave
 constexpr int KD = 4;         // K tiles (16 keys x 128 d, 4 KiB) per ring
@@ -117,58 +101,7 @@ __device__ __forceinline__ float rsum4(float v) {
     return v + __shfl_xor(v, 32);
 }
 
-// Buffer loads: a per-unit descriptor (wave-uniform base and size, reads past
-// the size return zero), one 32-bit lane offset and a uniform offset, so the
-// unrolled tile loops keep no 64-bit address per tile in vector registers.
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-__device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
-}
-__device__ __forceinline__ bf16x8 bload8(rsrc_t r, uint32_t voff, uint32_t soff) {
-    return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
-}
-// Direct-to-LDS loads: lane l's 16 (or 4) bytes land at lds + 16 l (4 l); no
-// register is involved, so a wave can keep several tiles in flight.  The
-// compiler does not order these writes against later LDS reads: every
-// consumer waits explicitly (wait_vm) for the loads it needs.
-#define FW_LDS(p) ((__attribute__((address_space(3))) void *)(p))
-__device__ __forceinline__ void dma16(rsrc_t r, void *lds, uint32_t voff, uint32_t soff) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, FW_LDS(lds), 16, voff, soff, 0, 0);
-}
-__device__ __forceinline__ void dma4(rsrc_t r, void *lds, uint32_t voff, uint32_t soff) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, FW_LDS(lds), 4, voff, soff, 0, 0);
-}
-// wait until at most n vector memory operations of this wave are outstanding
-// (loads complete in issue order); n folds to a constant in unrolled loops
-#define FW_VM(k) case k: asm volatile("s_waitcnt vmcnt(" #k ")" ::: "memory"); break;
-__device__ __forceinline__ void wait_vm(int n) {
-    switch (n) {
-        FW_VM(0) FW_VM(1) FW_VM(2) FW_VM(3) FW_VM(4) FW_VM(5) FW_VM(6) FW_VM(7)
-        FW_VM(8) FW_VM(9) FW_VM(10) FW_VM(11) FW_VM(12) FW_VM(13) FW_VM(14) FW_VM(15)
-        FW_VM(16) FW_VM(17) FW_VM(18) FW_VM(19) FW_VM(20) FW_VM(21) FW_VM(22) FW_VM(23)
-        FW_VM(24) FW_VM(25) FW_VM(26) FW_VM(27) FW_VM(28)
-        default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
-    }
-}
-#undef FW_VM
-__device__ __forceinline__ void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-// Every barrier of the fused kernel separates LDS writes from LDS reads (the
-// direct-to-LDS loads are per wave and waited for by that wave), so it uses
-// lds_barrier: a full __syncthreads would also wait for every outstanding
-// global store of the wave, exposing write latency at each one.
 }  // namespace
-
-struct FusedArgs {
-    const uint16_t *q, *k, *v;
-    const float *scale, *bias;
-    int64_t H, G;
-    int n;
-    KsArg ks;
-    float *o, *o_s, *gap, *dropped;
-    unsigned long long *sel;  // [R][kmax] selected keys, when indices are requested
-    int kmax;
-    int32_t *flags, *flag_list, *flag_count;
-};
 
 // ---------------------------------------------------------------------------
 template <int TILES, int NK, bool BIAS, bool SEL>
@@ -878,9 +811,10 @@ fused_fixup_kernel(FusedArgs a, int32_t *topk_idx) {
     __shared__ int scan[256];
     __shared__ int sh[4];
     __shared__ float redf[256];
-    __shared__ float acc_s[NT][FD + 1];
-    __shared__ float mass_s[NT];
-    __shared__ unsigned long long sb[4096];
+    __shared__ float acc_s[2][NT][FD + 1];   // [key half][tier][column]
+    __shared__ float mass_s[2][NT];
+    __shared__ float qs[FD];
+    __shared__ unsigned long long sb[4096];   // weights and tiers, then the sort buffer
     const int tid = threadIdx.x;
     const int n = a.n;
     const int count = *a.flag_count;
@@ -891,10 +825,21 @@ fused_fixup_kernel(FusedArgs a, int32_t *topk_idx) {
         const uint16_t *qr = a.q + r * FD;
         const uint16_t *kh = a.k + h * (int64_t)n * FD;
         const uint16_t *vh = a.v + h * (int64_t)n * FD;
+        for (int c = tid; c < FD; c += 256) qs[c] = bf16_bits_to_f32(qr[c]);
+        __syncthreads();
         for (int j = tid; j < n; j += 256) {
+            // the key row in 16-byte pieces
+            const uint4 *kr = (const uint4 *)(kh + (int64_t)j * FD);
             float s = 0.f;
-            for (int c = 0; c < FD; ++c)
-                s = fmaf(bf16_bits_to_f32(qr[c]), bf16_bits_to_f32(kh[(int64_t)j * FD + c]), s);
+            for (int c8 = 0; c8 < FD / 8; ++c8) {
+                const uint4 x = kr[c8];
+                const uint32_t wd[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    s = fmaf(qs[8 * c8 + 2 * u], __uint_as_float(wd[u] << 16), s);
+                    s = fmaf(qs[8 * c8 + 2 * u + 1], __uint_as_float(wd[u] & 0xFFFF0000u), s);
+                }
+            }
             z[j] = sc * s + (a.bias ? a.bias[j] : 0.f);
         }
         __syncthreads();
@@ -911,41 +856,61 @@ fused_fixup_kernel(FusedArgs a, int32_t *topk_idx) {
             radix_select_desc(z, n, a.ks.k[kk], hist, sh, &key[kk], &rem);
             cut[kk] = nth_tie(z, n, key[kk], rem, scan, sh);
         }
-        if (tid < FD) {
+        // every key's weight and tier, then the tier sums: thread (column c,
+        // key half hh) over the keys of its half
+        float *pw = (float *)sb;
+        int *tw = (int *)(pw + 4096);
+        for (int j = tid; j < n; j += 256) {
+            const uint32_t u = ord_key(z[j]);
+            int tier = NK;
+            for (int kk = NK - 1; kk >= 0; --kk)
+                if (u > key[kk] || (u == key[kk] && j <= cut[kk])) tier = kk;
+            pw[j] = expf(z[j] - m) / l;
+            tw[j] = tier;
+        }
+        __syncthreads();
+        {
+            const int c = tid & (FD - 1), hh = tid / FD;
+            const int j0 = hh * (n / 2), j1 = hh ? n : n / 2;
             float accl[NT], ml[NT];
             for (int tt = 0; tt < NT; ++tt) { accl[tt] = 0.f; ml[tt] = 0.f; }
-            for (int j = 0; j < n; ++j) {
-                const uint32_t u = ord_key(z[j]);
-                int tier = NK;
-                for (int kk = NK - 1; kk >= 0; --kk)
-                    if (u > key[kk] || (u == key[kk] && j <= cut[kk])) tier = kk;
-                const float p = expf(z[j] - m) / l;
-                const float vv = bf16_bits_to_f32(vh[(int64_t)j * FD + tid]);
+            for (int j = j0; j < j1; ++j) {
+                const float p = pw[j];
+                const int tier = tw[j];
+                const float vv = bf16_bits_to_f32(vh[(int64_t)j * FD + c]);
+#pragma unroll
                 for (int tt = 0; tt < NT; ++tt)
                     if (tt == tier) { accl[tt] = fmaf(p, vv, accl[tt]); ml[tt] += p; }
             }
             for (int tt = 0; tt < NT; ++tt) {
-                acc_s[tt][tid] = accl[tt];
-                if (tid == 0) mass_s[tt] = ml[tt];
+                acc_s[hh][tt][c] = accl[tt];
+                if (c == 0) mass_s[hh][tt] = ml[tt];
             }
+        }
+        __syncthreads();
+        if (tid < FD) {
+            for (int tt = 0; tt < NT; ++tt) acc_s[0][tt][tid] += acc_s[1][tt][tid];
+        }
+        if (tid == 0) {
+            for (int tt = 0; tt < NT; ++tt) mass_s[0][tt] += mass_s[1][tt];
         }
         __syncthreads();
         if (tid < 64) {
             const int64_t R = a.H * a.G;
             float mtot = 0.f;
-            for (int tt = 0; tt < NT; ++tt) mtot += mass_s[tt];
+            for (int tt = 0; tt < NT; ++tt) mtot += mass_s[0][tt];
             for (int c = tid; c < FD; c += 64) {
                 float s = 0.f;
-                for (int tt = 0; tt < NT; ++tt) s += acc_s[tt][c];
+                for (int tt = 0; tt < NT; ++tt) s += acc_s[0][tt][c];
                 if (a.o) a.o[r * FD + c] = s / mtot;
             }
             for (int kk = 0; kk < NK; ++kk) {
                 float km = 0.f, rm = 0.f;
-                for (int tt = 0; tt < NT; ++tt) { if (tt <= kk) km += mass_s[tt]; else rm += mass_s[tt]; }
+                for (int tt = 0; tt < NT; ++tt) { if (tt <= kk) km += mass_s[0][tt]; else rm += mass_s[0][tt]; }
                 float ss = 0.f;
                 for (int c = tid; c < FD; c += 64) {
                     float kt = 0.f, rt2 = 0.f;
-                    for (int tt = 0; tt < NT; ++tt) { if (tt <= kk) kt += acc_s[tt][c]; else rt2 += acc_s[tt][c]; }
+                    for (int tt = 0; tt < NT; ++tt) { if (tt <= kk) kt += acc_s[0][tt][c]; else rt2 += acc_s[0][tt][c]; }
                     const float oS = kt / km;
                     if (a.o_s) a.o_s[((int64_t)a.ks.perm[kk] * R + r) * FD + c] = oS;
                     if (rm > 0.f) { const float df = rt2 / rm - oS; ss = fmaf(df, df, ss); }
@@ -1050,26 +1015,35 @@ hipError_t launch_fused_topk(const fw_rows &rows, const KsArg &ks, float *o, flo
     a.flag_list = (int32_t *)(base + align_up(R * 4, 256));
     a.flag_count = (int32_t *)(base + 2 * align_up(R * 4, 256));
     a.sel = topk_idx ? (unsigned long long *)(base + 2 * align_up(R * 4, 256) + 256) : nullptr;
-    hipLaunchKernelGGL(fused_clear_kernel, dim3(1), dim3(64), 0, st, a.flag_count);
+    launch_fused_clear(a.flag_count, st);
     const unsigned blocks = (unsigned)(R / FR);
     switch (ks.n) {
         case 1: launch_fused_nk<1>(a, blocks, st); break;
         case 2: launch_fused_nk<2>(a, blocks, st); break;
         default: launch_fused_nk<3>(a, blocks, st); break;
     }
+    launch_fused_finish(a, ks.n, topk_idx, st);
+    return hipGetLastError();
+}
+
+void launch_fused_clear(int32_t *flag_count, hipStream_t st) {
+    hipLaunchKernelGGL(fused_clear_kernel, dim3(1), dim3(64), 0, st, flag_count);
+}
+
+void launch_fused_finish(const FusedArgs &a, int nk, int32_t *topk_idx, hipStream_t st) {
+    const size_t R = (size_t)a.H * a.G;
     if (topk_idx) {
         int sort_len = 1;
-        while (sort_len < kmax) sort_len <<= 1;
+        while (sort_len < a.kmax) sort_len <<= 1;
         hipLaunchKernelGGL(fused_sort_kernel, dim3((unsigned)R), dim3(256), (size_t)sort_len * 8, st,
-                           (const unsigned long long *)a.sel, (const int32_t *)a.flags, kmax, sort_len,
+                           (const unsigned long long *)a.sel, (const int32_t *)a.flags, a.kmax, sort_len,
                            topk_idx);
     }
-    switch (ks.n) {
+    switch (nk) {
         case 1: hipLaunchKernelGGL(fused_fixup_kernel<1>, dim3(64), dim3(256), 0, st, a, topk_idx); break;
         case 2: hipLaunchKernelGGL(fused_fixup_kernel<2>, dim3(64), dim3(256), 0, st, a, topk_idx); break;
         default: hipLaunchKernelGGL(fused_fixup_kernel<3>, dim3(64), dim3(256), 0, st, a, topk_idx); break;
     }
-    return hipGetLastError();
 }
 
 }  // namespace fw

@@ -23,7 +23,7 @@ ENTRY_POINTS = ("fw_dense_topk", "fw_best_subset", "fw_swap", "fw_dropped_mass_c
 NOALLOC_ENTRY_POINTS = ("fw_dense_topk_noalloc",)
 # columns of fw_pool_subset's stats (FW_POOL_* in include/fw.h)
 POOL_STATS = ("es_top", "es_pool", "es_bal", "kappa_hat", "c_hat", "kappa_bal", "dropped", "phi",
-              "diam", "sigma", "bound_diam", "bound_var")
+              "diam", "sigma", "bound_diam", "bound_var", "ef_fw", "es_geo", "pi_hat", "fw_steps")
 
 
 class FwError(RuntimeError):
@@ -59,7 +59,7 @@ _SIGS = {
     "fw_ragged_compact": (I32, [I32, P, P, I64, I64, I64, I64, P, I64, I32, I64, P, P, P, P, P, P, P,
                                 P, SZ, P]),
     "fw_pool_subset_workspace_size": (SZ, [RP, I32, P, P]),
-    "fw_pool_subset": (I32, [RP, I32, P, P, I32, P, P, P, P, P, ctypes.c_float, P, P, P, SZ, P]),
+    "fw_pool_subset": (I32, [RP, I32, P, P, I32, I32, P, P, P, P, P, P, ctypes.c_float, P, P, P, SZ, P]),
     "fw_group_vote_workspace_size": (SZ, [RP, I32, I32]),
     "fw_group_vote": (I32, [RP, I32, I32, P, P, P, P, P, SZ, P]),
     "fw_last_error": (ctypes.c_char_p, []),
@@ -224,12 +224,12 @@ def swap(q, k, v, kb: int, max_iters: int, scale=None, bias=None, *, ws=None) ->
 
 
 def pool_subset(q, k, v, budgets: Sequence, max_swaps: int, scale=None, bias=None, *,
-                flat_threshold: float = 0.25, want_cells=True, ws=None) -> Dict[str, object]:
+                fw_iters: int = 64, flat_threshold: float = 0.25, want_cells=True, ws=None) -> Dict[str, object]:
     """budgets: a sequence of (s, extra).  Returns, per budget b (lists in the
-    same order): pool_idx[b] [H][G][s+extra], best_idx[b] and bal_idx[b]
-    [H][G][s] (views of the concatenated per-row lists the library writes),
-    and stacked n_swaps [nb][H][G], stats [nb][H][G][12], cell_median and
-    cell_flat [nb][H]."""
+    same order): pool_idx[b] [H][G][s+extra], best_idx[b], bal_idx[b] and
+    geo_idx[b] [H][G][s] (views of the concatenated per-row lists the library
+    writes), and stacked n_swaps [nb][H][G], stats [nb][H][G][16] (columns
+    POOL_STATS), cell_median and cell_flat [nb][H]."""
     torch = _torch()
     rows = _rows(q, k, v, scale, bias)
     H, G = rows.H, rows.G
@@ -242,6 +242,7 @@ def pool_subset(q, k, v, budgets: Sequence, max_swaps: int, scale=None, bias=Non
     pool = torch.empty((H, G, Ptot), dtype=torch.int32, device=dev)
     best = torch.empty((H, G, Stot), dtype=torch.int32, device=dev)
     bal = torch.empty((H, G, Stot), dtype=torch.int32, device=dev)
+    geo = torch.empty((H, G, Stot), dtype=torch.int32, device=dev)
     out = {"n_swaps": torch.empty((nb, H, G), dtype=torch.int32, device=dev),
            "stats": torch.empty((nb, H, G, len(POOL_STATS)), dtype=torch.float32, device=dev),
            "cell_median": torch.empty((nb, H), dtype=torch.float32, device=dev) if want_cells else None,
@@ -250,16 +251,18 @@ def pool_subset(q, k, v, budgets: Sequence, max_swaps: int, scale=None, bias=Non
     need = L.fw_pool_subset_workspace_size(ctypes.byref(rows), nb, sv, ev)
     if ws is None or ws.numel() < need:
         ws = _workspace(need, dev)
-    _check(L.fw_pool_subset(ctypes.byref(rows), nb, sv, ev, max_swaps, pool.data_ptr(), best.data_ptr(),
-                            bal.data_ptr(), _ptr(out["n_swaps"]), _ptr(out["stats"]), float(flat_threshold),
+    _check(L.fw_pool_subset(ctypes.byref(rows), nb, sv, ev, max_swaps, fw_iters, pool.data_ptr(), best.data_ptr(),
+                            bal.data_ptr(), geo.data_ptr(), _ptr(out["n_swaps"]), _ptr(out["stats"]),
+                            float(flat_threshold),
                             _ptr(out["cell_median"]), _ptr(out["cell_flat"]), ws.data_ptr(), ws.numel(),
                             _stream()))
     po = so = 0
-    out["pool_idx"], out["best_idx"], out["bal_idx"] = [], [], []
+    out["pool_idx"], out["best_idx"], out["bal_idx"], out["geo_idx"] = [], [], [], []
     for s_, e_ in budgets:
         out["pool_idx"].append(pool[..., po:po + s_ + e_])
         out["best_idx"].append(best[..., so:so + s_])
         out["bal_idx"].append(bal[..., so:so + s_])
+        out["geo_idx"].append(geo[..., so:so + s_])
         po += s_ + e_
         so += s_
     out["_ws"] = ws

@@ -196,16 +196,18 @@ def shifted_key_rows(wid: int, seed: int, R: int, n: int, d: int,
 
 def window_rows(wid: int, seed: int, H: int, G: int, n: int, d: int,
                 dtype: str = BF16, t_lo: float = 0.5, t_hi: float = 2.0,
-                with_v: bool = True) -> Rows:
+                with_v: bool = True, first: int = 0) -> Rows:
     """Observation-window queries per cell with a per-cell temperature
-    T ~ U[t_lo, t_hi]; scale = 1/(sqrt(d)*T) (T < 1 sharpens the head)."""
+    T ~ U[t_lo, t_hi]; scale = 1/(sqrt(d)*T) (T < 1 sharpens the head).
+    Cells first .. first + H - 1 of the seeded sequence (each cell has its own
+    stream, so any cell can be drawn alone)."""
     q = np.empty((H, G, d), np.uint16 if dtype == BF16 else np.float32)
     k = np.empty((H, n, d), q.dtype)
     v = np.empty((H, n, d), q.dtype) if with_v else None
     temp = np.empty(H, np.float64)
 
     def one(h):
-        rng = _rng(wid, seed, h)
+        rng = _rng(wid, seed, first + h)
         temp[h] = rng.uniform(t_lo, t_hi)
         q[h] = _draw(rng, (G, d), dtype)
         k[h] = _draw(rng, (n, d), dtype)

@@ -47,3 +47,19 @@ class Tally:
 
     def __repr__(self):
         return f"exact={self.exact} ties={self.ties} fail={self.fail} {self.notes[:3]}"
+
+
+# test name -> what it measured (worst relative errors, tallies); written out
+# at the end of the session by tests/conftest.py
+SUMMARY = {}
+
+
+def record(name, **values):
+    SUMMARY[name] = {k: (v if not isinstance(v, Tally) else dict(exact=v.exact, ties=v.ties, fail=v.fail))
+                     for k, v in values.items()}
+
+
+def same_bits(a, b) -> bool:
+    """Two results are bitwise identical (NaNs included)."""
+    a, b = np.ascontiguousarray(a), np.ascontiguousarray(b)
+    return a.shape == b.shape and a.dtype == b.dtype and a.tobytes() == b.tobytes()

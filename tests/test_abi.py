@@ -167,10 +167,10 @@ def test_maxpool_validation(L):
 
 def test_pool_subset_validation(L):
     r = _rows(n=64, d=8)
-    def call(rows, s=(4,), e=(8,), ms=4, best=1, stats=1, ws=1, wsb=1 << 40, nb=None):
+    def call(rows, s=(4,), e=(8,), ms=4, best=1, stats=1, ws=1, wsb=1 << 40, nb=None, fwi=16):
         sv, ev = _ks(*s), _ks(*e)
-        return L.fw_pool_subset(rows, len(s) if nb is None else nb, sv, ev, ms, None, best, None, None, stats,
-                                0.25, None, None, ws, wsb, None)
+        return L.fw_pool_subset(rows, len(s) if nb is None else nb, sv, ev, ms, fwi, None, best, None, None, None,
+                                stats, 0.25, None, None, ws, wsb, None)
     assert call(None) == 1
     assert call(ctypes.byref(_rows(dtype=7))) == 3
     assert call(ctypes.byref(_rows(v=None))) == 1
@@ -179,6 +179,8 @@ def test_pool_subset_validation(L):
     assert call(ctypes.byref(_rows(n=6))) == 2                # s + extra > n
     assert call(ctypes.byref(r), ms=-1) == 2
     assert call(ctypes.byref(r), ms=5000) == 2
+    assert call(ctypes.byref(r), fwi=-1) == 2
+    assert call(ctypes.byref(r), fwi=5000) == 2
     assert call(ctypes.byref(r), s=(4, 8), e=(8, 4), nb=0) == 2
     assert call(ctypes.byref(r), s=(1,) * 5, e=(1,) * 5) == 2   # more than FW_POOL_MAX_BUDGETS
     assert call(ctypes.byref(_rows(n=200)), s=(40,), e=(30,)) == 4   # more than 64 pool keys

@@ -8,7 +8,8 @@ import pytest
 
 from oracle import fw_oracle as O
 from paper_2608_25230_amd import workloads as W
-from tests.parity import TOL, rel_vec, t2np
+from tests import parity_workers as PW
+from tests.parity import TOL, record, rel_vec, same_bits, t2np
 
 pytestmark = pytest.mark.gpu
 
@@ -178,11 +179,21 @@ def test_full_size_curve_and_compact(torch_fw):
     wl = W.curve_ragged(seed=0)
     rows = wl.rows
     dev, out = _curve(torch, fw, rows)
+    _, out2 = _curve(torch, fw, rows, dev)
+    for key in out:  # a second call gives the same bits
+        assert same_bits(out[key], out2[key]), key
     _check_curve(rows, out, [0, 137])
     assert np.allclose(out["curve"][:, 0], 1.0, atol=1e-4)
     imp_t = torch.from_numpy(out["importance"]).cuda()
     co = fw.ragged_compact(dev["k"], dev["v"], imp_t, wl.budget, wl.floor, wl.heads_per_layer)
+    co2 = fw.ragged_compact(dev["k"], dev["v"], imp_t, wl.budget, wl.floor, wl.heads_per_layer)
     torch.cuda.synchronize()
+    for key in ("offsets", "kept_pos", "k_out", "v_out", "tau", "dropped", "bytes_held"):
+        x, y = co[key], co2[key]
+        if x.dtype == torch.bfloat16:
+            x, y = x.view(torch.int16), y.view(torch.int16)
+        assert same_bits(t2np(x), t2np(y)), key
+    del co2
     offsets = t2np(co["offsets"])
     a = O.allocate(out["importance"].astype(np.float64), wl.budget, wl.floor)
     want = np.concatenate([[0], np.cumsum(a["counts"])])
@@ -200,6 +211,25 @@ def test_full_size_curve_and_compact(torch_fw):
     assert bh[0] == wl.budget * 2 * 128 * 2 and bh[2] == rows.H * rows.n * 2 * 128 * 2
     assert bh[0] <= bh[1] <= bh[2]
     print("bytes held ragged/padded/full:", bh.tolist(), "tau", t2np(co["tau"])[0])
+    # stage 2: against the allocation of the oracle's own float64 scores, the
+    # kept sets may differ only at entries whose score is within tolerance of
+    # the threshold
+    jobs = [(5, 0, h, rows.G, rows.n, rows.d) for h in range(rows.H)]
+    r_or = np.stack(PW.pool_map(PW.importance_cell, jobs))
+    a2 = O.allocate(r_or, wl.budget, wl.floor)
+    keep = np.zeros((rows.H, rows.n), bool)
+    for h in range(rows.H):
+        keep[h, kept[offsets[h]:offsets[h + 1]]] = True
+    diff = keep ^ a2["keep"]
+    tau = a2["tau"]
+    near = np.abs(r_or - tau) <= TOL[rows.dtype] * tau
+    far = int(np.count_nonzero(diff & ~near))
+    worst_imp = float(max(rel_vec(out["importance"][h], r_or[h]) for h in range(rows.H)))
+    record("allocation_full_size_stage2", differing_entries=int(diff.sum()), beyond_tolerance=far,
+           tau=float(tau), worst_importance_rel=worst_imp)
+    print("stage 2: entries kept differently", int(diff.sum()), "beyond tolerance of tau", far)
+    assert far == 0
+    assert worst_imp <= TOL[rows.dtype]
 
 
 @pytest.mark.parametrize("kernel", [1, 3, 7])

@@ -4,7 +4,8 @@ import pytest
 
 from oracle import fw_oracle as O
 from paper_2608_25230_amd import workloads as W
-from tests.parity import TOL, Tally, rel_scalar, t2np
+from tests import parity_workers as PW
+from tests.parity import TOL, Tally, record, same_bits, t2np
 
 pytestmark = pytest.mark.gpu
 
@@ -26,32 +27,38 @@ def _run(torch, fw, rows, k, iters):
     return {key: t2np(val) for key, val in out.items() if not key.startswith("_")}
 
 
-def _check(rows, k, iters, out, cells, method="auto"):
+def _check(rows, k, iters, out, cells, method="auto", min_exact=0.75, name=None):
+    """Each row of `cells` against the oracle's balancing selector, classified
+    at the first step where the two trajectories could part (see
+    tests.parity_workers.classify_swap); properties of the GPU's outputs on
+    every listed row.  At least `min_exact` of the rows must follow the
+    oracle exactly, and none may fail."""
     tol = TOL[rows.dtype]
-    q, K, V = rows.as_f64("q"), rows.as_f64("k"), rows.as_f64("v")
+    q, K = rows.as_f64("q"), rows.as_f64("k")
     bias = None if rows.bias is None else rows.bias.astype(np.float64)
-    tally = Tally()
+    if method == "auto":
+        method = "direct" if rows.n <= 32 else "gform"
+    jobs = []
     for h, g in cells:
         z = O.logits(q[h, g], K[h], float(rows.scale[h]), bias)
-        p = O.weights(z)
-        S, traj, ns = O.swap_rule(p, V[h], k, iters, start=O.top_mass_set(z, k), method=method)
         gs = out["s_idx"][h, g]
-        gt = out["gap_traj"][h, g]
+        gt = out["gap_traj"][h, g].astype(np.float64)
         gn = int(out["n_swaps"][h, g])
         assert np.all(np.diff(gs) > 0)
-        # the trajectory is the float64 es of each accepted set
-        es_final_gpu = O.forced_error(p, V[h], gs)
-        assert rel_scalar(gt[gn], es_final_gpu, 1e-9) <= tol
-        assert rel_scalar(gt[0], traj[0], 1e-9) <= tol
         assert np.all(np.diff(gt[: gn + 1]) < 0)
         assert np.all(np.isnan(gt[gn + 1:]))
-        exact = np.array_equal(gs, S) and gn == ns
-        if exact:
-            assert np.allclose(gt[: gn + 1], traj[: ns + 1], rtol=tol)
-        tie = abs(es_final_gpu - traj[ns]) <= tol * traj[ns] + 1e-12
-        tally.add(exact, tie, f"{(h, g)} gpu {gn} swaps es {es_final_gpu:.6g}, oracle {ns} es {traj[ns]:.6g}")
-        assert abs(out["dropped"][h, g] - O.dropped_mass(p, gs)) <= tol * max(O.dropped_mass(p, gs), 1e-6)
+        p = O.weights(z)
+        dref = O.dropped_mass(p, gs)
+        assert abs(out["dropped"][h, g] - dref) <= tol * max(dref, 1e-6)
+        jobs.append((z, rows.v[h], k, iters, gs, gt, gn, method, PW.SWAP_REL[rows.dtype]))
+    res = [PW.classify_swap(j) for j in jobs] if len(jobs) <= 4 else PW.pool_map(PW.classify_swap, jobs)
+    tally = Tally()
+    for (h, g), (st, note) in zip(cells, res):
+        tally.add(st == "exact", st == "tie", f"{(h, g)}: {note}")
     assert tally.fail == 0, tally
+    assert tally.exact >= min_exact * len(cells), tally
+    if name:
+        record(name, rows=len(cells), tally=tally)
     return tally
 
 
@@ -72,7 +79,8 @@ def test_tiny_rows_all(torch_fw):
     torch, fw = torch_fw
     wl = W.tiny_exhaustive(seed=0)
     out = _run(torch, fw, wl.rows, wl.k, 64)
-    t = _check(wl.rows, wl.k, 64, out, [(h, 0) for h in range(wl.rows.H)], method="direct")
+    t = _check(wl.rows, wl.k, 64, out, [(h, 0) for h in range(wl.rows.H)], method="direct",
+               name="swap_tiny_all_rows")
     print("tiny swap:", t)
 
 
@@ -93,7 +101,8 @@ def test_long_rows_bf16(torch_fw, shape):
     k, it = shape["k"], shape["max_iters"]
     out = _run(torch, fw, wl.rows, k, it)
     cells = [(h, g) for h in range(wl.rows.H) for g in range(wl.rows.G)]
-    t = _check(wl.rows, k, it, out, cells, method="gform")
+    t = _check(wl.rows, k, it, out, cells, method="gform",
+               name="swap_long_rows_n%d_d%d_k%d" % (shape["n"], shape["d"], shape["k"]))
     print(shape, t)
 
 
@@ -110,12 +119,17 @@ def test_long_rows_fp32_and_zero_iters(torch_fw):
 
 def test_full_size_swap_sampled(torch_fw):
     """8 kv units x 128 rows, n = 32768, k = 1024, up to 64 swaps, in the
-    benchmark's launch configuration; two rows against the oracle, properties
-    on all rows."""
+    benchmark's launch configuration; two rows of every unit (16 rows, one of
+    each of the first and the last query head) against the oracle step by
+    step, properties on all rows."""
     torch, fw = torch_fw
     wl = W.swap_long_rows(seed=0)
     out = _run(torch, fw, wl.rows, wl.k, wl.max_iters)
-    t = _check(wl.rows, wl.k, wl.max_iters, out, [(0, 0), (5, 77)], method="gform")
+    out2 = _run(torch, fw, wl.rows, wl.k, wl.max_iters)
+    for key in out:  # a second call gives the same bits
+        assert same_bits(out[key], out2[key]), key
+    cells = [(h, g) for h in range(wl.rows.H) for g in (3 + 5 * h, wl.rows.G - 1 - 7 * h)]
+    t = _check(wl.rows, wl.k, wl.max_iters, out, cells, method="gform", name="swap_full_size_16_rows")
     print("full-size swap sampled:", t, "swaps: median", np.median(out["n_swaps"]),
           "max", out["n_swaps"].max())
     gt = out["gap_traj"]
@@ -131,7 +145,8 @@ def test_long_rows_tied_pairs_fall_back_to_full_sweep(torch_fw):
     """Uniform weights over keys whose values repeat 8 distinct rows: every
     pair of the same two value kinds ties, so thousands of pairs survive the
     pruned search's lower bound and the row falls back to the full sweep.
-    The sets must still match the oracle (ties to the smaller (i, j))."""
+    Rows whose oracle path meets a float64 tie may take another tied pair;
+    every step must still take a best swap."""
     torch, fw = torch_fw
     rng = np.random.default_rng(11)
     n, d, k = 2048, 128, 512
@@ -142,6 +157,6 @@ def test_long_rows_tied_pairs_fall_back_to_full_sweep(torch_fw):
     rows = W.Rows("bf16", W.bf16_bits(q), W.bf16_bits(K), W.bf16_bits(V),
                   np.full(1, 1.0 / np.sqrt(d), np.float32))
     out = _run(torch, fw, rows, k, 4)
-    t = _check(rows, k, 4, out, [(0, 0), (0, 1)], method="gform")
+    t = _check(rows, k, 4, out, [(0, 0), (0, 1)], method="gform", min_exact=0.0, name="swap_tied_pairs")
     assert np.all(out["n_swaps"] >= 1)
     print("tied pairs:", t)
