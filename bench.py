@@ -72,6 +72,12 @@ def _stat(holder, b, name):
     return holder["stats"][b, ..., fw.POOL_STATS.index(name)].flatten().double()
 
 
+def _progress(msg):
+    """One line on stderr when a piece of the run ends (the JSON result is the
+    only line on stdout)."""
+    print("bench: " + msg, file=sys.stderr, flush=True)
+
+
 def _roofline(bound, achieved, peak, unit, traffic=None):
     return {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": unit,
             "frac": round(achieved / peak, 4), "traffic": traffic}
@@ -235,11 +241,13 @@ def cpu_configs(seconds):
     out["configs"].append({"config": 1, "workload": wl.name, "sample": f"all {done} rows", "wall_s": round(wall, 2),
                            "rows_per_s": round(done / wall, 1),
                            "subsets_per_s": round(done * math.comb(r.n, wl.k) / wall, 1)})
+    _progress("cpu config %d done" % out["configs"][-1]["config"])
 
     # 2. streaming top-k: the headline's own leg
     wl = W.streaming_topk(seed=0)
     b = cpu_baseline(wl, seconds)
     out["configs"].append({"config": 2, "workload": wl.name, "sample": b["sample"], "rows_per_s": b["value"]})
+    _progress("cpu config %d done" % out["configs"][-1]["config"])
 
     # 3. exhaustive: a sample of rows, sized from a calibration row
     wl = W.exhaustive_rows(seed=0, rows=cores * 64)
@@ -254,6 +262,7 @@ def cpu_configs(seconds):
                            "sample": f"the first {done} of 168192 rows", "wall_s": round(wall, 2),
                            "rows_per_s": round(done / wall, 2),
                            "subsets_per_s": round(done * math.comb(r.n, wl.k) / wall, 1)})
+    _progress("cpu config %d done" % out["configs"][-1]["config"])
 
     # 4. swap rule on long rows: a sample of rows, a bounded number of swaps
     wl = W.swap_long_rows(seed=0)
@@ -268,6 +277,7 @@ def cpu_configs(seconds):
                            "sample": f"{cores} rows (one per core) with at most {iters} swaps each, {sweeps} sweeps",
                            "wall_s": round(wall, 2), "pairs_per_s": round(sweeps * wl.k * (r.n - wl.k) / wall, 1),
                            "sweeps_per_s": round(sweeps / wall, 3)})
+    _progress("cpu config %d done" % out["configs"][-1]["config"])
 
     # 5. curve: a sample of cells (window importance, sort, suffix sums)
     # (cells are seeded one by one, so the first cells of a smaller call are
@@ -280,6 +290,7 @@ def cpu_configs(seconds):
     out["configs"].append({"config": 5, "workload": "curve_ragged_L32_kv8_n131072",
                            "sample": f"the first {done} of 256 cells (importance and curve)",
                            "wall_s": round(wall, 2), "cells_per_s": round(done / wall, 3)})
+    _progress("cpu config %d done" % out["configs"][-1]["config"])
     return out
 
 
@@ -325,8 +336,23 @@ def main():
         outb = R * r.d * 4 * (1 + len(wl.ks)) + 2 * len(wl.ks) * R * 4
         alg = kv + qb + outb
         head = dict(wl=wl, ms=ms, R=R, alg_bytes=alg, wall=wall, mean=sum(per) / len(per), lo=per[0], hi=per[-1])
+
+        # the same step with the rank-ordered top-k indices of the largest
+        # budget as a further output (int32 [rows][kmax])
+        def step_idx():
+            out = fw.dense_topk(dev["q"], dev["k"], dev["v"], wl.ks, dev["scale"], dev["bias"], ws=ws[0])
+            ws[0] = out["_ws"]
+
+        ms_i, _, _ = _time(torch, step_idx, a.steps, a.warmup)
+        alg_i = alg + R * max(wl.ks) * 4
+        components.append({"workload": wl.name + "_with_topk_idx", "metric": "attention rows/s (top-k gap)",
+                           "value": round(R / (ms_i / 1e3), 1), "unit": "rows/s", "ms": round(ms_i, 4),
+                           "outputs": "o, o_S, gap, dropped, topk_idx", "algorithmic_bytes": alg_i,
+                           "roofline": _roofline("hbm", alg_i / (ms_i / 1e3) / 1e9, HBM_PEAK_GBS, "GB/s"),
+                           "dtype": "bf16"})
         del dev, ws
         torch.cuda.empty_cache()
+        _progress("%s done" % wl.name)
 
     # ---- exhaustive best subset ------------------------------------------------
     if want("exhaustive"):
@@ -357,6 +383,7 @@ def main():
                            "d_dim_equivalent_tflops": round(sps * (3 * r.d + 6) / 1e12, 1)})
         del dev, ws
         torch.cuda.empty_cache()
+        _progress("%s done" % wl.name)
 
     # ---- swap rule --------------------------------------------------------------
     if want("swap"):
@@ -399,6 +426,7 @@ def main():
                            "dense_sweep_equivalent_tflops": round(dense_flop / (ms / 1e3) / 1e12, 1)})
         del dev, holder
         torch.cuda.empty_cache()
+        _progress("%s done" % components[-1]["workload"])
 
     # ---- candidate-set search (ES_pool, pool balancing, certificate) -------------
     if want("pool"):
@@ -442,6 +470,7 @@ def main():
                            "dtype": "f64"})
         del dev, holder
         torch.cuda.empty_cache()
+        _progress("%s done" % components[-1]["workload"])
 
     # ---- candidate-set search with the widened enumeration cap ---------------------
     if want("poolcap"):
@@ -470,6 +499,7 @@ def main():
                            "dtype": "f64"})
         del dev, holder
         torch.cuda.empty_cache()
+        _progress("%s done" % components[-1]["workload"])
 
     # ---- group vote ------------------------------------------------------------------
     if want("vote"):
@@ -498,6 +528,7 @@ def main():
                            "dtype": "f64"})
         del dev, holder
         torch.cuda.empty_cache()
+        _progress("%s done" % components[-1]["workload"])
 
     # ---- dropped-mass curve + ragged compaction --------------------------------
     if want("curve"):
@@ -525,6 +556,7 @@ def main():
                            "roofline": _roofline("hbm", alg / (ms / 1e3) / 1e9, HBM_PEAK_GBS, "GB/s")})
         del dev, holder
         torch.cuda.empty_cache()
+        _progress("%s done" % components[-1]["workload"])
 
     # ---- tiny exhaustive ------------------------------------------------------------
     if want("tiny"):
@@ -542,6 +574,7 @@ def main():
         components.append({"workload": wl.name, "metric": "subsets evaluated/s",
                            "value": round(subsets / (ms / 1e3), 1), "unit": "subsets/s",
                            "ms": round(ms, 4), "dtype": "f64", "note": "launch-bound"})
+        _progress("%s done" % wl.name)
 
     # ---- plain device copy (calibrates the HBM byte counters) -------------------
     if want("copy"):
@@ -553,6 +586,7 @@ def main():
                            "value": round(2 * nbytes / (ms / 1e3) / 1e9, 1), "unit": "GB/s",
                            "ms": round(ms, 4), "bytes_read": nbytes, "bytes_written": nbytes})
         del src, dst
+        _progress("copy done")
 
     if head is None:
         print(json.dumps({"components": components}))
@@ -581,6 +615,7 @@ def main():
     }
     if not a.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, a.cpu_seconds)
+        _progress("cpu baseline done")
     print(json.dumps(line))
 
 

@@ -96,7 +96,7 @@ __host__ __device__ inline bool plan_for(int n, int k, int m, EnumPlan *P, doubl
     return true;
 }
 
-__host__ inline bool choose_plan(int64_t n, int k, EnumPlan *out) {
+__host__ inline bool choose_plan(int64_t n, int k, EnumPlan *out, double *cost_out = nullptr) {
     bool found = false;
     double best = 0.0;
     for (int m = 1; m <= (int)n; ++m) {
@@ -109,6 +109,7 @@ __host__ inline bool choose_plan(int64_t n, int k, EnumPlan *out) {
             found = true;
         }
     }
+    if (found && cost_out) *cost_out = best;
     return found;
 }
 

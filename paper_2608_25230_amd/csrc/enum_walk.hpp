@@ -14,6 +14,17 @@
 // (S / p^2 from the Gram, ties to the lexicographically smaller set), lower
 // beta for the wave and rescale e.  Work items (h, a run of up to 64 owned
 // parts) are taken by the waves of the workgroup from a shared counter.
+//
+// With `cpl` the plan enumerates the dropped sets D (k = n - s keys) and the
+// scored set is the complement A = U \ D.  With c_x = sum_y Gm_xy and
+// D = O + W:
+//     S(A) = S_U - 2 c(D) + S(D),   p(A) = p_U - p(D),
+// so the test keeps the same linear form in the walked keys:
+//     S(A) - beta p(A)^2 = K1 + sum_{x in W} e[x] + S_W - beta p(W)^2,
+//     K1 = S_U - 2 c(O) + S_O - beta (p_U - p_O)^2,
+//     e[x] = 2 sum_{a in O} Gm_xa - 2 c_x + 2 beta (p_U - p_O) p_x,
+// and the walk itself is unchanged: pools that drop a few keys of many walk
+// small dropped sets instead of owning large kept parts.
 #pragma once
 
 #include "enum_plan.hpp"
@@ -30,11 +41,19 @@ template <int WMAX>
 __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const double *Gm, const double *ps, uint64_t seed_mask,
                                      const uint2 *__restrict__ g_io, const uint64_t *__restrict__ g_wmk,
                                      const EnumJob *__restrict__ g_jobs, const uint64_t *__restrict__ g_omk,
-                                     double2 *ent, double *PLt, double *redd, uint64_t *redm, int *ctr) {
+                                     double2 *ent, double *PLt, double *redd, uint64_t *redm, int *ctr,
+                                     bool cpl = false, double *cv = nullptr) {
     const int NT = blockDim.x;
     const int gp = pl.gp;
     const int tid = threadIdx.x, lane = tid & 63;
     const uint64_t top_mask = seed_mask;
+    const uint64_t allm = pl.n == 64 ? ~0ull : (1ull << pl.n) - 1ull;
+    if (cpl)  // Gram row sums c_x (LDS; written before the barrier below)
+        for (int x = tid; x < pl.n; x += NT) {
+            double c = 0.0;
+            for (int y = 0; y < pl.n; ++y) c += Gm[x * gp + y];
+            cv[x] = c;
+        }
     // per-row walk tables
     for (int t = tid; t < pl.nent; t += NT) {
         const uint64_t lm = g_wmk[t];
@@ -54,6 +73,12 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
     }
     if (tid == 0) ctr[0] = 0;
     __syncthreads();
+    double SU = 0.0, PU = 0.0;  // S and p of every key (complement walks)
+    if (cpl)
+        for (int x = 0; x < pl.n; ++x) {
+            SU += cv[x];
+            PU += ps[x];
+        }
 
     // seed: the top-k set, scored from the Gram
     double S_top = 0.0, P_top = 0.0;
@@ -77,7 +102,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
         // owned part of this lane (precomputed key mask; 0 on idle lanes):
         // p(O), S(O) and E[x] = sum_{a in O} Gm_{a, wb + x} over the walked range
         const uint64_t Om = g_omk[(size_t)jn * 64 + lane];
-        double PO = 0.0, SO = 0.0;
+        double PO = 0.0, SO = 0.0, CO = 0.0;
         double e[WMAX];
 #pragma unroll
         for (int x = 0; x < WMAX; ++x) e[x] = 0.0;
@@ -96,6 +121,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                 if (i < ls) {
                     const double *ri = Gm + kx[i] * gp;
                     PO += ps[kx[i]];
+                    if (cpl) CO += cv[kx[i]];
                     double sv = ri[kx[i]];
 #pragma unroll
                     for (int j = 0; j < i; ++j) sv = fma(2.0, ri[kx[j]], sv);
@@ -112,6 +138,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
             for (uint64_t a = Om; a; a &= a - 1) {
                 const int x = __ffsll((unsigned long long)a) - 1;
                 PO += ps[x];
+                if (cpl) CO += cv[x];
                 const double *row = Gm + x * gp;
                 for (uint64_t b2 = Om; b2; b2 &= b2 - 1) SO += row[__ffsll((unsigned long long)b2) - 1];
                 if (ws > 0) {
@@ -120,10 +147,20 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                 }
             }
         }
+        // the base (S, p) of the scored set before the walked keys, and the
+        // sign of the walked keys' masses in p
+        const double PB = cpl ? PU - PO : PO;
+        const double SB = cpl ? SU - 2.0 * CO + SO : SO;
+        const double sgn = cpl ? 1.0 : -1.0;
         if (ws > 0) {
-            const double b2p = 2.0 * beta * PO;
+            const double b2p = sgn * 2.0 * beta * PB;
+            if (cpl) {
 #pragma unroll
-            for (int x = 0; x < WMAX; ++x) e[x] = fma(2.0, e[x], -b2p * ps[wb + x]);
+                for (int x = 0; x < WMAX; ++x) e[x] = fma(2.0, e[x], fma(b2p, ps[wb + x], -2.0 * cv[wb + x]));
+            } else {
+#pragma unroll
+                for (int x = 0; x < WMAX; ++x) e[x] = fma(2.0, e[x], b2p * ps[wb + x]);
+            }
         }
         const double2 *en = ent + C.toff;
         const double *plt = PLt + C.toff;
@@ -132,16 +169,18 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
         // exact score of walk step t for this lane (a candidate)
         auto exact = [&](int t) __attribute__((always_inline)) {
             const uint64_t wm = wmk[t];
-            double S = SO + en[t].x;
+            double S = SB + en[t].x;
             for (uint64_t a = wm; a; a &= a - 1) {
-                const double *row = Gm + (__ffsll((unsigned long long)a) - 1) * gp;
+                const int ax = __ffsll((unsigned long long)a) - 1;
+                const double *row = Gm + ax * gp;
                 double E = 0.0;
                 for (uint64_t b2 = Om; b2; b2 &= b2 - 1) E += row[__ffsll((unsigned long long)b2) - 1];
                 S += 2.0 * E;
+                if (cpl) S -= 2.0 * cv[ax];
             }
-            const double P = PO + plt[t];
+            const double P = cpl ? PB - plt[t] : PO + plt[t];
             const double val = S / (P * P);
-            const uint64_t mask = Om | wm;
+            const uint64_t mask = cpl ? (allm & ~(Om | wm)) : (Om | wm);
             if (val < best_val || (val == best_val && lex_less(mask, best_mask))) {
                 best_val = val;
                 best_mask = mask;
@@ -193,17 +232,17 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                     const double dB = lower_beta();
 #pragma unroll
                     for (int x = 0; x < WMAX; ++x)
-                        e[x] -= 2.0 * dB * PO * ps[wb + x];
+                        e[x] += sgn * 2.0 * dB * PB * ps[wb + x];
                 }
             };
             if (ws == 0) {
-                const double YO = act ? SO - beta * PO * PO : INFINITY;
+                const double YO = act ? SB - beta * PB * PB : INFINITY;
                 if (__ballot(YO <= thr)) {
                     if (YO <= thr) exact(0);
                     lower_beta();  // nothing is walked: e is unused
                 }
             } else if (ws == 1) {
-                run(act ? SO - beta * PO * PO : INFINITY, 0, wn);
+                run(act ? SB - beta * PB * PB : INFINITY, 0, wn);
             } else {
                 // Walked pairs {i < j} below a limit L, after an outer base B
                 // (walked triples {i < j < l}: one block per l with
@@ -218,7 +257,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
 #pragma unroll
                         for (int x = 2; x < WMAX; ++x) el = l == x ? e[x] : el;
                     }
-                    const double B = act ? SO - beta * PO * PO + el : INFINITY;
+                    const double B = act ? SB - beta * PB * PB + el : INFINITY;
                     const int tl = ws == 3 ? l * (l - 1) * (l - 2) / 6 : 0;
                     uint64_t any = 0;
 #pragma unroll
@@ -253,7 +292,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                         const double dB = lower_beta();
 #pragma unroll
                         for (int x = 0; x < WMAX; ++x)
-                            e[x] -= 2.0 * dB * PO * ps[wb + x];
+                            e[x] += sgn * 2.0 * dB * PB * ps[wb + x];
                     }
                 }
             }
@@ -266,7 +305,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
         double er[WMAX];
 #pragma unroll
         for (int x = 0; x < WMAX; ++x) er[x] = e[x];
-        double Y = SO - beta * PO * PO;
+        double Y = SB - beta * PB * PB;
 #pragma unroll
         for (int x = 0; x < WMAX; ++x)
             if (x < ws) Y += er[x];
@@ -303,11 +342,11 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                 if (dB != 0.0) {
 #pragma unroll
                     for (int x = 0; x < WMAX; ++x)
-                        er[x] -= 2.0 * dB * PO * ps[wb + x];
+                        er[x] += sgn * 2.0 * dB * PB * ps[wb + x];
                     // Y for the round's last real step from the rescaled e
                     int tl = t0 + 3;
                     while (wmk[tl] == kPadMask) --tl;
-                    double yy = SO - beta * PO * PO;
+                    double yy = SB - beta * PB * PB;
                     for (uint64_t a = wmk[tl]; a; a &= a - 1) yy += er[__ffsll((unsigned long long)a) - 1 - wb];
                     Y = act ? yy : INFINITY;
                 }
@@ -350,8 +389,10 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
 __device__ inline uint64_t enum_best(const EnumPlan &pl, const double *Gm, const double *ps, uint64_t seed_mask,
                                      const uint2 *__restrict__ g_io, const uint64_t *__restrict__ g_wmk,
                                      const EnumJob *__restrict__ g_jobs, const uint64_t *__restrict__ g_omk,
-                                     double2 *ent, double *PLt, double *redd, uint64_t *redm, int *ctr) {
-    return enum_best_body<kMaxWalk>(pl, Gm, ps, seed_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd, redm, ctr);
+                                     double2 *ent, double *PLt, double *redd, uint64_t *redm, int *ctr,
+                                     bool cpl, double *cv) {
+    return enum_best_body<kMaxWalk>(pl, Gm, ps, seed_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd, redm, ctr,
+                                    cpl, cv);
 }
 
 }  // namespace fw

@@ -192,6 +192,7 @@ __device__ inline uint64_t enum_complement(const double *Gm, const double *ps, i
 struct PoolBudget {
     int s, extra, P, pool_off, set_off;
     int direct;  // through the dropped set (enum_complement), else the walk
+    int cpl;     // the walk enumerates the dropped sets (its plan: P keys, P - s of them)
     size_t tab_off;  // the walk tables' offset in the workspace
     EnumPlan pl;
     EnumTables tab;
@@ -422,7 +423,7 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
         // ES_pool
         const uint64_t best = B.direct ? enum_complement(Gm, ps, P, P - s, cv, redd, redm)
                                        : enum_best(B.pl, Gm, ps, seed, B.tab.io, B.tab.wmk, B.tab.jobs, B.tab.omk,
-                                                   ent, PLt, redd, redm, ctr);
+                                                   ent, PLt, redd, redm, ctr, B.cpl != 0, cv);
 
         // Balancing within the pool on wave 0 alone (P <= 64 keys, one per
         // lane, no workgroup barrier), while waves 1 and 2 take the reported
@@ -673,7 +674,13 @@ bool make_pool_plan(int64_t N, int d, int nb, const int32_t *s, const int32_t *e
         B.direct = eb <= kDirectDrop;
         if (!B.direct) {
             if (binom(P, sb) >= (1ull << 31)) return false;
-            if (!choose_plan(P, sb, &B.pl)) return false;
+            // walk the kept sets or the dropped sets, whichever plan costs less
+            EnumPlan pk, pd;
+            double ck = 0.0, cd = 0.0;
+            const bool okk = choose_plan(P, sb, &pk, &ck), okd = choose_plan(P, eb, &pd, &cd);
+            if (!okk && !okd) return false;
+            B.cpl = okd && (!okk || cd < ck);
+            B.pl = B.cpl ? pd : pk;
             B.pl.d = d;
             B.pl.G = 1;
             pp.nentmax = B.pl.nent > pp.nentmax ? B.pl.nent : pp.nentmax;

@@ -537,21 +537,32 @@ __global__ void __launch_bounds__(MTH, 1) topk_mp_kernel(FusedArgs a) {
 #pragma unroll
                 for (int t = 0; t < 2; ++t) {
                     float p[4];
-                    int tier[4];
+                    bool in[NK][4];   // in[kk][e]: the logit reaches budget kk's threshold
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         p[e] = __builtin_amdgcn_exp2f(fmaf(z[t][e], MLOG2E, mc2));
-                        int ti = NK;
 #pragma unroll
-                        for (int kk = 0; kk < NK; ++kk) ti -= (int)(z[t][e] >= tz[kk]);
-                        tier[e] = ti;
+                        for (int kk = 0; kk < NK; ++kk) in[kk][e] = z[t][e] >= tz[kk];
                     }
+                    // tier tt < NK: in budget tt's set but not in budget tt - 1's
+                    // (thresholds are non-increasing); tier NK: in none.  The
+                    // conditions are lane masks, combined on the scalar unit.
 #pragma unroll
                     for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
                         for (int pr = 0; pr < 2; ++pr) {
-                            const f32x2 pp = {tier[2 * pr] == tt ? p[2 * pr] : 0.f,
-                                              tier[2 * pr + 1] == tt ? p[2 * pr + 1] : 0.f};
+                            bool c0, c1;
+                            if (tt == 0) {
+                                c0 = in[0][2 * pr];
+                                c1 = in[0][2 * pr + 1];
+                            } else if (tt < NK) {
+                                c0 = in[tt][2 * pr] && !in[tt - 1][2 * pr];
+                                c1 = in[tt][2 * pr + 1] && !in[tt - 1][2 * pr + 1];
+                            } else {
+                                c0 = !in[NK - 1][2 * pr];
+                                c1 = !in[NK - 1][2 * pr + 1];
+                            }
+                            const f32x2 pp = {c0 ? p[2 * pr] : 0.f, c1 ? p[2 * pr + 1] : 0.f};
                             pw[tt][2 * t + pr] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pp, bf16x2));
                         }
                     if (SEL) {
@@ -576,31 +587,50 @@ __global__ void __launch_bounds__(MTH, 1) topk_mp_kernel(FusedArgs a) {
                     const u32x4 x = {pw[tt][0], pw[tt][1], pw[tt][2], pw[tt][3]};
                     pb[tt] = __builtin_bit_cast(bf16x8, x);
                 }
-                // V^T operands, one 64-column half at a time: transposed reads of
-                // rows 4 grp + cr (keys 0..15) and 16 + 4 grp + cr (2048 bytes on)
-                const uint32_t va = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char *)(slot + KBYTES + BBYTES);
+                // V^T operands of both 64-column halves: transposed reads of rows
+                // 4 grp + cr (keys 0..15) and 16 + 4 grp + cr (2048 bytes on) of
+                // each half, all issued at once; the second half's wait comes
+                // after the first half's products.  The operands pass through the
+                // wait statements so that no product is scheduled before its wait.
+                const uint32_t va =
+                    (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char *)(slot + KBYTES + BBYTES);
+                s16x4 vt[2][4][2];
+                asm volatile(
+                    "ds_read_b64_tr_b16 %0, %16\n"
+                    "ds_read_b64_tr_b16 %1, %16 offset:2048\n"
+                    "ds_read_b64_tr_b16 %2, %17\n"
+                    "ds_read_b64_tr_b16 %3, %17 offset:2048\n"
+                    "ds_read_b64_tr_b16 %4, %18\n"
+                    "ds_read_b64_tr_b16 %5, %18 offset:2048\n"
+                    "ds_read_b64_tr_b16 %6, %19\n"
+                    "ds_read_b64_tr_b16 %7, %19 offset:2048\n"
+                    "ds_read_b64_tr_b16 %8, %16 offset:4096\n"
+                    "ds_read_b64_tr_b16 %9, %16 offset:6144\n"
+                    "ds_read_b64_tr_b16 %10, %17 offset:4096\n"
+                    "ds_read_b64_tr_b16 %11, %17 offset:6144\n"
+                    "ds_read_b64_tr_b16 %12, %18 offset:4096\n"
+                    "ds_read_b64_tr_b16 %13, %18 offset:6144\n"
+                    "ds_read_b64_tr_b16 %14, %19 offset:4096\n"
+                    "ds_read_b64_tr_b16 %15, %19 offset:6144\n"
+                    "s_waitcnt lgkmcnt(8)"
+                    : "=&v"(vt[0][0][0]), "=&v"(vt[0][0][1]), "=&v"(vt[0][1][0]), "=&v"(vt[0][1][1]),
+                      "=&v"(vt[0][2][0]), "=&v"(vt[0][2][1]), "=&v"(vt[0][3][0]), "=&v"(vt[0][3][1]),
+                      "=&v"(vt[1][0][0]), "=&v"(vt[1][0][1]), "=&v"(vt[1][1][0]), "=&v"(vt[1][1][1]),
+                      "=&v"(vt[1][2][0]), "=&v"(vt[1][2][1]), "=&v"(vt[1][3][0]), "=&v"(vt[1][3][1])
+                    : "v"(va + vrd[0]), "v"(va + vrd[1]), "v"(va + vrd[2]), "v"(va + vrd[3])
+                    : "memory");
 #pragma unroll
                 for (int hf = 0; hf < 2; ++hf) {
-                    s16x4 vt[4][2];
-                    const uint32_t hb = va + 4096u * hf;
-                    asm volatile(
-                        "ds_read_b64_tr_b16 %0, %8\n"
-                        "ds_read_b64_tr_b16 %1, %8 offset:2048\n"
-                        "ds_read_b64_tr_b16 %2, %9\n"
-                        "ds_read_b64_tr_b16 %3, %9 offset:2048\n"
-                        "ds_read_b64_tr_b16 %4, %10\n"
-                        "ds_read_b64_tr_b16 %5, %10 offset:2048\n"
-                        "ds_read_b64_tr_b16 %6, %11\n"
-                        "ds_read_b64_tr_b16 %7, %11 offset:2048\n"
-                        "s_waitcnt lgkmcnt(0)"
-                        : "=&v"(vt[0][0]), "=&v"(vt[0][1]), "=&v"(vt[1][0]), "=&v"(vt[1][1]),
-                          "=&v"(vt[2][0]), "=&v"(vt[2][1]), "=&v"(vt[3][0]), "=&v"(vt[3][1])
-                        : "v"(hb + vrd[0]), "v"(hb + vrd[1]), "v"(hb + vrd[2]), "v"(hb + vrd[3])
-                        : "memory");
+                    if (hf == 1)
+                        asm volatile("s_waitcnt lgkmcnt(0)"
+                                     : "+v"(vt[1][0][0]), "+v"(vt[1][0][1]), "+v"(vt[1][1][0]), "+v"(vt[1][1][1]),
+                                       "+v"(vt[1][2][0]), "+v"(vt[1][2][1]), "+v"(vt[1][3][0]), "+v"(vt[1][3][1])
+                                     :
+                                     : "memory");
 #pragma unroll
                     for (int dt = 0; dt < 4; ++dt) {
                         const bf16x8 vb = __builtin_bit_cast(
-                            bf16x8, __builtin_shufflevector(vt[dt][0], vt[dt][1], 0, 1, 2, 3, 4, 5, 6, 7));
+                            bf16x8, __builtin_shufflevector(vt[hf][dt][0], vt[hf][dt][1], 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
                         for (int tt = 0; tt < NT; ++tt)
                             acc[tt][4 * hf + dt] =
