@@ -152,23 +152,29 @@ __global__ void sel_init_kernel(SelState *s, int64_t quota) {
     }
 }
 
-// histogram of the next 8-bit digit over non-floor entries matching the prefix
+// histogram of the next 8-bit digit over non-floor entries matching the prefix.
+// Block b reads slice b / H of unit b % H (the grid is a multiple of H), so
+// positions come without a division per entry; each wave counts into its own
+// copy of the bins (fewer lanes contend for one LDS word), summed at the end.
 __global__ void __launch_bounds__(256)
 sel_hist_kernel(const float *__restrict__ imp, int64_t H, int64_t n, int64_t nf, int shift,
                 SelState *s, const uint32_t *ckey, const int64_t *ccut) {
-    __shared__ uint32_t h[256];
-    const int t = threadIdx.x;
-    h[t] = 0;
+    __shared__ uint32_t hw[4][256];
+    const int t = threadIdx.x, w = t >> 6;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) hw[i][t] = 0;
     __syncthreads();
     const uint32_t prefix = s->prefix, pmask = s->pmask;
-    const int64_t total = H * nf;
-    for (int64_t e = (int64_t)blockIdx.x * 256 + t; e < total; e += (int64_t)gridDim.x * 256) {
-        const int64_t hh = e / nf, j = e % nf;
-        const uint32_t u = ord_key(imp[hh * n + j]);
-        if ((u & pmask) == prefix && offered(ckey, ccut, hh, j, u)) atomicAdd(&h[(u >> shift) & 255u], 1u);
+    const int64_t hh = blockIdx.x % H;
+    const int64_t nsl = gridDim.x / H, sl = blockIdx.x / H;
+    const float *row = imp + hh * n;
+    for (int64_t j = sl * 256 + t; j < nf; j += nsl * 256) {
+        const uint32_t u = ord_key(row[j]);
+        if ((u & pmask) == prefix && offered(ckey, ccut, hh, j, u)) atomicAdd(&hw[w][(u >> shift) & 255u], 1u);
     }
     __syncthreads();
-    if (h[t]) atomicAdd(&s->hist[t], h[t]);
+    const uint32_t c = hw[0][t] + hw[1][t] + hw[2][t] + hw[3][t];
+    if (c) atomicAdd(&s->hist[t], c);
 }
 
 // choose the digit holding the rem-th largest; clear the histogram
@@ -189,6 +195,7 @@ __global__ void sel_pick_kernel(SelState *s, int shift) {
 }
 
 // per unit: entries above tau and equal to tau among the non-floor positions
+// (16-byte loads of four scores where the row allows them)
 __global__ void __launch_bounds__(256)
 unit_counts_kernel(const float *__restrict__ imp, int64_t n, int64_t nf, const SelState *s,
                    int64_t quota, int64_t *cgt, int64_t *ceq, const uint32_t *ckey, const int64_t *ccut) {
@@ -196,14 +203,29 @@ unit_counts_kernel(const float *__restrict__ imp, int64_t n, int64_t nf, const S
     const int64_t h = blockIdx.x;
     const int t = threadIdx.x;
     const uint32_t key = s->prefix;
+    const float *row = imp + h * n;
     int64_t a = 0, b = 0;
-    if (quota > 0)
-        for (int64_t j = t; j < nf; j += 256) {
-            const uint32_t u = ord_key(imp[h * n + j]);
-            const bool o = offered(ckey, ccut, h, j, u);
-            a += o && (u > key);
-            b += o && (u == key);
+    auto one = [&](int64_t j, float x) {
+        const uint32_t u = ord_key(x);
+        const bool o = offered(ckey, ccut, h, j, u);
+        a += o && (u > key);
+        b += o && (u == key);
+    };
+    if (quota > 0) {
+        int64_t j0 = 0;
+        if ((n & 3) == 0) {
+            const int64_t nv = nf / 4;   // whole groups of four non-floor positions
+            for (int64_t g = t; g < nv; g += 256) {
+                const float4 y = *(const float4 *)(row + 4 * g);
+                one(4 * g, y.x);
+                one(4 * g + 1, y.y);
+                one(4 * g + 2, y.z);
+                one(4 * g + 3, y.w);
+            }
+            j0 = 4 * nv;
         }
+        for (int64_t j = j0 + t; j < nf; j += 256) one(j, row[j]);
+    }
     a = block_reduce(a, r1, OpSum());
     b = block_reduce(b, r2, OpSum());
     if (t == 0) {
@@ -212,97 +234,173 @@ unit_counts_kernel(const float *__restrict__ imp, int64_t n, int64_t nf, const S
     }
 }
 
-// ties taken per unit, offsets, tau and the bytes held (one workgroup)
+// ties taken per unit, offsets, tau and the bytes held (one workgroup).  The
+// units take the remaining ties in unit order: unit h takes
+// clamp(rem - (ties of the units before it), 0, its ties), so both the ties
+// taken and the offsets are prefix sums, formed 256 units at a time.
+__device__ __forceinline__ int64_t block_excl_scan64(int64_t v, int64_t *buf, int64_t *total) {
+    const int t = threadIdx.x, nt = blockDim.x;
+    buf[t] = v;
+    __syncthreads();
+    for (int s2 = 1; s2 < nt; s2 <<= 1) {
+        const int64_t add = (t >= s2) ? buf[t - s2] : 0;
+        __syncthreads();
+        buf[t] += add;
+        __syncthreads();
+    }
+    const int64_t incl = buf[t];
+    *total = buf[nt - 1];
+    __syncthreads();
+    return incl - v;
+}
+
 __global__ void __launch_bounds__(256)
 unit_offsets_kernel(int64_t H, int64_t hpl, int64_t n, int64_t f, int64_t quota, const SelState *s,
                     const int64_t *cgt, const int64_t *ceq, int64_t *take, int64_t *offsets,
                     float *tau, int64_t *bytes_held, int64_t row_bytes) {
-    if (threadIdx.x != 0) return;
-    int64_t rem = s->rem, acc = 0;
-    for (int64_t h = 0; h < H; ++h) {
-        int64_t t = 0;
-        if (quota > 0) {
-            t = rem < ceq[h] ? rem : ceq[h];
-            rem -= t;
+    __shared__ int64_t buf[256];
+    __shared__ int64_t red[256];
+    const int t = threadIdx.x;
+    const int64_t rem = s->rem;
+    int64_t eq_run = 0, acc = 0;   // ties and kept entries of the chunks before
+    for (int64_t h0 = 0; h0 < H; h0 += 256) {
+        const int64_t h = h0 + t;
+        const int64_t e = (h < H && quota > 0) ? ceq[h] : 0;
+        int64_t etot;
+        const int64_t ebefore = eq_run + block_excl_scan64(e, buf, &etot);
+        int64_t tk = 0;
+        if (h < H && quota > 0) {
+            const int64_t left = rem - ebefore;
+            tk = left <= 0 ? 0 : (left < e ? left : e);
         }
-        take[h] = t;
-        offsets[h] = acc;
-        acc += f + (quota > 0 ? cgt[h] : 0) + t;
+        const int64_t c = (h < H) ? f + (quota > 0 ? cgt[h] : 0) + tk : 0;
+        int64_t ctot;
+        const int64_t cbefore = acc + block_excl_scan64(c, buf, &ctot);
+        if (h < H) {
+            take[h] = tk;
+            offsets[h] = cbefore;
+        }
+        eq_run += etot;
+        acc += ctot;
     }
-    offsets[H] = acc;
-    if (tau) *tau = (quota > 0) ? key_to_float(s->prefix) : INFINITY;
+    if (t == 0) offsets[H] = acc;
+    if (t == 0 && tau) *tau = (quota > 0) ? key_to_float(s->prefix) : INFINITY;
     if (bytes_held) {
+        __threadfence_block();
+        __syncthreads();   // offsets of every unit are written
         int64_t padded = 0;
-        for (int64_t l = 0; l < H / hpl; ++l) {
+        for (int64_t l = t; l < H / hpl; l += 256) {
             int64_t mx = 0;
             for (int64_t h = l * hpl; h < (l + 1) * hpl; ++h) {
-                const int64_t c = offsets[h + 1] - offsets[h];
-                mx = c > mx ? c : mx;
+                const int64_t cc = offsets[h + 1] - offsets[h];
+                mx = cc > mx ? cc : mx;
             }
             padded += mx * hpl;
         }
-        bytes_held[0] = acc * row_bytes;
-        bytes_held[1] = padded * row_bytes;
-        bytes_held[2] = H * n * row_bytes;
+        padded = block_reduce(padded, red, OpSum());
+        if (t == 0) {
+            bytes_held[0] = acc * row_bytes;
+            bytes_held[1] = padded * row_bytes;
+            bytes_held[2] = H * n * row_bytes;
+        }
     }
 }
 
-// per unit: kept positions ascending, and the dropped score mass
+// per unit: kept positions ascending, and the dropped score mass.  The unit's
+// scores are read in tiles of 16 consecutive positions per thread (16-byte
+// loads: a wave reads whole lines), and one scan per tile places them.  Each
+// thread's count of plain keeps (floor, or offered above the threshold key)
+// and of offered keys equal to it share one word (16 bits each: a tile holds
+// 4096 positions), and ties are kept in position order while the unit's
+// quota of them lasts, so the number of ties kept before a thread follows
+// from the ties before it.
+__device__ __forceinline__ int keep_block_scan(int v, int *wsum, int *total) {
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6, nw = blockDim.x >> 6;
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    if (lane == 63) wsum[w] = x;
+    __syncthreads();
+    int before = 0, tot = 0;
+    for (int i = 0; i < nw; ++i) {
+        const int s = wsum[i];
+        before += i < w ? s : 0;
+        tot += s;
+    }
+    __syncthreads();   // wsum is reused by the next tile
+    *total = tot;
+    return before + x - v;
+}
+
 __global__ void __launch_bounds__(256)
 unit_keep_kernel(const float *__restrict__ imp, int64_t n, int64_t f, int64_t quota,
                  const SelState *s, const int64_t *take, const int64_t *offsets, int32_t *kept_pos,
                  float *dropped, const uint32_t *ckey, const int64_t *ccut) {
-    __shared__ int scan[256];
-    __shared__ int scan2[256];
+    constexpr int PER = 16;
+    __shared__ int wsum[4];
     __shared__ double red[256];
     const int64_t h = blockIdx.x;
     const int t = threadIdx.x;
     const uint32_t key = s->prefix;
     const int64_t tk = take[h];
     const int64_t nf = n - f;
-    const int64_t chunk = (n + 255) / 256;
-    const int64_t lo = t * chunk, hi = (lo + chunk < n) ? lo + chunk : n;
-    // ties before this thread's chunk (ascending position)
-    int c_eq = 0;
-    if (quota > 0)
-        for (int64_t j = lo; j < hi && j < nf; ++j) {
-            const uint32_t u = ord_key(imp[h * n + j]);
-            c_eq += (u == key) && offered(ckey, ccut, h, j, u);
-        }
-    int tot;
-    int eq_before = block_exclusive_scan(c_eq, scan2, &tot);
-    int c = 0;
+    const float *row = imp + h * n;
+    const bool vec = (n & 3) == 0;
+    int64_t out = offsets[h];
+    int64_t eq_run = 0;   // offered keys equal to the threshold key before this tile
     double dm = 0.0;
-    {
-        int eq = eq_before;
-        for (int64_t j = lo; j < hi; ++j) {
-            bool keep = j >= nf;
-            if (!keep && quota > 0) {
-                const uint32_t u = ord_key(imp[h * n + j]);
-                if (offered(ckey, ccut, h, j, u)) {
-                    if (u > key) keep = true;
-                    else if (u == key) keep = (eq++ < tk);
+    for (int64_t base = 0; base < n; base += (int64_t)PER * 256) {
+        const int64_t j0 = base + (int64_t)PER * t;
+        float x[PER];
+        if (vec && j0 + PER <= n) {
+#pragma unroll
+            for (int q = 0; q < PER / 4; ++q) {
+                const float4 y = *(const float4 *)(row + j0 + 4 * q);
+                x[4 * q] = y.x; x[4 * q + 1] = y.y; x[4 * q + 2] = y.z; x[4 * q + 3] = y.w;
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < PER; ++e) x[e] = (j0 + e < n) ? row[j0 + e] : 0.f;
+        }
+        // 0: not kept, 1: kept, 2: an offered key equal to the threshold key
+        uint32_t cls[PER];
+        int cplain = 0, ctie = 0;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+            const int64_t j = j0 + e;
+            uint32_t c = 0;
+            if (j < n) {
+                if (j >= nf) {
+                    c = 1;
+                } else if (quota > 0) {
+                    const uint32_t u = ord_key(x[e]);
+                    if (offered(ckey, ccut, h, j, u)) c = u > key ? 1u : (u == key ? 2u : 0u);
                 }
             }
-            c += keep;
-            if (!keep) dm += (double)imp[h * n + j];
+            cls[e] = c;
+            cplain += c == 1;
+            ctie += c == 2;
         }
-    }
-    int pos = block_exclusive_scan(c, scan, &tot) + (int)0;
-    int64_t out = offsets[h] + pos;
-    {
-        int eq = eq_before;
-        for (int64_t j = lo; j < hi; ++j) {
-            bool keep = j >= nf;
-            if (!keep && quota > 0) {
-                const uint32_t u = ord_key(imp[h * n + j]);
-                if (offered(ckey, ccut, h, j, u)) {
-                    if (u > key) keep = true;
-                    else if (u == key) keep = (eq++ < tk);
-                }
-            }
-            if (keep) kept_pos[out++] = (int32_t)j;
+        int tot;
+        const int pre = keep_block_scan(cplain | (ctie << 16), wsum, &tot);
+        const int64_t rem = tk - eq_run;   // ties still to keep
+        const int64_t tie_before = pre >> 16;
+        int64_t tied_kept = rem <= 0 ? 0 : (tie_before < rem ? tie_before : rem);
+        int64_t o = out + (pre & 0xFFFF) + tied_kept;
+        int64_t tie_rank = eq_run + tie_before;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+            bool keep = cls[e] == 1;
+            if (cls[e] == 2) keep = tie_rank++ < tk;
+            if (keep) kept_pos[o++] = (int32_t)(j0 + e);
+            else if (j0 + e < n) dm += (double)x[e];
         }
+        const int64_t tile_ties = tot >> 16;
+        out += (tot & 0xFFFF) + (rem <= 0 ? 0 : (tile_ties < rem ? tile_ties : rem));
+        eq_run += tile_ties;
     }
     dm = block_reduce(dm, red, OpSum());
     if (t == 0 && dropped) dropped[h] = (float)dm;
@@ -376,8 +474,12 @@ hipError_t launch_compact(int dtype, const void *k, const void *v, int64_t H, in
     const int64_t row_bytes = d * elem;
     hipLaunchKernelGGL(sel_init_kernel, dim3(1), dim3(256), 0, st, L.sel, quota);
     if (quota > 0) {
-        const int64_t total = H * nf;
-        const unsigned blocks = (unsigned)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
+        // slices per unit so that the grid holds about 4096 blocks (a multiple of H)
+        const int64_t per = (nf + 255) / 256;
+        int64_t nsl = 4096 / H;
+        if (nsl > per) nsl = per;
+        if (nsl < 1) nsl = 1;
+        const unsigned blocks = (unsigned)(H * nsl);
         for (int shift = 24; shift >= 0; shift -= 8) {
             hipLaunchKernelGGL(sel_hist_kernel, dim3(blocks), dim3(256), 0, st, importance, H, n, nf,
                                shift, L.sel, ckey, ccut);
@@ -386,7 +488,7 @@ hipError_t launch_compact(int dtype, const void *k, const void *v, int64_t H, in
     }
     hipLaunchKernelGGL(unit_counts_kernel, dim3((unsigned)H), dim3(256), 0, st, importance, n, nf,
                        L.sel, quota, L.cgt, L.ceq, ckey, ccut);
-    hipLaunchKernelGGL(unit_offsets_kernel, dim3(1), dim3(64), 0, st, H, hpl, n, f, quota, L.sel,
+    hipLaunchKernelGGL(unit_offsets_kernel, dim3(1), dim3(256), 0, st, H, hpl, n, f, quota, L.sel,
                        L.cgt, L.ceq, L.take, offsets, tau, bytes_held, 2 * row_bytes);
     hipLaunchKernelGGL(unit_keep_kernel, dim3((unsigned)H), dim3(256), 0, st, importance, n, f, quota,
                        L.sel, L.take, offsets, kept_pos, dropped, ckey, ccut);
