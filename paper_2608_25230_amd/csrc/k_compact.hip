@@ -406,25 +406,25 @@ unit_keep_kernel(const float *__restrict__ imp, int64_t n, int64_t f, int64_t qu
     if (t == 0 && dropped) dropped[h] = (float)dm;
 }
 
-// gather kept rows: 16-byte pieces, rows located by binary search on offsets
+// gather kept rows: 16-byte pieces.  Block b copies part b % per of unit
+// b / per, so each thread knows its unit without a search; one wave covers
+// four rows of up to 256 bytes (16 lanes per row) per step.
 __global__ void __launch_bounds__(256)
 gather_rows_kernel(const char *__restrict__ k, const char *__restrict__ v, int64_t H, int64_t n,
                    int64_t row_bytes, const int64_t *offsets, const int32_t *kept_pos, char *k_out,
-                   char *v_out, int64_t total) {
+                   char *v_out, int per) {
+    const int64_t h = blockIdx.x / per;
+    const int part = blockIdx.x % per;
     const int64_t pieces = row_bytes / 16;
-    const int64_t nwork = total * pieces;
-    for (int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; w < nwork;
-         w += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t row = w / pieces, pc = w % pieces;
-        int64_t lo = 0, hi = H;  // offsets[lo] <= row < offsets[hi]
-        while (hi - lo > 1) {
-            const int64_t mid = (lo + hi) / 2;
-            if (offsets[mid] <= row) lo = mid; else hi = mid;
-        }
-        const int64_t src = (lo * n + kept_pos[row]) * row_bytes + pc * 16;
+    const int64_t r0 = offsets[h], r1 = offsets[h + 1];
+    const int64_t nwork = (r1 - r0) * pieces;
+    const char *kh = k + h * n * row_bytes, *vh = v + h * n * row_bytes;
+    for (int64_t w = (int64_t)part * blockDim.x + threadIdx.x; w < nwork; w += (int64_t)per * blockDim.x) {
+        const int64_t row = r0 + w / pieces, pc = w % pieces;
+        const int64_t src = (int64_t)kept_pos[row] * row_bytes + pc * 16;
         const int64_t dst = row * row_bytes + pc * 16;
-        *(uint4 *)(k_out + dst) = *(const uint4 *)(k + src);
-        *(uint4 *)(v_out + dst) = *(const uint4 *)(v + src);
+        *(uint4 *)(k_out + dst) = *(const uint4 *)(kh + src);
+        *(uint4 *)(v_out + dst) = *(const uint4 *)(vh + src);
     }
 }
 
@@ -494,11 +494,14 @@ hipError_t launch_compact(int dtype, const void *k, const void *v, int64_t H, in
                        L.sel, L.take, offsets, kept_pos, dropped, ckey, ccut);
     if (budget > 0) {
         if (row_bytes % 16 == 0) {
+            // blocks per unit: about the unit's average share of 16 K blocks
             const int64_t work = budget * (row_bytes / 16);
-            const unsigned blocks = (unsigned)((work + 255) / 256 < 65536 ? (work + 255) / 256 : 65536);
-            hipLaunchKernelGGL(gather_rows_kernel, dim3(blocks), dim3(256), 0, st, (const char *)k,
+            int64_t per = (work + 255) / 256 / H;
+            per = per < 1 ? 1 : (per > 1024 ? 1024 : per);
+            if (H * per > (int64_t)1 << 30) per = 1;
+            hipLaunchKernelGGL(gather_rows_kernel, dim3((unsigned)(H * per)), dim3(256), 0, st, (const char *)k,
                                (const char *)v, H, n, row_bytes, offsets, kept_pos, (char *)k_out,
-                               (char *)v_out, budget);
+                               (char *)v_out, (int)per);
         } else {
             const int64_t work = budget * row_bytes;
             const unsigned blocks = (unsigned)((work + 255) / 256 < 65536 ? (work + 255) / 256 : 65536);
