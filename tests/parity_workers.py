@@ -97,6 +97,19 @@ def classify_swap(job):
             t += 1
 
 
+def local_optimum_margin(job):
+    """The float64 error of a final swap set and the least error over its full
+    (kept, dropped) neighbourhood (Lemma 2.2's g-form, one sweep)."""
+    z, Vb, S, gap_gpu = job
+    V = _bf16(Vb) if np.asarray(Vb).dtype == np.uint16 else np.asarray(Vb, np.float64)
+    with threadpool_limits(1):
+        p = O.weights(z)
+        S = np.sort(np.asarray(S, np.int64))
+        es_g = O.forced_error(p, V, S)
+        vals, _, _ = O.swap_values(p, V, S, "gform")
+        return es_g, float(vals.min()), gap_gpu
+
+
 def dense_topk_unit(job):
     """Worst relative errors and index tallies of one unit's rows against
     row_dense_topk (the rules of tests/parity.py).  Per row and budget, a GPU

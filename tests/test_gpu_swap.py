@@ -160,3 +160,33 @@ def test_long_rows_tied_pairs_fall_back_to_full_sweep(torch_fw):
     t = _check(rows, k, 4, out, [(0, 0), (0, 1)], method="gform", min_exact=0.0, name="swap_tied_pairs")
     assert np.all(out["n_swaps"] >= 1)
     print("tied pairs:", t)
+
+
+def test_full_size_rows_converge_to_local_optima(torch_fw):
+    """Rows of the full-size workload (n = 32,768, k = 1,024) with room for
+    enough swaps: most stop on their own, within about 100 to 700 swaps, and
+    the set a row stops at is a local optimum (no (kept, dropped) swap lowers
+    its float64 error beyond the float32 search's precision), checked by the
+    oracle's full neighbourhood."""
+    torch, fw = torch_fw
+    wl = W.swap_long_rows(seed=0)
+    r = wl.rows
+    rows = W.Rows(r.dtype, r.q[:1, :8], r.k[:1], r.v[:1], r.scale[:1], r.bias)
+    iters = 2048
+    out = _run(torch, fw, rows, wl.k, iters)
+    ns = out["n_swaps"][0]
+    stopped = [g for g in range(rows.G) if ns[g] < iters]
+    print("swaps until the rule stops:", ns.tolist())
+    assert len(stopped) >= 6
+    q, K = rows.as_f64("q"), rows.as_f64("k")
+    bias = rows.bias.astype(np.float64)
+    jobs = []
+    for g in stopped[:4]:
+        z = O.logits(q[0, g], K[0], float(rows.scale[0]), bias)
+        jobs.append((z, rows.v[0], out["s_idx"][0, g], float(out["gap_traj"][0, g, ns[g]])))
+    res = PW.pool_map(PW.local_optimum_margin, jobs)
+    for (es_g, best, gap_gpu), g in zip(res, stopped[:4]):
+        assert abs(gap_gpu - es_g) <= PW.SWAP_REL["bf16"] * es_g, (g, gap_gpu, es_g)
+        assert best >= es_g * (1 - PW.SWAP_REL["bf16"]), (g, best, es_g)
+    record("swap_full_size_converged_local_optima", rows=len(jobs), swaps=[int(ns[g]) for g in stopped[:4]],
+           worst_margin=float(min(b / e - 1 for e, b, _ in res)))
