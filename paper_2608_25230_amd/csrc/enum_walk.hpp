@@ -90,18 +90,36 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
     double best_val = S_top / (P_top * P_top);
     uint64_t best_mask = top_mask;
     double beta = best_val;  // wave-uniform
+    // Each wave takes its next work item, and loads that item's descriptor
+    // and owned parts, while it walks the current one, so that the global
+    // loads of a job start are not waited for between jobs.
+    auto take_job = [&]() {
+        int j = 0;
+        if (lane == 0) j = atomicAdd(ctr, 1);
+        return __builtin_amdgcn_readfirstlane(__shfl(j, 0));
+    };
+    int jn_next = take_job();
+    EnumJob jb_next{};
+    uint64_t om_next = 0;
+    if (jn_next < pl.njobs) {
+        jb_next = g_jobs[jn_next];
+        om_next = g_omk[(size_t)jn_next * 64 + lane];
+    }
     for (;;) {
-        int jn = 0;
-        if (lane == 0) jn = atomicAdd(ctr, 1);
-        jn = __builtin_amdgcn_readfirstlane(__shfl(jn, 0));
+        const int jn = jn_next;
         if (jn >= pl.njobs) break;
-        const EnumJob jb = g_jobs[jn];
+        const EnumJob jb = jb_next;
+        const uint64_t Om = om_next;
+        jn_next = take_job();
+        if (jn_next < pl.njobs) {
+            jb_next = g_jobs[jn_next];
+            om_next = g_omk[(size_t)jn_next * 64 + lane];
+        }
         const EnumClass C = pl.cls[jb.cls];
         const int wb = C.wb, wn = C.wn, ws = C.ws, ls = C.ls;
         const bool act = lane < jb.lanes;
         // owned part of this lane (precomputed key mask; 0 on idle lanes):
         // p(O), S(O) and E[x] = sum_{a in O} Gm_{a, wb + x} over the walked range
-        const uint64_t Om = g_omk[(size_t)jn * 64 + lane];
         double PO = 0.0, SO = 0.0, CO = 0.0;
         double e[WMAX];
 #pragma unroll
