@@ -772,27 +772,114 @@ __global__ void __launch_bounds__(FTH, 1) topk_fused_kernel(FusedArgs a) {
 // ---------------------------------------------------------------------------
 // rank-ordered indices: sort each row's selected keys (descending)
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(256)
-fused_sort_kernel(const unsigned long long *sel, const int32_t *flags, int kmax, int sort_len,
-                  int32_t *topk_idx) {
-    extern __shared__ unsigned long long sb[];
+// Bitonic sorts of a row's kmax entries, padded with zeros (which sort last)
+// to N = (threads) E; one workgroup per row, thread t holding entries
+// t E .. t E + E - 1 in registers.  For partner distance s (a power of two):
+// s < E pairs entries within a thread; E <= s < 64 E pairs threads of one wave
+// (lane exchanges); larger s pairs waves through LDS.  The stages are
+// unrolled, so every exchange has a fixed lane pattern.  An entry is
+// ord_key(z) << 32 | (2^32 - 1 - key), so descending order is logit desc,
+// then index asc.
+
+// the 64-bit value of lane (lane ^ M): quad permutes (DPP) for M = 1, 2,
+// swizzles within 32 lanes for M = 4 .. 16, a permute for M = 32
+template <int M>
+__device__ __forceinline__ unsigned long long xlane64(unsigned long long v) {
+    const int lo = (int)(uint32_t)v, hi = (int)(uint32_t)(v >> 32);
+    int a, b;
+    if constexpr (M == 1) {
+        a = __builtin_amdgcn_mov_dpp(lo, 0xB1, 0xF, 0xF, false);
+        b = __builtin_amdgcn_mov_dpp(hi, 0xB1, 0xF, 0xF, false);
+    } else if constexpr (M == 2) {
+        a = __builtin_amdgcn_mov_dpp(lo, 0x4E, 0xF, 0xF, false);
+        b = __builtin_amdgcn_mov_dpp(hi, 0x4E, 0xF, 0xF, false);
+    } else if constexpr (M < 32) {
+        a = __builtin_amdgcn_ds_swizzle(lo, 0x1F | (M << 10));
+        b = __builtin_amdgcn_ds_swizzle(hi, 0x1F | (M << 10));
+    } else {
+        a = __shfl_xor(lo, 32);
+        b = __shfl_xor(hi, 32);
+    }
+    return ((unsigned long long)(uint32_t)b << 32) | (uint32_t)a;
+}
+__device__ __forceinline__ unsigned long long xlane64(unsigned long long v, int m) {
+    switch (m) {   // m is a constant in the unrolled stages
+        case 1: return xlane64<1>(v);
+        case 2: return xlane64<2>(v);
+        case 4: return xlane64<4>(v);
+        case 8: return xlane64<8>(v);
+        case 16: return xlane64<16>(v);
+        default: return xlane64<32>(v);
+    }
+}
+
+template <int E, int T>
+__device__ __forceinline__ void bitonic_rows(unsigned long long (&x)[E], unsigned long long *sb) {
+    constexpr int N = T * E;
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int size = 2; size <= N; size <<= 1) {
+#pragma unroll
+        for (int stride = size >> 1; stride >= E; stride >>= 1) {
+            const int m = stride / E;   // partner thread t ^ m
+            // the larger of the pair goes to the lower position in a
+            // descending block ((position & size) == 0), else the smaller
+            const bool keep_max = (((t * E) & size) == 0) == ((t & m) == 0);
+            unsigned long long y[E];
+            if (m < 64) {
+#pragma unroll
+                for (int e = 0; e < E; ++e) y[e] = xlane64(x[e], m);
+            } else {
+#pragma unroll
+                for (int e = 0; e < E; ++e) sb[t * E + e] = x[e];
+                __syncthreads();
+#pragma unroll
+                for (int e = 0; e < E; ++e) y[e] = sb[(t ^ m) * E + e];
+                __syncthreads();
+            }
+#pragma unroll
+            for (int e = 0; e < E; ++e) x[e] = ((x[e] > y[e]) == keep_max) ? x[e] : y[e];
+        }
+#pragma unroll
+        for (int s = E / 2; s >= 1; s >>= 1) {
+            if (s < size) {
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    if ((e & s) == 0) {
+                        const bool desc = ((t * E + e) & size) == 0;
+                        const unsigned long long a = x[e], b = x[e + s];
+                        const bool sw = (a < b) == desc;
+                        x[e] = sw ? b : a;
+                        x[e + s] = sw ? a : b;
+                    }
+                }
+            }
+        }
+    }
+}
+
+// T threads per row: one wave up to 1024 entries, four waves beyond
+template <int E, int T>
+__global__ void __launch_bounds__(T)
+fused_sort_kernel(const unsigned long long *sel, const int32_t *flags, int kmax, int32_t *topk_idx) {
+    __shared__ unsigned long long sb[T > 64 ? T * E : 1];
     const int64_t r = blockIdx.x;
     if (flags[r]) return;
-    const int tid = threadIdx.x;
-    for (int i = tid; i < sort_len; i += 256) sb[i] = (i < kmax) ? sel[r * kmax + i] : 0ull;
-    __syncthreads();
-    for (int size = 2; size <= sort_len; size <<= 1)
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            for (int i = tid; i < sort_len / 2; i += 256) {
-                const int lo = 2 * stride * (i / stride) + (i % stride), hi = lo + stride;
-                const bool desc = (lo & size) == 0;
-                const unsigned long long x = sb[lo], y = sb[hi];
-                if (desc ? (x < y) : (x > y)) { sb[lo] = y; sb[hi] = x; }
-            }
-            __syncthreads();
-        }
-    for (int i = tid; i < kmax; i += 256)
-        topk_idx[r * kmax + i] = (int32_t)(0xFFFFFFFFu - (uint32_t)(sb[i] & 0xFFFFFFFFull));
+    const int t = threadIdx.x;
+    const unsigned long long *src = sel + r * kmax;
+    unsigned long long x[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int i = t * E + e;
+        x[e] = i < kmax ? src[i] : 0ull;
+    }
+    bitonic_rows<E, T>(x, sb);
+    int32_t *dst = topk_idx + r * kmax;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int i = t * E + e;
+        if (i < kmax) dst[i] = (int32_t)(0xFFFFFFFFu - (uint32_t)(x[e] & 0xFFFFFFFFull));
+    }
 }
 
 __global__ void fused_clear_kernel(int32_t *flag_count) {
@@ -1033,11 +1120,17 @@ void launch_fused_clear(int32_t *flag_count, hipStream_t st) {
 void launch_fused_finish(const FusedArgs &a, int nk, int32_t *topk_idx, hipStream_t st) {
     const size_t R = (size_t)a.H * a.G;
     if (topk_idx) {
-        int sort_len = 1;
-        while (sort_len < a.kmax) sort_len <<= 1;
-        hipLaunchKernelGGL(fused_sort_kernel, dim3((unsigned)R), dim3(256), (size_t)sort_len * 8, st,
-                           (const unsigned long long *)a.sel, (const int32_t *)a.flags, a.kmax, sort_len,
-                           topk_idx);
+        const dim3 g((unsigned)R), b(256);
+        const unsigned long long *sel = a.sel;
+        const int32_t *fl = a.flags;
+        const dim3 w(64);
+        if (a.kmax <= 64) hipLaunchKernelGGL((fused_sort_kernel<1, 64>), g, w, 0, st, sel, fl, a.kmax, topk_idx);
+        else if (a.kmax <= 128) hipLaunchKernelGGL((fused_sort_kernel<2, 64>), g, w, 0, st, sel, fl, a.kmax, topk_idx);
+        else if (a.kmax <= 256) hipLaunchKernelGGL((fused_sort_kernel<4, 64>), g, w, 0, st, sel, fl, a.kmax, topk_idx);
+        else if (a.kmax <= 512) hipLaunchKernelGGL((fused_sort_kernel<8, 64>), g, w, 0, st, sel, fl, a.kmax, topk_idx);
+        else if (a.kmax <= 1024) hipLaunchKernelGGL((fused_sort_kernel<16, 64>), g, w, 0, st, sel, fl, a.kmax, topk_idx);
+        else if (a.kmax <= 2048) hipLaunchKernelGGL((fused_sort_kernel<8, 256>), g, b, 0, st, sel, fl, a.kmax, topk_idx);
+        else hipLaunchKernelGGL((fused_sort_kernel<16, 256>), g, b, 0, st, sel, fl, a.kmax, topk_idx);
     }
     switch (nk) {
         case 1: hipLaunchKernelGGL(fused_fixup_kernel<1>, dim3(64), dim3(256), 0, st, a, topk_idx); break;

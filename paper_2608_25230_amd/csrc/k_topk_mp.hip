@@ -55,8 +55,7 @@ constexpr float MLOG2E = 1.4426950408889634f;
 //   pass B  histograms (two rows per 32-bit word, 16-bit counts), ring of 2 GB
 //   pass C  lists of threshold-bin logits (one pool per wave), ring of 2 GC
 //   pass D  ring of 2 GD key/value slots
-constexpr int L_LC = 0;                    // [MR][4] per-row list counters
-constexpr int L_FC = L_LC + MR * 4 * 4;    // [MR] per-row correction counts
+constexpr int L_FC = 0;                    // [MR] per-row correction counts
 constexpr int L_FX = L_FC + MR * 4;        // [MR][FIXC] corrections (budget << 16 | key)
 constexpr int L_R = L_FX + MR * FIXC * 4;
 constexpr int L_TOTAL = 159232;            // bytes of LDS per workgroup (one per CU)
@@ -102,12 +101,6 @@ __device__ __forceinline__ void lds_add(uint32_t *p, uint32_t x) {
     const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint32_t *)p;
     asm volatile("ds_add_u32 %0, %1" ::"v"(a), "v"(x) : "memory");
 }
-__device__ __forceinline__ int lds_fetch_inc(int *p) {
-    const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int *)p;
-    int r;
-    asm volatile("ds_add_rtn_u32 %0, %1, %2\n\ts_waitcnt lgkmcnt(0)" : "=v"(r) : "v"(a), "v"(1u) : "memory");
-    return r;
-}
 __device__ __forceinline__ void lds_store64(unsigned long long *p, unsigned long long x) {
     const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned long long *)p;
     asm volatile("ds_write_b64 %0, %1" ::"v"(a), "v"(x) : "memory");
@@ -145,7 +138,6 @@ __global__ void __launch_bounds__(MTH, 1) topk_mp_kernel(FusedArgs a) {
     unsigned char *rbase = smem + L_R;
     uint32_t *hist = (uint32_t *)rbase;                       // pass B: [MR / 2][NB]
     unsigned long long *lists = (unsigned long long *)rbase;  // pass C: [MW][POOLW]
-    int *lcnt = (int *)(smem + L_LC);
     int *fcnt = (int *)(smem + L_FC);
     int *fixl = (int *)(smem + L_FX);
 
@@ -522,7 +514,6 @@ __global__ void __launch_bounds__(MTH, 1) topk_mp_kernel(FusedArgs a) {
         vrd[dt] = (uint32_t)(((4 * grp + cr) * 64 + ((2 * dt + (cq >> 1)) ^ (4 * (grp & 1) + cr)) * 8 + 4 * (cq & 1)) * 2);
     const float mc2 = -c2;
     int selpos = 0;
-    if (SEL && grp == 0) lcnt[myr * 4] = 0;
     auto kvslot = [&](int i) { return rbase + (i % (2 * GD)) * KVSLOT; };
     ring_barrier();   // every wave's rank phase is done with the pools
     mp_ring<GD>(nblk, (w >> 2) * (GD / 2), [&](int i) { issue_kv(kvslot(i), i); },
@@ -566,16 +557,35 @@ __global__ void __launch_bounds__(MTH, 1) topk_mp_kernel(FusedArgs a) {
                             pw[tt][2 * t + pr] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pp, bf16x2));
                         }
                     if (SEL) {
-                        // the selected keys of the largest budget (exact rule)
+                        // the selected keys of the largest budget (exact rule),
+                        // listed in the row's order of arrival: positions from a
+                        // running count held by the row's four lanes and an
+                        // exclusive prefix over them, as in pass C
+                        bool in[4];
+                        int nh = 0;
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
                             const int j = i * KB + 16 * t + 4 * grp + e;
-                            const bool in = (z[t][e] > tz[NK - 1]) || (z[t][e] == tz[NK - 1] && j <= cut[NK - 1]);
-                            if (in) {
-                                const int ps = lds_fetch_inc(&lcnt[myr * 4]);
-                                if (ps < a.kmax)
-                                    a.sel[myrow * a.kmax + ps] =
+                            in[e] = (z[t][e] > tz[NK - 1]) || (z[t][e] == tz[NK - 1] && j <= cut[NK - 1]);
+                            nh += (int)in[e];
+                        }
+                        int sc4 = nh;
+                        {
+                            const int y1 = __shfl_up(sc4, 16);
+                            if (grp >= 1) sc4 += y1;
+                            const int y2 = __shfl_up(sc4, 32);
+                            if (grp >= 2) sc4 += y2;
+                        }
+                        int pos = selpos + sc4 - nh;
+                        selpos += __shfl(sc4, 48 + rl);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            if (in[e]) {
+                                const int j = i * KB + 16 * t + 4 * grp + e;
+                                if (pos < a.kmax)
+                                    a.sel[myrow * a.kmax + pos] =
                                         ((unsigned long long)ord_key(z[t][e]) << 32) | (0xFFFFFFFFu - (uint32_t)j);
+                                ++pos;
                             }
                         }
                     }
