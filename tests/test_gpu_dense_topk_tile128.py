@@ -43,6 +43,8 @@ def _flags(torch, out, rows):
     dict(n=992, ks=(5, 300), kv_heads=1, rows_per_q=32),
     dict(n=4096, ks=(4096, 7), kv_heads=1, rows_per_q=32),
     dict(n=64, ks=(1, 63), kv_heads=1, rows_per_q=32),
+    # index lists past 1024 keys: the rank sort on four waves
+    dict(n=3072, ks=(1800, 40), kv_heads=1, rows_per_q=32),
 ])
 def test_tile128_shapes_all_rows(torch_fw, cfg):
     torch, fw = torch_fw
