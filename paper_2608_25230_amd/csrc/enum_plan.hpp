@@ -120,7 +120,9 @@ struct EnumJob {
 
 
 // Row-independent tables of a plan in the caller's workspace: walk steps
-// (io, wmk), the job list and each job's owned parts.
+// (io, wmk), the job list and each job's owned parts (omk: njobs x 64 key
+// masks, then njobs x 64 lists of the first eight owned keys, ascending, one
+// byte each).
 struct EnumTables {
     uint2 *io;
     uint64_t *wmk;
@@ -142,7 +144,7 @@ __host__ inline EnumTables enum_tables(const EnumPlan &p, void *ws) {
     W.io = (uint2 *)take((size_t)p.nent * 8);
     W.wmk = (uint64_t *)take((size_t)p.nent * 8);
     W.jobs = (EnumJob *)take((size_t)p.njobs * sizeof(EnumJob));
-    W.omk = (uint64_t *)take((size_t)p.njobs * 64 * 8);
+    W.omk = (uint64_t *)take((size_t)p.njobs * 64 * 8 * 2);
     W.bytes = align_up(off, 256);
     return W;
 }

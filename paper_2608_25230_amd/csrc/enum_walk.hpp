@@ -100,20 +100,23 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
     };
     int jn_next = take_job();
     EnumJob jb_next{};
-    uint64_t om_next = 0;
+    uint64_t om_next = 0, ok_next = 0;
+    const uint64_t *g_okx = g_omk + (size_t)pl.njobs * 64;   // the owned parts' key lists
     if (jn_next < pl.njobs) {
         jb_next = g_jobs[jn_next];
         om_next = g_omk[(size_t)jn_next * 64 + lane];
+        ok_next = g_okx[(size_t)jn_next * 64 + lane];
     }
     for (;;) {
         const int jn = jn_next;
         if (jn >= pl.njobs) break;
         const EnumJob jb = jb_next;
-        const uint64_t Om = om_next;
+        const uint64_t Om = om_next, Ok = ok_next;
         jn_next = take_job();
         if (jn_next < pl.njobs) {
             jb_next = g_jobs[jn_next];
             om_next = g_omk[(size_t)jn_next * 64 + lane];
+            ok_next = g_okx[(size_t)jn_next * 64 + lane];
         }
         const EnumClass C = pl.cls[jb.cls];
         const int wb = C.wb, wn = C.wn, ws = C.ws, ls = C.ls;
@@ -125,15 +128,12 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
 #pragma unroll
         for (int x = 0; x < WMAX; ++x) e[x] = 0.0;
         if (kFastOwned > 1 && ls <= kFastOwned) {
-            // the owned keys in registers, then independent Gram reads (no
-            // loop-carried address chains); idle lanes read key 0
+            // the owned keys from the job's key list (a byte each), then
+            // independent Gram reads (no loop-carried address chains); idle
+            // lanes read key 0
             int kx[kFastOwned];
-            uint64_t a = Om;
 #pragma unroll
-            for (int i = 0; i < kFastOwned; ++i) {
-                kx[i] = a ? __ffsll((unsigned long long)a) - 1 : 0;
-                a &= a - 1;
-            }
+            for (int i = 0; i < kFastOwned; ++i) kx[i] = (int)((Ok >> (8 * i)) & 0xFFu);
 #pragma unroll
             for (int i = 0; i < kFastOwned; ++i) {
                 if (i < ls) {

@@ -169,6 +169,9 @@ __global__ void __launch_bounds__(64) enum_owned_kernel(EnumPlan p, const EnumJo
         }
     }
     omk[(size_t)j * 64 + lane] = m;
+    uint64_t keys = 0;   // the first eight keys of the part, ascending, a byte each
+    for (int i = 0; i < 8 && m; ++i, m &= m - 1) keys |= (uint64_t)(__ffsll((unsigned long long)m) - 1) << (8 * i);
+    omk[(size_t)(p.njobs + j) * 64 + lane] = keys;
 }
 
 template <typename T, int WMAX>
