@@ -25,6 +25,10 @@
 //     e[x] = 2 sum_{a in O} Gm_xa - 2 c_x + 2 beta (p_U - p_O) p_x,
 // and the walk itself is unchanged: pools that drop a few keys of many walk
 // small dropped sets instead of owning large kept parts.
+//
+// With HT (when the LDS has room), each wave keeps its own copy of the walk
+// table's step values at its current beta, T[t] = S_W - beta p(W)^2, rebuilt
+// when beta drops, so that a step is one add and a compare.
 #pragma once
 
 #include "enum_plan.hpp"
@@ -37,12 +41,13 @@ namespace fw {
 // the answer is never worse than it.  ent [nent] (double2), PLt [nent],
 // redd [NT] (double), redm [NT] (uint64) and ctr[1] are LDS scratch.
 // Returns the best mask, block-uniform.
-template <int WMAX>
+// wtab (HT): nent doubles per wave of the workgroup (LDS).
+template <int WMAX, bool HT = false>
 __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const double *Gm, const double *ps, uint64_t seed_mask,
                                      const uint2 *__restrict__ g_io, const uint64_t *__restrict__ g_wmk,
                                      const EnumJob *__restrict__ g_jobs, const uint64_t *__restrict__ g_omk,
                                      double2 *ent, double *PLt, double *redd, uint64_t *redm, int *ctr,
-                                     bool cpl = false, double *cv = nullptr) {
+                                     bool cpl = false, double *cv = nullptr, double *wtab = nullptr) {
     const int NT = blockDim.x;
     const int gp = pl.gp;
     const int tid = threadIdx.x, lane = tid & 63;
@@ -90,6 +95,16 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
     double best_val = S_top / (P_top * P_top);
     uint64_t best_mask = top_mask;
     double beta = best_val;  // wave-uniform
+    // HT: the wave's step values at its beta (padding steps stay +inf)
+    double *Tw = HT ? wtab + (size_t)(tid >> 6) * pl.nent : nullptr;
+    auto build_tw = [&]() __attribute__((always_inline)) {
+        if (HT)
+            for (int t = lane; t < pl.nent; t += 64) {
+                const double2 c = ent[t];
+                Tw[t] = fma(-beta, c.y, c.x);
+            }
+    };
+    build_tw();
     // Each wave takes its next work item, and loads that item's descriptor
     // and owned parts, while it walks the current one, so that the global
     // loads of a job start are not waited for between jobs.
@@ -181,6 +196,13 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
             }
         }
         const double2 *en = ent + C.toff;
+        const double *tw = HT ? Tw + C.toff : nullptr;
+        // the step value S_W - beta p(W)^2 of walk step t
+        auto stepv = [&](int t) __attribute__((always_inline)) -> double {
+            if (HT) return tw[t];
+            const double2 c = en[t];
+            return fma(-beta, c.y, c.x);
+        };
         const double *plt = PLt + C.toff;
         const uint64_t *wmk = g_wmk + C.toff;
         double thr = 1e-12 * beta;
@@ -214,6 +236,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
             const double dB = wbst - beta;
             beta = wbst;
             thr = 1e-12 * beta;
+            build_tw();
             return dB;
         };
 
@@ -230,11 +253,11 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
 #pragma unroll
                 for (int i0 = 0; i0 < WMAX; i0 += 4) {
                     if (i0 < lim) {
-                        double2 c[4];
+                        double c[4];
 #pragma unroll
-                        for (int u = 0; u < 4; ++u) c[u] = en[t0 + i0 + u];
+                        for (int u = 0; u < 4; ++u) c[u] = stepv(t0 + i0 + u);
 #pragma unroll
-                        for (int u = 0; u < 4; ++u) any |= __ballot(e[i0 + u] + fma(-beta, c[u].y, c[u].x) <= nb);
+                        for (int u = 0; u < 4; ++u) any |= __ballot(e[i0 + u] + c[u] <= nb);
                     }
                 }
                 if (any) {  // rare: the same tests again (steps of the run only), exact scores, new beta
@@ -242,8 +265,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
 #pragma unroll
                     for (int i = 0; i < WMAX; ++i) {
                         if (i < lim) {
-                            const double2 c = en[t0 + i];
-                            if (e[i] + fma(-beta, c.y, c.x) <= nb) cm |= 1u << i;
+                            if (e[i] + stepv(t0 + i) <= nb) cm |= 1u << i;
                         }
                     }
                     for (; cm; cm &= cm - 1) exact(t0 + __ffs(cm) - 1);
@@ -282,12 +304,9 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                     for (int j = 1; j < WMAX; ++j) {
                         if (j < l) {
                             const double nb = thr - (B + e[j]);
-                            const double2 *cj = en + tl + j * (j - 1) / 2;
+                            const int tj = tl + j * (j - 1) / 2;
 #pragma unroll
-                            for (int i = 0; i < j; ++i) {
-                                const double2 c = cj[i];
-                                any |= __ballot(e[i] + fma(-beta, c.y, c.x) <= nb);
-                            }
+                            for (int i = 0; i < j; ++i) any |= __ballot(e[i] + stepv(tj + i) <= nb);
                         }
                     }
                     if (any) {  // rare: the same tests again, exact scores, new beta
@@ -301,8 +320,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
 #pragma unroll
                             for (int i = 0; i < WMAX; ++i) {
                                 if (i < j) {
-                                    const double2 c = en[tj + i];
-                                    if (e[i] + fma(-beta, c.y, c.x) <= nb) cm |= 1u << i;
+                                    if (e[i] + stepv(tj + i) <= nb) cm |= 1u << i;
                                 }
                             }
                             for (; cm; cm &= cm - 1) exact(tj + __ffs(cm) - 1);
@@ -335,11 +353,11 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
         // the round only widens the filter of the remaining steps)
         for (int t0 = 0; t0 < steps; t0 += 4) {
             uint2 w[4];
-            double2 c[4];
+            double c[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 w[u] = io[t0 + u];
-                c[u] = en[t0 + u];
+                c[u] = stepv(t0 + u);
             }
             bool cand[4];
             uint64_t any = 0;
@@ -347,7 +365,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 y += er[w[u].x] - er[w[u].y];
-                const double f = y + fma(-beta, c[u].y, c[u].x);
+                const double f = y + c[u];
                 cand[u] = f <= thr;
                 any |= __ballot(cand[u]);  // wave masks: or-ed on the scalar unit
             }

@@ -29,6 +29,8 @@
 // (h, a run of up to 64 owned parts) are taken by the waves of the row's
 // workgroup from a shared counter, longest first.  Reported gaps are
 // recomputed from the d-dimensional residual sums of the chosen sets.
+#include <type_traits>
+
 #include "fw_internal.hpp"
 #include "instance64.hpp"
 #include "revdoor.hpp"
@@ -47,11 +49,13 @@ __host__ __device__ inline int gram_pitch(int n) { return n | 1; }
 constexpr size_t kSubsetLdsKeep = 40 * 1024;  // four workgroups per CU
 
 struct SubsetLds {
-    size_t gm, pz, mu, ent, pl, vs, red, ctr, total;
+    size_t gm, pz, mu, ent, pl, vs, red, ctr, wt, total;
     bool keep_vs;
 };
 
-__host__ __device__ inline SubsetLds subset_lds(int n, int d, int k, int nent, int nt) {
+// ht: each wave also keeps the walk's step values at its own beta (nent
+// doubles per wave)
+__host__ __device__ inline SubsetLds subset_lds(int n, int d, int k, int nent, int nt, bool ht) {
     SubsetLds L{};
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t at = o; o = align_up(o + bytes, 16); return at; };
@@ -60,8 +64,9 @@ __host__ __device__ inline SubsetLds subset_lds(int n, int d, int k, int nent, i
     L.mu = take((size_t)d * 8);
     const size_t tab = (size_t)nent * 16 + (size_t)nent * 8;
     const size_t vsb = (size_t)n * instance_pitch(d) * 4;
-    L.red = take((size_t)nt * 16);
+    L.red = take((size_t)(nt / 64) * 3 * 8);   // two doubles and one mask per wave
     L.ctr = take(16);
+    L.wt = take(ht ? (size_t)(nt / 64) * nent * 8 : 0);
     // the values stay staged through the walk when that keeps four
     // workgroups per CU; otherwise the walk tables overlay them and they
     // are staged again for the reported errors
@@ -174,7 +179,7 @@ __global__ void __launch_bounds__(64) enum_owned_kernel(EnumPlan p, const EnumJo
     omk[(size_t)(p.njobs + j) * 64 + lane] = keys;
 }
 
-template <typename T, int WMAX>
+template <typename T, int WMAX, bool HT>
 __global__ void __launch_bounds__(kSubsetThreads, 4)
 best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
                    const float *__restrict__ scale, const float *__restrict__ bias, EnumPlan pl,
@@ -185,7 +190,7 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
     extern __shared__ __align__(16) unsigned char smem[];
     const int NT = blockDim.x;
     const int n = pl.n, d = pl.d, kk = pl.k;
-    const SubsetLds L = subset_lds(n, d, kk, pl.nent, NT);
+    const SubsetLds L = subset_lds(n, d, kk, pl.nent, NT, HT);
     double *Gm = (double *)(smem + L.gm);
     double *ps = (double *)(smem + L.pz);
     double *zs = ps + n;
@@ -194,8 +199,9 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
     double *PLt = (double *)(smem + L.pl);     // p(L)
     float *Vs = (float *)(smem + L.vs);
     double *redd = (double *)(smem + L.red);
-    uint64_t *redm = (uint64_t *)(redd + NT);
+    uint64_t *redm = (uint64_t *)(redd + 2 * (NT >> 6));
     int *ctr = (int *)(smem + L.ctr);
+    double *wtab = (double *)(smem + L.wt);
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int64_t r = blockIdx.x;
@@ -208,7 +214,8 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
     // top-k set: rank by (z desc, index asc)
     const uint64_t top_mask = topk_mask64(zs, n, kk, topk_idx ? topk_idx + r * kk : nullptr);
     // (instance64 ends with a barrier: the walk tables may overlay Vs)
-    const uint64_t best = enum_best_body<WMAX>(pl, Gm, ps, top_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd, redm, ctr);
+    const uint64_t best = enum_best_body<WMAX, HT>(pl, Gm, ps, top_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd,
+                                                   redm, ctr, false, nullptr, wtab);
     if (tid == 0) {
         int i = 0;
         for (uint64_t a = best; a; a &= a - 1) best_idx[r * kk + i++] = __ffsll((unsigned long long)a) - 1;
@@ -265,25 +272,34 @@ hipError_t launch_best_subset(const fw_rows &rows, int k, int32_t *best_idx, flo
     hipError_t e = launch_enum_tables(p, W, st);
     if (e != hipSuccess) return e;
     const int nt = kSubsetThreads;
-    const SubsetLds L = subset_lds(p.n, p.d, k, p.nent, nt);
-    if (L.total > 160 * 1024) return hipErrorInvalidConfiguration;
-    const unsigned R = (unsigned)(rows.H * rows.G);
     // a narrower walk register file when every walked range allows it
     int wmax = 0;
     for (int q = 0; q < p.ncls; ++q) wmax = p.cls[q].wn > wmax ? p.cls[q].wn : wmax;
+    // per-wave step values when they fit beside the staged values within four
+    // workgroups per CU
+    const SubsetLds Lh = subset_lds(p.n, p.d, k, p.nent, nt, true);
+    const bool ht = Lh.keep_vs && Lh.total <= kSubsetLdsKeep;
+    const SubsetLds L = ht ? Lh : subset_lds(p.n, p.d, k, p.nent, nt, false);
+    if (L.total > 160 * 1024) return hipErrorInvalidConfiguration;
+    const unsigned R = (unsigned)(rows.H * rows.G);
     auto go = [&](auto kern, const auto *q, const auto *k, const auto *v) {
         hipLaunchKernelGGL(kern, dim3(R), dim3(nt), L.total, st, q, k, v, rows.scale, rows.bias, p, W.io, W.wmk,
                            W.jobs, W.omk, best_idx, best_gap, topk_gap, closed, dropped_topk, topk_idx);
     };
-    if (rows.dtype == FW_BF16) {
-        const uint16_t *q = (const uint16_t *)rows.q, *k = (const uint16_t *)rows.k, *v = (const uint16_t *)rows.v;
-        if (wmax <= 12) go(best_subset_kernel<uint16_t, 12>, q, k, v);
-        else go(best_subset_kernel<uint16_t, kMaxWalk>, q, k, v);
-    } else {
-        const float *q = (const float *)rows.q, *k = (const float *)rows.k, *v = (const float *)rows.v;
-        if (wmax <= 12) go(best_subset_kernel<float, 12>, q, k, v);
-        else go(best_subset_kernel<float, kMaxWalk>, q, k, v);
-    }
+    auto pick = [&](const auto *q, const auto *k, const auto *v) {
+        using T = std::remove_cv_t<std::remove_pointer_t<decltype(q)>>;
+        if (wmax <= 12) {
+            if (ht) go(best_subset_kernel<T, 12, true>, q, k, v);
+            else go(best_subset_kernel<T, 12, false>, q, k, v);
+        } else {
+            if (ht) go(best_subset_kernel<T, kMaxWalk, true>, q, k, v);
+            else go(best_subset_kernel<T, kMaxWalk, false>, q, k, v);
+        }
+    };
+    if (rows.dtype == FW_BF16)
+        pick((const uint16_t *)rows.q, (const uint16_t *)rows.k, (const uint16_t *)rows.v);
+    else
+        pick((const float *)rows.q, (const float *)rows.k, (const float *)rows.v);
     return hipGetLastError();
 }
 
