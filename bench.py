@@ -32,7 +32,7 @@ def _args():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--only", default="", help="comma list: topk,exhaustive,swap,pool,poolcap,vote,curve,tiny,copy")
+    ap.add_argument("--only", default="", help="comma list: topk,exhaustive,swap,pool,poolcap,vote,curve,tiny,copy (copy: device copy and read)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--cpu-configs", action="store_true",
@@ -587,6 +587,17 @@ def main():
                            "ms": round(ms, 4), "bytes_read": nbytes, "bytes_written": nbytes})
         del src, dst
         _progress("copy done")
+        # a plain streaming read (a library reduction over 8 GiB): the HBM read
+        # rate a kernel can reach on this part, context for the HBM-bound lines
+        nbytes = 8 << 30
+        src = torch.ones(nbytes // 8, dtype=torch.int64, device="cuda")
+        ms, _, _ = _time(torch, lambda: src.sum(), a.steps, a.warmup)
+        components.append({"workload": "device read 8 GiB", "metric": "GB/s",
+                           "value": round(nbytes / (ms / 1e3) / 1e9, 1), "unit": "GB/s",
+                           "ms": round(ms, 4), "bytes_read": nbytes,
+                           "note": "torch.sum over int64: achievable read rate, context only"})
+        del src
+        _progress("read done")
 
     if head is None:
         print(json.dumps({"components": components}))
