@@ -1,11 +1,14 @@
 // Enumeration plan of every k-subset of n <= 64 keys (shared by the
 // exhaustive best subset and the candidate-set search): the keys split into
-// a low range [0, m) and a high range [m, n); every k-subset is a high part H
-// (|H| = h) plus a low part (|L| = k - h).  For each h one part is owned by a
-// lane and the other is walked in revolving-door order over its range (at
-// most 16 keys) by all lanes of a wave in lockstep.  The host picks m and,
-// per h, which part the lanes own, to minimise walk steps plus per-lane
-// set-up; the device builds the walk tables and the job list from the plan.
+// two or three consecutive ranges, and every k-subset into its parts in
+// them.  A class fixes how many keys each range holds; in a class one range's
+// part is walked in revolving-door order over that range (at most 16 keys)
+// by all lanes of a wave in lockstep, and the other parts together are owned
+// by a lane.  The host picks the split and, per class, the walked range, to
+// minimise walk steps plus per-lane set-up; the device builds the walk tables
+// and the job list from the plan.  Three ranges pay off when two would leave
+// many classes with a long owned part and a walk of a step or two (a pool
+// dropping six of 38 keys); the split with the lower estimated cost wins.
 #pragma once
 
 #include "fw_common.hpp"
@@ -14,23 +17,28 @@ namespace fw {
 
 constexpr int kMaxWalk = 16;      // walked range size (per-lane e[] in registers)
 constexpr int kMaxEntries = 4096; // walk-table entries per row (LDS)
-constexpr int kMaxClass = 17;     // values of h with work (min(m, n - m) + 1)
+constexpr int kMaxClass = 32;     // classes with work (plans needing more are not taken)
 constexpr int kColexMax = 3;      // walked parts of at most this many keys run in colex order
 constexpr int kFastOwned = 8;     // owned parts of at most this many keys take the unrolled set-up
 
-// One value of h: which part the lanes own and which is walked.
+// One class: the walked part and the one or two owned parts (16-bit
+// fields: four budgets' plans travel in one kernel argument block).
 struct EnumClass {
-    int h;
-    int wb, wn, ws;  // walked part: range [wb, wb + wn), size ws
-    int lb, ln, ls;  // owned part: range [lb, lb + ln), size ls
-    int toff;        // first walk-table entry
+    int16_t wb, wn, ws;     // walked part: range [wb, wb + wn), size ws
+    int16_t lb, ln, ls;     // owned part: range [lb, lb + ln), size ls
+    int16_t lb2, ln2, ls2;  // second owned part (ln2 = 0: none)
+    int16_t toff;           // first walk-table entry (< kMaxEntries)
 };
+__host__ __device__ inline int owned_keys(const EnumClass &C) { return C.ls + C.ls2; }
+__host__ __device__ inline uint64_t owned_count(const EnumClass &C) {
+    return binom(C.ln, C.ls) * (C.ln2 ? binom(C.ln2, C.ls2) : 1ull);
+}
 
 // Enumeration plan shared by host (sizes) and device (tables, jobs).
 struct EnumPlan {
     int n, k, d, G;
     int gp;  // Gram row pitch (doubles), >= n
-    int m;
+    int m, m2;  // ranges [0, m), [m, m2), [m2, n) (two ranges: m2 = n)
     int ncls;
     EnumClass cls[kMaxClass];
     int nent;  // walk-table entries
@@ -58,6 +66,7 @@ __host__ __device__ inline bool plan_for(int n, int k, int m, EnumPlan *P, doubl
     p.k = k;
     p.gp = n;
     p.m = m;
+    p.m2 = n;
     const int N = n - m;
     const int hlo = k - m > 0 ? k - m : 0, hhi = k < N ? k : N;
     if (hlo > hhi || hhi - hlo + 1 > kMaxClass) return false;
@@ -73,8 +82,7 @@ __host__ __device__ inline bool plan_for(int n, int k, int m, EnumPlan *P, doubl
         const double cA = okA ? ceil64(binom(N, h)) * job_cost(m, kw, N, h) : 0.0;
         const double cB = okB ? ceil64(binom(m, kw)) * job_cost(N, h, m, kw) : 0.0;
         const bool useA = okA && (!okB || cA <= cB);
-        EnumClass c;
-        c.h = h;
+        EnumClass c{};
         if (useA) {
             c.wb = 0; c.wn = m; c.ws = kw; c.lb = m; c.ln = N; c.ls = h;
             if (toffA[kw] < 0) { toffA[kw] = (int)nent; nent += pad4(binom(m, kw)); }
@@ -85,9 +93,59 @@ __host__ __device__ inline bool plan_for(int n, int k, int m, EnumPlan *P, doubl
             c.toff = toffB[h];
         }
         total += useA ? cA : cB;
-        njobs += (uint64_t)ceil64(binom(c.ln, c.ls));
+        njobs += (uint64_t)ceil64(owned_count(c));
         p.cls[p.ncls++] = c;
     }
+    if (nent > (uint64_t)kMaxEntries || njobs > (1u << 17)) return false;
+    p.nent = (int)nent;
+    p.njobs = (int)njobs;
+    *P = p;
+    *cost = total;
+    return true;
+}
+
+// Three ranges [0, m1), [m1, m2), [m2, n): every split of k into (h0, h1, h2)
+// is a class; its walked range is the one (of at most kMaxWalk keys) with the
+// least estimated cost, the lanes owning the other two parts.
+__host__ inline bool plan_for3(int n, int k, int m1, int m2, EnumPlan *P, double *cost) {
+    EnumPlan p{};
+    p.n = n;
+    p.k = k;
+    p.gp = n;
+    p.m = m1;
+    p.m2 = m2;
+    const int rb[3] = {0, m1, m2}, rn[3] = {m1, m2 - m1, n - m2};
+    int toff[3][kMaxWalk + 1];
+    for (int r = 0; r < 3; ++r)
+        for (int q = 0; q <= kMaxWalk; ++q) toff[r][q] = -1;
+    double total = 0.0;
+    uint64_t nent = 0, njobs = 0;
+    for (int h0 = 0; h0 <= rn[0] && h0 <= k; ++h0)
+        for (int h1 = 0; h1 <= rn[1] && h0 + h1 <= k; ++h1) {
+            const int h2 = k - h0 - h1;
+            if (h2 > rn[2]) continue;
+            const int h[3] = {h0, h1, h2};
+            int bw = -1;
+            double bc = 0.0;
+            for (int r = 0; r < 3; ++r) {
+                if (rn[r] > kMaxWalk) continue;
+                const int a = (r + 1) % 3, b = (r + 2) % 3;
+                const double c = ceil64(binom(rn[a], h[a]) * binom(rn[b], h[b])) *
+                                 job_cost(rn[r], h[r], rn[a] + rn[b], h[a] + h[b]);
+                if (bw < 0 || c < bc) { bw = r; bc = c; }
+            }
+            if (bw < 0 || p.ncls == kMaxClass) return false;
+            const int a = bw == 0 ? 1 : 0, b = bw == 2 ? 1 : 2;   // owned ranges, ascending
+            EnumClass c{};
+            c.wb = rb[bw]; c.wn = rn[bw]; c.ws = h[bw];
+            c.lb = rb[a]; c.ln = rn[a]; c.ls = h[a];
+            c.lb2 = rb[b]; c.ln2 = rn[b]; c.ls2 = h[b];
+            if (toff[bw][c.ws] < 0) { toff[bw][c.ws] = (int)nent; nent += pad4(binom(c.wn, c.ws)); }
+            c.toff = toff[bw][c.ws];
+            total += bc;
+            njobs += (uint64_t)ceil64(owned_count(c));
+            p.cls[p.ncls++] = c;
+        }
     if (nent > (uint64_t)kMaxEntries || njobs > (1u << 17)) return false;
     p.nent = (int)nent;
     p.njobs = (int)njobs;
@@ -99,15 +157,46 @@ __host__ __device__ inline bool plan_for(int n, int k, int m, EnumPlan *P, doubl
 __host__ inline bool choose_plan(int64_t n, int k, EnumPlan *out, double *cost_out = nullptr) {
     bool found = false;
     double best = 0.0;
-    for (int m = 1; m <= (int)n; ++m) {
-        EnumPlan p;
-        double c;
-        if (!plan_for((int)n, k, m, &p, &c)) continue;
+    auto take = [&](const EnumPlan &p, double c) {
         if (!found || c < best) {
             best = c;
             *out = p;
             found = true;
         }
+    };
+    for (int m = 1; m <= (int)n; ++m) {
+        EnumPlan p;
+        double c;
+        if (plan_for((int)n, k, m, &p, &c)) take(p, c);
+    }
+    // Three ranges, near an even split (a few dozen candidates), only when
+    // the estimate is well below the best two-range plan's: three ranges walk
+    // shorter ranges, more of them in revolving-door order (dearer steps
+    // than the colex walks the estimate prices), and their longer walk tables
+    // can leave no LDS for the per-wave step values.  Measured: n = 38, k = 6
+    // at 0.55 of the two-range estimate ran 2.1 times faster; n = 24, k = 6 at
+    // 0.83 ran 1.24 times slower.
+    const int N = (int)n;
+    const bool two = found;
+    const double best2 = best;
+    EnumPlan p3{};
+    double c3 = 0.0;
+    bool f3 = false;
+    for (int m1 = N / 3 - 3; m1 <= N / 3 + 3; ++m1)
+        for (int m2 = 2 * N / 3 - 3; m2 <= 2 * N / 3 + 3; ++m2) {
+            if (m1 < 1 || m2 <= m1 || m2 >= N) continue;
+            EnumPlan p;
+            double c;
+            if (plan_for3(N, k, m1, m2, &p, &c) && (!f3 || c < c3)) {
+                p3 = p;
+                c3 = c;
+                f3 = true;
+            }
+        }
+    if (f3 && (!two || c3 < 0.7 * best2)) {
+        *out = p3;
+        best = c3;
+        found = true;
     }
     if (found && cost_out) *cost_out = best;
     return found;

@@ -134,7 +134,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
             ok_next = g_okx[(size_t)jn_next * 64 + lane];
         }
         const EnumClass C = pl.cls[jb.cls];
-        const int wb = C.wb, wn = C.wn, ws = C.ws, ls = C.ls;
+        const int wb = C.wb, wn = C.wn, ws = C.ws, ls = owned_keys(C);
         const bool act = lane < jb.lanes;
         // owned part of this lane (precomputed key mask; 0 on idle lanes):
         // p(O), S(O) and E[x] = sum_{a in O} Gm_{a, wb + x} over the walked range

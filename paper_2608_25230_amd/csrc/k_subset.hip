@@ -138,12 +138,12 @@ __global__ void enum_plan_kernel(EnumPlan p, uint2 *io, uint64_t *wmk, EnumJob *
         double best = 0.0;
         for (int q = 0; q < p.ncls; ++q) {
             const EnumClass &C = p.cls[q];
-            const double cq = job_cost(C.wn, C.ws, C.ln, C.ls);
+            const double cq = job_cost(C.wn, C.ws, C.ln + C.ln2, owned_keys(C));
             if (!done[q] && (qb < 0 || cq > best)) { qb = q; best = cq; }
         }
         done[qb] = true;
         const EnumClass &C = p.cls[qb];
-        const uint64_t tot = binom(C.ln, C.ls);
+        const uint64_t tot = owned_count(C);
         const int steps = (int)pad4(binom(C.wn, C.ws));
         for (uint64_t s0 = 0; s0 < tot; s0 += 64) {
             EnumJob jb;
@@ -162,16 +162,25 @@ __global__ void __launch_bounds__(64) enum_owned_kernel(EnumPlan p, const EnumJo
     const int j = blockIdx.x, lane = threadIdx.x;
     const EnumJob jb = jobs[j];
     const EnumClass &C = p.cls[jb.cls];
-    uint64_t m = 0;
-    if (lane < jb.lanes) {
-        uint64_t rr = (uint64_t)jb.start + lane;
-        int c = C.ln - 1;
-        for (int sz = C.ls; sz >= 1; --sz) {
+    // the colex rank of an ls-subset of [lb, lb + ln) as a key mask
+    auto unrank = [](uint64_t rr, int lb, int ln, int ls) {
+        uint64_t m = 0;
+        int c = ln - 1;
+        for (int sz = ls; sz >= 1; --sz) {
             while (binom(c, sz) > rr) --c;
-            m |= 1ull << (C.lb + c);
+            m |= 1ull << (lb + c);
             rr -= binom(c, sz);
             --c;
         }
+        return m;
+    };
+    uint64_t m = 0;
+    if (lane < jb.lanes) {
+        // rank = first part's rank x (second part's count) + second part's rank
+        const uint64_t rr = (uint64_t)jb.start + lane;
+        const uint64_t n2 = C.ln2 ? binom(C.ln2, C.ls2) : 1ull;
+        m = unrank(rr / n2, C.lb, C.ln, C.ls);
+        if (C.ln2) m |= unrank(rr % n2, C.lb2, C.ln2, C.ls2);
     }
     omk[(size_t)j * 64 + lane] = m;
     uint64_t keys = 0;   // the first eight keys of the part, ascending, a byte each
