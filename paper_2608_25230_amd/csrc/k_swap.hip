@@ -154,7 +154,7 @@ struct SwapState {
     int nblk;
 };
 
-constexpr int kSwapCand = 4096;  // surviving pairs kept per row
+constexpr int kSwapCand = 8192;  // surviving pairs kept per row (8192 and 16384 measured alike, 4096 11 % slower)
 constexpr int kSwapSweepRows = 64;  // rows a fallback sweep takes at a time
 constexpr int kSwapSL = 16;      // keys per slice of the bound pass's whole-slice test (<= 32)
 constexpr int kSwapSort = 2048;  // kept keys ordered for the bound pass
