@@ -86,49 +86,50 @@ __host__ __device__ inline SubsetLds subset_lds(int n, int d, int k, int nent, i
 // revolving-door order, where entry t also holds the keys entering and
 // leaving at step t relative to the range -- as masks of the walked part
 // (absolute key positions), and the job list, longest jobs first.
-__global__ void enum_plan_kernel(EnumPlan p, uint2 *io, uint64_t *wmk, EnumJob *jobs) {
-    if (blockIdx.x != 0) return;
-    int c[kMaxWalk + 2];
-    // one lane per class (the tables are independent)
-    if (const int q = threadIdx.x; q < p.ncls) {
-        const EnumClass &C = p.cls[q];
+__global__ void __launch_bounds__(256) enum_plan_kernel(EnumPlan p, uint2 *io, uint64_t *wmk, EnumJob *jobs) {
+    // Walk tables: block row y builds class y's table (unless an earlier
+    // class shares it), one entry per thread, each entry unranked on its own:
+    // colex order by the combinatorial number system, the revolving-door
+    // order by revdoor_unrank; a revolving-door step's entering and leaving
+    // keys are the bits in which it differs from the step before.
+    {
+        const EnumClass &C = p.cls[blockIdx.y];
         bool first = true;  // tables are shared by classes with the same walk
-        for (int q2 = 0; q2 < q; ++q2)
+        for (int q2 = 0; q2 < (int)blockIdx.y; ++q2)
             if (p.cls[q2].toff == C.toff) first = false;
-        if (first) {
-            int t = C.toff;
-            uint32_t rel = C.ws == 0 ? 0u : ((1u << C.ws) - 1u);
-            io[t] = make_uint2(0u, 0u);
-            wmk[t] = (uint64_t)rel << C.wb;
-            if (C.ws <= kColexMax) {
-                // colex order: Gosper's successor (the next larger integer with
-                // the same number of bits)
-                const int cnt = (int)binom(C.wn, C.ws);
-                for (int e = 1; e < cnt; ++e) {
-                    const uint32_t low = rel & (~rel + 1u), r = rel + low;
-                    rel = (((r ^ rel) >> 2) >> (__ffs(low) - 1)) | r;
-                    ++t;
-                    io[t] = make_uint2(0u, 0u);
-                    wmk[t] = (uint64_t)rel << C.wb;
-                }
-            } else if (C.ws > 0 && C.ws < C.wn) {
-                revdoor_init(c, C.ws, C.wn);
-                int in, out;
-                while (revdoor_next(c, C.ws, &in, &out)) {
-                    ++t;
-                    rel ^= (1u << in) ^ (1u << out);
-                    io[t] = make_uint2((uint32_t)in, (uint32_t)out);
-                    wmk[t] = (uint64_t)rel << C.wb;
-                }
+        const uint64_t cnt = binom(C.wn, C.ws), end = pad4(cnt);
+        const bool colex = C.ws <= kColexMax;
+        auto colex_mask = [&](uint64_t rr) {
+            uint64_t m = 0;
+            int c = C.wn - 1;
+            for (int sz = C.ws; sz >= 1; --sz) {
+                while (binom(c, sz) > rr) --c;
+                m |= 1ull << c;
+                rr -= binom(c, sz);
+                --c;
             }
-            const int end = C.toff + (int)pad4(binom(C.wn, C.ws));
-            for (++t; t < end; ++t) {  // neutral steps: no key moves, never a candidate
-                io[t] = make_uint2(0u, 0u);
-                wmk[t] = kPadMask;
+            return m;
+        };
+        for (uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; first && t < end;
+             t += (uint64_t)gridDim.x * blockDim.x) {
+            const size_t at = (size_t)C.toff + t;
+            if (t >= cnt) {  // neutral steps: no key moves, never a candidate
+                io[at] = make_uint2(0u, 0u);
+                wmk[at] = kPadMask;
+                continue;
             }
+            const uint64_t rel = colex ? colex_mask(t) : revdoor_unrank(t, C.wn, C.ws);
+            uint2 st = make_uint2(0u, 0u);
+            if (!colex && t > 0) {
+                const uint64_t prev = revdoor_unrank(t - 1, C.wn, C.ws);
+                st = make_uint2((uint32_t)(__ffsll((unsigned long long)(rel & ~prev)) - 1),
+                                (uint32_t)(__ffsll((unsigned long long)(prev & ~rel)) - 1));
+            }
+            io[at] = st;
+            wmk[at] = rel << C.wb;
         }
     }
-    if (threadIdx.x != 0) return;
+    if (blockIdx.x != 0 || blockIdx.y != 0 || threadIdx.x != 0) return;
     // jobs: classes in order of decreasing job cost
     int nj = 0;
     bool done[kMaxClass];
@@ -252,7 +253,8 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
 }
 
 hipError_t launch_enum_tables(const EnumPlan &p, const EnumTables &W, hipStream_t st) {
-    hipLaunchKernelGGL(enum_plan_kernel, dim3(1), dim3(64), 0, st, p, W.io, W.wmk, W.jobs);
+    // up to kMaxEntries entries per table over 16 blocks of 256 threads
+    hipLaunchKernelGGL(enum_plan_kernel, dim3(16, (unsigned)p.ncls), dim3(256), 0, st, p, W.io, W.wmk, W.jobs);
     hipLaunchKernelGGL(enum_owned_kernel, dim3((unsigned)p.njobs), dim3(64), 0, st, p,
                        (const EnumJob *)W.jobs, W.omk);
     return hipGetLastError();

@@ -1,13 +1,19 @@
 // Host check of the enumeration plans (enum_plan.hpp) and of the owned-part
 // unranking the job kernel uses: for each (n, k), the classes of the chosen
 // plan, each an owned part (one or two ranges) times a walked part, cover
-// every k-subset of {0..n-1} exactly once.  Prints "plans OK" on success.
+// every k-subset of {0..n-1} exactly once.  Also the walk tables' entries as
+// the table kernel forms them, each on its own (colex by the combinatorial
+// number system, revolving door by unranking, a step's keys from the bits in
+// which it differs from the step before), against the sequential walks
+// (Gosper's successor, Algorithm R).  Prints "plans OK" on success.
 #include <cstdio>
 #include <cstdint>
 #include <unordered_set>
+#include <utility>
 #include <vector>
 
 #include "enum_plan.hpp"
+#include "revdoor.hpp"
 
 using namespace fw;
 
@@ -74,13 +80,56 @@ static bool check(int n, int k, bool enumerate) {
     return !enumerate || seen.size() == binom(n, k);
 }
 
+static bool tables_match() {
+    for (int wn = 1; wn <= kMaxWalk; ++wn)
+        for (int ws = 0; ws <= wn; ++ws) {
+            const uint64_t cnt = binom(wn, ws);
+            std::vector<uint64_t> seq;
+            std::vector<std::pair<int, int>> steps;
+            uint32_t rel = ws == 0 ? 0u : ((1u << ws) - 1u);
+            seq.push_back(rel);
+            steps.push_back({0, 0});
+            if (ws <= kColexMax) {
+                for (uint64_t e = 1; e < cnt; ++e) {
+                    const uint32_t low = rel & (~rel + 1u), r = rel + low;
+                    rel = (((r ^ rel) >> 2) >> (__builtin_ffs(low) - 1)) | r;
+                    seq.push_back(rel);
+                    steps.push_back({0, 0});
+                }
+            } else if (ws > 0 && ws < wn) {
+                int c[kMaxWalk + 2], in, out;
+                revdoor_init(c, ws, wn);
+                while (revdoor_next(c, ws, &in, &out)) {
+                    rel ^= (1u << in) ^ (1u << out);
+                    seq.push_back(rel);
+                    steps.push_back({in, out});
+                }
+            }
+            if (seq.size() != cnt) return false;
+            for (uint64_t t = 0; t < cnt; ++t) {
+                const uint64_t m = ws <= kColexMax ? unrank(t, 0, wn, ws) : revdoor_unrank(t, wn, ws);
+                int in = 0, out = 0;
+                if (ws > kColexMax && t > 0) {
+                    const uint64_t pv = revdoor_unrank(t - 1, wn, ws);
+                    in = __builtin_ffsll(m & ~pv) - 1;
+                    out = __builtin_ffsll(pv & ~m) - 1;
+                }
+                if (m != seq[t] || in != steps[t].first || out != steps[t].second) {
+                    printf("walk table (%d, %d) differs at step %llu\n", wn, ws, (unsigned long long)t);
+                    return false;
+                }
+            }
+        }
+    return true;
+}
+
 int main() {
     // the benchmark's plans (n = 24, k = 6; the candidate sets' kept and
     // dropped plans, among them the widened cap's 5 and 6 of 37 and 38) and
     // edge shapes
     const int cases[][2] = {{24, 6}, {38, 6}, {37, 5}, {28, 4}, {20, 8}, {22, 6}, {36, 4}, {16, 4}, {12, 5},
                             {30, 3}, {40, 4}, {64, 2}, {26, 13}, {10, 10}, {9, 1}, {1, 1}, {33, 16}};
-    bool ok = true;
+    bool ok = tables_match();
     for (const auto &c : cases) ok = check(c[0], c[1], binom(c[0], c[1]) <= 3000000) && ok;
     puts(ok ? "plans OK" : "plans FAILED");
     return ok ? 0 : 1;
