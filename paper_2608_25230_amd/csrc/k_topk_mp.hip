@@ -418,10 +418,13 @@ __global__ void __launch_bounds__(MTH, 1) topk_mp_kernel(FusedArgs a) {
     ring_barrier();   // every wave is done with the key ring; lists complete
 
     // ---- exact k-th key of every budget, per row ---------------------------
-    // Row r's list holds c <= 128 entries: lane L takes entries L and L + 64
-    // and ranks each among the entries of its own bin by counting the larger
-    // ones; a budget's key is the entry of rank need - 1 in its threshold
-    // bin.  Entries of that bin equal to it in logit but with a larger index
+    // Row r's list holds c <= 128 entries: lane L takes entries L and L + 64,
+    // and a bitonic network over the 128 slots (zeros past c, below every
+    // entry) sorts them descending, that is by logit desc, then index asc,
+    // with each bin's entries contiguous (bins run from the highest logits).
+    // A budget's key is then the entry need - 1 places after the start of its
+    // threshold bin, which follows the listed entries of the higher listed
+    // bins.  Entries of that bin equal to it in logit but with a larger index
     // are outside the set although their logit reaches the threshold: they are
     // listed as corrections for the tier products (budget << 16 | key).
     float tz[NK];
@@ -433,48 +436,60 @@ __global__ void __launch_bounds__(MTH, 1) topk_mp_kernel(FusedArgs a) {
         if (__builtin_amdgcn_readlane((int)bad, r)) continue;   // wave-uniform: the fallback recomputes the row
         const int c = __builtin_amdgcn_readlane(rtot, r);
         const int rb = __builtin_amdgcn_readlane(pbase, r);
-        int rtb[NK], rneed[NK];
+        int rtb[NK], rneed[NK], rcnt[NK];
 #pragma unroll
         for (int kk = 0; kk < NK; ++kk) {
             rtb[kk] = __builtin_amdgcn_readlane(tb[kk], r);
             rneed[kk] = __builtin_amdgcn_readlane(need[kk], r);
+            rcnt[kk] = __builtin_amdgcn_readlane(cntb[kk], r);
         }
         const unsigned long long *lp = pool + rb;
-        const unsigned long long e0 = lane < c ? lp[lane] : 0ull;
-        const unsigned long long e1 = lane + 64 < c ? lp[lane + 64] : 0ull;
-        const uint32_t b0 = ((uint32_t)e0 >> 16) & 0xFFFFu, b1 = ((uint32_t)e1 >> 16) & 0xFFFFu;
-        int rk0 = 0, rk1 = 0;
-        int x = 0;
-        for (; x + 4 <= c; x += 4) {   // four independent broadcast reads per step
-            const unsigned long long f[4] = {lp[x], lp[x + 1], lp[x + 2], lp[x + 3]};
+        unsigned long long e0 = lane < c ? lp[lane] : 0ull;
+        unsigned long long e1 = lane + 64 < c ? lp[lane + 64] : 0ull;
+        // slots L (e0) and L + 64 (e1); the larger of a pair goes to the lower
+        // slot in a descending block ((slot & size) == 0), else the smaller
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const uint32_t bf = ((uint32_t)f[u] >> 16) & 0xFFFFu;
-                rk0 += (int)((bf == b0) & (f[u] > e0));
-                rk1 += (int)((bf == b1) & (f[u] > e1));
+        for (int size = 2; size <= 128; size <<= 1) {
+#pragma unroll
+            for (int stride = size >> 1; stride > 0; stride >>= 1) {
+                if (stride == 64) {   // size 128: slots L and L + 64, descending
+                    const bool sw = e0 < e1;
+                    const unsigned long long t0 = e0;
+                    e0 = sw ? e1 : e0;
+                    e1 = sw ? t0 : e1;
+                } else {
+                    const unsigned long long y0 = xlane64(e0, stride), y1 = xlane64(e1, stride);
+                    const bool lo = (lane & stride) == 0;
+                    const bool k0 = ((lane & size) == 0) == lo, k1 = (((lane + 64) & size) == 0) == lo;
+                    e0 = ((e0 > y0) == k0) ? e0 : y0;
+                    e1 = ((e1 > y1) == k1) ? e1 : y1;
+                }
             }
         }
-        for (; x < c; ++x) {
-            const unsigned long long f = lp[x];
-            const uint32_t bf = ((uint32_t)f >> 16) & 0xFFFFu;
-            rk0 += (int)((bf == b0) & (f > e0));
-            rk1 += (int)((bf == b1) & (f > e1));
-        }
+        const uint32_t b0 = ((uint32_t)e0 >> 16) & 0xFFFFu, b1 = ((uint32_t)e1 >> 16) & 0xFFFFu;
         bool fail = false;
         int xk0 = -1, xk1 = -1;   // the smallest budget each entry is a correction for
         const int j0 = (int)(0xFFFFu - ((uint32_t)e0 & 0xFFFFu)), j1 = (int)(0xFFFFu - ((uint32_t)e1 & 0xFFFFu));
 #pragma unroll
         for (int kk = NK - 1; kk >= 0; --kk) {
             if (a.ks.k[kk] >= n) continue;   // keeps every key
-            const int nd = rneed[kk];
-            const unsigned long long s0 = __ballot(lane < c && (int)b0 == rtb[kk] && rk0 == nd - 1);
-            const unsigned long long s1 = __ballot(lane + 64 < c && (int)b1 == rtb[kk] && rk1 == nd - 1);
-            if (!(s0 | s1)) { fail = true; continue; }
-            const bool in0 = s0 != 0;
-            const int fl = in0 ? __ffsll((long long)s0) - 1 : __ffsll((long long)s1) - 1;
-            const unsigned long long sel = in0 ? e0 : e1;
+            // the threshold bin starts after the listed entries of the higher
+            // listed bins (each distinct bin counted once)
+            int start = 0;
+#pragma unroll
+            for (int k2 = 0; k2 < NK; ++k2) {
+                bool first = rtb[k2] >= 0 && rtb[k2] < rtb[kk];
+#pragma unroll
+                for (int k3 = 0; k3 < k2; ++k3) first &= rtb[k3] != rtb[k2];
+                if (first) start += rcnt[k2];
+            }
+            const int pos = start + rneed[kk] - 1;
+            if (rneed[kk] < 1 || pos >= c) { fail = true; continue; }
+            const int fl = pos & 63;
+            const unsigned long long sel = pos < 64 ? e0 : e1;
             const uint32_t shi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(sel >> 32), fl);
             const uint32_t slo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)sel, fl);
+            if ((int)((slo >> 16) & 0xFFFFu) != rtb[kk]) { fail = true; continue; }
             const int ct = (int)(0xFFFFu - (slo & 0xFFFFu));
             if (rl == r) {
                 tz[kk] = key_to_float(shi);

@@ -79,6 +79,38 @@ __device__ __forceinline__ void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)"
 // across it.
 __device__ __forceinline__ void ring_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
+// the 64-bit value of lane (lane ^ M): quad permutes (DPP) for M = 1, 2,
+// swizzles within 32 lanes for M = 4 .. 16, a permute for M = 32
+template <int M>
+__device__ __forceinline__ unsigned long long xlane64(unsigned long long v) {
+    const int lo = (int)(uint32_t)v, hi = (int)(uint32_t)(v >> 32);
+    int a, b;
+    if constexpr (M == 1) {
+        a = __builtin_amdgcn_mov_dpp(lo, 0xB1, 0xF, 0xF, false);
+        b = __builtin_amdgcn_mov_dpp(hi, 0xB1, 0xF, 0xF, false);
+    } else if constexpr (M == 2) {
+        a = __builtin_amdgcn_mov_dpp(lo, 0x4E, 0xF, 0xF, false);
+        b = __builtin_amdgcn_mov_dpp(hi, 0x4E, 0xF, 0xF, false);
+    } else if constexpr (M < 32) {
+        a = __builtin_amdgcn_ds_swizzle(lo, 0x1F | (M << 10));
+        b = __builtin_amdgcn_ds_swizzle(hi, 0x1F | (M << 10));
+    } else {
+        a = __shfl_xor(lo, 32);
+        b = __shfl_xor(hi, 32);
+    }
+    return ((unsigned long long)(uint32_t)b << 32) | (uint32_t)a;
+}
+__device__ __forceinline__ unsigned long long xlane64(unsigned long long v, int m) {
+    switch (m) {   // m is a constant in the unrolled stages
+        case 1: return xlane64<1>(v);
+        case 2: return xlane64<2>(v);
+        case 4: return xlane64<4>(v);
+        case 8: return xlane64<8>(v);
+        case 16: return xlane64<16>(v);
+        default: return xlane64<32>(v);
+    }
+}
+
 struct FusedArgs {
     const uint16_t *q, *k, *v;
     const float *scale, *bias;
