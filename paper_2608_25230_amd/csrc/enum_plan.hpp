@@ -154,6 +154,25 @@ __host__ inline bool plan_for3(int n, int k, int m1, int m2, EnumPlan *P, double
     return true;
 }
 
+// Classes in order of decreasing job cost (stable): the job list follows the
+// class order, so the longest jobs are taken first.
+__host__ inline void order_classes(EnumPlan *p) {
+    double c[kMaxClass];
+    for (int q = 0; q < p->ncls; ++q) {
+        const EnumClass &C = p->cls[q];
+        c[q] = job_cost(C.wn, C.ws, C.ln + C.ln2, owned_keys(C));
+    }
+    for (int i = 1; i < p->ncls; ++i)
+        for (int j = i; j > 0 && c[j] > c[j - 1]; --j) {
+            const EnumClass t = p->cls[j];
+            p->cls[j] = p->cls[j - 1];
+            p->cls[j - 1] = t;
+            const double tc = c[j];
+            c[j] = c[j - 1];
+            c[j - 1] = tc;
+        }
+}
+
 __host__ inline bool choose_plan(int64_t n, int k, EnumPlan *out, double *cost_out = nullptr) {
     bool found = false;
     double best = 0.0;
@@ -179,6 +198,13 @@ __host__ inline bool choose_plan(int64_t n, int k, EnumPlan *out, double *cost_o
     const int N = (int)n;
     const bool two = found;
     const double best2 = best;
+    // (skipped when the two-range plan is already small: the search costs
+    // host time on every call, which a small enumeration would not recover)
+    if (two && best2 < 1e5) {
+        order_classes(out);
+        if (cost_out) *cost_out = best;
+        return true;
+    }
     EnumPlan p3{};
     double c3 = 0.0;
     bool f3 = false;
@@ -198,6 +224,7 @@ __host__ inline bool choose_plan(int64_t n, int k, EnumPlan *out, double *cost_o
         best = c3;
         found = true;
     }
+    if (found) order_classes(out);
     if (found && cost_out) *cost_out = best;
     return found;
 }
@@ -238,7 +265,7 @@ __host__ inline EnumTables enum_tables(const EnumPlan &p, void *ws) {
     return W;
 }
 
-// k_subset.hip: fills the tables of a plan (two small launches on `st`).
+// k_subset.hip: fills the tables of a plan (one small launch on `st`).
 hipError_t launch_enum_tables(const EnumPlan &p, const EnumTables &W, hipStream_t st);
 
 }  // namespace fw

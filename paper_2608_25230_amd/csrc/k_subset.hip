@@ -81,22 +81,26 @@ __host__ __device__ inline SubsetLds subset_lds(int n, int d, int k, int nent, i
 
 }  // namespace
 
-// Walk tables (row independent): for every walked (range, size) the walk's
-// sequence -- colex order for parts of at most kColexMax keys, else the
-// revolving-door order, where entry t also holds the keys entering and
-// leaving at step t relative to the range -- as masks of the walked part
-// (absolute key positions), and the job list, longest jobs first.
-__global__ void __launch_bounds__(256) enum_plan_kernel(EnumPlan p, uint2 *io, uint64_t *wmk, EnumJob *jobs) {
-    // Walk tables: block row y builds class y's table (unless an earlier
-    // class shares it), one entry per thread, each entry unranked on its own:
-    // colex order by the combinatorial number system, the revolving-door
-    // order by revdoor_unrank; a revolving-door step's entering and leaving
-    // keys are the bits in which it differs from the step before.
-    {
-        const EnumClass &C = p.cls[blockIdx.y];
-        bool first = true;  // tables are shared by classes with the same walk
-        for (int q2 = 0; q2 < (int)blockIdx.y; ++q2)
-            if (p.cls[q2].toff == C.toff) first = false;
+// Row-independent tables of a plan, one launch: blocks [0, 16 ncls) build
+// the walk tables, block row y = b / 16 class y's table (unless an earlier
+// class shares it), one entry per thread, each entry unranked on its own:
+// colex order (parts of at most kColexMax keys) by the combinatorial number
+// system, else the revolving-door order by revdoor_unrank, with the keys
+// entering and leaving at step t (relative to the range) taken from the bits
+// in which entry t differs from entry t - 1; masks hold absolute key
+// positions.  The remaining blocks hold one job per wave: jobs run through
+// the classes in plan order (the host orders them by decreasing job cost),
+// ceil(count / 64) jobs per class, and lane l of job j holds the owned part
+// of colex rank start + l (a key mask, and its first eight keys, ascending,
+// one byte each).
+__global__ void __launch_bounds__(256) enum_tables_kernel(EnumPlan p, uint2 *io, uint64_t *wmk, EnumJob *jobs,
+                                                          uint64_t *omk) {
+    const int ntab = 16 * p.ncls;
+    if ((int)blockIdx.x < ntab) {
+        const int y = blockIdx.x / 16, x = blockIdx.x % 16;
+        const EnumClass &C = p.cls[y];
+        for (int q2 = 0; q2 < y; ++q2)
+            if (p.cls[q2].toff == C.toff) return;  // built by class q2
         const uint64_t cnt = binom(C.wn, C.ws), end = pad4(cnt);
         const bool colex = C.ws <= kColexMax;
         auto colex_mask = [&](uint64_t rr) {
@@ -110,8 +114,7 @@ __global__ void __launch_bounds__(256) enum_plan_kernel(EnumPlan p, uint2 *io, u
             }
             return m;
         };
-        for (uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; first && t < end;
-             t += (uint64_t)gridDim.x * blockDim.x) {
+        for (uint64_t t = (uint64_t)x * blockDim.x + threadIdx.x; t < end; t += 16ull * blockDim.x) {
             const size_t at = (size_t)C.toff + t;
             if (t >= cnt) {  // neutral steps: no key moves, never a candidate
                 io[at] = make_uint2(0u, 0u);
@@ -128,41 +131,38 @@ __global__ void __launch_bounds__(256) enum_plan_kernel(EnumPlan p, uint2 *io, u
             io[at] = st;
             wmk[at] = rel << C.wb;
         }
+        return;
     }
-    if (blockIdx.x != 0 || blockIdx.y != 0 || threadIdx.x != 0) return;
-    // jobs: classes in order of decreasing job cost
-    int nj = 0;
-    bool done[kMaxClass];
-    for (int q = 0; q < p.ncls; ++q) done[q] = false;
-    for (int round = 0; round < p.ncls; ++round) {
-        int qb = -1;
-        double best = 0.0;
-        for (int q = 0; q < p.ncls; ++q) {
-            const EnumClass &C = p.cls[q];
-            const double cq = job_cost(C.wn, C.ws, C.ln + C.ln2, owned_keys(C));
-            if (!done[q] && (qb < 0 || cq > best)) { qb = q; best = cq; }
-        }
-        done[qb] = true;
-        const EnumClass &C = p.cls[qb];
-        const uint64_t tot = owned_count(C);
-        const int steps = (int)pad4(binom(C.wn, C.ws));
-        for (uint64_t s0 = 0; s0 < tot; s0 += 64) {
-            EnumJob jb;
-            jb.cls = qb;
-            jb.start = (int32_t)s0;
-            jb.lanes = (int32_t)((tot - s0) < 64 ? (tot - s0) : 64);
-            jb.steps = steps;
-            jobs[nj++] = jb;
-        }
+    __shared__ int jfirst[kMaxClass + 1], jsteps[kMaxClass];
+    __shared__ uint64_t jcount[kMaxClass];
+    const int tid = threadIdx.x, lane = tid & 63;
+    if (tid < p.ncls) {
+        const EnumClass &C = p.cls[tid];
+        jcount[tid] = owned_count(C);
+        jfirst[tid + 1] = ceil64(jcount[tid]);
+        jsteps[tid] = (int)pad4(binom(C.wn, C.ws));
     }
-}
-
-// Owned parts (row independent): job j, lane l holds the colex rank
-// start + l among the ls-subsets of [lb, lb + ln), as a key mask.
-__global__ void __launch_bounds__(64) enum_owned_kernel(EnumPlan p, const EnumJob *jobs, uint64_t *omk) {
-    const int j = blockIdx.x, lane = threadIdx.x;
-    const EnumJob jb = jobs[j];
-    const EnumClass &C = p.cls[jb.cls];
+    __syncthreads();
+    if (tid == 0) {
+        jfirst[0] = 0;
+        for (int q = 0; q < p.ncls; ++q) jfirst[q + 1] += jfirst[q];
+    }
+    __syncthreads();
+    const int j = (blockIdx.x - ntab) * 4 + (tid >> 6);
+    if (j >= p.njobs) return;
+    int q = 0;
+    while (q + 1 < p.ncls && jfirst[q + 1] <= j) ++q;
+    const EnumClass &C = p.cls[q];
+    const uint64_t s0 = (uint64_t)(j - jfirst[q]) * 64;
+    const int nl = (jcount[q] - s0) < 64 ? (int)(jcount[q] - s0) : 64;
+    if (lane == 0) {
+        EnumJob jb;
+        jb.cls = q;
+        jb.start = (int32_t)s0;
+        jb.lanes = nl;
+        jb.steps = jsteps[q];
+        jobs[j] = jb;
+    }
     // the colex rank of an ls-subset of [lb, lb + ln) as a key mask
     auto unrank = [](uint64_t rr, int lb, int ln, int ls) {
         uint64_t m = 0;
@@ -176,15 +176,15 @@ __global__ void __launch_bounds__(64) enum_owned_kernel(EnumPlan p, const EnumJo
         return m;
     };
     uint64_t m = 0;
-    if (lane < jb.lanes) {
+    if (lane < nl) {
         // rank = first part's rank x (second part's count) + second part's rank
-        const uint64_t rr = (uint64_t)jb.start + lane;
+        const uint64_t rr = s0 + lane;
         const uint64_t n2 = C.ln2 ? binom(C.ln2, C.ls2) : 1ull;
         m = unrank(rr / n2, C.lb, C.ln, C.ls);
         if (C.ln2) m |= unrank(rr % n2, C.lb2, C.ln2, C.ls2);
     }
     omk[(size_t)j * 64 + lane] = m;
-    uint64_t keys = 0;   // the first eight keys of the part, ascending, a byte each
+    uint64_t keys = 0;
     for (int i = 0; i < 8 && m; ++i, m &= m - 1) keys |= (uint64_t)(__ffsll((unsigned long long)m) - 1) << (8 * i);
     omk[(size_t)(p.njobs + j) * 64 + lane] = keys;
 }
@@ -253,10 +253,10 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
 }
 
 hipError_t launch_enum_tables(const EnumPlan &p, const EnumTables &W, hipStream_t st) {
-    // up to kMaxEntries entries per table over 16 blocks of 256 threads
-    hipLaunchKernelGGL(enum_plan_kernel, dim3(16, (unsigned)p.ncls), dim3(256), 0, st, p, W.io, W.wmk, W.jobs);
-    hipLaunchKernelGGL(enum_owned_kernel, dim3((unsigned)p.njobs), dim3(64), 0, st, p,
-                       (const EnumJob *)W.jobs, W.omk);
+    // up to kMaxEntries entries per table over 16 blocks of 256 threads, then
+    // four jobs per block
+    const unsigned nb = 16u * (unsigned)p.ncls + (unsigned)((p.njobs + 3) / 4);
+    hipLaunchKernelGGL(enum_tables_kernel, dim3(nb), dim3(256), 0, st, p, W.io, W.wmk, W.jobs, W.omk);
     return hipGetLastError();
 }
 

@@ -1,11 +1,12 @@
 // Host check of the enumeration plans (enum_plan.hpp) and of the owned-part
-// unranking the job kernel uses: for each (n, k), the classes of the chosen
-// plan, each an owned part (one or two ranges) times a walked part, cover
-// every k-subset of {0..n-1} exactly once.  Also the walk tables' entries as
-// the table kernel forms them, each on its own (colex by the combinatorial
-// number system, revolving door by unranking, a step's keys from the bits in
-// which it differs from the step before), against the sequential walks
-// (Gosper's successor, Algorithm R).  Prints "plans OK" on success.
+// unranking the table kernel uses: for each (n, k), the classes of the chosen
+// plan (in order of decreasing job cost), each an owned part (one or two
+// ranges) times a walked part, cover every k-subset of {0..n-1} exactly once.
+// Also the walk tables' entries as the table kernel forms them, each on its
+// own (colex by the combinatorial number system, revolving door by unranking,
+// a step's keys from the bits in which it differs from the step before),
+// against the sequential walks (Gosper's successor, Algorithm R).  Prints
+// "plans OK" on success.
 #include <cstdio>
 #include <cstdint>
 #include <unordered_set>
@@ -42,6 +43,13 @@ static bool check(int n, int k, bool enumerate) {
            p.m2, p.m2, n, p.ncls, p.njobs, p.nent);
     uint64_t total = 0;
     int jobs = 0;
+    for (int q = 1; q < p.ncls; ++q) {  // longest jobs first
+        const EnumClass &A = p.cls[q - 1], &B = p.cls[q];
+        if (job_cost(A.wn, A.ws, A.ln + A.ln2, owned_keys(A)) < job_cost(B.wn, B.ws, B.ln + B.ln2, owned_keys(B))) {
+            printf("  classes out of job-cost order\n");
+            return false;
+        }
+    }
     std::unordered_set<uint64_t> seen;
     for (int q = 0; q < p.ncls; ++q) {
         const EnumClass &C = p.cls[q];
