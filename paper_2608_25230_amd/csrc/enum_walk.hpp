@@ -29,6 +29,11 @@
 // With HT (when the LDS has room), each wave keeps its own copy of the walk
 // table's step values at its current beta, T[t] = S_W - beta p(W)^2, rebuilt
 // when beta drops, so that a step is one add and a compare.
+//
+// The test runs at half scale: e, the step values, the base terms and the
+// slack are all halved (the walk tables hold S_W / 2 and p(W)^2 / 2), which
+// moves no comparison (halving is exact) and saves the doubling of e in
+// every lane's set-up.
 #pragma once
 
 #include "enum_plan.hpp"
@@ -73,7 +78,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
             P += ps[x];
             for (uint64_t b2 = lm; b2; b2 &= b2 - 1) S += Gm[x * gp + (__ffsll((unsigned long long)b2) - 1)];
         }
-        ent[t] = make_double2(S, P * P);
+        ent[t] = make_double2(0.5 * S, 0.5 * (P * P));
         PLt[t] = P;
     }
     if (tid == 0) ctr[0] = 0;
@@ -152,18 +157,19 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
 #pragma unroll
             for (int i = 0; i < kFastOwned; ++i) {
                 if (i < ls) {
+                    // (the first key assigns: no adds of zero)
                     const double *ri = Gm + kx[i] * gp;
-                    PO += ps[kx[i]];
-                    if (cpl) CO += cv[kx[i]];
+                    PO = i ? PO + ps[kx[i]] : ps[kx[i]];
+                    if (cpl) CO = i ? CO + cv[kx[i]] : cv[kx[i]];
                     double sv = ri[kx[i]];
 #pragma unroll
                     for (int j = 0; j < i; ++j) sv = fma(2.0, ri[kx[j]], sv);
-                    SO += sv;
+                    SO = i ? SO + sv : sv;
                     if (ws > 0) {
                         // all WMAX positions, unguarded: those past the walked
                         // range read neighbouring LDS words and are never used
 #pragma unroll
-                        for (int x = 0; x < WMAX; ++x) e[x] += ri[wb + x];
+                        for (int x = 0; x < WMAX; ++x) e[x] = i ? e[x] + ri[wb + x] : ri[wb + x];
                     }
                 }
             }
@@ -185,14 +191,14 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
         const double PB = cpl ? PU - PO : PO;
         const double SB = cpl ? SU - 2.0 * CO + SO : SO;
         const double sgn = cpl ? 1.0 : -1.0;
-        if (ws > 0) {
-            const double b2p = sgn * 2.0 * beta * PB;
+        if (ws > 0) {  // e at half scale
+            const double bp = sgn * beta * PB;
             if (cpl) {
 #pragma unroll
-                for (int x = 0; x < WMAX; ++x) e[x] = fma(2.0, e[x], fma(b2p, ps[wb + x], -2.0 * cv[wb + x]));
+                for (int x = 0; x < WMAX; ++x) e[x] = fma(bp, ps[wb + x], e[x] - cv[wb + x]);
             } else {
 #pragma unroll
-                for (int x = 0; x < WMAX; ++x) e[x] = fma(2.0, e[x], b2p * ps[wb + x]);
+                for (int x = 0; x < WMAX; ++x) e[x] = fma(bp, ps[wb + x], e[x]);
             }
         }
         const double2 *en = ent + C.toff;
@@ -205,11 +211,11 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
         };
         const double *plt = PLt + C.toff;
         const uint64_t *wmk = g_wmk + C.toff;
-        double thr = 1e-12 * beta;
+        double thr = 0.5e-12 * beta;  // the slack, at half scale
         // exact score of walk step t for this lane (a candidate)
         auto exact = [&](int t) __attribute__((always_inline)) {
             const uint64_t wm = wmk[t];
-            double S = SB + en[t].x;
+            double S = SB + 2.0 * en[t].x;
             for (uint64_t a = wm; a; a &= a - 1) {
                 const int ax = __ffsll((unsigned long long)a) - 1;
                 const double *row = Gm + ax * gp;
@@ -235,7 +241,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
             if (!(wbst < beta)) return 0.0;
             const double dB = wbst - beta;
             beta = wbst;
-            thr = 1e-12 * beta;
+            thr = 0.5e-12 * beta;
             build_tw();
             return dB;
         };
@@ -272,17 +278,17 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                     const double dB = lower_beta();
 #pragma unroll
                     for (int x = 0; x < WMAX; ++x)
-                        e[x] += sgn * 2.0 * dB * PB * ps[wb + x];
+                        e[x] += sgn * dB * PB * ps[wb + x];
                 }
             };
             if (ws == 0) {
-                const double YO = act ? SB - beta * PB * PB : INFINITY;
+                const double YO = act ? 0.5 * (SB - beta * PB * PB) : INFINITY;
                 if (__ballot(YO <= thr)) {
                     if (YO <= thr) exact(0);
                     lower_beta();  // nothing is walked: e is unused
                 }
             } else if (ws == 1) {
-                run(act ? SB - beta * PB * PB : INFINITY, 0, wn);
+                run(act ? 0.5 * (SB - beta * PB * PB) : INFINITY, 0, wn);
             } else {
                 // Walked pairs {i < j} below a limit L, after an outer base B
                 // (walked triples {i < j < l}: one block per l with
@@ -297,7 +303,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
 #pragma unroll
                         for (int x = 2; x < WMAX; ++x) el = l == x ? e[x] : el;
                     }
-                    const double B = act ? SB - beta * PB * PB + el : INFINITY;
+                    const double B = act ? 0.5 * (SB - beta * PB * PB) + el : INFINITY;
                     const int tl = ws == 3 ? l * (l - 1) * (l - 2) / 6 : 0;
                     uint64_t any = 0;
 #pragma unroll
@@ -328,7 +334,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                         const double dB = lower_beta();
 #pragma unroll
                         for (int x = 0; x < WMAX; ++x)
-                            e[x] += sgn * 2.0 * dB * PB * ps[wb + x];
+                            e[x] += sgn * dB * PB * ps[wb + x];
                     }
                 }
             }
@@ -341,7 +347,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
         double er[WMAX];
 #pragma unroll
         for (int x = 0; x < WMAX; ++x) er[x] = e[x];
-        double Y = SB - beta * PB * PB;
+        double Y = 0.5 * (SB - beta * PB * PB);
 #pragma unroll
         for (int x = 0; x < WMAX; ++x)
             if (x < ws) Y += er[x];
@@ -378,11 +384,11 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                 if (dB != 0.0) {
 #pragma unroll
                     for (int x = 0; x < WMAX; ++x)
-                        er[x] += sgn * 2.0 * dB * PB * ps[wb + x];
+                        er[x] += sgn * dB * PB * ps[wb + x];
                     // Y for the round's last real step from the rescaled e
                     int tl = t0 + 3;
                     while (wmk[tl] == kPadMask) --tl;
-                    double yy = SB - beta * PB * PB;
+                    double yy = 0.5 * (SB - beta * PB * PB);
                     for (uint64_t a = wmk[tl]; a; a &= a - 1) yy += er[__ffsll((unsigned long long)a) - 1 - wb];
                     Y = act ? yy : INFINITY;
                 }
