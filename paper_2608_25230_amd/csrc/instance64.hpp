@@ -48,6 +48,83 @@ __device__ __forceinline__ void stage_rows(const T *src, int n, int d, float *ds
     stage_rows_from(src, n, d, dst, pitch, 0);
 }
 
+// The Gram entries of instance64 for L lanes per 4 x 4 block (L a power of
+// two up to 8, at most blockDim.x / L blocks at a time).  The columns a lane
+// takes are c = part + i L: a uniform count of whole rounds (d / L) and at
+// most one more, so the loads are fixed offsets from nine row pointers
+// (constants throughout for d = 128 and L >= 4).
+template <int L>
+__device__ __forceinline__ void gram_blocks(int n, int d, int pitch, int nb, int nblk, const float *Vs,
+                                            const double *ps, const double *mu, double *Gm, int gp) {
+    const int tid = threadIdx.x, NT = blockDim.x;
+    constexpr int lgL = L == 8 ? 3 : L == 4 ? 2 : L == 2 ? 1 : 0;
+    const int ntask = ((nblk * L + 63) / 64) * 64;
+    const int full = d / L;
+    for (int task = tid; task < ntask; task += NT) {
+        const int blk = task >> lgL, part = task & (L - 1);
+        int A = 0, rem = blk < nblk ? blk : 0;
+        while (rem >= nb - A) { rem -= nb - A; ++A; }
+        const int B = A + rem;
+        const float *ra[4], *rb[4];
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+            ra[x] = Vs + min(4 * A + x, n - 1) * pitch + part;
+            rb[x] = Vs + min(4 * B + x, n - 1) * pitch + part;
+        }
+        const double *mc = mu + part;
+        double sg[4][4];
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+#pragma unroll
+            for (int y = 0; y < 4; ++y) sg[x][y] = 0.0;
+        auto col = [&](int o) __attribute__((always_inline)) {
+            const double m = mc[o];
+            double va[4], vb[4];
+#pragma unroll
+            for (int x = 0; x < 4; ++x) {
+                va[x] = (double)ra[x][o] - m;
+                vb[x] = (double)rb[x][o] - m;
+            }
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+#pragma unroll
+                for (int y = 0; y < 4; ++y) sg[x][y] = fma(va[x], vb[y], sg[x][y]);
+        };
+        if (L >= 4 && d == 128) {  // the common head size: every offset a constant
+#pragma unroll
+            for (int i = 0; i < 128 / L; ++i) {
+                col(i * L);
+                if (i & 1) __builtin_amdgcn_sched_barrier(0);
+            }
+        } else {
+            int i = 0;
+            for (; i + 2 <= full; i += 2) {
+                col(i * L);
+                col((i + 1) * L);
+            }
+            for (; i < full; ++i) col(i * L);
+            if (part < d - full * L) col(full * L);
+        }
+        for (int off = 1; off < L; off <<= 1)
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+#pragma unroll
+                for (int y = 0; y < 4; ++y) sg[x][y] += __shfl_xor(sg[x][y], off);
+        if (blk < nblk) {
+            // lane `part` of the group writes entries part, part + L, .. of 16
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int ii = 4 * A + e / 4, jj = 4 * B + e % 4;
+                if ((e & (L - 1)) == part && ii < n && jj < n) {
+                    const double g = ps[ii] * ps[jj] * sg[e / 4][e % 4];
+                    Gm[ii * gp + jj] = g;
+                    Gm[jj * gp + ii] = g;
+                }
+            }
+        }
+    }
+}
+
 // Whole workgroup; n <= 64 <= blockDim.x, blockDim.x a multiple of 64.
 // Vs [n][d + 1] float (LDS) stages the keys, then the values; zs, ps [n],
 // mu [d], Gm [n][gp] (LDS, row pitch gp >= n) receive the instance.  Global
@@ -120,55 +197,11 @@ __device__ __forceinline__ void instance64(const T *qr, const T *kh, const T *vh
     const int nb = (n + 3) >> 2, nblk = nb * (nb + 1) / 2;
     int lgL = 3;
     while (lgL > 0 && (nblk << lgL) > NT) --lgL;
-    const int L = 1 << lgL;
-    const int ntask = ((nblk * L + 63) / 64) * 64;
-    for (int task = tid; task < ntask; task += NT) {
-        const int blk = task >> lgL, part = task & (L - 1);
-        int A = 0, rem = blk < nblk ? blk : 0;
-        while (rem >= nb - A) { rem -= nb - A; ++A; }
-        const int B = A + rem;
-        const float *ra[4], *rb[4];
-#pragma unroll
-        for (int x = 0; x < 4; ++x) {
-            ra[x] = Vs + min(4 * A + x, n - 1) * pitch;
-            rb[x] = Vs + min(4 * B + x, n - 1) * pitch;
-        }
-        double sg[4][4];
-#pragma unroll
-        for (int x = 0; x < 4; ++x)
-#pragma unroll
-            for (int y = 0; y < 4; ++y) sg[x][y] = 0.0;
-#pragma unroll 1
-        for (int c = part; c < d; c += L) {
-            const double m = mu[c];
-            double va[4], vb[4];
-#pragma unroll
-            for (int x = 0; x < 4; ++x) {
-                va[x] = (double)ra[x][c] - m;
-                vb[x] = (double)rb[x][c] - m;
-            }
-#pragma unroll
-            for (int x = 0; x < 4; ++x)
-#pragma unroll
-                for (int y = 0; y < 4; ++y) sg[x][y] = fma(va[x], vb[y], sg[x][y]);
-        }
-        for (int off = 1; off < L; off <<= 1)
-#pragma unroll
-            for (int x = 0; x < 4; ++x)
-#pragma unroll
-                for (int y = 0; y < 4; ++y) sg[x][y] += __shfl_xor(sg[x][y], off);
-        if (blk < nblk) {
-            // lane `part` of the group writes entries part, part + L, .. of 16
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int i = 4 * A + e / 4, j = 4 * B + e % 4;
-                if ((e & (L - 1)) == part && i < n && j < n) {
-                    const double g = ps[i] * ps[j] * sg[e / 4][e % 4];
-                    Gm[i * gp + j] = g;
-                    Gm[j * gp + i] = g;
-                }
-            }
-        }
+    switch (lgL) {
+        case 3: gram_blocks<8>(n, d, pitch, nb, nblk, Vs, ps, mu, Gm, gp); break;
+        case 2: gram_blocks<4>(n, d, pitch, nb, nblk, Vs, ps, mu, Gm, gp); break;
+        case 1: gram_blocks<2>(n, d, pitch, nb, nblk, Vs, ps, mu, Gm, gp); break;
+        default: gram_blocks<1>(n, d, pitch, nb, nblk, Vs, ps, mu, Gm, gp); break;
     }
     __syncthreads();
 }
