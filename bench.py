@@ -455,7 +455,7 @@ def main():
                            "rows_per_s": round(R / (ms / 1e3), 1), "subsets": subsets,
                            "roofline": dict(_roofline("alu", lane_ops / (ms / 1e3) / 1e12,
                                                       round(VALU_LANE_OPS / 1e12, 2), "TOP/s"),
-                                            kernel="pool_row_kernel", lane_ops=lane_ops),
+                                            kernel="pool_row_kernel + pool_enum_kernel", lane_ops=lane_ops),
                            "budgets": [list(b) for b in wl.meta["budgets"]],
                            "median_swaps": {str(s_): float(holder["n_swaps"][b].float().median().item())
                                             for b, (s_, _) in enumerate(wl.meta["budgets"])},
@@ -495,7 +495,7 @@ def main():
                            "subsets_per_row": [math.comb(s_ + e_, s_) for s_, e_ in budgets],
                            "roofline": dict(_roofline("alu", lane_ops / (ms / 1e3) / 1e12,
                                                       round(VALU_LANE_OPS / 1e12, 2), "TOP/s"),
-                                            kernel="pool_row_kernel", lane_ops=lane_ops),
+                                            kernel="pool_row_kernel + pool_enum_kernel", lane_ops=lane_ops),
                            "dtype": "f64"})
         del dev, holder
         torch.cuda.empty_cache()

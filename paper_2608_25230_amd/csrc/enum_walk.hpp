@@ -256,14 +256,16 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                 const double nb = thr - base;  // test: e[i] + S_W - beta p(W)^2 <= thr - base
                 uint64_t any = 0;
                 // chunks of four steps: one batch of table reads per chunk
+                // (positions past WMAX are padding steps of the table: skipped)
 #pragma unroll
                 for (int i0 = 0; i0 < WMAX; i0 += 4) {
                     if (i0 < lim) {
                         double c[4];
 #pragma unroll
-                        for (int u = 0; u < 4; ++u) c[u] = stepv(t0 + i0 + u);
+                        for (int u = 0; u < 4; ++u) c[u] = i0 + u < WMAX ? stepv(t0 + i0 + u) : 0.0;
 #pragma unroll
-                        for (int u = 0; u < 4; ++u) any |= __ballot(e[i0 + u] + c[u] <= nb);
+                        for (int u = 0; u < 4; ++u)
+                            if (i0 + u < WMAX) any |= __ballot(e[i0 + u] + c[u] <= nb);
                     }
                 }
                 if (any) {  // rare: the same tests again (steps of the run only), exact scores, new beta
@@ -423,18 +425,6 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
     const uint64_t best = redm[0];
     __syncthreads();
     return best;
-}
-
-// The same walk, inlined or called at the compiler's choice (the candidate-set
-// kernel, whose row phase already holds many registers); the exhaustive
-// kernel calls the body inlined, which keeps it at four waves per SIMD.
-__device__ inline uint64_t enum_best(const EnumPlan &pl, const double *Gm, const double *ps, uint64_t seed_mask,
-                                     const uint2 *__restrict__ g_io, const uint64_t *__restrict__ g_wmk,
-                                     const EnumJob *__restrict__ g_jobs, const uint64_t *__restrict__ g_omk,
-                                     double2 *ent, double *PLt, double *redd, uint64_t *redm, int *ctr,
-                                     bool cpl, double *cv) {
-    return enum_best_body<kMaxWalk>(pl, Gm, ps, seed_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd, redm, ctr,
-                                    cpl, cv);
 }
 
 }  // namespace fw

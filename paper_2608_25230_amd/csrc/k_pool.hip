@@ -13,7 +13,10 @@
 //      u_i = p_i (v_i - mu) over the pool's keys in ascending key order, with
 //      the full row's p and mu (es is the full row's error);
 //   4. ES_pool: every s-subset of the pool by the lockstep revolving-door walk
-//      shared with the exhaustive best subset, seeded by A*_s;
+//      shared with the exhaustive best subset, seeded by A*_s -- in a kernel
+//      of its own (pool_enum_kernel, four workgroups per CU), to which the
+//      row kernel hands each pool's instance through the workspace; pools
+//      that drop at most four keys are enumerated in the row kernel;
 //   5. the balancing selector drawing from the pool: every (kept, dropped)
 //      pair of the pool scored from the Gram each round, ties to the smallest
 //      (out, in) key pair, accepted only on a strict decrease;
@@ -24,7 +27,9 @@
 //      EF; the appendix's penalty estimate), run on the Gram matrix of the
 //      deviations v_i - mu and reported from a d-dimensional sum, with the
 //      geometric set (its support padded with top-mass keys in rank order).
-// A second kernel takes each cell's median dropped mass over its rows.
+// The enumeration kernel also takes the ES_pool set's reported error and the
+// statistics that depend on it.  A last kernel takes each cell's median
+// dropped mass over its rows.
 #include "fw_internal.hpp"
 #include "instance64.hpp"
 #include "enum_walk.hpp"
@@ -42,13 +47,13 @@ constexpr int kMaxBudgets = FW_POOL_MAX_BUDGETS;
 struct PoolLds {
     size_t xq, mu, red, ctr, rank, eord, tmp, plist, pps, sc, seed;  // persistent
     size_t zz, ee, rk;                                   // row phase
-    size_t gm, vs, cv, ent, pl, yd, wf;                  // pool phase (overlays the row phase)
+    size_t gm, vs, cv, yd, wf;                           // pool phase (overlays the row phase)
     size_t total;
 };
 
-// The pool phase is sized for the largest pool (Pmax keys) and the largest
-// walk table (nentmax entries) of the call's budgets.
-__host__ __device__ inline PoolLds pool_lds(int64_t N, int d, int Pmax, int nentmax) {
+// The pool phase is sized for the largest pool (Pmax keys) of the call's
+// budgets (the walks, with their tables, run in the enumeration kernel).
+__host__ __device__ inline PoolLds pool_lds(int64_t N, int d, int Pmax) {
     PoolLds L{};
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t at = o; o = align_up(o + bytes, 16); return at; };
@@ -71,9 +76,7 @@ __host__ __device__ inline PoolLds pool_lds(int64_t N, int d, int Pmax, int nent
     L.gm = base;
     L.vs = align_up(L.gm + (size_t)Pmax * Pmax * 8, 16);
     L.cv = align_up(L.vs + (size_t)Pmax * (d + 1) * 4, 16);
-    L.ent = align_up(L.cv + (size_t)Pmax * 8, 16);
-    L.pl = L.ent + (size_t)nentmax * 16;
-    L.yd = align_up(L.pl + (size_t)nentmax * 8, 16);   // Gram matrix of v_i - mu
+    L.yd = align_up(L.cv + (size_t)Pmax * 8, 16);      // Gram matrix of v_i - mu
     L.wf = align_up(L.yd + (size_t)Pmax * Pmax * 8, 16);  // Frank-Wolfe weights
     const size_t pool_end = L.wf + (size_t)Pmax * 8;
     L.total = align_up(row_end > pool_end ? row_end : pool_end, 16);
@@ -194,18 +197,45 @@ struct PoolBudget {
     int direct;  // through the dropped set (enum_complement), else the walk
     int cpl;     // the walk enumerates the dropped sets (its plan: P keys, P - s of them)
     size_t tab_off;  // the walk tables' offset in the workspace
+    size_t inst_off, inst_stride;  // walked budgets: the rows' instances in the workspace
     EnumPlan pl;
     EnumTables tab;
 };
+
+// A walked budget's row instance, handed from the row kernel to the
+// enumeration kernel: the pool's Gram matrix (P x P, row pitch P, float64),
+// masses (P), the reported errors of A*_s and of the balancing set and EF_FW
+// (float64), the seed mask A*_s and the pool's keys (ascending, int32).
+struct PoolInst {
+    size_t gm, ps, es, seed, keys, bytes;
+};
+__host__ __device__ inline PoolInst pool_inst(int P) {
+    PoolInst I{};
+    size_t o = 0;
+    I.gm = o;
+    o += (size_t)P * P * 8;
+    I.ps = o;
+    o += (size_t)P * 8;
+    I.es = o;
+    o += 3 * 8;
+    I.seed = o;
+    o += 8;
+    I.keys = o;
+    o += (size_t)P * 4;
+    I.bytes = align_up(o, 16);
+    return I;
+}
 
 struct PoolArgs {
     const void *q, *k, *v;
     const float *scale, *bias;
     int64_t H, G, N;
-    int d, nb, max_swaps, fw_iters, Smax, Ptot, Stot, Pmax, nentmax;
+    int d, nb, max_swaps, fw_iters, Smax, Ptot, Stot, Pmax;
     PoolBudget b[kMaxBudgets];
     int32_t *pool_idx, *best_idx, *bal_idx, *geo_idx, *n_swaps;
     float *stats;
+    char *ws;       // the workspace (walked budgets' instances, the rows' mu)
+    size_t mu_off;  // [R][d] float64
 };
 
 }  // namespace
@@ -217,7 +247,7 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
     const int64_t N = a.N;
     const int d = a.d, nb = a.nb;
     const int64_t R = a.H * a.G;
-    const PoolLds L = pool_lds(N, d, a.Pmax, a.nentmax);
+    const PoolLds L = pool_lds(N, d, a.Pmax);
     double *xq = (double *)(smem + L.xq);
     double *mu = (double *)(smem + L.mu);
     double *redd = (double *)(smem + L.red);
@@ -319,6 +349,10 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
         }
     }
 
+    // the row's mu for the enumeration kernel's reported errors
+    if (a.ws)
+        for (int c = tid; c < d; c += NT) ((double *)(a.ws + a.mu_off))[r * d + c] = mu[c];
+
     // deviations: single-key errors, sigma^2 and D
     double s2 = 0.0, dmax = 0.0;
     lane_columns<T>(d, [&](int c, int slot) { xr[slot] = mu[c]; });
@@ -387,8 +421,6 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
     double *Gm = (double *)(smem + L.gm);
     float *Vs = (float *)(smem + L.vs);
     double *cv = (double *)(smem + L.cv);
-    double2 *ent = (double2 *)(smem + L.ent);
-    double *PLt = (double *)(smem + L.pl);
     double *Yd = (double *)(smem + L.yd);
     double *wf = (double *)(smem + L.wf);
     const int pitch = d + 1;
@@ -417,13 +449,21 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
             Yd[i * P + j] = acc;
             Yd[j * P + i] = acc;
         }
-        if (tid == 0) ctr[0] = 0;
         __syncthreads();
 
-        // ES_pool
-        const uint64_t best = B.direct ? enum_complement(Gm, ps, P, P - s, cv, redd, redm)
-                                       : enum_best(B.pl, Gm, ps, seed, B.tab.io, B.tab.wmk, B.tab.jobs, B.tab.omk,
-                                                   ent, PLt, redd, redm, ctr, B.cpl != 0, cv);
+        // ES_pool: pools dropping a few keys here; the walked ones hand their
+        // instance to the enumeration kernel
+        char *inst = B.direct ? nullptr : a.ws + B.inst_off + r * B.inst_stride;
+        const PoolInst I = pool_inst(P);
+        if (inst) {
+            for (int e = tid; e < P * P; e += NT) ((double *)(inst + I.gm))[e] = Gm[e];
+            for (int e = tid; e < P; e += NT) {
+                ((double *)(inst + I.ps))[e] = ps[e];
+                ((int32_t *)(inst + I.keys))[e] = pid[e];
+            }
+            if (tid == 0) *(uint64_t *)(inst + I.seed) = seed;
+        }
+        const uint64_t best = B.direct ? enum_complement(Gm, ps, P, P - s, cv, redd, redm) : 0ull;
 
         // Balancing within the pool on wave 0 alone (P <= 64 keys, one per
         // lane, no workgroup barrier), while waves 1 and 2 take the reported
@@ -501,7 +541,7 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
                 }
             }
             es_bal = wave_es(A);
-        } else if (w <= 2) {
+        } else if (w == 1 || (w == 2 && B.direct)) {
             const double e = wave_es(w == 1 ? seed : best);
             if (lane == 0) redd[w] = e;
         } else if (w == 3) {
@@ -583,7 +623,7 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
         if (tid == 0) {
             int t = 0, u = 0, v = 0;
             for (int i = 0; i < P; ++i) {
-                if (((best >> i) & 1ull) && t < s) a.best_idx[r * a.Stot + B.set_off + t++] = pid[i];
+                if (B.direct && ((best >> i) & 1ull) && t < s) a.best_idx[r * a.Stot + B.set_off + t++] = pid[i];
                 if (a.bal_idx && ((A >> i) & 1ull) && u < s) a.bal_idx[r * a.Stot + B.set_off + u++] = pid[i];
                 if (a.geo_idx && ((geo >> i) & 1ull) && v < s) a.geo_idx[r * a.Stot + B.set_off + v++] = pid[i];
             }
@@ -597,11 +637,19 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
             };
             float *o = a.stats + (b * R + r) * FW_POOL_NSTATS;
             o[0] = (float)es_top;
-            o[1] = (float)es_pool;
             o[2] = (float)es_bal;
-            o[3] = (float)ratio(es_top, es_pool);
-            o[4] = (float)(es_top > 0.0 ? 1.0 - es_pool / es_top : 0.0);
-            o[5] = (float)ratio(es_bal, es_pool);
+            if (B.direct) {
+                o[1] = (float)es_pool;
+                o[3] = (float)ratio(es_top, es_pool);
+                o[4] = (float)(es_top > 0.0 ? 1.0 - es_pool / es_top : 0.0);
+                o[5] = (float)ratio(es_bal, es_pool);
+                o[14] = (float)ratio(es_pool, ef_fw);
+            } else {  // the enumeration kernel forms the ES_pool columns
+                double *ev = (double *)(inst + I.es);
+                ev[0] = es_top;
+                ev[1] = es_bal;
+                ev[2] = ef_fw;
+            }
             o[6] = (float)m;
             o[7] = (float)(es_top * ptop);
             o[8] = (float)D;
@@ -610,10 +658,117 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
             o[11] = (float)(m < 1.0 ? sqrt(m / (1.0 - m)) * sigma : (double)INFINITY);
             o[12] = (float)ef_fw;
             o[13] = (float)es_geo;
-            o[14] = (float)ratio(es_pool, ef_fw);
             o[15] = (float)fw_steps;
         }
         __syncthreads();  // the next budget overwrites the pool arrays
+    }
+}
+
+// ---------------------------------------------------------------------------
+// ES_pool of a walked budget: one workgroup per row takes the row's pool
+// instance from the workspace, runs the walk shared with the exhaustive best
+// subset (seeded by A*_s), and forms the ES_pool set's reported error from
+// d-dimensional sums over the pool's values (the same sums, in the same
+// order, as the row kernel's other reported errors) and the statistics that
+// depend on it.
+namespace {
+struct PoolEnumArgs {
+    const void *v;
+    int64_t G, N, R;
+    int d, P, s, cpl, Stot, set_off, b;
+    EnumPlan pl;
+    EnumTables tab;
+    const char *inst;
+    size_t inst_stride;
+    const double *mu;
+    int32_t *best_idx;
+    float *stats;
+};
+
+struct PoolEnumLds {
+    size_t gm, ps, cv, keys, ent, pl, red, ctr, wt, total;
+};
+// ht: each wave also keeps the walk's step values at its own beta
+__host__ __device__ inline PoolEnumLds pool_enum_lds(int P, int nent, int nt, bool ht) {
+    PoolEnumLds L{};
+    size_t o = 0;
+    auto take = [&](size_t bytes) { size_t at = o; o = align_up(o + bytes, 16); return at; };
+    L.gm = take((size_t)P * P * 8);
+    L.ps = take((size_t)P * 8);
+    L.cv = take((size_t)P * 8);
+    L.keys = take((size_t)P * 4);
+    L.ent = take((size_t)nent * 16);
+    L.pl = take((size_t)nent * 8);
+    L.red = take((size_t)(nt / 64) * 3 * 8);
+    L.ctr = take(16);
+    L.wt = take(ht ? (size_t)(nt / 64) * nent * 8 : 0);
+    L.total = o;
+    return L;
+}
+constexpr size_t kPoolEnumLdsHT = 40 * 1024;  // per-wave step values within four workgroups per CU
+}  // namespace
+
+template <typename T, int WMAX, bool HT>
+__global__ void __launch_bounds__(PT, 4) pool_enum_kernel(PoolEnumArgs e) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int tid = threadIdx.x, NT = blockDim.x, lane = tid & 63;
+    const int P = e.P, d = e.d;
+    const PoolEnumLds L = pool_enum_lds(P, e.pl.nent, NT, HT);
+    double *Gm = (double *)(smem + L.gm);
+    double *ps = (double *)(smem + L.ps);
+    double *cv = (double *)(smem + L.cv);
+    int32_t *pid = (int32_t *)(smem + L.keys);
+    double *redd = (double *)(smem + L.red);
+    uint64_t *redm = (uint64_t *)(redd + 2 * (NT >> 6));
+    const int64_t r = blockIdx.x;
+    const char *rec = e.inst + r * e.inst_stride;
+    const PoolInst I = pool_inst(P);
+    for (int x = tid; x < P * P; x += NT) Gm[x] = ((const double *)(rec + I.gm))[x];
+    for (int x = tid; x < P; x += NT) {
+        ps[x] = ((const double *)(rec + I.ps))[x];
+        pid[x] = ((const int32_t *)(rec + I.keys))[x];
+    }
+    const uint64_t seed = *(const uint64_t *)(rec + I.seed);
+    __syncthreads();
+    const uint64_t best = enum_best_body<WMAX, HT>(e.pl, Gm, ps, seed, e.tab.io, e.tab.wmk, e.tab.jobs, e.tab.omk,
+                                                   (double2 *)(smem + L.ent), (double *)(smem + L.pl), redd, redm,
+                                                   (int *)(smem + L.ctr), e.cpl != 0, cv, (double *)(smem + L.wt));
+    if (tid >= 64) return;
+    // es(best) = ||sum_{i in best} p_i (v_i - mu)|| / p(best), columns across
+    // the lanes of wave 0
+    const T *vh = (const T *)e.v + (r / e.G) * e.N * d;
+    const double *mu = e.mu + r * d;
+    double es_pool = 0.0;
+    if ((int64_t)__popcll(best) != e.N) {
+        double g2 = 0.0;
+        for (int c = lane; c < d; c += 64) {
+            double g = 0.0;
+            for (uint64_t m = best; m; m &= m - 1) {
+                const int i = __ffsll((unsigned long long)m) - 1;
+                g = fma(ps[i], (double)(float)Elem<T>::load(vh, (int64_t)pid[i] * d + c) - mu[c], g);
+            }
+            g2 = fma(g, g, g2);
+        }
+        g2 = wave_sum(g2);
+        double pm = 0.0;
+        for (uint64_t m = best; m; m &= m - 1) pm += ps[__ffsll((unsigned long long)m) - 1];
+        es_pool = sqrt(g2) / pm;
+    }
+    if (lane == 0) {
+        int t = 0;
+        for (int i = 0; i < P; ++i)
+            if (((best >> i) & 1ull) && t < e.s) e.best_idx[r * e.Stot + e.set_off + t++] = pid[i];
+        const double *ev = (const double *)(rec + I.es);
+        const double es_top = ev[0], es_bal = ev[1], ef_fw = ev[2];
+        auto ratio = [](double num, double den) {
+            return den > 0.0 ? num / den : (num == 0.0 ? 1.0 : (double)INFINITY);
+        };
+        float *o = e.stats + (e.b * e.R + r) * FW_POOL_NSTATS;
+        o[1] = (float)es_pool;
+        o[3] = (float)ratio(es_top, es_pool);
+        o[4] = (float)(es_top > 0.0 ? 1.0 - es_pool / es_top : 0.0);
+        o[5] = (float)ratio(es_bal, es_pool);
+        o[14] = (float)ratio(es_pool, ef_fw);
     }
 }
 
@@ -648,12 +803,14 @@ __global__ void __launch_bounds__(256) pool_cell_kernel(const float *stats, int6
 // Host: plans of every budget, launch configuration.
 namespace {
 struct PoolPlan {
-    int nb, Smax, Ptot, Stot, Pmax, nentmax;
+    int nb, Smax, Ptot, Stot, Pmax;
     PoolBudget b[kMaxBudgets];
-    size_t lds, ws;
+    size_t lds, ws, mu_off;
+    bool walked;  // some budget is enumerated by the enumeration kernel
 };
 
-bool make_pool_plan(int64_t N, int d, int nb, const int32_t *s, const int32_t *extra, PoolPlan *out) {
+// R rows: the workspace holds every walked budget's row instances.
+bool make_pool_plan(int64_t N, int d, int nb, const int32_t *s, const int32_t *extra, int64_t R, PoolPlan *out) {
     if (nb < 1 || nb > kMaxBudgets) return false;
     PoolPlan pp{};
     pp.nb = nb;
@@ -683,13 +840,28 @@ bool make_pool_plan(int64_t N, int d, int nb, const int32_t *s, const int32_t *e
             B.pl = B.cpl ? pd : pk;
             B.pl.d = d;
             B.pl.G = 1;
-            pp.nentmax = B.pl.nent > pp.nentmax ? B.pl.nent : pp.nentmax;
             ws = align_up(ws, 256);
             B.tab_off = ws;
             ws += enum_tables(B.pl, nullptr).bytes;
+            if (pool_enum_lds(P, B.pl.nent, PT, false).total > 160 * 1024) return false;
+            pp.walked = true;
         }
     }
-    pp.lds = pool_lds(N, d, pp.Pmax, pp.nentmax).total;
+    if (pp.walked) {
+        ws = align_up(ws, 256);
+        pp.mu_off = ws;
+        ws += (size_t)R * d * 8;
+        for (int b = 0; b < nb; ++b) {
+            PoolBudget &B = pp.b[b];
+            if (B.direct) continue;
+            ws = align_up(ws, 256);
+            B.inst_off = ws;
+            B.inst_stride = pool_inst(B.P).bytes;
+            ws += (size_t)R * B.inst_stride;
+        }
+    }
+    // the row kernel holds no walk tables: the walks run in the enumeration kernel
+    pp.lds = pool_lds(N, d, pp.Pmax).total;
     if (pp.lds > 160 * 1024) return false;
     // 0 is the size query's answer for invalid arguments: a call whose pools
     // are all enumerated directly asks for a token 256 bytes it does not use
@@ -701,12 +873,12 @@ bool make_pool_plan(int64_t N, int d, int nb, const int32_t *s, const int32_t *e
 
 bool pool_plannable(int64_t N, int d, int nb, const int32_t *s, const int32_t *extra) {
     PoolPlan pp;
-    return make_pool_plan(N, d, nb, s, extra, &pp);
+    return make_pool_plan(N, d, nb, s, extra, 1, &pp);
 }
 
 size_t pool_ws_bytes(const fw_rows &rows, int nb, const int32_t *s, const int32_t *extra) {
     PoolPlan pp;
-    if (!make_pool_plan(rows.n, (int)rows.d, nb, s, extra, &pp)) return 0;
+    if (!make_pool_plan(rows.n, (int)rows.d, nb, s, extra, rows.H * rows.G, &pp)) return 0;
     return pp.ws;
 }
 
@@ -715,7 +887,8 @@ hipError_t launch_pool(const fw_rows &rows, int nb, const int32_t *s, const int3
                        int32_t *n_swaps, float *stats,
                        float flat_threshold, float *cell_median, uint8_t *cell_flat, void *ws, hipStream_t st) {
     PoolPlan pp;
-    if (!make_pool_plan(rows.n, (int)rows.d, nb, s, extra, &pp)) return hipErrorInvalidConfiguration;
+    if (!make_pool_plan(rows.n, (int)rows.d, nb, s, extra, rows.H * rows.G, &pp))
+        return hipErrorInvalidConfiguration;
     PoolArgs a{};
     hipError_t e = hipSuccess;
     for (int b = 0; b < nb; ++b) {
@@ -741,19 +914,65 @@ hipError_t launch_pool(const fw_rows &rows, int nb, const int32_t *s, const int3
     a.Ptot = pp.Ptot;
     a.Stot = pp.Stot;
     a.Pmax = pp.Pmax;
-    a.nentmax = pp.nentmax;
     a.pool_idx = pool_idx;
     a.best_idx = best_idx;
     a.bal_idx = bal_idx;
     a.geo_idx = geo_idx;
     a.n_swaps = n_swaps;
     a.stats = stats;
+    a.ws = pp.walked ? (char *)ws : nullptr;
+    a.mu_off = pp.mu_off;
     const unsigned R = (unsigned)(rows.H * rows.G);
     if (rows.dtype == FW_BF16)
         hipLaunchKernelGGL(pool_row_kernel<uint16_t>, dim3(R), dim3(PT), pp.lds, st, a);
     else
         hipLaunchKernelGGL(pool_row_kernel<float>, dim3(R), dim3(PT), pp.lds, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    for (int b = 0; b < nb; ++b) {
+        const PoolBudget &B = a.b[b];
+        if (B.direct) continue;
+        PoolEnumArgs g{};
+        g.v = rows.v;
+        g.G = rows.G;
+        g.N = rows.n;
+        g.R = (int64_t)R;
+        g.d = (int)rows.d;
+        g.P = B.P;
+        g.s = B.s;
+        g.cpl = B.cpl;
+        g.Stot = pp.Stot;
+        g.set_off = B.set_off;
+        g.b = b;
+        g.pl = B.pl;
+        g.tab = B.tab;
+        g.inst = (const char *)ws + B.inst_off;
+        g.inst_stride = B.inst_stride;
+        g.mu = (const double *)((const char *)ws + pp.mu_off);
+        g.best_idx = best_idx;
+        g.stats = stats;
+        int wmax = 0;
+        for (int q = 0; q < B.pl.ncls; ++q) wmax = B.pl.cls[q].wn > wmax ? B.pl.cls[q].wn : wmax;
+        const PoolEnumLds Lh = pool_enum_lds(B.P, B.pl.nent, PT, true);
+        const bool ht = Lh.total <= kPoolEnumLdsHT;
+        const size_t lds = ht ? Lh.total : pool_enum_lds(B.P, B.pl.nent, PT, false).total;
+        auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(R), dim3(PT), lds, st, g); };
+        auto pick = [&](auto tag) {
+            using T = decltype(tag);
+            if (wmax <= 12) {
+                if (ht) go(pool_enum_kernel<T, 12, true>);
+                else go(pool_enum_kernel<T, 12, false>);
+            } else if (wmax <= 14) {
+                if (ht) go(pool_enum_kernel<T, 14, true>);
+                else go(pool_enum_kernel<T, 14, false>);
+            } else {
+                if (ht) go(pool_enum_kernel<T, kMaxWalk, true>);
+                else go(pool_enum_kernel<T, kMaxWalk, false>);
+            }
+        };
+        if (rows.dtype == FW_BF16) pick(uint16_t{});
+        else pick(float{});
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
     if (cell_median || cell_flat)
         hipLaunchKernelGGL(pool_cell_kernel, dim3((unsigned)rows.H, (unsigned)nb), dim3(256), 0, st, stats, rows.H,
                            rows.G, flat_threshold, cell_median, cell_flat);
