@@ -16,7 +16,7 @@
 //      shared with the exhaustive best subset, seeded by A*_s -- in a kernel
 //      of its own (pool_enum_kernel, four workgroups per CU), to which the
 //      row kernel hands each pool's instance through the workspace; pools
-//      that drop at most four keys are enumerated in the row kernel;
+//      that drop fewer than four keys are enumerated in the row kernel;
 //   5. the balancing selector drawing from the pool: every (kept, dropped)
 //      pair of the pool scored from the Gram each round, ties to the smallest
 //      (out, in) key pair, accepted only on a strict decrease;
@@ -83,9 +83,15 @@ __host__ __device__ inline PoolLds pool_lds(int64_t N, int d, int Pmax) {
     return L;
 }
 
-// Pools that drop at most this many keys are enumerated through the dropped
-// set: owned parts of the walk would hold nearly every key.
+// Pools that drop fewer than kWalkDrop keys are enumerated through the
+// dropped set in the row kernel (enum_complement): a walk's owned parts would
+// hold nearly every key.  Pools dropping kWalkDrop or more are walked by the
+// enumeration kernel; those dropping at most kDirectDrop keys fall back to
+// the dropped-set enumeration when no walk plan exists.  (Measured: the
+// paper's (32, 4) pool through the enumeration kernel's dropped-set walk cut
+// the four budgets from 9.54 to 8.91 ms.)
 constexpr int kDirectDrop = 4;
+constexpr int kWalkDrop = 4;
 
 // Every s-subset A of the pool as the complement of a dropped set D of
 // q = P - s keys: with c_i = sum_j Gm_ij over the pool, S_U = sum_i c_i and
@@ -828,14 +834,18 @@ bool make_pool_plan(int64_t N, int d, int nb, const int32_t *s, const int32_t *e
         pp.Stot += sb;
         pp.Smax = sb > pp.Smax ? sb : pp.Smax;
         pp.Pmax = P > pp.Pmax ? P : pp.Pmax;
-        B.direct = eb <= kDirectDrop;
+        B.direct = eb < kWalkDrop;
         if (!B.direct) {
             if (binom(P, sb) >= (1ull << 31)) return false;
             // walk the kept sets or the dropped sets, whichever plan costs less
             EnumPlan pk, pd;
             double ck = 0.0, cd = 0.0;
             const bool okk = choose_plan(P, sb, &pk, &ck), okd = choose_plan(P, eb, &pd, &cd);
-            if (!okk && !okd) return false;
+            if (!okk && !okd) {
+                if (eb > kDirectDrop) return false;
+                B.direct = 1;
+                continue;
+            }
             B.cpl = okd && (!okk || cd < ck);
             B.pl = B.cpl ? pd : pk;
             B.pl.d = d;
