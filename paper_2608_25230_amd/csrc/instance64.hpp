@@ -55,7 +55,7 @@ __device__ __forceinline__ void stage_rows(const T *src, int n, int d, float *ds
 // (constants throughout for d = 128 and L >= 4).
 template <int L>
 __device__ __forceinline__ void gram_blocks(int n, int d, int pitch, int nb, int nblk, const float *Vs,
-                                            const double *ps, const double *mu, double *Gm, int gp) {
+                                            const double *ps, const double *mu, double *Gm, int gp, double *Yd) {
     const int tid = threadIdx.x, NT = blockDim.x;
     constexpr int lgL = L == 8 ? 3 : L == 4 ? 2 : L == 2 ? 1 : 0;
     const int ntask = ((nblk * L + 63) / 64) * 64;
@@ -119,9 +119,32 @@ __device__ __forceinline__ void gram_blocks(int n, int d, int pitch, int nb, int
                     const double g = ps[ii] * ps[jj] * sg[e / 4][e % 4];
                     Gm[ii * gp + jj] = g;
                     Gm[jj * gp + ii] = g;
+                    if (Yd) {
+                        Yd[ii * gp + jj] = sg[e / 4][e % 4];
+                        Yd[jj * gp + ii] = sg[e / 4][e % 4];
+                    }
                 }
             }
         }
+    }
+}
+
+// Whole workgroup: Gm[i][j] = p_i p_j <v_i - mu, v_j - mu> (row pitch gp)
+// for the n rows of Vs (pitch `pitch` floats), and, when Yd is given, the
+// inner products themselves, in 4 x 4 blocks of rows (4A .. 4A + 3) x
+// (4B .. 4B + 3), A <= B, each on L adjacent lanes that split the columns and
+// add their sums by a butterfly; rows past n read row n - 1 and are not
+// written.  Whole waves take part, so every butterfly sees its group.
+__device__ __forceinline__ void gram_matrix(int n, int d, int pitch, const float *Vs, const double *ps,
+                                            const double *mu, double *Gm, int gp, double *Yd) {
+    const int nb = (n + 3) >> 2, nblk = nb * (nb + 1) / 2;
+    int lgL = 3;
+    while (lgL > 0 && (nblk << lgL) > (int)blockDim.x) --lgL;
+    switch (lgL) {
+        case 3: gram_blocks<8>(n, d, pitch, nb, nblk, Vs, ps, mu, Gm, gp, Yd); break;
+        case 2: gram_blocks<4>(n, d, pitch, nb, nblk, Vs, ps, mu, Gm, gp, Yd); break;
+        case 1: gram_blocks<2>(n, d, pitch, nb, nblk, Vs, ps, mu, Gm, gp, Yd); break;
+        default: gram_blocks<1>(n, d, pitch, nb, nblk, Vs, ps, mu, Gm, gp, Yd); break;
     }
 }
 
@@ -190,19 +213,7 @@ __device__ __forceinline__ void instance64(const T *qr, const T *kh, const T *vh
         mu[c] = s;
     }
     __syncthreads();
-    // Gram: 4 x 4 blocks of rows (4A .. 4A + 3) x (4B .. 4B + 3), A <= B, each
-    // on L adjacent lanes that split the columns (c = part mod L) and add
-    // their sums by a butterfly; rows past n read row n - 1 and are not
-    // written.  Whole waves take part, so every butterfly sees its group.
-    const int nb = (n + 3) >> 2, nblk = nb * (nb + 1) / 2;
-    int lgL = 3;
-    while (lgL > 0 && (nblk << lgL) > NT) --lgL;
-    switch (lgL) {
-        case 3: gram_blocks<8>(n, d, pitch, nb, nblk, Vs, ps, mu, Gm, gp); break;
-        case 2: gram_blocks<4>(n, d, pitch, nb, nblk, Vs, ps, mu, Gm, gp); break;
-        case 1: gram_blocks<2>(n, d, pitch, nb, nblk, Vs, ps, mu, Gm, gp); break;
-        default: gram_blocks<1>(n, d, pitch, nb, nblk, Vs, ps, mu, Gm, gp); break;
-    }
+    gram_matrix(n, d, pitch, Vs, ps, mu, Gm, gp, nullptr);
     __syncthreads();
 }
 

@@ -442,19 +442,9 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
             Vs[i * pitch + c] = Elem<T>::load(vh, (int64_t)pid[i] * d + c);
         }
         __syncthreads();
-        for (int e = tid; e < P * (P + 1) / 2; e += NT) {
-            int i = 0, rem = e;
-            while (rem >= P - i) { rem -= P - i; ++i; }
-            const int j = i + rem;
-            double acc = 0.0;
-            for (int c = 0; c < d; ++c)
-                acc = fma((double)Vs[i * pitch + c] - mu[c], (double)Vs[j * pitch + c] - mu[c], acc);
-            const double g = ps[i] * ps[j] * acc;
-            Gm[i * P + j] = g;
-            Gm[j * P + i] = g;
-            Yd[i * P + j] = acc;
-            Yd[j * P + i] = acc;
-        }
+        // the Gram matrices of u_i = p_i (v_i - mu) and of v_i - mu (blocked,
+        // as for the exhaustive search's rows)
+        gram_matrix(P, d, pitch, Vs, ps, mu, Gm, P, Yd);
         __syncthreads();
 
         // ES_pool: pools dropping a few keys here; the walked ones hand their
