@@ -109,6 +109,17 @@ __device__ inline int block_exclusive_scan(int v, int *buf, int *total) {
 
 __host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Workgroups are dealt to the eight XCDs round-robin.  Workgroup b of a grid
+// of nb takes logical index xcd_order(b, nb): the workgroups of one XCD take
+// consecutive logical indices (the tail past a multiple of eight keeps its
+// own), so neighbouring logical indices -- rows of one unit reading the same
+// keys and values -- share that XCD's L2.
+__device__ __forceinline__ int64_t xcd_order(int64_t b, int64_t nb) {
+    const int64_t full = nb & ~(int64_t)7;
+    if (b >= full) return b;
+    return (b & 7) * (full >> 3) + (b >> 3);
+}
+
 // Binomial coefficient C(n, r), n <= 64, saturating at 2^62 (exact below).
 __host__ __device__ inline uint64_t binom(int n, int r) {
     if (r < 0 || r > n) return 0;

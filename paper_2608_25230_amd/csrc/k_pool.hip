@@ -271,7 +271,7 @@ __global__ void __launch_bounds__(PT) pool_row_kernel(PoolArgs a) {
     unsigned char *rk = smem + L.rk;  // rank among the top keys, 255 beyond them
     uint64_t *seeds = (uint64_t *)(smem + L.seed);
 
-    const int64_t r = blockIdx.x;
+    const int64_t r = xcd_order(blockIdx.x, gridDim.x);  // a unit's rows on one XCD
     const int64_t h = r / a.G;
     const T *qr = (const T *)a.q + r * d;
     const T *kh = (const T *)a.k + h * N * d;

@@ -86,7 +86,8 @@ __global__ void __launch_bounds__(VT) vote_group_kernel(VoteArgs a) {
     double *pk = redd + NT;  // the vote keys' masses ([s] <= NT doubles, after the row loop)
 
     const int64_t T_ = a.G / gs;  // positions per unit
-    const int64_t h = blockIdx.x / T_, t = blockIdx.x % T_;
+    const int64_t bl = xcd_order(blockIdx.x, gridDim.x);  // a unit's groups on one XCD
+    const int64_t h = bl / T_, t = bl % T_;
     const T *kh = (const T *)a.k + h * N * d;
     const T *vh = (const T *)a.v + h * N * d;
     const double scale = a.scale ? (double)a.scale[h] : (double)default_scale(d);
