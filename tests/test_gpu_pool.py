@@ -168,6 +168,8 @@ def test_example_2_3_pool_on_gpu(torch_fw):
     (2, 6, 20, 16, 2, 4, 3.0, 0.0),     # dropped set larger than the kept set, still direct
     (1, 3, 4500, 16, 6, 10, 2.0, 4.0),  # over 16 keys per thread: the top-key picks rescan LDS
     (1, 3, 100, 16, 62, 2, 2.0, 0.0),   # a pool of 64 keys: the full mask, one balancing lane per key
+    (2, 3, 200, 16, 4, 24, 2.0, 4.0),   # 28 keys, walks of 14: a walk width not a multiple of four
+    (1, 2, 120, 16, 32, 5, 2.0, 0.0),   # dropped sets of 37 keys over three ranges, walks of up to 15
 ])
 def test_small_rows_fp32_all(torch_fw, cfg):
     torch, fw = torch_fw
