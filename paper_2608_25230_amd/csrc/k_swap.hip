@@ -942,46 +942,60 @@ swap_ub_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, Swa
     for (int t = tid; t < kk; t += NT) s.ord[r * kk + t] = sval[t];
 }
 
-// every (kept i, dropped j) pair of a tile against the lower bound: 256
-// kept keys (one per thread) x JC keys per workgroup.  With Pi = P - p_i the
+// every (kept i, dropped j) pair of a tile against the lower bound: BT KT
+// kept keys (KT per thread) x JC keys per workgroup.  With Pi = P - p_i the
 // test  A_i + B_j - 2 r_i r_j <= UB (Pi + p_j)^2  is, expanded,
 //     (B_j - UB p_j^2) - 2 r_i r_j - 2 UB Pi p_j <= UB Pi^2 - A_i,
 // two fused multiply-adds and a compare per pair; the keys' terms are staged
-// in LDS per tile and read by all threads alike.  Each 16-key slice of a tile
-// is first tested as a whole, with its smallest B_j - UB p_j^2 and largest
-// r_j and p_j (a lower bound for every pair of the slice): a wave whose lanes
-// all fail skips the slice.
-template <int JC, int BT>
+// in LDS per tile and read by all threads alike, each read serving a thread's
+// KT kept keys.  Each 16-key slice of a tile is first tested as a whole, with
+// its smallest B_j - UB p_j^2 and largest r_j and p_j (a lower bound for
+// every pair of the slice): a wave whose kept keys all fail skips the slice.
+// A wave holds 64 KT consecutive kept keys of the bound pass's order (lane l
+// keys l, l + 64, ..), so the few that pass share waves.
+template <int JC, int BT, int KT>
 __global__ void __launch_bounds__(BT)
 swap_bound_kernel(int64_t n, int kk, SwapState s) {
     __shared__ float4 tile[2][BT];
     __shared__ float4 slice[2][BT / kSwapSL];
     const int64_t r = blockIdx.y;
     if (!s.st[r * 2]) return;
-    const int tid = threadIdx.x;
-    const int nic = (kk + BT - 1) / BT, ic = blockIdx.x % nic, jc = blockIdx.x / nic;
+    const int tid = threadIdx.x, lane = tid & 63;
+    constexpr int KB = BT * KT;  // kept keys per workgroup
+    const int nic = (kk + KB - 1) / KB, ic = blockIdx.x % nic, jc = blockIdx.x / nic;
     const double *sc = s.sc + r * 4;
     const double P = sc[0], g2 = sc[1], UB = s.ub[r * 2 + 0];
     // the kept keys most likely to pass (first in the order) fill one wave
     // per workgroup; which wave rotates with the key chunk, so that those
     // waves of the workgroups on a CU sit on different SIMDs
-    const int t = ic * BT + (((tid >> 6) + jc) % (BT / 64)) * 64 + (tid & 63);
-    int64_t i = -1;
-    float ci = -INFINITY, m2r = 0.f, m2u = 0.f;
-    if (t < kk) {
-        i = s.ord ? s.ord[r * kk + t] : s.Sl[r * kk + t];
-        const double bqi = (double)s.bq[r * n + i];
-        const double Ai = g2 + bqi - 2.0 * (double)s.a[r * n + i];
-        const double Pi = P - (double)s.p[r * n + i];
-        // margins cover the float32 rounding of A, B and the test itself
-        ci = (float)(UB * (1.0 + 1e-5) * Pi * Pi - Ai + 1e-4 * g2);
-        m2r = (float)(-2.0 * sqrt(bqi));
-        m2u = (float)(-2.0 * UB * (1.0 + 1e-5) * Pi);
+    const int wv = ((tid >> 6) + jc) % (BT / 64);
+    int64_t i[KT];
+    float ci[KT], m2r[KT], m2u[KT];
+#pragma unroll
+    for (int q = 0; q < KT; ++q) {
+        const int t = ic * KB + wv * 64 * KT + q * 64 + lane;
+        i[q] = -1;
+        ci[q] = -INFINITY;
+        m2r[q] = 0.f;
+        m2u[q] = 0.f;
+        if (t < kk) {
+            i[q] = s.ord ? s.ord[r * kk + t] : s.Sl[r * kk + t];
+            const double bqi = (double)s.bq[r * n + i[q]];
+            const double Ai = g2 + bqi - 2.0 * (double)s.a[r * n + i[q]];
+            const double Pi = P - (double)s.p[r * n + i[q]];
+            // margins cover the float32 rounding of A, B and the test itself
+            ci[q] = (float)(UB * (1.0 + 1e-5) * Pi * Pi - Ai + 1e-4 * g2);
+            m2r[q] = (float)(-2.0 * sqrt(bqi));
+            m2u[q] = (float)(-2.0 * UB * (1.0 + 1e-5) * Pi);
+        }
     }
     const float ubf = (float)(UB * (1.0 + 1e-5));
     const float2 *br = s.br + r * n;
     const float *pr = s.p + r * n;
     const int64_t j0 = (int64_t)jc * JC, j1 = j0 + JC < n ? j0 + JC : n;
+    auto pass = [&](const float4 &b, int q) __attribute__((always_inline)) {
+        return fmaf(m2u[q], b.z, fmaf(m2r[q], b.y, b.x)) <= ci[q];
+    };
     // the next tile's keys are loaded while this one is tested; two LDS
     // buffers, one barrier per tile
     float2 nb = make_float2(INFINITY, 0.f);
@@ -1015,33 +1029,40 @@ swap_bound_kernel(int64_t n, int kk, SwapState s) {
         __syncthreads();
         for (int u0 = 0; u0 < BT; u0 += kSwapSL) {
             const float4 sl = slice[buf][u0 / kSwapSL];
-            if (!__ballot(fmaf(m2u, sl.z, fmaf(m2r, sl.y, sl.x)) <= ci)) continue;
+            bool hs = false;
+#pragma unroll
+            for (int q = 0; q < KT; ++q) hs |= pass(sl, q);
+            if (!__ballot(hs)) continue;
             uint64_t any = 0;
 #pragma unroll
             for (int u = 0; u < kSwapSL; ++u) {
                 const float4 b = tile_b[u0 + u];
-                any |= __ballot(fmaf(m2u, b.z, fmaf(m2r, b.y, b.x)) <= ci);
+                bool h = false;
+#pragma unroll
+                for (int q = 0; q < KT; ++q) h |= pass(b, q);
+                any |= __ballot(h);
             }
-            if (any) {  // rare: this lane's survivors of the slice, one list slot range per wave
-                uint32_t m = 0;
+            if (any) {  // rare: each kept key's survivors of the slice, one list slot range per wave
 #pragma unroll
-                for (int u = 0; u < kSwapSL; ++u) {
-                    const float4 b = tile_b[u0 + u];
-                    m |= (fmaf(m2u, b.z, fmaf(m2r, b.y, b.x)) <= ci ? 1u : 0u) << u;
-                }
-                const int lane = tid & 63, c = __popc(m);
-                int incl = c;
+                for (int q = 0; q < KT; ++q) {
+                    uint32_t m = 0;
 #pragma unroll
-                for (int off = 1; off < 64; off <<= 1) {
-                    const int y = __shfl_up(incl, off);
-                    if (lane >= off) incl += y;
+                    for (int u = 0; u < kSwapSL; ++u) m |= (pass(tile_b[u0 + u], q) ? 1u : 0u) << u;
+                    const int c = __popc(m);
+                    if (!__ballot(c > 0)) continue;
+                    int incl = c;
+#pragma unroll
+                    for (int off = 1; off < 64; off <<= 1) {
+                        const int y = __shfl_up(incl, off);
+                        if (lane >= off) incl += y;
+                    }
+                    int base = 0;
+                    if (lane == 63) base = atomicAdd(&s.cnt[r], incl);
+                    base = __shfl(base, 63);
+                    int pos = base + incl - c;
+                    for (; m; m &= m - 1, ++pos)
+                        if (pos < kSwapCand) s.cand[r * kSwapCand + pos] = i[q] * n + (jt + u0 + __ffs(m) - 1);
                 }
-                int base = 0;
-                if (lane == 63) base = atomicAdd(&s.cnt[r], incl);
-                base = __shfl(base, 63);
-                int pos = base + incl - c;
-                for (; m; m &= m - 1, ++pos)
-                    if (pos < kSwapCand) s.cand[r * kSwapCand + pos] = i * n + (jt + u0 + __ffs(m) - 1);
             }
         }
     }
@@ -1206,7 +1227,8 @@ swap_final_kernel(int64_t n, int kk, SwapState s, int32_t *s_idx, float *gap_tra
 namespace {
 
 constexpr int kSwapJC = 4096;  // keys per workgroup of the bound pass
-constexpr int kSwapBT = 256;   // kept keys (threads) per workgroup of the bound pass
+constexpr int kSwapBT = 256;   // threads per workgroup of the bound pass
+constexpr int kSwapKT = 4;     // kept keys per thread of the bound pass
 constexpr int kSwapRB = 32;    // rows of one unit per workgroup of the dots pass
 
 // the MFMA pair sweep: bf16, d = 128, whole 16-key tiles
@@ -1321,8 +1343,9 @@ static hipError_t swap_large(const fw_rows &rows, int k, int max_iters, int32_t 
                                n, d, L.s);
         if (L.s.br) {  // pruned search; the sweep below then runs only for overflowing rows
             hipLaunchKernelGGL(swap_ub_kernel<T>, dim3((unsigned)R), dim3(256), 0, st, v, G, n, d, k, L.s);
-            hipLaunchKernelGGL((swap_bound_kernel<kSwapJC, kSwapBT>),
-                               dim3((unsigned)(((k + kSwapBT - 1) / kSwapBT) * ((n + kSwapJC - 1) / kSwapJC)),
+            hipLaunchKernelGGL((swap_bound_kernel<kSwapJC, kSwapBT, kSwapKT>),
+                               dim3((unsigned)(((k + kSwapBT * kSwapKT - 1) / (kSwapBT * kSwapKT)) *
+                                               ((n + kSwapJC - 1) / kSwapJC)),
                                     (unsigned)R),
                                dim3(kSwapBT), 0, st, n, k, L.s);
             hipLaunchKernelGGL(swap_cand_kernel<T>, dim3((unsigned)R), dim3(256), 0, st, v, G, n, d, L.s);
