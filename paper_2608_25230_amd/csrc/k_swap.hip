@@ -151,6 +151,7 @@ struct SwapState {
     int32_t *fbn;    // [1]      their count (cleared by the init and apply passes)
     int64_t *cand;   // [R][kSwapCand] surviving pairs i n + j
     int32_t *ord;    // [R][k]    kept keys in the bound pass's order (k <= kSwapSort)
+    float4 *kd;      // [R][k]    per kept key in that order: its bound-test terms and index
     int nblk;
 };
 
@@ -939,7 +940,19 @@ swap_ub_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, Swa
             __syncthreads();
         }
     }
-    for (int t = tid; t < kk; t += NT) s.ord[r * kk + t] = sval[t];
+    // each kept key's terms of the bound test, in the order, so that every
+    // workgroup of the bound pass reads them contiguously instead of
+    // gathering them per key (see swap_bound_kernel for the test)
+    for (int t = tid; t < kk; t += NT) {
+        const int32_t i = sval[t];
+        s.ord[r * kk + t] = i;
+        const double bqi = (double)bq[i];
+        const double Ai = g2 + bqi - 2.0 * (double)a[i];
+        const double Pi = P - (double)p[i];
+        s.kd[r * kk + t] = make_float4((float)(val * (1.0 + 1e-5) * Pi * Pi - Ai + 1e-4 * g2),
+                                       (float)(-2.0 * sqrt(bqi)), (float)(-2.0 * val * (1.0 + 1e-5) * Pi),
+                                       __int_as_float(i));
+    }
 }
 
 // every (kept i, dropped j) pair of a tile against the lower bound: BT KT
@@ -978,8 +991,14 @@ swap_bound_kernel(int64_t n, int kk, SwapState s) {
         ci[q] = -INFINITY;
         m2r[q] = 0.f;
         m2u[q] = 0.f;
-        if (t < kk) {
-            i[q] = s.ord ? s.ord[r * kk + t] : s.Sl[r * kk + t];
+        if (t < kk && s.kd) {  // formed by the upper-bound pass, in this order
+            const float4 e = s.kd[r * kk + t];
+            ci[q] = e.x;
+            m2r[q] = e.y;
+            m2u[q] = e.z;
+            i[q] = __float_as_int(e.w);
+        } else if (t < kk) {
+            i[q] = s.Sl[r * kk + t];
             const double bqi = (double)s.bq[r * n + i[q]];
             const double Ai = g2 + bqi - 2.0 * (double)s.a[r * n + i[q]];
             const double Pi = P - (double)s.p[r * n + i[q]];
@@ -1295,7 +1314,10 @@ SwapLayout swap_layout(const fw_rows &rows, int k, void *ws) {
         L.s.fbl = (int32_t *)take(R * 4);
         L.s.fbn = (int32_t *)take(16);
         L.s.cand = (int64_t *)take(R * (size_t)kSwapCand * 8);
-        if (k <= kSwapSort) L.s.ord = (int32_t *)take(R * (size_t)k * 4);
+        if (k <= kSwapSort) {
+            L.s.ord = (int32_t *)take(R * (size_t)k * 4);
+            L.s.kd = (float4 *)take(R * (size_t)k * 16);
+        }
     }
     L.s.z = L.z;
     L.s.row_m = L.row_m;
