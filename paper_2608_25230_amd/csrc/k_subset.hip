@@ -46,7 +46,7 @@ constexpr int kSubsetThreads = 256;
 // fall on different LDS banks.
 __host__ __device__ inline int gram_pitch(int n) { return n | 1; }
 
-constexpr size_t kSubsetLdsKeep = 40 * 1024;  // four workgroups per CU
+constexpr size_t kSubsetLdsKeep = 32 * 1024;  // five workgroups per CU
 
 struct SubsetLds {
     size_t gm, pz, mu, ent, pl, vs, red, ctr, wt, total;
@@ -67,7 +67,7 @@ __host__ __device__ inline SubsetLds subset_lds(int n, int d, int k, int nent, i
     L.red = take((size_t)(nt / 64) * 3 * 8);   // two doubles and one mask per wave
     L.ctr = take(16);
     L.wt = take(ht ? (size_t)(nt / 64) * nent * 8 : 0);
-    // the values stay staged through the walk when that keeps four
+    // the values stay staged through the walk when that keeps five
     // workgroups per CU; otherwise the walk tables overlay them and they
     // are staged again for the reported errors
     L.keep_vs = o + tab + vsb + 32 <= kSubsetLdsKeep;
@@ -190,7 +190,7 @@ __global__ void __launch_bounds__(256) enum_tables_kernel(EnumPlan p, uint2 *io,
 }
 
 template <typename T, int WMAX, bool HT>
-__global__ void __launch_bounds__(kSubsetThreads, 4)
+__global__ void __launch_bounds__(kSubsetThreads, 5)
 best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
                    const float *__restrict__ scale, const float *__restrict__ bias, EnumPlan pl,
                    const uint2 *__restrict__ g_io, const uint64_t *__restrict__ g_wmk,
@@ -286,8 +286,9 @@ hipError_t launch_best_subset(const fw_rows &rows, int k, int32_t *best_idx, flo
     // a narrower walk register file when every walked range allows it
     int wmax = 0;
     for (int q = 0; q < p.ncls; ++q) wmax = p.cls[q].wn > wmax ? p.cls[q].wn : wmax;
-    // per-wave step values when they fit beside the staged values within four
-    // workgroups per CU
+    // per-wave step values when they fit beside the staged values within five
+    // workgroups per CU (at n = 24, k = 6 neither does: five workgroups per CU
+    // without them ran 7 % faster than four with both)
     const SubsetLds Lh = subset_lds(p.n, p.d, k, p.nent, nt, true);
     const bool ht = Lh.keep_vs && Lh.total <= kSubsetLdsKeep;
     const SubsetLds L = ht ? Lh : subset_lds(p.n, p.d, k, p.nent, nt, false);
