@@ -47,7 +47,9 @@ namespace fw {
 // redd [NT] (double), redm [NT] (uint64) and ctr[1] are LDS scratch.
 // Returns the best mask, block-uniform.
 // wtab (HT): nent doubles per wave of the workgroup (LDS).
-template <int WMAX, bool HT = false>
+// RD = false: the plan walks no part of more than kColexMax keys (no
+// revolving-door walk is compiled).
+template <int WMAX, bool HT = false, bool RD = true>
 __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const double *Gm, const double *ps, uint64_t seed_mask,
                                      const uint2 *__restrict__ g_io, const uint64_t *__restrict__ g_wmk,
                                      const EnumJob *__restrict__ g_jobs, const uint64_t *__restrict__ g_omk,
@@ -246,7 +248,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
             return dB;
         };
 
-        if (kColexMax >= 0 && ws <= kColexMax) {
+        if (!RD || (kColexMax >= 0 && ws <= kColexMax)) {
             // Colex walk of the walked part W = {i < j < l}: the outer keys'
             // terms are summed once per run of the innermost key, and the
             // innermost key indexes e at a compile-time position, so a step is
@@ -342,7 +344,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
             }
             continue;
         }
-
+        if constexpr (RD) {
         // Revolving-door walk (walked parts of more than kColexMax keys): one
         // key leaves and one enters per step, both wave-uniform, so e is read
         // at uniform register positions (its own copy: only indexed here).
@@ -396,6 +398,7 @@ __device__ __forceinline__ uint64_t enum_best_body(const EnumPlan &pl, const dou
                 }
             }
         }
+        }  // RD
     }
     // workgroup argmin with the lexicographic tie rule: within each wave by
     // shuffles, then over the waves

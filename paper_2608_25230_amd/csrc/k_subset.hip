@@ -189,7 +189,7 @@ __global__ void __launch_bounds__(256) enum_tables_kernel(EnumPlan p, uint2 *io,
     omk[(size_t)(p.njobs + j) * 64 + lane] = keys;
 }
 
-template <typename T, int WMAX, bool HT>
+template <typename T, int WMAX, bool HT, bool RD>
 __global__ void __launch_bounds__(kSubsetThreads, 5)
 best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
                    const float *__restrict__ scale, const float *__restrict__ bias, EnumPlan pl,
@@ -224,7 +224,7 @@ best_subset_kernel(const T *__restrict__ q, const T *__restrict__ k, const T *__
     // top-k set: rank by (z desc, index asc)
     const uint64_t top_mask = topk_mask64(zs, n, kk, topk_idx ? topk_idx + r * kk : nullptr);
     // (instance64 ends with a barrier: the walk tables may overlay Vs)
-    const uint64_t best = enum_best_body<WMAX, HT>(pl, Gm, ps, top_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd,
+    const uint64_t best = enum_best_body<WMAX, HT, RD>(pl, Gm, ps, top_mask, g_io, g_wmk, g_jobs, g_omk, ent, PLt, redd,
                                                    redm, ctr, false, nullptr, wtab);
     if (tid == 0) {
         int i = 0;
@@ -285,7 +285,11 @@ hipError_t launch_best_subset(const fw_rows &rows, int k, int32_t *best_idx, flo
     const int nt = kSubsetThreads;
     // a narrower walk register file when every walked range allows it
     int wmax = 0;
-    for (int q = 0; q < p.ncls; ++q) wmax = p.cls[q].wn > wmax ? p.cls[q].wn : wmax;
+    bool rd = false;  // some walked part takes the revolving-door order
+    for (int q = 0; q < p.ncls; ++q) {
+        wmax = p.cls[q].wn > wmax ? p.cls[q].wn : wmax;
+        rd = rd || p.cls[q].ws > kColexMax;
+    }
     // per-wave step values when they fit beside the staged values within five
     // workgroups per CU (at n = 24, k = 6 neither does: five workgroups per CU
     // without them ran 7 % faster than four with both)
@@ -301,11 +305,12 @@ hipError_t launch_best_subset(const fw_rows &rows, int k, int32_t *best_idx, flo
     auto pick = [&](const auto *q, const auto *k, const auto *v) {
         using T = std::remove_cv_t<std::remove_pointer_t<decltype(q)>>;
         if (wmax <= 12) {
-            if (ht) go(best_subset_kernel<T, 12, true>, q, k, v);
-            else go(best_subset_kernel<T, 12, false>, q, k, v);
+            if (ht) go(best_subset_kernel<T, 12, true, true>, q, k, v);
+            else if (rd) go(best_subset_kernel<T, 12, false, true>, q, k, v);
+            else go(best_subset_kernel<T, 12, false, false>, q, k, v);  // colex walks only
         } else {
-            if (ht) go(best_subset_kernel<T, kMaxWalk, true>, q, k, v);
-            else go(best_subset_kernel<T, kMaxWalk, false>, q, k, v);
+            if (ht) go(best_subset_kernel<T, kMaxWalk, true, true>, q, k, v);
+            else go(best_subset_kernel<T, kMaxWalk, false, true>, q, k, v);
         }
     };
     if (rows.dtype == FW_BF16)
