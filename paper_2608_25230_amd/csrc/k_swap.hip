@@ -855,7 +855,18 @@ swap_ub_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, Swa
             pi = bi;
         }
     };
-    top8([&](int64_t j, int64_t &id) { id = j; return (double)br[j].x; }, n, topj);
+    // (the same pass sums the dropped keys' r_j and p_j for the order below)
+    double sr = 0.0, sp = 0.0, nd = 0.0;
+    top8([&](int64_t j, int64_t &id) {
+        id = j;
+        const float2 b = br[j];
+        if (b.x < INFINITY) {
+            sr += (double)b.y;
+            sp += (double)p[j];
+            nd += 1.0;
+        }
+        return (double)b.x;
+    }, n, topj);
     top8([&](int64_t t, int64_t &id) {
         const int64_t i = Sl[t];
         id = i;
@@ -889,15 +900,6 @@ swap_ub_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, int kk, Swa
     // a slice test (largest first), so that the few that do share waves and
     // the other waves skip whole slices: kappa_i = c_i + 2 r_i rt + 2 UB Pi pt
     // with rt, pt four times the mean r_j and p_j of the dropped keys.
-    double sr = 0.0, sp = 0.0, nd = 0.0;
-    for (int64_t j = tid; j < n; j += NT) {
-        const float2 b = br[j];
-        if (b.x < INFINITY) {
-            sr += (double)b.y;
-            sp += (double)p[j];
-            nd += 1.0;
-        }
-    }
     sr = block_reduce(sr, redv, OpSum());
     sp = block_reduce(sp, redv, OpSum());
     nd = block_reduce(nd, redv, OpSum());
