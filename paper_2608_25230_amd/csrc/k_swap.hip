@@ -352,7 +352,7 @@ swap_dots_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, SwapState
         const float aj = pj * (float)((double)acc - mg);
         s.a[r * n + j] = aj;
         const float bj = s.inS[r * n + j] ? INFINITY : s.bq[r * n + j] + 2.f * aj;
-        if (s.jd) s.jd[r * n + j] = make_float4(bj, pj, 2.f * s.w[r * n + j], P + pj);
+        if (s.jd && !s.br) s.jd[r * n + j] = make_float4(bj, pj, 2.f * s.w[r * n + j], P + pj);
         if (s.br) s.br[r * n + j] = make_float2(bj, sqrtf(s.bq[r * n + j]));
     }
 }
@@ -420,7 +420,7 @@ swap_dots_group_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, Swa
             const float aj = pj * (float)((double)acc[rr] - mgs[rr]);
             s.a[r * n + j] = aj;
             const float bj = s.inS[r * n + j] ? INFINITY : s.bq[r * n + j] + 2.f * aj;
-            if (s.jd) s.jd[r * n + j] = make_float4(bj, pj, 2.f * s.w[r * n + j], Ps[rr] + pj);
+            if (s.jd && !s.br) s.jd[r * n + j] = make_float4(bj, pj, 2.f * s.w[r * n + j], Ps[rr] + pj);
             if (s.br) s.br[r * n + j] = make_float2(bj, sqrtf(s.bq[r * n + j]));
         }
     }
@@ -443,6 +443,21 @@ __device__ __forceinline__ void sweep_rows(const SwapState &s, F &&body) {
         if (s.st[r * 2]) body(r);
         __syncthreads();  // LDS is reused by the next row
     }
+}
+
+// The per-key records of the full sweep, (B_j or +inf if kept, p_j, 2 w_j,
+// P + p_j), for the rows the fallback sweep takes: under the pruned search
+// the dots pass does not write them for every row (they are the same values
+// it would have written).
+__global__ void __launch_bounds__(256) swap_jd_kernel(int64_t n, SwapState s) {
+    sweep_rows(s, [&](int64_t r) {
+        const float P = (float)s.sc[r * 4 + 0];
+        for (int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x; j < n; j += (int64_t)gridDim.x * 256) {
+            const float pj = s.p[r * n + j];
+            const float bj = s.inS[r * n + j] ? INFINITY : s.bq[r * n + j] + 2.f * s.a[r * n + j];
+            s.jd[r * n + j] = make_float4(bj, pj, 2.f * s.w[r * n + j], P + pj);
+        }
+    });
 }
 
 // every (kept i, dropped j) pair of a tile: 32 kept x 128 keys per workgroup
@@ -1376,6 +1391,9 @@ static hipError_t swap_large(const fw_rows &rows, int k, int max_iters, int32_t 
         }
         // under the pruned search the sweep takes only the listed rows
         const unsigned sweep_y = L.s.fbl ? (unsigned)(R < kSwapSweepRows ? R : kSwapSweepRows) : (unsigned)R;
+        if (swap_mfma_ok(rows) && L.s.br)  // the listed rows' sweep records
+            hipLaunchKernelGGL(swap_jd_kernel, dim3((unsigned)((n + 1023) / 1024), sweep_y), dim3(256), 0, st,
+                               n, L.s);
         if (swap_mfma_ok(rows))
             hipLaunchKernelGGL(swap_pairs_mfma_kernel, dim3((unsigned)L.s.nblk, sweep_y), dim3(512),
                                (size_t)(2 * SP_STAGE + 2 * SPT * 16 * 16 + 8 * 4 + 8 * 8), st,
