@@ -152,6 +152,8 @@ struct SwapState {
     int64_t *cand;   // [R][kSwapCand] surviving pairs i n + j
     int32_t *ord;    // [R][k]    kept keys in the bound pass's order (k <= kSwapSort)
     float4 *kd;      // [R][k]    per kept key in that order: its bound-test terms and index
+    int a_all;       // a is written for every key (else for the kept keys only: the
+                     // MFMA sweep of the pruned search reads B_j from br instead)
     int nblk;
 };
 
@@ -350,8 +352,9 @@ swap_dots_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, SwapState
         for (int c = 0; c < d; ++c) acc = fmaf(Elem<T>::load(vh, j * d + c), gs[c], acc);
         const float pj = s.p[r * n + j];
         const float aj = pj * (float)((double)acc - mg);
-        s.a[r * n + j] = aj;
-        const float bj = s.inS[r * n + j] ? INFINITY : s.bq[r * n + j] + 2.f * aj;
+        const bool kept = s.inS[r * n + j];
+        if (kept || s.a_all) s.a[r * n + j] = aj;
+        const float bj = kept ? INFINITY : s.bq[r * n + j] + 2.f * aj;
         if (s.jd && !s.br) s.jd[r * n + j] = make_float4(bj, pj, 2.f * s.w[r * n + j], P + pj);
         if (s.br) s.br[r * n + j] = make_float2(bj, sqrtf(s.bq[r * n + j]));
     }
@@ -418,8 +421,9 @@ swap_dots_group_kernel(const T *__restrict__ v, int64_t G, int64_t n, int d, Swa
             if (!s.st[r * 2]) continue;
             const float pj = s.p[r * n + j];
             const float aj = pj * (float)((double)acc[rr] - mgs[rr]);
-            s.a[r * n + j] = aj;
-            const float bj = s.inS[r * n + j] ? INFINITY : s.bq[r * n + j] + 2.f * aj;
+            const bool kept = s.inS[r * n + j];
+            if (kept || s.a_all) s.a[r * n + j] = aj;
+            const float bj = kept ? INFINITY : s.bq[r * n + j] + 2.f * aj;
             if (s.jd && !s.br) s.jd[r * n + j] = make_float4(bj, pj, 2.f * s.w[r * n + j], Ps[rr] + pj);
             if (s.br) s.br[r * n + j] = make_float2(bj, sqrtf(s.bq[r * n + j]));
         }
@@ -454,8 +458,7 @@ __global__ void __launch_bounds__(256) swap_jd_kernel(int64_t n, SwapState s) {
         const float P = (float)s.sc[r * 4 + 0];
         for (int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x; j < n; j += (int64_t)gridDim.x * 256) {
             const float pj = s.p[r * n + j];
-            const float bj = s.inS[r * n + j] ? INFINITY : s.bq[r * n + j] + 2.f * s.a[r * n + j];
-            s.jd[r * n + j] = make_float4(bj, pj, 2.f * s.w[r * n + j], P + pj);
+            s.jd[r * n + j] = make_float4(s.br[r * n + j].x, pj, 2.f * s.w[r * n + j], P + pj);
         }
     });
 }
@@ -1336,6 +1339,9 @@ SwapLayout swap_layout(const fw_rows &rows, int k, void *ws) {
             L.s.kd = (float4 *)take(R * (size_t)k * 16);
         }
     }
+    // the dots pass writes a only for the kept keys when the fallback sweep
+    // is the MFMA one (it takes B_j from br); the float sweep reads a[j]
+    L.s.a_all = (L.s.br && swap_mfma_ok(rows)) ? 0 : 1;
     L.s.z = L.z;
     L.s.row_m = L.row_m;
     L.s.row_l = L.row_l;
