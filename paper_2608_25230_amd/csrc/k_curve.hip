@@ -124,24 +124,28 @@ __global__ void window_combine_kernel(int64_t rows, int nchunks, const float *pa
 }
 
 // Pass 4: stable LSD radix sort of one unit's scores, descending (keys are
-// the complement of the order-preserving bits), payload = key index.  One
-// workgroup per unit; four 8-bit passes.  The digit histograms of all four
-// passes come from one read.  Each pass takes tiles of kSortTile keys, 8 per
-// thread in index order (wave, slot, lane): a key's rank among the equal
-// digits of its wave comes from ballots slot by slot with running per-wave
-// counters, the tile is placed digit-ordered in LDS, and then written out as
-// contiguous runs (coalesced) at the digit's running global offset.
+// the complement of the order-preserving bits), payload = key index (only
+// when the order is asked for: a separate instance, whose payload registers
+// and LDS traffic are gone).  One workgroup per unit; four 8-bit passes.
+// The digit histograms of all four passes come from one read.  Each pass
+// takes tiles of kSortTile keys, 8 per thread in index order (wave, slot,
+// lane): a key's rank among the equal digits of its wave comes from ballots
+// slot by slot with running per-wave counters, the tile is placed
+// digit-ordered in LDS, and then written out as contiguous runs (coalesced)
+// at the digit's running global offset.  (Longer tiles, 12 or 16 keys per
+// thread, run out of registers at 16 waves per workgroup.)
 constexpr int kSortWaves = kSortThreads / 64;
 constexpr int kSortE = 8;
 constexpr int kSortTile = kSortThreads * kSortE;
+template <bool with_vals>
 __global__ void __launch_bounds__(kSortThreads)
 unit_sort_kernel(const float *__restrict__ importance, int64_t n, uint32_t *keys_a, uint32_t *keys_b,
-                 int32_t *vals_a, int32_t *vals_b, int with_vals) {
+                 int32_t *vals_a, int32_t *vals_b) {
     __shared__ int gb[4][256];             // per pass: running global offset of each digit
     __shared__ int wc[kSortWaves][256];    // per wave: digit counts, then their cross-wave prefix
     __shared__ int tdp[256], ttot[256];    // tile: digit prefix, digit totals
     __shared__ uint32_t stk[kSortTile];
-    __shared__ int32_t stv[kSortTile];
+    __shared__ int32_t stv[with_vals ? kSortTile : 1];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int64_t h = blockIdx.x;
     const float *imp = importance + h * n;
@@ -212,29 +216,33 @@ unit_sort_kernel(const float *__restrict__ importance, int64_t n, uint32_t *keys
             for (int i = lane; i < 256; i += 64) wc[wv][i] = 0;
             uint32_t key[kSortE];
             int32_t val[kSortE];
-            int dg[kSortE], lr[kSortE];
+            int lr[kSortE];
+            // the slot's digit (256: past the end), recomputed where used
+            const int64_t ebase = t0 + (int64_t)wv * 64 * kSortE + lane;
+            auto digit = [&](int s) -> int {
+                return (ebase + s * 64 < n) ? (int)((key[s] >> shift) & 255u) : 256;
+            };
 #pragma unroll
             for (int s = 0; s < kSortE; ++s) {
-                const int64_t e = t0 + (int64_t)wv * 64 * kSortE + s * 64 + lane;
                 key[s] = nkey[s];
                 val[s] = nval[s];
-                dg[s] = (e < n) ? (int)((key[s] >> shift) & 255u) : 256;
             }
             if (t0 + kSortTile < n) load_tile(t0 + kSortTile);
 #pragma unroll
             for (int s = 0; s < kSortE; ++s) {
                 // lanes of this wave holding the same digit in this slot
-                uint64_t same = __ballot(dg[s] < 256);
+                const int dg = digit(s);
+                uint64_t same = __ballot(dg < 256);
 #pragma unroll
                 for (int b = 0; b < 8; ++b) {
-                    const uint64_t bal = __ballot((dg[s] >> b) & 1);
-                    same &= ((dg[s] >> b) & 1) ? bal : ~bal;
+                    const uint64_t bal = __ballot((dg >> b) & 1);
+                    same &= ((dg >> b) & 1) ? bal : ~bal;
                 }
                 const int below = __popcll(same & below_mask);
                 int pre = 0;
-                if (dg[s] < 256) pre = wc[wv][dg[s]];
+                if (dg < 256) pre = wc[wv][dg];
                 lr[s] = pre + below;
-                if (dg[s] < 256 && below == 0) wc[wv][dg[s]] = pre + __popcll(same);
+                if (dg < 256 && below == 0) wc[wv][dg] = pre + __popcll(same);
             }
             lds_barrier();
             if (tid < 256) {
@@ -264,8 +272,9 @@ unit_sort_kernel(const float *__restrict__ importance, int64_t n, uint32_t *keys
             lds_barrier();
 #pragma unroll
             for (int s = 0; s < kSortE; ++s) {
-                if (dg[s] < 256) {
-                    const int lp = tdp[dg[s]] + wc[wv][dg[s]] + lr[s];
+                const int dg = digit(s);
+                if (dg < 256) {
+                    const int lp = tdp[dg] + wc[wv][dg] + lr[s];
                     stk[lp] = key[s];
                     if (with_vals) stv[lp] = val[s];
                 }
@@ -407,8 +416,12 @@ static hipError_t curve_impl(const fw_rows &rows, float *importance, float *curv
         hipLaunchKernelGGL((window_logits_kernel<T, 1>), grid, dim3(256), 0, st, q, k, rows.scale,
                            rows.bias, G, n, d, nch, nullptr, nullptr, L.row_m, L.row_il, importance);
     }
-    hipLaunchKernelGGL(unit_sort_kernel, dim3((unsigned)H), dim3(kSortThreads), 0, st, importance, n,
-                       L.ka, L.kb, L.va, L.vb, order ? 1 : 0);
+    if (order)
+        hipLaunchKernelGGL((unit_sort_kernel<true>), dim3((unsigned)H), dim3(kSortThreads), 0, st,
+                           importance, n, L.ka, L.kb, L.va, L.vb);
+    else
+        hipLaunchKernelGGL((unit_sort_kernel<false>), dim3((unsigned)H), dim3(kSortThreads), 0, st,
+                           importance, n, L.ka, L.kb, L.va, L.vb);
     hipLaunchKernelGGL(unit_curve_kernel, dim3((unsigned)H), dim3(kSortThreads), 0, st,
                        (const uint32_t *)L.ka, n, (const int32_t *)L.va, curve, order);
     return hipGetLastError();
