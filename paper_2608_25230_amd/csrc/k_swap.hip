@@ -1265,7 +1265,7 @@ swap_final_kernel(int64_t n, int kk, SwapState s, int32_t *s_idx, float *gap_tra
 // ===========================================================================
 namespace {
 
-constexpr int kSwapJC = 4096;  // keys per workgroup of the bound pass
+constexpr int kSwapJC = 1024;  // keys per workgroup of the bound pass
 constexpr int kSwapBT = 256;   // threads per workgroup of the bound pass
 constexpr int kSwapKT = 4;     // kept keys per thread of the bound pass
 constexpr int kSwapRB = 32;    // rows of one unit per workgroup of the dots pass
